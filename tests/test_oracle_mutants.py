@@ -1,0 +1,104 @@
+"""Planted-mistake check of the oracle's pins (CPU only).
+
+Each case copies the oracle's source, plants one plausible slip (transposed operand,
+wrong sign, dropped term, wrong scale, off-by-one mask, wrong tie rule ...), loads the
+copy as a separate module and runs the pins of tests/test_oracle_pins.py against it.
+At least one pin must fail for every slip; the real oracle is never modified.
+"""
+import os
+import sys
+import types
+
+import pytest
+
+import tests.test_oracle_pins as pins
+
+SRC_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "oracle", "momentkv.py")
+with open(SRC_PATH) as _f:
+    SRC = _f.read()
+
+MUTANTS = {
+    "S_transposed": ("return Moments(int(e.size), ke.sum(axis=0), ve.sum(axis=0), ve.T @ ke)",
+                     "return Moments(int(e.size), ke.sum(axis=0), ve.sum(axis=0), ke.T @ ve)"),
+    "centering_outer_transposed": ("S_t = m.S - np.outer(m.s_v, m.s_k) / n",
+                                   "S_t = m.S - np.outer(m.s_k, m.s_v) / n"),
+    "centering_sign": ("S_t = m.S - np.outer(m.s_v, m.s_k) / n",
+                       "S_t = m.S + np.outer(m.s_v, m.s_k) / n"),
+    "clamp_relative": ("S_t = np.where(np.abs(S_t) < tau, 0.0, S_t)",
+                       "S_t = np.where(np.abs(S_t) <= tau, 0.0, S_t)"),
+    "mask_off_by_one": ("visible = np.arange(N)[None, :] <= (N - w + t)[:, None]",
+                        "visible = np.arange(N)[None, :] < (N - w + t)[:, None]"),
+    "no_causal_mask": ("logits = np.where(visible, logits, -np.inf)", "pass"),
+    "mass_not_row_normalised": ("p /= p.sum(axis=1, keepdims=True)", "pass"),
+    "chunk_alignment_shift": ("for c0 in range((n_sink // chunk) * chunk, n_cand_end, chunk):",
+                              "for c0 in range(n_sink, n_cand_end, chunk):"),
+    "ties_keep_higher_index": ("order = np.lexsort((np.arange(s.shape[0]), -s))",
+                               "order = np.lexsort((-np.arange(s.shape[0]), -s))"),
+    "residual_drops_mean": ("return vv - v_bar[None, :] - (scale / F64(m.n_e)) * (kk @ S_t.T)",
+                            "return vv - (scale / F64(m.n_e)) * (kk @ S_t.T)"),
+    "residual_transposed_cov": ("return vv - v_bar[None, :] - (scale / F64(m.n_e)) * (kk @ S_t.T)",
+                                "return vv - v_bar[None, :] - (scale / F64(m.n_e)) * (kk @ S_t)"),
+    "residual_wrong_scale": ("return vv - v_bar[None, :] - (scale / F64(m.n_e)) * (kk @ S_t.T)",
+                             "return vv - v_bar[None, :] - (1.0 / F64(m.n_e)) * (kk @ S_t.T)"),
+    "decode_cov_sign": ("f_E_hat = f_E_hat + (scale / F64(m.n_e)) * (S_t @ q)",
+                        "f_E_hat = f_E_hat - (scale / F64(m.n_e)) * (S_t @ q)"),
+    "decode_cov_transposed": ("f_E_hat = f_E_hat + (scale / F64(m.n_e)) * (S_t @ q)",
+                              "f_E_hat = f_E_hat + (scale / F64(m.n_e)) * (S_t.T @ q)"),
+    "decode_missing_scale": ("f_E_hat = f_E_hat + (scale / F64(m.n_e)) * (S_t @ q)",
+                             "f_E_hat = f_E_hat + (1.0 / F64(m.n_e)) * (S_t @ q)"),
+    "jensen_missing_count": ("log_Z_E = math.log(m.n_e) + s_bar", "log_Z_E = s_bar"),
+    "jensen_unscaled_mean_logit": ("s_bar = float(scale * (q @ k_bar))", "s_bar = float(q @ k_bar)"),
+    "mix_weights_swapped": ("out = w_R * f_R + (1.0 - w_R) * f_E_hat",
+                            "out = (1.0 - w_R) * f_R + w_R * f_E_hat"),
+    "provisional_score_unweighted": ("sigma0 = _f64(abar) * vnorm", "sigma0 = vnorm"),
+    "moment_round_uses_retained": ("evicted = np.setdiff1d(everyone, kept)",
+                                   "evicted = kept"),
+    "moment_round_skipped": ("kept = np.sort(select_top(sigma, k_keep))", "pass"),
+}
+
+PIN_TESTS = [name for name in dir(pins) if name.startswith("test_")]
+
+
+def _load(old, new):
+    assert SRC.count(old) == 1, f"mutation anchor not unique: {old!r}"
+    name = "oracle_mutant"
+    mod = types.ModuleType(name)
+    mod.__file__ = SRC_PATH
+    sys.modules[name] = mod
+    try:
+        exec(compile(SRC.replace(old, new), SRC_PATH, "exec"), mod.__dict__)
+    finally:
+        del sys.modules[name]
+    return mod
+
+
+def _run_pins(monkeypatch):
+    """Run every pin (all parametrisations); return the names that failed."""
+    failed = []
+    for name in PIN_TESTS:
+        fn = getattr(pins, name)
+        marks = getattr(fn, "pytestmark", [])
+        cases = [()]
+        for m in marks:
+            if m.name == "parametrize":
+                cases = list(m.args[1])
+        for case in cases:
+            args = case if isinstance(case, tuple) else (case,)
+            try:
+                fn(*args)
+            except Exception:          # noqa: BLE001 - any failure counts as caught
+                failed.append(name)
+                break
+    return failed
+
+
+def test_real_oracle_passes_all_pins(monkeypatch):
+    assert _run_pins(monkeypatch) == []
+
+
+@pytest.mark.parametrize("mutant", sorted(MUTANTS))
+def test_planted_mistake_is_caught(monkeypatch, mutant):
+    old, new = MUTANTS[mutant]
+    monkeypatch.setattr(pins, "O", _load(old, new))
+    assert _run_pins(monkeypatch), f"no pin caught the planted mistake {mutant}"

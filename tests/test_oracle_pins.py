@@ -1,0 +1,469 @@
+"""Pins of the fp64 oracle against things other than itself (CPU only).
+
+Each test ties one oracle function to a library routine (torch SDPA, numpy cov,
+Python's stable sort), a closed form the paper derives, an invariant, or brute force on
+a tiny input.  They are chosen so that a plausible slip (dropped term, wrong sign or
+index, transposed operand, wrong scale, off-by-one mask) fails at least one of them;
+tests/test_oracle_mutants.py plants such slips and checks that they are caught.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def sdpa(q, K, V, scale, mask=None):
+    """Textbook softmax attention via torch (fp64): q [m,d], K [n,d], V [n,e] -> [m,e]."""
+    qt = torch.from_numpy(np.asarray(q, np.float64))[None, None]
+    Kt = torch.from_numpy(np.asarray(K, np.float64))[None, None]
+    Vt = torch.from_numpy(np.asarray(V, np.float64))[None, None]
+    m = None if mask is None else torch.from_numpy(mask)[None, None]
+    return F.scaled_dot_product_attention(qt, Kt, Vt, attn_mask=m, scale=scale)[0, 0].numpy()
+
+
+def lse(x):
+    return float(torch.logsumexp(torch.from_numpy(np.asarray(x, np.float64)), 0))
+
+
+# ------------------------------------------------------------------------ window mass
+def test_window_mass_equals_sdpa_probabilities():
+    """a_j = mean over window rows of softmax probabilities (Sec. 5.1 protocol).
+
+    SDPA with one-hot values returns each row's attention weights; the mask is torch's
+    bottom-right causal band (row t of the window sits at position N-w+t)."""
+    rng = np.random.default_rng(1)
+    G, w, d, N = 3, 5, 8, 37
+    q = rng.normal(size=(G, w, d)) * 1.5
+    K = rng.normal(size=(N, d))
+    scale = 1 / math.sqrt(d)
+    band = torch.ones(w, N, dtype=torch.bool).tril(diagonal=N - w).numpy()
+    mask = np.tile(band, (G, 1))
+    P = sdpa(q.reshape(G * w, d), K, np.eye(N), scale, mask)
+    expect = P[:, : N - w].mean(axis=0)
+    got = O.window_attention_mass(q, K, scale)
+    np.testing.assert_allclose(got, expect, rtol=1e-12, atol=1e-15)
+    # every row is a distribution over its visible keys
+    np.testing.assert_allclose(P.sum(axis=1), 1.0, rtol=1e-12)
+
+
+def test_window_mass_bruteforce_loops():
+    rng = np.random.default_rng(2)
+    G, w, d, N = 2, 3, 4, 11
+    q = rng.normal(size=(G, w, d))
+    K = rng.normal(size=(N, d))
+    scale = 0.37
+    acc = [0.0] * (N - w)
+    for g in range(G):
+        for t in range(w):
+            vis = N - w + t
+            logit = [scale * sum(q[g, t, i] * K[j, i] for i in range(d)) for j in range(vis + 1)]
+            z = sum(math.exp(x) for x in logit)
+            for j in range(N - w):
+                acc[j] += math.exp(logit[j]) / z / (G * w)
+    np.testing.assert_allclose(O.window_attention_mass(q, K, scale), acc, rtol=1e-12)
+
+
+# ------------------------------------------------------------------------ chunk pooling
+@pytest.mark.parametrize("n_sink,chunk,n", [(1, 4, 23), (1, 4, 24), (0, 4, 9), (2, 3, 17), (1, 1, 10)])
+def test_chunk_pool_invariants(n_sink, chunk, n):
+    rng = np.random.default_rng(3)
+    a = rng.random(n)
+    ab = O.chunk_pool(a, n_sink, chunk)
+    assert ab.shape == (n - n_sink,)
+    pos = np.arange(n_sink, n)
+    cid = pos // chunk
+    for c in np.unique(cid):
+        sel = cid == c
+        assert np.ptp(ab[sel]) == 0.0                              # constant inside a chunk
+        np.testing.assert_allclose(ab[sel].sum(), a[pos[sel]].sum(), rtol=1e-13)  # sum kept
+    # locality: changing one candidate's mass moves only its own chunk
+    a2 = a.copy()
+    j = n - 2
+    a2[j] += 1.0
+    ab2 = O.chunk_pool(a2, n_sink, chunk)
+    changed = np.nonzero(ab2 != ab)[0] + n_sink
+    assert set(changed) == set(pos[cid == j // chunk])
+    if chunk == 1:
+        np.testing.assert_array_equal(ab, a[n_sink:])
+
+
+# ------------------------------------------------------------------------ selection
+def test_select_top_matches_python_stable_sort_with_ties():
+    rng = np.random.default_rng(4)
+    for trial in range(20):
+        n = int(rng.integers(1, 60))
+        s = rng.integers(0, 6, size=n).astype(np.float64) / 4.0   # many exact ties
+        k = int(rng.integers(0, n + 1))
+        expect = sorted(range(n), key=lambda j: (-s[j], j))[:k]
+        assert list(O.select_top(s, k)) == expect
+
+
+# ------------------------------------------------------------------------ moments
+def test_moments_equal_sequential_rank_one_updates():
+    """Batched sums == the per-eviction additive update of Eq. app_update, in a random order."""
+    rng = np.random.default_rng(5)
+    N, d = 40, 6
+    K, V = rng.normal(size=(N, d)), rng.normal(size=(N, d))
+    E = rng.choice(N, size=17, replace=False)
+    n, sk, sv, S = 0, np.zeros(d), np.zeros(d), np.zeros((d, d))
+    for i in rng.permutation(E):
+        n += 1
+        sk = sk + K[i]
+        sv = sv + V[i]
+        for a in range(d):
+            for b in range(d):
+                S[a, b] += V[i, a] * K[i, b]
+    m = O.evicted_moments(K, V, E)
+    assert m.n_e == n
+    np.testing.assert_allclose(m.s_k, sk, rtol=1e-12)
+    np.testing.assert_allclose(m.s_v, sv, rtol=1e-12)
+    np.testing.assert_allclose(m.S, S, rtol=1e-12, atol=1e-13)
+
+
+def test_covariance_identity_against_numpy_cov():
+    """S_tilde = sum_E v_i (k_i - k_bar)^T = n_e * cross-covariance(v, k) (App. A.1)."""
+    rng = np.random.default_rng(6)
+    N, d = 50, 7
+    K = rng.normal(size=(N, d)) + 2.0
+    V = rng.normal(size=(N, d)) - 1.0
+    E = np.arange(3, 41)
+    m = O.evicted_moments(K, V, E)
+    k_bar, v_bar, St = O.centered_moments(m, tau=0.0)
+    C = np.cov(np.vstack([V[E].T, K[E].T]), bias=True)
+    np.testing.assert_allclose(St, len(E) * C[:d, d:], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(k_bar, K[E].mean(axis=0), rtol=1e-13)
+    np.testing.assert_allclose(v_bar, V[E].mean(axis=0), rtol=1e-13)
+
+
+def test_single_evicted_token_closed_form():
+    """n_e = 1: k_bar = k, v_bar = v and S_tilde = 0 exactly."""
+    rng = np.random.default_rng(7)
+    K, V = rng.normal(size=(5, 4)), rng.normal(size=(5, 4))
+    m = O.evicted_moments(K, V, [3])
+    k_bar, v_bar, St = O.centered_moments(m, tau=0.0)
+    np.testing.assert_array_equal(k_bar, K[3])
+    np.testing.assert_array_equal(v_bar, V[3])
+    assert np.abs(St).max() <= 1e-15
+
+
+def test_clamp_zeroes_entries_below_tau():
+    d = 3
+    S = np.array([[5e-7, -2e-6, 0.3], [-9.99e-7, 1e-6, 0.0], [1.0, -1.0, 2e-7]])
+    m = O.Moments(1, np.zeros(d), np.zeros(d), S)   # zero means: S_tilde == S
+    _, _, St = O.centered_moments(m, tau=1e-6)
+    keep = np.abs(S) >= 1e-6
+    np.testing.assert_array_equal(St, np.where(keep, S, 0.0))
+
+
+def test_zero_sum_of_centered_logits():
+    rng = np.random.default_rng(8)
+    K = rng.normal(size=(30, 8)) * 3
+    m = O.evicted_moments(K, K, np.arange(30))
+    k_bar, _, _ = O.centered_moments(m, 0.0)
+    q = rng.normal(size=8)
+    delta = (K - k_bar) @ q / math.sqrt(8)
+    assert abs(delta.sum()) < 1e-11
+
+
+# ------------------------------------------------------------------------ decode
+def _split_case(rng, n=60, d=16, n_ret=20, spread=1.0, q_norm=1.0):
+    K = rng.normal(size=(n, d))
+    V = rng.normal(size=(n, d))
+    R = np.sort(rng.choice(n, size=n_ret, replace=False))
+    E = np.setdiff1d(np.arange(n), R)
+    kc = K[E].mean(axis=0)
+    K[E] = kc + spread * (K[E] - kc)
+    q = rng.normal(size=d) * q_norm
+    return q, K, V, R, E
+
+
+def test_decode_without_eviction_is_softmax_attention():
+    rng = np.random.default_rng(9)
+    d = 16
+    q, K, V = rng.normal(size=d) * 2, rng.normal(size=(33, d)), rng.normal(size=(33, d))
+    r = O.decode_head(q, K, V, O.Moments.zeros(d))
+    np.testing.assert_allclose(r.out, sdpa(q[None], K, V, 1 / math.sqrt(d))[0], rtol=1e-12)
+    assert r.w_R == 1.0
+    np.testing.assert_allclose(r.log_Z_R, lse(K @ q / math.sqrt(d)), rtol=1e-13)
+
+
+def test_decode_zero_key_spread_recovers_full_attention():
+    """All evicted keys equal: delta = 0, f_E_hat = v_bar = f_E and Z_E_hat = Z_E, so the
+    corrected output is exact full attention over R and E (Sec. 4.2, App. B.2)."""
+    rng = np.random.default_rng(10)
+    q, K, V, R, E = _split_case(rng, spread=0.0, q_norm=3.0)
+    m = O.evicted_moments(K, V, E)
+    r = O.decode_head(q, K[R], V[R], m, tau=0.0)
+    full = sdpa(q[None], K, V, 1 / math.sqrt(len(q)))[0]
+    np.testing.assert_allclose(r.out, full, rtol=1e-11, atol=1e-13)
+    s = K @ q / math.sqrt(len(q))
+    w_R = math.exp(lse(s[R]) - lse(s))
+    np.testing.assert_allclose(r.w_R, w_R, rtol=1e-12)
+    np.testing.assert_allclose(r.log_Z_E_hat, lse(s[E]), rtol=1e-12)
+
+
+def test_decode_query_orthogonal_to_key_spread_is_exact():
+    """q orthogonal to every k_i - k_bar: S_tilde != 0 but S_tilde q = 0 and delta = 0, so
+    the output equals full attention; a transposed covariance would not vanish."""
+    rng = np.random.default_rng(11)
+    d, n = 12, 50
+    q = rng.normal(size=d)
+    K = rng.normal(size=(n, d))
+    V = rng.normal(size=(n, d)) + K[:, ::-1]
+    R = np.arange(0, n, 3)
+    E = np.setdiff1d(np.arange(n), R)
+    P = np.eye(d) - np.outer(q, q) / (q @ q)
+    K[E] = K[E] @ P + 0.7 * q                     # spread lies in q's orthogonal complement
+    m = O.evicted_moments(K, V, E)
+    _, _, St = O.centered_moments(m, 0.0)
+    assert np.abs(St).max() > 1.0
+    r = O.decode_head(q, K[R], V[R], m, tau=0.0)
+    np.testing.assert_allclose(r.out, sdpa(q[None], K, V, 1 / math.sqrt(d))[0], rtol=1e-10,
+                               atol=1e-12)
+
+
+def _err_ratios(errs):
+    return [errs[i] / errs[i + 1] for i in range(len(errs) - 1)]
+
+
+def test_decode_first_order_error_is_second_order_in_key_spread():
+    """||f_E - f_E_hat|| = O(eps^2) when the evicted key deviations shrink by eps
+    (App. B.1 Eq. app_error_bound): halving eps divides the error by ~4.  The
+    zeroth-order variant (v_bar only) is only O(eps): ratio ~2."""
+    d = 16
+    errs1, errs0, errs_full = [], [], []
+    eps_list = [0.4, 0.2, 0.1, 0.05, 0.025]
+    for eps in eps_list:
+        rng = np.random.default_rng(12)
+        q, K, V, R, E = _split_case(rng, n=80, d=d, n_ret=10, spread=eps, q_norm=2.0)
+        m = O.evicted_moments(K, V, E)
+        f_E = sdpa(q[None], K[E], V[E], 1 / math.sqrt(d))[0]
+        r1 = O.decode_head(q, K[R], V[R], m, tau=0.0, order=1)
+        r0 = O.decode_head(q, K[R], V[R], m, tau=0.0, order=0)
+        errs1.append(np.linalg.norm(f_E - r1.f_E_hat))
+        errs0.append(np.linalg.norm(f_E - r0.f_E_hat))
+        full = sdpa(q[None], K, V, 1 / math.sqrt(d))[0]
+        errs_full.append(np.linalg.norm(full - r1.out))
+        # explicit bound of Eq. app_error_bound (leading term; sigma small here)
+        k_bar = K[E].mean(axis=0)
+        sig = np.abs((K[E] - k_bar) @ q / math.sqrt(d)).max()
+        vmax = np.linalg.norm(V[E], axis=1).max()
+        bound = sig ** 2 * math.exp(sig) / 2 * (vmax + np.linalg.norm(r1.f_E_hat))
+        assert errs1[-1] <= bound * 1.05
+    for r in _err_ratios(errs1[1:]):
+        assert 3.6 < r < 4.4, errs1
+    for r in _err_ratios(errs_full[1:]):
+        assert 3.6 < r < 4.4, errs_full
+    for r in _err_ratios(errs0[2:]):
+        assert 1.8 < r < 2.2, errs0
+
+
+def test_jensen_lower_bound_and_weight_bias_identity():
+    """Z_E_hat <= Z_E and w_R_hat >= w_R (Eq. jensen); the exact bias identity of
+    Eq. app_weight_bias; Z_E/Z_E_hat -> 1 + Var(delta)/2 (Eq. app_ratio)."""
+    rng = np.random.default_rng(13)
+    for trial in range(10):
+        q, K, V, R, E = _split_case(rng, spread=rng.uniform(0.1, 2.0), q_norm=2.0)
+        d = len(q)
+        m = O.evicted_moments(K, V, E)
+        r = O.decode_head(q, K[R], V[R], m, tau=0.0)
+        s = K @ q / math.sqrt(d)
+        lZ, lZR, lZE = lse(s), lse(s[R]), lse(s[E])
+        assert r.log_Z_E_hat <= lZE + 1e-12
+        w_R = math.exp(lZR - lZ)
+        assert r.w_R >= w_R - 1e-15
+        eps = math.exp(lZE - r.log_Z_E_hat) - 1.0
+        w_E_hat = 1.0 - r.w_R
+        # Eq. app_weight_bias's middle line, simplified: w_R * w_E_hat * eps; the printed
+        # closing form carries 1/(1 + eps w_E_hat), which belongs with w_R_hat in front.
+        np.testing.assert_allclose(r.w_R - w_R, w_R * w_E_hat * eps, rtol=1e-8, atol=1e-15)
+        np.testing.assert_allclose(r.w_R - w_R, r.w_R * w_E_hat * eps / (1 + eps * w_E_hat),
+                                   rtol=1e-8, atol=1e-15)
+    # logit-variance law at small spread
+    q, K, V, R, E = _split_case(np.random.default_rng(14), spread=0.02, q_norm=2.0)
+    d = len(q)
+    m = O.evicted_moments(K, V, E)
+    r = O.decode_head(q, K[R], V[R], m, tau=0.0)
+    s = K @ q / math.sqrt(d)
+    ratio = math.exp(lse(s[E]) - r.log_Z_E_hat)
+    kc = K[E] - K[E].mean(axis=0)
+    var = q @ (kc.T @ kc / len(E)) @ q / d
+    np.testing.assert_allclose(ratio - 1.0, var / 2, rtol=2e-2)
+
+
+def test_exact_decomposition_of_full_attention():
+    rng = np.random.default_rng(15)
+    q, K, V, R, E = _split_case(rng, q_norm=2.0)
+    p = O.attention_parts(q, K, V, R)
+    full = sdpa(q[None], K, V, 1 / math.sqrt(len(q)))[0]
+    np.testing.assert_allclose(p["f"], full, rtol=1e-12)
+    np.testing.assert_allclose(p["w_R"] * p["f_R"] + p["w_E"] * p["f_E"], full, rtol=1e-12)
+    np.testing.assert_allclose(p["f_R"], sdpa(q[None], K[R], V[R], 1 / math.sqrt(len(q)))[0],
+                               rtol=1e-12)
+    np.testing.assert_allclose(np.linalg.norm(full - p["f_R"]), p["w_E"] * p["gamma"] *
+                               np.linalg.norm(full), rtol=1e-10)
+
+
+# ------------------------------------------------------------------------ residual
+def test_residual_is_second_order_close_to_true_evicted_output_at_own_key():
+    """r_j = v_j - f_E_hat(q = k_j): the residual's prediction term is the first-order
+    estimate of the evicted attention output evaluated at token j's own key, so
+    r_j - (v_j - f_E(k_j)) is O(eps^2) in the evicted key spread (Sec. 4.2, App. B.1)."""
+    d = 8
+    errs = []
+    for eps in [0.2, 0.1, 0.05, 0.025]:
+        rng = np.random.default_rng(16)
+        _, K, V, R, E = _split_case(rng, n=70, d=d, n_ret=12, spread=eps)
+        m = O.evicted_moments(K, V, E)
+        r = O.moment_residuals(K[R], V[R], m, 1 / math.sqrt(d), tau=0.0)
+        f_E = sdpa(K[R], K[E], V[E], 1 / math.sqrt(d))
+        errs.append(np.abs(r - (V[R] - f_E)).max())
+    for x in _err_ratios(errs):
+        assert 3.5 < x < 4.5, errs
+
+
+def test_residual_with_empty_summary_is_the_value():
+    rng = np.random.default_rng(17)
+    K, V = rng.normal(size=(9, 4)), rng.normal(size=(9, 4))
+    s, rn = O.residual_scores(K, V, np.full(9, 0.5), np.arange(9), O.Moments.zeros(4), 0.5, 1e-6)
+    np.testing.assert_allclose(rn, np.linalg.norm(V, axis=1), rtol=1e-14)
+    np.testing.assert_allclose(s, 0.5 * rn, rtol=1e-14)
+
+
+# ------------------------------------------------------------------------ compress
+def _tiny_prefill(seed, G=2, w=4, d=8, N=48):
+    rng = np.random.default_rng(seed)
+    K = rng.normal(size=(N, d))
+    V = rng.normal(size=(N, d)) + 0.5 * K
+    q = K[rng.integers(0, N, size=(G, w))] + 0.3 * rng.normal(size=(G, w, d))
+    return q, K, V
+
+
+def test_compress_full_budget_keeps_everything():
+    q, K, V = _tiny_prefill(18)
+    r = O.compress_head(q, K, V, budget=len(K))
+    np.testing.assert_array_equal(r.idx, np.arange(len(K)))
+    assert r.moments.n_e == 0 and not r.moments.S.any()
+
+
+@pytest.mark.parametrize("mi_rounds", [-1, 0, 1, 2])
+def test_compress_structure(mi_rounds):
+    q, K, V = _tiny_prefill(19)
+    N, w, L = len(K), q.shape[1], 20
+    r = O.compress_head(q, K, V, budget=L, mi_rounds=mi_rounds)
+    assert len(r.idx) == L and np.all(np.diff(r.idx) > 0)
+    assert 0 in r.idx and set(range(N - w, N)) <= set(r.idx)
+    cand = set(range(1, N - w))
+    assert set(r.retained) | set(r.evicted) == cand
+    assert not set(r.retained) & set(r.evicted)
+    assert r.moments.n_e == len(cand) - (L - 1 - w)
+    np.testing.assert_array_equal(r.k_out, K[r.idx])
+    np.testing.assert_array_equal(r.v_out, V[r.idx])
+    m = O.evicted_moments(K, V, r.evicted)
+    np.testing.assert_allclose(r.moments.S, m.S, rtol=1e-13)
+
+
+def test_snapkv_mode_is_top_pooled_mass():
+    q, K, V = _tiny_prefill(20)
+    N, w, L = len(K), q.shape[1], 17
+    r = O.compress_head(q, K, V, budget=L, mi_rounds=-1)
+    a = O.window_attention_mass(q, K, 1 / math.sqrt(K.shape[1]))
+    ab = O.chunk_pool(a, 1, 4)
+    cand = list(range(1, N - w))
+    best = sorted(range(len(cand)), key=lambda i: (-ab[i], i))[: L - 1 - w]
+    assert sorted(cand[i] for i in best) == list(r.retained)
+
+
+def test_provisional_round_is_greedy_first_eviction():
+    """With an empty summary Algorithm 1 scores alpha_j ||v_j||; the greedy loop's first
+    eviction is the lowest-scored candidate of the provisional round."""
+    q, K, V = _tiny_prefill(21)
+    N, w = len(K), q.shape[1]
+    r = O.compress_head(q, K, V, budget=12, mi_rounds=0)
+    alpha = np.zeros(N)
+    alpha[1:N - w] = r.abar
+    prot = [0] + list(range(N - w, N))
+    kept, m = O.greedy_evict(alpha, K, V, prot, budget=N - 1)
+    ev = int(np.setdiff1d(np.arange(N), kept)[0])
+    order = sorted(range(len(r.sigma0)), key=lambda i: (r.sigma0[i], i))
+    assert ev == order[0] + 1
+    assert m.n_e == 1
+
+
+def test_moment_round_evicts_tokens_the_summary_already_predicts():
+    """Closed-form case of the moment round (Sec. 4.2): dyadic values make every sum exact.
+
+    Candidates 0-5 share one key and one small value v_A (low mass): round 0 evicts them,
+    so the summary is v_bar = v_A, S_tilde = 0.  Candidates 6-7 ("twins") carry v_A too
+    but high mass, so round 0 keeps them; their residual is then exactly 0, like that of
+    0-5.  Candidates 8-11 have large distinct values.  With k_keep = 6 the moment round
+    keeps 8-11 plus the two lowest-index zero-score tokens (0, 1): the twins go."""
+    d = 4
+    k_A = np.array([1.0, 0.5, -0.25, 2.0])
+    v_A = np.array([0.125, -0.25, 0.0, 0.0625])
+    K = np.zeros((12, d))
+    V = np.zeros((12, d))
+    K[:6], V[:6] = k_A, v_A
+    K[6:8] = np.array([[0.5, 1.0, 1.0, -1.0], [-2.0, 0.25, 0.5, 1.0]])
+    V[6:8] = v_A
+    K[8:] = np.array([[1, 2, 3, 4], [-1, 0, 2, 1], [3, -2, 1, 0], [0, 1, -1, 2]], float)
+    V[8:] = np.array([[4, 0, 1, 2], [0, -4, 2, 1], [2, 2, -4, 0], [-3, 1, 0, 4]], float)
+    abar = np.array([1.0] * 6 + [10.0] * 2 + [1.0] * 4)
+    sel = O.select_candidates(abar, K, V, 6, mi_rounds=1, scale=0.5, tau=1e-6)
+    assert list(sel["rounds"][0]) == [6, 7, 8, 9, 10, 11]
+    np.testing.assert_array_equal(sel["sigma"][:8], 0.0)
+    assert list(sel["rounds"][1]) == [0, 1, 8, 9, 10, 11]
+    np.testing.assert_allclose(sel["sigma"][8:], np.linalg.norm(V[8:] - v_A, axis=1), rtol=1e-15)
+
+
+def test_compress_is_permutation_equivariant_without_chunks():
+    """Window mass, residuals and moments depend on the candidate multiset only: permuting
+    candidate rows (chunk = 1) permutes the selection and leaves the moments unchanged."""
+    q, K, V = _tiny_prefill(22, N=40)
+    N, w = len(K), q.shape[1]
+    rng = np.random.default_rng(23)
+    perm = np.arange(N)
+    perm[1:N - w] = 1 + rng.permutation(N - w - 1)
+    r1 = O.compress_head(q, K, V, budget=14, chunk=1)
+    r2 = O.compress_head(q, K[perm], V[perm], budget=14, chunk=1)
+    assert sorted(perm[r2.retained]) == list(r1.retained)
+    np.testing.assert_allclose(r2.moments.S, r1.moments.S, rtol=1e-12)
+    np.testing.assert_allclose(r2.moments.s_k, r1.moments.s_k, rtol=1e-12)
+
+
+def test_compress_rejects_budget_below_sink_plus_window():
+    q, K, V = _tiny_prefill(24)
+    with pytest.raises(ValueError):
+        O.compress_head(q, K, V, budget=q.shape[1])
+
+
+def test_moment_storage_matches_paper_table():
+    with open(os.path.join(GOLDEN, "storage_table.json")) as f:
+        g = json.load(f)
+    for row in g["rows"]:
+        b = O.moment_storage_bytes(row["layers"], row["kv_heads"], row["head_dim"], 2)
+        assert round(b / 1e6, 1) == row["moment_overhead_MB"]
+    assert 128 * 128 * 2 == g["S_bytes_per_head_d128_16bit"]
+
+
+def test_corrected_output_beats_retained_only_on_average():
+    """Quality check (reported in Sec. 4.2 as the purpose of the correction): over random
+    queries the corrected output is closer to full attention than f_R on average."""
+    rng = np.random.default_rng(25)
+    q, K, V = _tiny_prefill(26, G=2, w=4, d=16, N=200)
+    r = O.compress_head(q, K, V, budget=40)
+    gains = []
+    for _ in range(30):
+        qq = K[rng.integers(0, len(K), 4)].mean(axis=0) + 0.5 * rng.normal(size=16)
+        full = sdpa(qq[None], K, V, 0.25)[0]
+        dec = O.decode_head(qq, r.k_out, r.v_out, r.moments)
+        gains.append(np.linalg.norm(full - dec.f_R) - np.linalg.norm(full - dec.out))
+    assert np.mean(gains) > 0
