@@ -1,0 +1,195 @@
+/*
+ * momentkv.h - C ABI of libmomentkv.so, the MomentKV hot path on MI355X (gfx950).
+ *
+ * MomentKV (arXiv 2606.01563) keeps, per KV head, four running sums over the evicted
+ * tokens E: the count n_e, the key sum s_k, the value sum s_v and the value-key
+ * outer-product sum S = sum_E v_i k_i^T (Sec. 4.1; App. A.1 Eq. app_sufficient).
+ * This library implements the two data-parallel halves of the method:
+ *
+ *   momentkv_compress     one-shot prefill eviction: observation-window scoring
+ *                         (Sec. 5.1 prefill protocol), moment-informed selection of the
+ *                         retained set (Sec. 4.2 Eq. residual; Algorithm 1 Phase 1 in
+ *                         batched form), and the moments of the evicted set.
+ *   momentkv_decode_attn  attention over the retained cache fused with the first-order
+ *                         correction for the evicted tokens (Algorithm 1 Phase 2;
+ *                         Eqs. fhat, jensen, fused; log-domain weight of App. C.2).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are dense, contiguous, row-major, in device memory (HBM) unless stated.
+ *     Parameter structs are host memory.  Shapes use B = batch, Hq = query heads,
+ *     Hkv = KV heads, G = Hq / Hkv (query head hq reads KV head hq / G), d = head dim.
+ *   - K/V/Q tensors and outputs use the element type `dtype` (fp32, or bf16 stored as
+ *     uint16 bit patterns, round-to-nearest-even).  Moments are always fp32 (n_e int32).
+ *   - The caller owns every buffer, including the workspace sized by the matching
+ *     *_workspace_size query.  The library never allocates, frees or synchronises; all
+ *     work is enqueued on `stream` (a hipStream_t; NULL = the default stream) and is
+ *     stream-ordered.  There is no global mutable state: calls on different streams
+ *     with different buffers may run concurrently.
+ *   - Every argument is validated on the host before the first launch.  On any error
+ *     nothing is launched and the status says why.  A launch failure reported by HIP
+ *     returns MKV_ERR_HIP.
+ *   - Results are deterministic: all reductions run in a fixed order (no float
+ *     atomics), so identical inputs give bit-identical outputs.
+ */
+#ifndef MOMENTKV_H
+#define MOMENTKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOMENTKV_ABI_VERSION 1
+
+typedef enum {
+  MKV_OK = 0,
+  MKV_ERR_NULL = 1,        /* a required pointer is NULL                               */
+  MKV_ERR_SHAPE = 2,       /* non-positive size, Hq % Hkv != 0, bad d/window/chunk ... */
+  MKV_ERR_BUDGET = 3,      /* budget < n_sink + window (the protected tokens)          */
+  MKV_ERR_DTYPE = 4,       /* dtype is not MKV_F32 or MKV_BF16                          */
+  MKV_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the size query            */
+  MKV_ERR_CAPACITY = 6,    /* output cache rows too few, or max_len > cap              */
+  MKV_ERR_ALIAS = 7,       /* an output overlaps an input it must not overwrite        */
+  MKV_ERR_HIP = 8,         /* a HIP launch failed                                       */
+  MKV_ERR_UNSUPPORTED = 9  /* valid request outside this build's limits (see below)    */
+} mkv_status;
+
+typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
+
+/* Limits of this build: head_dim in {64, 128}; G = Hq/Hkv <= 16; G * window <= 512. */
+
+/* ------------------------------------------------------------------------------------
+ * Prefill compression (Sec. 5.1 protocol; Sec. 4.2; App. A.1)
+ *
+ * Per (sequence b, KV head h), with N = ctx_len, w = window, n_s = n_sink:
+ *   1. Window scoring.  The G*w window queries of the group attend causally to the
+ *      prefix (row t of the window sits at position N-w+t and sees keys 0..N-w+t);
+ *      a_j is the mean over those rows of the softmax probability on key j, j < N-w.
+ *      Logits are scale * q.k (scale = 1/sqrt(d) when the field is 0).
+ *   2. Candidates are C = [n_s, N-w); the sinks [0, n_s) and the window [N-w, N) are
+ *      always kept.  k_keep = budget - n_s - w candidates survive.
+ *   3. Chunk pooling: abar_j = mean of a over the candidates of j's aligned chunk
+ *      [c*m, c*m+c) of absolute positions (chunk = 1 disables pooling).
+ *   4. Selection (batched Algorithm 1 Phase 1):
+ *        provisional round: score0_j = abar_j * ||v_j|| (the empty summary gives
+ *        r_j = v_j); keep the k_keep best; E0 = the other candidates;
+ *        moment rounds (mi_rounds >= 1): summary = moments of the previous round's
+ *        evicted set, k_bar/v_bar = sums / n, S_tilde = S - s_v s_k^T / n with entries
+ *        |S_tilde_ab| < tau set to 0 (App. C.2), r_j = v_j - v_bar - scale/n *
+ *        S_tilde k_j (Eq. residual), score_j = abar_j * ||r_j||; keep the k_keep best.
+ *        "Best" = larger score; equal scores keep the lower position.
+ *      mi_rounds = -1 keeps the k_keep largest abar (attention only); 0 stops after the
+ *      provisional round.  This build supports mi_rounds in {-1, 0, 1}.
+ *   5. Outputs: the retained positions idx (ascending: sinks, kept candidates, window)
+ *      and their K/V rows copied to k_out/v_out; lens = min(budget, N); the raw sums of
+ *      the final evicted set E (n_e = |E|, s_k, s_v, S = sum_E v_i k_i^T, fp32).
+ *   budget >= N keeps every token: idx = 0..N-1, n_e = 0 and zero moments.
+ * ---------------------------------------------------------------------------------- */
+typedef struct {
+  int32_t batch;        /* B                                                         */
+  int32_t n_q_heads;    /* Hq                                                        */
+  int32_t n_kv_heads;   /* Hkv, divides Hq                                           */
+  int32_t head_dim;     /* d in {64, 128}                                            */
+  int32_t ctx_len;      /* N, prefill length                                         */
+  int32_t budget;       /* L, retained tokens per KV head (sinks and window included) */
+  int32_t window;       /* w, 1 <= w < N                                             */
+  int32_t n_sink;       /* n_s >= 0 attention-sink tokens kept at the start          */
+  int32_t chunk;        /* c >= 1 pooling chunk                                      */
+  int32_t mi_rounds;    /* -1, 0 or 1 (see step 4)                                   */
+  int32_t cap;          /* rows per head of k_out/v_out, >= min(budget, N)           */
+  int32_t dtype;        /* mkv_dtype of q_win, k, v, k_out, v_out                    */
+  float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
+  float tau;            /* covariance clamp threshold (paper: 1e-6); >= 0            */
+} mkv_compress_params;
+
+/* Optional per-candidate diagnostics (any field may be NULL).  n_c = N - w - n_s.
+ * Written only when budget < N (otherwise nothing is scored).                         */
+typedef struct {
+  float* abar;          /* [B, Hkv, n_c] pooled window mass                           */
+  float* score0;        /* [B, Hkv, n_c] provisional score abar * ||v||               */
+  float* score;         /* [B, Hkv, n_c] moment-round score (mi_rounds = 1)           */
+  int32_t* kept0;       /* [B, Hkv, k_keep] provisional kept positions, ascending    */
+} mkv_compress_debug;
+
+/* Bytes of device workspace momentkv_compress needs for these parameters (0 on invalid
+ * parameters).  Pure host computation. */
+size_t momentkv_compress_workspace_size(const mkv_compress_params* p);
+
+/* q_win   [B, Hq, w, d]      window queries (post-RoPE), read only
+ * k, v    [B, Hkv, N, d]     prefill keys (post-RoPE) and values, read only
+ * k_out, v_out [B, Hkv, cap, d]  retained rows written to rows 0..min(L,N)-1; must not
+ *                            overlap k or v (MKV_ERR_ALIAS)
+ * idx_out [B, Hkv, min(L,N)] int32 retained positions, ascending
+ * lens_out [B, Hkv]          int32, set to min(L, N)
+ * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d] fp32, S [B, Hkv, d, d] fp32: outputs,
+ *                            overwritten (zero-initialised summary per generation)
+ * dbg                        NULL or optional diagnostics
+ * workspace                  >= momentkv_compress_workspace_size(p) bytes, 256-aligned */
+mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, const void* k,
+                             const void* v, void* k_out, void* v_out, int32_t* idx_out,
+                             int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, float* S,
+                             const mkv_compress_debug* dbg, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * Corrected decode attention (Algorithm 1 Phase 2; Eqs. fhat, jensen, fused; App. C.2)
+ *
+ * Per (b, query head hq), KV head h = hq / G, one query q:
+ *   0. if k_new/v_new are given, append them at row lens[b,h] of the cache and
+ *      increment lens[b,h] (the new token joins the retained set; the summary is
+ *      unchanged);
+ *   1. f_R, log Z_R = softmax attention of q over rows 0..lens-1 (logits scale * q.k);
+ *   2. if n_e = 0: out = f_R, w_R = 1;
+ *   3. else k_bar = s_k/n_e, v_bar = s_v/n_e, S_tilde = S - s_v s_k^T/n_e clamped at tau,
+ *      log Z_E_hat = log n_e + scale * q.k_bar (Jensen lower bound),
+ *      f_E_hat = v_bar + scale/n_e * S_tilde q (first-order estimate; order 0 drops the
+ *      covariance term), w_R = exp(log Z_R - logsumexp(log Z_R, log Z_E_hat)),
+ *      out = w_R f_R + (1 - w_R) f_E_hat.
+ * ---------------------------------------------------------------------------------- */
+typedef struct {
+  int32_t batch;        /* B (any number of independent caches, e.g. layers x seqs)  */
+  int32_t n_q_heads;    /* Hq                                                        */
+  int32_t n_kv_heads;   /* Hkv                                                       */
+  int32_t head_dim;     /* d in {64, 128}                                            */
+  int32_t cap;          /* rows per head of the cache                                */
+  int32_t max_len;      /* upper bound of lens after the append, 1 <= max_len <= cap */
+  int32_t order;        /* 1 = first order (default), 0 = v_bar only                 */
+  int32_t dtype;        /* mkv_dtype of q, caches, k_new, v_new, out                 */
+  float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
+  float tau;            /* covariance clamp threshold, >= 0                          */
+} mkv_decode_params;
+
+size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
+
+/* q         [B, Hq, d]
+ * k_cache, v_cache [B, Hkv, cap, d]  retained cache; row lens[b,h] is written when
+ *           appending (a head whose lens >= cap skips the append and is flagged)
+ * lens      [B, Hkv] int32 device, 0 <= lens (+1 when appending) <= max_len; updated.
+ *           An empty retained set gives log Z_R = -inf, w_R = 0 and out = f_E_hat
+ *           (out = 0 when n_e = 0 as well).
+ * k_new, v_new [B, Hkv, d] or both NULL
+ * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d], S [B, Hkv, d, d] fp32: the summary, read only
+ * out       [B, Hq, d]
+ * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
+ * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R
+ * workspace >= momentkv_decode_workspace_size(p) bytes.  Its first int32 is a sticky
+ *           overflow flag: set to 1 when an append found a full cache. */
+mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
+                                void* v_cache, int32_t* lens, const void* k_new,
+                                const void* v_new, const int32_t* n_e, const float* s_k,
+                                const float* s_v, const float* S, void* out, float* lse_out,
+                                float* w_r_out, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
+/* Static description of a status code. */
+const char* momentkv_status_string(int32_t status);
+
+/* MOMENTKV_ABI_VERSION of the loaded library. */
+int32_t momentkv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOMENTKV_H */

@@ -1,0 +1,83 @@
+// Host <-> device interface of the MomentKV kernels: argument blocks passed by value to
+// the kernels and the launchers the C ABI layer calls.  Pointers are device pointers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mkv {
+
+struct DecodeArgs {
+  const void* q;            // [B, Hq, D]
+  void* k_cache;            // [B, Hkv, cap, D]
+  void* v_cache;
+  int32_t* lens;            // [B, Hkv]
+  const void* k_new;        // [B, Hkv, D] or null
+  const void* v_new;
+  const int32_t* n_e;       // [B, Hkv]
+  const float* s_k;         // [B, Hkv, D]
+  const float* s_v;
+  const float* S;           // [B, Hkv, D, D]
+  void* out;                // [B, Hq, D]
+  float* lse_out;           // [B, Hq] or null
+  float* w_r_out;           // [B, Hq] or null
+  float* part_o;            // [B*Hkv, nsplit, G, D]
+  float* part_ml;           // [B*Hkv, nsplit, G, 2]  (max in log2 units, sum)
+  float* sq;                // [B*Hkv, G, D]  S_tilde q (unscaled)
+  int32_t* flag;            // sticky append-overflow flag
+  int n_heads;              // B * Hkv
+  int n_pairs;              // B * Hq
+  int Hkv, G, cap, nsplit, split_len, order;
+  float scale, tau;
+};
+
+hipError_t launch_decode(const DecodeArgs& a, bool bf16, int d, hipStream_t st);
+
+struct CompressArgs {
+  const void* q_win;        // [B, Hq, w, D]
+  const void* k;            // [B, Hkv, N, D]
+  const void* v;
+  void* k_out;              // [B, Hkv, cap, D]
+  void* v_out;
+  int32_t* idx_out;         // [B, Hkv, L']
+  int32_t* lens_out;        // [B, Hkv]
+  int32_t* n_e;             // [B, Hkv]
+  float* s_k;               // [B, Hkv, D]
+  float* s_v;
+  float* S;                 // [B, Hkv, D, D]
+  // workspace
+  float* rowpart;           // [H, nsl1, R, 2]   per-slice (max log2, sum) of each window row
+  float* rowstat;           // [H, R, 2]         (max log2, 1/Z)
+  float* vnorm;             // [H, n_c]          ||v_j||
+  float* abar;              // [H, n_c]          pooled window mass
+  float* score0;            // [H, n_c]          provisional score
+  float* score;             // [H, n_c]          moment-round score
+  int32_t* kept0;           // [H, kmax]         provisional kept positions (ascending)
+  int32_t* kept;            // [H, kmax]         final kept positions (ascending)
+  float* spart;             // [H, nslot, D, D]  covariance partials
+  float* svkpart;           // [H, nslot, 2, D]  (s_v, s_k) partials
+  float* stil;              // [H, D, D]         clamped provisional S_tilde (fp32)
+  void* stil_hl;            // [H, 2, D, D]      bf16 hi/lo split of stil (bf16 inputs)
+  float* vbar;              // [H, D]            provisional v_bar
+  void* gath_k;             // [H, kmax, D]      rows of the provisional kept set
+  void* gath_v;
+  int B, Hq, Hkv, G, N, L, w, n_s, chunk, mi_rounds, cap, D;
+  int H;                    // B * Hkv
+  int R;                    // G * w window rows per KV head
+  int n_c;                  // N - w - n_s candidates
+  int k_keep;               // L - n_s - w
+  int kmax;                 // row capacity of kept/gath buffers (>= k_keep, >= 1)
+  int ntile;                // ceil(N / 64)
+  int nsl1, tps1;           // window-row/covariance pass: slices, tiles per slice
+  int nslr, tpsr;           // downdate covariance pass over k_keep rows
+  int nslot;                // nsl1 + nslr
+  int nsl3, tps3;           // residual pass: slices over candidate tiles of 256
+  float scale, tau;
+};
+
+// Full compress pipeline on one stream (see compress.hip for the stage list).
+hipError_t launch_compress(const CompressArgs& a, bool bf16, hipStream_t st,
+                           float* dbg_abar, float* dbg_score0, float* dbg_score,
+                           int32_t* dbg_kept0);
+
+}  // namespace mkv

@@ -1,0 +1,297 @@
+// C ABI of libmomentkv.so: argument validation, workspace layout and launch sequencing.
+// Nothing here allocates, frees or synchronises; every launch goes to the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/momentkv.h"
+#include "mkv_launch.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+inline int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+struct Carver {
+  size_t off = 0;
+  char* base = nullptr;
+  template <class P> P* take(size_t bytes) {
+    P* p = base ? reinterpret_cast<P*>(base + off) : nullptr;
+    off += align_up(bytes);
+    return p;
+  }
+};
+
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+size_t elem_size(int32_t dtype) { return dtype == MKV_BF16 ? 2 : 4; }
+
+// ----------------------------------------------------------------------- compress
+mkv_status check_compress_params(const mkv_compress_params* p) {
+  if (!p) return MKV_ERR_NULL;
+  if (p->dtype != MKV_F32 && p->dtype != MKV_BF16) return MKV_ERR_DTYPE;
+  if (p->batch < 1 || p->n_q_heads < 1 || p->n_kv_heads < 1 || p->head_dim < 1 || p->ctx_len < 2)
+    return MKV_ERR_SHAPE;
+  if (p->n_q_heads % p->n_kv_heads) return MKV_ERR_SHAPE;
+  if (p->window < 1 || p->window >= p->ctx_len) return MKV_ERR_SHAPE;
+  if (p->n_sink < 0 || p->n_sink > p->ctx_len - p->window) return MKV_ERR_SHAPE;
+  if (p->chunk < 1 || p->budget < 1) return MKV_ERR_SHAPE;
+  if (!(p->scale >= 0.f) || !std::isfinite(p->scale) || !(p->tau >= 0.f) || !std::isfinite(p->tau))
+    return MKV_ERR_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;
+  if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
+  if ((p->n_q_heads / p->n_kv_heads) * p->window > 512) return MKV_ERR_UNSUPPORTED;
+  if (64 % p->chunk) return MKV_ERR_UNSUPPORTED;
+  if (p->mi_rounds < -1 || p->mi_rounds > 1) return MKV_ERR_UNSUPPORTED;
+  if (p->budget < p->ctx_len && p->budget < p->n_sink + p->window) return MKV_ERR_BUDGET;
+  const int n_out = p->budget < p->ctx_len ? p->budget : p->ctx_len;
+  if (p->cap < n_out) return MKV_ERR_CAPACITY;
+  const double elems = (double)p->batch * p->n_kv_heads * p->ctx_len * p->head_dim;
+  if (elems > 4.0e12) return MKV_ERR_UNSUPPORTED;
+  return MKV_OK;
+}
+
+mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t* total) {
+  mkv::CompressArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.B = p->batch;
+  a.Hq = p->n_q_heads;
+  a.Hkv = p->n_kv_heads;
+  a.G = p->n_q_heads / p->n_kv_heads;
+  a.D = p->head_dim;
+  a.N = p->ctx_len;
+  a.L = p->budget;
+  a.w = p->window;
+  a.n_s = p->n_sink;
+  a.chunk = p->chunk;
+  a.mi_rounds = p->mi_rounds;
+  a.cap = p->cap;
+  a.H = a.B * a.Hkv;
+  a.R = a.G * a.w;
+  a.n_c = a.N - a.w - a.n_s;
+  a.k_keep = a.L < a.N ? a.L - a.n_s - a.w : 0;
+  a.kmax = a.k_keep > 1 ? a.k_keep : 1;
+  a.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)a.D);
+  a.tau = p->tau;
+  a.ntile = ceil_div(a.N, 64);
+  // window-row / covariance pass: about 512 workgroups, whole 64-token tiles each
+  a.nsl1 = clampi(ceil_div(512, a.H), 1, a.ntile);
+  a.tps1 = ceil_div(a.ntile, a.nsl1);
+  a.nsl1 = ceil_div(a.ntile, a.tps1);
+  // downdate covariance over the kept rows
+  if (a.k_keep > 0) {
+    const int ntr = ceil_div(a.k_keep, 64);
+    a.nslr = clampi(ceil_div(256, a.H), 1, ntr);
+    a.tpsr = ceil_div(ntr, a.nslr);
+    a.nslr = ceil_div(ntr, a.tpsr);
+  } else {
+    a.nslr = 0;
+    a.tpsr = 1;
+  }
+  a.nslot = a.nsl1 + a.nslr;
+  // residual pass: 256 candidates per workgroup iteration
+  {
+    const int nu = ceil_div(a.n_c > 0 ? a.n_c : 1, 256);
+    a.nsl3 = clampi(ceil_div(1024, a.H), 1, nu);
+    a.tps3 = ceil_div(nu, a.nsl3);
+    a.nsl3 = ceil_div(nu, a.tps3);
+  }
+  const size_t H = a.H, D = a.D, es = elem_size(p->dtype);
+  const size_t nc = a.n_c > 0 ? a.n_c : 1;
+  Carver c;
+  c.base = static_cast<char*>(ws);
+  a.rowpart = c.take<float>(H * a.nsl1 * a.R * 2 * sizeof(float));
+  a.rowstat = c.take<float>(H * a.R * 2 * sizeof(float));
+  a.vnorm = c.take<float>(H * nc * sizeof(float));
+  a.abar = c.take<float>(H * nc * sizeof(float));
+  a.score0 = c.take<float>(H * nc * sizeof(float));
+  a.score = c.take<float>(H * nc * sizeof(float));
+  a.kept0 = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
+  a.kept = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
+  a.spart = c.take<float>(H * a.nslot * D * D * sizeof(float));
+  a.svkpart = c.take<float>(H * a.nslot * 2 * D * sizeof(float));
+  a.stil = c.take<float>(H * D * D * sizeof(float));
+  a.stil_hl = c.take<void>(H * 2 * D * D * 2);
+  a.vbar = c.take<float>(H * D * sizeof(float));
+  a.gath_k = c.take<void>(H * a.kmax * D * es);
+  a.gath_v = c.take<void>(H * a.kmax * D * es);
+  *total = c.off;
+  return a;
+}
+
+// ----------------------------------------------------------------------- decode
+mkv_status check_decode_params(const mkv_decode_params* p) {
+  if (!p) return MKV_ERR_NULL;
+  if (p->dtype != MKV_F32 && p->dtype != MKV_BF16) return MKV_ERR_DTYPE;
+  if (p->batch < 1 || p->n_q_heads < 1 || p->n_kv_heads < 1 || p->head_dim < 1 || p->cap < 1)
+    return MKV_ERR_SHAPE;
+  if (p->n_q_heads % p->n_kv_heads) return MKV_ERR_SHAPE;
+  if (p->order != 0 && p->order != 1) return MKV_ERR_SHAPE;
+  if (!(p->scale >= 0.f) || !std::isfinite(p->scale) || !(p->tau >= 0.f) || !std::isfinite(p->tau))
+    return MKV_ERR_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;
+  if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
+  if (p->max_len < 1 || p->max_len > p->cap) return MKV_ERR_CAPACITY;
+  return MKV_OK;
+}
+
+mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* total) {
+  mkv::DecodeArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.n_heads = p->batch * p->n_kv_heads;
+  a.G = p->n_q_heads / p->n_kv_heads;
+  a.n_pairs = p->batch * p->n_q_heads;
+  a.Hkv = p->n_kv_heads;
+  a.cap = p->cap;
+  a.order = p->order;
+  a.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)p->head_dim);
+  a.tau = p->tau;
+  // about 1024 workgroups; slices of at least 64 rows, multiples of 16
+  const int target = clampi(ceil_div(1024, a.n_heads), 1, 1 << 20);
+  int sl = ceil_div(p->max_len, target);
+  sl = ceil_div(sl, 16) * 16;
+  if (sl < 64) sl = 64;
+  a.split_len = sl;
+  a.nsplit = ceil_div(p->max_len, sl);
+  const size_t H = a.n_heads, D = p->head_dim, G = a.G;
+  Carver c;
+  c.base = static_cast<char*>(ws);
+  a.flag = c.take<int32_t>(sizeof(int32_t));
+  a.part_o = c.take<float>(H * a.nsplit * G * D * sizeof(float));
+  a.part_ml = c.take<float>(H * a.nsplit * G * 2 * sizeof(float));
+  a.sq = c.take<float>(H * G * D * sizeof(float));
+  *total = c.off;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t momentkv_compress_workspace_size(const mkv_compress_params* p) {
+  if (check_compress_params(p) != MKV_OK) return 0;
+  size_t total = 0;
+  compress_layout(p, nullptr, &total);
+  return total;
+}
+
+mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, const void* k,
+                             const void* v, void* k_out, void* v_out, int32_t* idx_out,
+                             int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, float* S,
+                             const mkv_compress_debug* dbg, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  mkv_status st = check_compress_params(p);
+  if (st != MKV_OK) return st;
+  if (!q_win || !k || !v || !k_out || !v_out || !idx_out || !lens_out || !n_e || !s_k || !s_v || !S)
+    return MKV_ERR_NULL;
+  size_t need = 0;
+  compress_layout(p, nullptr, &need);
+  if (!workspace || workspace_bytes < need) return MKV_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return MKV_ERR_WORKSPACE;
+  const size_t es = elem_size(p->dtype);
+  const size_t in_bytes = (size_t)p->batch * p->n_kv_heads * p->ctx_len * p->head_dim * es;
+  const size_t out_bytes = (size_t)p->batch * p->n_kv_heads * p->cap * p->head_dim * es;
+  if (ranges_overlap(k_out, out_bytes, k, in_bytes) || ranges_overlap(k_out, out_bytes, v, in_bytes) ||
+      ranges_overlap(v_out, out_bytes, k, in_bytes) || ranges_overlap(v_out, out_bytes, v, in_bytes) ||
+      ranges_overlap(k_out, out_bytes, v_out, out_bytes) ||
+      ranges_overlap(workspace, need, k, in_bytes) || ranges_overlap(workspace, need, v, in_bytes) ||
+      ranges_overlap(workspace, need, k_out, out_bytes) || ranges_overlap(workspace, need, v_out, out_bytes))
+    return MKV_ERR_ALIAS;
+  size_t total = 0;
+  mkv::CompressArgs a = compress_layout(p, workspace, &total);
+  a.q_win = q_win;
+  a.k = k;
+  a.v = v;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.idx_out = idx_out;
+  a.lens_out = lens_out;
+  a.n_e = n_e;
+  a.s_k = s_k;
+  a.s_v = s_v;
+  a.S = S;
+  hipError_t e = mkv::launch_compress(a, p->dtype == MKV_BF16, static_cast<hipStream_t>(stream),
+                                      dbg ? dbg->abar : nullptr, dbg ? dbg->score0 : nullptr,
+                                      dbg ? dbg->score : nullptr, dbg ? dbg->kept0 : nullptr);
+  return e == hipSuccess ? MKV_OK : MKV_ERR_HIP;
+}
+
+size_t momentkv_decode_workspace_size(const mkv_decode_params* p) {
+  if (check_decode_params(p) != MKV_OK) return 0;
+  size_t total = 0;
+  decode_layout(p, nullptr, &total);
+  return total;
+}
+
+mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
+                                void* v_cache, int32_t* lens, const void* k_new,
+                                const void* v_new, const int32_t* n_e, const float* s_k,
+                                const float* s_v, const float* S, void* out, float* lse_out,
+                                float* w_r_out, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  mkv_status st = check_decode_params(p);
+  if (st != MKV_OK) return st;
+  if (!q || !k_cache || !v_cache || !lens || !n_e || !s_k || !s_v || !S || !out) return MKV_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return MKV_ERR_NULL;
+  size_t need = 0;
+  decode_layout(p, nullptr, &need);
+  if (!workspace || workspace_bytes < need) return MKV_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return MKV_ERR_WORKSPACE;
+  const size_t es = elem_size(p->dtype);
+  const size_t cache_bytes = (size_t)p->batch * p->n_kv_heads * p->cap * p->head_dim * es;
+  const size_t out_bytes = (size_t)p->batch * p->n_q_heads * p->head_dim * es;
+  if (ranges_overlap(out, out_bytes, k_cache, cache_bytes) ||
+      ranges_overlap(out, out_bytes, v_cache, cache_bytes) ||
+      ranges_overlap(out, out_bytes, q, out_bytes) ||
+      ranges_overlap(k_cache, cache_bytes, v_cache, cache_bytes) ||
+      ranges_overlap(workspace, need, k_cache, cache_bytes) ||
+      ranges_overlap(workspace, need, v_cache, cache_bytes) ||
+      ranges_overlap(workspace, need, out, out_bytes))
+    return MKV_ERR_ALIAS;
+  size_t total = 0;
+  mkv::DecodeArgs a = decode_layout(p, workspace, &total);
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.lens = lens;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.n_e = n_e;
+  a.s_k = s_k;
+  a.s_v = s_v;
+  a.S = S;
+  a.out = out;
+  a.lse_out = lse_out;
+  a.w_r_out = w_r_out;
+  hipError_t e = mkv::launch_decode(a, p->dtype == MKV_BF16, p->head_dim,
+                                    static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MKV_OK : MKV_ERR_HIP;
+}
+
+const char* momentkv_status_string(int32_t s) {
+  switch (s) {
+    case MKV_OK: return "ok";
+    case MKV_ERR_NULL: return "a required pointer is NULL";
+    case MKV_ERR_SHAPE: return "invalid shape or parameter";
+    case MKV_ERR_BUDGET: return "budget smaller than sink + window";
+    case MKV_ERR_DTYPE: return "unsupported dtype";
+    case MKV_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case MKV_ERR_CAPACITY: return "cache capacity too small";
+    case MKV_ERR_ALIAS: return "output buffer overlaps an input";
+    case MKV_ERR_HIP: return "HIP launch failed";
+    case MKV_ERR_UNSUPPORTED: return "request outside this build's limits";
+    default: return "unknown status";
+  }
+}
+
+int32_t momentkv_abi_version(void) { return MOMENTKV_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,250 @@
+"""Thin ctypes binding of libmomentkv.so (C ABI in include/momentkv.h).
+
+Functions carry the C names.  `momentkv_compress` and `momentkv_decode_attn` take torch
+tensors that already live on the GPU, allocate the outputs and the workspace when the
+caller does not pass them, and forward device pointers plus the current HIP stream to
+the library.  No arithmetic of the method happens here: every step runs in the HIP
+kernels.  The library is loaded on first use; a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmomentkv.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "momentkv.h")
+
+MKV_F32, MKV_BF16 = 0, 1
+STATUS = {0: "MKV_OK", 1: "MKV_ERR_NULL", 2: "MKV_ERR_SHAPE", 3: "MKV_ERR_BUDGET",
+          4: "MKV_ERR_DTYPE", 5: "MKV_ERR_WORKSPACE", 6: "MKV_ERR_CAPACITY",
+          7: "MKV_ERR_ALIAS", 8: "MKV_ERR_HIP", 9: "MKV_ERR_UNSUPPORTED"}
+
+
+class MomentKVError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {STATUS.get(code, code)} ({momentkv_status_string(code)})")
+        self.code = code
+
+
+class CompressParams(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("ctx_len", ctypes.c_int32), ("budget", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("n_sink", ctypes.c_int32),
+                ("chunk", ctypes.c_int32), ("mi_rounds", ctypes.c_int32),
+                ("cap", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("tau", ctypes.c_float)]
+
+
+class CompressDebug(ctypes.Structure):
+    _fields_ = [("abar", ctypes.c_void_p), ("score0", ctypes.c_void_p),
+                ("score", ctypes.c_void_p), ("kept0", ctypes.c_void_p)]
+
+
+class DecodeParams(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("cap", ctypes.c_int32), ("max_len", ctypes.c_int32),
+                ("order", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("tau", ctypes.c_float)]
+
+
+_lib = None
+_VP = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmomentkv.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        L.momentkv_compress_workspace_size.argtypes = [ctypes.POINTER(CompressParams)]
+        L.momentkv_compress_workspace_size.restype = ctypes.c_size_t
+        L.momentkv_compress.argtypes = [ctypes.POINTER(CompressParams)] + [_VP] * 11 + \
+            [ctypes.POINTER(CompressDebug), _VP, ctypes.c_size_t, _VP]
+        L.momentkv_compress.restype = ctypes.c_int
+        L.momentkv_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeParams)]
+        L.momentkv_decode_workspace_size.restype = ctypes.c_size_t
+        L.momentkv_decode_attn.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 13 + \
+            [_VP, ctypes.c_size_t, _VP]
+        L.momentkv_decode_attn.restype = ctypes.c_int
+        L.momentkv_status_string.argtypes = [ctypes.c_int32]
+        L.momentkv_status_string.restype = ctypes.c_char_p
+        L.momentkv_abi_version.argtypes = []
+        L.momentkv_abi_version.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def declared_symbols() -> list[str]:
+    """Entry points declared in include/momentkv.h."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(momentkv_[a-z_]+)\s*\(", text)))
+
+
+def momentkv_status_string(code: int) -> str:
+    return lib().momentkv_status_string(int(code)).decode()
+
+
+def momentkv_abi_version() -> int:
+    return int(lib().momentkv_abi_version())
+
+
+def momentkv_compress_workspace_size(p: CompressParams) -> int:
+    return int(lib().momentkv_compress_workspace_size(ctypes.byref(p)))
+
+
+def momentkv_decode_workspace_size(p: DecodeParams) -> int:
+    return int(lib().momentkv_decode_workspace_size(ctypes.byref(p)))
+
+
+# ------------------------------------------------------------------------ marshalling
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return MKV_F32
+    if t.dtype == torch.bfloat16:
+        return MKV_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _workspace(nbytes: int, device, ws: torch.Tensor | None) -> torch.Tensor:
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    if ws.data_ptr() % 256:
+        raise ValueError("workspace must be 256-byte aligned")
+    return ws
+
+
+@dataclass
+class CompressOutput:
+    k_out: torch.Tensor       # [B, Hkv, cap, d]
+    v_out: torch.Tensor
+    idx: torch.Tensor         # [B, Hkv, min(L, N)] int32
+    lens: torch.Tensor        # [B, Hkv] int32
+    n_e: torch.Tensor         # [B, Hkv] int32
+    s_k: torch.Tensor         # [B, Hkv, d] fp32
+    s_v: torch.Tensor
+    S: torch.Tensor           # [B, Hkv, d, d] fp32
+    abar: torch.Tensor | None = None
+    score0: torch.Tensor | None = None
+    score: torch.Tensor | None = None
+    kept0: torch.Tensor | None = None
+
+
+def compress_params(q_win, k, budget, *, n_sink=1, chunk=4, mi_rounds=1, cap=None,
+                    scale=0.0, tau=1e-6) -> CompressParams:
+    B, Hq, w, d = q_win.shape
+    _, Hkv, N, _ = k.shape
+    n_out = min(budget, N)
+    return CompressParams(B, Hq, Hkv, d, N, budget, w, n_sink, chunk, mi_rounds,
+                          n_out if cap is None else cap, _dtype_code(k), scale, tau)
+
+
+def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, budget: int, *,
+                      n_sink: int = 1, chunk: int = 4, mi_rounds: int = 1, cap: int | None = None,
+                      scale: float = 0.0, tau: float = 1e-6, debug: bool = False,
+                      out: CompressOutput | None = None,
+                      workspace: torch.Tensor | None = None) -> CompressOutput:
+    """Compress [B, Hkv, N, d] prefill K/V to `budget` rows per KV head (see the header)."""
+    p = compress_params(q_win, k, budget, n_sink=n_sink, chunk=chunk, mi_rounds=mi_rounds,
+                        cap=cap, scale=scale, tau=tau)
+    B, Hq, w, d = q_win.shape
+    _, Hkv, N, _ = k.shape
+    dev = k.device
+    n_out = min(budget, N)
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=dev)
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = CompressOutput(
+            k_out=torch.empty(B, Hkv, p.cap, d, dtype=k.dtype, device=dev),
+            v_out=torch.empty(B, Hkv, p.cap, d, dtype=k.dtype, device=dev),
+            idx=torch.empty(B, Hkv, n_out, **i32), lens=torch.empty(B, Hkv, **i32),
+            n_e=torch.empty(B, Hkv, **i32), s_k=torch.empty(B, Hkv, d, **f32),
+            s_v=torch.empty(B, Hkv, d, **f32), S=torch.empty(B, Hkv, d, d, **f32))
+    dbg = None
+    if debug and budget < N:
+        n_c = N - w - n_sink
+        k_keep = budget - n_sink - w
+        f32 = dict(dtype=torch.float32, device=dev)
+        out.abar = torch.zeros(B, Hkv, n_c, **f32)
+        out.score0 = torch.zeros(B, Hkv, n_c, **f32)
+        out.score = torch.zeros(B, Hkv, n_c, **f32)
+        out.kept0 = torch.zeros(B, Hkv, max(k_keep, 0), dtype=torch.int32, device=dev)
+        dbg = CompressDebug(_ptr(out.abar), _ptr(out.score0), _ptr(out.score),
+                            _ptr(out.kept0) if k_keep > 0 else None)
+    nbytes = momentkv_compress_workspace_size(p)
+    if nbytes == 0:
+        code = lib().momentkv_compress(ctypes.byref(p), *([None] * 11), None, None, 0, None)
+        raise MomentKVError(code, "momentkv_compress")
+    ws = _workspace(nbytes, dev, workspace)
+    code = lib().momentkv_compress(
+        ctypes.byref(p), _ptr(q_win), _ptr(k), _ptr(v), _ptr(out.k_out), _ptr(out.v_out),
+        _ptr(out.idx), _ptr(out.lens), _ptr(out.n_e), _ptr(out.s_k), _ptr(out.s_v), _ptr(out.S),
+        ctypes.byref(dbg) if dbg is not None else None, ws.data_ptr(), ws.numel(), _stream())
+    if code != 0:
+        raise MomentKVError(code, "momentkv_compress")
+    return out
+
+
+def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6) -> DecodeParams:
+    B, Hq, d = q.shape
+    _, Hkv, cap, _ = k_cache.shape
+    return DecodeParams(B, Hq, Hkv, d, cap, max_len, order, _dtype_code(q), scale, tau)
+
+
+def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                         lens: torch.Tensor, n_e: torch.Tensor, s_k: torch.Tensor,
+                         s_v: torch.Tensor, S: torch.Tensor, *, k_new: torch.Tensor | None = None,
+                         v_new: torch.Tensor | None = None, max_len: int | None = None,
+                         order: int = 1, scale: float = 0.0, tau: float = 1e-6,
+                         out: torch.Tensor | None = None, lse: torch.Tensor | None = None,
+                         w_r: torch.Tensor | None = None,
+                         workspace: torch.Tensor | None = None):
+    """Corrected decode attention (see the header).  Returns (out, lse, w_r, workspace).
+
+    `max_len` bounds lens after the append (defaults to the cache capacity).  The first
+    int32 of the workspace is the append-overflow flag; a fresh workspace is zeroed.
+    """
+    cap = k_cache.shape[2]
+    p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
+                      scale=scale, tau=tau)
+    dev = q.device
+    if out is None:
+        out = torch.empty_like(q)
+    nbytes = momentkv_decode_workspace_size(p)
+    if nbytes == 0:
+        code = lib().momentkv_decode_attn(ctypes.byref(p), *([None] * 13), None, 0, None)
+        raise MomentKVError(code, "momentkv_decode_attn")
+    fresh = workspace is None or workspace.numel() < nbytes
+    ws = _workspace(nbytes, dev, workspace)
+    if fresh:
+        ws[:256].zero_()
+    code = lib().momentkv_decode_attn(
+        ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lens), _ptr(k_new),
+        _ptr(v_new), _ptr(n_e), _ptr(s_k), _ptr(s_v), _ptr(S), _ptr(out), _ptr(lse), _ptr(w_r),
+        ws.data_ptr(), ws.numel(), _stream())
+    if code != 0:
+        raise MomentKVError(code, "momentkv_decode_attn")
+    return out, lse, w_r, ws

@@ -1,0 +1,148 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared entry point,
+sizes workspaces, and rejects invalid arguments before launching anything.
+
+Every call below fails host-side validation (or is a pure size query), so no HIP work
+is ever enqueued.
+"""
+import ctypes
+import os
+
+import pytest
+
+from paper_2606_01563_amd import momentkv as mk
+
+OK, NULL, SHAPE, BUDGET, DTYPE, WORKSPACE, CAPACITY, ALIAS, HIP, UNSUP = range(10)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(mk.LIB_PATH):
+        pytest.fail("libmomentkv.so is not built (run __graft_entry__.build())")
+    return mk.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    syms = mk.declared_symbols()
+    assert {"momentkv_compress", "momentkv_decode_attn"} <= set(syms)
+    for s in syms:
+        assert hasattr(L, s), s
+
+
+def test_abi_version_and_status_strings(L):
+    assert mk.momentkv_abi_version() == 1
+    for code in range(10):
+        assert mk.momentkv_status_string(code) not in ("", "unknown status")
+    assert mk.momentkv_status_string(99) == "unknown status"
+
+
+def cparams(**kw):
+    base = dict(batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, ctx_len=32768, budget=512,
+                window=32, n_sink=1, chunk=4, mi_rounds=1, cap=512, dtype=1, scale=0.0, tau=1e-6)
+    base.update(kw)
+    return mk.CompressParams(**base)
+
+
+def dparams(**kw):
+    base = dict(batch=36, n_q_heads=32, n_kv_heads=8, head_dim=128, cap=640, max_len=640,
+                order=1, dtype=1, scale=0.0, tau=1e-6)
+    base.update(kw)
+    return mk.DecodeParams(**base)
+
+
+def compress_status(p, ptr=1 << 20, ws_bytes=None, ws=1 << 40):
+    """Call momentkv_compress with fake, non-overlapping device addresses; validation must
+    reject the call before any of them is touched."""
+    size = mk.momentkv_compress_workspace_size(p)
+    if ws_bytes is None:
+        ws_bytes = size
+    step = 1 << 36
+    ptrs = [ptr + i * step if ptr else None for i in range(11)]
+    return mk.lib().momentkv_compress(ctypes.byref(p), *ptrs, None, ws, ws_bytes, None)
+
+
+def decode_status(p, ptr=1 << 20, ws=1 << 40, ws_bytes=None, k_new=True):
+    size = mk.momentkv_decode_workspace_size(p)
+    if ws_bytes is None:
+        ws_bytes = size
+    step = 1 << 36
+    ptrs = [ptr + i * step if ptr else None for i in range(13)]
+    if not k_new:
+        ptrs[4] = None
+    return mk.lib().momentkv_decode_attn(ctypes.byref(p), *ptrs, ws, ws_bytes, None)
+
+
+def test_workspace_sizes(L):
+    assert mk.momentkv_compress_workspace_size(cparams()) > 0
+    assert mk.momentkv_decode_workspace_size(dparams()) > 0
+    assert mk.momentkv_compress_workspace_size(cparams(head_dim=96)) == 0
+    assert mk.momentkv_decode_workspace_size(dparams(max_len=641)) == 0
+    # size grows with context and with budget
+    assert mk.momentkv_compress_workspace_size(cparams(ctx_len=131072, window=64, budget=1024, cap=1024)) > \
+        mk.momentkv_compress_workspace_size(cparams())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_q_heads=30), SHAPE),            # Hq % Hkv != 0
+    (dict(batch=0), SHAPE),
+    (dict(window=0), SHAPE),
+    (dict(window=32768), SHAPE),            # w >= N
+    (dict(chunk=0), SHAPE),
+    (dict(tau=-1.0), SHAPE),
+    (dict(scale=float("nan")), SHAPE),
+    (dict(head_dim=96), UNSUP),
+    (dict(chunk=3), UNSUP),                 # chunk must divide 64
+    (dict(mi_rounds=2), UNSUP),
+    (dict(n_q_heads=8 * 17), UNSUP),        # G > 16
+    (dict(window=200), UNSUP),              # G * w > 512
+    (dict(budget=20), BUDGET),              # < n_sink + window
+    (dict(cap=100), CAPACITY),
+    (dict(dtype=7), DTYPE),
+])
+def test_compress_rejects_invalid_parameters(L, kw, code):
+    assert compress_status(cparams(**kw)) == code
+
+
+def test_compress_rejects_null_alias_and_small_workspace(L):
+    p = cparams()
+    assert compress_status(p, ptr=0) == NULL
+    assert mk.lib().momentkv_compress(None, *([None] * 11), None, None, 0, None) == NULL
+    assert compress_status(p, ws_bytes=16) == WORKSPACE
+    assert compress_status(p, ws=0) == WORKSPACE
+    assert compress_status(p, ws=(1 << 40) + 8) == WORKSPACE       # misaligned
+    # k_out aliasing k
+    ptrs = [(1 << 20) + i * (1 << 36) for i in range(11)]
+    ptrs[3] = ptrs[1]
+    size = mk.momentkv_compress_workspace_size(p)
+    assert mk.lib().momentkv_compress(ctypes.byref(p), *ptrs, None, 1 << 40, size, None) == ALIAS
+    # workspace overlapping v
+    ptrs = [(1 << 20) + i * (1 << 36) for i in range(11)]
+    assert mk.lib().momentkv_compress(ctypes.byref(p), *ptrs, None, ptrs[2], size, None) == ALIAS
+
+
+def test_budget_at_least_context_is_valid(L):
+    p = cparams(ctx_len=300, budget=5000, cap=300)
+    assert mk.momentkv_compress_workspace_size(p) > 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_q_heads=30), SHAPE),
+    (dict(cap=0), SHAPE),
+    (dict(order=2), SHAPE),
+    (dict(head_dim=80), UNSUP),
+    (dict(max_len=0), CAPACITY),
+    (dict(max_len=641), CAPACITY),
+    (dict(dtype=3), DTYPE),
+])
+def test_decode_rejects_invalid_parameters(L, kw, code):
+    assert decode_status(dparams(**kw)) == code
+
+
+def test_decode_rejects_null_alias_and_small_workspace(L):
+    p = dparams()
+    assert decode_status(p, ptr=0) == NULL
+    assert decode_status(p, k_new=False) == NULL        # k_new without v_new
+    assert decode_status(p, ws_bytes=8) == WORKSPACE
+    ptrs = [(1 << 20) + i * (1 << 36) for i in range(13)]
+    ptrs[10] = ptrs[1]                                   # out aliases the key cache
+    size = mk.momentkv_decode_workspace_size(p)
+    assert mk.lib().momentkv_decode_attn(ctypes.byref(p), *ptrs, 1 << 40, size, None) == ALIAS

@@ -1,0 +1,187 @@
+"""GPU parity of the HIP path against the fp64 oracle (through the C ABI).
+
+Inputs are the seeded synthetic workloads; the oracle consumes host copies of exactly
+the bits the GPU consumed.  Sizes are small enough for the oracle to finish in seconds
+while spanning many 64-token tiles and a ragged tail; the full-size cases check sampled
+heads.  See tests/parity_util.py for the protocol and tolerances.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2606_01563_amd import synth
+from paper_2606_01563_amd import momentkv as mk
+from tests import parity_util as P
+
+pytestmark = pytest.mark.gpu
+
+
+def layer(name, layer_idx=0, steps=None, **over):
+    wl = synth.WORKLOADS[name]
+    if over:
+        wl = synth.shrink(wl, **over)
+    cpu = synth.make_layer(wl, layer_idx, device="cpu", decode_steps=steps)
+    gpu = {k: v.cuda() for k, v in cpu.items()}
+    return wl, cpu, gpu
+
+
+def announce(msg):
+    print(f"[parity] {msg}", flush=True)
+
+
+# ---------------------------------------------------------------- tiny fp32 workload
+def test_tiny_fp32_compress_and_decode():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=16)
+    L = wl.budgets[0]
+    announce(f"{wl.name} compress L={L}")
+    out = P.run_compress(gpu, L, cap=L + 16)
+    errs = P.check_compress_head(cpu, out, 0, 0, L)
+    announce(f"errors {errs}")
+    assert errs["swaps"] == 0 and errs["swaps0"] == 0
+    worst = P.run_decode_steps(gpu, out, 16)
+    announce(f"decode worst rel err {max(worst):.2e}")
+
+
+def test_llama_layer_bf16_compress_and_decode():
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=24)
+    L = wl.budgets[0]
+    announce(f"{wl.name} compress L={L}")
+    out = P.run_compress(gpu, L, cap=L + 24)
+    for h in range(wl.n_kv_heads):
+        errs = P.check_compress_head(cpu, out, 0, h, L)
+        announce(f"head {h} errors {errs}")
+    worst = P.run_decode_steps(gpu, out, 24)
+    announce(f"decode worst rel err {max(worst):.2e}")
+
+
+# ---------------------------------------------------------------- edge cases
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("d", [64, 128])
+def test_ragged_shapes_and_both_head_dims(dtype, d):
+    """N not a multiple of 64, batch 2, GQA 2, both head dims and dtypes."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=d, ctx_len=1000,
+                         batch=2, n_q_heads=4, n_kv_heads=2, window=16, budgets=(97,))
+    announce(f"ragged d={d} {dtype}")
+    out = P.run_compress(gpu, 97, cap=100)
+    for b in range(2):
+        for h in range(2):
+            P.check_compress_head(cpu, out, b, h, 97)
+    P.run_decode_steps(gpu, out, 3)
+
+
+@pytest.mark.parametrize("mi_rounds", [-1, 0, 1])
+@pytest.mark.parametrize("chunk", [1, 4, 8])
+def test_selection_modes_and_chunks(mi_rounds, chunk):
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, ctx_len=700, budgets=(80,))
+    out = P.run_compress(gpu, 80, chunk=chunk, mi_rounds=mi_rounds)
+    P.check_compress_head(cpu, out, 0, 0, 80, chunk=chunk, mi_rounds=mi_rounds)
+
+
+def test_budget_equal_to_protected_tokens_evicts_every_candidate():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=2, ctx_len=300)
+    L = 1 + wl.window
+    out = P.run_compress(gpu, L, cap=L + 2)
+    P.check_compress_head(cpu, out, 0, 0, L)
+    assert int(out.n_e[0, 0]) == 300 - L
+    P.run_decode_steps(gpu, out, 2)
+
+
+@pytest.mark.parametrize("budget", [300, 5000])
+def test_budget_at_least_context_keeps_everything(budget):
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=2, ctx_len=300)
+    out = P.run_compress(gpu, budget, cap=302)
+    P.check_compress_head(cpu, out, 0, 0, budget)
+    P.run_decode_steps(gpu, out, 2)  # n_e = 0: plain softmax attention
+
+
+def test_long_window_group_rows_256():
+    """G * w = 256 window rows (the 128K workload's window of 64)."""
+    wl, cpu, gpu = layer("ruler_n131072", steps=2, ctx_len=3000, budgets=(200,),
+                         n_q_heads=8, n_kv_heads=2)
+    out = P.run_compress(gpu, 200, cap=202)
+    for h in range(2):
+        P.check_compress_head(cpu, out, 0, h, 200)
+    P.run_decode_steps(gpu, out, 2)
+
+
+def test_zeroth_order_decode_and_no_append():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, ctx_len=600, budgets=(64,))
+    out = P.run_compress(gpu, 64, cap=64)
+    P.run_decode_steps(gpu, out, 3, order=0, append=False)
+
+
+def test_append_into_full_cache_sets_flag_and_skips():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, ctx_len=400, budgets=(64,))
+    out = P.run_compress(gpu, 64, cap=64)
+    lens_before = out.lens.clone()
+    res, _, _, ws = mk.momentkv_decode_attn(
+        gpu["q_dec"][0], out.k_out, out.v_out, out.lens, out.n_e, out.s_k, out.s_v, out.S,
+        k_new=gpu["k_new"][0], v_new=gpu["v_new"][0], max_len=64)
+    torch.cuda.synchronize()
+    assert int(ws[:4].view(torch.int32)[0]) == 1
+    assert torch.equal(out.lens, lens_before)
+    m = [[P.oracle_moments(out, 0, 0)]]
+    ref, _, _, _ = O.decode(P.h64(gpu["q_dec"][0]), P.h64(out.k_out), P.h64(out.v_out),
+                            out.lens.cpu().numpy(), m)
+    assert P.rel_l2(P.h64(res)[0, 0], ref[0, 0]) <= 1e-5
+
+
+def test_compress_and_decode_are_bit_deterministic():
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=1, ctx_len=4000)
+    a = P.run_compress(gpu, 300, cap=301)
+    b = P.run_compress(gpu, 300, cap=301)
+    for f in ("k_out", "v_out", "idx", "lens", "n_e", "s_k", "s_v", "S", "abar", "score0",
+              "score", "kept0"):
+        assert torch.equal(getattr(a, f), getattr(b, f)), f
+    outs = []
+    for c in (a, b):
+        o, _, _, _ = mk.momentkv_decode_attn(gpu["q_dec"][0], c.k_out, c.v_out, c.lens, c.n_e,
+                                             c.s_k, c.s_v, c.S, k_new=gpu["k_new"][0],
+                                             v_new=gpu["v_new"][0], max_len=301)
+        outs.append(o)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+
+
+def test_zero_key_spread_decode_equals_full_attention_on_gpu():
+    """Paper invariant end to end: with every candidate key equal, the corrected decode
+    output equals full attention over all N tokens (Sec. 4.2, App. B.2)."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, ctx_len=500, budgets=(100,))
+    k = cpu["k"].clone()
+    k[0, 0, 1:500 - wl.window] = k[0, 0, 7]
+    cpu["k"] = k
+    gpu["k"] = k.cuda()
+    out = P.run_compress(gpu, 100, cap=100)
+    res, _, _, _ = mk.momentkv_decode_attn(gpu["q_dec"][0], out.k_out, out.v_out, out.lens,
+                                           out.n_e, out.s_k, out.s_v, out.S, max_len=100)
+    torch.cuda.synchronize()
+    q = P.h64(cpu["q_dec"][0])[0]
+    K, V = P.h64(k)[0, 0], P.h64(cpu["v"])[0, 0]
+    full = np.stack([O.attention_parts(q[g], K, V, np.arange(500))["f"] for g in range(4)])
+    assert P.rel_l2(P.h64(res)[0], full) <= 1e-5
+
+
+# ---------------------------------------------------------------- full-size sampled heads
+@pytest.mark.parametrize("budget", [128, 2048])
+def test_qwen_stack_layer_full_size_sampled_heads(budget):
+    """One 32K-context layer of the Qwen3-4B-shaped stack, both ends of the budget range,
+    checked on two sampled KV heads."""
+    wl, cpu, gpu = layer("qwen3_4b_stack_n32768", layer_idx=3, steps=2)
+    announce(f"{wl.name} L={budget}")
+    out = P.run_compress(gpu, budget, cap=budget + 2)
+    for h in (0, 5):
+        errs = P.check_compress_head(cpu, out, 0, h, budget)
+        announce(f"head {h} {errs}")
+    P.run_decode_steps(gpu, out, 2)
+
+
+def test_ruler_128k_full_size_sampled_head():
+    wl, cpu, gpu = layer("ruler_n131072", layer_idx=0, steps=1)
+    announce(f"{wl.name}")
+    out = P.run_compress(gpu, 1024, cap=1025)
+    errs = P.check_compress_head(cpu, out, 0, 2, 1024)
+    announce(f"head 2 {errs}")
+    P.run_decode_steps(gpu, out, 1)
