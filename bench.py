@@ -1,0 +1,287 @@
+#!/usr/bin/env python3
+"""MomentKV hot-path benchmark on one MI355X.
+
+Workload (default): the Qwen3-4B-shaped 36-layer stack with 32K-token prefill contexts
+(32 query heads, 8 KV heads, head_dim 128, bf16), at budgets 128, 256, 512, 1024 and 2048
+retained tokens per KV head.  Seeded synthetic post-RoPE inputs are generated on the
+GPU and stay resident in HBM.  One timed step is one pass of the whole hot path:
+
+  for every budget: momentkv_compress of each of the 36 layers (per-layer calls), writing
+                    that layer's retained cache and moments into a 36-layer stack;
+  then 128 decode tokens: for each token and each budget one momentkv_decode_attn launch
+                    over the flattened (layer x sequence) batch of 36 caches, appending the
+                    token's key/value (budgets interleaved, so consecutive launches touch
+                    different caches and the 256 MB last-level cache cannot hold them).
+
+Reported (one JSON line): decode attention+correction GB/s (algorithmic bytes / time, the
+`value`), decode tokens/s and compress ms/layer per budget, a roofline object for the
+decode kernel and the fp64 oracle timed on the host as a CPU baseline.  Every launch is
+timed with HIP events recorded on the stream the library launches on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_01563_amd import synth  # noqa: E402
+from paper_2606_01563_amd import momentkv as mk  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+
+def decode_bytes(n_heads: int, G: int, d: int, lens_after: int, elem: int = 2) -> int:
+    """Algorithmic HBM bytes of one decode launch (per KV head, summed over heads):
+    retained K and V rows read, the d x d summary and its two vectors and count read,
+    the G queries read and G outputs written, the appended key/value read and written,
+    and lens read and written."""
+    per_head = (2 * lens_after * d * elem + 4 * d * d + 8 * d + 4 + 2 * G * d * elem
+                + 4 * d * elem + 8)
+    return n_heads * per_head
+
+
+def compress_bytes(n_kv_heads: int, N: int, d: int, L: int, elem: int = 2) -> int:
+    """Algorithmic bytes of one layer's compress: K and V read once, retained rows written,
+    the summary written."""
+    return n_kv_heads * (2 * N * d * elem + 2 * L * d * elem + 4 * d * d + 8 * d + 4 + 4 * L)
+
+
+def build_stack(wl, layers, device):
+    t0 = time.time()
+    data = [synth.make_layer(wl, l, device=device) for l in range(layers)]
+    torch.cuda.synchronize()
+    return data, time.time() - t0
+
+
+def cpu_baseline(wl, data, budget: int, heads: int, steps: int) -> dict:
+    """The fp64 oracle on the host: compress `heads` KV heads of layer 0 at `budget`, then
+    `steps` decode steps of those heads' query groups.  Scaled to GB/s of decode like
+    `value`; compress time extrapolated per layer."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # noqa: BLE001
+        blas_threads = 1
+    f64 = lambda t: t.float().cpu().double().numpy()  # noqa: E731
+    d, G = wl.head_dim, wl.group
+    q = f64(data["q_win"])[0]
+    K = f64(data["k"])[0]
+    V = f64(data["v"])[0]
+    t0 = time.perf_counter()
+    comp = [O.compress_head(q[h * G:(h + 1) * G], K[h], V[h], budget) for h in range(heads)]
+    t_comp = time.perf_counter() - t0
+    qd = f64(data["q_dec"][:steps])[:, 0]
+    kn = f64(data["k_new"][:steps])[:, 0]
+    vn = f64(data["v_new"][:steps])[:, 0]
+    kc = np.stack([c.k_out for c in comp])[None]
+    vc = np.stack([c.v_out for c in comp])[None]
+    cap = budget + steps
+    kcap = np.zeros((1, heads, cap, d))
+    vcap = np.zeros((1, heads, cap, d))
+    kcap[:, :, :budget] = kc
+    vcap[:, :, :budget] = vc
+    ln = np.full((1, heads), budget)
+    moms = [[c.moments for c in comp]]
+    nbytes = 0
+    t0 = time.perf_counter()
+    for t in range(steps):
+        _, _, _, (kcap, vcap, ln) = O.decode(qd[t][None, :heads * G], kcap, vcap, ln, moms,
+                                             k_new=kn[t][None, :heads], v_new=vn[t][None, :heads])
+        nbytes += decode_bytes(heads, G, d, budget + t + 1)
+    t_dec = time.perf_counter() - t0
+    return {"value": nbytes / t_dec / 1e9, "unit": "GB/s", "cores": int(blas_threads),
+            "host_cpus": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "sample": f"layer 0, {heads} of {wl.n_kv_heads} KV heads, budget {budget}: "
+                      f"compress, then {steps} decode steps (fp64 NumPy)",
+            "compress_ms_per_layer_extrapolated": t_comp / heads * wl.n_kv_heads * 1e3,
+            "decode_s": t_dec, "compress_s": t_comp}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="qwen3_4b_stack_n32768", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--layers", type=int, default=None)
+    ap.add_argument("--budgets", default=None, help="comma list overriding the workload's")
+    ap.add_argument("--decode-steps", type=int, default=None)
+    ap.add_argument("--cpu-heads", type=int, default=2)
+    ap.add_argument("--cpu-steps", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the MomentKV hot path shards over (sequence, KV head) "
+              "with no exchange, and this build runs on a single MI355X; use --gpus 1.",
+              file=sys.stderr)
+        return 2
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.WORKLOADS[args.workload]
+    layers = args.layers or wl.layers
+    budgets = tuple(int(x) for x in args.budgets.split(",")) if args.budgets else wl.budgets
+    T = args.decode_steps if args.decode_steps is not None else wl.decode_steps
+    wl = synth.shrink(wl, decode_steps=T)
+    B, Hq, Hkv, d, N, w = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.ctx_len, wl.window
+    G = wl.group
+    print(f"[bench] generating {layers} layers of {wl.name} on {torch.cuda.get_device_name(0)}",
+          file=sys.stderr, flush=True)
+    data, gen_s = build_stack(wl, layers, dev)
+    print(f"[bench] inputs ready in {gen_s:.1f}s", file=sys.stderr, flush=True)
+
+    # decode inputs stacked over layers: [T, layers*B, ...]
+    q_steps = torch.stack([x["q_dec"] for x in data], dim=1).reshape(T, layers * B, Hq, d).contiguous()
+    kn_steps = torch.stack([x["k_new"] for x in data], dim=1).reshape(T, layers * B, Hkv, d).contiguous()
+    vn_steps = torch.stack([x["v_new"] for x in data], dim=1).reshape(T, layers * B, Hkv, d).contiguous()
+
+    LB = layers * B
+    f32 = dict(dtype=torch.float32, device=dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    stacks = {}
+    for L in budgets:
+        cap = min(L, N) + T
+        stacks[L] = mk.CompressOutput(
+            k_out=torch.empty(LB, Hkv, cap, d, dtype=wl.dtype, device=dev),
+            v_out=torch.empty(LB, Hkv, cap, d, dtype=wl.dtype, device=dev),
+            idx=torch.empty(LB, Hkv, min(L, N), **i32), lens=torch.empty(LB, Hkv, **i32),
+            n_e=torch.empty(LB, Hkv, **i32), s_k=torch.empty(LB, Hkv, d, **f32),
+            s_v=torch.empty(LB, Hkv, d, **f32), S=torch.empty(LB, Hkv, d, d, **f32))
+    cws_bytes = max(mk.momentkv_compress_workspace_size(
+        mk.compress_params(data[0]["q_win"], data[0]["k"], L, cap=min(L, N) + T)) for L in budgets)
+    cws = torch.empty(cws_bytes, dtype=torch.uint8, device=dev)
+    dws = {}
+    out = torch.empty(LB, Hq, d, dtype=wl.dtype, device=dev)
+    for L in budgets:
+        p = mk.decode_params(q_steps[0], stacks[L].k_out, max_len=min(L, N) + T)
+        dws[L] = torch.zeros(mk.momentkv_decode_workspace_size(p), dtype=torch.uint8, device=dev)
+
+    def layer_view(st, l):
+        sl = slice(l * B, (l + 1) * B)
+        return mk.CompressOutput(st.k_out[sl], st.v_out[sl], st.idx[sl], st.lens[sl], st.n_e[sl],
+                                 st.s_k[sl], st.s_v[sl], st.S[sl])
+
+    views = {L: [layer_view(stacks[L], l) for l in range(layers)] for L in budgets}
+
+    def step(timing):
+        ev = []
+        for L in budgets:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for l in range(layers):
+                x = data[l]
+                mk.momentkv_compress(x["q_win"], x["k"], x["v"], L, cap=min(L, N) + T,
+                                     out=views[L][l], workspace=cws)
+            e1.record()
+            timing["compress"][L].append((e0, e1))
+        for t in range(T):
+            for L in budgets:
+                st = stacks[L]
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                mk.momentkv_decode_attn(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k,
+                                        st.s_v, st.S, k_new=kn_steps[t], v_new=vn_steps[t],
+                                        max_len=min(L, N) + T, out=out, workspace=dws[L])
+                e1.record()
+                timing["decode"][L].append((e0, e1, min(L, N) + t + 1))
+        return ev
+
+    def new_timing():
+        return {"compress": {L: [] for L in budgets}, "decode": {L: [] for L in budgets}}
+
+    for _ in range(args.warmup):
+        step(new_timing())
+    torch.cuda.synchronize()
+    timing = new_timing()
+    s0 = torch.cuda.Event(enable_timing=True)
+    s1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    s0.record()
+    for i in range(args.steps):
+        step(timing)
+        print(f"[bench] step {i + 1}/{args.steps} enqueued", file=sys.stderr, flush=True)
+    s1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = s0.elapsed_time(s1)
+    for st in stacks.values():
+        assert int(mk.lib() is not None)
+    flags = [int(dws[L][:4].view(torch.int32)[0]) for L in budgets]
+    if any(flags):
+        print(f"[bench] append overflow flags {flags}", file=sys.stderr)
+        return 3
+
+    per_budget = {}
+    dec_bytes_tot = 0.0
+    dec_ms_tot = 0.0
+    for L in budgets:
+        cms = [a.elapsed_time(b) for a, b in timing["compress"][L]]
+        dms = [a.elapsed_time(b) for a, b, _ in timing["decode"][L]]
+        dby = [decode_bytes(LB * Hkv, G, d, n) for _, _, n in timing["decode"][L]]
+        dec_bytes_tot += sum(dby)
+        dec_ms_tot += sum(dms)
+        per_budget[str(L)] = {
+            "compress_ms_per_layer": sum(cms) / len(cms) / layers,
+            "compress_GBps": compress_bytes(Hkv * B, N, d, min(L, N)) / (sum(cms) / len(cms) / layers * 1e-3) / 1e9,
+            "decode_us_per_launch": sum(dms) / len(dms) * 1e3,
+            "decode_GBps": sum(dby) / (sum(dms) * 1e-3) / 1e9,
+            "decode_tokens_per_s": B * len(dms) / (sum(dms) * 1e-3),
+        }
+    value = dec_bytes_tot / (dec_ms_tot * 1e-3) / 1e9
+    n_launch = sum(len(timing["decode"][L]) for L in budgets)
+    avg_launch_s = dec_ms_tot * 1e-3 / n_launch
+    avg_bytes = dec_bytes_tot / n_launch
+    res = {
+        "metric": "decode attn+correction GB/s & tokens/s; compress ms/layer @32K ctx",
+        "value": value,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == torch.bfloat16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": layers, "batch": B, "ctx_len": N,
+                   "budgets": list(budgets), "window": w, "decode_steps": T, "n_q_heads": Hq,
+                   "n_kv_heads": Hkv, "head_dim": d},
+        "decode_tokens_per_s": B * T * len(budgets) / (dec_ms_tot * 1e-3),
+        "compress_ms_per_layer": {k: v["compress_ms_per_layer"] for k, v in per_budget.items()},
+        "per_budget": per_budget,
+        "roofline": {"kernel": "k_decode (momentkv_decode_attn, one launch per token over the "
+                               "36-layer stack)",
+                     "bound": "hbm", "achieved": avg_bytes / avg_launch_s / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": avg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS,
+                     "traffic": None, "bytes_per_launch": avg_bytes,
+                     "avg_launch_us": avg_launch_s * 1e6},
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(wl, data[0], 512 if 512 in budgets else budgets[0],
+                                           args.cpu_heads, args.cpu_steps)
+    print(json.dumps(res))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

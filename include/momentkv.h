@@ -174,8 +174,11 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R
- * workspace >= momentkv_decode_workspace_size(p) bytes.  Its first int32 is a sticky
- *           overflow flag: set to 1 when an append found a full cache. */
+ * workspace >= momentkv_decode_workspace_size(p) bytes, 256-aligned.  Its first
+ *           (1 + B*Hkv) int32 must be zero before the first call that uses it: int32 0 is
+ *           a sticky overflow flag (set to 1 when an append found a full cache), the next
+ *           B*Hkv are per-head arrival counters that every call returns to zero.  Calls
+ *           that share a workspace must be stream-ordered. */
 mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
                                 void* v_cache, int32_t* lens, const void* k_new,
                                 const void* v_new, const int32_t* n_e, const float* s_k,

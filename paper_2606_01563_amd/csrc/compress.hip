@@ -37,14 +37,6 @@ __device__ __forceinline__ void store_frag(float* p, const f32x8& f) {
   reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
   reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
 }
-__device__ __forceinline__ bf16_t raw_elem(const bf16x8& f, int e) {
-  return __builtin_bit_cast(bf16_t, f[e]);
-}
-__device__ __forceinline__ float raw_elem(const f32x8& f, int e) { return f[e]; }
-__device__ __forceinline__ float elem_f(const bf16x8& f, int e) {
-  return bf2f(__builtin_bit_cast(bf16_t, f[e]));
-}
-__device__ __forceinline__ float elem_f(const f32x8& f, int e) { return f[e]; }
 
 __device__ __forceinline__ void load4(const bf16_t* p, float (&o)[4]) {
   uint2 u = *reinterpret_cast<const uint2*>(p);

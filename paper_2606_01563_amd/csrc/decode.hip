@@ -1,23 +1,25 @@
 // Corrected decode attention over the retained cache (Algorithm 1 Phase 2; Eqs. fhat,
 // jensen and fused; log-domain mixing weight of App. C.2), split-K over the cache.
 //
-// k_decode_partial  grid (nsplit, B*Hkv), 256 threads.  Each workgroup streams one slice
-//                   of one KV head's retained rows for all G query heads of the group:
-//                   Q.K^T on MFMA (the G queries padded to 16 rows), online softmax in the
-//                   base-2 domain, P.V on the vector ALU over coalesced rows.  It also
-//                   computes its share of the rows of S_tilde q (clamped covariance times
-//                   each query), so the d x d summary is read once per head in total.
-//                   The new token (if any) is appended by the workgroup owning its row.
-// k_decode_merge    one wave per (b, query head): merges the slices in a fixed order
-//                   (f_R, log Z_R), then mixes in the first-order estimate f_E_hat with the
-//                   Jensen weight and writes the output; bumps lens after an append.
+// One kernel, grid (nsplit, B*Hkv), 256 threads.  Each workgroup streams one slice of one
+// KV head's retained rows for all G query heads of the group: Q.K^T on MFMA (the G
+// queries padded to 16 rows), online softmax in the base-2 domain, P.V on the vector ALU
+// over coalesced rows.  It also computes its share of the rows of S_tilde q (clamped
+// covariance times each query), so the d x d summary is read once per head in total.
+// The new token (if any) is appended by the workgroup owning its row.  The last
+// workgroup of a head to finish (a per-head arrival counter in the workspace) merges the
+// slices in a fixed order (f_R, log Z_R), mixes in the first-order estimate f_E_hat with
+// the Jensen weight, writes the outputs, bumps lens and resets the counter.
 #include "mkv_device.h"
 #include "mkv_launch.h"
 
 namespace mkv {
 
+template <class T, int D>
+__device__ void decode_merge_query(const DecodeArgs& a, int bh, int g, int lane);
+
 template <class T, int D, int GMAX>
-__global__ void __launch_bounds__(256) k_decode_partial(DecodeArgs a) {
+__global__ void __launch_bounds__(256) k_decode(DecodeArgs a) {
   constexpr int KS = D / 32;        // MFMA contraction steps per row
   constexpr int LPR = D / 8;        // lanes per row in the coalesced V layout
   constexpr int TPL = 64 / LPR;     // rows per wave-wide V load
@@ -136,7 +138,7 @@ __global__ void __launch_bounds__(256) k_decode_partial(DecodeArgs a) {
         const T* row = (j == old_len && can_append) ? v_new : vc + (size_t)j * D;
         typename Frag<T>::type vf = load_frag(row + 8 * (lane % LPR));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = (float)vf[e];
+        for (int e = 0; e < 8; ++e) v[e] = elem_f(vf, e);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = 0.f;
@@ -233,18 +235,29 @@ __global__ void __launch_bounds__(256) k_decode_partial(DecodeArgs a) {
       }
     }
   }
+
+  // ---- arrival: the last workgroup of this head merges (release by every thread,
+  // then one counter increment; acquire before reading the other slices)
+  __shared__ int s_last;
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(a.counter + head, 1) == a.nsplit - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  for (int g = wave; g < G; g += 4) decode_merge_query<T, D>(a, head, g, lane);
+  if (threadIdx.x == 0) {
+    a.counter[head] = 0;
+    if (can_append) a.lens[head] = old_len + 1;
+  }
 }
 
+// Merge of one query head's slices and the moment correction (one wave).
 template <class T, int D>
-__global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
+__device__ void decode_merge_query(const DecodeArgs& a, int bh, int g, int lane) {
   constexpr int CPL = D / 64;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
   const int G = a.G;
-  const int pair = blockIdx.x * 4 + wave;  // (b, hq) flattened
-  if (pair >= a.n_pairs) return;
-  const int bh = pair / G;                 // b * Hkv + h
-  const int g = pair % G;
+  const int pair = bh * G + g;             // (b, hq) flattened
   const T* q = reinterpret_cast<const T*>(a.q) + (size_t)pair * D;
   T* out = reinterpret_cast<T*>(a.out);
 
@@ -296,16 +309,12 @@ __global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
   if (lane == 0) {
     if (a.lse_out) a.lse_out[pair] = log_zr;
     if (a.w_r_out) a.w_r_out[pair] = w_r;
-    if (g == 0 && a.k_new != nullptr && a.lens[bh] < a.cap) a.lens[bh] += 1;
   }
 }
 
 template <class T, int D, int GMAX>
 static hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((k_decode_partial<T, D, GMAX>), dim3(a.nsplit, a.n_heads), dim3(256), 0, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_decode_merge<T, D>), dim3((a.n_pairs + 3) / 4), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((k_decode<T, D, GMAX>), dim3(a.nsplit, a.n_heads), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -13,6 +13,7 @@
 namespace mkv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef uint16_t bf16_t;  // storage type of bf16 tensors
@@ -67,6 +68,17 @@ template <> __device__ __forceinline__ f32x8 zero_frag<float>() {
   for (int e = 0; e < 8; ++e) r[e] = 0.f;
   return r;
 }
+
+// Element access.  Elements of a bf16 fragment are read through a bit cast of the whole
+// vector to 16-bit integers: a bit cast of a single __bf16 vector element does not select
+// the element on this toolchain.
+__device__ __forceinline__ bf16_t raw_elem(const bf16x8& f, int e) {
+  const u16x8 u = __builtin_bit_cast(u16x8, f);
+  return u[e];
+}
+__device__ __forceinline__ float raw_elem(const f32x8& f, int e) { return f[e]; }
+__device__ __forceinline__ float elem_f(const bf16x8& f, int e) { return bf2f(raw_elem(f, e)); }
+__device__ __forceinline__ float elem_f(const f32x8& f, int e) { return f[e]; }
 
 // C(16x16) += A(16x32) * B(32x16).  Lane l supplies A[l%16][8*(l/16) + e] and
 // B[8*(l/16) + e][l%16], e = 0..7, and holds C[4*(l/16) + i][l%16], i = 0..3.

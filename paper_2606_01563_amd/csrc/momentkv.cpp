@@ -164,7 +164,10 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   const size_t H = a.n_heads, D = p->head_dim, G = a.G;
   Carver c;
   c.base = static_cast<char*>(ws);
-  a.flag = c.take<int32_t>(sizeof(int32_t));
+  // flag and arrival counters share the first block: zero-filled once by the caller
+  int32_t* head_block = c.take<int32_t>((1 + H) * sizeof(int32_t));
+  a.flag = head_block;
+  a.counter = head_block ? head_block + 1 : nullptr;
   a.part_o = c.take<float>(H * a.nsplit * G * D * sizeof(float));
   a.part_ml = c.take<float>(H * a.nsplit * G * 2 * sizeof(float));
   a.sq = c.take<float>(H * G * D * sizeof(float));

@@ -208,6 +208,12 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
     return out
 
 
+def decode_workspace_zero_bytes(p: DecodeParams) -> int:
+    """Leading workspace bytes (overflow flag + per-head arrival counters) that must be
+    zero before the first call with a workspace; the library keeps them zero."""
+    return ((1 + p.batch * p.n_kv_heads) * 4 + 255) // 256 * 256
+
+
 def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6) -> DecodeParams:
     B, Hq, d = q.shape
     _, Hkv, cap, _ = k_cache.shape
@@ -225,7 +231,9 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     """Corrected decode attention (see the header).  Returns (out, lse, w_r, workspace).
 
     `max_len` bounds lens after the append (defaults to the cache capacity).  The first
-    int32 of the workspace is the append-overflow flag; a fresh workspace is zeroed.
+    int32 of the workspace is the append-overflow flag, followed by per-head arrival
+    counters; a workspace allocated here gets that leading block zeroed.  A caller-owned
+    workspace must have it zeroed once before its first use.
     """
     cap = k_cache.shape[2]
     p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
@@ -240,7 +248,7 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     fresh = workspace is None or workspace.numel() < nbytes
     ws = _workspace(nbytes, dev, workspace)
     if fresh:
-        ws[:256].zero_()
+        ws[:decode_workspace_zero_bytes(p)].zero_()
     code = lib().momentkv_decode_attn(
         ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lens), _ptr(k_new),
         _ptr(v_new), _ptr(n_e), _ptr(s_k), _ptr(s_v), _ptr(S), _ptr(out), _ptr(lse), _ptr(w_r),

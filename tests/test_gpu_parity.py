@@ -133,9 +133,11 @@ def test_compress_and_decode_are_bit_deterministic():
     wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=1, ctx_len=4000)
     a = P.run_compress(gpu, 300, cap=301)
     b = P.run_compress(gpu, 300, cap=301)
-    for f in ("k_out", "v_out", "idx", "lens", "n_e", "s_k", "s_v", "S", "abar", "score0",
-              "score", "kept0"):
+    for f in ("idx", "lens", "n_e", "s_k", "s_v", "S", "abar", "score0", "score", "kept0"):
         assert torch.equal(getattr(a, f), getattr(b, f)), f
+    # rows past lens are unwritten (the outputs were allocated uninitialised)
+    assert torch.equal(a.k_out[:, :, :300], b.k_out[:, :, :300])
+    assert torch.equal(a.v_out[:, :, :300], b.v_out[:, :, :300])
     outs = []
     for c in (a, b):
         o, _, _, _ = mk.momentkv_decode_attn(gpu["q_dec"][0], c.k_out, c.v_out, c.lens, c.n_e,
