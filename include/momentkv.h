@@ -58,7 +58,8 @@ typedef enum {
 
 typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
 
-/* Limits of this build: head_dim in {64, 128}; G = Hq/Hkv <= 16; G * window <= 512. */
+/* Limits of this build: head_dim in {64, 128}; G = Hq/Hkv <= 16; G * window <= 512;
+ * at most 262144 eviction candidates (ctx_len - window - n_sink) per head. */
 
 /* ------------------------------------------------------------------------------------
  * Prefill compression (Sec. 5.1 protocol; Sec. 4.2; App. A.1)
@@ -159,6 +160,8 @@ typedef struct {
   int32_t dtype;        /* mkv_dtype of q, caches, k_new, v_new, out                 */
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
   float tau;            /* covariance clamp threshold, >= 0                          */
+  int32_t n_split;      /* slices per KV head: 0 = automatic, 1 = one workgroup per  */
+                        /* head (no second launch), k > 1 = k slices + merge launch   */
 } mkv_decode_params;
 
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
@@ -174,11 +177,10 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R
- * workspace >= momentkv_decode_workspace_size(p) bytes, 256-aligned.  Its first
- *           (1 + B*Hkv) int32 must be zero before the first call that uses it: int32 0 is
- *           a sticky overflow flag (set to 1 when an append found a full cache), the next
- *           B*Hkv are per-head arrival counters that every call returns to zero.  Calls
- *           that share a workspace must be stream-ordered. */
+ * workspace >= momentkv_decode_workspace_size(p) bytes, 256-aligned.  Its first int32
+ *           is a sticky overflow flag (set to 1 when an append found a full cache; zero it
+ *           before first use to read it).  Calls that share a workspace must be
+ *           stream-ordered. */
 mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
                                 void* v_cache, int32_t* lens, const void* k_new,
                                 const void* v_new, const int32_t* n_e, const float* s_k,

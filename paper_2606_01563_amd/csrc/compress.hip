@@ -10,15 +10,17 @@
 //   3 k_mass          per (slice, head): logits again, softmax mass summed over the
 //                     window rows -> a_j, aligned chunk pooling -> abar_j,
 //                     provisional score abar_j ||v_j||.                    [reads K]
-//   4 k_topk          per head: radix select of the k_keep best scores, lower position
+//   4 k_topk_*        per head: radix select of the k_keep best scores, lower position
 //                     first on ties; writes the kept positions in ascending order.
 //   5 k_gather_rows   rows of the provisional kept set into a compact buffer.
 //   6 k_cov_rows      their covariance and sums, stored negated as extra partial slots.
-//   7 k_reduce        fixed-order sum of all slots = moments of the provisional evicted
-//                     set; centring, clamp at tau -> S_tilde (fp32 + bf16 hi/lo), v_bar.
-//   8 k_residual      per (slice, head): S_tilde k_j on MFMA, ||v_j - v_bar - c S_tilde k_j||,
-//                     score_j = abar_j * that norm.                        [reads K, V]
-//   9 k_topk          final kept set.
+//   7 k_reduce        fixed-order sum of all slots = raw moments of the provisional
+//                     evicted set.
+//   8 k_residual      per (slice, head): centring and clamp of the provisional summary
+//                     into LDS (fp32, or a bf16 hi/lo pair), S_tilde k_j on MFMA,
+//                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm.
+//                                                                          [reads K, V]
+//   9 k_topk_*        final kept set.
 //  10 k_gather_out    retained rows (sinks, kept, window) -> k_out/v_out, idx, lens.
 //  11 k_cov_rows      covariance of the final kept rows (from k_out), negated.
 //  12 k_reduce        final raw moments S, s_k, s_v, n_e.
@@ -72,22 +74,28 @@ __device__ __forceinline__ const T* window_row(const CompressArgs& a, int head, 
          (((size_t)b * a.Hq + (size_t)h * a.G) * a.w + r) * a.D;
 }
 
-// Covariance tile work split: D=128 -> each wave a 64x64 quadrant (4x4 MFMA tiles);
-// D=64 -> each wave 16 rows x 64 columns (1x4 tiles).
-template <int D> struct CovSplit {
-  static constexpr int QM = D == 128 ? 4 : 1;
-  static constexpr int QN = 4;
-  static __device__ __forceinline__ int a0(int wave) { return D == 128 ? 64 * (wave >> 1) : 16 * wave; }
-  static __device__ __forceinline__ int b0(int wave) { return D == 128 ? 64 * (wave & 1) : 0; }
+// Covariance work split over the NW waves of a workgroup, in 16x16 MFMA tiles of the
+// D x D output: wave w owns QM x QN tiles at rows a0(w), columns b0(w).
+//   D=128: 4 waves -> 64x64 quadrants; 8 waves -> 32x64 blocks.
+//   D=64:  4 waves -> 16x64 strips;    8 waves -> 16x32 blocks.
+template <int D, int NW> struct CovSplit {
+  static constexpr int QM = D == 128 ? (NW == 4 ? 4 : 2) : 1;
+  static constexpr int QN = D == 128 ? 4 : (NW == 4 ? 4 : 2);
+  static __device__ __forceinline__ int a0(int wave) {
+    return D == 128 ? (NW == 4 ? 64 * (wave >> 1) : 32 * (wave >> 1)) : (NW == 4 ? 16 * wave : 16 * (wave >> 1));
+  }
+  static __device__ __forceinline__ int b0(int wave) {
+    return D == 128 ? 64 * (wave & 1) : (NW == 4 ? 0 : 32 * (wave & 1));
+  }
 };
 
 // cacc += V_tile^T K_tile over the TILE tokens held transposed in LDS.
-template <class T, int D, int LD>
+template <class T, int D, int NW, int LD>
 __device__ __forceinline__ void cov_tile(const T (*sVT)[LD], const T (*sKT)[LD],
-                                         f32x4 (&cacc)[CovSplit<D>::QM][CovSplit<D>::QN],
+                                         f32x4 (&cacc)[CovSplit<D, NW>::QM][CovSplit<D, NW>::QN],
                                          int wave, int lane) {
-  constexpr int QM = CovSplit<D>::QM, QN = CovSplit<D>::QN;
-  const int a0 = CovSplit<D>::a0(wave), b0 = CovSplit<D>::b0(wave);
+  constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
+  const int a0 = CovSplit<D, NW>::a0(wave), b0 = CovSplit<D, NW>::b0(wave);
 #pragma unroll
   for (int kk = 0; kk < TILE / 32; ++kk) {
     typename Frag<T>::type af[QM];
@@ -103,15 +111,121 @@ __device__ __forceinline__ void cov_tile(const T (*sVT)[LD], const T (*sKT)[LD],
   }
 }
 
+// Register staging of one 64-token tile of K and V for NT threads.  Thread t holds tokens
+// 2p and 2p+1 (p = t % 32) in the 8-column groups g0 + (NT/32)*i (g0 = t / 32, i < NDG):
+// lanes run along tokens, so the transposed LDS copies are written as packed pairs of
+// consecutive tokens and the 32 lanes of a half-wave hit 32 different banks.  With more
+// half-waves than column groups (NT = 512, D = 64) the surplus threads hold nothing.
+template <class T, int D, int NT> struct TileRegs {
+  static constexpr int GROUPS = D / 8, HALVES = NT / 32;
+  static constexpr int NDG = GROUPS > HALVES ? GROUPS / HALVES : 1;
+  typename Frag<T>::type k[NDG][2], v[NDG][2];
+  static __device__ __forceinline__ bool active(int tid) { return (tid >> 5) < GROUPS; }
+  static __device__ __forceinline__ int group(int tid, int i) { return (tid >> 5) + HALVES * i; }
+};
+
+__device__ __forceinline__ void store_pair(bf16_t* p, bf16_t lo, bf16_t hi) {
+  *reinterpret_cast<uint32_t*>(p) = (uint32_t)lo | ((uint32_t)hi << 16);
+}
+__device__ __forceinline__ void store_pair(float* p, float lo, float hi) {
+  *reinterpret_cast<float2*>(p) = make_float2(lo, hi);
+}
+
+// Rows row0 + 2p and row0 + 2p + 1 of K and V (head base pointers); a false flag loads zeros.
+template <class T, int D, int NT>
+__device__ __forceinline__ void tile_load(TileRegs<T, D, NT>& R, const T* Kh, const T* Vh, int row0,
+                                          bool k0, bool k1, bool v0, bool v1, int tid) {
+  typedef TileRegs<T, D, NT> TR;
+  const int p = tid & 31;
+  const bool act = TR::active(tid);
+  const size_t r0 = (size_t)(row0 + 2 * p) * D, r1 = r0 + D;
+#pragma unroll
+  for (int i = 0; i < TR::NDG; ++i) {
+    const int col = 8 * TR::group(tid, i);
+    R.k[i][0] = (act && k0) ? load_frag(Kh + r0 + col) : zero_frag<T>();
+    R.k[i][1] = (act && k1) ? load_frag(Kh + r1 + col) : zero_frag<T>();
+    R.v[i][0] = (act && v0) ? load_frag(Vh + r0 + col) : zero_frag<T>();
+    R.v[i][1] = (act && v1) ? load_frag(Vh + r1 + col) : zero_frag<T>();
+  }
+}
+
+// Transposed copies K^T, V^T of the tile (K rows of non-candidates zeroed), running sums
+// of k and v over the thread's columns and the thread's share of each row's ||v||^2.
+// bf16: the two tokens' elements are paired with one byte permute per column, and the
+// sums and squares use the bf16 dot2 instruction (exact products, fp32 accumulation).
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b),
+                                         c, false);
+}
+
+template <class T, int D, int NT, int LDT>
+__device__ __forceinline__ void tile_store_t(const TileRegs<T, D, NT>& R, T (*sKT)[LDT],
+                                             T (*sVT)[LDT], bool c0, bool c1,
+                                             float (&sk)[TileRegs<T, D, NT>::NDG][8],
+                                             float (&sv)[TileRegs<T, D, NT>::NDG][8], float& ss0,
+                                             float& ss1, int tid) {
+  typedef TileRegs<T, D, NT> TR;
+  const int p = tid & 31;
+  ss0 = ss1 = 0.f;
+  if (!TR::active(tid)) return;
+  if constexpr (sizeof(T) == 2) {
+    constexpr uint32_t ONES = 0x3F803F80u;  // (1.0, 1.0) in bf16
+#pragma unroll
+    for (int i = 0; i < TR::NDG; ++i) {
+      const int row = 8 * TR::group(tid, i);
+      const u32x4 k0 = __builtin_bit_cast(u32x4, R.k[i][0]), k1 = __builtin_bit_cast(u32x4, R.k[i][1]);
+      const u32x4 v0 = __builtin_bit_cast(u32x4, R.v[i][0]), v1 = __builtin_bit_cast(u32x4, R.v[i][1]);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t a0 = c0 ? k0[w] : 0u, a1 = c1 ? k1[w] : 0u;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t sel = h ? 0x07060302u : 0x05040100u;  // (token 0, token 1) of column 2w+h
+          const uint32_t kp = __builtin_amdgcn_perm(a1, a0, sel);
+          const uint32_t vp = __builtin_amdgcn_perm(v1[w], v0[w], sel);
+          *reinterpret_cast<uint32_t*>(&sKT[row + 2 * w + h][2 * p]) = kp;
+          *reinterpret_cast<uint32_t*>(&sVT[row + 2 * w + h][2 * p]) = vp;
+          sk[i][2 * w + h] = dot2_bf16(kp, ONES, sk[i][2 * w + h]);
+          sv[i][2 * w + h] = dot2_bf16(vp, ONES, sv[i][2 * w + h]);
+        }
+        ss0 = dot2_bf16(v0[w], v0[w], ss0);
+        ss1 = dot2_bf16(v1[w], v1[w], ss1);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TR::NDG; ++i) {
+      const int row = 8 * TR::group(tid, i);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float k0 = c0 ? elem_f(R.k[i][0], e) : 0.f, k1 = c1 ? elem_f(R.k[i][1], e) : 0.f;
+        const float x0 = elem_f(R.v[i][0], e), x1 = elem_f(R.v[i][1], e);
+        store_pair(&sKT[row + e][2 * p], k0, k1);
+        store_pair(&sVT[row + e][2 * p], x0, x1);
+        ss0 += x0 * x0;
+        ss1 += x1 * x1;
+        sv[i][e] += x0 + x1;
+        sk[i][e] += k0 + k1;
+      }
+    }
+  }
+}
+
 // Write one slot of covariance and (s_v, s_k) partials; `sign` = -1 for downdates.
-template <class T, int D>
-__device__ __forceinline__ void write_cov_partials(const CompressArgs& a, int head, int slot,
-                                                   f32x4 (&cacc)[CovSplit<D>::QM][CovSplit<D>::QN],
-                                                   float (&sv)[8], float (&sk)[8], float sign,
-                                                   float (*sRed)[2][D], int tid) {
-  constexpr int QM = CovSplit<D>::QM, QN = CovSplit<D>::QN, DG = D / 8;
+template <class T, int D, int NT>
+__device__ __forceinline__ void write_cov_partials(
+    const CompressArgs& a, int head, int slot,
+    f32x4 (&cacc)[CovSplit<D, NT / 64>::QM][CovSplit<D, NT / 64>::QN],
+    float (&sv)[TileRegs<T, D, NT>::NDG][8], float (&sk)[TileRegs<T, D, NT>::NDG][8], float sign,
+    int tid) {
+  constexpr int NW = NT / 64;
+  constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
+  typedef TileRegs<T, D, NT> TR;
   const int lane = tid & 63, wave = tid >> 6;
-  const int a0 = CovSplit<D>::a0(wave), b0 = CovSplit<D>::b0(wave);
+  const int a0 = CovSplit<D, NW>::a0(wave), b0 = CovSplit<D, NW>::b0(wave);
   float* sp = a.spart + ((size_t)head * a.nslot + slot) * D * D;
 #pragma unroll
   for (int mi = 0; mi < QM; ++mi)
@@ -121,39 +235,40 @@ __device__ __forceinline__ void write_cov_partials(const CompressArgs& a, int he
       for (int i = 0; i < 4; ++i)
         sp[(size_t)(a0 + 16 * mi + 4 * (lane >> 4) + i) * D + b0 + 16 * ni + (lane & 15)] =
             sign * cacc[mi][ni][i];
+  // the 32 lanes of a half-wave share the column groups of TileRegs
+  float* svk = a.svkpart + ((size_t)head * a.nslot + slot) * 2 * D;
+  const bool act = TR::active(tid);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    sv[e] = same_group_sum<DG>(sv[e]);
-    sk[e] = same_group_sum<DG>(sk[e]);
-  }
-  if (lane < DG) {
+  for (int i = 0; i < TR::NDG; ++i)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      sRed[wave][0][8 * lane + e] = sv[e];
-      sRed[wave][1][8 * lane + e] = sk[e];
+      float x = row16_sum(sv[i][e]);
+      x += __shfl_xor(x, 16);
+      float y = row16_sum(sk[i][e]);
+      y += __shfl_xor(y, 16);
+      if ((lane & 31) == 0 && act) {
+        svk[8 * TR::group(tid, i) + e] = sign * x;
+        svk[D + 8 * TR::group(tid, i) + e] = sign * y;
+      }
     }
-  }
-  __syncthreads();
-  float* svk = a.svkpart + ((size_t)head * a.nslot + slot) * 2 * D;
-  for (int t = tid; t < 2 * D; t += 256) {
-    const int which = t / D, e = t % D;
-    svk[t] = sign * (((sRed[0][which][e] + sRed[1][which][e]) + sRed[2][which][e]) + sRed[3][which][e]);
-  }
 }
 
 // ------------------------------------------------------------------------------------
 // Stage 1: window-row statistics + candidate covariance, sums and value norms.
 // ------------------------------------------------------------------------------------
+constexpr int RC_THREADS = 512;  // k_rows_cov workgroup: 8 waves
+
 template <class T, int D, int MTW>
-__global__ void __launch_bounds__(256) k_rows_cov(CompressArgs a) {
-  constexpr int KS = D / 32, DG = D / 8, PAD = 16 / (int)sizeof(T);
+__global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
+  constexpr int NT = RC_THREADS, NW = NT / 64;
+  constexpr int KS = D / 32, PAD = 16 / (int)sizeof(T);
   constexpr int LDK = D + PAD, LDT = TILE + PAD;
-  constexpr int CPT = TILE * DG / 256;   // 8-element chunks per thread per tensor
-  constexpr int QM = CovSplit<D>::QM, QN = CovSplit<D>::QN;
+  constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
+  typedef TileRegs<T, D, NT> TR;
   __shared__ __align__(16) T sK[TILE][LDK];
   __shared__ __align__(16) T sKT[D][LDT];
   __shared__ __align__(16) T sVT[D][LDT];
-  __shared__ float sRed[4][2][D];
+  __shared__ float sVn[NW][TILE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
@@ -163,12 +278,13 @@ __global__ void __launch_bounds__(256) k_rows_cov(CompressArgs a) {
   const int RT = (a.R + 15) >> 4;
   const float c2 = a.scale * kLog2e;
 
+  // window query row tiles of this wave: mt = wave + NW*k
   typename Frag<T>::type qf[MTW][KS];
   int lim[MTW][4];     // last visible key position of each of the lane's rows (-1: padding)
   float rm[MTW][4], rl[MTW][4];
 #pragma unroll
   for (int k = 0; k < MTW; ++k) {
-    const int mt = wave + 4 * k;
+    const int mt = wave + NW * k;
     const int r = 16 * mt + (lane & 15);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
@@ -187,67 +303,89 @@ __global__ void __launch_bounds__(256) k_rows_cov(CompressArgs a) {
   for (int mi = 0; mi < QM; ++mi)
 #pragma unroll
     for (int ni = 0; ni < QN; ++ni) cacc[mi][ni] = zero4();
-  float sk[8], sv[8];
+  float sk[TR::NDG][8], sv[TR::NDG][8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) sk[e] = sv[e] = 0.f;
-  const int dg = tid % DG;
+  for (int i = 0; i < TR::NDG; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sk[i][e] = sv[i][e] = 0.f;
+  const int p2 = 2 * (tid & 31);
+  auto is_cand = [&](int j) { return j >= c_lo && j < c_hi; };
 
   const int t_beg = sl * a.tps1, t_end = min(t_beg + a.tps1, a.ntile);
+  TR R;
+  if (t_beg < t_end) {
+    const int j = t_beg * TILE + p2;
+    tile_load<T, D, NT>(R, Kh, Vh, t_beg * TILE, j < a.N, j + 1 < a.N, is_cand(j), is_cand(j + 1), tid);
+  }
   for (int t = t_beg; t < t_end; ++t) {
     const int tok0 = t * TILE;
     const bool tile_has_cand = tok0 < c_hi && tok0 + TILE > c_lo;
+    {
+      const int j = tok0 + p2;
+      if (TR::active(tid)) {
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i;
-      const int tt = c / DG;
-      const int j = tok0 + tt;
-      const bool cand = j >= c_lo && j < c_hi;
-      typename Frag<T>::type kf = zero_frag<T>(), vf = zero_frag<T>();
-      if (j < a.N) kf = load_frag(Kh + (size_t)j * D + 8 * dg);
-      if (cand) vf = load_frag(Vh + (size_t)j * D + 8 * dg);
-      store_frag(&sK[tt][8 * dg], kf);
-      float ss = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sKT[8 * dg + e][tt] = cand ? raw_elem(kf, e) : raw_elem(zero_frag<T>(), e);
-        sVT[8 * dg + e][tt] = raw_elem(vf, e);
-        const float x = elem_f(vf, e);
-        ss += x * x;
-        sv[e] += x;
-        sk[e] += cand ? elem_f(kf, e) : 0.f;
+        for (int i = 0; i < TR::NDG; ++i) {
+          store_frag(&sK[p2][8 * TR::group(tid, i)], R.k[i][0]);
+          store_frag(&sK[p2 + 1][8 * TR::group(tid, i)], R.k[i][1]);
+        }
       }
-      ss = row_group_sum<DG>(ss);
-      if (cand && (lane % DG) == 0) a.vnorm[(size_t)head * a.n_c + (j - c_lo)] = sqrtf(ss);
+      float ss0, ss1;
+      tile_store_t<T, D, NT, LDT>(R, sKT, sVT, is_cand(j), is_cand(j + 1), sk, sv, ss0, ss1, tid);
+      ss0 += __shfl_xor(ss0, 32);
+      ss1 += __shfl_xor(ss1, 32);
+      if (lane < 32) {
+        sVn[wave][p2] = ss0;
+        sVn[wave][p2 + 1] = ss1;
+      }
+      if (t + 1 < t_end) {  // prefetch the next tile while this one is consumed
+        const int jn = j + TILE;
+        tile_load<T, D, NT>(R, Kh, Vh, tok0 + TILE, jn < a.N, jn + 1 < a.N, is_cand(jn), is_cand(jn + 1), tid);
+      }
     }
     __syncthreads();
+    if (tid < TILE && is_cand(tok0 + tid)) {
+      float ss = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) ss += sVn[w][tid];
+      a.vnorm[(size_t)head * a.n_c + (tok0 + tid - c_lo)] = sqrtf(ss);
+    }
 
-    // window logits for this wave's row tiles; per-lane online (max, sum)
+    // window logits for this wave's row tiles; per-lane online (max, sum), updated once
+    // per row and tile.  Only tiles reaching past position N-w need the causal/tail mask.
+    const bool need_mask = tok0 + TILE - 1 > a.N - a.w;
 #pragma unroll
     for (int k = 0; k < MTW; ++k) {
-      const int mt = wave + 4 * k;
+      const int mt = wave + NW * k;
       if (mt >= RT) continue;
+      f32x4 acc[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
-        f32x4 acc = zero4();
+        acc[nt] = zero4();
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          mma(acc, qf[k][ks], load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]));
-        const int j = tok0 + 16 * nt + (lane & 15);
+          mma(acc[nt], qf[k][ks], load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]));
+      }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (j <= lim[k][i] && j < a.N) {
-            const float s2 = acc[i] * c2;
-            if (s2 > rm[k][i]) {
-              rl[k][i] = rl[k][i] * fast_exp2(rm[k][i] - s2) + 1.f;
-              rm[k][i] = s2;
-            } else {
-              rl[k][i] += fast_exp2(s2 - rm[k][i]);
-            }
+      for (int i = 0; i < 4; ++i) {
+        float x[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          x[nt] = acc[nt][i] * c2;
+          if (need_mask) {
+            const int j = tok0 + 16 * nt + (lane & 15);
+            if (!(j <= lim[k][i] && j < a.N)) x[nt] = -INFINITY;
           }
+        }
+        const float mn = fmaxf(rm[k][i], fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+        if (mn != -INFINITY) {
+          rl[k][i] = rl[k][i] * fast_exp2(rm[k][i] - mn) +
+                     ((fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn)) +
+                      (fast_exp2(x[2] - mn) + fast_exp2(x[3] - mn)));
+          rm[k][i] = mn;
         }
       }
     }
-    if (tile_has_cand) cov_tile<T, D, LDT>(sVT, sKT, cacc, wave, lane);
+    if (tile_has_cand) cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
   }
 
@@ -261,7 +399,7 @@ __global__ void __launch_bounds__(256) k_rows_cov(CompressArgs a) {
       ml_merge(m, l, dpp_f<0x124>(m), dpp_f<0x124>(l));
       ml_merge(m, l, dpp_f<0x122>(m), dpp_f<0x122>(l));
       ml_merge(m, l, dpp_f<0x121>(m), dpp_f<0x121>(l));
-      const int mt = wave + 4 * k;
+      const int mt = wave + NW * k;
       const int r = 16 * mt + 4 * (lane >> 4) + i;
       if ((lane & 15) == 0 && mt < RT && r < a.R) {
         float* rp = a.rowpart + (((size_t)head * a.nsl1 + sl) * a.R + r) * 2;
@@ -269,20 +407,31 @@ __global__ void __launch_bounds__(256) k_rows_cov(CompressArgs a) {
         rp[1] = l;
       }
     }
-  write_cov_partials<T, D>(a, head, sl, cacc, sv, sk, 1.f, sRed, tid);
+  write_cov_partials<T, D, NT>(a, head, sl, cacc, sv, sk, 1.f, tid);
 }
 
 // ------------------------------------------------------------------------------------
-// Stage 2: merge row partials -> (max, 1/Z) per window row.
+// Stage 2: merge row partials -> (max, 1/Z) per window row.  Eight lanes per row, each
+// merging every eighth slice, then a fixed xor tree across the eight.
 // ------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) k_row_combine(CompressArgs a) {
-  const int head = blockIdx.x;
-  for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
-    float m = -INFINITY, l = 0.f;
-    for (int s = 0; s < a.nsl1; ++s) {
+  const int head = blockIdx.y;
+  const int r = blockIdx.x * 32 + (threadIdx.x >> 3);
+  const int sub = threadIdx.x & 7;
+  float m = -INFINITY, l = 0.f;
+  if (r < a.R) {
+#pragma unroll 4
+    for (int s = sub; s < a.nsl1; s += 8) {
       const float* rp = a.rowpart + (((size_t)head * a.nsl1 + s) * a.R + r) * 2;
       ml_merge(m, l, rp[0], rp[1]);
     }
+  }
+#pragma unroll
+  for (int x = 1; x < 8; x <<= 1) {
+    const float m2 = __shfl_xor(m, x), l2 = __shfl_xor(l, x);
+    ml_merge(m, l, m2, l2);
+  }
+  if (r < a.R && sub == 0) {
     a.rowstat[((size_t)head * a.R + r) * 2 + 0] = m;
     a.rowstat[((size_t)head * a.R + r) * 2 + 1] = 1.f / l;
   }
@@ -326,19 +475,24 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
   const int dg = tid % DG;
   __syncthreads();
 
-  const int t_beg = sl * a.tps1, t_end = min(t_beg + a.tps1, a.ntile);
-  for (int t = t_beg; t < t_end; ++t) {
-    const int tok0 = t * TILE;
-    if (!(tok0 < c_hi && tok0 + TILE > c_lo)) continue;  // uniform: no candidate here
+  // tiles of this slice that hold candidates (a contiguous range); the next tile's rows
+  // are loaded into registers while the current one is consumed
+  const int t_beg = max(sl * a.tps2, c_lo / TILE);
+  const int t_end = min(min(sl * a.tps2 + a.tps2, a.ntile), (c_hi + TILE - 1) / TILE);
+  typename Frag<T>::type pk[CPT];
+  auto load_tile = [&](int t) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i;
-      const int tt = c / DG;
-      const int j = tok0 + tt;
-      typename Frag<T>::type kf = zero_frag<T>();
-      if (j >= c_lo && j < c_hi) kf = load_frag(Kh + (size_t)j * D + 8 * dg);
-      store_frag(&sK[tt][8 * dg], kf);
+      const int j = t * TILE + (tid + 256 * i) / DG;
+      pk[i] = (j >= c_lo && j < c_hi) ? load_frag(Kh + (size_t)j * D + 8 * dg) : zero_frag<T>();
     }
+  };
+  if (t_beg < t_end) load_tile(t_beg);
+  for (int t = t_beg; t < t_end; ++t) {
+    const int tok0 = t * TILE;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) store_frag(&sK[(tid + 256 * i) / DG][8 * dg], pk[i]);
+    if (t + 1 < t_end) load_tile(t + 1);
     __syncthreads();
     float col[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -389,19 +543,42 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
-// Stage 4/9: per-head radix select of the k best scores (ties: lower position first),
+// Stage 4/9: per-head selection of the k best scores (ties: lower position first),
 // output in ascending position order.  Scores are non-negative floats, so their bit
-// patterns order like unsigned integers.
+// patterns (bit 31 clear) order like unsigned integers.
+//   k_topk_hist    grid (slices, heads): histogram of key bits 30..20 per slice.
+//   k_topk_select  one 1024-thread workgroup per head: sums the slice histograms, finds
+//                  the bin of the k-th largest key, refines bits 19..10 and 9..0 over the
+//                  keys still matching, which gives the k-th key T and how many keys equal
+//                  to T are needed; marks keys > T and keys == T in LDS bitmaps (one
+//                  ballot per wave), then compacts the kept positions in order with two
+//                  block scans (equal keys before each run; kept keys before each run).
 // ------------------------------------------------------------------------------------
 constexpr int TK_THREADS = 1024;
 constexpr int TK_WAVES = TK_THREADS / 64;
+constexpr int TK_BINS0 = 2048;
 
 __device__ __forceinline__ uint32_t score_key(float s) {
   uint32_t u = __float_as_uint(s);
   return (u & 0x80000000u) ? 0u : u;  // -0 and negatives sort as 0
 }
 
-// Exclusive block scan of one int per thread; returns the prefix, total in *total.
+__global__ void __launch_bounds__(256) k_topk_hist(const float* __restrict__ scores, int n,
+                                                     int per_slice, uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[TK_BINS0];
+  const int head = blockIdx.y, sl = blockIdx.x;
+  for (int i = threadIdx.x; i < TK_BINS0; i += 256) h[i] = 0;
+  __syncthreads();
+  const float* s = scores + (size_t)head * n;
+  const int j1 = min(n, (sl + 1) * per_slice);
+  for (int j = sl * per_slice + threadIdx.x; j < j1; j += 256)
+    atomicAdd(&h[score_key(s[j]) >> 20], 1u);
+  __syncthreads();
+  uint32_t* out = hist + ((size_t)head * gridDim.x + sl) * TK_BINS0;
+  for (int i = threadIdx.x; i < TK_BINS0; i += 256) out[i] = h[i];
+}
+
+// Exclusive block scan of one int per thread; the block total goes to *total.
 __device__ int block_excl_scan(int x, int* sW, int* total) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int inc = x;
@@ -430,101 +607,116 @@ __device__ int block_excl_scan(int x, int* sW, int* total) {
   return res;
 }
 
-__global__ void __launch_bounds__(TK_THREADS) k_topk(const float* __restrict__ scores, int n,
-                                                       int k, int32_t* __restrict__ out,
-                                                       int out_stride, int pos_offset) {
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t sh_prefix, sh_remaining;
+// Find, over bins in descending order, the bin where the running count reaches `need`;
+// thread t owns `per` consecutive bins from the top.  Returns (bin, count above it).
+__device__ __forceinline__ void find_bin(const uint32_t* hist, int nb, int need, int* sW,
+                                         uint32_t* sh_bin, uint32_t* sh_above) {
+  const int tid = threadIdx.x;
+  const int per = nb / TK_THREADS;
+  int c = 0;
+  for (int q = 0; q < per; ++q) c += (int)hist[nb - 1 - per * tid - q];
+  int tot;
+  int before = block_excl_scan(c, sW, &tot);
+  for (int q = 0; q < per; ++q) {
+    const int bin = nb - 1 - per * tid - q;
+    const int h = (int)hist[bin];
+    if (before < need && before + h >= need) {
+      *sh_bin = (uint32_t)bin;
+      *sh_above = (uint32_t)before;
+    }
+    before += h;
+  }
+  __syncthreads();
+}
+
+__global__ void __launch_bounds__(TK_THREADS) k_topk_select(const float* __restrict__ scores, int n,
+                                                              int k, const uint32_t* __restrict__ hist,
+                                                              int n_slices, int32_t* __restrict__ out,
+                                                              int out_stride, int pos_offset) {
+  extern __shared__ uint32_t bits[];          // [2][nw]: keys > T, keys == T
+  __shared__ uint32_t hst[TK_BINS0];
+  __shared__ uint32_t sh_bin, sh_above;
   __shared__ int sW[2 * TK_WAVES + 1];
   const int tid = threadIdx.x, lane = tid & 63;
   const int head = blockIdx.x;
   const float* s = scores + (size_t)head * n;
   int32_t* o = out + (size_t)head * out_stride;
   if (k <= 0) return;
+  const int nw = (n + 31) / 32;
+  uint32_t* gtw = bits;
+  uint32_t* eqw = bits + nw;
 
-  uint32_t prefix = 0, mask = 0, remaining = (uint32_t)k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int i = tid; i < 256; i += TK_THREADS) hist[i] = 0;
+  // bits 30..20 from the slice histograms (fixed order over slices)
+  for (int b = tid; b < TK_BINS0; b += TK_THREADS) {
+    uint32_t c = 0;
+    for (int sl = 0; sl < n_slices; ++sl) c += hist[((size_t)head * n_slices + sl) * TK_BINS0 + b];
+    hst[b] = c;
+  }
+  __syncthreads();
+  find_bin(hst, TK_BINS0, k, sW, &sh_bin, &sh_above);
+  uint32_t prefix = sh_bin << 20, mask = 0x7FF00000u;
+  int remaining = k - (int)sh_above;
+  __syncthreads();
+  // bits 19..10, then 9..0, over the keys that still match
+  for (int pass = 0; pass < 2; ++pass) {
+    const int shift = pass == 0 ? 10 : 0;
+    for (int i = tid; i < 1024; i += TK_THREADS) hst[i] = 0;
     __syncthreads();
-    for (int base = 0; base < n; base += TK_THREADS) {
-      const int j = base + tid;
-      uint32_t u = 0;
-      bool active = false;
-      if (j < n) {
-        u = score_key(s[j]);
-        active = (u & mask) == prefix;
-      }
-      const uint32_t d = (u >> shift) & 255u;
-      // aggregate equal digits within the wave (scores tend to share high bits)
-      unsigned long long act = __ballot(active);
-      for (int it = 0; it < 4 && act; ++it) {
-        const int leader = __ffsll((long long)act) - 1;
-        const uint32_t dl = __shfl(d, leader);
-        const unsigned long long same = __ballot(active && d == dl);
-        if (lane == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
-        if (active && d == dl) active = false;
-        act &= ~same;
-      }
-      if (active) atomicAdd(&hist[d], 1u);
+    for (int j = tid; j < n; j += TK_THREADS) {
+      const uint32_t u = score_key(s[j]);
+      if ((u & mask) == prefix) atomicAdd(&hst[(u >> shift) & 1023u], 1u);
     }
     __syncthreads();
-    if (tid == 0) {
-      uint32_t cum = 0;
-      int chosen = 0;
-      for (int bin = 255; bin >= 0; --bin) {
-        if (cum + hist[bin] >= remaining) { chosen = bin; break; }
-        cum += hist[bin];
-      }
-      sh_prefix = prefix | ((uint32_t)chosen << shift);
-      sh_remaining = remaining - cum;
-    }
-    __syncthreads();
-    prefix = sh_prefix;
-    remaining = sh_remaining;
-    mask |= 255u << shift;
+    find_bin(hst, 1024, remaining, sW, &sh_bin, &sh_above);
+    prefix |= sh_bin << shift;
+    mask |= 1023u << shift;
+    remaining -= (int)sh_above;
     __syncthreads();
   }
-  // keys > T are all kept; of the keys == T the `need` lowest positions are kept
   const uint32_t T = prefix;
-  const int need = (int)remaining;
-  constexpr int IT = 4;
-  int eq_carry = 0, out_carry = 0;
-  for (int base = 0; base < n; base += TK_THREADS * IT) {
-    uint32_t u[IT];
-    int n_eq = 0;
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int j = base + tid * IT + it;
-      u[it] = j < n ? score_key(s[j]) : 0u;
-      n_eq += (j < n && u[it] == T);
+  const int need = remaining;  // keys equal to T to keep (>= 1)
+
+  // bitmaps of keys > T and keys == T (each wave covers 64 consecutive positions)
+  for (int base = 0; base < n; base += TK_THREADS) {
+    const int j = base + tid;
+    const uint32_t u = j < n ? score_key(s[j]) : 0u;
+    const unsigned long long g = __ballot(j < n && u > T);
+    const unsigned long long e = __ballot(j < n && u == T);
+    if (lane == 0) {
+      const int w0 = j >> 5;
+      if (w0 < nw) { gtw[w0] = (uint32_t)g; eqw[w0] = (uint32_t)e; }
+      if (w0 + 1 < nw) { gtw[w0 + 1] = (uint32_t)(g >> 32); eqw[w0 + 1] = (uint32_t)(e >> 32); }
     }
-    int eq_tot;
-    int eq_before = block_excl_scan(n_eq, sW, &eq_tot) + eq_carry;
-    bool take[IT];
-    int n_take = 0;
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int j = base + tid * IT + it;
-      bool tk = false;
-      if (j < n) {
-        if (u[it] > T) tk = true;
-        else if (u[it] == T) { tk = eq_before < need; ++eq_before; }
-      }
-      take[it] = tk;
-      n_take += tk;
+  }
+  __syncthreads();
+  // ordered compaction: thread t owns words [t*W, t*W + W)
+  const int W = (nw + TK_THREADS - 1) / TK_THREADS;
+  const int w0 = tid * W, w1 = min(nw, w0 + W);
+  int n_eq = 0;
+  for (int w = w0; w < w1; ++w) n_eq += __popc(eqw[w]);
+  int tot;
+  int eq_before = block_excl_scan(n_eq, sW, &tot);
+  int n_take = 0;
+  for (int w = w0; w < w1; ++w) {
+    uint32_t e = eqw[w], keep = 0;
+    while (e && eq_before < need) {
+      const uint32_t low = e & (0u - e);
+      keep |= low;
+      e ^= low;
+      ++eq_before;
     }
-    int out_tot;
-    int pos = block_excl_scan(n_take, sW, &out_tot) + out_carry;
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      if (take[it]) {
-        if (pos < k) o[pos] = base + tid * IT + it + pos_offset;
-        ++pos;
-      }
+    eqw[w] = keep;  // each thread rewrites only its own words
+    n_take += __popc(gtw[w] | keep);
+  }
+  int pos = block_excl_scan(n_take, sW, &tot);
+  for (int w = w0; w < w1; ++w) {
+    uint32_t x = gtw[w] | eqw[w];
+    while (x) {
+      const int b = __ffs((int)x) - 1;
+      x &= x - 1;
+      if (pos < k) o[pos] = w * 32 + b + pos_offset;
+      ++pos;
     }
-    eq_carry += eq_tot;
-    out_carry += out_tot;
   }
 }
 
@@ -553,13 +745,13 @@ template <class T, int D>
 __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kbase,
                                                    const void* vbase, int head_rows,
                                                    int row_off, int nrows) {
-  constexpr int DG = D / 8, PAD = 16 / (int)sizeof(T);
+  constexpr int NT = 256, NW = 4;
+  constexpr int PAD = 16 / (int)sizeof(T);
   constexpr int LDT = TILE + PAD;
-  constexpr int CPT = TILE * DG / 256;
-  constexpr int QM = CovSplit<D>::QM, QN = CovSplit<D>::QN;
+  constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
+  typedef TileRegs<T, D, NT> TR;
   __shared__ __align__(16) T sKT[D][LDT];
   __shared__ __align__(16) T sVT[D][LDT];
-  __shared__ float sRed[4][2][D];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
   const T* Kh = reinterpret_cast<const T*>(kbase) + ((size_t)head * head_rows + row_off) * D;
@@ -569,175 +761,227 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kb
   for (int mi = 0; mi < QM; ++mi)
 #pragma unroll
     for (int ni = 0; ni < QN; ++ni) cacc[mi][ni] = zero4();
-  float sk[8], sv[8];
+  float sk[TR::NDG][8], sv[TR::NDG][8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) sk[e] = sv[e] = 0.f;
-  const int dg = tid % DG;
+  for (int i = 0; i < TR::NDG; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sk[i][e] = sv[i][e] = 0.f;
+  const int p2 = 2 * (tid & 31);
   const int ntiles = (nrows + TILE - 1) / TILE;
   const int t_beg = sl * a.tpsr, t_end = min(t_beg + a.tpsr, ntiles);
+  TR R;
+  if (t_beg < t_end) {
+    const int j = t_beg * TILE + p2;
+    tile_load<T, D, NT>(R, Kh, Vh, t_beg * TILE, j < nrows, j + 1 < nrows, j < nrows, j + 1 < nrows, tid);
+  }
   for (int t = t_beg; t < t_end; ++t) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i;
-      const int tt = c / DG;
-      const int j = t * TILE + tt;
-      typename Frag<T>::type kf = zero_frag<T>(), vf = zero_frag<T>();
-      if (j < nrows) {
-        kf = load_frag(Kh + (size_t)j * D + 8 * dg);
-        vf = load_frag(Vh + (size_t)j * D + 8 * dg);
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sKT[8 * dg + e][tt] = raw_elem(kf, e);
-        sVT[8 * dg + e][tt] = raw_elem(vf, e);
-        sv[e] += elem_f(vf, e);
-        sk[e] += elem_f(kf, e);
-      }
+    const int j = t * TILE + p2;
+    float ss0, ss1;
+    tile_store_t<T, D, NT, LDT>(R, sKT, sVT, true, true, sk, sv, ss0, ss1, tid);
+    if (t + 1 < t_end) {
+      const int jn = j + TILE;
+      tile_load<T, D, NT>(R, Kh, Vh, (t + 1) * TILE, jn < nrows, jn + 1 < nrows, jn < nrows, jn + 1 < nrows, tid);
     }
     __syncthreads();
-    cov_tile<T, D, LDT>(sVT, sKT, cacc, wave, lane);
+    cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
   }
-  write_cov_partials<T, D>(a, head, a.nsl1 + sl, cacc, sv, sk, -1.f, sRed, tid);
+  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, -1.f, tid);
 }
 
 // ------------------------------------------------------------------------------------
-// Stage 7/12: fixed-order sum of the slots.  final == 0: centre, clamp and keep the
-// provisional summary; final == 1: write the raw output moments.
+// Stage 7/12: fixed-order sum of the partial slots -> raw S, s_v, s_k of the evicted set
+// (stage 7: the provisional set, into the workspace; stage 12: the output moments).
+// Eight lanes per float4 of a head's D*D + 2D values, lane `sub` summing slots
+// sub, sub+8, ..., then a fixed xor tree across the eight lanes.
 // ------------------------------------------------------------------------------------
-template <int D, bool BF16>
-__global__ void __launch_bounds__(256) k_reduce(CompressArgs a, int final_pass) {
-  __shared__ float sTot[2][D];
-  const int tid = threadIdx.x;
+template <int D>
+__global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, float* sv_out,
+                                                 float* sk_out, int32_t* ne_out) {
+  constexpr int NSF4 = D * D / 4, NF4 = (D * D + 2 * D) / 4;
   const int head = blockIdx.y;
-  const int n = a.n_c - a.k_keep;  // evicted count
-  for (int t = tid; t < 2 * D; t += 256) {
-    float acc = 0.f;
-    for (int s = 0; s < a.nslot; ++s) acc += a.svkpart[((size_t)head * a.nslot + s) * 2 * D + t];
-    sTot[t / D][t % D] = acc;  // [0] = s_v, [1] = s_k
-  }
-  __syncthreads();
-  const int e0 = (blockIdx.x * 256 + tid) * 4;
-  if (e0 < D * D) {
-    const int row = e0 / D, col = e0 % D;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s = 0; s < a.nslot; ++s) {
-      const float4 p = *reinterpret_cast<const float4*>(a.spart + ((size_t)head * a.nslot + s) * D * D + e0);
+  const int f4 = blockIdx.x * 32 + (threadIdx.x >> 3);
+  const int sub = threadIdx.x & 7;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (f4 < NF4) {
+    const bool in_S = f4 < NSF4;
+    const float* base = in_S ? a.spart + (size_t)head * a.nslot * D * D + 4 * f4
+                             : a.svkpart + (size_t)head * a.nslot * 2 * D + 4 * (f4 - NSF4);
+    const size_t stride = in_S ? (size_t)D * D : (size_t)2 * D;
+#pragma unroll 4
+    for (int sl = sub; sl < a.nslot; sl += 8) {
+      const float4 p = *reinterpret_cast<const float4*>(base + sl * stride);
       acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
     }
-    if (final_pass) {
-      *reinterpret_cast<float4*>(a.S + (size_t)head * D * D + e0) = acc;
-    } else {
-      const float inv_n = 1.f / (float)n;
-      const float sv = sTot[0][row];
-      float st[4] = {acc.x - sv * sTot[1][col] * inv_n, acc.y - sv * sTot[1][col + 1] * inv_n,
-                     acc.z - sv * sTot[1][col + 2] * inv_n, acc.w - sv * sTot[1][col + 3] * inv_n};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) if (fabsf(st[i]) < a.tau) st[i] = 0.f;
-      *reinterpret_cast<float4*>(a.stil + (size_t)head * D * D + e0) = make_float4(st[0], st[1], st[2], st[3]);
-      if (BF16) {
-        bf16_t* hl = reinterpret_cast<bf16_t*>(a.stil_hl) + (size_t)head * 2 * D * D;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const bf16_t hi = f2bf(st[i]);
-          hl[e0 + i] = hi;
-          hl[D * D + e0 + i] = f2bf(st[i] - bf2f(hi));
-        }
-      }
-    }
   }
-  if (blockIdx.x == 0) {
-    if (final_pass) {
-      for (int t = tid; t < D; t += 256) {
-        a.s_v[(size_t)head * D + t] = sTot[0][t];
-        a.s_k[(size_t)head * D + t] = sTot[1][t];
-      }
-      if (tid == 0) a.n_e[head] = n;
-    } else {
-      for (int t = tid; t < D; t += 256) a.vbar[(size_t)head * D + t] = sTot[0][t] / (float)n;
-    }
+#pragma unroll
+  for (int x = 1; x < 8; x <<= 1) {
+    acc.x += __shfl_xor(acc.x, x);
+    acc.y += __shfl_xor(acc.y, x);
+    acc.z += __shfl_xor(acc.z, x);
+    acc.w += __shfl_xor(acc.w, x);
   }
+  if (f4 < NF4 && sub == 0) {
+    float* dst;
+    if (f4 < NSF4) {
+      dst = S_out + (size_t)head * D * D + 4 * f4;
+    } else {
+      const int e = 4 * (f4 - NSF4);  // [0, D): s_v, [D, 2D): s_k
+      dst = e < D ? sv_out + (size_t)head * D + e : sk_out + (size_t)head * D + (e - D);
+    }
+    *reinterpret_cast<float4*>(dst) = acc;
+  }
+  if (ne_out && blockIdx.x == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - a.k_keep;
 }
 
 // ------------------------------------------------------------------------------------
-// Stage 8: moment residual score of every candidate.
+// Stage 8: moment residual score of every candidate (Sec. 4.2 Eq. residual).
+// Wave w owns rows [32w, 32w+32) of S_tilde0 (D = 128; 16 rows for D = 64), built in
+// registers from the raw provisional sums (centring and clamp, App. A.1 Eq. app_S_tilde,
+// App. C.2) and kept as MFMA A fragments: fp32, or a bf16 hi/lo pair whose two products
+// add up to fp32-level accuracy.  Candidate tiles of 64 rows of K and V stream through
+// LDS (natural layout) with the next tile prefetched into registers.  Each wave forms
+// S_tilde0 k_j for its rows, the partial ||v_j - v_bar - c S_tilde0 k_j||^2 over them, and
+// the four partials are added in wave order.
 // ------------------------------------------------------------------------------------
 template <class T, int D>
 __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
-  constexpr int KS = D / 32, PAD = 16 / (int)sizeof(T);
-  constexpr int LDS_ = D + PAD;
+  constexpr int KS = D / 32, DG = D / 8, PAD = 16 / (int)sizeof(T);
+  constexpr int LDK = D + PAD;
+  constexpr int CPT = TILE * DG / 256;
   constexpr bool BF = sizeof(T) == 2;
-  constexpr int NPL = BF ? 2 : 1;  // planes: bf16 hi + lo, or fp32
-  __shared__ __align__(16) T sS[NPL][D][LDS_];
-  __shared__ float sVbar[D];
+  constexpr int NPL = BF ? 2 : 1;          // A fragment planes: bf16 hi + lo, or fp32
+  constexpr int MTPW = D / 64;             // 16-row tiles of S_tilde0 per wave
+  typedef typename Frag<T>::type FragT;
+  __shared__ __align__(16) T sK[TILE][LDK];
+  __shared__ __align__(16) T sV[TILE][LDK];
+  __shared__ float sRho[4][TILE];
+  __shared__ float sSv[D], sSk[D];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
   const int c_lo = a.n_s, c_hi = a.N - a.w;
-  const float coef = a.scale / (float)(a.n_c - a.k_keep);
+  const float n0 = (float)(a.n_c - a.k_keep);
+  const float inv_n = 1.f / n0;
+  const float coef = a.scale / n0;
   const T* Kh = reinterpret_cast<const T*>(a.k) + (size_t)head * a.N * D;
   const T* Vh = reinterpret_cast<const T*>(a.v) + (size_t)head * a.N * D;
-  {
-    const T* src = BF ? reinterpret_cast<const T*>(a.stil_hl) + (size_t)head * 2 * D * D
-                      : reinterpret_cast<const T*>(a.stil) + (size_t)head * D * D;
-    for (int c = tid; c < NPL * D * D / 8; c += 256) {
-      const int pl = c / (D * D / 8), rem = c % (D * D / 8);
-      const int row = rem / (D / 8), cg = rem % (D / 8);
-      store_frag(&sS[pl][row][8 * cg], load_frag(src + (size_t)pl * D * D + (size_t)row * D + 8 * cg));
-    }
-    for (int t = tid; t < D; t += 256) sVbar[t] = a.vbar[(size_t)head * D + t];
+
+  for (int t = tid; t < D; t += 256) {
+    sSv[t] = a.sv0[(size_t)head * D + t];
+    sSk[t] = a.sk0[(size_t)head * D + t];
   }
   __syncthreads();
-
-  for (int it = 0; it < a.tps3; ++it) {
-    const int base = c_lo + ((sl * a.tps3 + it) * 4 + wave) * TILE;
-    if (base >= c_hi) break;
-    typename Frag<T>::type kf[4][KS];
+  // A fragments: row 16*(MTPW*wave + m) + lane%16, columns 32*ks + 8*(lane/16) + e
+  FragT af[MTPW][KS][NPL];
+  const float* S0 = a.s0 + (size_t)head * D * D;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      const int j = base + 16 * nt + (lane & 15);
+  for (int m = 0; m < MTPW; ++m) {
+    const int row = 16 * (MTPW * wave + m) + (lane & 15);
+    const float sv = sSv[row];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int col = 32 * ks + 8 * (lane >> 4);
+      const f32x8 raw = load_frag(S0 + (size_t)row * D + col);
+      float st[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        st[e] = raw[e] - sv * sSk[col + e] * inv_n;
+        if (fabsf(st[e]) < a.tau) st[e] = 0.f;
+      }
+      if constexpr (BF) {
+        u16x8 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bf16_t h = f2bf(st[e]);
+          hi[e] = h;
+          lo[e] = f2bf(st[e] - bf2f(h));
+        }
+        af[m][ks][0] = __builtin_bit_cast(FragT, hi);
+        af[m][ks][NPL - 1] = __builtin_bit_cast(FragT, lo);
+      } else {
+        f32x8 f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = st[e];
+        af[m][ks][0] = __builtin_bit_cast(FragT, f);
+      }
+    }
+  }
+  // v_bar0 for this lane's result rows: 16*(MTPW*wave + m) + 4*(lane/16) + i
+  float vb[MTPW][4];
+#pragma unroll
+  for (int m = 0; m < MTPW; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) vb[m][i] = sSv[16 * (MTPW * wave + m) + 4 * (lane >> 4) + i] * inv_n;
+
+  const int n_tiles = (a.n_c + TILE - 1) / TILE;
+  const int t_beg = sl * a.tps3, t_end = min(t_beg + a.tps3, n_tiles);
+  const int dg = tid % DG;
+  FragT pk[CPT], pv[CPT];
+  auto load_tile = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int j = c_lo + t * TILE + (tid + 256 * i) / DG;
+      const bool ok = j < c_hi;
+      pk[i] = ok ? load_frag(Kh + (size_t)j * D + 8 * dg) : zero_frag<T>();
+      pv[i] = ok ? load_frag(Vh + (size_t)j * D + 8 * dg) : zero_frag<T>();
+    }
+  };
+  if (t_beg < t_end) load_tile(t_beg);
+  for (int t = t_beg; t < t_end; ++t) {
+    const int tok0 = c_lo + t * TILE;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int tt = (tid + 256 * i) / DG;
+      store_frag(&sK[tt][8 * dg], pk[i]);
+      store_frag(&sV[tt][8 * dg], pv[i]);
+    }
+    if (t + 1 < t_end) load_tile(t + 1);
+    __syncthreads();
+    FragT bfr[4][KS];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        kf[nt][ks] = j < c_hi ? load_frag(Kh + (size_t)j * D + 32 * ks + 8 * (lane >> 4)) : zero_frag<T>();
-    }
+        bfr[nt][ks] = load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
     float rho[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 1
-    for (int mt = 0; mt < D / 16; ++mt) {
+#pragma unroll
+    for (int m = 0; m < MTPW; ++m) {
       f32x4 acc[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) acc[nt] = zero4();
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int pl = 0; pl < NPL; ++pl) {
-          const typename Frag<T>::type af = load_frag(&sS[pl][16 * mt + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
+        for (int pl = 0; pl < NPL; ++pl)
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt) mma(acc[nt], af, kf[nt][ks]);
-        }
-      }
-      const int a0 = 16 * mt + 4 * (lane >> 4);
+          for (int nt = 0; nt < 4; ++nt) mma(acc[nt], af[m][ks][pl], bfr[nt][ks]);
+      const int a0 = 16 * (MTPW * wave + m) + 4 * (lane >> 4);
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
-        const int j = base + 16 * nt + (lane & 15);
-        if (j < c_hi) {
-          float v[4];
-          load4(Vh + (size_t)j * D + a0, v);
+        float v[4];
+        load4(&sV[16 * nt + (lane & 15)][a0], v);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float r = v[i] - sVbar[a0 + i] - coef * acc[nt][i];
-            rho[nt] += r * r;
-          }
+        for (int i = 0; i < 4; ++i) {
+          const float r = v[i] - vb[m][i] - coef * acc[nt][i];
+          rho[nt] += r * r;
         }
       }
     }
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
       const float x = cross_row_sum(rho[nt]);
-      const int j = base + 16 * nt + (lane & 15);
-      if (lane < 16 && j < c_hi) {
+      if (lane < 16) sRho[wave][16 * nt + lane] = x;
+    }
+    __syncthreads();
+    if (tid < TILE) {
+      const int j = tok0 + tid;
+      if (j < c_hi) {
+        const float x = ((sRho[0][tid] + sRho[1][tid]) + sRho[2][tid]) + sRho[3][tid];
         const size_t o = (size_t)head * a.n_c + (j - c_lo);
         a.score[o] = a.abar[o] * sqrtf(x);
       }
     }
+    __syncthreads();
   }
 }
 
@@ -785,6 +1029,19 @@ __global__ void __launch_bounds__(256) k_zero_moments(CompressArgs a) {
     if (e_ != hipSuccess) return e_;        \
   } while (0)
 
+static hipError_t launch_topk(const CompressArgs& a, const float* scores, int32_t* out,
+                              hipStream_t st) {
+  if (a.k_keep <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_topk_hist, dim3(a.ntk, a.H), dim3(256), 0, st, scores, a.n_c, a.tk_per,
+                     a.tk_hist);
+  MKV_CHECK_LAUNCH();
+  const size_t smem = 2 * (size_t)((a.n_c + 31) / 32) * sizeof(uint32_t);
+  hipLaunchKernelGGL(k_topk_select, dim3(a.H), dim3(TK_THREADS), smem, st, scores, a.n_c,
+                     a.k_keep, (const uint32_t*)a.tk_hist, a.ntk, out, a.kmax, a.n_s);
+  MKV_CHECK_LAUNCH();
+  return hipSuccess;
+}
+
 template <class T, int D, int MTW>
 static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg_abar,
                                float* dbg_score0, float* dbg_score, int32_t* dbg_kept0) {
@@ -799,18 +1056,17 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
     MKV_CHECK_LAUNCH();
     return hipSuccess;
   }
-  hipLaunchKernelGGL((k_rows_cov<T, D, MTW>), dim3(a.nsl1, H), blk, 0, st, a);
+  hipLaunchKernelGGL((k_rows_cov<T, D, MTW>), dim3(a.nsl1, H), dim3(RC_THREADS), 0, st, a);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_row_combine, dim3(H), blk, 0, st, a);
+  hipLaunchKernelGGL(k_row_combine, dim3((a.R + 31) / 32, H), blk, 0, st, a);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL((k_mass<T, D, MTW>), dim3(a.nsl1, H), blk, 0, st, a);
+  hipLaunchKernelGGL((k_mass<T, D, 2 * MTW>), dim3(a.nsl2, H), blk, 0, st, a);
   MKV_CHECK_LAUNCH();
   const float* first_scores = a.mi_rounds < 0 ? a.abar : a.score0;
   int32_t* first_out = a.mi_rounds >= 1 ? a.kept0 : a.kept;
-  hipLaunchKernelGGL(k_topk, dim3(H), dim3(TK_THREADS), 0, st, first_scores, a.n_c, a.k_keep,
-                     first_out, a.kmax, a.n_s);
-  MKV_CHECK_LAUNCH();
-  const dim3 red_grid((D * D / 4 + 255) / 256, H);
+  hipError_t te = launch_topk(a, first_scores, first_out, st);
+  if (te != hipSuccess) return te;
+  const dim3 red_grid(((D * D + 2 * D) / 4 + 31) / 32, H);
   if (a.mi_rounds >= 1) {
     if (a.k_keep > 0) {
       hipLaunchKernelGGL((k_gather_rows<T, D>), dim3((a.k_keep * (D / 8) + 255) / 256, H), blk, 0, st, a);
@@ -819,13 +1075,12 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
                          (const void*)a.gath_v, a.kmax, 0, a.k_keep);
       MKV_CHECK_LAUNCH();
     }
-    hipLaunchKernelGGL((k_reduce<D, BF>), red_grid, blk, 0, st, a, 0);
+    hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.s0, a.sv0, a.sk0, (int32_t*)nullptr);
     MKV_CHECK_LAUNCH();
     hipLaunchKernelGGL((k_residual<T, D>), dim3(a.nsl3, H), blk, 0, st, a);
     MKV_CHECK_LAUNCH();
-    hipLaunchKernelGGL(k_topk, dim3(H), dim3(TK_THREADS), 0, st, (const float*)a.score, a.n_c,
-                       a.k_keep, a.kept, a.kmax, a.n_s);
-    MKV_CHECK_LAUNCH();
+    te = launch_topk(a, a.score, a.kept, st);
+    if (te != hipSuccess) return te;
   }
   hipLaunchKernelGGL((k_gather_out<T, D>), dim3((a.L * (D / 8) + 255) / 256, H), blk, 0, st, a, a.L, 0);
   MKV_CHECK_LAUNCH();
@@ -834,7 +1089,7 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
                        (const void*)a.v_out, a.cap, a.n_s, a.k_keep);
     MKV_CHECK_LAUNCH();
   }
-  hipLaunchKernelGGL((k_reduce<D, BF>), red_grid, blk, 0, st, a, 1);
+  hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.S, a.s_v, a.s_k, a.n_e);
   MKV_CHECK_LAUNCH();
   // diagnostics
   const size_t nc_bytes = (size_t)H * a.n_c * sizeof(float);
@@ -859,10 +1114,9 @@ template <class T, int D>
 static hipError_t run_compress_r(const CompressArgs& a, hipStream_t st, float* d0, float* d1,
                                  float* d2, int32_t* d3) {
   const int rt = (a.R + 15) / 16;         // 16-row tiles of window queries
-  const int mtw = (rt + 3) / 4;           // tiles per wave
-  if (mtw <= 2) return run_compress<T, D, 2>(a, st, d0, d1, d2, d3);
-  if (mtw <= 4) return run_compress<T, D, 4>(a, st, d0, d1, d2, d3);
-  return run_compress<T, D, 8>(a, st, d0, d1, d2, d3);
+  if (rt <= 8) return run_compress<T, D, 1>(a, st, d0, d1, d2, d3);
+  if (rt <= 16) return run_compress<T, D, 2>(a, st, d0, d1, d2, d3);
+  return run_compress<T, D, 4>(a, st, d0, d1, d2, d3);
 }
 
 hipError_t launch_compress(const CompressArgs& a, bool bf16, hipStream_t st, float* dbg_abar,

@@ -25,7 +25,6 @@ struct DecodeArgs {
   float* part_ml;           // [B*Hkv, nsplit, G, 2]  (max in log2 units, sum)
   float* sq;                // [B*Hkv, G, D]  S_tilde q (unscaled)
   int32_t* flag;            // sticky append-overflow flag
-  int32_t* counter;         // [B*Hkv] workgroup arrival counters (zero between launches)
   int n_heads;              // B * Hkv
   int n_pairs;              // B * Hq
   int Hkv, G, cap, nsplit, split_len, order;
@@ -55,11 +54,12 @@ struct CompressArgs {
   float* score;             // [H, n_c]          moment-round score
   int32_t* kept0;           // [H, kmax]         provisional kept positions (ascending)
   int32_t* kept;            // [H, kmax]         final kept positions (ascending)
+  uint32_t* tk_hist;        // [H, ntk, 2048]    top-k histograms of the key's top bits
   float* spart;             // [H, nslot, D, D]  covariance partials
   float* svkpart;           // [H, nslot, 2, D]  (s_v, s_k) partials
-  float* stil;              // [H, D, D]         clamped provisional S_tilde (fp32)
-  void* stil_hl;            // [H, 2, D, D]      bf16 hi/lo split of stil (bf16 inputs)
-  float* vbar;              // [H, D]            provisional v_bar
+  float* s0;                // [H, D, D]         raw S of the provisional evicted set
+  float* sv0;               // [H, D]            its s_v
+  float* sk0;               // [H, D]            its s_k
   void* gath_k;             // [H, kmax, D]      rows of the provisional kept set
   void* gath_v;
   int B, Hq, Hkv, G, N, L, w, n_s, chunk, mi_rounds, cap, D;
@@ -70,9 +70,11 @@ struct CompressArgs {
   int kmax;                 // row capacity of kept/gath buffers (>= k_keep, >= 1)
   int ntile;                // ceil(N / 64)
   int nsl1, tps1;           // window-row/covariance pass: slices, tiles per slice
+  int nsl2, tps2;           // window-mass pass: slices, tiles per slice
   int nslr, tpsr;           // downdate covariance pass over k_keep rows
   int nslot;                // nsl1 + nslr
-  int nsl3, tps3;           // residual pass: slices over candidate tiles of 256
+  int nsl3, tps3;           // residual pass: slices over candidate tiles of 64
+  int ntk, tk_per;          // top-k histogram slices and keys per slice
   float scale, tau;
 };
 

@@ -12,6 +12,7 @@
 namespace {
 
 constexpr size_t kAlign = 256;
+constexpr int kMaxCandidates = 1 << 18;  // top-k bitmaps live in LDS (2 x 32 KB)
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -51,6 +52,7 @@ mkv_status check_compress_params(const mkv_compress_params* p) {
   if ((p->n_q_heads / p->n_kv_heads) * p->window > 512) return MKV_ERR_UNSUPPORTED;
   if (64 % p->chunk) return MKV_ERR_UNSUPPORTED;
   if (p->mi_rounds < -1 || p->mi_rounds > 1) return MKV_ERR_UNSUPPORTED;
+  if (p->ctx_len - p->window - p->n_sink > kMaxCandidates) return MKV_ERR_UNSUPPORTED;
   if (p->budget < p->ctx_len && p->budget < p->n_sink + p->window) return MKV_ERR_BUDGET;
   const int n_out = p->budget < p->ctx_len ? p->budget : p->ctx_len;
   if (p->cap < n_out) return MKV_ERR_CAPACITY;
@@ -82,10 +84,15 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)a.D);
   a.tau = p->tau;
   a.ntile = ceil_div(a.N, 64);
-  // window-row / covariance pass: about 512 workgroups, whole 64-token tiles each
-  a.nsl1 = clampi(ceil_div(512, a.H), 1, a.ntile);
+  // window-row / covariance pass: about one workgroup per CU (it runs one per CU),
+  // whole 64-token tiles each
+  a.nsl1 = clampi(ceil_div(256, a.H), 1, a.ntile);
   a.tps1 = ceil_div(a.ntile, a.nsl1);
   a.nsl1 = ceil_div(a.ntile, a.tps1);
+  // window-mass pass: about 1024 workgroups of 256 threads
+  a.nsl2 = clampi(ceil_div(1024, a.H), 1, a.ntile);
+  a.tps2 = ceil_div(a.ntile, a.nsl2);
+  a.nsl2 = ceil_div(a.ntile, a.tps2);
   // downdate covariance over the kept rows
   if (a.k_keep > 0) {
     const int ntr = ceil_div(a.k_keep, 64);
@@ -97,13 +104,16 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
     a.tpsr = 1;
   }
   a.nslot = a.nsl1 + a.nslr;
-  // residual pass: 256 candidates per workgroup iteration
+  // residual pass: 64-candidate tiles, about 512 workgroups
   {
-    const int nu = ceil_div(a.n_c > 0 ? a.n_c : 1, 256);
-    a.nsl3 = clampi(ceil_div(1024, a.H), 1, nu);
+    const int nu = ceil_div(a.n_c > 0 ? a.n_c : 1, 64);
+    a.nsl3 = clampi(ceil_div(512, a.H), 1, nu);
     a.tps3 = ceil_div(nu, a.nsl3);
     a.nsl3 = ceil_div(nu, a.tps3);
   }
+  // top-k histogram slices: about 4096 keys each, at most 32
+  a.ntk = clampi(ceil_div(a.n_c > 0 ? a.n_c : 1, 4096), 1, 32);
+  a.tk_per = ceil_div(a.n_c > 0 ? a.n_c : 1, a.ntk);
   const size_t H = a.H, D = a.D, es = elem_size(p->dtype);
   const size_t nc = a.n_c > 0 ? a.n_c : 1;
   Carver c;
@@ -116,11 +126,12 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.score = c.take<float>(H * nc * sizeof(float));
   a.kept0 = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
   a.kept = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
+  a.tk_hist = c.take<uint32_t>(H * a.ntk * 2048 * sizeof(uint32_t));
   a.spart = c.take<float>(H * a.nslot * D * D * sizeof(float));
   a.svkpart = c.take<float>(H * a.nslot * 2 * D * sizeof(float));
-  a.stil = c.take<float>(H * D * D * sizeof(float));
-  a.stil_hl = c.take<void>(H * 2 * D * D * 2);
-  a.vbar = c.take<float>(H * D * sizeof(float));
+  a.s0 = c.take<float>(H * D * D * sizeof(float));
+  a.sv0 = c.take<float>(H * D * sizeof(float));
+  a.sk0 = c.take<float>(H * D * sizeof(float));
   a.gath_k = c.take<void>(H * a.kmax * D * es);
   a.gath_v = c.take<void>(H * a.kmax * D * es);
   *total = c.off;
@@ -139,6 +150,7 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
     return MKV_ERR_SHAPE;
   if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;
   if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
+  if (p->n_split < 0) return MKV_ERR_SHAPE;
   if (p->max_len < 1 || p->max_len > p->cap) return MKV_ERR_CAPACITY;
   return MKV_OK;
 }
@@ -154,20 +166,19 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   a.order = p->order;
   a.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)p->head_dim);
   a.tau = p->tau;
-  // about 1024 workgroups; slices of at least 64 rows, multiples of 16
-  const int target = clampi(ceil_div(1024, a.n_heads), 1, 1 << 20);
-  int sl = ceil_div(p->max_len, target);
+  // Slices per KV head: one (merge in the same launch) once the batch alone gives about
+  // one workgroup per CU; otherwise about 1024 workgroups of at least 64 rows.
+  int want = p->n_split;
+  if (want == 0) want = a.n_heads >= 240 ? 1 : clampi(ceil_div(1024, a.n_heads), 1, 1 << 20);
+  int sl = ceil_div(p->max_len, want);
   sl = ceil_div(sl, 16) * 16;
-  if (sl < 64) sl = 64;
+  if (sl < 64 && want > 1) sl = 64;
   a.split_len = sl;
   a.nsplit = ceil_div(p->max_len, sl);
   const size_t H = a.n_heads, D = p->head_dim, G = a.G;
   Carver c;
   c.base = static_cast<char*>(ws);
-  // flag and arrival counters share the first block: zero-filled once by the caller
-  int32_t* head_block = c.take<int32_t>((1 + H) * sizeof(int32_t));
-  a.flag = head_block;
-  a.counter = head_block ? head_block + 1 : nullptr;
+  a.flag = c.take<int32_t>(sizeof(int32_t));  // zero-filled once by the caller
   a.part_o = c.take<float>(H * a.nsplit * G * D * sizeof(float));
   a.part_ml = c.take<float>(H * a.nsplit * G * 2 * sizeof(float));
   a.sq = c.take<float>(H * G * D * sizeof(float));

@@ -51,7 +51,8 @@ class DecodeParams(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("cap", ctypes.c_int32), ("max_len", ctypes.c_int32),
                 ("order", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("tau", ctypes.c_float)]
+                ("scale", ctypes.c_float), ("tau", ctypes.c_float),
+                ("n_split", ctypes.c_int32)]
 
 
 _lib = None
@@ -209,15 +210,15 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
 
 
 def decode_workspace_zero_bytes(p: DecodeParams) -> int:
-    """Leading workspace bytes (overflow flag + per-head arrival counters) that must be
-    zero before the first call with a workspace; the library keeps them zero."""
-    return ((1 + p.batch * p.n_kv_heads) * 4 + 255) // 256 * 256
+    """Leading workspace bytes (the append-overflow flag) to zero before first use."""
+    return 256
 
 
-def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6) -> DecodeParams:
+def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6,
+                  n_split=0) -> DecodeParams:
     B, Hq, d = q.shape
     _, Hkv, cap, _ = k_cache.shape
-    return DecodeParams(B, Hq, Hkv, d, cap, max_len, order, _dtype_code(q), scale, tau)
+    return DecodeParams(B, Hq, Hkv, d, cap, max_len, order, _dtype_code(q), scale, tau, n_split)
 
 
 def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
@@ -225,19 +226,19 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
                          s_v: torch.Tensor, S: torch.Tensor, *, k_new: torch.Tensor | None = None,
                          v_new: torch.Tensor | None = None, max_len: int | None = None,
                          order: int = 1, scale: float = 0.0, tau: float = 1e-6,
+                         n_split: int = 0,
                          out: torch.Tensor | None = None, lse: torch.Tensor | None = None,
                          w_r: torch.Tensor | None = None,
                          workspace: torch.Tensor | None = None):
     """Corrected decode attention (see the header).  Returns (out, lse, w_r, workspace).
 
     `max_len` bounds lens after the append (defaults to the cache capacity).  The first
-    int32 of the workspace is the append-overflow flag, followed by per-head arrival
-    counters; a workspace allocated here gets that leading block zeroed.  A caller-owned
-    workspace must have it zeroed once before its first use.
+    int32 of the workspace is the sticky append-overflow flag; a workspace allocated here
+    gets it zeroed, a caller-owned one should be zeroed once before first use.
     """
     cap = k_cache.shape[2]
     p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
-                      scale=scale, tau=tau)
+                      scale=scale, tau=tau, n_split=n_split)
     dev = q.device
     if out is None:
         out = torch.empty_like(q)

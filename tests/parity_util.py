@@ -149,7 +149,7 @@ def oracle_moments(out: mk.CompressOutput, b: int, h: int) -> O.Moments:
 
 
 def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1, tau=1e-6,
-                     append=True):
+                     append=True, n_split=0):
     """Run `steps` decode calls on the GPU, each checked against the oracle fed the GPU's
     retained cache and fp32 moments.  Returns the list of max relative errors."""
     dt = inp["k"].dtype
@@ -172,7 +172,8 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
         vn = inp["v_new"][t] if append else None
         out, _, _, ws = mk.momentkv_decode_attn(
             q, comp.k_out, comp.v_out, lens, comp.n_e, comp.s_k, comp.s_v, comp.S, k_new=kn,
-            v_new=vn, max_len=cap, order=order, tau=tau, lse=lse, w_r=w_r, workspace=ws)
+            v_new=vn, max_len=cap, order=order, tau=tau, lse=lse, w_r=w_r, workspace=ws,
+            n_split=n_split)
         torch.cuda.synchronize()
         ref_out, ref_lz, ref_wr, (kc_ref, vc_ref, ln_ref) = O.decode(
             h64(q), kc_ref, vc_ref, ln_ref, moments,

@@ -44,7 +44,7 @@ def cparams(**kw):
 
 def dparams(**kw):
     base = dict(batch=36, n_q_heads=32, n_kv_heads=8, head_dim=128, cap=640, max_len=640,
-                order=1, dtype=1, scale=0.0, tau=1e-6)
+                order=1, dtype=1, scale=0.0, tau=1e-6, n_split=0)
     base.update(kw)
     return mk.DecodeParams(**base)
 
@@ -128,6 +128,7 @@ def test_budget_at_least_context_is_valid(L):
     (dict(n_q_heads=30), SHAPE),
     (dict(cap=0), SHAPE),
     (dict(order=2), SHAPE),
+    (dict(n_split=-1), SHAPE),
     (dict(head_dim=80), UNSUP),
     (dict(max_len=0), CAPACITY),
     (dict(max_len=641), CAPACITY),

@@ -57,6 +57,15 @@ def test_llama_layer_bf16_compress_and_decode():
     announce(f"decode worst rel err {max(worst):.2e}")
 
 
+@pytest.mark.parametrize("n_split", [1, 2, 5])
+def test_decode_slice_counts(n_split):
+    """The single-launch path (one workgroup per KV head) and explicit slice counts give the
+    same results as the oracle."""
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=3, ctx_len=3000, batch=2)
+    out = P.run_compress(gpu, 400, cap=403)
+    P.run_decode_steps(gpu, out, 3, n_split=n_split)
+
+
 # ---------------------------------------------------------------- edge cases
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("d", [64, 128])
