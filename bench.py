@@ -13,10 +13,16 @@ GPU and stay resident in HBM.  One timed step is one pass of the whole hot path:
                     token's key/value (budgets interleaved, so consecutive launches touch
                     different caches and the 256 MB last-level cache cannot hold them).
 
-Reported (one JSON line): decode attention+correction GB/s (algorithmic bytes / time, the
-`value`), decode tokens/s and compress ms/layer per budget, a roofline object for the
-decode kernel and the fp64 oracle timed on the host as a CPU baseline.  Every launch is
-timed with HIP events recorded on the stream the library launches on.
+The decode phase of a step (all 128 x 5 launches) is captured once as a HIP graph and
+replayed, as a serving loop would run it: the host does not pace the GPU.  The graph's
+replay is checked bit for bit against the same phase run eagerly.
+
+Reported (one JSON line): decode attention+correction GB/s (algorithmic bytes / replay
+time, the `value`), decode tokens/s, compress ms/layer per budget, per-budget decode
+times (replay of the whole phase minus replay of the phase without that budget, so the
+other budgets still keep the last-level cache cold), a roofline object for the decode call
+and the fp64 oracle timed on the host as a CPU baseline.  Events are recorded on the
+stream the library launches on.
 """
 from __future__ import annotations
 
@@ -176,8 +182,7 @@ def main() -> int:
 
     views = {L: [layer_view(stacks[L], l) for l in range(layers)] for L in budgets}
 
-    def step(timing):
-        ev = []
+    def compress_phase(timing):
         for L in budgets:
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
@@ -187,66 +192,120 @@ def main() -> int:
                 mk.momentkv_compress(x["q_win"], x["k"], x["v"], L, cap=min(L, N) + T,
                                      out=views[L][l], workspace=cws)
             e1.record()
-            timing["compress"][L].append((e0, e1))
+            if timing is not None:
+                timing["compress"][L].append((e0, e1))
+
+    def decode_call(t, L):
+        st = stacks[L]
+        mk.momentkv_decode_attn(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k,
+                                st.s_v, st.S, k_new=kn_steps[t], v_new=vn_steps[t],
+                                max_len=min(L, N) + T, out=out, workspace=dws[L])
+
+    def decode_phase(skip=None):
         for t in range(T):
             for L in budgets:
-                st = stacks[L]
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record()
-                mk.momentkv_decode_attn(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k,
-                                        st.s_v, st.S, k_new=kn_steps[t], v_new=vn_steps[t],
-                                        max_len=min(L, N) + T, out=out, workspace=dws[L])
-                e1.record()
-                timing["decode"][L].append((e0, e1, min(L, N) + t + 1))
-        return ev
+                if L != skip:
+                    decode_call(t, L)
 
     def new_timing():
-        return {"compress": {L: [] for L in budgets}, "decode": {L: [] for L in budgets}}
+        return {"compress": {L: [] for L in budgets}}
 
+    def capture(skip=None):
+        g = torch.cuda.CUDAGraph()
+        cap_stream = torch.cuda.Stream()
+        cap_stream.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap_stream):
+            compress_phase(None)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=cap_stream):
+                decode_phase(skip)
+        torch.cuda.current_stream().wait_stream(cap_stream)
+        torch.cuda.synchronize()
+        return g
+
+    def timed_replay(g):
+        d0 = torch.cuda.Event(enable_timing=True)
+        d1 = torch.cuda.Event(enable_timing=True)
+        d0.record()
+        g.replay()
+        d1.record()
+        return d0, d1
+
+    # warm-up, eagerly
     for _ in range(args.warmup):
-        step(new_timing())
+        compress_phase(None)
+        decode_phase()
     torch.cuda.synchronize()
+    # capture the decode phase (the library allocates nothing and records no memset), and
+    # the phase without each budget in turn: a budget's decode time is the difference
+    graph = capture()
+    graph_without = {L: capture(skip=L) for L in budgets}
+
     timing = new_timing()
+    dec_events = []
     s0 = torch.cuda.Event(enable_timing=True)
     s1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     s0.record()
     for i in range(args.steps):
-        step(timing)
+        compress_phase(timing)
+        dec_events.append(timed_replay(graph))
         print(f"[bench] step {i + 1}/{args.steps} enqueued", file=sys.stderr, flush=True)
     s1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = s0.elapsed_time(s1)
-    for st in stacks.values():
-        assert int(mk.lib() is not None)
     flags = [int(dws[L][:4].view(torch.int32)[0]) for L in budgets]
     if any(flags):
         print(f"[bench] append overflow flags {flags}", file=sys.stderr)
         return 3
 
+    # the replayed graph against the same phase run eagerly, bit for bit
+    compress_phase(None)
+    graph.replay()
+    torch.cuda.synchronize()
+    got = (out.clone(), [stacks[L].lens.clone() for L in budgets],
+           [stacks[L].k_out.clone() for L in budgets])
+    compress_phase(None)
+    decode_phase()
+    torch.cuda.synchronize()
+    same = torch.equal(got[0], out) and all(
+        torch.equal(a, stacks[L].lens) and torch.equal(k, stacks[L].k_out)
+        for a, k, L in zip(got[1], got[2], budgets))
+    del got
+    if not same:
+        print("[bench] graph replay differs from the eager decode phase", file=sys.stderr)
+        return 4
+    without_ms = {}
+    for L in budgets:
+        ev = []
+        for _ in range(args.steps):
+            compress_phase(None)
+            ev.append(timed_replay(graph_without[L]))
+        torch.cuda.synchronize()
+        without_ms[L] = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+
     per_budget = {}
-    dec_bytes_tot = 0.0
-    dec_ms_tot = 0.0
+    phase_bytes = 0.0
+    dec_ms = [a.elapsed_time(b) for a, b in dec_events]      # one graph replay per step
+    dec_s = sum(dec_ms) * 1e-3
     for L in budgets:
         cms = [a.elapsed_time(b) for a, b in timing["compress"][L]]
-        dms = [a.elapsed_time(b) for a, b, _ in timing["decode"][L]]
-        dby = [decode_bytes(LB * Hkv, G, d, n) for _, _, n in timing["decode"][L]]
-        dec_bytes_tot += sum(dby)
-        dec_ms_tot += sum(dms)
+        dby = sum(decode_bytes(LB * Hkv, G, d, min(L, N) + t + 1) for t in range(T))
+        phase_bytes += dby
+        budget_ms = sum(dec_ms) / len(dec_ms) - without_ms[L]
         per_budget[str(L)] = {
             "compress_ms_per_layer": sum(cms) / len(cms) / layers,
             "compress_GBps": compress_bytes(Hkv * B, N, d, min(L, N)) / (sum(cms) / len(cms) / layers * 1e-3) / 1e9,
-            "decode_us_per_launch": sum(dms) / len(dms) * 1e3,
-            "decode_GBps": sum(dby) / (sum(dms) * 1e-3) / 1e9,
-            "decode_tokens_per_s": B * len(dms) / (sum(dms) * 1e-3),
+            "decode_us_per_call": budget_ms / T * 1e3,
+            "decode_GBps": dby / (budget_ms * 1e-3) / 1e9,
+            "decode_tokens_per_s": B * T / (budget_ms * 1e-3),
         }
-    value = dec_bytes_tot / (dec_ms_tot * 1e-3) / 1e9
-    n_launch = sum(len(timing["decode"][L]) for L in budgets)
-    avg_launch_s = dec_ms_tot * 1e-3 / n_launch
-    avg_bytes = dec_bytes_tot / n_launch
+    value = phase_bytes * len(dec_ms) / dec_s / 1e9
+    n_launch = T * len(budgets)
+    avg_launch_s = dec_s / len(dec_ms) / n_launch
+    avg_bytes = phase_bytes / n_launch
     res = {
         "metric": "decode attn+correction GB/s & tokens/s; compress ms/layer @32K ctx",
         "value": value,
@@ -263,11 +322,13 @@ def main() -> int:
         "config": {"workload": wl.name, "layers": layers, "batch": B, "ctx_len": N,
                    "budgets": list(budgets), "window": w, "decode_steps": T, "n_q_heads": Hq,
                    "n_kv_heads": Hkv, "head_dim": d},
-        "decode_tokens_per_s": B * T * len(budgets) / (dec_ms_tot * 1e-3),
+        "decode_tokens_per_s": B * T * len(budgets) * len(dec_ms) / dec_s,
+        "decode_ms_per_step": sum(dec_ms) / len(dec_ms),
         "compress_ms_per_layer": {k: v["compress_ms_per_layer"] for k, v in per_budget.items()},
         "per_budget": per_budget,
-        "roofline": {"kernel": "k_decode (momentkv_decode_attn, one launch per token over the "
-                               "36-layer stack)",
+        "roofline": {"kernel": "momentkv_decode_attn call over the 36-layer stack: "
+                               "k_decode_fused (max_len <= 384) or k_decode_slice + "
+                               "k_decode_merge; time per call from the graph replays",
                      "bound": "hbm", "achieved": avg_bytes / avg_launch_s / 1e9,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": avg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS,

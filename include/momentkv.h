@@ -59,7 +59,8 @@ typedef enum {
 typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
 
 /* Limits of this build: head_dim in {64, 128}; G = Hq/Hkv <= 16; G * window <= 512;
- * at most 262144 eviction candidates (ctx_len - window - n_sink) per head. */
+ * at most 262144 eviction candidates (ctx_len - window - n_sink) per head; a decode grid
+ * of at most 2^24 waves (B * Hkv * (token slices + head_dim / 32)). */
 
 /* ------------------------------------------------------------------------------------
  * Prefill compression (Sec. 5.1 protocol; Sec. 4.2; App. A.1)
@@ -160,8 +161,11 @@ typedef struct {
   int32_t dtype;        /* mkv_dtype of q, caches, k_new, v_new, out                 */
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
   float tau;            /* covariance clamp threshold, >= 0                          */
-  int32_t n_split;      /* slices per KV head: 0 = automatic, 1 = one workgroup per  */
-                        /* head (no second launch), k > 1 = k slices + merge launch   */
+  int32_t n_split;      /* work split over each KV head's cache: 1 = one workgroup   */
+                        /* per KV head, single launch; k > 1 = k token slices of one */
+                        /* wave each (rows rounded up to a multiple of 32) followed  */
+                        /* by a merge launch; 0 = automatic (single launch up to     */
+                        /* max_len 384, else about 4096 slices in the whole grid).   */
 } mkv_decode_params;
 
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p);

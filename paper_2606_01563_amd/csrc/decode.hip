@@ -1,75 +1,344 @@
 // Corrected decode attention over the retained cache (Algorithm 1 Phase 2; Eqs. fhat,
-// jensen and fused; log-domain mixing weight of App. C.2), split-K over the cache.
+// jensen and fused; log-domain mixing weight of App. C.2).
 //
-// k_decode<.., FUSED = false>  grid (nsplit, B*Hkv), 256 threads.  Each workgroup streams
-//                 one slice of one KV head's retained rows for all G query heads of the
-//                 group: Q.K^T on MFMA (the G queries padded to 16 rows), online softmax in
-//                 the base-2 domain, P.V on the vector ALU over coalesced rows, the next
-//                 16-row block prefetched while the current one is consumed.  It also
-//                 computes its share of the rows of S_tilde q (clamped covariance times
-//                 each query) on fp32 MFMA, so the d x d summary is read once per head in
-//                 total.  The new token (if any) is appended by the workgroup owning its row.
-// k_decode_merge  one wave per (b, query head): merges the slices in a fixed order
-//                 (f_R, log Z_R), mixes in the first-order estimate f_E_hat with the Jensen
-//                 weight, writes the outputs and bumps lens after an append.
-// k_decode<.., FUSED = true>   one workgroup per KV head (nsplit = 1): the same stream,
-//                 then the merge and the correction in the epilogue, no second launch.
-// A same-launch "last workgroup merges" scheme for nsplit > 1 would need a device-scope
-// release/acquire in every workgroup, which on this multi-XCD part is a whole-L2
-// write-back and invalidate per wave; the merge is therefore a separate launch.
+// Two launch shapes, chosen by the host from the cache length bound:
+//
+// fused   k_decode_fused: one 4-wave workgroup per KV head, one launch.  Wave w computes
+//         rows [32w, 32w + 32) of S_tilde q (S_tilde = S - s_v s_k^T / n_e, clamped as it
+//         is loaded) and attends to the 32-row blocks w, w + 4, ... of the retained cache
+//         for all G query heads of the group; the four partial softmax states are merged
+//         in LDS, the new token is folded in, and the moment correction is applied.  The
+//         S rows and the first cache block are requested together, so the S_tilde q
+//         products run while the cache rows are in flight.  Used for short caches, where
+//         a decode call is latency bound.
+//
+// split   k_decode_slice + k_decode_merge: a 1-D grid of n_heads x (nsq + nsplit)
+//         single-wave workgroups, then one wave per (b, query head).
+//         * x < nsq: 32 rows of S_tilde q, written to the workspace;
+//         * x >= nsq: a token slice (split_len rows below lens) of one KV head, written as
+//           an unnormalised (o, max, sum) partial;
+//         * merge: the slices in a fixed order, then the new token, then the correction.
+//         Used for long caches: reading is bound by how much each CU keeps in flight, so
+//         the finishing time is set by the busiest CU, and thousands of short slices let
+//         the dispatcher balance a few hundred heads over 256 CUs.  Merging in the same
+//         launch (the last slice to finish merges) would need a device-scope
+//         release/acquire per workgroup, which on this multi-XCD part is a write-back and
+//         an invalidate of the whole L2 each time: dearer than the second launch.
+//
+// Common to both: Q.K^T and P.V run on MFMA over 32-token blocks (the G queries padded to
+// 16 rows) with the online softmax in the base-2 domain.  The new token (k_new, v_new) is
+// written to row lens of the cache by the wave whose range holds that row and is attended
+// to from k_new / v_new, so no cache read depends on the append.
 #include "mkv_device.h"
 #include "mkv_launch.h"
 
 namespace mkv {
 
-// Rows [r0, r1) of S_tilde q for the G queries of one KV head (unscaled), on fp32 MFMA:
-// A = 16-row tiles of S_tilde = S - s_v s_k^T / n_e, centred and clamped as they are
-// loaded; B = the queries as fp32 (query g in column g).  Wave w takes the tiles starting
-// at r0 + 16w, r0 + 16w + 64, ...; result (g, r) goes to dst[g * D + r].
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// Length of one KV head's retained set for this call.  lens is clamped so that a
+// corrupt value can never move a read or the append outside the cache.
+struct HeadLen {
+  int old_len;      // lens before the append
+  bool can_append;  // a new token is given and its row is inside the cache
+  int cache_len;    // cache rows attended to: old_len clamped to [0, cap]
+};
+__device__ __forceinline__ HeadLen head_len(const DecodeArgs& a, int old_len) {
+  HeadLen r;
+  r.old_len = old_len;
+  r.can_append = a.k_new != nullptr && old_len >= 0 && old_len < a.cap;
+  r.cache_len = min(max(old_len, 0), a.cap);
+  return r;
+}
+__device__ __forceinline__ int live_slices(const DecodeArgs& a, int cache_len) {
+  return min(a.nsplit, (cache_len + a.split_len - 1) / a.split_len);
+}
+
+// Orders the wave's own LDS writes and reads for the compiler.  A wave's LDS operations
+// are carried out in issue order, so lanes of one wave exchanging data through LDS need
+// no hardware wait beyond that.
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Query fragments of one KV head's group (A operand of Q.K^T, B operand of S_tilde q):
+// lane l holds 8 dims at 32 ks + 8 (l / 16) of query l % 16; queries past G are zero.
 template <class T, int D>
-__device__ __forceinline__ void stilde_q(const DecodeArgs& a, int head, const T* qh, int G,
-                                         int r0, int r1, int wave, int lane, float inv_n,
-                                         float* dst) {
-  constexpr int KS = D / 32;
-  const float* Sh = a.S + (size_t)head * D * D;
-  const float* skh = a.s_k + (size_t)head * D;
-  const float* svh = a.s_v + (size_t)head * D;
-  const int g = lane & 15;
-  f32x8 qb[KS];
-  float skc[KS][8];
+__device__ __forceinline__ void load_query_frags(const T* qh, int G, int lane,
+                                                 typename Frag<T>::type (&qf)[D / 32]) {
+  const int g = lane & 15, gc = min(g, G - 1);
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
+  for (int ks = 0; ks < D / 32; ++ks) {
+    const typename Frag<T>::type f = load_frag(qh + (size_t)gc * D + 32 * ks + 8 * (lane >> 4));
+    qf[ks] = g < G ? f : zero_frag<T>();
+  }
+}
+
+// The new token: the wave given the job copies k_new / v_new to cache row `row`, 16 bytes
+// per lane (loads first, then stores).
+template <class T, int D>
+__device__ __forceinline__ void append_row(const DecodeArgs& a, int head, int row, int lane) {
+  constexpr int NV = D * (int)sizeof(T) / 16;  // 16-byte pieces of a row
+  if (lane < 2 * NV) {
+    const bool is_v = lane >= NV;
+    const int piece = lane % NV;
+    const uint4* src = reinterpret_cast<const uint4*>(
+        reinterpret_cast<const T*>(is_v ? a.v_new : a.k_new) + (size_t)head * D) + piece;
+    T* cache = reinterpret_cast<T*>(is_v ? a.v_cache : a.k_cache);
+    uint4* dst = reinterpret_cast<uint4*>(cache + ((size_t)head * a.cap + row) * D) + piece;
+    *dst = *src;
+  }
+}
+
+// ---------------------------------------------------------------- S_tilde q
+// Rows [r0, r0 + 32) of S_tilde q (unscaled) for the queries held in the query fragments,
+// on fp32 MFMA: A = two 16-row tiles of S_tilde, centred and clamped as they are loaded;
+// B = the queries as fp32 (query g in column g).  load() issues every read; compute()
+// writes result (g, r) to dst[g * D + r] for g < G.
+template <class T, int D>
+struct SqRows {
+  static constexpr int KS = D / 32;
+  f32x8 raw[2][KS];
+  f32x8 skc[KS];
+  float sv[2];
+  int ne;
+
+  __device__ __forceinline__ void load(const DecodeArgs& a, int head, int r0, int lane) {
+    const float* Sh = a.S + (size_t)head * D * D;
+    const float* svh = a.s_v + (size_t)head * D;
+    ne = a.n_e[head];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int col = 32 * ks + 8 * (lane >> 4) + e;
-      qb[ks][e] = g < G ? to_f(qh[(size_t)g * D + col]) : 0.f;
-      skc[ks][e] = skh[col] * inv_n;
+    for (int u = 0; u < 2; ++u) {
+      const int row = r0 + 16 * u + (lane & 15);
+      sv[u] = svh[row];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) raw[u][ks] = load_frag(Sh + (size_t)row * D + 32 * ks + 8 * (lane >> 4));
     }
-  for (int m0 = r0 + 16 * wave; m0 < r1; m0 += 64) {
-    const int row = m0 + (lane & 15);
-    const bool ok = row < r1;
-    const float sv = ok ? svh[row] : 0.f;
-    f32x8 raw[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) skc[ks] = load_frag(a.s_k + (size_t)head * D + 32 * ks + 8 * (lane >> 4));
+  }
+
+  __device__ __forceinline__ void compute(const DecodeArgs& a, const typename Frag<T>::type (&qf)[KS],
+                                          int r0, int lane, float* dst) {
+    const int g = lane & 15;
+    const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+    f32x8 qb[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      raw[ks] = ok ? load_frag(Sh + (size_t)row * D + 32 * ks + 8 * (lane >> 4)) : zero_frag<float>();
-    f32x4 acc = zero4();
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      f32x8 af;
+      for (int e = 0; e < 8; ++e) qb[ks][e] = elem_f(qf[ks], e);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float st = raw[ks][e] - sv * skc[ks][e];
-        af[e] = fabsf(st) < a.tau ? 0.f : st;
+    for (int u = 0; u < 2; ++u) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        f32x8 af;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float st = raw[u][ks][e] - sv[u] * (skc[ks][e] * inv_n);
+          af[e] = fabsf(st) < a.tau ? 0.f : st;
+        }
+        mma(acc, af, qb[ks]);
       }
-      mma(acc, af, qb[ks]);
-    }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = m0 + 4 * (lane >> 4) + i;
-      if (g < G && r < r1) dst[(size_t)g * D + r] = acc[i];
+      for (int i = 0; i < 4; ++i)
+        if (g < a.G) dst[(size_t)g * D + r0 + 16 * u + 4 * (lane >> 4) + i] = acc[i];
     }
   }
+};
+
+// ---------------------------------------------------------------- block attention
+// One wave's online-softmax attention over 32-row blocks of one KV head's cache rows
+// below t_end, for the G queries of the group:
+//  * K rows are MFMA B fragments of Q.K^T (lane: row (lane%16) + 16h, 8 dims at
+//    8*(lane/16) + 32*ks);
+//  * V rows are loaded as token pairs (lane: rows 2p, 2p+1 with p = lane%16, 8-column
+//    groups lane/16 + 4c) and written transposed to the wave's LDS tile, each dword
+//    holding the two tokens of one column;
+//  * P goes to LDS as the A operand of P.V (bf16 for bf16 caches, fp32 otherwise) and P.V
+//    runs on MFMA: out[g][dim] in the same lane layout as the logits, so the online
+//    softmax rescale needs no shuffles.
+// The next block's rows are requested once the current ones have left the registers.
+// Lane l ends with rows g = 4 (l / 16) + i: (m_run[i], l_run[i]) in log2 units and
+// o[g][16 nt + l % 16] = oacc[nt][i].
+template <class T, int D, int GMAX>
+struct BlockAttn {
+  static constexpr int KS = D / 32;        // MFMA contraction steps per row
+  static constexpr int TB = 32;            // tokens per block
+  static constexpr int NVC = D / 32;       // V chunks (16 or 32 bytes) per lane and token
+  static constexpr int NT = D / 16;        // 16-column output tiles of P.V
+  static constexpr int PT = 16 / (int)sizeof(T);  // LDS row padding (16 bytes)
+  typedef typename Frag<T>::type FragT;
+  typedef T VtTile[D][TB + PT];
+  typedef T PTile[16][TB + PT];
+
+  const T* kc;
+  const T* vc;
+  int t_end;
+  FragT kf[2][KS], vf[2][NVC];
+  float m_run[4], l_run[4];
+  f32x4 oacc[NT];
+
+  __device__ __forceinline__ void load(int j0, int lane) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int j = j0 + 16 * hh + (lane & 15);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        kf[hh][ks] = (j < t_end) ? load_frag(kc + (size_t)j * D + 32 * ks + 8 * (lane >> 4)) : zero_frag<T>();
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int j = j0 + 2 * (lane & 15) + hh;
+#pragma unroll
+      for (int c = 0; c < NVC; ++c)
+        vf[hh][c] = (j < t_end) ? load_frag(vc + (size_t)j * D + 8 * ((lane >> 4) + 4 * c)) : zero_frag<T>();
+    }
+  }
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) oacc[nt] = zero4();
+  }
+
+  // Blocks at j_first, j_first + stride, ... below t_end; load(j_first) was issued.
+  __device__ __forceinline__ void run(const FragT (&qf)[KS], int j_first, int stride, float c2,
+                                      int G, int lane, VtTile& vt, PTile& sp) {
+    const int gbase = 4 * (lane >> 4);
+    for (int j0 = j_first; j0 < t_end; j0 += stride) {
+      // ---- logits for the two 16-token halves
+      f32x4 acc[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        acc[hh] = zero4();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) mma(acc[hh], qf[ks], kf[hh][ks]);
+      }
+      wave_lds_order();  // the previous block's reads of vt / sp come first
+      // ---- V^T into LDS (columns 2p, 2p+1 of row dim)
+      {
+        const int p2 = 2 * (lane & 15);
+#pragma unroll
+        for (int c = 0; c < NVC; ++c) {
+          const int col0 = 8 * ((lane >> 4) + 4 * c);
+          if constexpr (sizeof(T) == 2) {
+            const u32x4_t w0 = __builtin_bit_cast(u32x4_t, vf[0][c]);
+            const u32x4_t w1 = __builtin_bit_cast(u32x4_t, vf[1][c]);
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+#pragma unroll
+              for (int hh = 0; hh < 2; ++hh)
+                *reinterpret_cast<uint32_t*>(&vt[col0 + 2 * w + hh][p2]) =
+                    __builtin_amdgcn_perm(w1[w], w0[w], hh ? 0x07060302u : 0x05040100u);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              *reinterpret_cast<float2*>(&vt[col0 + e][p2]) = make_float2(elem_f(vf[0][c], e), elem_f(vf[1][c], e));
+          }
+        }
+      }
+      if (j0 + stride < t_end) load(j0 + stride, lane);
+      // ---- online softmax over the 32 tokens (rows g = gbase + i)
+      float alpha[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ja = j0 + (lane & 15), jb = ja + 16;
+        const bool gok = gbase + i < G;
+        const float xa = (ja < t_end && gok) ? acc[0][i] * c2 : -INFINITY;
+        const float xb = (jb < t_end && gok) ? acc[1][i] * c2 : -INFINITY;
+        const float bm = row16_max(fmaxf(xa, xb));
+        const float mn = fmaxf(m_run[i], bm);
+        float pa = 0.f, pb = 0.f;
+        if (mn == -INFINITY) {
+          alpha[i] = 1.f;
+        } else {
+          alpha[i] = fast_exp2(m_run[i] - mn);
+          pa = fast_exp2(xa - mn);
+          pb = fast_exp2(xb - mn);
+        }
+        l_run[i] = l_run[i] * alpha[i] + row16_sum(pa + pb);
+        m_run[i] = mn;
+        if (gbase + i < GMAX) {
+          sp[gbase + i][lane & 15] = from_f<T>(pa);
+          sp[gbase + i][16 + (lane & 15)] = from_f<T>(pb);
+        }
+      }
+      wave_lds_order();  // P and V^T are in LDS before they are read back
+      // ---- O = alpha * O + P . V on MFMA (A = P rows g, B = V^T)
+      const FragT pfr = ((lane & 15) < G) ? load_frag(&sp[lane & 15][8 * (lane >> 4)]) : zero_frag<T>();
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
+        mma(oacc[nt], pfr, load_frag(&vt[16 * nt + (lane & 15)][8 * (lane >> 4)]));
+      }
+    }
+  }
+
+  // o rows g < G to so[g * D + col] (a wave-private float buffer), max/sum to ml[g * 2].
+  __device__ __forceinline__ void store_lds(float* so, float* ml, int G, int lane) {
+    const int gbase = 4 * (lane >> 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (gbase + i < G) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) so[(gbase + i) * D + 16 * nt + (lane & 15)] = oacc[nt][i];
+        if ((lane & 15) == 0) {
+          ml[(gbase + i) * 2 + 0] = m_run[i];
+          ml[(gbase + i) * 2 + 1] = l_run[i];
+        }
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------- correction
+// CPL consecutive elements as floats (CPL = 1 or 2), one load.
+template <int CPL>
+__device__ __forceinline__ void load_cols(const float* p, float (&v)[CPL]) {
+  if constexpr (CPL == 2) {
+    const float2 t = *reinterpret_cast<const float2*>(p);
+    v[0] = t.x;
+    v[1] = t.y;
+  } else {
+    v[0] = p[0];
+  }
+}
+template <int CPL>
+__device__ __forceinline__ void load_cols(const bf16_t* p, float (&v)[CPL]) {
+  if constexpr (CPL == 2) {
+    const uint32_t t = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = __uint_as_float(t << 16);
+    v[1] = __uint_as_float(t & 0xffff0000u);
+  } else {
+    v[0] = bf2f(p[0]);
+  }
+}
+
+// Per-query inputs of the correction, lane holding columns CPL * lane ...: the query, the
+// new token's key and value (the query stands in when there is none; never used) and the
+// summary's key and value sums.
+template <int CPL>
+struct QueryCols {
+  float q[CPL], kn[CPL], vn[CPL], sk[CPL], sv[CPL];
+};
+template <class T, int D>
+__device__ __forceinline__ QueryCols<D / 64> load_query_cols(const DecodeArgs& a, int bh, int g,
+                                                             int lane) {
+  constexpr int CPL = D / 64;
+  const int col = lane * CPL;
+  const T* q = reinterpret_cast<const T*>(a.q) + ((size_t)bh * a.G + g) * D + col;
+  const bool has_new = a.k_new != nullptr;
+  QueryCols<CPL> r;
+  load_cols<CPL>(q, r.q);
+  load_cols<CPL>(has_new ? reinterpret_cast<const T*>(a.k_new) + (size_t)bh * D + col : q, r.kn);
+  load_cols<CPL>(has_new ? reinterpret_cast<const T*>(a.v_new) + (size_t)bh * D + col : q, r.vn);
+  load_cols<CPL>(a.s_k + (size_t)bh * D + col, r.sk);
+  load_cols<CPL>(a.s_v + (size_t)bh * D + col, r.sv);
+  return r;
 }
 
 // log Z_R from the merged (max in log2 units, sum) and the Jensen mixing weight w_R.
@@ -90,310 +359,46 @@ __device__ __forceinline__ Mix mix_weights(float M, float l, int ne, float q_dot
   return r;
 }
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
-// Two tokens' values of one V column packed for the transposed LDS tile.
-__device__ __forceinline__ void store_vpair(bf16_t* p, uint32_t lo_dw, uint32_t hi_dw, int h) {
-  *reinterpret_cast<uint32_t*>(p) = __builtin_amdgcn_perm(hi_dw, lo_dw, h ? 0x07060302u : 0x05040100u);
-}
-
-template <class T, int D, int GMAX, bool FUSED>
-__global__ void __launch_bounds__(256) k_decode(DecodeArgs a) {
-  constexpr int KS = D / 32;        // MFMA contraction steps per row
-  constexpr int TB = 32;            // tokens per wave iteration
-  constexpr int DG = D / 8;         // 8-column groups of a row
-  constexpr int NVC = DG / 4;       // V chunks (16 or 32 bytes) per lane and token
-  constexpr int NT = D / 16;        // 16-column output tiles of P.V
-  constexpr int PT = 16 / (int)sizeof(T);  // row padding (16 bytes)
-  static_assert(GMAX <= 16, "G <= 16");
-  typedef typename Frag<T>::type FragT;
-
-  __shared__ __align__(16) T s_vt[4][D][TB + PT];     // per-wave V^T tile
-  __shared__ __align__(16) T s_p[4][16][TB + PT];     // per-wave P (A operand of P.V)
-  __shared__ float s_o[4][GMAX][D];
-  __shared__ float s_m[4][GMAX];
-  __shared__ float s_l[4][GMAX];
-  __shared__ float s_sq[FUSED ? GMAX : 1][FUSED ? D : 1];
-
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int head = blockIdx.y;          // b * Hkv + h
-  const int split = blockIdx.x;
-  const int G = a.G;
-  const int b = head / a.Hkv, h = head % a.Hkv;
-  const size_t cache_off = (size_t)head * a.cap * D;
-  T* const k_cache = reinterpret_cast<T*>(a.k_cache);
-  T* const v_cache = reinterpret_cast<T*>(a.v_cache);
-  const T* kc = k_cache + cache_off;
-  const T* vc = v_cache + cache_off;
-  const T* qh = reinterpret_cast<const T*>(a.q) + ((size_t)b * a.Hkv * G + (size_t)h * G) * D;
-
-  const int old_len = a.lens[head];
-  const bool append = a.k_new != nullptr;
-  const bool can_append = append && old_len < a.cap;
-  if (append && !can_append && split == 0 && threadIdx.x == 0) atomicOr(a.flag, 1);
-  const int eff_len = can_append ? old_len + 1 : old_len;
-  const T* k_new = append ? reinterpret_cast<const T*>(a.k_new) + (size_t)head * D : nullptr;
-  const T* v_new = append ? reinterpret_cast<const T*>(a.v_new) + (size_t)head * D : nullptr;
-
-  // Append: the workgroup whose slice holds row old_len writes it to the cache.  Nobody
-  // reads that row from the cache in this launch (the new token is read from k_new).
-  if (can_append && min(old_len / a.split_len, a.nsplit - 1) == split) {
-    for (int e = threadIdx.x; e < D; e += blockDim.x) {
-      k_cache[cache_off + (size_t)old_len * D + e] = k_new[e];
-      v_cache[cache_off + (size_t)old_len * D + e] = v_new[e];
-    }
-  }
-
-  int t0 = split * a.split_len;
-  const int t1 = (split == a.nsplit - 1) ? eff_len : min(t0 + a.split_len, eff_len);
-  if (t0 > t1) t0 = t1;
-
-  // Query fragments (A operand): row m = query g (zero beyond G), 8 dims per lane.
-  FragT qf[KS];
-  {
-    const int g = lane & 15;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[ks] = (g < G) ? load_frag(qh + (size_t)g * D + 32 * ks + 8 * (lane >> 4)) : zero_frag<T>();
-  }
-  const float c2 = a.scale * kLog2e;
-
-  // Token blocks of TB = 32 rows; wave w takes blocks w, w+4, ...
-  //  * K rows are MFMA B fragments of Q.K^T (lane: row (lane%16) + 16h, 8 dims at
-  //    8*(lane/16) + 32*ks);
-  //  * V rows are loaded as token pairs (lane: rows 2p, 2p+1 with p = lane%16, 8-column
-  //    groups lane/16 + 4c) and written transposed to the wave's LDS tile, each dword
-  //    holding the two tokens of one column;
-  //  * P goes to LDS as the A operand of P.V (bf16 for bf16 caches, fp32 otherwise) and
-  //    P.V runs on MFMA: out[g][dim] in the same lane layout as the logits, so the online
-  //    softmax rescale needs no shuffles.
-  // The next block's rows are requested once the current ones have left the registers.
-  FragT kf[2][KS], vf[2][NVC];
-  auto load_block = [&](int j0) {
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int j = j0 + 16 * hh + (lane & 15);
-      const T* row = (j == old_len && can_append) ? k_new : kc + (size_t)j * D;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        kf[hh][ks] = (j < t1) ? load_frag(row + 32 * ks + 8 * (lane >> 4)) : zero_frag<T>();
-    }
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int j = j0 + 2 * (lane & 15) + hh;
-      const T* row = (j == old_len && can_append) ? v_new : vc + (size_t)j * D;
-#pragma unroll
-      for (int c = 0; c < NVC; ++c)
-        vf[hh][c] = (j < t1) ? load_frag(row + 8 * ((lane >> 4) + 4 * c)) : zero_frag<T>();
-    }
-  };
-  const int nblk = (t1 - t0 + TB - 1) / TB;
-  if (wave < nblk) load_block(t0 + TB * wave);
-
-  // ---- rows of S_tilde q for this slice (all rows when fused)
-  const int ne = a.n_e[head];
-  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
-  if (ne > 0 && a.order >= 1) {
-    const int rs = (D + a.nsplit - 1) / a.nsplit;
-    const int r0 = split * rs, r1 = min(D, r0 + rs);
-    float* dst = FUSED ? &s_sq[0][0] : a.sq + (size_t)head * G * D;
-    stilde_q<T, D>(a, head, qh, G, r0, r1, wave, lane, inv_n, dst);
-  }
-
-  float m_run[4], l_run[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
-  f32x4 oacc[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) oacc[nt] = zero4();
-  T (*vt)[TB + PT] = s_vt[wave];
-  T (*sp)[TB + PT] = s_p[wave];
-  const int gbase = 4 * (lane >> 4);
-
-  for (int blk = wave; blk < nblk; blk += 4) {
-    const int j0 = t0 + TB * blk;
-    // ---- logits for the two 16-token halves
-    f32x4 acc[2];
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      acc[hh] = zero4();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) mma(acc[hh], qf[ks], kf[hh][ks]);
-    }
-    // ---- V^T into the wave's LDS tile (columns 2p, 2p+1 of row dim)
-    {
-      const int p2 = 2 * (lane & 15);
-#pragma unroll
-      for (int c = 0; c < NVC; ++c) {
-        const int col0 = 8 * ((lane >> 4) + 4 * c);
-        if constexpr (sizeof(T) == 2) {
-          const u32x4_t w0 = __builtin_bit_cast(u32x4_t, vf[0][c]);
-          const u32x4_t w1 = __builtin_bit_cast(u32x4_t, vf[1][c]);
-#pragma unroll
-          for (int w = 0; w < 4; ++w)
-#pragma unroll
-            for (int hh = 0; hh < 2; ++hh)
-              store_vpair(reinterpret_cast<bf16_t*>(&vt[col0 + 2 * w + hh][p2]), w0[w], w1[w], hh);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            *reinterpret_cast<float2*>(&vt[col0 + e][p2]) = make_float2(elem_f(vf[0][c], e), elem_f(vf[1][c], e));
-        }
-      }
-    }
-    if (blk + 4 < nblk) load_block(j0 + 4 * TB);
-    // ---- online softmax over the 32 tokens (rows g = gbase + i)
-    float alpha[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ja = j0 + (lane & 15), jb = ja + 16;
-      const bool gok = gbase + i < G;
-      const float xa = (ja < t1 && gok) ? acc[0][i] * c2 : -INFINITY;
-      const float xb = (jb < t1 && gok) ? acc[1][i] * c2 : -INFINITY;
-      const float bm = row16_max(fmaxf(xa, xb));
-      const float mn = fmaxf(m_run[i], bm);
-      float pa = 0.f, pb = 0.f;
-      if (mn == -INFINITY) {
-        alpha[i] = 1.f;
-      } else {
-        alpha[i] = fast_exp2(m_run[i] - mn);
-        pa = fast_exp2(xa - mn);
-        pb = fast_exp2(xb - mn);
-      }
-      l_run[i] = l_run[i] * alpha[i] + row16_sum(pa + pb);
-      m_run[i] = mn;
-      if (gbase + i < GMAX) {
-        sp[gbase + i][lane & 15] = from_f<T>(pa);
-        sp[gbase + i][16 + (lane & 15)] = from_f<T>(pb);
-      }
-    }
-    // ---- O = alpha * O + P . V on MFMA (A = P rows g, B = V^T)
-    const FragT pfr = ((lane & 15) < G) ? load_frag(&sp[lane & 15][8 * (lane >> 4)]) : zero_frag<T>();
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
-      mma(oacc[nt], pfr, load_frag(&vt[16 * nt + (lane & 15)][8 * (lane >> 4)]));
-    }
-  }
-
-  // ---- per-wave results to LDS: lane holds out[g = gbase + i][16*nt + lane%16]
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (gbase + i < GMAX) s_o[wave][gbase + i][16 * nt + (lane & 15)] = oacc[nt][i];
-  if ((lane & 15) == 0) {
-    const int gb = 4 * (lane >> 4);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (gb + i < GMAX) { s_m[wave][gb + i] = m_run[i]; s_l[wave][gb + i] = l_run[i]; }
-  }
-  __syncthreads();
-
-  if constexpr (!FUSED) {
-    const size_t pbase = ((size_t)head * a.nsplit + split) * G;
-    for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
-      const int g = idx / D, e = idx % D;
-      float M = -INFINITY;
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][g]);
-      float acc = 0.f;
-      if (M != -INFINITY)
-        for (int w = 0; w < 4; ++w) acc += s_o[w][g][e] * fast_exp2(s_m[w][g] - M);
-      a.part_o[(pbase + g) * D + e] = acc;
-    }
-    for (int g = threadIdx.x; g < G; g += blockDim.x) {
-      float M = -INFINITY;
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][g]);
-      float l = 0.f;
-      if (M != -INFINITY)
-        for (int w = 0; w < 4; ++w) l += s_l[w][g] * fast_exp2(s_m[w][g] - M);
-      a.part_ml[(pbase + g) * 2 + 0] = M;
-      a.part_ml[(pbase + g) * 2 + 1] = l;
-    }
-  } else {
-    // a single slice: merge the waves and apply the correction here (one wave per query)
-    for (int g = wave; g < G; g += 4) {
-      float M = -INFINITY;
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][g]);
-      float l = 0.f;
-      if (M != -INFINITY)
-        for (int w = 0; w < 4; ++w) l += s_l[w][g] * fast_exp2(s_m[w][g] - M);
-      float dot = 0.f;
-      if (ne > 0) {
-        for (int e = lane; e < D; e += 64) dot += to_f(qh[(size_t)g * D + e]) * a.s_k[(size_t)head * D + e];
-        dot = wave_sum(dot);
-      }
-      const Mix mx = mix_weights(M, l, ne, dot, a.scale);
-      const size_t pair = (size_t)head * G + g;
-      if (lane == 0) {
-        if (a.lse_out) a.lse_out[pair] = mx.log_zr;
-        if (a.w_r_out) a.w_r_out[pair] = mx.w_r;
-      }
-      T* out = reinterpret_cast<T*>(a.out) + pair * D;
-      for (int e = lane; e < D; e += 64) {
-        float num = 0.f;
-        if (M != -INFINITY)
-          for (int w = 0; w < 4; ++w) num += s_o[w][g][e] * fast_exp2(s_m[w][g] - M);
-        const float f_r = l > 0.f ? num / l : 0.f;
-        float res = f_r;
-        if (ne > 0) {
-          float fe = a.s_v[(size_t)head * D + e] * inv_n;
-          if (a.order >= 1) fe += a.scale * inv_n * s_sq[g][e];
-          res = mx.w_r * f_r + (1.f - mx.w_r) * fe;
-        }
-        out[e] = from_f<T>(res);
-      }
-    }
-    if (threadIdx.x == 0 && can_append) a.lens[head] = old_len + 1;
-  }
-}
-
-// Merge of one query head's slices and the moment correction (one wave).
+// One query head (one wave): fold the new token into the merged cache state (M, l, o),
+// mix in f_E_hat = v_bar + scale / n_e * S_tilde q (sqv, used when use_sq) with the
+// Jensen weight, write out / lse / w_R.
 template <class T, int D>
-__device__ void decode_merge_query(const DecodeArgs& a, int bh, int g, int lane) {
+__device__ __forceinline__ void finish_query(const DecodeArgs& a, int bh, int g, int lane,
+                                             float M, float l, float (&o)[D / 64],
+                                             const QueryCols<D / 64>& qc, const float (&sqv)[D / 64],
+                                             bool use_sq, int ne, bool add_new) {
   constexpr int CPL = D / 64;
-  const int G = a.G;
-  const int pair = bh * G + g;             // (b, hq) flattened
-  const T* q = reinterpret_cast<const T*>(a.q) + (size_t)pair * D;
-  T* out = reinterpret_cast<T*>(a.out);
-
-  float M = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, a.part_ml[(((size_t)bh * a.nsplit + s) * G + g) * 2]);
-  float l = 0.f, o[CPL];
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) o[c] = 0.f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < a.nsplit; ++s) {
-      const size_t pb = ((size_t)bh * a.nsplit + s) * G + g;
-      const float w = fast_exp2(a.part_ml[pb * 2] - M);
-      l += a.part_ml[pb * 2 + 1] * w;
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) o[c] += a.part_o[pb * D + lane * CPL + c] * w;
-    }
-  }
-  const int ne = a.n_e[bh];
-  float dot = 0.f;
-  if (ne > 0) {
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) dot += to_f(q[lane * CPL + c]) * a.s_k[(size_t)bh * D + lane * CPL + c];
-    dot = wave_sum(dot);
-  }
-  const Mix mx = mix_weights(M, l, ne, dot, a.scale);
-  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+  float dot_k = 0.f, dot_s = 0.f;
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
-    const int e = lane * CPL + c;
+    dot_k += qc.q[c] * qc.kn[c];
+    dot_s += qc.q[c] * qc.sk[c];
+  }
+  dot_k = wave_sum(dot_k);
+  dot_s = wave_sum(dot_s);
+  if (add_new) {  // the new token, after the cache rows (logit in log2 units)
+    const float x = dot_k * a.scale * kLog2e;
+    const float mn = fmaxf(M, x);
+    const float r = fast_exp2(M - mn), w = fast_exp2(x - mn);
+    l = l * r + w;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) o[c] = o[c] * r + w * qc.vn[c];
+    M = mn;
+  }
+  const Mix mx = mix_weights(M, l, ne, dot_s, a.scale);
+  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+  const int pair = bh * a.G + g;
+  T* out = reinterpret_cast<T*>(a.out) + (size_t)pair * D + lane * CPL;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
     const float f_r = (l > 0.f) ? o[c] / l : 0.f;
     float res = f_r;
     if (ne > 0) {
-      float fe = a.s_v[(size_t)bh * D + e] * inv_n;
-      if (a.order >= 1) fe += a.scale * inv_n * a.sq[((size_t)bh * G + g) * D + e];
+      float fe = qc.sv[c] * inv_n;
+      if (use_sq) fe += a.scale * inv_n * sqv[c];
       res = mx.w_r * f_r + (1.f - mx.w_r) * fe;
     }
-    out[(size_t)pair * D + e] = from_f<T>(res);
+    out[c] = from_f<T>(res);
   }
   if (lane == 0) {
     if (a.lse_out) a.lse_out[pair] = mx.log_zr;
@@ -401,25 +406,207 @@ __device__ void decode_merge_query(const DecodeArgs& a, int bh, int g, int lane)
   }
 }
 
-// Merge kernel: one wave per (b, query head); the g == 0 wave of a KV head also bumps
-// lens after an append (every slice workgroup read lens in the previous launch).
+// ---------------------------------------------------------------- fused launch
+template <class T, int D, int GMAX>
+__global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
+  typedef BlockAttn<T, D, GMAX> BA;
+  constexpr int CPL = D / 64;
+  constexpr int KS = D / 32;
+  // per-wave V^T tile; after the wave's blocks it holds the wave's o rows as floats
+  constexpr int VT_BYTES = (int)sizeof(typename BA::VtTile);
+  static_assert(VT_BYTES >= GMAX * D * 4, "o rows fit in the V^T tile");
+  __shared__ __align__(16) unsigned char s_vt[4][VT_BYTES];
+  __shared__ __align__(16) T s_p[4][16][BA::TB + BA::PT];
+  __shared__ float s_ml[4][GMAX * 2];
+  __shared__ float s_sq[GMAX * D];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int head = blockIdx.x;
+  const int G = a.G;
+  const T* qh = reinterpret_cast<const T*>(a.q) + (size_t)head * G * D;
+  typename BA::VtTile& vt = *reinterpret_cast<typename BA::VtTile*>(s_vt[wave]);
+
+  typename BA::FragT qf[KS];
+  load_query_frags<T, D>(qh, G, lane, qf);
+  const bool sq_rows = a.nsq > 0 && 32 * wave < D;
+  SqRows<T, D> sq;
+  if (sq_rows) sq.load(a, head, 32 * wave, lane);
+  const QueryCols<CPL> qc = load_query_cols<T, D>(a, head, min(wave, G - 1), lane);
+  const int ne = a.n_e[head];
+
+  const HeadLen hl = head_len(a, a.lens[head]);
+  BA ba;
+  ba.kc = reinterpret_cast<const T*>(a.k_cache) + (size_t)head * a.cap * D;
+  ba.vc = reinterpret_cast<const T*>(a.v_cache) + (size_t)head * a.cap * D;
+  ba.t_end = hl.cache_len;
+  ba.init();
+  ba.load(BA::TB * wave, lane);
+  if (wave == 0 && lane == 0 && a.k_new != nullptr && !hl.can_append) atomicOr(a.flag, 1);
+  if (wave == 3 && hl.can_append) append_row<T, D>(a, head, hl.old_len, lane);
+  if (sq_rows) sq.compute(a, qf, 32 * wave, lane, s_sq);
+  ba.run(qf, BA::TB * wave, 4 * BA::TB, a.scale * kLog2e, G, lane, vt, s_p[wave]);
+  wave_lds_order();  // the last block's reads of the V^T tile come before it is reused
+  ba.store_lds(reinterpret_cast<float*>(s_vt[wave]), s_ml[wave], G, lane);
+  __syncthreads();
+
+  // one wave per query: merge the four waves' states, then the new token and correction
+  for (int g = wave; g < G; g += 4) {
+    const QueryCols<CPL> qg = g == wave ? qc : load_query_cols<T, D>(a, head, g, lane);
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][2 * g]);
+    float l = 0.f, o[CPL], sqv[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      o[c] = 0.f;
+      sqv[c] = s_sq[g * D + lane * CPL + c];
+    }
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float wt = fast_exp2(s_ml[w][2 * g] - M);
+        l += s_ml[w][2 * g + 1] * wt;
+        const float* so = reinterpret_cast<const float*>(s_vt[w]) + g * D + lane * CPL;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) o[c] += so[c] * wt;
+      }
+    }
+    finish_query<T, D>(a, head, g, lane, M, l, o, qg, sqv, a.nsq > 0, ne, hl.can_append);
+  }
+  if (threadIdx.x == 0 && hl.can_append) a.lens[head] = hl.old_len + 1;
+}
+
+// ---------------------------------------------------------------- split launch
+template <class T, int D, int GMAX>
+__global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
+  typedef BlockAttn<T, D, GMAX> BA;
+  constexpr int KS = D / 32;
+  constexpr int VT_BYTES = (int)sizeof(typename BA::VtTile);
+  static_assert(VT_BYTES >= GMAX * D * 4, "o rows fit in the V^T tile");
+  __shared__ __align__(16) unsigned char s_vt[VT_BYTES];
+  __shared__ __align__(16) T s_p[16][BA::TB + BA::PT];
+  __shared__ float s_ml[GMAX * 2];
+
+  const int lane = threadIdx.x;
+  const int per_head = a.nsq + a.nsplit;
+  const int head = blockIdx.x / per_head;         // b * Hkv + h
+  const int part = blockIdx.x % per_head;
+  const int G = a.G;
+  const T* qh = reinterpret_cast<const T*>(a.q) + (size_t)head * G * D;
+  typename BA::FragT qf[KS];
+  load_query_frags<T, D>(qh, G, lane, qf);
+  if (part < a.nsq) {
+    SqRows<T, D> sq;
+    sq.load(a, head, 32 * part, lane);
+    sq.compute(a, qf, 32 * part, lane, a.sq + (size_t)head * G * D);
+    return;
+  }
+  const int split = part - a.nsq;
+  const HeadLen hl = head_len(a, a.lens[head]);
+  const int t0 = split * a.split_len;
+  BA ba;
+  ba.kc = reinterpret_cast<const T*>(a.k_cache) + (size_t)head * a.cap * D;
+  ba.vc = reinterpret_cast<const T*>(a.v_cache) + (size_t)head * a.cap * D;
+  ba.t_end = max(t0, min(t0 + a.split_len, hl.cache_len));
+  ba.init();
+  ba.load(t0, lane);  // nothing for an empty slice
+  if (a.k_new != nullptr && !hl.can_append && split == 0 && lane == 0) atomicOr(a.flag, 1);
+  // the slice whose range holds row old_len (the last slice for rows past the split)
+  if (hl.can_append && min(hl.old_len / a.split_len, a.nsplit - 1) == split)
+    append_row<T, D>(a, head, hl.old_len, lane);
+  if (t0 >= ba.t_end) return;  // empty slice: the merge skips it
+  typename BA::VtTile& vt = *reinterpret_cast<typename BA::VtTile*>(s_vt);
+  ba.run(qf, t0, BA::TB, a.scale * kLog2e, G, lane, vt, s_p);
+
+  // partials through LDS so that they leave in 16-byte stores
+  wave_lds_order();
+  float* so = reinterpret_cast<float*>(s_vt);
+  ba.store_lds(so, s_ml, G, lane);
+  wave_lds_order();
+  const size_t pbase = ((size_t)head * a.nsplit + split) * G;
+  float4* po = reinterpret_cast<float4*>(a.part_o + pbase * D);
+  for (int c = lane; c < G * D / 4; c += kWave) po[c] = reinterpret_cast<const float4*>(so)[c];
+  if (lane < 2 * G) a.part_ml[pbase * 2 + lane] = s_ml[lane];
+}
+
+// Merge of one query head's slices, the new token and the moment correction (one wave;
+// lane holds columns CPL * lane ...).  Every load is issued before the first reduction:
+// slice indices are clamped to the slice count and slices past the retained length are
+// loaded with the rest but never combined (their workspace rows hold stale data).
+template <class T, int D>
+__device__ __forceinline__ void decode_merge_query(const DecodeArgs& a, int bh, int g, int lane) {
+  constexpr int CPL = D / 64;       // columns per lane
+  constexpr int SUB = 16;           // slices whose o rows are in flight together
+  const int G = a.G;
+  const int col = lane * CPL;
+  const size_t sbase = (size_t)bh * a.nsplit;
+  const int last = a.nsplit - 1;
+  auto o_row = [&](int s) { return a.part_o + ((sbase + min(s, last)) * G + g) * D + col; };
+
+  float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((sbase + min(lane, last)) * G + g) * 2);
+  float ov[SUB][CPL];
+#pragma unroll
+  for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(u), ov[u]);
+  const int old_len = a.lens[bh];
+  const int ne = a.n_e[bh];
+  float sqv[CPL];
+  load_cols<CPL>(a.sq + ((size_t)bh * G + g) * D + col, sqv);  // meaningful when nsq > 0
+  const QueryCols<CPL> qc = load_query_cols<T, D>(a, bh, g, lane);
+
+  const HeadLen hl = head_len(a, old_len);
+  const int n_live = live_slices(a, hl.cache_len);
+  float M = -INFINITY, l = 0.f, o[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+  for (int c0 = 0; c0 < n_live; c0 += kWave) {
+    if (c0 > 0) ml = *reinterpret_cast<const float2*>(a.part_ml + ((sbase + min(c0 + lane, last)) * G + g) * 2);
+    const bool live = c0 + lane < n_live;
+    const float mn = fmaxf(M, wave_max(live ? ml.x : -INFINITY));
+    if (mn == -INFINITY) continue;  // nothing attended to so far
+    const float r = fast_exp2(M - mn);
+    const float w = live ? fast_exp2(ml.x - mn) : 0.f;
+    l = l * r + wave_sum(live ? ml.y * w : 0.f);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) o[c] *= r;
+    M = mn;
+    const int cn = min(kWave, n_live - c0);
+    for (int s0 = 0; s0 < cn; s0 += SUB) {
+      if (c0 + s0 > 0) {
+#pragma unroll
+        for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(c0 + s0 + u), ov[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < SUB; ++u) {
+        if (s0 + u < cn) {
+          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) o[c] += wu * ov[u][c];
+        }
+      }
+    }
+  }
+  finish_query<T, D>(a, bh, g, lane, M, l, o, qc, sqv, a.nsq > 0, ne, hl.can_append);
+  // the g == 0 wave of a KV head bumps lens (every slice read it in the previous launch)
+  if (lane == 0 && g == 0 && hl.can_append) a.lens[bh] = old_len + 1;
+}
+
 template <class T, int D>
 __global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
   const int pair = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (pair >= a.n_pairs) return;
-  const int bh = pair / a.G, g = pair % a.G;
-  decode_merge_query<T, D>(a, bh, g, lane);
-  if (g == 0 && lane == 0 && a.k_new != nullptr && a.lens[bh] < a.cap) a.lens[bh] += 1;
+  decode_merge_query<T, D>(a, pair / a.G, pair % a.G, lane);
 }
 
 template <class T, int D, int GMAX>
 static hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  if (a.nsplit == 1) {
-    hipLaunchKernelGGL((k_decode<T, D, GMAX, true>), dim3(1, a.n_heads), dim3(256), 0, st, a);
+  if (a.fused) {
+    hipLaunchKernelGGL((k_decode_fused<T, D, GMAX>), dim3(a.n_heads), dim3(256), 0, st, a);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((k_decode<T, D, GMAX, false>), dim3(a.nsplit, a.n_heads), dim3(256), 0, st, a);
+  const unsigned grid = (unsigned)a.n_heads * (unsigned)(a.nsq + a.nsplit);
+  hipLaunchKernelGGL((k_decode_slice<T, D, GMAX>), dim3(grid), dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_decode_merge<T, D>), dim3((a.n_pairs + 3) / 4), dim3(256), 0, st, a);

@@ -21,13 +21,17 @@ struct DecodeArgs {
   void* out;                // [B, Hq, D]
   float* lse_out;           // [B, Hq] or null
   float* w_r_out;           // [B, Hq] or null
-  float* part_o;            // [B*Hkv, nsplit, G, D]
+  float* part_o;            // [B*Hkv, nsplit, G, D]  unnormalised slice outputs
   float* part_ml;           // [B*Hkv, nsplit, G, 2]  (max in log2 units, sum)
   float* sq;                // [B*Hkv, G, D]  S_tilde q (unscaled)
   int32_t* flag;            // sticky append-overflow flag
   int n_heads;              // B * Hkv
   int n_pairs;              // B * Hq
-  int Hkv, G, cap, nsplit, split_len, order;
+  int Hkv, G, cap;
+  int fused;                // 1: one workgroup per KV head, single launch
+  int nsplit, split_len;    // split launch: token slices per KV head, rows per slice (x 32)
+  int nsq;                  // S_tilde q waves per KV head (D / 32 rows each; 0 at order 0)
+  int order;
   float scale, tau;
 };
 

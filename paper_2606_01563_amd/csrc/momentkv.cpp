@@ -13,6 +13,9 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kMaxCandidates = 1 << 18;  // top-k bitmaps live in LDS (2 x 32 KB)
+constexpr int64_t kDecodeWaves = 4096;     // target slice count of an automatic decode split
+constexpr int64_t kMaxDecodeWaves = 1 << 24;  // decode grid limit (single-wave workgroups)
+constexpr int kFusedMaxLen = 384;          // automatic decode: single launch up to this length
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -139,6 +142,25 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
 }
 
 // ----------------------------------------------------------------------- decode
+// Token slices per KV head.  Automatic (n_split = 0): about kDecodeWaves single-wave
+// slices in the whole grid, at least 32 rows each, so that the dispatcher can balance the
+// CUs.  Rows per slice are a multiple of the 32-row block.
+void decode_split(const mkv_decode_params* p, int* split_len, int* nsplit) {
+  const int64_t heads = (int64_t)p->batch * p->n_kv_heads;
+  const int want = p->n_split > 0 ? p->n_split
+                                  : (int)std::min<int64_t>(std::max<int64_t>((kDecodeWaves + heads - 1) / heads, 1), 1 << 20);
+  int sl = ceil_div(p->max_len, want);
+  sl = std::max(32, ceil_div(sl, 32) * 32);
+  *split_len = sl;
+  *nsplit = ceil_div(p->max_len, sl);
+}
+
+// One workgroup per KV head (single launch) for n_split = 1, or automatically for short
+// caches, where a call is bound by latency rather than by how the heads spread over CUs.
+bool decode_fused(const mkv_decode_params* p) {
+  return p->n_split == 1 || (p->n_split == 0 && p->max_len <= kFusedMaxLen);
+}
+
 mkv_status check_decode_params(const mkv_decode_params* p) {
   if (!p) return MKV_ERR_NULL;
   if (p->dtype != MKV_F32 && p->dtype != MKV_BF16) return MKV_ERR_DTYPE;
@@ -152,6 +174,11 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
   if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
   if (p->n_split < 0) return MKV_ERR_SHAPE;
   if (p->max_len < 1 || p->max_len > p->cap) return MKV_ERR_CAPACITY;
+  // grid of single-wave workgroups: B * Hkv * (slices + covariance waves)
+  int split_len = 0, nsplit = 0;
+  decode_split(p, &split_len, &nsplit);
+  const int64_t waves = (int64_t)p->batch * p->n_kv_heads * (nsplit + p->head_dim / 32);
+  if (waves > kMaxDecodeWaves) return MKV_ERR_UNSUPPORTED;
   return MKV_OK;
 }
 
@@ -166,15 +193,9 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   a.order = p->order;
   a.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)p->head_dim);
   a.tau = p->tau;
-  // Slices per KV head: one (merge in the same launch) once the batch alone gives about
-  // one workgroup per CU; otherwise about 1024 workgroups of at least 64 rows.
-  int want = p->n_split;
-  if (want == 0) want = a.n_heads >= 240 ? 1 : clampi(ceil_div(1024, a.n_heads), 1, 1 << 20);
-  int sl = ceil_div(p->max_len, want);
-  sl = ceil_div(sl, 16) * 16;
-  if (sl < 64 && want > 1) sl = 64;
-  a.split_len = sl;
-  a.nsplit = ceil_div(p->max_len, sl);
+  decode_split(p, &a.split_len, &a.nsplit);
+  a.fused = decode_fused(p) ? 1 : 0;
+  a.nsq = p->order >= 1 ? p->head_dim / 32 : 0;
   const size_t H = a.n_heads, D = p->head_dim, G = a.G;
   Carver c;
   c.base = static_cast<char*>(ws);

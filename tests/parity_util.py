@@ -149,19 +149,25 @@ def oracle_moments(out: mk.CompressOutput, b: int, h: int) -> O.Moments:
 
 
 def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1, tau=1e-6,
-                     append=True, n_split=0):
+                     append=True, n_split=0, lens0=None):
     """Run `steps` decode calls on the GPU, each checked against the oracle fed the GPU's
-    retained cache and fp32 moments.  Returns the list of max relative errors."""
+    retained cache and fp32 moments.  `lens0` ([B, Hkv], each at most the compressed
+    length) replaces the retained lengths before the first step.  Returns the list of max
+    relative errors."""
     dt = inp["k"].dtype
     tol = TOL[dt]
     B, Hkv, cap, d = comp.k_out.shape
     Hq = inp["q_win"].shape[1]
     G = Hq // Hkv
     lens = comp.lens.clone()
+    if lens0 is not None:
+        lens0 = torch.as_tensor(lens0, dtype=torch.int32)
+        assert bool((lens0 <= comp.lens.cpu()).all())
+        lens.copy_(lens0)
     moments = [[oracle_moments(comp, b, h) for h in range(Hkv)] for b in range(B)]
     kc_ref = h64(comp.k_out)
     vc_ref = h64(comp.v_out)
-    ln_ref = comp.lens.cpu().numpy().astype(np.int64)
+    ln_ref = lens.cpu().numpy().astype(np.int64)
     lse = torch.empty(B, Hq, dtype=torch.float32, device=comp.k_out.device)
     w_r = torch.empty_like(lse)
     ws = None
@@ -182,8 +188,10 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
         got = h64(out)
         e = max(rel_l2(got[b, hq], ref_out[b, hq]) for b in range(B) for hq in range(Hq))
         e_w = float(np.max(np.abs(w_r.cpu().double().numpy() - ref_wr)))
-        e_l = float(np.max(np.abs(lse.cpu().double().numpy() - ref_lz) /
-                           np.maximum(1.0, np.abs(ref_lz))))
+        got_lz = lse.cpu().double().numpy()
+        same = got_lz == ref_lz                     # equal infinities (empty retained set)
+        e_l = float(np.max(np.where(same, 0.0, np.abs(got_lz - ref_lz) /
+                                    np.maximum(1.0, np.abs(np.where(same, 0.0, ref_lz))))))
         assert e <= tol, (t, e)
         assert e_w <= max(tol, 1e-5), (t, e_w)
         assert e_l <= max(tol, 1e-5), (t, e_l)

@@ -57,13 +57,29 @@ def test_llama_layer_bf16_compress_and_decode():
     announce(f"decode worst rel err {max(worst):.2e}")
 
 
-@pytest.mark.parametrize("n_split", [1, 2, 5])
+@pytest.mark.parametrize("n_split", [1, 2, 5, 0])
 def test_decode_slice_counts(n_split):
-    """The single-launch path (one workgroup per KV head) and explicit slice counts give the
-    same results as the oracle."""
+    """The single-launch path (one workgroup per KV head), explicit slice counts and the
+    automatic choice give the same results as the oracle."""
     wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=3, ctx_len=3000, batch=2)
     out = P.run_compress(gpu, 400, cap=403)
     P.run_decode_steps(gpu, out, 3, n_split=n_split)
+
+
+@pytest.mark.parametrize("append", [True, False])
+@pytest.mark.parametrize("n_split", [0, 3, 4])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_decode_varied_lengths_and_slice_boundaries(dtype, n_split, append):
+    """Per-head retained lengths 0, 31, 32, 33, 64 and 65: an empty retained set, a ragged
+    first block, and appends landing on the first row of a block (single launch, n_split
+    0 here) or of a 64- or 32-row slice (n_split 3, 4: that slice writes the row and
+    attends to nothing; the next step reads the row back)."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=128, ctx_len=1000,
+                         batch=3, n_q_heads=4, n_kv_heads=2, window=16, budgets=(97,))
+    out = P.run_compress(gpu, 97, cap=100)
+    lens0 = [[0, 31], [32, 33], [64, 65]]
+    announce(f"lengths {lens0} {dtype} n_split={n_split} append={append}")
+    P.run_decode_steps(gpu, out, 3, n_split=n_split, append=append, lens0=lens0)
 
 
 # ---------------------------------------------------------------- edge cases
