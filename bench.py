@@ -7,7 +7,8 @@ retained tokens per KV head.  Seeded synthetic post-RoPE inputs are generated on
 GPU and stay resident in HBM.  One timed step is one pass of the whole hot path:
 
   for every budget: momentkv_compress of each of the 36 layers (per-layer calls), writing
-                    that layer's retained cache and moments into a 36-layer stack;
+                    that layer's retained cache and moments into a 36-layer stack, then
+                    momentkv_prepare_summary over the stack (the summaries' decode form);
   then 128 decode tokens: for each token and each budget one momentkv_decode_attn launch
                     over the flattened (layer x sequence) batch of 36 caches, appending the
                     token's key/value (budgets interleaved, so consecutive launches touch
@@ -181,6 +182,8 @@ def main() -> int:
                                  st.s_k[sl], st.s_v[sl], st.S[sl])
 
     views = {L: [layer_view(stacks[L], l) for l in range(layers)] for L in budgets}
+    pshape = (LB, Hkv, 2, d, d) if wl.dtype == torch.bfloat16 else (LB, Hkv, d, d)
+    prepared = {L: torch.empty(pshape, dtype=wl.dtype, device=dev) for L in budgets}
 
     def compress_phase(timing):
         for L in budgets:
@@ -191,6 +194,9 @@ def main() -> int:
                 x = data[l]
                 mk.momentkv_compress(x["q_win"], x["k"], x["v"], L, cap=min(L, N) + T,
                                      out=views[L][l], workspace=cws)
+            st = stacks[L]   # the decode form of the 36 summaries, once per compression
+            mk.momentkv_prepare_summary(st.n_e, st.s_k, st.s_v, st.S, dtype=wl.dtype,
+                                        out=prepared[L])
             e1.record()
             if timing is not None:
                 timing["compress"][L].append((e0, e1))
@@ -198,8 +204,8 @@ def main() -> int:
     def decode_call(t, L):
         st = stacks[L]
         mk.momentkv_decode_attn(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k,
-                                st.s_v, st.S, k_new=kn_steps[t], v_new=vn_steps[t],
-                                max_len=min(L, N) + T, out=out, workspace=dws[L])
+                                st.s_v, prepared[L], k_new=kn_steps[t], v_new=vn_steps[t],
+                                max_len=min(L, N) + T, out=out, workspace=dws[L], summary=1)
 
     def decode_phase(skip=None):
         for t in range(T):

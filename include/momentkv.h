@@ -13,6 +13,9 @@
  *   momentkv_decode_attn  attention over the retained cache fused with the first-order
  *                         correction for the evicted tokens (Algorithm 1 Phase 2;
  *                         Eqs. fhat, jensen, fused; log-domain weight of App. C.2).
+ *   momentkv_prepare_summary  the centred, clamped covariance of a summary in the form
+ *                         the decode reads fastest; the summary is fixed between
+ *                         compressions, so this runs once per compression.
  *
  * Conventions shared by every entry point
  *   - Tensors are dense, contiguous, row-major, in device memory (HBM) unless stated.
@@ -41,7 +44,7 @@
 extern "C" {
 #endif
 
-#define MOMENTKV_ABI_VERSION 1
+#define MOMENTKV_ABI_VERSION 2
 
 typedef enum {
   MKV_OK = 0,
@@ -165,10 +168,28 @@ typedef struct {
                         /* per KV head, single launch; k > 1 = k token slices of one */
                         /* wave each (rows rounded up to a multiple of 32) followed  */
                         /* by a merge launch; 0 = automatic (single launch up to     */
-                        /* max_len 384, else about 4096 slices in the whole grid).   */
+                        /* max_len 384, else about 768 slices in the whole grid).    */
+  int32_t summary;      /* form of the S argument: 0 = the raw sum S (fp32); 1 = the */
+                        /* prepared form written by momentkv_prepare_summary         */
 } mkv_decode_params;
 
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
+
+/* Decode form of a summary (Eq. fhat's covariance term; clamp of App. C.2).
+ *
+ * Per (b, h) with n_e > 0: S_tilde = S - s_v s_k^T / n_e in fp32, entries with
+ * |S_tilde| < tau set to 0 (the same arithmetic the decode applies to a raw S), stored as
+ *   dtype bf16: two bf16 planes [B, Hkv, 2, d, d]: hi = RNE(S_tilde), lo = RNE(S_tilde - hi),
+ *               so hi + lo equals S_tilde to within 2^-16 of its magnitude;
+ *   dtype fp32: S_tilde itself, fp32 [B, Hkv, d, d].
+ * Heads with n_e = 0 get zeros.  Uses batch, n_q_heads, n_kv_heads, head_dim, dtype and
+ * tau of p (the other fields are validated as for the decode).  `prepared` holds
+ * momentkv_prepared_summary_size(p) bytes (16-byte aligned) and must not overlap the
+ * inputs.  Decode calls with p->summary = 1 read it in place of S. */
+size_t momentkv_prepared_summary_size(const mkv_decode_params* p);
+mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n_e,
+                                    const float* s_k, const float* s_v, const float* S,
+                                    void* prepared, void* stream);
 
 /* q         [B, Hq, d]
  * k_cache, v_cache [B, Hkv, cap, d]  retained cache; row lens[b,h] is written when
@@ -177,7 +198,9 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
  *           An empty retained set gives log Z_R = -inf, w_R = 0 and out = f_E_hat
  *           (out = 0 when n_e = 0 as well).
  * k_new, v_new [B, Hkv, d] or both NULL
- * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d], S [B, Hkv, d, d] fp32: the summary, read only
+ * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d] fp32: the summary, read only
+ * S         p->summary = 0: the raw sum, fp32 [B, Hkv, d, d]; p->summary = 1: the output of
+ *           momentkv_prepare_summary for the same summary, tau and dtype
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R
@@ -188,7 +211,7 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
 mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
                                 void* v_cache, int32_t* lens, const void* k_new,
                                 const void* v_new, const int32_t* n_e, const float* s_k,
-                                const float* s_v, const float* S, void* out, float* lse_out,
+                                const float* s_v, const void* S, void* out, float* lse_out,
                                 float* w_r_out, void* workspace, size_t workspace_bytes,
                                 void* stream);
 

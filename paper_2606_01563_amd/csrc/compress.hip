@@ -545,18 +545,23 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
 // ------------------------------------------------------------------------------------
 // Stage 4/9: per-head selection of the k best scores (ties: lower position first),
 // output in ascending position order.  Scores are non-negative floats, so their bit
-// patterns (bit 31 clear) order like unsigned integers.
-//   k_topk_hist    grid (slices, heads): histogram of key bits 30..20 per slice.
-//   k_topk_select  one 1024-thread workgroup per head: sums the slice histograms, finds
-//                  the bin of the k-th largest key, refines bits 19..10 and 9..0 over the
-//                  keys still matching, which gives the k-th key T and how many keys equal
-//                  to T are needed; marks keys > T and keys == T in LDS bitmaps (one
-//                  ballot per wave), then compacts the kept positions in order with two
-//                  block scans (equal keys before each run; kept keys before each run).
+// patterns (bit 31 clear) order like unsigned integers.  One 1024-thread workgroup per
+// head finds the k-th largest key T by radix histograms of bits 30..20, 19..10 and 9..0
+// (each over the keys still matching the prefix), which also gives how many keys equal
+// to T are kept (the lowest positions).  Compaction: each wave owns a contiguous chunk of
+// positions, counts keys > T and == T with ballots, a scan over the 16 waves gives every
+// wave its share of equal keys and its output offset, and a second ballot pass writes the
+// kept positions in order.
+//   keys in LDS (n <= TK_LDS_KEYS, e.g. 32K contexts): the scores are read once, every
+//     pass runs on LDS, one launch;
+//   larger n: k_topk_hist builds the first histogram over slices of all CUs, and the
+//     passes read the (cache-resident) scores eight loads deep.
 // ------------------------------------------------------------------------------------
 constexpr int TK_THREADS = 1024;
 constexpr int TK_WAVES = TK_THREADS / 64;
 constexpr int TK_BINS0 = 2048;
+constexpr int TK_LDS_KEYS = 34816;  // 136 KB of keys
+constexpr int TK_UNROLL = 8;
 
 __device__ __forceinline__ uint32_t score_key(float s) {
   uint32_t u = __float_as_uint(s);
@@ -629,42 +634,73 @@ __device__ __forceinline__ void find_bin(const uint32_t* hist, int nb, int need,
   __syncthreads();
 }
 
+template <bool LDS>
 __global__ void __launch_bounds__(TK_THREADS) k_topk_select(const float* __restrict__ scores, int n,
                                                               int k, const uint32_t* __restrict__ hist,
                                                               int n_slices, int32_t* __restrict__ out,
                                                               int out_stride, int pos_offset) {
-  extern __shared__ uint32_t bits[];          // [2][nw]: keys > T, keys == T
+  __shared__ uint32_t keys_lds[LDS ? TK_LDS_KEYS : 1];
   __shared__ uint32_t hst[TK_BINS0];
   __shared__ uint32_t sh_bin, sh_above;
   __shared__ int sW[2 * TK_WAVES + 1];
-  const int tid = threadIdx.x, lane = tid & 63;
+  __shared__ int s_gt[TK_WAVES], s_eq[TK_WAVES], s_eqb[TK_WAVES], s_ob[TK_WAVES];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.x;
   const float* s = scores + (size_t)head * n;
   int32_t* o = out + (size_t)head * out_stride;
   if (k <= 0) return;
-  const int nw = (n + 31) / 32;
-  uint32_t* gtw = bits;
-  uint32_t* eqw = bits + nw;
+  auto key = [&](int j) -> uint32_t {
+    if constexpr (LDS) return keys_lds[j];
+    else return score_key(s[j]);
+  };
 
-  // bits 30..20 from the slice histograms (fixed order over slices)
-  for (int b = tid; b < TK_BINS0; b += TK_THREADS) {
-    uint32_t c = 0;
-    for (int sl = 0; sl < n_slices; ++sl) c += hist[((size_t)head * n_slices + sl) * TK_BINS0 + b];
-    hst[b] = c;
+  // ---- bits 30..20
+  if constexpr (LDS) {
+    for (int base = 0; base < n; base += TK_THREADS * TK_UNROLL) {
+      float v[TK_UNROLL];
+#pragma unroll
+      for (int u = 0; u < TK_UNROLL; ++u) {
+        const int j = base + u * TK_THREADS + tid;
+        v[u] = j < n ? s[j] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < TK_UNROLL; ++u) {
+        const int j = base + u * TK_THREADS + tid;
+        if (j < n) keys_lds[j] = score_key(v[u]);
+      }
+    }
+    for (int b = tid; b < TK_BINS0; b += TK_THREADS) hst[b] = 0;
+    __syncthreads();
+    for (int j = tid; j < n; j += TK_THREADS) atomicAdd(&hst[keys_lds[j] >> 20], 1u);
+  } else {
+    for (int b = tid; b < TK_BINS0; b += TK_THREADS) {  // fixed order over the slices
+      uint32_t c = 0;
+      for (int sl = 0; sl < n_slices; ++sl) c += hist[((size_t)head * n_slices + sl) * TK_BINS0 + b];
+      hst[b] = c;
+    }
   }
   __syncthreads();
   find_bin(hst, TK_BINS0, k, sW, &sh_bin, &sh_above);
   uint32_t prefix = sh_bin << 20, mask = 0x7FF00000u;
   int remaining = k - (int)sh_above;
   __syncthreads();
-  // bits 19..10, then 9..0, over the keys that still match
+  // ---- bits 19..10, then 9..0, over the keys that still match
   for (int pass = 0; pass < 2; ++pass) {
     const int shift = pass == 0 ? 10 : 0;
     for (int i = tid; i < 1024; i += TK_THREADS) hst[i] = 0;
     __syncthreads();
-    for (int j = tid; j < n; j += TK_THREADS) {
-      const uint32_t u = score_key(s[j]);
-      if ((u & mask) == prefix) atomicAdd(&hst[(u >> shift) & 1023u], 1u);
+    for (int base = 0; base < n; base += TK_THREADS * TK_UNROLL) {
+      uint32_t kk[TK_UNROLL];
+#pragma unroll
+      for (int u = 0; u < TK_UNROLL; ++u) {
+        const int j = base + u * TK_THREADS + tid;
+        kk[u] = j < n ? key(j) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < TK_UNROLL; ++u) {
+        const int j = base + u * TK_THREADS + tid;
+        if (j < n && (kk[u] & mask) == prefix) atomicAdd(&hst[(kk[u] >> shift) & 1023u], 1u);
+      }
     }
     __syncthreads();
     find_bin(hst, 1024, remaining, sW, &sh_bin, &sh_above);
@@ -674,48 +710,61 @@ __global__ void __launch_bounds__(TK_THREADS) k_topk_select(const float* __restr
     __syncthreads();
   }
   const uint32_t T = prefix;
-  const int need = remaining;  // keys equal to T to keep (>= 1)
+  const int need = remaining;  // keys equal to T to keep (>= 1), the lowest positions
 
-  // bitmaps of keys > T and keys == T (each wave covers 64 consecutive positions)
-  for (int base = 0; base < n; base += TK_THREADS) {
-    const int j = base + tid;
-    const uint32_t u = j < n ? score_key(s[j]) : 0u;
-    const unsigned long long g = __ballot(j < n && u > T);
-    const unsigned long long e = __ballot(j < n && u == T);
-    if (lane == 0) {
-      const int w0 = j >> 5;
-      if (w0 < nw) { gtw[w0] = (uint32_t)g; eqw[w0] = (uint32_t)e; }
-      if (w0 + 1 < nw) { gtw[w0 + 1] = (uint32_t)(g >> 32); eqw[w0 + 1] = (uint32_t)(e >> 32); }
+  // ---- ordered compaction over wave chunks of CH positions
+  const int CH = ((n + TK_WAVES * 64 - 1) / (TK_WAVES * 64)) * 64;
+  const int c0 = wave * CH, c1 = min(n, c0 + CH);
+  const unsigned long long below = (1ull << lane) - 1ull;
+  int n_gt = 0, n_eq = 0;
+  for (int g0 = c0; g0 < c1; g0 += 64 * TK_UNROLL) {
+    uint32_t kk[TK_UNROLL];
+#pragma unroll
+    for (int u = 0; u < TK_UNROLL; ++u) {
+      const int j = g0 + 64 * u + lane;
+      kk[u] = j < c1 ? key(j) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < TK_UNROLL; ++u) {
+      const bool v = g0 + 64 * u + lane < c1;
+      n_gt += __popcll(__ballot(v && kk[u] > T));
+      n_eq += __popcll(__ballot(v && kk[u] == T));
+    }
+  }
+  if (lane == 0) { s_gt[wave] = n_gt; s_eq[wave] = n_eq; }
+  __syncthreads();
+  if (tid == 0) {
+    int eb = 0, ob = 0;
+    for (int w = 0; w < TK_WAVES; ++w) {
+      s_eqb[w] = eb;
+      s_ob[w] = ob;
+      ob += s_gt[w] + min(max(need - eb, 0), s_eq[w]);
+      eb += s_eq[w];
     }
   }
   __syncthreads();
-  // ordered compaction: thread t owns words [t*W, t*W + W)
-  const int W = (nw + TK_THREADS - 1) / TK_THREADS;
-  const int w0 = tid * W, w1 = min(nw, w0 + W);
-  int n_eq = 0;
-  for (int w = w0; w < w1; ++w) n_eq += __popc(eqw[w]);
-  int tot;
-  int eq_before = block_excl_scan(n_eq, sW, &tot);
-  int n_take = 0;
-  for (int w = w0; w < w1; ++w) {
-    uint32_t e = eqw[w], keep = 0;
-    while (e && eq_before < need) {
-      const uint32_t low = e & (0u - e);
-      keep |= low;
-      e ^= low;
-      ++eq_before;
+  int eqb = s_eqb[wave], ob = s_ob[wave];
+  for (int g0 = c0; g0 < c1; g0 += 64 * TK_UNROLL) {
+    uint32_t kk[TK_UNROLL];
+#pragma unroll
+    for (int u = 0; u < TK_UNROLL; ++u) {
+      const int j = g0 + 64 * u + lane;
+      kk[u] = j < c1 ? key(j) : 0u;
     }
-    eqw[w] = keep;  // each thread rewrites only its own words
-    n_take += __popc(gtw[w] | keep);
-  }
-  int pos = block_excl_scan(n_take, sW, &tot);
-  for (int w = w0; w < w1; ++w) {
-    uint32_t x = gtw[w] | eqw[w];
-    while (x) {
-      const int b = __ffs((int)x) - 1;
-      x &= x - 1;
-      if (pos < k) o[pos] = w * 32 + b + pos_offset;
-      ++pos;
+#pragma unroll
+    for (int u = 0; u < TK_UNROLL; ++u) {
+      const int j = g0 + 64 * u + lane;
+      const bool v = j < c1;
+      const bool eq = v && kk[u] == T;
+      const unsigned long long em = __ballot(eq);
+      const bool keep = (v && kk[u] > T) || (eq && eqb + __popcll(em & below) < need);
+      const unsigned long long km = __ballot(keep);
+      if (keep) {
+        const int p = ob + __popcll(km & below);
+        if (p < k) o[p] = j + pos_offset;
+      }
+      ob += __popcll(km);
+      eqb += __popcll(em);
     }
   }
 }
@@ -730,7 +779,9 @@ __global__ void __launch_bounds__(256) k_gather_rows(CompressArgs a) {
   const int c = blockIdx.x * 256 + threadIdx.x;
   const int i = c / DG, dg = c % DG;
   if (i >= a.k_keep) return;
-  const int pos = a.kept0[(size_t)head * a.kmax + i];
+  // kept positions are read as addresses: clamped to the context, so that no selection
+  // result can move a read outside the head's rows
+  const int pos = min(max(a.kept0[(size_t)head * a.kmax + i], 0), a.N - 1);
   const size_t src = ((size_t)head * a.N + pos) * D + 8 * dg;
   const size_t dst = ((size_t)head * a.kmax + i) * D + 8 * dg;
   store_frag(reinterpret_cast<T*>(a.gath_k) + dst, load_frag(reinterpret_cast<const T*>(a.k) + src));
@@ -1001,6 +1052,7 @@ __global__ void __launch_bounds__(256) k_gather_out(CompressArgs a, int n_out, i
   if (keep_all || i < a.n_s) pos = i;
   else if (i < a.n_s + a.k_keep) pos = a.kept[(size_t)head * a.kmax + (i - a.n_s)];
   else pos = a.N - a.w + (i - a.n_s - a.k_keep);
+  pos = min(max(pos, 0), a.N - 1);  // a kept position is an address: never outside the rows
   const size_t src = ((size_t)head * a.N + pos) * D + 8 * dg;
   const size_t dst = ((size_t)head * a.cap + i) * D + 8 * dg;
   store_frag(reinterpret_cast<T*>(a.k_out) + dst, load_frag(reinterpret_cast<const T*>(a.k) + src));
@@ -1032,11 +1084,16 @@ __global__ void __launch_bounds__(256) k_zero_moments(CompressArgs a) {
 static hipError_t launch_topk(const CompressArgs& a, const float* scores, int32_t* out,
                               hipStream_t st) {
   if (a.k_keep <= 0) return hipSuccess;
+  if (a.n_c <= TK_LDS_KEYS) {
+    hipLaunchKernelGGL(k_topk_select<true>, dim3(a.H), dim3(TK_THREADS), 0, st, scores, a.n_c,
+                       a.k_keep, (const uint32_t*)nullptr, 0, out, a.kmax, a.n_s);
+    MKV_CHECK_LAUNCH();
+    return hipSuccess;
+  }
   hipLaunchKernelGGL(k_topk_hist, dim3(a.ntk, a.H), dim3(256), 0, st, scores, a.n_c, a.tk_per,
                      a.tk_hist);
   MKV_CHECK_LAUNCH();
-  const size_t smem = 2 * (size_t)((a.n_c + 31) / 32) * sizeof(uint32_t);
-  hipLaunchKernelGGL(k_topk_select, dim3(a.H), dim3(TK_THREADS), smem, st, scores, a.n_c,
+  hipLaunchKernelGGL(k_topk_select<false>, dim3(a.H), dim3(TK_THREADS), 0, st, scores, a.n_c,
                      a.k_keep, (const uint32_t*)a.tk_hist, a.ntk, out, a.kmax, a.n_s);
   MKV_CHECK_LAUNCH();
   return hipSuccess;

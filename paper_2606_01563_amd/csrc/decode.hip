@@ -4,9 +4,10 @@
 // Two launch shapes, chosen by the host from the cache length bound:
 //
 // fused   k_decode_fused: one 4-wave workgroup per KV head, one launch.  Wave w computes
-//         rows [32w, 32w + 32) of S_tilde q (S_tilde = S - s_v s_k^T / n_e, clamped as it
-//         is loaded) and attends to the 32-row blocks w, w + 4, ... of the retained cache
-//         for all G query heads of the group; the four partial softmax states are merged
+//         rows [32w, 32w + 32) of S_tilde q (S_tilde = S - s_v s_k^T / n_e, clamped; formed
+//         from the raw S as it is loaded, or read in the prepared form) and attends to the
+//         32-row blocks w, w + 4, ... of the retained cache for all G query heads of the
+//         group; the four partial softmax states are merged
 //         in LDS, the new token is folded in, and the moment correction is applied.  The
 //         S rows and the first cache block are requested together, so the S_tilde q
 //         products run while the cache rows are in flight.  Used for short caches, where
@@ -14,9 +15,9 @@
 //
 // split   k_decode_slice + k_decode_merge: a 1-D grid of n_heads x (nsq + nsplit)
 //         single-wave workgroups, then one wave per (b, query head).
-//         * x < nsq: 32 rows of S_tilde q, written to the workspace;
-//         * x >= nsq: a token slice (split_len rows below lens) of one KV head, written as
-//           an unnormalised (o, max, sum) partial;
+//         * n_heads x nsq waves of 32 rows of S_tilde q, written to the workspace;
+//         * n_heads x nsplit token slices (split_len rows below lens) of one KV head,
+//           each written as an unnormalised (o, max, sum) partial;
 //         * merge: the slices in a fixed order, then the new token, then the correction.
 //         Used for long caches: reading is bound by how much each CU keeps in flight, so
 //         the finishing time is set by the busiest CU, and thousands of short slices let
@@ -92,61 +93,142 @@ __device__ __forceinline__ void append_row(const DecodeArgs& a, int head, int ro
 }
 
 // ---------------------------------------------------------------- S_tilde q
-// Rows [r0, r0 + 32) of S_tilde q (unscaled) for the queries held in the query fragments,
-// on fp32 MFMA: A = two 16-row tiles of S_tilde, centred and clamped as they are loaded;
-// B = the queries as fp32 (query g in column g).  load() issues every read; compute()
-// writes result (g, r) to dst[g * D + r] for g < G.
-template <class T, int D>
+// Rows [r0, r0 + 32) of S_tilde q (unscaled) for the queries held in the query fragments
+// (query g in MFMA column g).  load() issues every read; compute() writes result (g, r) to
+// dst[g * D + r] for g < G.  Three forms of the summary:
+//  * raw S (PREP = false): fp32 MFMA; S_tilde = S - s_v s_k^T / n_e, clamped at tau, is
+//    formed as the rows are loaded;
+//  * prepared, fp32 caches: the stored S_tilde on fp32 MFMA;
+//  * prepared, bf16 caches: the stored hi / lo bf16 planes on bf16 MFMA, two products per
+//    32-wide step against the (exact) bf16 queries.
+template <class T, int D, bool PREP>
 struct SqRows {
   static constexpr int KS = D / 32;
+  static constexpr bool HILO = PREP && sizeof(T) == 2;
   f32x8 raw[2][KS];
+  bf16x8 hi[2][KS], lo[2][KS];
   f32x8 skc[KS];
   float sv[2];
   int ne;
 
   __device__ __forceinline__ void load(const DecodeArgs& a, int head, int r0, int lane) {
-    const float* Sh = a.S + (size_t)head * D * D;
-    const float* svh = a.s_v + (size_t)head * D;
-    ne = a.n_e[head];
+    const int col = 8 * (lane >> 4);
+    if constexpr (HILO) {
+      const bf16_t* P = reinterpret_cast<const bf16_t*>(a.S) + (size_t)head * 2 * D * D;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int row = r0 + 16 * u + (lane & 15);
-      sv[u] = svh[row];
+      for (int u = 0; u < 2; ++u) {
+        const int row = r0 + 16 * u + (lane & 15);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) raw[u][ks] = load_frag(Sh + (size_t)row * D + 32 * ks + 8 * (lane >> 4));
+        for (int ks = 0; ks < KS; ++ks) {
+          hi[u][ks] = load_frag(P + (size_t)row * D + 32 * ks + col);
+          lo[u][ks] = load_frag(P + (size_t)(D + row) * D + 32 * ks + col);
+        }
+      }
+    } else {
+      const float* Sh = a.S + (size_t)head * D * D;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int row = r0 + 16 * u + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) raw[u][ks] = load_frag(Sh + (size_t)row * D + 32 * ks + col);
+        if constexpr (!PREP) sv[u] = a.s_v[(size_t)head * D + row];
+      }
+      if constexpr (!PREP) {
+        ne = a.n_e[head];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) skc[ks] = load_frag(a.s_k + (size_t)head * D + 32 * ks + col);
+      }
     }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) skc[ks] = load_frag(a.s_k + (size_t)head * D + 32 * ks + 8 * (lane >> 4));
   }
 
   __device__ __forceinline__ void compute(const DecodeArgs& a, const typename Frag<T>::type (&qf)[KS],
                                           int r0, int lane, float* dst) {
     const int g = lane & 15;
-    const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
-    f32x8 qb[KS];
+    f32x4 acc[2];
+    if constexpr (HILO) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+      for (int u = 0; u < 2; ++u) {
+        acc[u] = zero4();
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qb[ks][e] = elem_f(qf[ks], e);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      f32x4 acc = zero4();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        f32x8 af;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float st = raw[u][ks][e] - sv[u] * (skc[ks][e] * inv_n);
-          af[e] = fabsf(st) < a.tau ? 0.f : st;
+        for (int ks = 0; ks < KS; ++ks) {
+          mma(acc[u], hi[u][ks], qf[ks]);
+          mma(acc[u], lo[u][ks], qf[ks]);
         }
-        mma(acc, af, qb[ks]);
       }
+    } else {
+      float inv_n = 0.f;
+      if constexpr (!PREP) inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+      f32x8 qb[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qb[ks][e] = elem_f(qf[ks], e);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        acc[u] = zero4();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          f32x8 af;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if constexpr (PREP) {
+              af[e] = raw[u][ks][e];
+            } else {
+              const float st = raw[u][ks][e] - sv[u] * (skc[ks][e] * inv_n);
+              af[e] = fabsf(st) < a.tau ? 0.f : st;
+            }
+          }
+          mma(acc[u], af, qb[ks]);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (g < a.G) dst[(size_t)g * D + r0 + 16 * u + 4 * (lane >> 4) + i] = acc[i];
-    }
+        if (g < a.G) dst[(size_t)g * D + r0 + 16 * u + 4 * (lane >> 4) + i] = acc[u][i];
   }
 };
+
+// Decode form of the summary: S_tilde = S - s_v s_k^T / n_e with entries below tau set to
+// zero, computed with the same fp32 arithmetic as the raw-summary decode path, stored as
+// hi = RNE_bf16(S_tilde) and lo = RNE_bf16(S_tilde - hi) planes for bf16 caches, or as fp32.
+// Grid (D * D / 8 / 256, n_heads); a thread handles 8 consecutive entries of one row.
+template <class T, int D>
+__global__ void __launch_bounds__(256) k_prepare_summary(DecodeArgs a, void* prepared) {
+  const int head = blockIdx.y;
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= D * D / 8) return;
+  const int row = idx / (D / 8), c0 = 8 * (idx % (D / 8));
+  const int ne = a.n_e[head];
+  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+  const f32x8 raw = load_frag(a.S + ((size_t)head * D + row) * D + c0);
+  const f32x8 skc = load_frag(a.s_k + (size_t)head * D + c0);
+  const float sv = a.s_v[(size_t)head * D + row];
+  float st[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float t = raw[e] - sv * (skc[e] * inv_n);
+    st[e] = (ne <= 0 || fabsf(t) < a.tau) ? 0.f : t;
+  }
+  if constexpr (sizeof(T) == 2) {
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const bf16_t h0 = f2bf(st[e]), h1 = f2bf(st[e + 1]);
+      const bf16_t l0 = f2bf(st[e] - bf2f(h0)), l1 = f2bf(st[e + 1] - bf2f(h1));
+      h[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      l[e / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    }
+    bf16_t* P = reinterpret_cast<bf16_t*>(prepared) + (size_t)head * 2 * D * D;
+    *reinterpret_cast<uint4*>(P + (size_t)row * D + c0) = make_uint4(h[0], h[1], h[2], h[3]);
+    *reinterpret_cast<uint4*>(P + (size_t)(D + row) * D + c0) = make_uint4(l[0], l[1], l[2], l[3]);
+  } else {
+    float4* P = reinterpret_cast<float4*>(reinterpret_cast<float*>(prepared) + ((size_t)head * D + row) * D + c0);
+    P[0] = make_float4(st[0], st[1], st[2], st[3]);
+    P[1] = make_float4(st[4], st[5], st[6], st[7]);
+  }
+}
 
 // ---------------------------------------------------------------- block attention
 // One wave's online-softmax attention over 32-row blocks of one KV head's cache rows
@@ -407,7 +489,7 @@ __device__ __forceinline__ void finish_query(const DecodeArgs& a, int bh, int g,
 }
 
 // ---------------------------------------------------------------- fused launch
-template <class T, int D, int GMAX>
+template <class T, int D, int GMAX, bool PREP>
 __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int CPL = D / 64;
@@ -430,7 +512,7 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   typename BA::FragT qf[KS];
   load_query_frags<T, D>(qh, G, lane, qf);
   const bool sq_rows = a.nsq > 0 && 32 * wave < D;
-  SqRows<T, D> sq;
+  SqRows<T, D, PREP> sq;
   if (sq_rows) sq.load(a, head, 32 * wave, lane);
   const QueryCols<CPL> qc = load_query_cols<T, D>(a, head, min(wave, G - 1), lane);
   const int ne = a.n_e[head];
@@ -478,7 +560,7 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------- split launch
-template <class T, int D, int GMAX>
+template <class T, int D, int GMAX, bool PREP>
 __global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int KS = D / 32;
@@ -488,21 +570,27 @@ __global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
   __shared__ __align__(16) T s_p[16][BA::TB + BA::PT];
   __shared__ float s_ml[GMAX * 2];
 
+  // Workgroups reach the XCDs round-robin by id, so each kind of wave is numbered
+  // contiguously: the S_tilde q waves first (head-major), then the token slices
+  // (head-major); either kind then spreads evenly over the XCDs whatever nsq and nsplit.
   const int lane = threadIdx.x;
-  const int per_head = a.nsq + a.nsplit;
-  const int head = blockIdx.x / per_head;         // b * Hkv + h
-  const int part = blockIdx.x % per_head;
+  const int n_sq = a.n_heads * a.nsq;
+  const bool is_sq = (int)blockIdx.x < n_sq;
+  const int idx = is_sq ? (int)blockIdx.x : (int)blockIdx.x - n_sq;
+  const int nsq = max(a.nsq, 1);  // no S_tilde q waves when a.nsq = 0 (is_sq is false)
+  const int head = is_sq ? idx / nsq : idx / a.nsplit;   // b * Hkv + h
   const int G = a.G;
   const T* qh = reinterpret_cast<const T*>(a.q) + (size_t)head * G * D;
   typename BA::FragT qf[KS];
   load_query_frags<T, D>(qh, G, lane, qf);
-  if (part < a.nsq) {
-    SqRows<T, D> sq;
-    sq.load(a, head, 32 * part, lane);
-    sq.compute(a, qf, 32 * part, lane, a.sq + (size_t)head * G * D);
+  if (is_sq) {
+    const int r0 = 32 * (idx % nsq);
+    SqRows<T, D, PREP> sq;
+    sq.load(a, head, r0, lane);
+    sq.compute(a, qf, r0, lane, a.sq + (size_t)head * G * D);
     return;
   }
-  const int split = part - a.nsq;
+  const int split = idx % a.nsplit;
   const HeadLen hl = head_len(a, a.lens[head]);
   const int t0 = split * a.split_len;
   BA ba;
@@ -599,18 +687,23 @@ __global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
   decode_merge_query<T, D>(a, pair / a.G, pair % a.G, lane);
 }
 
-template <class T, int D, int GMAX>
-static hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t st) {
+template <class T, int D, int GMAX, bool PREP>
+static hipError_t launch_decode_p(const DecodeArgs& a, hipStream_t st) {
   if (a.fused) {
-    hipLaunchKernelGGL((k_decode_fused<T, D, GMAX>), dim3(a.n_heads), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_decode_fused<T, D, GMAX, PREP>), dim3(a.n_heads), dim3(256), 0, st, a);
     return hipGetLastError();
   }
   const unsigned grid = (unsigned)a.n_heads * (unsigned)(a.nsq + a.nsplit);
-  hipLaunchKernelGGL((k_decode_slice<T, D, GMAX>), dim3(grid), dim3(64), 0, st, a);
+  hipLaunchKernelGGL((k_decode_slice<T, D, GMAX, PREP>), dim3(grid), dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_decode_merge<T, D>), dim3((a.n_pairs + 3) / 4), dim3(256), 0, st, a);
   return hipGetLastError();
+}
+
+template <class T, int D, int GMAX>
+static hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t st) {
+  return a.summary ? launch_decode_p<T, D, GMAX, true>(a, st) : launch_decode_p<T, D, GMAX, false>(a, st);
 }
 
 template <class T, int D>
@@ -623,6 +716,18 @@ static hipError_t launch_decode_g(const DecodeArgs& a, hipStream_t st) {
 hipError_t launch_decode(const DecodeArgs& a, bool bf16, int d, hipStream_t st) {
   if (bf16) return d == 64 ? launch_decode_g<bf16_t, 64>(a, st) : launch_decode_g<bf16_t, 128>(a, st);
   return d == 64 ? launch_decode_g<float, 64>(a, st) : launch_decode_g<float, 128>(a, st);
+}
+
+template <class T, int D>
+static hipError_t launch_prepare_t(const DecodeArgs& a, void* prepared, hipStream_t st) {
+  hipLaunchKernelGGL((k_prepare_summary<T, D>), dim3((D * D / 8 + 255) / 256, a.n_heads), dim3(256), 0,
+                     st, a, prepared);
+  return hipGetLastError();
+}
+
+hipError_t launch_prepare_summary(const DecodeArgs& a, void* prepared, bool bf16, int d, hipStream_t st) {
+  if (bf16) return d == 64 ? launch_prepare_t<bf16_t, 64>(a, prepared, st) : launch_prepare_t<bf16_t, 128>(a, prepared, st);
+  return d == 64 ? launch_prepare_t<float, 64>(a, prepared, st) : launch_prepare_t<float, 128>(a, prepared, st);
 }
 
 }  // namespace mkv

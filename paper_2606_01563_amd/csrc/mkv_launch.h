@@ -17,7 +17,7 @@ struct DecodeArgs {
   const int32_t* n_e;       // [B, Hkv]
   const float* s_k;         // [B, Hkv, D]
   const float* s_v;
-  const float* S;           // [B, Hkv, D, D]
+  const float* S;           // [B, Hkv, D, D] raw sum, or the prepared form (summary = 1)
   void* out;                // [B, Hq, D]
   float* lse_out;           // [B, Hq] or null
   float* w_r_out;           // [B, Hq] or null
@@ -31,11 +31,15 @@ struct DecodeArgs {
   int fused;                // 1: one workgroup per KV head, single launch
   int nsplit, split_len;    // split launch: token slices per KV head, rows per slice (x 32)
   int nsq;                  // S_tilde q waves per KV head (D / 32 rows each; 0 at order 0)
+  int summary;              // 0: S is the raw sum; 1: S is the prepared form
   int order;
   float scale, tau;
 };
 
 hipError_t launch_decode(const DecodeArgs& a, bool bf16, int d, hipStream_t st);
+// Prepared summary from a.n_e, a.s_k, a.s_v, a.S (raw) into `prepared`.
+hipError_t launch_prepare_summary(const DecodeArgs& a, void* prepared, bool bf16, int d,
+                                  hipStream_t st);
 
 struct CompressArgs {
   const void* q_win;        // [B, Hq, w, D]

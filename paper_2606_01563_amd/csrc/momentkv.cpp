@@ -13,7 +13,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kMaxCandidates = 1 << 18;  // top-k bitmaps live in LDS (2 x 32 KB)
-constexpr int64_t kDecodeWaves = 4096;     // target slice count of an automatic decode split
+constexpr int64_t kDecodeWaves = 768;      // target slice count of an automatic decode split
 constexpr int64_t kMaxDecodeWaves = 1 << 24;  // decode grid limit (single-wave workgroups)
 constexpr int kFusedMaxLen = 384;          // automatic decode: single launch up to this length
 
@@ -143,8 +143,9 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
 
 // ----------------------------------------------------------------------- decode
 // Token slices per KV head.  Automatic (n_split = 0): about kDecodeWaves single-wave
-// slices in the whole grid, at least 32 rows each, so that the dispatcher can balance the
-// CUs.  Rows per slice are a multiple of the 32-row block.
+// slices in the whole grid (three per CU), at least 32 rows each.  Measured on a 288-head
+// stack, longer slices (fewer partials to merge) beat finer splits once every CU holds a
+// few slices.  Rows per slice are a multiple of the 32-row block.
 void decode_split(const mkv_decode_params* p, int* split_len, int* nsplit) {
   const int64_t heads = (int64_t)p->batch * p->n_kv_heads;
   const int want = p->n_split > 0 ? p->n_split
@@ -173,6 +174,7 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
   if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;
   if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
   if (p->n_split < 0) return MKV_ERR_SHAPE;
+  if (p->summary != 0 && p->summary != 1) return MKV_ERR_SHAPE;
   if (p->max_len < 1 || p->max_len > p->cap) return MKV_ERR_CAPACITY;
   // grid of single-wave workgroups: B * Hkv * (slices + covariance waves)
   int split_len = 0, nsplit = 0;
@@ -196,6 +198,7 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   decode_split(p, &a.split_len, &a.nsplit);
   a.fused = decode_fused(p) ? 1 : 0;
   a.nsq = p->order >= 1 ? p->head_dim / 32 : 0;
+  a.summary = p->summary;
   const size_t H = a.n_heads, D = p->head_dim, G = a.G;
   Carver c;
   c.base = static_cast<char*>(ws);
@@ -266,10 +269,40 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p) {
   return total;
 }
 
+size_t momentkv_prepared_summary_size(const mkv_decode_params* p) {
+  if (check_decode_params(p) != MKV_OK) return 0;
+  return (size_t)p->batch * p->n_kv_heads * p->head_dim * p->head_dim * 4;
+}
+
+mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n_e,
+                                    const float* s_k, const float* s_v, const float* S,
+                                    void* prepared, void* stream) {
+  mkv_status st = check_decode_params(p);
+  if (st != MKV_OK) return st;
+  if (!n_e || !s_k || !s_v || !S || !prepared) return MKV_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(prepared) % 16) return MKV_ERR_SHAPE;
+  const size_t heads = (size_t)p->batch * p->n_kv_heads, d = p->head_dim;
+  const size_t out_bytes = heads * d * d * 4;
+  if (ranges_overlap(prepared, out_bytes, S, heads * d * d * 4) ||
+      ranges_overlap(prepared, out_bytes, s_k, heads * d * 4) ||
+      ranges_overlap(prepared, out_bytes, s_v, heads * d * 4) ||
+      ranges_overlap(prepared, out_bytes, n_e, heads * 4))
+    return MKV_ERR_ALIAS;
+  size_t total = 0;
+  mkv::DecodeArgs a = decode_layout(p, nullptr, &total);
+  a.n_e = n_e;
+  a.s_k = s_k;
+  a.s_v = s_v;
+  a.S = S;
+  hipError_t e = mkv::launch_prepare_summary(a, prepared, p->dtype == MKV_BF16, p->head_dim,
+                                             static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MKV_OK : MKV_ERR_HIP;
+}
+
 mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
                                 void* v_cache, int32_t* lens, const void* k_new,
                                 const void* v_new, const int32_t* n_e, const float* s_k,
-                                const float* s_v, const float* S, void* out, float* lse_out,
+                                const float* s_v, const void* S, void* out, float* lse_out,
                                 float* w_r_out, void* workspace, size_t workspace_bytes,
                                 void* stream) {
   mkv_status st = check_decode_params(p);
@@ -302,7 +335,7 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
   a.n_e = n_e;
   a.s_k = s_k;
   a.s_v = s_v;
-  a.S = S;
+  a.S = static_cast<const float*>(S);
   a.out = out;
   a.lse_out = lse_out;
   a.w_r_out = w_r_out;

@@ -52,7 +52,7 @@ class DecodeParams(ctypes.Structure):
                 ("cap", ctypes.c_int32), ("max_len", ctypes.c_int32),
                 ("order", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("tau", ctypes.c_float),
-                ("n_split", ctypes.c_int32)]
+                ("n_split", ctypes.c_int32), ("summary", ctypes.c_int32)]
 
 
 _lib = None
@@ -77,6 +77,10 @@ def lib() -> ctypes.CDLL:
             [_VP, ctypes.c_size_t, _VP]
         L.momentkv_decode_attn.restype = ctypes.c_int
         L.momentkv_status_string.argtypes = [ctypes.c_int32]
+        L.momentkv_prepared_summary_size.argtypes = [ctypes.POINTER(DecodeParams)]
+        L.momentkv_prepared_summary_size.restype = ctypes.c_size_t
+        L.momentkv_prepare_summary.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 6
+        L.momentkv_prepare_summary.restype = ctypes.c_int
         L.momentkv_status_string.restype = ctypes.c_char_p
         L.momentkv_abi_version.argtypes = []
         L.momentkv_abi_version.restype = ctypes.c_int32
@@ -105,6 +109,10 @@ def momentkv_compress_workspace_size(p: CompressParams) -> int:
 
 def momentkv_decode_workspace_size(p: DecodeParams) -> int:
     return int(lib().momentkv_decode_workspace_size(ctypes.byref(p)))
+
+
+def momentkv_prepared_summary_size(p: DecodeParams) -> int:
+    return int(lib().momentkv_prepared_summary_size(ctypes.byref(p)))
 
 
 # ------------------------------------------------------------------------ marshalling
@@ -215,10 +223,31 @@ def decode_workspace_zero_bytes(p: DecodeParams) -> int:
 
 
 def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6,
-                  n_split=0) -> DecodeParams:
+                  n_split=0, summary=0) -> DecodeParams:
     B, Hq, d = q.shape
     _, Hkv, cap, _ = k_cache.shape
-    return DecodeParams(B, Hq, Hkv, d, cap, max_len, order, _dtype_code(q), scale, tau, n_split)
+    return DecodeParams(B, Hq, Hkv, d, cap, max_len, order, _dtype_code(q), scale, tau, n_split,
+                        summary)
+
+
+def momentkv_prepare_summary(n_e: torch.Tensor, s_k: torch.Tensor, s_v: torch.Tensor,
+                             S: torch.Tensor, *, dtype: torch.dtype, tau: float = 1e-6,
+                             out: torch.Tensor | None = None) -> torch.Tensor:
+    """Decode form of the summary (see the header): bf16 hi/lo planes [B, Hkv, 2, d, d] for
+    dtype bf16, fp32 [B, Hkv, d, d] for fp32.  Pass it as `S` with summary=1."""
+    B, Hkv, d, _ = S.shape
+    code = MKV_BF16 if dtype == torch.bfloat16 else MKV_F32
+    p = DecodeParams(B, Hkv, Hkv, d, 1, 1, 1, code, 0.0, tau, 0, 0)
+    if out is None:
+        shape = (B, Hkv, 2, d, d) if dtype == torch.bfloat16 else (B, Hkv, d, d)
+        out = torch.empty(shape, dtype=dtype, device=S.device)
+    if out.numel() * out.element_size() < momentkv_prepared_summary_size(p):
+        raise ValueError("prepared summary buffer too small")
+    code = lib().momentkv_prepare_summary(ctypes.byref(p), _ptr(n_e), _ptr(s_k), _ptr(s_v),
+                                          _ptr(S), _ptr(out), _stream())
+    if code != 0:
+        raise MomentKVError(code, "momentkv_prepare_summary")
+    return out
 
 
 def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
@@ -226,11 +255,13 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
                          s_v: torch.Tensor, S: torch.Tensor, *, k_new: torch.Tensor | None = None,
                          v_new: torch.Tensor | None = None, max_len: int | None = None,
                          order: int = 1, scale: float = 0.0, tau: float = 1e-6,
-                         n_split: int = 0,
+                         n_split: int = 0, summary: int = 0,
                          out: torch.Tensor | None = None, lse: torch.Tensor | None = None,
                          w_r: torch.Tensor | None = None,
                          workspace: torch.Tensor | None = None):
     """Corrected decode attention (see the header).  Returns (out, lse, w_r, workspace).
+
+    `S` is the raw sum (summary=0) or the output of momentkv_prepare_summary (summary=1).
 
     `max_len` bounds lens after the append (defaults to the cache capacity).  The first
     int32 of the workspace is the sticky append-overflow flag; a workspace allocated here
@@ -238,7 +269,7 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     """
     cap = k_cache.shape[2]
     p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
-                      scale=scale, tau=tau, n_split=n_split)
+                      scale=scale, tau=tau, n_split=n_split, summary=summary)
     dev = q.device
     if out is None:
         out = torch.empty_like(q)

@@ -149,16 +149,19 @@ def oracle_moments(out: mk.CompressOutput, b: int, h: int) -> O.Moments:
 
 
 def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1, tau=1e-6,
-                     append=True, n_split=0, lens0=None):
+                     append=True, n_split=0, lens0=None, summary=0):
     """Run `steps` decode calls on the GPU, each checked against the oracle fed the GPU's
     retained cache and fp32 moments.  `lens0` ([B, Hkv], each at most the compressed
     length) replaces the retained lengths before the first step.  Returns the list of max
-    relative errors."""
+    relative errors.  summary=1 passes the prepared summary (the oracle reads the raw
+    moments)."""
     dt = inp["k"].dtype
     tol = TOL[dt]
     B, Hkv, cap, d = comp.k_out.shape
     Hq = inp["q_win"].shape[1]
     G = Hq // Hkv
+    S_arg = comp.S if summary == 0 else mk.momentkv_prepare_summary(
+        comp.n_e, comp.s_k, comp.s_v, comp.S, dtype=dt, tau=tau)
     lens = comp.lens.clone()
     if lens0 is not None:
         lens0 = torch.as_tensor(lens0, dtype=torch.int32)
@@ -177,9 +180,9 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
         kn = inp["k_new"][t] if append else None
         vn = inp["v_new"][t] if append else None
         out, _, _, ws = mk.momentkv_decode_attn(
-            q, comp.k_out, comp.v_out, lens, comp.n_e, comp.s_k, comp.s_v, comp.S, k_new=kn,
+            q, comp.k_out, comp.v_out, lens, comp.n_e, comp.s_k, comp.s_v, S_arg, k_new=kn,
             v_new=vn, max_len=cap, order=order, tau=tau, lse=lse, w_r=w_r, workspace=ws,
-            n_split=n_split)
+            n_split=n_split, summary=summary)
         torch.cuda.synchronize()
         ref_out, ref_lz, ref_wr, (kc_ref, vc_ref, ln_ref) = O.decode(
             h64(q), kc_ref, vc_ref, ln_ref, moments,

@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert mk.momentkv_abi_version() == 1
+    assert mk.momentkv_abi_version() == 2
     for code in range(10):
         assert mk.momentkv_status_string(code) not in ("", "unknown status")
     assert mk.momentkv_status_string(99) == "unknown status"
@@ -44,7 +44,7 @@ def cparams(**kw):
 
 def dparams(**kw):
     base = dict(batch=36, n_q_heads=32, n_kv_heads=8, head_dim=128, cap=640, max_len=640,
-                order=1, dtype=1, scale=0.0, tau=1e-6, n_split=0)
+                order=1, dtype=1, scale=0.0, tau=1e-6, n_split=0, summary=0)
     base.update(kw)
     return mk.DecodeParams(**base)
 
@@ -129,6 +129,8 @@ def test_budget_at_least_context_is_valid(L):
     (dict(cap=0), SHAPE),
     (dict(order=2), SHAPE),
     (dict(n_split=-1), SHAPE),
+    (dict(summary=2), SHAPE),
+    (dict(batch=500000), UNSUP),            # decode grid limit: 4M heads x 5 waves
     (dict(head_dim=80), UNSUP),
     (dict(max_len=0), CAPACITY),
     (dict(max_len=641), CAPACITY),
@@ -147,3 +149,16 @@ def test_decode_rejects_null_alias_and_small_workspace(L):
     ptrs[10] = ptrs[1]                                   # out aliases the key cache
     size = mk.momentkv_decode_workspace_size(p)
     assert mk.lib().momentkv_decode_attn(ctypes.byref(p), *ptrs, 1 << 40, size, None) == ALIAS
+
+
+def test_prepared_summary_size_and_validation(L):
+    p = dparams()
+    assert mk.momentkv_prepared_summary_size(p) == 36 * 8 * 128 * 128 * 4
+    assert mk.momentkv_prepared_summary_size(dparams(head_dim=80)) == 0
+    ptrs = [(1 << 20) + i * (1 << 36) for i in range(5)]
+    f = mk.lib().momentkv_prepare_summary
+    assert f(ctypes.byref(p), None, *ptrs[1:], None) == NULL
+    assert f(ctypes.byref(p), *ptrs[:4], None, None) == NULL
+    assert f(ctypes.byref(p), *ptrs[:4], ptrs[4] + 8, None) == SHAPE      # misaligned
+    assert f(ctypes.byref(p), *ptrs[:4], ptrs[3] + 64, None) == ALIAS     # overlaps S
+    assert f(ctypes.byref(dparams(dtype=5)), *ptrs, None) == DTYPE

@@ -79,22 +79,26 @@ def test_decode_varied_lengths_and_slice_boundaries(dtype, n_split, append):
     out = P.run_compress(gpu, 97, cap=100)
     lens0 = [[0, 31], [32, 33], [64, 65]]
     announce(f"lengths {lens0} {dtype} n_split={n_split} append={append}")
-    P.run_decode_steps(gpu, out, 3, n_split=n_split, append=append, lens0=lens0)
+    P.run_decode_steps(gpu, out, 3, n_split=n_split, append=append, lens0=lens0,
+                       summary=int(append))
 
 
 # ---------------------------------------------------------------- edge cases
+@pytest.mark.parametrize("summary", [0, 1])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("d", [64, 128])
-def test_ragged_shapes_and_both_head_dims(dtype, d):
-    """N not a multiple of 64, batch 2, GQA 2, both head dims and dtypes."""
+def test_ragged_shapes_and_both_head_dims(dtype, d, summary):
+    """N not a multiple of 64, batch 2, GQA 2, both head dims and dtypes, raw and prepared
+    summary."""
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=d, ctx_len=1000,
                          batch=2, n_q_heads=4, n_kv_heads=2, window=16, budgets=(97,))
-    announce(f"ragged d={d} {dtype}")
+    announce(f"ragged d={d} {dtype} summary={summary}")
     out = P.run_compress(gpu, 97, cap=100)
     for b in range(2):
         for h in range(2):
             P.check_compress_head(cpu, out, b, h, 97)
-    P.run_decode_steps(gpu, out, 3)
+    P.run_decode_steps(gpu, out, 3, summary=summary)
+    P.run_decode_steps(gpu, out, 2, summary=summary, n_split=2)
 
 
 @pytest.mark.parametrize("mi_rounds", [-1, 0, 1])
@@ -191,6 +195,34 @@ def test_zero_key_spread_decode_equals_full_attention_on_gpu():
     assert P.rel_l2(P.h64(res)[0], full) <= 1e-5
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("d", [64, 128])
+def test_prepared_summary_matches_centred_clamped_covariance(dtype, d):
+    """momentkv_prepare_summary against the oracle's S_tilde from the same fp32 moments: the
+    fp32 centring error (a few ulp of |S| + |s_v s_k^T| / n_e), the bf16 hi + lo split
+    (2^-16 of |S_tilde|) and, for entries within that of tau, the clamp decision."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, dtype=dtype, head_dim=d, ctx_len=1500,
+                         batch=2, n_q_heads=4, n_kv_heads=2, window=16, budgets=(97,))
+    out = P.run_compress(gpu, 97, cap=97)
+    prep = mk.momentkv_prepare_summary(out.n_e, out.s_k, out.s_v, out.S, dtype=dtype)
+    torch.cuda.synchronize()
+    if dtype == torch.bfloat16:
+        got = P.h64(prep[:, :, 0]) + P.h64(prep[:, :, 1])
+    else:
+        got = P.h64(prep)
+    tau = 1e-6
+    for b in range(2):
+        for h in range(2):
+            m = P.oracle_moments(out, b, h)
+            _, _, ref = O.centered_moments(m, tau)
+            S, sv, sk = P.h64(out.S[b, h]), P.h64(out.s_v[b, h]), P.h64(out.s_k[b, h])
+            bound = (2.0 ** -16 * np.abs(ref) + 2.0 ** -21 * (np.abs(S) + np.abs(np.outer(sv, sk)) / m.n_e)
+                     + 2 * tau)
+            err = np.abs(got[b, h] - ref)
+            assert np.all(err <= bound), float(np.max(err / bound))
+            assert np.any(ref != 0)
+
+
 # ---------------------------------------------------------------- full-size sampled heads
 @pytest.mark.parametrize("budget", [128, 2048])
 def test_qwen_stack_layer_full_size_sampled_heads(budget):
@@ -202,7 +234,8 @@ def test_qwen_stack_layer_full_size_sampled_heads(budget):
     for h in (0, 5):
         errs = P.check_compress_head(cpu, out, 0, h, budget)
         announce(f"head {h} {errs}")
-    P.run_decode_steps(gpu, out, 2)
+    P.run_decode_steps(gpu, out, 1)
+    P.run_decode_steps(gpu, out, 1, summary=1)
 
 
 def test_ruler_128k_full_size_sampled_head():
