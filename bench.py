@@ -61,6 +61,31 @@ def compress_bytes(n_kv_heads: int, N: int, d: int, L: int, elem: int = 2) -> in
     return n_kv_heads * (2 * N * d * elem + 2 * L * d * elem + 4 * d * d + 8 * d + 4 + 4 * L)
 
 
+def measured_traffic(workload: str, alg_per_call: dict) -> float | None:
+    """HBM bytes per decode call from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary
+    (profiles/traffic_decode_<workload>.md): its measured traffic / algorithmic ratio per
+    budget applied to this run's algorithmic bytes per call, averaged over the budgets.
+    None when there is no summary for the workload or budgets, or when the decode sources
+    differ from the ones the counters were taken with."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"traffic_decode_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(\{.*?\})\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    data = json.loads(m.group(1))
+    h = hashlib.sha256()
+    for src in data["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    ratios = data["traffic_over_algorithmic"]
+    if h.hexdigest() != data["decode_sources_sha256"] or any(str(L) not in ratios for L in alg_per_call):
+        return None
+    return sum(ratios[str(L)] * b for L, b in alg_per_call.items()) / len(alg_per_call)
+
+
 def build_stack(wl, layers, device):
     t0 = time.time()
     data = [synth.make_layer(wl, l, device=device) for l in range(layers)]
@@ -126,6 +151,10 @@ def main() -> int:
     ap.add_argument("--cpu-heads", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one plain copy of "
+                         "known size, then 4 tokens x budgets of eager decode calls; prints "
+                         "the dispatch plan as JSON and exits")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -237,6 +266,25 @@ def main() -> int:
         d1.record()
         return d0, d1
 
+    if args.traffic_probe:
+        compress_phase(None)
+        torch.cuda.synchronize()
+        copy_bytes = 256 << 20
+        src = torch.empty(copy_bytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)                 # calibration: copy_bytes read, copy_bytes written
+        calls = []
+        for t in range(4):
+            for L in budgets:
+                decode_call(t, L)
+                n = min(L, N) + t + 1
+                calls.append({"token": t, "budget": L, "lens_after": n,
+                              "fused": min(L, N) + T <= 384,
+                              "bytes": decode_bytes(LB * Hkv, G, d, n)})
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": copy_bytes, "calls": calls}))
+        return 0
+
     # warm-up, eagerly
     for _ in range(args.warmup):
         compress_phase(None)
@@ -293,6 +341,7 @@ def main() -> int:
         without_ms[L] = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
 
     per_budget = {}
+    alg_per_call = {}
     phase_bytes = 0.0
     dec_ms = [a.elapsed_time(b) for a, b in dec_events]      # one graph replay per step
     dec_s = sum(dec_ms) * 1e-3
@@ -300,6 +349,7 @@ def main() -> int:
         cms = [a.elapsed_time(b) for a, b in timing["compress"][L]]
         dby = sum(decode_bytes(LB * Hkv, G, d, min(L, N) + t + 1) for t in range(T))
         phase_bytes += dby
+        alg_per_call[L] = dby / T
         budget_ms = sum(dec_ms) / len(dec_ms) - without_ms[L]
         per_budget[str(L)] = {
             "compress_ms_per_layer": sum(cms) / len(cms) / layers,
@@ -338,7 +388,8 @@ def main() -> int:
                      "bound": "hbm", "achieved": avg_bytes / avg_launch_s / 1e9,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": avg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS,
-                     "traffic": None, "bytes_per_launch": avg_bytes,
+                     "traffic": measured_traffic(wl.name, alg_per_call),
+                     "bytes_per_launch": avg_bytes,
                      "avg_launch_us": avg_launch_s * 1e6},
         "wall_s_timed": wall,
     }
