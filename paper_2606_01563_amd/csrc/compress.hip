@@ -10,7 +10,7 @@
 //   3 k_mass          per (slice, head): logits again, softmax mass summed over the
 //                     window rows -> a_j, aligned chunk pooling -> abar_j,
 //                     provisional score abar_j ||v_j||.                    [reads K]
-//   4 k_topk_*        per head: radix select of the k_keep best scores, lower position
+//   4 k_tk_*          per head: radix select of the k_keep best scores, lower position
 //                     first on ties; writes the kept positions in ascending order.
 //   5 k_gather_rows   rows of the provisional kept set into a compact buffer.
 //   6 k_cov_rows      their covariance and sums, stored negated as extra partial slots.
@@ -20,7 +20,7 @@
 //                     into LDS (fp32, or a bf16 hi/lo pair), S_tilde k_j on MFMA,
 //                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm.
 //                                                                          [reads K, V]
-//   9 k_topk_*        final kept set.
+//   9 k_tk_*          final kept set.
 //  10 k_gather_out    retained rows (sinks, kept, window) -> k_out/v_out, idx, lens.
 //  11 k_cov_rows      covariance of the final kept rows (from k_out), negated.
 //  12 k_reduce        final raw moments S, s_k, s_v, n_e.
@@ -312,12 +312,13 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
   auto is_cand = [&](int j) { return j >= c_lo && j < c_hi; };
 
   const int t_beg = sl * a.tps1, t_end = min(t_beg + a.tps1, a.ntile);
-  TR R;
-  if (t_beg < t_end) {
-    const int j = t_beg * TILE + p2;
-    tile_load<T, D, NT>(R, Kh, Vh, t_beg * TILE, j < a.N, j + 1 < a.N, is_cand(j), is_cand(j + 1), tid);
-  }
-  for (int t = t_beg; t < t_end; ++t) {
+  // Two tiles in flight: tile t is staged in R[t & 1], and the load of tile t + 2 is issued
+  // into the same registers as soon as tile t has been written to LDS.
+  auto issue = [&](TR& R, int t) {
+    const int j = t * TILE + p2;
+    tile_load<T, D, NT>(R, Kh, Vh, t * TILE, j < a.N, j + 1 < a.N, is_cand(j), is_cand(j + 1), tid);
+  };
+  auto step = [&](TR& R, int t) {
     const int tok0 = t * TILE;
     const bool tile_has_cand = tok0 < c_hi && tok0 + TILE > c_lo;
     {
@@ -337,10 +338,7 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         sVn[wave][p2] = ss0;
         sVn[wave][p2 + 1] = ss1;
       }
-      if (t + 1 < t_end) {  // prefetch the next tile while this one is consumed
-        const int jn = j + TILE;
-        tile_load<T, D, NT>(R, Kh, Vh, tok0 + TILE, jn < a.N, jn + 1 < a.N, is_cand(jn), is_cand(jn + 1), tid);
-      }
+      if (t + 2 < t_end) issue(R, t + 2);
     }
     __syncthreads();
     if (tid < TILE && is_cand(tok0 + tid)) {
@@ -372,21 +370,28 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         for (int nt = 0; nt < 4; ++nt) {
           x[nt] = acc[nt][i] * c2;
           if (need_mask) {
-            const int j = tok0 + 16 * nt + (lane & 15);
-            if (!(j <= lim[k][i] && j < a.N)) x[nt] = -INFINITY;
+            const int jj = tok0 + 16 * nt + (lane & 15);
+            if (!(jj <= lim[k][i] && jj < a.N)) x[nt] = -INFINITY;
           }
         }
+        // branch-free update: with no finite logit yet, shifting by 0 keeps (-inf, 0)
         const float mn = fmaxf(rm[k][i], fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
-        if (mn != -INFINITY) {
-          rl[k][i] = rl[k][i] * fast_exp2(rm[k][i] - mn) +
-                     ((fast_exp2(x[0] - mn) + fast_exp2(x[1] - mn)) +
-                      (fast_exp2(x[2] - mn) + fast_exp2(x[3] - mn)));
-          rm[k][i] = mn;
-        }
+        const float ms = mn == -INFINITY ? 0.f : mn;
+        rl[k][i] = rl[k][i] * fast_exp2(rm[k][i] - ms) +
+                   ((fast_exp2(x[0] - ms) + fast_exp2(x[1] - ms)) +
+                    (fast_exp2(x[2] - ms) + fast_exp2(x[3] - ms)));
+        rm[k][i] = mn;
       }
     }
     if (tile_has_cand) cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
+  };
+  TR R0, R1;
+  if (t_beg < t_end) issue(R0, t_beg);
+  if (t_beg + 1 < t_end) issue(R1, t_beg + 1);
+  for (int t = t_beg; t < t_end; t += 2) {
+    step(R0, t);
+    if (t + 1 < t_end) step(R1, t + 1);
   }
 
   // merge the per-lane row statistics over the 16 lanes holding a row
@@ -545,46 +550,36 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
 // ------------------------------------------------------------------------------------
 // Stage 4/9: per-head selection of the k best scores (ties: lower position first),
 // output in ascending position order.  Scores are non-negative floats, so their bit
-// patterns (bit 31 clear) order like unsigned integers.  One 1024-thread workgroup per
-// head finds the k-th largest key T by radix histograms of bits 30..20, 19..10 and 9..0
-// (each over the keys still matching the prefix), which also gives how many keys equal
-// to T are kept (the lowest positions).  Compaction: each wave owns a contiguous chunk of
-// positions, counts keys > T and == T with ballots, a scan over the 16 waves gives every
-// wave its share of equal keys and its output offset, and a second ballot pass writes the
-// kept positions in order.
-//   keys in LDS (n <= TK_LDS_KEYS, e.g. 32K contexts): the scores are read once, every
-//     pass runs on LDS, one launch;
-//   larger n: k_topk_hist builds the first histogram over slices of all CUs, and the
-//     passes read the (cache-resident) scores eight loads deep.
+// patterns (bit 31 clear) order like unsigned integers ("keys").  Every full pass over a
+// head's keys runs over slices of TKS positions spread over all CUs:
+//   k_tk_hist   slices x heads: histogram of key bits 30..20 per slice;
+//   k_tk_bin    one workgroup per head: sums the slice histograms in a fixed order and
+//               finds the bin B of the k-th largest key and the count of keys above B;
+//   k_tk_cand   slices x heads: counts the slice's keys above B and writes its keys inside
+//               B (the candidates) in position order;
+//   k_tk_write  slices x heads: refines bits 19..10 and 9..0 over the head's candidates
+//               (few: one bin spans an eighth of an octave), which gives the k-th key T and
+//               how many keys equal to T are kept (the lowest positions); from the per-slice
+//               counts it gets its slice's output offset and share of equal keys, then
+//               writes the slice's kept positions in order.
 // ------------------------------------------------------------------------------------
-constexpr int TK_THREADS = 1024;
-constexpr int TK_WAVES = TK_THREADS / 64;
+constexpr int TKS = 2048;          // positions per slice
+constexpr int TKT = 256;           // threads per slice workgroup
+constexpr int TKPT = TKS / TKT;    // consecutive positions per thread
 constexpr int TK_BINS0 = 2048;
-constexpr int TK_LDS_KEYS = 34816;  // 136 KB of keys
-constexpr int TK_UNROLL = 8;
+constexpr int TK_MAX_SLICES = 128; // 262144 candidates
+constexpr int TK_CAND_LDS = 8192;  // candidates of the k-th key's bin staged in LDS
 
 __device__ __forceinline__ uint32_t score_key(float s) {
   uint32_t u = __float_as_uint(s);
   return (u & 0x80000000u) ? 0u : u;  // -0 and negatives sort as 0
 }
 
-__global__ void __launch_bounds__(256) k_topk_hist(const float* __restrict__ scores, int n,
-                                                     int per_slice, uint32_t* __restrict__ hist) {
-  __shared__ uint32_t h[TK_BINS0];
-  const int head = blockIdx.y, sl = blockIdx.x;
-  for (int i = threadIdx.x; i < TK_BINS0; i += 256) h[i] = 0;
-  __syncthreads();
-  const float* s = scores + (size_t)head * n;
-  const int j1 = min(n, (sl + 1) * per_slice);
-  for (int j = sl * per_slice + threadIdx.x; j < j1; j += 256)
-    atomicAdd(&h[score_key(s[j]) >> 20], 1u);
-  __syncthreads();
-  uint32_t* out = hist + ((size_t)head * gridDim.x + sl) * TK_BINS0;
-  for (int i = threadIdx.x; i < TK_BINS0; i += 256) out[i] = h[i];
-}
-
-// Exclusive block scan of one int per thread; the block total goes to *total.
+// Exclusive scan of one int per thread over an NT-thread block; the total goes to *total.
+// sW holds 2 * NT / 64 + 1 ints.
+template <int NT>
 __device__ int block_excl_scan(int x, int* sW, int* total) {
+  constexpr int NW = NT / 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int inc = x;
 #pragma unroll
@@ -595,33 +590,35 @@ __device__ int block_excl_scan(int x, int* sW, int* total) {
   if (lane == 63) sW[wave] = inc;
   __syncthreads();
   if (wave == 0) {
-    int v = lane < TK_WAVES ? sW[lane] : 0;
+    int v = lane < NW ? sW[lane] : 0;
     int vi = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       int y = __shfl_up(vi, o);
       if (lane >= o) vi += y;
     }
-    if (lane < TK_WAVES) sW[TK_WAVES + lane] = vi - v;  // exclusive wave offsets
-    if (lane == TK_WAVES - 1) sW[2 * TK_WAVES] = vi;
+    if (lane < NW) sW[NW + lane] = vi - v;  // exclusive wave offsets
+    if (lane == NW - 1) sW[2 * NW] = vi;
   }
   __syncthreads();
-  const int res = sW[TK_WAVES + wave] + inc - x;
-  *total = sW[2 * TK_WAVES];
+  const int res = sW[NW + wave] + inc - x;
+  *total = sW[2 * NW];
   __syncthreads();
   return res;
 }
 
-// Find, over bins in descending order, the bin where the running count reaches `need`;
-// thread t owns `per` consecutive bins from the top.  Returns (bin, count above it).
+// Over bins in descending order, the bin where the running count reaches `need`
+// (1 <= need <= total); thread t owns nb / NT consecutive bins from the top.  Writes
+// (bin, count above it).
+template <int NT>
 __device__ __forceinline__ void find_bin(const uint32_t* hist, int nb, int need, int* sW,
                                          uint32_t* sh_bin, uint32_t* sh_above) {
   const int tid = threadIdx.x;
-  const int per = nb / TK_THREADS;
+  const int per = nb / NT;
   int c = 0;
   for (int q = 0; q < per; ++q) c += (int)hist[nb - 1 - per * tid - q];
   int tot;
-  int before = block_excl_scan(c, sW, &tot);
+  int before = block_excl_scan<NT>(c, sW, &tot);
   for (int q = 0; q < per; ++q) {
     const int bin = nb - 1 - per * tid - q;
     const int h = (int)hist[bin];
@@ -634,76 +631,176 @@ __device__ __forceinline__ void find_bin(const uint32_t* hist, int nb, int need,
   __syncthreads();
 }
 
-template <bool LDS>
-__global__ void __launch_bounds__(TK_THREADS) k_topk_select(const float* __restrict__ scores, int n,
-                                                              int k, const uint32_t* __restrict__ hist,
-                                                              int n_slices, int32_t* __restrict__ out,
-                                                              int out_stride, int pos_offset) {
-  __shared__ uint32_t keys_lds[LDS ? TK_LDS_KEYS : 1];
+// The TKPT consecutive keys of thread tid in slice sl (positions >= n give valid = false).
+__device__ __forceinline__ void slice_keys(const float* s, int n, int sl, uint32_t (&key)[TKPT],
+                                           bool (&valid)[TKPT]) {
+  const int j0 = sl * TKS + TKPT * threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u) {
+    valid[u] = j0 + u < n;
+    key[u] = valid[u] ? score_key(s[j0 + u]) : 0u;
+  }
+}
+
+__global__ void __launch_bounds__(TKT) k_tk_hist(const float* __restrict__ scores, int n,
+                                                   uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[TK_BINS0];
+  const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x, tid = threadIdx.x;
+  for (int b = tid; b < TK_BINS0; b += TKT) h[b] = 0;
+  __syncthreads();
+  const float* s = scores + (size_t)head * n;
+  float v[TKPT];
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u) {  // coalesced: consecutive threads, consecutive positions
+    const int j = sl * TKS + u * TKT + tid;
+    v[u] = j < n ? s[j] : 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u)
+    if (sl * TKS + u * TKT + tid < n) atomicAdd(&h[score_key(v[u]) >> 20], 1u);
+  __syncthreads();
+  uint32_t* o = hist + ((size_t)head * ntk + sl) * TK_BINS0;
+  for (int b = tid; b < TK_BINS0; b += TKT) o[b] = h[b];
+}
+
+__global__ void __launch_bounds__(1024) k_tk_bin(const uint32_t* __restrict__ hist, int ntk, int k,
+                                                 int* __restrict__ state) {
   __shared__ uint32_t hst[TK_BINS0];
   __shared__ uint32_t sh_bin, sh_above;
-  __shared__ int sW[2 * TK_WAVES + 1];
-  __shared__ int s_gt[TK_WAVES], s_eq[TK_WAVES], s_eqb[TK_WAVES], s_ob[TK_WAVES];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ int sW[2 * 16 + 1];
   const int head = blockIdx.x;
-  const float* s = scores + (size_t)head * n;
-  int32_t* o = out + (size_t)head * out_stride;
-  if (k <= 0) return;
-  auto key = [&](int j) -> uint32_t {
-    if constexpr (LDS) return keys_lds[j];
-    else return score_key(s[j]);
-  };
-
-  // ---- bits 30..20
-  if constexpr (LDS) {
-    for (int base = 0; base < n; base += TK_THREADS * TK_UNROLL) {
-      float v[TK_UNROLL];
+  for (int b = threadIdx.x; b < TK_BINS0; b += 1024) {
+    uint32_t c = 0;
+    for (int s0 = 0; s0 < ntk; s0 += 8) {  // eight slices' loads in flight
+      uint32_t v[8];
 #pragma unroll
-      for (int u = 0; u < TK_UNROLL; ++u) {
-        const int j = base + u * TK_THREADS + tid;
-        v[u] = j < n ? s[j] : 0.f;
-      }
+      for (int u = 0; u < 8; ++u)
+        v[u] = s0 + u < ntk ? hist[((size_t)head * ntk + s0 + u) * TK_BINS0 + b] : 0u;
 #pragma unroll
-      for (int u = 0; u < TK_UNROLL; ++u) {
-        const int j = base + u * TK_THREADS + tid;
-        if (j < n) keys_lds[j] = score_key(v[u]);
-      }
+      for (int u = 0; u < 8; ++u) c += v[u];
     }
-    for (int b = tid; b < TK_BINS0; b += TK_THREADS) hst[b] = 0;
-    __syncthreads();
-    for (int j = tid; j < n; j += TK_THREADS) atomicAdd(&hst[keys_lds[j] >> 20], 1u);
-  } else {
-    for (int b = tid; b < TK_BINS0; b += TK_THREADS) {  // fixed order over the slices
-      uint32_t c = 0;
-      for (int sl = 0; sl < n_slices; ++sl) c += hist[((size_t)head * n_slices + sl) * TK_BINS0 + b];
-      hst[b] = c;
+    hst[b] = c;
+  }
+  __syncthreads();
+  find_bin<1024>(hst, TK_BINS0, k, sW, &sh_bin, &sh_above);
+  if (threadIdx.x == 0) {
+    state[2 * head] = (int)sh_bin;
+    state[2 * head + 1] = (int)sh_above;
+  }
+}
+
+__global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ scores, int n,
+                                                   const int* __restrict__ state,
+                                                   int* __restrict__ cnt, uint32_t* __restrict__ cand) {
+  __shared__ int sW[2 * (TKT / 64) + 1];
+  const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x;
+  const uint32_t B = (uint32_t)state[2 * head];
+  uint32_t key[TKPT];
+  bool valid[TKPT];
+  slice_keys(scores + (size_t)head * n, n, sl, key, valid);
+  int n_gt = 0, n_c = 0;
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u) {
+    n_gt += valid[u] && (key[u] >> 20) > B;
+    n_c += valid[u] && (key[u] >> 20) == B;
+  }
+  int tot_gt, tot_c;
+  block_excl_scan<TKT>(n_gt, sW, &tot_gt);
+  int pos = block_excl_scan<TKT>(n_c, sW, &tot_c);
+  uint32_t* c = cand + ((size_t)head * ntk + sl) * TKS;
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u)
+    if (valid[u] && (key[u] >> 20) == B) c[pos++] = key[u];
+  if (threadIdx.x == 0) {
+    cnt[((size_t)head * ntk + sl) * 2] = tot_gt;
+    cnt[((size_t)head * ntk + sl) * 2 + 1] = tot_c;
+  }
+}
+
+__global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scores, int n, int k,
+                                                    const int* __restrict__ state,
+                                                    const int* __restrict__ cnt,
+                                                    const uint32_t* __restrict__ cand,
+                                                    int32_t* __restrict__ out, int out_stride,
+                                                    int pos_offset) {
+  __shared__ int s_gt[TK_MAX_SLICES], s_cn[TK_MAX_SLICES], s_gtT[TK_MAX_SLICES], s_eqT[TK_MAX_SLICES];
+  __shared__ uint32_t hst[1024];
+  __shared__ uint32_t sh_bin, sh_above;
+  __shared__ int sW[2 * (TKT / 64) + 1];
+  __shared__ int s_off, s_eqb;
+  __shared__ int s_start[TK_MAX_SLICES + 1];
+  __shared__ uint32_t c_key[TK_CAND_LDS];
+  __shared__ uint8_t c_sl[TK_CAND_LDS];
+  const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x, tid = threadIdx.x;
+  // the slice's own keys are needed last but depend on nothing: requested first
+  uint32_t key[TKPT];
+  bool valid[TKPT];
+  slice_keys(scores + (size_t)head * n, n, sl, key, valid);
+  const uint32_t B = (uint32_t)state[2 * head];
+  const int above = state[2 * head + 1];
+  for (int i = tid; i < ntk; i += TKT) {
+    s_gt[i] = cnt[((size_t)head * ntk + i) * 2];
+    s_cn[i] = cnt[((size_t)head * ntk + i) * 2 + 1];
+    s_gtT[i] = 0;
+    s_eqT[i] = 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int i = 0; i < ntk; ++i) { s_start[i] = acc; acc += s_cn[i]; }
+    s_start[ntk] = acc;
+  }
+  __syncthreads();
+  // The head's candidates, flattened in slice order, go to LDS with all loads in flight
+  // (a flat index finds its slice by bisection over the slice starts); past TK_CAND_LDS
+  // candidates the passes read them from global memory instead.
+  const int m = s_start[ntk];
+  const bool in_lds = m <= TK_CAND_LDS;
+  if (in_lds) {
+    for (int f0 = 0; f0 < m; f0 += TKT * 8) {
+      uint32_t v[8];
+      int vs[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int f = f0 + u * TKT + tid;
+        int lo = 0, hi = ntk;  // s_start[lo] <= f < s_start[hi]
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (s_start[mid] <= f) lo = mid; else hi = mid;
+        }
+        vs[u] = lo;
+        v[u] = f < m ? cand[((size_t)head * ntk + lo) * TKS + (f - s_start[lo])] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int f = f0 + u * TKT + tid;
+        if (f < m) { c_key[f] = v[u]; c_sl[f] = (uint8_t)vs[u]; }
+      }
     }
   }
   __syncthreads();
-  find_bin(hst, TK_BINS0, k, sW, &sh_bin, &sh_above);
-  uint32_t prefix = sh_bin << 20, mask = 0x7FF00000u;
-  int remaining = k - (int)sh_above;
-  __syncthreads();
-  // ---- bits 19..10, then 9..0, over the keys that still match
-  for (int pass = 0; pass < 2; ++pass) {
-    const int shift = pass == 0 ? 10 : 0;
-    for (int i = tid; i < 1024; i += TK_THREADS) hst[i] = 0;
-    __syncthreads();
-    for (int base = 0; base < n; base += TK_THREADS * TK_UNROLL) {
-      uint32_t kk[TK_UNROLL];
-#pragma unroll
-      for (int u = 0; u < TK_UNROLL; ++u) {
-        const int j = base + u * TK_THREADS + tid;
-        kk[u] = j < n ? key(j) : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < TK_UNROLL; ++u) {
-        const int j = base + u * TK_THREADS + tid;
-        if (j < n && (kk[u] & mask) == prefix) atomicAdd(&hst[(kk[u] >> shift) & 1023u], 1u);
+  auto for_each_cand = [&](auto&& fn) {
+    if (in_lds) {
+      for (int f = tid; f < m; f += TKT) fn(c_key[f], (int)c_sl[f]);
+    } else {
+      for (int s2 = 0; s2 < ntk; ++s2) {
+        const uint32_t* c = cand + ((size_t)head * ntk + s2) * TKS;
+        for (int i = tid; i < s_cn[s2]; i += TKT) fn(c[i], s2);
       }
     }
+  };
+  // bits 19..10, then 9..0, over the candidates (all of them have bits 30..20 = B)
+  uint32_t prefix = B << 20, mask = 0x7FF00000u;
+  int remaining = k - above;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int shift = pass == 0 ? 10 : 0;
+    for (int i = tid; i < 1024; i += TKT) hst[i] = 0;
     __syncthreads();
-    find_bin(hst, 1024, remaining, sW, &sh_bin, &sh_above);
+    for_each_cand([&](uint32_t key, int) {
+      if ((key & mask) == prefix) atomicAdd(&hst[(key >> shift) & 1023u], 1u);
+    });
+    __syncthreads();
+    find_bin<TKT>(hst, 1024, remaining, sW, &sh_bin, &sh_above);
     prefix |= sh_bin << shift;
     mask |= 1023u << shift;
     remaining -= (int)sh_above;
@@ -711,60 +808,44 @@ __global__ void __launch_bounds__(TK_THREADS) k_topk_select(const float* __restr
   }
   const uint32_t T = prefix;
   const int need = remaining;  // keys equal to T to keep (>= 1), the lowest positions
-
-  // ---- ordered compaction over wave chunks of CH positions
-  const int CH = ((n + TK_WAVES * 64 - 1) / (TK_WAVES * 64)) * 64;
-  const int c0 = wave * CH, c1 = min(n, c0 + CH);
-  const unsigned long long below = (1ull << lane) - 1ull;
-  int n_gt = 0, n_eq = 0;
-  for (int g0 = c0; g0 < c1; g0 += 64 * TK_UNROLL) {
-    uint32_t kk[TK_UNROLL];
-#pragma unroll
-    for (int u = 0; u < TK_UNROLL; ++u) {
-      const int j = g0 + 64 * u + lane;
-      kk[u] = j < c1 ? key(j) : 0u;
-    }
-#pragma unroll
-    for (int u = 0; u < TK_UNROLL; ++u) {
-      const bool v = g0 + 64 * u + lane < c1;
-      n_gt += __popcll(__ballot(v && kk[u] > T));
-      n_eq += __popcll(__ballot(v && kk[u] == T));
-    }
-  }
-  if (lane == 0) { s_gt[wave] = n_gt; s_eq[wave] = n_eq; }
+  // per slice: candidates above T and equal to T
+  for_each_cand([&](uint32_t key, int s2) {
+    if (key > T) atomicAdd(&s_gtT[s2], 1);
+    else if (key == T) atomicAdd(&s_eqT[s2], 1);
+  });
   __syncthreads();
-  if (tid == 0) {
+  if (tid == 0) {  // fixed order over the slices
     int eb = 0, ob = 0;
-    for (int w = 0; w < TK_WAVES; ++w) {
-      s_eqb[w] = eb;
-      s_ob[w] = ob;
-      ob += s_gt[w] + min(max(need - eb, 0), s_eq[w]);
-      eb += s_eq[w];
+    for (int s2 = 0; s2 < ntk; ++s2) {
+      if (s2 == sl) { s_off = ob; s_eqb = eb; }
+      ob += s_gt[s2] + s_gtT[s2] + min(max(need - eb, 0), s_eqT[s2]);
+      eb += s_eqT[s2];
     }
   }
   __syncthreads();
-  int eqb = s_eqb[wave], ob = s_ob[wave];
-  for (int g0 = c0; g0 < c1; g0 += 64 * TK_UNROLL) {
-    uint32_t kk[TK_UNROLL];
+  // the slice's kept positions, in order
+  int n_eq = 0;
 #pragma unroll
-    for (int u = 0; u < TK_UNROLL; ++u) {
-      const int j = g0 + 64 * u + lane;
-      kk[u] = j < c1 ? key(j) : 0u;
-    }
+  for (int u = 0; u < TKPT; ++u) n_eq += valid[u] && key[u] == T;
+  int tot;
+  int eq_rank = s_eqb + block_excl_scan<TKT>(n_eq, sW, &tot);
+  bool keep[TKPT];
+  int n_keep = 0;
 #pragma unroll
-    for (int u = 0; u < TK_UNROLL; ++u) {
-      const int j = g0 + 64 * u + lane;
-      const bool v = j < c1;
-      const bool eq = v && kk[u] == T;
-      const unsigned long long em = __ballot(eq);
-      const bool keep = (v && kk[u] > T) || (eq && eqb + __popcll(em & below) < need);
-      const unsigned long long km = __ballot(keep);
-      if (keep) {
-        const int p = ob + __popcll(km & below);
-        if (p < k) o[p] = j + pos_offset;
-      }
-      ob += __popcll(km);
-      eqb += __popcll(em);
+  for (int u = 0; u < TKPT; ++u) {
+    const bool eq = valid[u] && key[u] == T;
+    keep[u] = (valid[u] && key[u] > T) || (eq && eq_rank < need);
+    eq_rank += eq;
+    n_keep += keep[u];
+  }
+  int p = s_off + block_excl_scan<TKT>(n_keep, sW, &tot);
+  int32_t* o = out + (size_t)head * out_stride;
+  const int j0 = sl * TKS + TKPT * tid;
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u) {
+    if (keep[u]) {
+      if (p < k) o[p] = j0 + u + pos_offset;
+      ++p;
     }
   }
 }
@@ -1084,17 +1165,18 @@ __global__ void __launch_bounds__(256) k_zero_moments(CompressArgs a) {
 static hipError_t launch_topk(const CompressArgs& a, const float* scores, int32_t* out,
                               hipStream_t st) {
   if (a.k_keep <= 0) return hipSuccess;
-  if (a.n_c <= TK_LDS_KEYS) {
-    hipLaunchKernelGGL(k_topk_select<true>, dim3(a.H), dim3(TK_THREADS), 0, st, scores, a.n_c,
-                       a.k_keep, (const uint32_t*)nullptr, 0, out, a.kmax, a.n_s);
-    MKV_CHECK_LAUNCH();
-    return hipSuccess;
-  }
-  hipLaunchKernelGGL(k_topk_hist, dim3(a.ntk, a.H), dim3(256), 0, st, scores, a.n_c, a.tk_per,
-                     a.tk_hist);
+  const dim3 grid(a.ntk, a.H);
+  hipLaunchKernelGGL(k_tk_hist, grid, dim3(TKT), 0, st, scores, a.n_c, a.tk_hist);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_topk_select<false>, dim3(a.H), dim3(TK_THREADS), 0, st, scores, a.n_c,
-                     a.k_keep, (const uint32_t*)a.tk_hist, a.ntk, out, a.kmax, a.n_s);
+  hipLaunchKernelGGL(k_tk_bin, dim3(a.H), dim3(1024), 0, st, (const uint32_t*)a.tk_hist, a.ntk,
+                     a.k_keep, a.tk_state);
+  MKV_CHECK_LAUNCH();
+  hipLaunchKernelGGL(k_tk_cand, grid, dim3(TKT), 0, st, scores, a.n_c, (const int*)a.tk_state,
+                     a.tk_cnt, a.tk_cand);
+  MKV_CHECK_LAUNCH();
+  hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep,
+                     (const int*)a.tk_state, (const int*)a.tk_cnt, (const uint32_t*)a.tk_cand, out,
+                     a.kmax, a.n_s);
   MKV_CHECK_LAUNCH();
   return hipSuccess;
 }

@@ -279,6 +279,16 @@ struct BlockAttn {
     }
   }
 
+  // V rows of the block at j0 at or past t_end to zero (K rows there only feed masked logits)
+  __device__ __forceinline__ void clear_v_past_end(int j0, int lane) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const bool ok = j0 + 2 * (lane & 15) + hh < t_end;
+#pragma unroll
+      for (int c = 0; c < NVC; ++c) vf[hh][c] = ok ? vf[hh][c] : zero_frag<T>();
+    }
+  }
+
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
@@ -517,13 +527,18 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   const QueryCols<CPL> qc = load_query_cols<T, D>(a, head, min(wave, G - 1), lane);
   const int ne = a.n_e[head];
 
-  const HeadLen hl = head_len(a, a.lens[head]);
   BA ba;
   ba.kc = reinterpret_cast<const T*>(a.k_cache) + (size_t)head * a.cap * D;
   ba.vc = reinterpret_cast<const T*>(a.v_cache) + (size_t)head * a.cap * D;
-  ba.t_end = hl.cache_len;
   ba.init();
+  // The wave's first block is requested together with lens, bounded by the capacity only
+  // (rows 32w.. exist whatever lens is); once lens is known, V rows at or past it are
+  // cleared (they may hold any bits) and their logits are masked like any row past t_end.
+  ba.t_end = a.cap;
   ba.load(BA::TB * wave, lane);
+  const HeadLen hl = head_len(a, a.lens[head]);
+  ba.t_end = hl.cache_len;
+  if (BA::TB * (wave + 1) > ba.t_end) ba.clear_v_past_end(BA::TB * wave, lane);
   if (wave == 0 && lane == 0 && a.k_new != nullptr && !hl.can_append) atomicOr(a.flag, 1);
   if (wave == 3 && hl.can_append) append_row<T, D>(a, head, hl.old_len, lane);
   if (sq_rows) sq.compute(a, qf, 32 * wave, lane, s_sq);

@@ -62,7 +62,10 @@ struct CompressArgs {
   float* score;             // [H, n_c]          moment-round score
   int32_t* kept0;           // [H, kmax]         provisional kept positions (ascending)
   int32_t* kept;            // [H, kmax]         final kept positions (ascending)
-  uint32_t* tk_hist;        // [H, ntk, 2048]    top-k histograms of the key's top bits
+  uint32_t* tk_hist;        // [H, ntk, 2048]    top-k: histograms of key bits 30..20
+  int32_t* tk_state;        // [H, 2]            top-k: bin of the k-th key, count above it
+  int32_t* tk_cnt;          // [H, ntk, 2]       top-k: per slice, keys above the bin, in it
+  uint32_t* tk_cand;        // [H, ntk, 2048]    top-k: per slice, the keys in the bin
   float* spart;             // [H, nslot, D, D]  covariance partials
   float* svkpart;           // [H, nslot, 2, D]  (s_v, s_k) partials
   float* s0;                // [H, D, D]         raw S of the provisional evicted set
@@ -82,7 +85,7 @@ struct CompressArgs {
   int nslr, tpsr;           // downdate covariance pass over k_keep rows
   int nslot;                // nsl1 + nslr
   int nsl3, tps3;           // residual pass: slices over candidate tiles of 64
-  int ntk, tk_per;          // top-k histogram slices and keys per slice
+  int ntk;                  // top-k slices of 2048 candidates
   float scale, tau;
 };
 

@@ -12,7 +12,7 @@
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kMaxCandidates = 1 << 18;  // top-k bitmaps live in LDS (2 x 32 KB)
+constexpr int kMaxCandidates = 1 << 18;  // top-k: at most 128 slices of 2048 candidates
 constexpr int64_t kDecodeWaves = 768;      // target slice count of an automatic decode split
 constexpr int64_t kMaxDecodeWaves = 1 << 24;  // decode grid limit (single-wave workgroups)
 constexpr int kFusedMaxLen = 384;          // automatic decode: single launch up to this length
@@ -114,9 +114,8 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
     a.tps3 = ceil_div(nu, a.nsl3);
     a.nsl3 = ceil_div(nu, a.tps3);
   }
-  // top-k histogram slices: about 4096 keys each, at most 32
-  a.ntk = clampi(ceil_div(a.n_c > 0 ? a.n_c : 1, 4096), 1, 32);
-  a.tk_per = ceil_div(a.n_c > 0 ? a.n_c : 1, a.ntk);
+  // top-k slices of 2048 candidates (at most 128 for kMaxCandidates)
+  a.ntk = ceil_div(a.n_c > 0 ? a.n_c : 1, 2048);
   const size_t H = a.H, D = a.D, es = elem_size(p->dtype);
   const size_t nc = a.n_c > 0 ? a.n_c : 1;
   Carver c;
@@ -130,6 +129,9 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.kept0 = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
   a.kept = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
   a.tk_hist = c.take<uint32_t>(H * a.ntk * 2048 * sizeof(uint32_t));
+  a.tk_state = c.take<int32_t>(H * 2 * sizeof(int32_t));
+  a.tk_cnt = c.take<int32_t>(H * a.ntk * 2 * sizeof(int32_t));
+  a.tk_cand = c.take<uint32_t>(H * a.ntk * 2048 * sizeof(uint32_t));
   a.spart = c.take<float>(H * a.nslot * D * D * sizeof(float));
   a.svkpart = c.take<float>(H * a.nslot * 2 * D * sizeof(float));
   a.s0 = c.take<float>(H * D * D * sizeof(float));
