@@ -69,9 +69,9 @@ def check_compress_head(inp_cpu: dict, out: mk.CompressOutput, b: int, h: int, b
     """Full protocol for one (sequence, KV head).  Returns a dict of measured errors."""
     dt = inp_cpu["k"].dtype
     tol, band = TOL[dt], SEL_BAND[dt]
-    q = h64(inp_cpu["q_win"])
-    K = h64(inp_cpu["k"])[b, h]
-    V = h64(inp_cpu["v"])[b, h]
+    q = h64(inp_cpu["q_win"][b:b + 1])   # one sequence, converted after slicing
+    K = h64(inp_cpu["k"][b, h])
+    V = h64(inp_cpu["v"][b, h])
     Hkv = inp_cpu["k"].shape[1]
     G = q.shape[1] // Hkv
     N, d = K.shape
@@ -111,7 +111,7 @@ def check_compress_head(inp_cpu: dict, out: mk.CompressOutput, b: int, h: int, b
         if mi_rounds >= 1:
             check_selection_against_own_scores(s1_g, kept, k_keep, n_sink)
     # 2. scores against the oracle (moment round fed the GPU's provisional set)
-    ref = O.compress_head(q[b, h * G:(h + 1) * G], K, V, budget, n_sink=n_sink, chunk=chunk,
+    ref = O.compress_head(q[0, h * G:(h + 1) * G], K, V, budget, n_sink=n_sink, chunk=chunk,
                           mi_rounds=mi_rounds, tau=tau,
                           r0_override=kept0 if (mi_rounds >= 1 and k_keep > 0) else None)
     if check_oracle_scores:
@@ -126,7 +126,7 @@ def check_compress_head(inp_cpu: dict, out: mk.CompressOutput, b: int, h: int, b
         # 3. sets equal the oracle's up to near-ties
         if k_keep > 0:
             if mi_rounds >= 1:
-                ref_own = O.compress_head(q[b, h * G:(h + 1) * G], K, V, budget, n_sink=n_sink,
+                ref_own = O.compress_head(q[0, h * G:(h + 1) * G], K, V, budget, n_sink=n_sink,
                                           chunk=chunk, mi_rounds=0, tau=tau)
                 errs["swaps0"] = check_set_near_ties(kept0, ref_own.sigma0, k_keep, n_sink, band)
                 errs["swaps"] = check_set_near_ties(kept, ref.sigma, k_keep, n_sink, band)

@@ -238,6 +238,19 @@ def test_qwen_stack_layer_full_size_sampled_heads(budget):
     P.run_decode_steps(gpu, out, 1, summary=1)
 
 
+def test_llama_stack_batch8_needles_full_size_sampled_heads():
+    """One 32K-context layer of the LLaMA-3.1-8B-shaped stack with 8 sequences and
+    planted-needle queries at budget 256: 64 KV heads compressed in one call, sampled
+    (sequence, head) pairs checked, then decode with the prepared summary."""
+    wl, cpu, gpu = layer("llama31_8b_stack_b8_n32768", layer_idx=5, steps=2)
+    announce(f"{wl.name} B={wl.batch}")
+    out = P.run_compress(gpu, 256, cap=258)
+    for b, h in ((0, 0), (3, 5), (7, 7)):
+        errs = P.check_compress_head(cpu, out, b, h, 256)
+        announce(f"seq {b} head {h} {errs}")
+    P.run_decode_steps(gpu, out, 2, summary=1)
+
+
 def test_ruler_128k_full_size_sampled_head():
     wl, cpu, gpu = layer("ruler_n131072", layer_idx=0, steps=1)
     announce(f"{wl.name}")
