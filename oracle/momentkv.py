@@ -26,6 +26,12 @@ Pinning status (what fixes each function other than itself; see tests/):
   decode                  pinned: no-eviction == SDPA, zero key spread == full
                           attention, second-order error, Jensen bound, weight bias
   greedy_evict            quality reference only (parity unpinned; no printed example)
+  evict_scores_head       pinned: planted zero-residual token, alpha ordering at equal
+                          residual norms, n_e = 0 reduction to alpha ||v||
+  decode_evict            pinned: zero key spread (evicts the value nearest the mean and
+                          still equals full attention over every token seen), moments
+                          equal brute-force sums over everything evicted, token
+                          conservation, Phase 2 on the post-eviction state
 """
 from __future__ import annotations
 
@@ -42,7 +48,7 @@ __all__ = [
     "centered_moments", "moment_residuals", "residual_scores", "select_candidates",
     "compress", "compress_head",
     "decode", "decode_head", "append_tokens", "attention_parts", "greedy_evict",
-    "moment_storage_bytes",
+    "evict_scores_head", "decode_evict_head", "decode_evict", "moment_storage_bytes",
 ]
 
 
@@ -492,6 +498,118 @@ def greedy_evict(alpha, k, v, protected, budget: int, scale: float | None = None
         alive[j] = False
         m = Moments(m.n_e + 1, m.s_k + K[j], m.s_v + V[j], m.S + np.outer(V[j], K[j]))
     return np.nonzero(alive)[0], m
+
+
+# --------------------------------------------------------------------------------------
+# Decode-time eviction: Algorithm 1 Phase 1 run at every generated token, then Phase 2
+# --------------------------------------------------------------------------------------
+def evict_scores_head(q, k, v, m: Moments, *, scale: float, tau: float = 1e-6):
+    """Phase 1 scores of every retained row for the current decode query group.
+
+    q: [G, d] queries of the G query heads sharing the KV head; k, v: [n, d] the
+    retained rows (the appended token included).  alpha_g = softmax_j(scale q_g^T k_j)
+    over the n rows (Algorithm 1, the softmax before the residual loop); with grouped
+    queries alpha_j is the mean of the G heads' weights (reading: the same group mean
+    as the window mass).  r_j is the moment residual of Sec. 4.2 Eq. residual under the
+    current summary, score_j = alpha_j ||r_j|| (low = safe to evict).
+    Returns (score, alpha, ||r||), each [n].
+    """
+    Q = np.atleast_2d(_f64(q))
+    K = _f64(k)
+    s = scale * (K @ Q.T)                       # [n, G]
+    e = np.exp(s - s.max(axis=0, keepdims=True))
+    alpha = (e / e.sum(axis=0, keepdims=True)).mean(axis=1)
+    r = moment_residuals(K, v, m, scale, tau)
+    rn = np.sqrt((r * r).sum(axis=1))
+    return alpha * rn, alpha, rn
+
+
+def decode_evict_head(q, k_cache, v_cache, length: int, k_new, v_new, m: Moments,
+                      budget: int, *, scale: float | None = None, tau: float = 1e-6,
+                      order: int = 1, forced: int | None = None) -> dict:
+    """One decoding step of Algorithm 1 for one KV head and its G query heads.
+
+    1. The new key/value joins R in slot `length` (Algorithm 1, before Phase 1).
+    2. Phase 1 (reading: one eviction per call, the loop's single pass when R held at
+       most `budget` rows before the append): if more than `budget` rows are retained,
+       score them (evict_scores_head), evict the argmin (the lowest slot among equal
+       scores) or the slot `forced`, and fold it into the summary by the rank-one update
+       of App. A.1 Eq. app_update.  The last retained row moves into the freed slot
+       (R is a set; this fixes the slot layout that a cache in memory keeps).
+    3. Phase 2: corrected attention of every query over the new R and summary
+       (decode_head).
+    k_cache, v_cache: [cap, d] (copied, not modified).  Returns a dict with out [G, d],
+    log_Z_R [G], w_R [G], k_cache, v_cache, length, moments (after the step), evicted
+    (the slot, or -1) and score / alpha / rnorm over the slots scored (or None).
+    """
+    Q = np.atleast_2d(_f64(q))
+    G, d = Q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    kc = _f64(k_cache).copy()
+    vc = _f64(v_cache).copy()
+    if length >= kc.shape[0]:
+        raise ValueError("cache full")
+    kc[length] = _f64(k_new)
+    vc[length] = _f64(v_new)
+    n = length + 1
+    evicted, score, alpha, rn = -1, None, None, None
+    if n > budget:
+        score, alpha, rn = evict_scores_head(Q, kc[:n], vc[:n], m, scale=scale, tau=tau)
+        evicted = int(np.argmin(score)) if forced is None else int(forced)
+        kj, vj = kc[evicted].copy(), vc[evicted].copy()
+        m = Moments(m.n_e + 1, m.s_k + kj, m.s_v + vj, m.S + np.outer(vj, kj))
+        kc[evicted] = kc[n - 1]
+        vc[evicted] = vc[n - 1]
+        n -= 1
+    out = np.zeros((G, d), F64)
+    lz = np.zeros(G, F64)
+    wr = np.zeros(G, F64)
+    for g in range(G):
+        r = decode_head(Q[g], kc[:n], vc[:n], m, scale=scale, tau=tau, order=order)
+        out[g], lz[g], wr[g] = r.out, r.log_Z_R, r.w_R
+    return dict(out=out, log_Z_R=lz, w_R=wr, k_cache=kc, v_cache=vc, length=n, moments=m,
+                evicted=evicted, score=score, alpha=alpha, rnorm=rn)
+
+
+def decode_evict(q, k_cache, v_cache, lens, moments, k_new, v_new, budget: int, *,
+                 scale: float | None = None, tau: float = 1e-6, order: int = 1,
+                 forced=None):
+    """Batched decode_evict_head over every (sequence, KV head).
+
+    q: [B, Hq, d]; k_cache, v_cache: [B, Hkv, cap, d]; lens: [B, Hkv]; moments: nested
+    [B][Hkv] Moments; k_new, v_new: [B, Hkv, d]; forced: optional [B, Hkv] slots to
+    evict in place of the argmin (-1 or None entries: the argmin).
+    Returns (out [B,Hq,d], log_Z_R [B,Hq], w_R [B,Hq],
+             (k_cache', v_cache', lens', moments'), evicted [B,Hkv], per-head dicts).
+    """
+    Q = _f64(q)
+    B, Hq, d = Q.shape
+    kc = _f64(k_cache).copy()
+    vc = _f64(v_cache).copy()
+    ln = np.asarray(lens, dtype=np.int64).copy()
+    Hkv = kc.shape[1]
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, d), F64)
+    lz = np.zeros((B, Hq), F64)
+    wr = np.zeros((B, Hq), F64)
+    ev = np.full((B, Hkv), -1, np.int64)
+    mom = [[None] * Hkv for _ in range(B)]
+    heads = [[None] * Hkv for _ in range(B)]
+    for b in range(B):
+        for h in range(Hkv):
+            f = None if forced is None or forced[b][h] < 0 else int(forced[b][h])
+            r = decode_evict_head(Q[b, h * G:(h + 1) * G], kc[b, h], vc[b, h], int(ln[b, h]),
+                                  _f64(k_new)[b, h], _f64(v_new)[b, h], moments[b][h], budget,
+                                  scale=scale, tau=tau, order=order, forced=f)
+            out[b, h * G:(h + 1) * G] = r["out"]
+            lz[b, h * G:(h + 1) * G] = r["log_Z_R"]
+            wr[b, h * G:(h + 1) * G] = r["w_R"]
+            kc[b, h], vc[b, h], ln[b, h] = r["k_cache"], r["v_cache"], r["length"]
+            mom[b][h] = r["moments"]
+            ev[b, h] = r["evicted"]
+            heads[b][h] = r
+    return out, lz, wr, (kc, vc, ln, mom), ev, heads
 
 
 def moment_storage_bytes(n_layers: int, n_kv_heads: int, head_dim: int,

@@ -55,6 +55,19 @@ MUTANTS = {
     "moment_round_uses_retained": ("evicted = np.setdiff1d(everyone, kept)",
                                    "evicted = kept"),
     "moment_round_skipped": ("kept = np.sort(select_top(sigma, k_keep))", "pass"),
+    "evict_softmax_over_queries": ("alpha = (e / e.sum(axis=0, keepdims=True)).mean(axis=1)",
+                                   "alpha = (e / e.sum(axis=1, keepdims=True)).mean(axis=1)"),
+    "evict_alpha_max_not_mean": ("alpha = (e / e.sum(axis=0, keepdims=True)).mean(axis=1)",
+                                 "alpha = (e / e.sum(axis=0, keepdims=True)).max(axis=1)"),
+    "evict_score_unweighted": ("return alpha * rn, alpha, rn", "return rn, alpha, rn"),
+    "evict_argmax": ("evicted = int(np.argmin(score)) if forced is None else int(forced)",
+                     "evicted = int(np.argmax(score)) if forced is None else int(forced)"),
+    "evict_update_outer_swapped": ("m = Moments(m.n_e + 1, m.s_k + kj, m.s_v + vj, m.S + np.outer(vj, kj))",
+                                   "m = Moments(m.n_e + 1, m.s_k + kj, m.s_v + vj, m.S + np.outer(kj, vj))"),
+    "evict_update_no_count": ("m = Moments(m.n_e + 1, m.s_k + kj, m.s_v + vj, m.S + np.outer(vj, kj))",
+                              "m = Moments(m.n_e, m.s_k + kj, m.s_v + vj, m.S + np.outer(vj, kj))"),
+    "evict_no_slot_move": ("        kc[evicted] = kc[n - 1]\n", "\n"),
+    "evict_at_budget": ("    if n > budget:\n", "    if n >= budget:\n"),
 }
 
 PIN_TESTS = [name for name in dir(pins) if name.startswith("test_")]

@@ -467,3 +467,156 @@ def test_corrected_output_beats_retained_only_on_average():
         dec = O.decode_head(qq, r.k_out, r.v_out, r.moments)
         gains.append(np.linalg.norm(full - dec.f_R) - np.linalg.norm(full - dec.out))
     assert np.mean(gains) > 0
+
+
+# ------------------------------------------------------------ decode-time eviction
+def _evict_case(rng, d=6, G=2, n_hist=9, L=7, key=None):
+    """History of n_hist evicted tokens (their moments) and L retained rows in a cache of
+    L+3 slots, plus a new token.  key: a shared key for every token (zero spread)."""
+    def keys(n):
+        return np.tile(key, (n, 1)) if key is not None else rng.normal(size=(n, d))
+    KE, VE = keys(n_hist), rng.normal(size=(n_hist, d))
+    m = O.evicted_moments(KE, VE, np.arange(n_hist))
+    kc = np.zeros((L + 3, d))
+    vc = np.zeros((L + 3, d))
+    kc[:L], vc[:L] = keys(L), rng.normal(size=(L, d))
+    k_new, v_new = keys(1)[0], rng.normal(size=d)
+    q = rng.normal(size=(G, d))
+    return q, kc, vc, m, k_new, v_new, (KE, VE)
+
+
+def test_evict_zero_key_spread_evicts_value_nearest_mean_and_stays_exact():
+    """Every key equal: S_tilde = 0 and alpha is uniform, so score_j is ||v_j - v_bar||
+    up to a constant and the step evicts the retained value nearest the evicted mean
+    (brute force).  After the rank-one update the corrected output is still exact full
+    attention over every token seen, i.e. the plain mean of all values."""
+    rng = np.random.default_rng(40)
+    d, L = 6, 7
+    key = rng.normal(size=d)
+    q, kc, vc, m, k_new, v_new, (KE, VE) = _evict_case(rng, d=d, L=L, key=key)
+    r = O.decode_evict_head(q, kc, vc, L, k_new, v_new, m, L)
+    rows = [vc[i] for i in range(L)] + [v_new]
+    v_bar = VE.mean(axis=0)
+    dist = [math.sqrt(sum((a - b) ** 2 for a, b in zip(row, v_bar))) for row in rows]
+    want = min(range(len(dist)), key=lambda i: (dist[i], i))
+    assert r["evicted"] == want
+    assert r["length"] == L
+    every = np.vstack([VE] + rows)
+    for g in range(q.shape[0]):
+        np.testing.assert_allclose(r["out"][g], every.mean(axis=0), rtol=1e-10, atol=1e-12)
+    assert r["moments"].n_e == len(VE) + 1
+
+
+def test_evict_scores_follow_softmax_weights_at_equal_residual_norms():
+    """With an empty summary r_j = v_j; values of equal norm make the score the group-mean
+    softmax weight alone (torch softmax over the rows of each query), so the evicted
+    row is the least attended on average."""
+    rng = np.random.default_rng(41)
+    d, G, L = 8, 3, 11
+    for trial in range(6):
+        q = rng.normal(size=(G, d)) * 2.0
+        kc = np.zeros((L + 2, d))
+        vc = np.zeros((L + 2, d))
+        kc[:L] = rng.normal(size=(L, d))
+        V = rng.normal(size=(L + 1, d))
+        V /= np.linalg.norm(V, axis=1, keepdims=True)
+        vc[:L] = V[:L]
+        k_new = rng.normal(size=d)
+        r = O.decode_evict_head(q, kc, vc, L, k_new, V[L], O.Moments.zeros(d), L)
+        K = np.vstack([kc[:L], k_new[None]])
+        logits = torch.from_numpy(K @ q.T / math.sqrt(d))          # [n, G]
+        alpha = torch.softmax(logits, dim=0).mean(dim=1).numpy()
+        want = int(np.argmin(alpha))
+        assert r["evicted"] == want, trial
+        np.testing.assert_allclose(r["alpha"], alpha, rtol=1e-12)
+        np.testing.assert_allclose(r["rnorm"], 1.0, rtol=1e-12)
+
+
+def test_evict_equal_scores_evict_lowest_slot():
+    """Two identical rows share the minimal score: the lower slot is evicted and the
+    last row moves into it."""
+    rng = np.random.default_rng(42)
+    d, L = 5, 6
+    q, kc, vc, m, k_new, v_new, _ = _evict_case(rng, d=d, G=1, L=L)
+    vc[:L] *= 4.0
+    kc[2], vc[2] = k_new, v_new * 0.01        # rows 2 and L (the new one) are twins
+    v_new = v_new * 0.01
+    r = O.decode_evict_head(q, kc, vc, L, k_new, v_new, O.Moments.zeros(d), L)
+    s = r["score"]
+    assert s[2] == s[L] and s[2] == s.min()
+    assert r["evicted"] == 2
+    np.testing.assert_array_equal(r["v_cache"][2], v_new)
+
+
+def test_evict_without_overflow_is_plain_decode_with_append():
+    """While the cache holds fewer than `budget` rows nothing is evicted and the step is
+    the corrected decode with the append."""
+    rng = np.random.default_rng(43)
+    d, G, L = 6, 2, 7
+    q, kc, vc, m, k_new, v_new, _ = _evict_case(rng, d=d, G=G, L=L)
+    r = O.decode_evict_head(q, kc, vc, L, k_new, v_new, m, L + 1)
+    assert r["evicted"] == -1 and r["length"] == L + 1
+    out, lz, wr, _ = O.decode(q[None], kc[None, None], vc[None, None], np.array([[L]]),
+                              [[m]], k_new=k_new[None, None], v_new=v_new[None, None])
+    np.testing.assert_allclose(r["out"], out[0], rtol=1e-13)
+    np.testing.assert_allclose(r["w_R"], wr[0], rtol=1e-13)
+
+
+def test_evict_steps_conserve_tokens_and_moments_sum_everything_evicted():
+    """Over several steps: the retained rows and the evicted rows together are exactly the
+    tokens seen, the cache stays at `budget` rows, and the summary equals brute-force
+    sums over every evicted token (the compressed history and each step's victim)."""
+    rng = np.random.default_rng(44)
+    d, G, L, T = 6, 2, 6, 8
+    q, kc, vc, m, k_new, v_new, (KE, VE) = _evict_case(rng, d=d, G=G, L=L)
+    kc = np.zeros((L + 1, d)); vc = np.zeros((L + 1, d))
+    kc[:L], vc[:L] = rng.normal(size=(L, d)), rng.normal(size=(L, d))
+    seen_k, seen_v = [KE[i] for i in range(len(KE))] + list(kc[:L]), \
+        [VE[i] for i in range(len(VE))] + list(vc[:L])
+    gone_k, gone_v = [KE[i] for i in range(len(KE))], [VE[i] for i in range(len(VE))]
+    n = L
+    for t in range(T):
+        kn, vn = rng.normal(size=d), rng.normal(size=d)
+        seen_k.append(kn); seen_v.append(vn)
+        qt = rng.normal(size=(G, d))
+        pre_k = kc.copy(); pre_v = vc.copy()
+        pre_k[n], pre_v[n] = kn, vn
+        r = O.decode_evict_head(qt, kc, vc, n, kn, vn, m, L)
+        j = r["evicted"]
+        assert 0 <= j <= n and r["length"] == L
+        gone_k.append(pre_k[j]); gone_v.append(pre_v[j])
+        kc, vc, n, m = r["k_cache"], r["v_cache"], r["length"], r["moments"]
+    def as_set(rows):
+        return sorted(tuple(np.round(x, 12)) for x in rows)
+    assert as_set(list(kc[:n]) + gone_k) == as_set(seen_k)
+    assert as_set(list(vc[:n]) + gone_v) == as_set(seen_v)
+    S = np.zeros((d, d)); sk = np.zeros(d); sv = np.zeros(d)
+    for kk, vv in zip(gone_k, gone_v):
+        for a in range(d):
+            sk[a] += kk[a]; sv[a] += vv[a]
+            for b in range(d):
+                S[a, b] += vv[a] * kk[b]
+    assert m.n_e == len(gone_k)
+    np.testing.assert_allclose(m.s_k, sk, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(m.s_v, sv, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(m.S, S, rtol=1e-12, atol=1e-12)
+
+
+def test_evict_batched_matches_per_head():
+    rng = np.random.default_rng(45)
+    B, Hkv, G, d, L = 2, 2, 2, 5, 5
+    kc = rng.normal(size=(B, Hkv, L + 2, d)); vc = rng.normal(size=(B, Hkv, L + 2, d))
+    lens = np.array([[L, L - 1], [L, L]])
+    q = rng.normal(size=(B, Hkv * G, d))
+    kn, vn = rng.normal(size=(B, Hkv, d)), rng.normal(size=(B, Hkv, d))
+    mom = [[O.evicted_moments(rng.normal(size=(4, d)), rng.normal(size=(4, d)), np.arange(4))
+            for _ in range(Hkv)] for _ in range(B)]
+    out, lz, wr, (kc2, vc2, ln2, mom2), ev, _ = O.decode_evict(q, kc, vc, lens, mom, kn, vn, L)
+    for b in range(B):
+        for h in range(Hkv):
+            r = O.decode_evict_head(q[b, h * G:(h + 1) * G], kc[b, h], vc[b, h], lens[b, h],
+                                    kn[b, h], vn[b, h], mom[b][h], L)
+            assert ev[b, h] == r["evicted"] and ln2[b, h] == r["length"]
+            np.testing.assert_array_equal(out[b, h * G:(h + 1) * G], r["out"])
+            np.testing.assert_array_equal(kc2[b, h], r["k_cache"])
+    assert ev[0, 1] == -1 and ln2[0, 1] == L
