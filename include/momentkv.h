@@ -16,6 +16,10 @@
  *   momentkv_prepare_summary  the centred, clamped covariance of a summary in the form
  *                         the decode reads fastest; the summary is fixed between
  *                         compressions, so this runs once per compression.
+ *   momentkv_decode_evict a decoding step with moment-informed eviction: the new token
+ *                         joins the cache, the row with the lowest alpha_j ||r_j|| is
+ *                         folded into the summary (Algorithm 1 Phase 1, run at every
+ *                         generated token), then the corrected attention of Phase 2.
  *
  * Conventions shared by every entry point
  *   - Tensors are dense, contiguous, row-major, in device memory (HBM) unless stated.
@@ -44,13 +48,13 @@
 extern "C" {
 #endif
 
-#define MOMENTKV_ABI_VERSION 2
+#define MOMENTKV_ABI_VERSION 3
 
 typedef enum {
   MKV_OK = 0,
   MKV_ERR_NULL = 1,        /* a required pointer is NULL                               */
   MKV_ERR_SHAPE = 2,       /* non-positive size, Hq % Hkv != 0, bad d/window/chunk ... */
-  MKV_ERR_BUDGET = 3,      /* budget < n_sink + window (the protected tokens)          */
+  MKV_ERR_BUDGET = 3,      /* budget < n_sink + window; eviction budget < 1            */
   MKV_ERR_DTYPE = 4,       /* dtype is not MKV_F32 or MKV_BF16                          */
   MKV_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the size query            */
   MKV_ERR_CAPACITY = 6,    /* output cache rows too few, or max_len > cap              */
@@ -214,6 +218,52 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
                                 const float* s_v, const void* S, void* out, float* lse_out,
                                 float* w_r_out, void* workspace, size_t workspace_bytes,
                                 void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * Decode step with moment-informed eviction (Algorithm 1, Phase 1 then Phase 2)
+ *
+ * Per (b, h) and its G queries q_g (query heads hG .. hG + G - 1):
+ *   0. the new token joins R at row lens[b,h] (Algorithm 1, before Phase 1);
+ *   1. Phase 1, when R now holds more than `budget` rows.  One eviction per call: a cache
+ *      that held at most `budget` rows before the append (every step after a
+ *      compression to `budget`) is back at `budget` rows, so Algorithm 1's loop runs once;
+ *      a cache that already held more keeps its length and is flagged:
+ *        alpha_j = mean over g of softmax_j(scale q_g . k_j) over R (the group mean is this
+ *                  library's reading for grouped queries),
+ *        r_j = v_j - v_bar - (scale / n_e) S_tilde k_j (Sec. 4.2 Eq. residual; v_bar and
+ *              S_tilde are zero when n_e = 0), S_tilde clamped at tau as in the decode,
+ *        j* = the row with the lowest alpha_j ||r_j|| (the lowest row among equal scores),
+ *        n_e += 1, s_k += k_j*, s_v += v_j*, S += v_j* k_j*^T (App. A.1 Eq. app_update),
+ *        the last row of R moves into row j*, lens -= 1;
+ *   2. Phase 2: the corrected attention of momentkv_decode_attn (no append) on the
+ *      updated cache and summary.
+ * The decision is taken on fp32 scores in the log domain (log alpha_j + log ||r_j||, so
+ * no weight underflows); near-equal scores may order differently from exact arithmetic.
+ * ---------------------------------------------------------------------------------- */
+size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);
+
+/* p         as for momentkv_decode_attn with summary = 0: S is the raw sum, updated in
+ *           place.  max_len bounds lens after the append (budget < max_len <= cap leaves
+ *           room for the new row)
+ * budget    rows per KV head kept by Phase 1, >= 1 (MKV_ERR_BUDGET otherwise)
+ * q, k_cache, v_cache, lens, out, lse_out, w_r_out: as momentkv_decode_attn; row lens (the
+ *           new token) and row j* of the caches are written, lens is updated
+ * k_new, v_new [B, Hkv, d]: required
+ * n_e, s_k, s_v, S: the raw summary (fp32; n_e int32), read and updated in place
+ * evicted_out  NULL or [B, Hkv] int32: the row j* evicted by this call (it now holds what
+ *           was the last row, unless j* was the last row itself), -1 if none
+ * workspace >= momentkv_decode_evict_workspace_size(p) bytes, 256-aligned.  Its first
+ *           int32 is a sticky flag: bit 0 = a full cache (lens >= cap) skipped the append
+ *           and the eviction; bit 1 = lens + 1 exceeded max_len (appended, no eviction);
+ *           bit 2 = no finite score (nothing evicted); bit 3 = lens was above budget
+ *           before the append (one row evicted, the length kept).  Zero it before first
+ *           use. */
+mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, const void* q,
+                                 void* k_cache, void* v_cache, int32_t* lens,
+                                 const void* k_new, const void* v_new, int32_t* n_e,
+                                 float* s_k, float* s_v, float* S, void* out, float* lse_out,
+                                 float* w_r_out, int32_t* evicted_out, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* momentkv_status_string(int32_t status);

@@ -531,7 +531,8 @@ def decode_evict_head(q, k_cache, v_cache, length: int, k_new, v_new, m: Moments
 
     1. The new key/value joins R in slot `length` (Algorithm 1, before Phase 1).
     2. Phase 1 (reading: one eviction per call, the loop's single pass when R held at
-       most `budget` rows before the append): if more than `budget` rows are retained,
+       most `budget` rows before the append; a cache above `budget` keeps its length):
+       if more than `budget` rows are retained,
        score them (evict_scores_head), evict the argmin (the lowest slot among equal
        scores) or the slot `forced`, and fold it into the summary by the rank-one update
        of App. A.1 Eq. app_update.  The last retained row moves into the freed slot

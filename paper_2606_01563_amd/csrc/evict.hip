@@ -1,0 +1,416 @@
+// Moment-informed eviction at a decoding step (Algorithm 1 Phase 1), run ahead of the
+// corrected attention of Phase 2 (which then goes through the decode launches on the
+// updated cache and summary).
+//
+// k_evict_scores: n_heads x nslice workgroups of 4 waves.  The workgroup first forms the
+//   summary's clamped covariance S_tilde = S - s_v s_k^T / n_e (entries below tau set to
+//   zero; zero when n_e = 0) from the raw moments into LDS: hi / lo bf16 planes for bf16
+//   caches, fp32 otherwise.  Each wave then takes 32-row blocks of the workgroup's rows
+//   of R, the new token included (row lens, read from k_new / v_new), and writes for
+//   every row j
+//     x_gj = scale log2(e) q_g . k_j           (base-2 logits of the G queries)
+//     y_j  = log2 ||r_j||,  r_j = v_j - v_bar - (scale / n_e) S_tilde k_j   (Eq. residual)
+//   S_tilde k_j runs on MFMA with the same K fragments as the logits (B operand) and
+//   S_tilde rows from LDS (A operand).  The rows of each 16-row MFMA tile are taken in
+//   the order that leaves every lane holding the products for exactly the dimensions of
+//   v_j it loaded (dims 32c + 8 (lane / 16) + e), so r_j and its squared norm are formed
+//   in registers and finished with a 4-lane sum.
+// k_evict_select: one workgroup per KV head.  log2 Z_g over R from the logits, the
+//   group-mean softmax weight alpha_j = mean_g 2^(x_gj - log2 Z_g) in the log domain (so
+//   no weight underflows), the argmin of log2 alpha_j + y_j (the lowest row on ties),
+//   then the rank-one update n_e += 1, s_k += k*, s_v += v*, S += v* k*^T (App. A.1
+//   Eq. app_update) and the move of the last row into the freed one.
+#include <climits>
+
+#include "mkv_device.h"
+#include "mkv_launch.h"
+
+namespace mkv {
+
+namespace {
+
+constexpr int kEvThreads = 256;
+constexpr int kEvTB = 32;  // rows per block
+
+// LDS copy of S_tilde with rows padded by 16 bytes.
+template <class T, int D> struct SumLds;
+template <int D> struct SumLds<bf16_t, D> {
+  static constexpr int RS = D + 8;
+  bf16_t hi[D * RS];
+  bf16_t lo[D * RS];
+};
+template <int D> struct SumLds<float, D> {
+  static constexpr int RS = D + 4;
+  float st[D * RS];
+};
+
+__device__ __forceinline__ bf16x8 lds_frag(const bf16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+}
+__device__ __forceinline__ f32x8 lds_frag(const float* p) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  f32x8 r;
+  r[0] = a.x; r[1] = a.y; r[2] = a.z; r[3] = a.w;
+  r[4] = b.x; r[5] = b.y; r[6] = b.z; r[7] = b.w;
+  return r;
+}
+
+// S_tilde of one head into LDS; every thread handles D*D/8/256 chunks of 8 entries of a
+// row (all loads issued before any is used).
+template <class T, int D>
+__device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumLds<T, D>& sm) {
+  constexpr int PER = D * D / 8 / kEvThreads;
+  constexpr int RS = SumLds<T, D>::RS;
+  const int tid = threadIdx.x;
+  const int c0 = 8 * (tid % (D / 8));
+  const int ne = e.n_e[head];
+  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+  const float* Sh = e.S + (size_t)head * D * D;
+  const f32x8 skc = load_frag(e.s_k + (size_t)head * D + c0);
+  f32x8 raw[PER];
+  float sv[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int row = (tid + kEvThreads * u) / (D / 8);
+    raw[u] = load_frag(Sh + (size_t)row * D + c0);
+    sv[u] = e.s_v[(size_t)head * D + row];
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int row = (tid + kEvThreads * u) / (D / 8);
+    float st[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const float t = raw[u][x] - sv[u] * (skc[x] * inv_n);
+      st[x] = (ne <= 0 || fabsf(t) < e.tau) ? 0.f : t;
+    }
+    if constexpr (sizeof(T) == 2) {
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int x = 0; x < 8; x += 2) {
+        const bf16_t h0 = f2bf(st[x]), h1 = f2bf(st[x + 1]);
+        const bf16_t l0 = f2bf(st[x] - bf2f(h0)), l1 = f2bf(st[x + 1] - bf2f(h1));
+        h[x / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        l[x / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+      }
+      *reinterpret_cast<uint4*>(&sm.hi[row * RS + c0]) = make_uint4(h[0], h[1], h[2], h[3]);
+      *reinterpret_cast<uint4*>(&sm.lo[row * RS + c0]) = make_uint4(l[0], l[1], l[2], l[3]);
+    } else {
+      float4* P = reinterpret_cast<float4*>(&sm.st[row * RS + c0]);
+      P[0] = make_float4(st[0], st[1], st[2], st[3]);
+      P[1] = make_float4(st[4], st[5], st[6], st[7]);
+    }
+  }
+}
+
+// The new token: wave 0 of the workgroup given the job copies k_new / v_new to cache row
+// `row`, 16 bytes per lane.
+template <class T, int D>
+__device__ __forceinline__ void append_new_row(const EvictArgs& e, int head, int row, int lane) {
+  constexpr int NV = D * (int)sizeof(T) / 16;
+  if (lane < 2 * NV) {
+    const bool is_v = lane >= NV;
+    const int piece = lane % NV;
+    const uint4* src = reinterpret_cast<const uint4*>(
+        reinterpret_cast<const T*>(is_v ? e.v_new : e.k_new) + (size_t)head * D) + piece;
+    T* cache = reinterpret_cast<T*>(is_v ? e.v_cache : e.k_cache);
+    uint4* dst = reinterpret_cast<uint4*>(cache + ((size_t)head * e.cap + row) * D) + piece;
+    *dst = *src;
+  }
+}
+
+// Whether this call evicts from the head: the new row fits in the cache and in the
+// row bound, and the cache then holds more than `budget` rows.
+__device__ __forceinline__ bool head_evicts(const EvictArgs& e, int old_len) {
+  return old_len >= 0 && old_len < e.cap && old_len + 1 <= e.max_len && old_len + 1 > e.budget;
+}
+
+}  // namespace
+
+template <class T, int D>
+__global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
+  typedef typename Frag<T>::type FragT;
+  constexpr int KS = D / 32;  // contraction steps; also 8-dim groups per lane and row
+  constexpr int NT = D / 16;  // 16-row tiles of S_tilde k
+  constexpr int RS = SumLds<T, D>::RS;
+  __shared__ __align__(16) SumLds<T, D> sm;
+
+  const int head = blockIdx.x / e.nslice, slice = blockIdx.x % e.nslice;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q4 = lane >> 4, r16 = lane & 15;
+  const int old_len = e.lens[head];
+  const bool can_append = old_len >= 0 && old_len < e.cap;
+  // the workgroup whose rows hold the new one appends it (the last one for rows past them)
+  if (can_append && wave == 0 && min(old_len / e.slice_len, e.nslice - 1) == slice)
+    append_new_row<T, D>(e, head, old_len, lane);
+  const int t0 = slice * e.slice_len;
+  const int t1 = min(t0 + e.slice_len, old_len + 1);
+  if (!head_evicts(e, old_len) || t0 >= t1) return;  // uniform over the workgroup
+
+  build_summary<T, D>(e, head, sm);
+
+  const int G = e.G;
+  const T* qh = reinterpret_cast<const T*>(e.q) + (size_t)head * G * D;
+  FragT qf[KS];
+  {
+    const int gc = min(r16, G - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const FragT f = load_frag(qh + (size_t)gc * D + 32 * ks + 8 * q4);
+      qf[ks] = r16 < G ? f : zero_frag<T>();
+    }
+  }
+  const int ne = e.n_e[head];
+  const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
+  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+  f32x8 vbar[KS];
+#pragma unroll
+  for (int c = 0; c < KS; ++c) {
+    vbar[c] = load_frag(e.s_v + (size_t)head * D + 32 * c + 8 * q4);
+#pragma unroll
+    for (int x = 0; x < 8; ++x) vbar[c][x] *= inv_n;
+  }
+  const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
+  const T* vc = reinterpret_cast<const T*>(e.v_cache) + (size_t)head * e.cap * D;
+  const T* kn = reinterpret_cast<const T*>(e.k_new) + (size_t)head * D;
+  const T* vn = reinterpret_cast<const T*>(e.v_new) + (size_t)head * D;
+  const int ML = e.max_len;
+  float* rec = e.rec + (size_t)head * (G + 1) * ML;
+  const float c2 = e.scale * kLog2e;
+  __syncthreads();  // S_tilde is in LDS
+
+  FragT kf[2][KS], vf[2][KS];
+  for (int j0 = t0 + kEvTB * wave; j0 < t1; j0 += 4 * kEvTB) {
+    // rows j0 + 16 hh + lane % 16: K and V fragments at dims 32 ks + 8 (lane / 16)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int j = j0 + 16 * hh + r16;
+      const bool ok = j < t1;
+      const T* kr = j == old_len ? kn : kc + (size_t)j * D;
+      const T* vr = j == old_len ? vn : vc + (size_t)j * D;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        kf[hh][ks] = ok ? load_frag(kr + 32 * ks + 8 * q4) : zero_frag<T>();
+        vf[hh][ks] = ok ? load_frag(vr + 32 * ks + 8 * q4) : zero_frag<T>();
+      }
+    }
+    f32x4 lg[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      lg[hh] = zero4();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) mma(lg[hh], qf[ks], kf[hh][ks]);
+    }
+    // S_tilde k: tile t = 2c + s holds dims 32c + 8 (lane/16) + 4s + i in lane rows
+    // 4 (lane/16) + i, i.e. element 4s + i of the lane's V fragment c.
+    float rr[2] = {0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int c = t >> 1, s = t & 1;
+      const int row = 32 * c + 8 * (r16 >> 2) + 4 * s + (r16 & 3);
+      f32x4 ta[2] = {zero4(), zero4()};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if constexpr (sizeof(T) == 2) {
+          const bf16x8 ah = lds_frag(&sm.hi[row * RS + 32 * ks + 8 * q4]);
+          const bf16x8 al = lds_frag(&sm.lo[row * RS + 32 * ks + 8 * q4]);
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            mma(ta[hh], ah, kf[hh][ks]);
+            mma(ta[hh], al, kf[hh][ks]);
+          }
+        } else {
+          const f32x8 af = lds_frag(&sm.st[row * RS + 32 * ks + 8 * q4]);
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) mma(ta[hh], af, kf[hh][ks]);
+        }
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int x = 4 * s + i;
+          const float r = elem_f(vf[hh][c], x) - vbar[c][x] - cf * ta[hh][i];
+          rr[hh] += r * r;
+        }
+      // one tile's LDS reads in flight at a time: hoisting all of them would not fit
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      rr[hh] = cross_row_sum(rr[hh]);
+      const int j = j0 + 16 * hh + r16;
+      if (j < t1) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int g = 4 * q4 + i;
+          if (g < G) rec[(size_t)g * ML + j] = lg[hh][i] * c2;
+        }
+        if (q4 == 0) rec[(size_t)G * ML + j] = 0.5f * log2f(rr[hh]);
+      }
+    }
+  }
+}
+
+template <class T, int D>
+__global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
+  constexpr int GM = 16;
+  __shared__ float s_m[4][GM], s_l[4][GM], s_lz[GM];
+  __shared__ float s_best[4];
+  __shared__ int s_bj[4], s_pick;
+  __shared__ float s_kv[2][D];
+  const int head = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int old_len = e.lens[head];
+  const bool can_append = old_len >= 0 && old_len < e.cap;
+  if (!head_evicts(e, old_len)) {
+    if (tid == 0) {
+      if (!can_append) {
+        atomicOr(e.flag, 1);
+      } else {
+        if (old_len + 1 > e.max_len) atomicOr(e.flag, 2);
+        e.lens[head] = old_len + 1;
+      }
+      if (e.evicted) e.evicted[head] = -1;
+    }
+    return;
+  }
+  const int n_tok = old_len + 1;
+  const int G = e.G, ML = e.max_len;
+  const float* rec = e.rec + (size_t)head * (G + 1) * ML;
+  if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
+
+  // log2 Z_g over the n_tok rows
+  float m[GM], l[GM];
+#pragma unroll
+  for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
+  for (int j = tid; j < n_tok; j += kEvThreads) {
+#pragma unroll
+    for (int g = 0; g < GM; ++g) {
+      if (g < G) {
+        const float x = rec[(size_t)g * ML + j];
+        const float mn = fmaxf(m[g], x);
+        l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x - mn);
+        m[g] = mn;
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < GM; ++g) {
+    if (g < G) {
+      const float M = wave_max(m[g]);
+      const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
+      if (lane == 0) { s_m[wave][g] = M; s_l[wave][g] = ls; }
+    }
+  }
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][tid]);
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (s_m[w][tid] != -INFINITY) L += s_l[w][tid] * fast_exp2(s_m[w][tid] - M);
+    s_lz[tid] = M + log2f(L);
+  }
+  __syncthreads();
+
+  // argmin over rows of log2(mean_g alpha_gj) + log2 ||r_j||, lowest row on ties
+  float lz[GM];
+#pragma unroll
+  for (int g = 0; g < GM; ++g) lz[g] = g < G ? s_lz[g] : 0.f;
+  const float log2_g = log2f((float)G);
+  float best = INFINITY;
+  int bj = INT_MAX;
+  for (int j = tid; j < n_tok; j += kEvThreads) {
+    float x[GM];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < GM; ++g) {
+      x[g] = g < G ? rec[(size_t)g * ML + j] - lz[g] : -INFINITY;
+      mx = fmaxf(mx, x[g]);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int g = 0; g < GM; ++g)
+      if (g < G) s += fast_exp2(x[g] - mx);
+    const float sc = mx + log2f(s) - log2_g + rec[(size_t)G * ML + j];
+    if (sc < best) { best = sc; bj = j; }  // rows rise along a thread: ties keep the first
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ob = __shfl_xor(best, off);
+    const int oj = __shfl_xor(bj, off);
+    if (ob < best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+  }
+  if (lane == 0) { s_best[wave] = best; s_bj[wave] = bj; }
+  __syncthreads();
+  if (tid == 0) {
+    float b = s_best[0];
+    int j = s_bj[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w)
+      if (s_best[w] < b || (s_best[w] == b && s_bj[w] < j)) { b = s_best[w]; j = s_bj[w]; }
+    s_pick = j;
+  }
+  __syncthreads();
+  const int js = s_pick;
+  if (js < 0 || js >= n_tok) {  // no comparable score (non-finite inputs): keep every row
+    if (tid == 0) {
+      atomicOr(e.flag, 4);
+      e.lens[head] = n_tok;
+      if (e.evicted) e.evicted[head] = -1;
+    }
+    return;
+  }
+
+  // rank-one update and the move of the last row into slot js
+  const int last = n_tok - 1;
+  T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
+  T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
+  if (tid < D) {
+    const T ks = kc[(size_t)js * D + tid], vs = vc[(size_t)js * D + tid];
+    const T kl = kc[(size_t)last * D + tid], vl = vc[(size_t)last * D + tid];
+    const float kf = to_f<T>(ks), vf = to_f<T>(vs);
+    s_kv[0][tid] = kf;
+    s_kv[1][tid] = vf;
+    if (js != last) {
+      kc[(size_t)js * D + tid] = kl;
+      vc[(size_t)js * D + tid] = vl;
+    }
+    e.s_k[(size_t)head * D + tid] += kf;
+    e.s_v[(size_t)head * D + tid] += vf;
+  }
+  if (tid == 0) {
+    e.n_e[head] += 1;
+    e.lens[head] = last;
+    if (e.evicted) e.evicted[head] = js;
+  }
+  __syncthreads();
+  float* Sh = e.S + (size_t)head * D * D;
+  for (int idx = tid; idx < D * D / 4; idx += kEvThreads) {
+    const int row = idx / (D / 4), c = 4 * (idx % (D / 4));
+    float4 s4 = *reinterpret_cast<const float4*>(Sh + (size_t)row * D + c);
+    const float va = s_kv[1][row];
+    s4.x = fmaf(va, s_kv[0][c], s4.x);
+    s4.y = fmaf(va, s_kv[0][c + 1], s4.y);
+    s4.z = fmaf(va, s_kv[0][c + 2], s4.z);
+    s4.w = fmaf(va, s_kv[0][c + 3], s4.w);
+    *reinterpret_cast<float4*>(Sh + (size_t)row * D + c) = s4;
+  }
+}
+
+template <class T, int D>
+static hipError_t launch_evict_t(const EvictArgs& e, hipStream_t st) {
+  hipLaunchKernelGGL((k_evict_scores<T, D>), dim3(e.n_heads * e.nslice), dim3(kEvThreads), 0, st, e);
+  hipLaunchKernelGGL((k_evict_select<T, D>), dim3(e.n_heads), dim3(kEvThreads), 0, st, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_evict(const EvictArgs& e, bool bf16, int d, hipStream_t st) {
+  if (bf16) return d == 64 ? launch_evict_t<bf16_t, 64>(e, st) : launch_evict_t<bf16_t, 128>(e, st);
+  return d == 64 ? launch_evict_t<float, 64>(e, st) : launch_evict_t<float, 128>(e, st);
+}
+
+}  // namespace mkv

@@ -81,6 +81,11 @@ def lib() -> ctypes.CDLL:
         L.momentkv_prepared_summary_size.restype = ctypes.c_size_t
         L.momentkv_prepare_summary.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 6
         L.momentkv_prepare_summary.restype = ctypes.c_int
+        L.momentkv_decode_evict_workspace_size.argtypes = [ctypes.POINTER(DecodeParams)]
+        L.momentkv_decode_evict_workspace_size.restype = ctypes.c_size_t
+        L.momentkv_decode_evict.argtypes = [ctypes.POINTER(DecodeParams), ctypes.c_int32] + \
+            [_VP] * 14 + [_VP, ctypes.c_size_t, _VP]
+        L.momentkv_decode_evict.restype = ctypes.c_int
         L.momentkv_status_string.restype = ctypes.c_char_p
         L.momentkv_abi_version.argtypes = []
         L.momentkv_abi_version.restype = ctypes.c_int32
@@ -109,6 +114,10 @@ def momentkv_compress_workspace_size(p: CompressParams) -> int:
 
 def momentkv_decode_workspace_size(p: DecodeParams) -> int:
     return int(lib().momentkv_decode_workspace_size(ctypes.byref(p)))
+
+
+def momentkv_decode_evict_workspace_size(p: DecodeParams) -> int:
+    return int(lib().momentkv_decode_evict_workspace_size(ctypes.byref(p)))
 
 
 def momentkv_prepared_summary_size(p: DecodeParams) -> int:
@@ -288,3 +297,39 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     if code != 0:
         raise MomentKVError(code, "momentkv_decode_attn")
     return out, lse, w_r, ws
+
+
+def momentkv_decode_evict(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                          lens: torch.Tensor, n_e: torch.Tensor, s_k: torch.Tensor,
+                          s_v: torch.Tensor, S: torch.Tensor, k_new: torch.Tensor,
+                          v_new: torch.Tensor, budget: int, *, max_len: int | None = None,
+                          order: int = 1, scale: float = 0.0, tau: float = 1e-6,
+                          n_split: int = 0, out: torch.Tensor | None = None,
+                          lse: torch.Tensor | None = None, w_r: torch.Tensor | None = None,
+                          evicted: torch.Tensor | None = None,
+                          workspace: torch.Tensor | None = None):
+    """Decode step with moment-informed eviction (see the header).  The caches, lens and
+    the raw summary (n_e, s_k, s_v, S) are updated in place.
+    Returns (out, lse, w_r, evicted, workspace)."""
+    cap = k_cache.shape[2]
+    p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
+                      scale=scale, tau=tau, n_split=n_split, summary=0)
+    dev = q.device
+    if out is None:
+        out = torch.empty_like(q)
+    nbytes = momentkv_decode_evict_workspace_size(p)
+    if nbytes == 0:
+        code = lib().momentkv_decode_evict(ctypes.byref(p), int(budget), *([None] * 14), None,
+                                           0, None)
+        raise MomentKVError(code, "momentkv_decode_evict")
+    fresh = workspace is None or workspace.numel() < nbytes
+    ws = _workspace(nbytes, dev, workspace)
+    if fresh:
+        ws[:decode_workspace_zero_bytes(p)].zero_()
+    code = lib().momentkv_decode_evict(
+        ctypes.byref(p), int(budget), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lens),
+        _ptr(k_new), _ptr(v_new), _ptr(n_e), _ptr(s_k), _ptr(s_v), _ptr(S), _ptr(out),
+        _ptr(lse), _ptr(w_r), _ptr(evicted), ws.data_ptr(), ws.numel(), _stream())
+    if code != 0:
+        raise MomentKVError(code, "momentkv_decode_evict")
+    return out, lse, w_r, evicted, ws

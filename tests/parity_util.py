@@ -206,3 +206,87 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
         np.testing.assert_array_equal(h64(comp.v_out), vc_ref)
     assert int(ws[:4].view(torch.int32)[0]) == 0
     return worst
+
+
+EVICT_BAND = 1e-4   # relative band of the oracle's lowest score within which rows may swap
+
+
+def run_evict_steps(inp: dict, comp: mk.CompressOutput, steps: int, budget: int, *, order=1,
+                    tau=1e-6, n_split=0, flag=0, start=None):
+    """Run `steps` decode calls with eviction on the GPU against the oracle's own
+    trajectory.  The oracle starts from the GPU's compressed state (cache rows, lens and
+    fp32 moments, all checked by the compress parity) and then evolves on its own.  At
+    every step, per head:
+      * the evicted row is the oracle's argmin, or a row whose oracle score lies within
+        EVICT_BAND of the lowest (then the oracle follows that row, and it is counted);
+      * lens, n_e and every cache row are exact; s_k, s_v, S within 1e-5 (relative L2);
+      * out, w_R and log Z_R are within the dtype's tolerance.
+    The GPU buffers are copies, so `comp` is left as it was; `start` = (lens, n_e) replaces
+    the compressed lengths and counts first.  The workspace flag must end equal to `flag`.
+    Returns (worst rel err of out, band swaps, evictions)."""
+    dt = inp["k"].dtype
+    tol = TOL[dt]
+    B, Hkv, cap, d = comp.k_out.shape
+    Hq = inp["q_win"].shape[1]
+    G = Hq // Hkv
+    kc, vc, lens = comp.k_out.clone(), comp.v_out.clone(), comp.lens.clone()
+    n_e, s_k, s_v, S = comp.n_e.clone(), comp.s_k.clone(), comp.s_v.clone(), comp.S.clone()
+    if start is not None:
+        lens.copy_(torch.as_tensor(start[0], dtype=torch.int32))
+        n_e.copy_(torch.as_tensor(start[1], dtype=torch.int32))
+    moments = [[O.Moments(int(n_e[b, h]), h64(s_k[b, h]), h64(s_v[b, h]), h64(S[b, h]))
+                for h in range(Hkv)] for b in range(B)]
+    kc_ref, vc_ref = h64(comp.k_out), h64(comp.v_out)
+    ln_ref = lens.cpu().numpy().astype(np.int64)
+    lse = torch.empty(B, Hq, dtype=torch.float32, device=kc.device)
+    w_r = torch.empty_like(lse)
+    ev = torch.empty(B, Hkv, dtype=torch.int32, device=kc.device)
+    ws = None
+    worst, swaps, evictions = 0.0, 0, 0
+    for t in range(steps):
+        q, kn, vn = inp["q_dec"][t], inp["k_new"][t], inp["v_new"][t]
+        out, _, _, _, ws = mk.momentkv_decode_evict(
+            q, kc, vc, lens, n_e, s_k, s_v, S, kn, vn, budget, max_len=cap, order=order,
+            tau=tau, n_split=n_split, lse=lse, w_r=w_r, evicted=ev, workspace=ws)
+        torch.cuda.synchronize()
+        ev_gpu = ev.cpu().numpy().astype(np.int64)
+        args = (h64(q), kc_ref, vc_ref, ln_ref, moments, h64(kn), h64(vn), budget)
+        ref = O.decode_evict(*args, tau=tau, order=order)
+        ev_ref, heads = ref[4], ref[5]
+        if not np.array_equal(ev_gpu, ev_ref):
+            for b in range(B):
+                for h in range(Hkv):
+                    if ev_gpu[b, h] == ev_ref[b, h]:
+                        continue
+                    assert ev_gpu[b, h] >= 0 and ev_ref[b, h] >= 0, (t, b, h)
+                    sc = heads[b][h]["score"]
+                    lo = sc.min()
+                    assert sc[ev_gpu[b, h]] <= lo * (1 + EVICT_BAND) + 1e-300, \
+                        (t, b, h, sc[ev_gpu[b, h]], lo)
+                    swaps += 1
+            ref = O.decode_evict(*args, tau=tau, order=order, forced=ev_gpu)
+        ref_out, ref_lz, ref_wr, (kc_ref, vc_ref, ln_ref, moments), ev_ref, _ = ref
+        np.testing.assert_array_equal(ev_gpu, ev_ref)
+        evictions += int((ev_gpu >= 0).sum())
+        np.testing.assert_array_equal(lens.cpu().numpy(), ln_ref)
+        np.testing.assert_array_equal(h64(kc), kc_ref)
+        np.testing.assert_array_equal(h64(vc), vc_ref)
+        ne_g = n_e.cpu().numpy()
+        for b in range(B):
+            for h in range(Hkv):
+                m = moments[b][h]
+                assert int(ne_g[b, h]) == m.n_e, (t, b, h)
+                assert rel_l2(h64(s_k[b, h]), m.s_k) <= 1e-5
+                assert rel_l2(h64(s_v[b, h]), m.s_v) <= 1e-5
+                assert rel_l2(h64(S[b, h]), m.S) <= 1e-5
+        got = h64(out)
+        e = max(rel_l2(got[b, hq], ref_out[b, hq]) for b in range(B) for hq in range(Hq))
+        e_w = float(np.max(np.abs(w_r.cpu().double().numpy() - ref_wr)))
+        e_l = float(np.max(np.abs(lse.cpu().double().numpy() - ref_lz) /
+                           np.maximum(1.0, np.abs(ref_lz))))
+        assert e <= tol, (t, e)
+        assert e_w <= max(tol, 1e-5), (t, e_w)
+        assert e_l <= max(tol, 1e-5), (t, e_l)
+        worst = max(worst, e)
+    assert int(ws[:4].view(torch.int32)[0]) == flag
+    return worst, swaps, evictions

@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert mk.momentkv_abi_version() == 2
+    assert mk.momentkv_abi_version() == 3
     for code in range(10):
         assert mk.momentkv_status_string(code) not in ("", "unknown status")
     assert mk.momentkv_status_string(99) == "unknown status"
@@ -162,3 +162,36 @@ def test_prepared_summary_size_and_validation(L):
     assert f(ctypes.byref(p), *ptrs[:4], ptrs[4] + 8, None) == SHAPE      # misaligned
     assert f(ctypes.byref(p), *ptrs[:4], ptrs[3] + 64, None) == ALIAS     # overlaps S
     assert f(ctypes.byref(dparams(dtype=5)), *ptrs, None) == DTYPE
+
+
+def evict_status(p, budget, ptr=1 << 20, ws=1 << 40, ws_bytes=None, drop=None):
+    size = mk.momentkv_decode_evict_workspace_size(p)
+    if ws_bytes is None:
+        ws_bytes = size
+    ptrs = [ptr + i * (1 << 36) if ptr else None for i in range(14)]
+    if drop is not None:
+        ptrs[drop] = None
+    return mk.lib().momentkv_decode_evict(ctypes.byref(p), budget, *ptrs, ws, ws_bytes, None)
+
+
+def test_decode_evict_sizes_and_validation(L):
+    p = dparams()
+    size = mk.momentkv_decode_evict_workspace_size(p)
+    # the decode workspace plus (G + 1) fp32 records per row of every head
+    assert size >= mk.momentkv_decode_workspace_size(p) + 36 * 8 * 5 * 640 * 4
+    assert mk.momentkv_decode_evict_workspace_size(dparams(summary=1)) == 0
+    assert evict_status(p, 0) == BUDGET
+    assert evict_status(dparams(summary=1), 512) == SHAPE
+    assert evict_status(dparams(head_dim=80), 512) == UNSUP
+    assert evict_status(dparams(max_len=641), 512) == CAPACITY
+    assert evict_status(p, 512, ptr=0) == NULL
+    for i in (4, 5, 10):                      # k_new, v_new and out are required
+        assert evict_status(p, 512, drop=i) == NULL
+    assert evict_status(p, 512, ws_bytes=size - 1) == WORKSPACE
+    assert evict_status(p, 512, ws=(1 << 40) + 64) == WORKSPACE
+    ptrs = [(1 << 20) + i * (1 << 36) for i in range(14)]
+    ptrs[10] = ptrs[9]                        # out overlaps S
+    assert mk.lib().momentkv_decode_evict(ctypes.byref(p), 512, *ptrs, 1 << 40, size, None) == ALIAS
+    ptrs = [(1 << 20) + i * (1 << 36) for i in range(14)]
+    ptrs[9] = ptrs[1]                         # S overlaps the key cache
+    assert mk.lib().momentkv_decode_evict(ctypes.byref(p), 512, *ptrs, 1 << 40, size, None) == ALIAS

@@ -258,3 +258,81 @@ def test_ruler_128k_full_size_sampled_head():
     errs = P.check_compress_head(cpu, out, 0, 2, 1024)
     announce(f"head 2 {errs}")
     P.run_decode_steps(gpu, out, 1)
+
+
+# ---------------------------------------------------------------- decode-time eviction
+def test_evict_tiny_fp32_follows_oracle_trajectory():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=16)
+    L = wl.budgets[0]
+    out = P.run_compress(gpu, L, cap=L + 1)
+    announce(f"{wl.name} evict L={L}")
+    worst, swaps, n = P.run_evict_steps(gpu, out, 16, L)
+    announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
+    assert n == 16 and swaps == 0
+
+
+@pytest.mark.parametrize("n_split", [0, 1, 3])
+def test_evict_llama_layer_bf16_launch_shapes(n_split):
+    """Two sequences x 8 KV heads; the attention after the eviction on the automatic, the
+    single-launch and a 3-slice split shape."""
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=10, ctx_len=3000, batch=2)
+    L = 300
+    out = P.run_compress(gpu, L, cap=L + 1)
+    announce(f"{wl.name} evict L={L} n_split={n_split}")
+    worst, swaps, n = P.run_evict_steps(gpu, out, 10, L, n_split=n_split)
+    announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
+    assert n == 10 * 16 and swaps <= n // 50
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("d", [64, 128])
+def test_evict_budgets_and_lengths_around_the_bound(dtype, d):
+    """Rows over several 128-row scoring slices with a ragged tail, G = 4; per-head
+    lengths below the budget (no eviction: the step is the decode with the append), at it
+    (steady state) and one row over it (flag bit 3, length kept)."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=d, ctx_len=1200,
+                         batch=2, n_q_heads=8, n_kv_heads=2, window=16, budgets=(290,))
+    out = P.run_compress(gpu, 290, cap=293)
+    announce(f"evict dtype={dtype} d={d}")
+    P.run_evict_steps(gpu, out, 3, 290)                                   # steady state
+    P.run_evict_steps(gpu, out, 3, 292, start=([[290, 289], [260, 1]], out.n_e.cpu()))
+    P.run_evict_steps(gpu, out, 2, 289, flag=8)                           # above budget
+
+
+def test_evict_with_empty_summary_scores_alpha_times_value_norm():
+    """Budget above the context keeps every token, so n_e = 0: the first evictions use
+    v_bar = S_tilde = 0 and later ones the summary they build."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=6, dtype=torch.bfloat16, head_dim=128,
+                         ctx_len=700, batch=1, n_q_heads=4, n_kv_heads=2, window=16,
+                         budgets=(900,))
+    out = P.run_compress(gpu, 900, cap=701)
+    assert int(out.n_e.max()) == 0 and int(out.lens.min()) == 700
+    worst, swaps, n = P.run_evict_steps(gpu, out, 6, 700)
+    assert n == 12
+
+
+def test_evict_full_cache_sets_flag_and_keeps_state():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, dtype=torch.bfloat16, head_dim=64,
+                         ctx_len=600, batch=1, n_q_heads=4, n_kv_heads=1, window=16,
+                         budgets=(100,))
+    out = P.run_compress(gpu, 100, cap=100)
+    kc, vc, lens = out.k_out.clone(), out.v_out.clone(), out.lens.clone()
+    n_e, s_k, s_v, S = out.n_e.clone(), out.s_k.clone(), out.s_v.clone(), out.S.clone()
+    ev = torch.empty_like(lens)
+    res, _, _, _, ws = mk.momentkv_decode_evict(gpu["q_dec"][0], kc, vc, lens, n_e, s_k, s_v, S,
+                                                gpu["k_new"][0], gpu["v_new"][0], 99)
+    torch.cuda.synchronize()
+    assert int(ws[:4].view(torch.int32)[0]) & 1
+    assert torch.equal(lens, out.lens) and torch.equal(n_e, out.n_e) and torch.equal(S, out.S)
+    assert torch.equal(kc, out.k_out)
+
+
+def test_evict_qwen_stack_layer_full_size_budget_2048():
+    """One layer of the 32K-context stack at budget 2048 (rows over 17 scoring slices of
+    128), two steps, every head checked."""
+    wl, cpu, gpu = layer("qwen3_4b_stack_n32768", steps=2)
+    out = P.run_compress(gpu, 2048, cap=2049)
+    announce(f"{wl.name} evict L=2048")
+    worst, swaps, n = P.run_evict_steps(gpu, out, 2, 2048)
+    announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
+    assert n == 2 * 8 and swaps <= 1
