@@ -139,6 +139,105 @@ def cpu_baseline(wl, data, budget: int, heads: int, steps: int) -> dict:
             "decode_s": t_dec, "compress_s": t_comp}
 
 
+def evict_bytes(n_heads: int, G: int, d: int, L: int, elem: int = 2) -> int:
+    """Algorithmic HBM bytes of one decode call with eviction at budget L (per KV head,
+    summed): the decode bytes over the L + 1 rows seen by Phase 1 (retained rows read once,
+    the new row read and written, the summary, queries and outputs), plus the summary
+    written back by the rank-one update (S, s_k, s_v, n_e) and the row moved into the
+    freed slot (read and written)."""
+    per_head = 4 * d * d + 8 * d + 4 + 2 * 2 * d * elem
+    return decode_bytes(n_heads, G, d, L + 1) + n_heads * per_head
+
+
+def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out,
+                      compress_phase, capture, timed_replay) -> dict:
+    """Decode with moment-informed eviction (Algorithm 1 Phase 1 then Phase 2) on the same
+    compressed stacks: for each of the decode tokens and each budget one
+    momentkv_decode_evict call over the 36 caches (cache held at the budget, summary
+    updated by each eviction).  Captured as a graph like the decode phase; per-budget
+    times by subtraction."""
+    dev = out.device
+    N, Hkv, d = wl.ctx_len, wl.n_kv_heads, wl.head_dim
+    G = wl.group
+    T = q_steps.shape[0]
+    LB = q_steps.shape[1]
+    ews = {}
+    for L in budgets:
+        Lr = min(L, N)
+        p = mk.decode_params(q_steps[0], stacks[L].k_out, max_len=Lr + 1)
+        ews[L] = torch.zeros(mk.momentkv_decode_evict_workspace_size(p), dtype=torch.uint8,
+                             device=dev)
+
+    def evict_call(t, L):
+        st = stacks[L]
+        Lr = min(L, N)
+        mk.momentkv_decode_evict(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k,
+                                 st.s_v, st.S, kn_steps[t], vn_steps[t], Lr, max_len=Lr + 1,
+                                 out=out, workspace=ews[L])
+
+    def evict_phase(skip=None):
+        for t in range(T):
+            for L in budgets:
+                if L != skip:
+                    evict_call(t, L)
+
+    print("[bench] decode with eviction: warm-up and capture", file=sys.stderr, flush=True)
+    compress_phase(None)
+    evict_phase()
+    torch.cuda.synchronize()
+    graph = capture(phase=evict_phase)
+    without = {L: capture(skip=L, phase=evict_phase) for L in budgets}
+    ev = []
+    for i in range(args.steps):
+        compress_phase(None)
+        ev.append(timed_replay(graph))
+    torch.cuda.synchronize()
+    flags = [int(ews[L][:4].view(torch.int32)[0]) for L in budgets]
+    if any(flags):
+        return {"error": f"eviction flags {flags}"}
+    # replay against the eager phase, bit for bit (output, lengths, counts, summary, cache)
+    compress_phase(None)
+    graph.replay()
+    torch.cuda.synchronize()
+    got = [out.clone()] + [x.clone() for L in budgets for x in
+                           (stacks[L].lens, stacks[L].n_e, stacks[L].S, stacks[L].k_out)]
+    compress_phase(None)
+    evict_phase()
+    torch.cuda.synchronize()
+    now = [out] + [x for L in budgets for x in
+                   (stacks[L].lens, stacks[L].n_e, stacks[L].S, stacks[L].k_out)]
+    if not all(torch.equal(a, b) for a, b in zip(got, now)):
+        return {"error": "eviction graph replay differs from the eager phase"}
+    del got
+    ms = [a.elapsed_time(b) for a, b in ev]
+    total = sum(ms) / len(ms)
+    per_budget = {}
+    all_bytes = 0
+    for L in budgets:
+        tl = []
+        for _ in range(args.steps):
+            compress_phase(None)
+            tl.append(timed_replay(without[L]))
+        torch.cuda.synchronize()
+        budget_ms = total - sum(a.elapsed_time(b) for a, b in tl) / len(tl)
+        by = evict_bytes(LB * Hkv, G, d, min(L, N)) * T
+        all_bytes += by
+        per_budget[str(L)] = {"us_per_call": budget_ms / T * 1e3,
+                              "GBps": by / (budget_ms * 1e-3) / 1e9,
+                              "tokens_per_s": wl.batch * T / (budget_ms * 1e-3)}
+    achieved = all_bytes / (total * 1e-3) / 1e9
+    return {"what": "per token and budget one momentkv_decode_evict call over the 36 "
+                    "caches: append, Phase 1 eviction (k_evict_scores, k_evict_select), "
+                    "Phase 2 corrected attention; cache kept at the budget",
+            "ms_per_step": total, "tokens_per_s": wl.batch * T * len(budgets) / (total * 1e-3),
+            "per_budget": per_budget,
+            "roofline": {"kernel": "momentkv_decode_evict call (3-4 launches)", "bound": "hbm",
+                         "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                         "bytes_per_call": all_bytes / (T * len(budgets)),
+                         "avg_call_us": total / (T * len(budgets)) * 1e3}}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +250,8 @@ def main() -> int:
     ap.add_argument("--cpu-heads", type=int, default=2)
     ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-evict", action="store_true",
+                    help="skip the decode-with-eviction measurement")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one plain copy of "
                          "known size, then 4 tokens x budgets of eager decode calls; prints "
@@ -245,7 +346,7 @@ def main() -> int:
     def new_timing():
         return {"compress": {L: [] for L in budgets}}
 
-    def capture(skip=None):
+    def capture(skip=None, phase=None):
         g = torch.cuda.CUDAGraph()
         cap_stream = torch.cuda.Stream()
         cap_stream.wait_stream(torch.cuda.current_stream())
@@ -253,7 +354,7 @@ def main() -> int:
             compress_phase(None)
             torch.cuda.synchronize()
             with torch.cuda.graph(g, stream=cap_stream):
-                decode_phase(skip)
+                (phase or decode_phase)(skip)
         torch.cuda.current_stream().wait_stream(cap_stream)
         torch.cuda.synchronize()
         return g
@@ -359,6 +460,12 @@ def main() -> int:
             "decode_tokens_per_s": B * T / (budget_ms * 1e-3),
         }
     value = phase_bytes * len(dec_ms) / dec_s / 1e9
+    evict = None if args.no_evict else evict_measurement(
+        args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out, compress_phase, capture,
+        timed_replay)
+    if evict is not None and evict.get("error"):
+        print(f"[bench] {evict['error']}", file=sys.stderr)
+        return 5
     n_launch = T * len(budgets)
     avg_launch_s = dec_s / len(dec_ms) / n_launch
     avg_bytes = phase_bytes / n_launch
@@ -393,6 +500,8 @@ def main() -> int:
                      "avg_launch_us": avg_launch_s * 1e6},
         "wall_s_timed": wall,
     }
+    if evict is not None:
+        res["evict_decode"] = evict
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl, data[0], 512 if 512 in budgets else budgets[0],

@@ -56,6 +56,13 @@ __device__ __forceinline__ f32x8 lds_frag(const float* p) {
   return r;
 }
 
+// RNE bf16 of a finite value (no NaN case: the summary of finite inputs is finite)
+__device__ __forceinline__ bf16_t f2bf_finite(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
 // S_tilde of one head into LDS; every thread handles D*D/8/256 chunks of 8 entries of a
 // row (all loads issued before any is used).
 template <class T, int D>
@@ -89,8 +96,8 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumL
       uint32_t h[4], l[4];
 #pragma unroll
       for (int x = 0; x < 8; x += 2) {
-        const bf16_t h0 = f2bf(st[x]), h1 = f2bf(st[x + 1]);
-        const bf16_t l0 = f2bf(st[x] - bf2f(h0)), l1 = f2bf(st[x + 1] - bf2f(h1));
+        const bf16_t h0 = f2bf_finite(st[x]), h1 = f2bf_finite(st[x + 1]);
+        const bf16_t l0 = f2bf_finite(st[x] - bf2f(h0)), l1 = f2bf_finite(st[x + 1] - bf2f(h1));
         h[x / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
         l[x / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
       }
@@ -129,12 +136,15 @@ __device__ __forceinline__ bool head_evicts(const EvictArgs& e, int old_len) {
 }  // namespace
 
 template <class T, int D>
-__global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
+__global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_scores(EvictArgs e) {
   typedef typename Frag<T>::type FragT;
   constexpr int KS = D / 32;  // contraction steps; also 8-dim groups per lane and row
   constexpr int NT = D / 16;  // 16-row tiles of S_tilde k
   constexpr int RS = SumLds<T, D>::RS;
   __shared__ __align__(16) SumLds<T, D> sm;
+  __shared__ __align__(16) float s_vbar[D];
+  constexpr int QRS = D + 16 / (int)sizeof(T);  // query rows padded by 16 bytes
+  __shared__ __align__(16) T s_q[16 * QRS];
 
   const int head = blockIdx.x / e.nslice, slice = blockIdx.x % e.nslice;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -148,29 +158,7 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
   const int t1 = min(t0 + e.slice_len, old_len + 1);
   if (!head_evicts(e, old_len) || t0 >= t1) return;  // uniform over the workgroup
 
-  build_summary<T, D>(e, head, sm);
-
   const int G = e.G;
-  const T* qh = reinterpret_cast<const T*>(e.q) + (size_t)head * G * D;
-  FragT qf[KS];
-  {
-    const int gc = min(r16, G - 1);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const FragT f = load_frag(qh + (size_t)gc * D + 32 * ks + 8 * q4);
-      qf[ks] = r16 < G ? f : zero_frag<T>();
-    }
-  }
-  const int ne = e.n_e[head];
-  const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
-  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
-  f32x8 vbar[KS];
-#pragma unroll
-  for (int c = 0; c < KS; ++c) {
-    vbar[c] = load_frag(e.s_v + (size_t)head * D + 32 * c + 8 * q4);
-#pragma unroll
-    for (int x = 0; x < 8; ++x) vbar[c][x] *= inv_n;
-  }
   const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
   const T* vc = reinterpret_cast<const T*>(e.v_cache) + (size_t)head * e.cap * D;
   const T* kn = reinterpret_cast<const T*>(e.k_new) + (size_t)head * D;
@@ -178,11 +166,9 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
   const int ML = e.max_len;
   float* rec = e.rec + (size_t)head * (G + 1) * ML;
   const float c2 = e.scale * kLog2e;
-  __syncthreads();  // S_tilde is in LDS
 
-  FragT kf[2][KS], vf[2][KS];
-  for (int j0 = t0 + kEvTB * wave; j0 < t1; j0 += 4 * kEvTB) {
-    // rows j0 + 16 hh + lane % 16: K and V fragments at dims 32 ks + 8 (lane / 16)
+  // rows j0 + 16 hh + lane % 16: K and V fragments at dims 32 ks + 8 (lane / 16)
+  auto load = [&](FragT (&kf)[2][KS], FragT (&vf)[2][KS], int j0) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       const int j = j0 + 16 * hh + r16;
@@ -195,12 +181,51 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
         vf[hh][ks] = ok ? load_frag(vr + 32 * ks + 8 * q4) : zero_frag<T>();
       }
     }
-    f32x4 lg[2];
+  };
+  FragT ka[2][KS], va[2][KS], kb[2][KS], vb[2][KS];
+  int j0 = t0 + kEvTB * wave;
+  if (j0 < t1) load(ka, va, j0);  // in flight while the summary is formed
+
+  // the G queries (rows past G zero) go to LDS as the A fragments of the logits, and
+  // v_bar = s_v / n_e next to them; their reads are issued before the summary's
+  constexpr int QPR = D * (int)sizeof(T) / 16;          // 16-byte pieces per query row
+  constexpr int QPT = (16 * QPR + kEvThreads - 1) / kEvThreads;
+  uint4 qv[QPT];
+  const T* qh = reinterpret_cast<const T*>(e.q) + (size_t)head * G * D;
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int p = threadIdx.x + kEvThreads * u, row = p / QPR;
+    qv[u] = (p < 16 * QPR && row < G)
+                ? *reinterpret_cast<const uint4*>(qh + (size_t)row * D + (p % QPR) * (16 / (int)sizeof(T)))
+                : make_uint4(0, 0, 0, 0);
+  }
+  const int ne = e.n_e[head];
+  const float svv = threadIdx.x < D ? e.s_v[(size_t)head * D + threadIdx.x] : 0.f;
+
+  build_summary<T, D>(e, head, sm);
+
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int p = threadIdx.x + kEvThreads * u;
+    if (p < 16 * QPR)
+      *reinterpret_cast<uint4*>(&s_q[(p / QPR) * QRS + (p % QPR) * (16 / (int)sizeof(T))]) = qv[u];
+  }
+  const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
+  if (threadIdx.x < D) s_vbar[threadIdx.x] = ne > 0 ? svv / (float)ne : 0.f;
+  auto process = [&](const FragT (&kf)[2][KS], const FragT (&vf)[2][KS], int j0) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      lg[hh] = zero4();
+      f32x4 lg = zero4();
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) mma(lg[hh], qf[ks], kf[hh][ks]);
+      for (int ks = 0; ks < KS; ++ks) mma(lg, lds_frag(&s_q[r16 * QRS + 32 * ks + 8 * q4]), kf[hh][ks]);
+      const int j = j0 + 16 * hh + r16;
+      if (j < t1) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int g = 4 * q4 + i;
+          if (g < G) rec[(size_t)g * ML + j] = lg[i] * c2;
+        }
+      }
     }
     // S_tilde k: tile t = 2c + s holds dims 32c + 8 (lane/16) + 4s + i in lane rows
     // 4 (lane/16) + i, i.e. element 4s + i of the lane's V fragment c.
@@ -226,12 +251,13 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
           for (int hh = 0; hh < 2; ++hh) mma(ta[hh], af, kf[hh][ks]);
         }
       }
+      const float4 vb = *reinterpret_cast<const float4*>(&s_vbar[32 * c + 8 * q4 + 4 * s]);
+      const float vbv[4] = {vb.x, vb.y, vb.z, vb.w};
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int x = 4 * s + i;
-          const float r = elem_f(vf[hh][c], x) - vbar[c][x] - cf * ta[hh][i];
+          const float r = elem_f(vf[hh][c], 4 * s + i) - vbv[i] - cf * ta[hh][i];
           rr[hh] += r * r;
         }
       // one tile's LDS reads in flight at a time: hoisting all of them would not fit
@@ -241,24 +267,38 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_scores(EvictArgs e) {
     for (int hh = 0; hh < 2; ++hh) {
       rr[hh] = cross_row_sum(rr[hh]);
       const int j = j0 + 16 * hh + r16;
-      if (j < t1) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int g = 4 * q4 + i;
-          if (g < G) rec[(size_t)g * ML + j] = lg[hh][i] * c2;
-        }
-        if (q4 == 0) rec[(size_t)G * ML + j] = 0.5f * log2f(rr[hh]);
-      }
+      if (j < t1 && q4 == 0) rec[(size_t)G * ML + j] = 0.5f * log2f(rr[hh]);
     }
+  };
+  __syncthreads();  // S_tilde and v_bar are in LDS
+
+  // 32-row blocks j0, j0 + 128, ... of this wave; the next block's rows are requested
+  // before the current block is processed (two register sets)
+  for (; j0 < t1; j0 += 8 * kEvTB) {
+    if (j0 + 4 * kEvTB < t1) load(kb, vb, j0 + 4 * kEvTB);
+    process(ka, va, j0);
+    if (j0 + 4 * kEvTB >= t1) break;
+    if (j0 + 8 * kEvTB < t1) load(ka, va, j0 + 8 * kEvTB);
+    process(kb, vb, j0 + 4 * kEvTB);
   }
 }
 
-template <class T, int D>
-__global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
-  constexpr int GM = 16;
-  __shared__ float s_m[4][GM], s_l[4][GM], s_lz[GM];
-  __shared__ float s_best[4];
-  __shared__ int s_bj[4], s_pick;
+// Selection: 512 threads per KV head (two heads fit on a CU, so a grid of a few hundred
+// heads runs in one round).  Everything that does not depend on the choice
+// (the summary S, the last row, the score records of up to kSelBatch rows per thread) is
+// requested before any of it is used, so a short cache costs three round trips to
+// memory: lens, then the records and S together, then the evicted row.
+// GM bounds the group size G (4, 8 or 16); rows per thread per batch shrink as it grows.
+constexpr int kSelThreads = 512;
+
+template <class T, int D, int GM>
+__global__ void __launch_bounds__(kSelThreads) k_evict_select(EvictArgs e) {
+  constexpr int NW = kSelThreads / kWave;
+  constexpr int UB = GM <= 4 ? 8 : (GM <= 8 ? 4 : 2);
+  constexpr int SPER = D * D / 4 / kSelThreads;  // float4 entries of S per thread
+  __shared__ float s_m[NW][GM], s_l[NW][GM], s_lz[GM];
+  __shared__ float s_best[NW];
+  __shared__ int s_bj[NW], s_pick;
   __shared__ float s_kv[2][D];
   const int head = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -276,25 +316,53 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
     }
     return;
   }
-  const int n_tok = old_len + 1;
+  const int n_tok = old_len + 1, last = n_tok - 1;
   const int G = e.G, ML = e.max_len;
   const float* rec = e.rec + (size_t)head * (G + 1) * ML;
+  T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
+  T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
+  float4* Sh = reinterpret_cast<float4*>(e.S + (size_t)head * D * D);
   if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
+
+  // requests independent of the choice
+  float4 s4[SPER];
+#pragma unroll
+  for (int u = 0; u < SPER; ++u) s4[u] = Sh[tid + kSelThreads * u];
+  T kl = T(), vl = T();
+  if (tid < D) {
+    kl = kc[(size_t)last * D + tid];
+    vl = vc[(size_t)last * D + tid];
+  }
+  float x[UB][GM], y[UB];
+  auto load_batch = [&](int base) {
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int j = base + tid + kSelThreads * u;
+      const bool ok = j < n_tok;
+#pragma unroll
+      for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
+      y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
+    }
+  };
+  const int step = UB * kSelThreads;
+  const int nb = (n_tok + step - 1) / step;
 
   // log2 Z_g over the n_tok rows
   float m[GM], l[GM];
 #pragma unroll
   for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
-  for (int j = tid; j < n_tok; j += kEvThreads) {
+  for (int b = 0; b < nb; ++b) {
+    load_batch(b * step);
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g < G) {
-        const float x = rec[(size_t)g * ML + j];
-        const float mn = fmaxf(m[g], x);
-        l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x - mn);
-        m[g] = mn;
+    for (int u = 0; u < UB; ++u)
+#pragma unroll
+      for (int g = 0; g < GM; ++g) {
+        const float mn = fmaxf(m[g], x[u][g]);
+        if (mn != -INFINITY) {
+          l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x[u][g] - mn);
+          m[g] = mn;
+        }
       }
-    }
   }
 #pragma unroll
   for (int g = 0; g < GM; ++g) {
@@ -308,9 +376,9 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
   if (tid < G) {
     float M = -INFINITY, L = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][tid]);
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][tid]);
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+    for (int w = 0; w < NW; ++w)
       if (s_m[w][tid] != -INFINITY) L += s_l[w][tid] * fast_exp2(s_m[w][tid] - M);
     s_lz[tid] = M + log2f(L);
   }
@@ -323,20 +391,21 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
   const float log2_g = log2f((float)G);
   float best = INFINITY;
   int bj = INT_MAX;
-  for (int j = tid; j < n_tok; j += kEvThreads) {
-    float x[GM];
-    float mx = -INFINITY;
+  for (int b = 0; b < nb; ++b) {
+    if (nb > 1) load_batch(b * step);  // one batch: still in registers
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      x[g] = g < G ? rec[(size_t)g * ML + j] - lz[g] : -INFINITY;
-      mx = fmaxf(mx, x[g]);
+    for (int u = 0; u < UB; ++u) {
+      const int j = b * step + tid + kSelThreads * u;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < GM; ++g) mx = fmaxf(mx, g < G ? x[u][g] - lz[g] : -INFINITY);
+      float sm = 0.f;
+#pragma unroll
+      for (int g = 0; g < GM; ++g)
+        if (g < G) sm += fast_exp2(x[u][g] - lz[g] - mx);
+      const float sc = mx + log2f(sm) - log2_g + y[u];
+      if (j < n_tok && sc < best) { best = sc; bj = j; }  // rows rise along a thread
     }
-    float s = 0.f;
-#pragma unroll
-    for (int g = 0; g < GM; ++g)
-      if (g < G) s += fast_exp2(x[g] - mx);
-    const float sc = mx + log2f(s) - log2_g + rec[(size_t)G * ML + j];
-    if (sc < best) { best = sc; bj = j; }  // rows rise along a thread: ties keep the first
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
@@ -347,11 +416,11 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
   if (lane == 0) { s_best[wave] = best; s_bj[wave] = bj; }
   __syncthreads();
   if (tid == 0) {
-    float b = s_best[0];
+    float bb = s_best[0];
     int j = s_bj[0];
 #pragma unroll
-    for (int w = 1; w < 4; ++w)
-      if (s_best[w] < b || (s_best[w] == b && s_bj[w] < j)) { b = s_best[w]; j = s_bj[w]; }
+    for (int w = 1; w < NW; ++w)
+      if (s_best[w] < bb || (s_best[w] == bb && s_bj[w] < j)) { bb = s_best[w]; j = s_bj[w]; }
     s_pick = j;
   }
   __syncthreads();
@@ -366,12 +435,8 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
   }
 
   // rank-one update and the move of the last row into slot js
-  const int last = n_tok - 1;
-  T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
-  T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
   if (tid < D) {
     const T ks = kc[(size_t)js * D + tid], vs = vc[(size_t)js * D + tid];
-    const T kl = kc[(size_t)last * D + tid], vl = vc[(size_t)last * D + tid];
     const float kf = to_f<T>(ks), vf = to_f<T>(vs);
     s_kv[0][tid] = kf;
     s_kv[1][tid] = vf;
@@ -388,23 +453,28 @@ __global__ void __launch_bounds__(kEvThreads) k_evict_select(EvictArgs e) {
     if (e.evicted) e.evicted[head] = js;
   }
   __syncthreads();
-  float* Sh = e.S + (size_t)head * D * D;
-  for (int idx = tid; idx < D * D / 4; idx += kEvThreads) {
+#pragma unroll
+  for (int u = 0; u < SPER; ++u) {
+    const int idx = tid + kSelThreads * u;
     const int row = idx / (D / 4), c = 4 * (idx % (D / 4));
-    float4 s4 = *reinterpret_cast<const float4*>(Sh + (size_t)row * D + c);
     const float va = s_kv[1][row];
-    s4.x = fmaf(va, s_kv[0][c], s4.x);
-    s4.y = fmaf(va, s_kv[0][c + 1], s4.y);
-    s4.z = fmaf(va, s_kv[0][c + 2], s4.z);
-    s4.w = fmaf(va, s_kv[0][c + 3], s4.w);
-    *reinterpret_cast<float4*>(Sh + (size_t)row * D + c) = s4;
+    s4[u].x = fmaf(va, s_kv[0][c], s4[u].x);
+    s4[u].y = fmaf(va, s_kv[0][c + 1], s4[u].y);
+    s4[u].z = fmaf(va, s_kv[0][c + 2], s4[u].z);
+    s4[u].w = fmaf(va, s_kv[0][c + 3], s4[u].w);
+    Sh[idx] = s4[u];
   }
 }
 
 template <class T, int D>
 static hipError_t launch_evict_t(const EvictArgs& e, hipStream_t st) {
   hipLaunchKernelGGL((k_evict_scores<T, D>), dim3(e.n_heads * e.nslice), dim3(kEvThreads), 0, st, e);
-  hipLaunchKernelGGL((k_evict_select<T, D>), dim3(e.n_heads), dim3(kEvThreads), 0, st, e);
+  if (e.G <= 4)
+    hipLaunchKernelGGL((k_evict_select<T, D, 4>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
+  else if (e.G <= 8)
+    hipLaunchKernelGGL((k_evict_select<T, D, 8>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
+  else
+    hipLaunchKernelGGL((k_evict_select<T, D, 16>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
   return hipGetLastError();
 }
 

@@ -58,7 +58,7 @@ struct EvictArgs {
   float* rec;               // [B*Hkv, G + 1, max_len]  per row: G base-2 logits, log2 ||r||
   int32_t* flag;            // sticky flag: 1 = no room for the new row, 2 = lens past max_len
   int n_heads, G, cap, max_len, budget;
-  int nslice, slice_len;    // scoring workgroups per KV head, rows per workgroup (x 128)
+  int nslice, slice_len;    // scoring workgroups per KV head, rows per workgroup (x 32)
   float scale, tau;
 };
 

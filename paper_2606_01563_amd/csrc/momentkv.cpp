@@ -214,7 +214,8 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
 
 // ------------------------------------------------------------------ decode + eviction
 // Workspace: the decode layout (its flag first), then the per-row score records.  Scoring
-// workgroups: about two per CU over the grid, each a multiple of 128 rows (4 waves x 32).
+// workgroups: about two per CU over the grid, each a multiple of 32 rows and at least 256
+// rows, since each one first forms the head's S_tilde.
 mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws,
                             size_t* total, mkv::DecodeArgs* da) {
   size_t dec = 0;
@@ -229,8 +230,8 @@ mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws
   e.scale = da->scale;
   e.tau = da->tau;
   e.flag = da->flag;
-  const int want = clampi(ceil_div(512, e.n_heads), 1, ceil_div(p->max_len, 128));
-  e.slice_len = ceil_div(ceil_div(p->max_len, want), 128) * 128;
+  const int want = clampi(ceil_div(512, e.n_heads), 1, std::max(1, p->max_len / 256));
+  e.slice_len = ceil_div(ceil_div(p->max_len, want), 32) * 32;
   e.nslice = ceil_div(p->max_len, e.slice_len);
   Carver c;
   c.base = static_cast<char*>(ws);

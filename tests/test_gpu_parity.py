@@ -336,3 +336,18 @@ def test_evict_qwen_stack_layer_full_size_budget_2048():
     worst, swaps, n = P.run_evict_steps(gpu, out, 2, 2048)
     announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
     assert n == 2 * 8 and swaps <= 1
+
+
+@pytest.mark.parametrize("G,budget", [(1, 300), (8, 1100), (16, 1100), (4, 4200)])
+def test_evict_group_sizes_and_long_caches(G, budget):
+    """Group sizes 1, 8 and 16 (the selection's register layouts for G <= 4, <= 8 and
+    <= 16), and rows past one selection batch (more than 4096 rows at G = 4, 1024 at
+    G = 16)."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=2, dtype=torch.bfloat16, head_dim=128,
+                         ctx_len=max(2000, budget + 900), batch=1, n_q_heads=2 * G,
+                         n_kv_heads=2, window=32, budgets=(budget,))
+    out = P.run_compress(gpu, budget, cap=budget + 1)
+    announce(f"evict G={G} budget={budget}")
+    worst, swaps, n = P.run_evict_steps(gpu, out, 2, budget)
+    announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
+    assert n == 4
