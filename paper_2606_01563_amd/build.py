@@ -2,7 +2,7 @@
 
     python -m paper_2606_01563_amd.build        # or __graft_entry__.build()
 
-Sources: csrc/*.hip (kernels) and csrc/momentkv.cpp (C ABI), compiled in parallel to
+Sources: csrc/*.hip (kernels) and csrc/*.cpp (C ABI), compiled in parallel to
 objects under csrc/_build/ and linked into paper_2606_01563_amd/libmomentkv.so.
 Always recompiles (a cheap, explicit "does it build" step).
 """
@@ -43,7 +43,7 @@ def build(verbose: bool = False) -> str:
     if not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     os.makedirs(OBJ, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + [os.path.join(CSRC, "momentkv.cpp")]
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
     jobs = min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
     with ThreadPoolExecutor(jobs) as ex:
         results = list(ex.map(_compile, srcs))

@@ -23,7 +23,7 @@
 #include <climits>
 
 #include "mkv_device.h"
-#include "mkv_launch.h"
+#include "mkv_evict.h"
 
 namespace mkv {
 

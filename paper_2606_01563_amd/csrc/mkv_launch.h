@@ -41,29 +41,6 @@ hipError_t launch_decode(const DecodeArgs& a, bool bf16, int d, hipStream_t st);
 hipError_t launch_prepare_summary(const DecodeArgs& a, void* prepared, bool bf16, int d,
                                   hipStream_t st);
 
-// Decode step with eviction (Algorithm 1 Phase 1): scoring and selection ahead of the
-// corrected attention, which then runs through launch_decode on the updated state.
-struct EvictArgs {
-  const void* q;            // [B, Hq, D]
-  void* k_cache;            // [B, Hkv, cap, D]
-  void* v_cache;
-  int32_t* lens;            // [B, Hkv]
-  const void* k_new;        // [B, Hkv, D]
-  const void* v_new;
-  int32_t* n_e;             // [B, Hkv]      raw summary, updated in place
-  float* s_k;               // [B, Hkv, D]
-  float* s_v;
-  float* S;                 // [B, Hkv, D, D]
-  int32_t* evicted;         // [B, Hkv] or null: slot evicted by this call, -1 if none
-  float* rec;               // [B*Hkv, G + 1, max_len]  per row: G base-2 logits, log2 ||r||
-  int32_t* flag;            // sticky flag: 1 = no room for the new row, 2 = lens past max_len
-  int n_heads, G, cap, max_len, budget;
-  int nslice, slice_len;    // scoring workgroups per KV head, rows per workgroup (x 32)
-  float scale, tau;
-};
-
-hipError_t launch_evict(const EvictArgs& e, bool bf16, int d, hipStream_t st);
-
 struct CompressArgs {
   const void* q_win;        // [B, Hq, w, D]
   const void* k;            // [B, Hkv, N, D]

@@ -7,36 +7,17 @@
 #include <cstring>
 
 #include "../../include/momentkv.h"
+#include "mkv_abi.h"
 #include "mkv_launch.h"
+
+using namespace mkv::abi;
 
 namespace {
 
-constexpr size_t kAlign = 256;
 constexpr int kMaxCandidates = 1 << 18;  // top-k: at most 128 slices of 2048 candidates
 constexpr int64_t kDecodeWaves = 768;      // target slice count of an automatic decode split
 constexpr int64_t kMaxDecodeWaves = 1 << 24;  // decode grid limit (single-wave workgroups)
 constexpr int kFusedMaxLen = 384;          // automatic decode: single launch up to this length
-
-inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
-inline int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
-
-struct Carver {
-  size_t off = 0;
-  char* base = nullptr;
-  template <class P> P* take(size_t bytes) {
-    P* p = base ? reinterpret_cast<P*>(base + off) : nullptr;
-    off += align_up(bytes);
-    return p;
-  }
-};
-
-bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
-  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
-  return x < y + nb && y < x + na;
-}
-
-size_t elem_size(int32_t dtype) { return dtype == MKV_BF16 ? 2 : 4; }
 
 // ----------------------------------------------------------------------- compress
 mkv_status check_compress_params(const mkv_compress_params* p) {
@@ -164,6 +145,11 @@ bool decode_fused(const mkv_decode_params* p) {
   return p->n_split == 1 || (p->n_split == 0 && p->max_len <= kFusedMaxLen);
 }
 
+}  // namespace
+
+namespace mkv {
+namespace abi {
+
 mkv_status check_decode_params(const mkv_decode_params* p) {
   if (!p) return MKV_ERR_NULL;
   if (p->dtype != MKV_F32 && p->dtype != MKV_BF16) return MKV_ERR_DTYPE;
@@ -212,44 +198,8 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   return a;
 }
 
-// ------------------------------------------------------------------ decode + eviction
-// Workspace: the decode layout (its flag first), then the per-row score records.  Scoring
-// workgroups: about two per CU over the grid, each a multiple of 32 rows and at least 256
-// rows, since each one first forms the head's S_tilde.
-mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws,
-                            size_t* total, mkv::DecodeArgs* da) {
-  size_t dec = 0;
-  *da = decode_layout(p, ws, &dec);
-  mkv::EvictArgs e;
-  std::memset(&e, 0, sizeof e);
-  e.n_heads = da->n_heads;
-  e.G = da->G;
-  e.cap = p->cap;
-  e.max_len = p->max_len;
-  e.budget = budget;
-  e.scale = da->scale;
-  e.tau = da->tau;
-  e.flag = da->flag;
-  const int want = clampi(ceil_div(512, e.n_heads), 1, std::max(1, p->max_len / 256));
-  e.slice_len = ceil_div(ceil_div(p->max_len, want), 32) * 32;
-  e.nslice = ceil_div(p->max_len, e.slice_len);
-  Carver c;
-  c.base = static_cast<char*>(ws);
-  c.off = dec;
-  e.rec = c.take<float>((size_t)e.n_heads * (e.G + 1) * p->max_len * sizeof(float));
-  *total = c.off;
-  return e;
-}
-
-mkv_status check_evict_params(const mkv_decode_params* p, int32_t budget) {
-  mkv_status st = check_decode_params(p);
-  if (st != MKV_OK) return st;
-  if (p->summary != 0) return MKV_ERR_SHAPE;
-  if (budget < 1) return MKV_ERR_BUDGET;
-  return MKV_OK;
-}
-
-}  // namespace
+}  // namespace abi
+}  // namespace mkv
 
 extern "C" {
 
@@ -381,73 +331,6 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
   hipError_t e = mkv::launch_decode(a, p->dtype == MKV_BF16, p->head_dim,
                                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MKV_OK : MKV_ERR_HIP;
-}
-
-size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p) {
-  if (check_evict_params(p, 1) != MKV_OK) return 0;
-  size_t total = 0;
-  mkv::DecodeArgs da;
-  evict_layout(p, 1, nullptr, &total, &da);
-  return total;
-}
-
-mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, const void* q,
-                                 void* k_cache, void* v_cache, int32_t* lens,
-                                 const void* k_new, const void* v_new, int32_t* n_e,
-                                 float* s_k, float* s_v, float* S, void* out, float* lse_out,
-                                 float* w_r_out, int32_t* evicted_out, void* workspace,
-                                 size_t workspace_bytes, void* stream) {
-  mkv_status st = check_evict_params(p, budget);
-  if (st != MKV_OK) return st;
-  if (!q || !k_cache || !v_cache || !lens || !k_new || !v_new || !n_e || !s_k || !s_v || !S || !out)
-    return MKV_ERR_NULL;
-  size_t need = 0;
-  mkv::DecodeArgs da;
-  evict_layout(p, budget, nullptr, &need, &da);
-  if (!workspace || workspace_bytes < need) return MKV_ERR_WORKSPACE;
-  if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return MKV_ERR_WORKSPACE;
-  const size_t es = elem_size(p->dtype);
-  const size_t heads = (size_t)p->batch * p->n_kv_heads, d = p->head_dim;
-  const size_t cache_bytes = heads * p->cap * d * es;
-  const size_t out_bytes = (size_t)p->batch * p->n_q_heads * d * es;
-  const size_t s_bytes = heads * d * d * 4, vec_bytes = heads * d * 4;
-  const void* outs[] = {k_cache, v_cache, out, S, s_k, s_v, workspace};
-  const size_t outn[] = {cache_bytes, cache_bytes, out_bytes, s_bytes, vec_bytes, vec_bytes, need};
-  for (int i = 0; i < 7; ++i)
-    for (int j = i + 1; j < 7; ++j)
-      if (ranges_overlap(outs[i], outn[i], outs[j], outn[j])) return MKV_ERR_ALIAS;
-  if (ranges_overlap(out, out_bytes, q, out_bytes)) return MKV_ERR_ALIAS;
-  size_t total = 0;
-  mkv::EvictArgs e = evict_layout(p, budget, workspace, &total, &da);
-  e.q = q;
-  e.k_cache = k_cache;
-  e.v_cache = v_cache;
-  e.lens = lens;
-  e.k_new = k_new;
-  e.v_new = v_new;
-  e.n_e = n_e;
-  e.s_k = s_k;
-  e.s_v = s_v;
-  e.S = S;
-  e.evicted = evicted_out;
-  const hipStream_t hs = static_cast<hipStream_t>(stream);
-  hipError_t err = mkv::launch_evict(e, p->dtype == MKV_BF16, p->head_dim, hs);
-  if (err != hipSuccess) return MKV_ERR_HIP;
-  da.q = q;
-  da.k_cache = k_cache;
-  da.v_cache = v_cache;
-  da.lens = lens;
-  da.k_new = nullptr;  // appended by the eviction step
-  da.v_new = nullptr;
-  da.n_e = n_e;
-  da.s_k = s_k;
-  da.s_v = s_v;
-  da.S = S;
-  da.out = out;
-  da.lse_out = lse_out;
-  da.w_r_out = w_r_out;
-  err = mkv::launch_decode(da, p->dtype == MKV_BF16, p->head_dim, hs);
-  return err == hipSuccess ? MKV_OK : MKV_ERR_HIP;
 }
 
 const char* momentkv_status_string(int32_t s) {
