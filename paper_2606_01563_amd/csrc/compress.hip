@@ -26,7 +26,7 @@
 //  12 k_reduce        final raw moments S, s_k, s_v, n_e.
 // Every reduction has a fixed order, so results are bit-reproducible.
 #include "mkv_device.h"
-#include "mkv_launch.h"
+#include "mkv_compress.h"
 
 namespace mkv {
 

@@ -31,7 +31,7 @@
 // written to row lens of the cache by the wave whose range holds that row and is attended
 // to from k_new / v_new, so no cache read depends on the append.
 #include "mkv_device.h"
-#include "mkv_launch.h"
+#include "mkv_decode.h"
 
 namespace mkv {
 

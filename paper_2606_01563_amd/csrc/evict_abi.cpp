@@ -10,7 +10,7 @@
 #include "../../include/momentkv.h"
 #include "mkv_abi.h"
 #include "mkv_evict.h"
-#include "mkv_launch.h"
+#include "mkv_decode.h"
 
 using namespace mkv::abi;
 

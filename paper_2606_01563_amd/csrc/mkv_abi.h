@@ -6,7 +6,7 @@
 #include <cstdint>
 
 #include "../../include/momentkv.h"
-#include "mkv_launch.h"
+#include "mkv_decode.h"
 
 namespace mkv {
 namespace abi {
