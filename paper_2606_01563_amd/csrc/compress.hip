@@ -6,10 +6,12 @@
 //                     per-row online (max, sum) over the visible keys; for candidate
 //                     tokens also the covariance V^T K on MFMA (tiles transposed through
 //                     LDS), the sums s_k, s_v and ||v_j||.                 [reads K, V]
-//   2 k_row_combine   per head: merge the row partials in slice order -> (max, 1/Z).
+//   2 k_row_combine   per head: merge the row partials in slice order -> (max, 1/Z);
+//                     zeroes the head's two top-k key histograms.
 //   3 k_mass          per (slice, head): logits again, softmax mass summed over the
 //                     window rows -> a_j, aligned chunk pooling -> abar_j,
-//                     provisional score abar_j ||v_j||.                    [reads K]
+//                     provisional score abar_j ||v_j||, added to the key histogram of
+//                     the first selection.                                 [reads K]
 //   4 k_tk_*          per head: radix select of the k_keep best scores, lower position
 //                     first on ties; writes the kept positions in ascending order.
 //   5 k_gather_rows   rows of the provisional kept set into a compact buffer.
@@ -18,8 +20,8 @@
 //                     evicted set.
 //   8 k_residual      per (slice, head): centring and clamp of the provisional summary
 //                     into LDS (fp32, or a bf16 hi/lo pair), S_tilde k_j on MFMA,
-//                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm.
-//                                                                          [reads K, V]
+//                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm,
+//                     added to the final selection's key histogram.       [reads K, V]
 //   9 k_tk_*          final kept set.
 //  10 k_gather_out    retained rows (sinks, kept, window) -> k_out/v_out, idx, lens.
 //  11 k_cov_rows      covariance of the final kept rows (from k_out), negated.
@@ -31,6 +33,31 @@
 namespace mkv {
 
 constexpr int TILE = 64;  // tokens per tile
+
+// Top-k selection (lowest score evicted first): scores as monotone 32-bit keys, a
+// per-head histogram of key bits 30..20 filled by the kernel that produces the scores,
+// then slices of TKS positions.
+constexpr int TKS = 2048;          // positions per slice
+constexpr int TKT = 256;           // threads per slice workgroup
+constexpr int TKPT = TKS / TKT;    // consecutive positions per thread
+constexpr int TK_BINS0 = 2048;
+constexpr int TK_MAX_SLICES = 128; // 262144 candidates
+constexpr int TK_CAND_LDS = 8192;  // candidates of the k-th key's bin staged in LDS
+
+__device__ __forceinline__ uint32_t score_key(float s) {
+  uint32_t u = __float_as_uint(s);
+  return (u & 0x80000000u) ? 0u : u;  // -0 and negatives sort as 0
+}
+
+constexpr int TK_HBINS = 2048;     // bins of the per-head histogram (key bits 30..20)
+
+// Adds a workgroup's LDS histogram to the head's histogram in global memory (integer
+// atomics: the result is exact whatever the order).
+template <int NT>
+__device__ __forceinline__ void hist_flush(const uint32_t* lh, uint32_t* gh) {
+  for (int b = threadIdx.x; b < TK_HBINS; b += NT)
+    if (lh[b]) atomicAdd(&gh[b], lh[b]);
+}
 
 __device__ __forceinline__ void store_frag(bf16_t* p, const bf16x8& f) {
   *reinterpret_cast<uint4*>(p) = __builtin_bit_cast(uint4, f);
@@ -421,6 +448,9 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
 // ------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) k_row_combine(CompressArgs a) {
   const int head = blockIdx.y;
+  if (blockIdx.x == 0)  // the score producers below add into these
+    for (int b = threadIdx.x; b < 2 * TK_HBINS; b += 256)
+      a.tk_hh[((size_t)(b / TK_HBINS) * a.H + head) * TK_HBINS + b % TK_HBINS] = 0u;
   const int r = blockIdx.x * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
   float m = -INFINITY, l = 0.f;
@@ -454,6 +484,7 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
   __shared__ float sA[4][TILE];
   __shared__ float sAj[TILE];
   __shared__ float sRow[512][2];
+  __shared__ uint32_t sHist[TK_HBINS];  // keys of the first selection's scores
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
@@ -467,6 +498,7 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
     sRow[r][0] = a.rowstat[((size_t)head * a.R + r) * 2 + 0];
     sRow[r][1] = a.rowstat[((size_t)head * a.R + r) * 2 + 1];
   }
+  for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = 0u;
   typename Frag<T>::type qf[MTW][KS];
 #pragma unroll
   for (int k = 0; k < MTW; ++k) {
@@ -539,42 +571,33 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
         for (int i = lo; i < hi; ++i) s += sAj[i - tok0];
         const float ab = s / (float)(hi - lo);
         const size_t o = (size_t)head * a.n_c + (j - c_lo);
+        const float s0 = ab * a.vnorm[o];
         a.abar[o] = ab;
-        a.score0[o] = ab * a.vnorm[o];
+        a.score0[o] = s0;
+        atomicAdd(&sHist[score_key(a.mi_rounds < 0 ? ab : s0) >> 20], 1u);
       }
     }
     __syncthreads();
   }
+  hist_flush<256>(sHist, a.tk_hh + (size_t)head * TK_HBINS);
 }
 
 // ------------------------------------------------------------------------------------
 // Stage 4/9: per-head selection of the k best scores (ties: lower position first),
 // output in ascending position order.  Scores are non-negative floats, so their bit
-// patterns (bit 31 clear) order like unsigned integers ("keys").  Every full pass over a
-// head's keys runs over slices of TKS positions spread over all CUs:
-//   k_tk_hist   slices x heads: histogram of key bits 30..20 per slice;
-//   k_tk_bin    one workgroup per head: sums the slice histograms in a fixed order and
-//               finds the bin B of the k-th largest key and the count of keys above B;
-//   k_tk_cand   slices x heads: counts the slice's keys above B and writes its keys inside
-//               B (the candidates) in position order;
+// patterns (bit 31 clear) order like unsigned integers ("keys").  The kernel producing
+// the scores (k_mass, k_residual) also adds each key's bits 30..20 into the head's
+// histogram; then two launches over slices of TKS positions spread over all CUs:
+//   k_tk_cand   slices x heads: from the head's histogram, the bin B of the k-th largest
+//               key and the count of keys above B (every slice finds the same); counts the
+//               slice's keys above B and writes its keys inside B (the candidates) in
+//               position order;
 //   k_tk_write  slices x heads: refines bits 19..10 and 9..0 over the head's candidates
 //               (few: one bin spans an eighth of an octave), which gives the k-th key T and
 //               how many keys equal to T are kept (the lowest positions); from the per-slice
 //               counts it gets its slice's output offset and share of equal keys, then
 //               writes the slice's kept positions in order.
 // ------------------------------------------------------------------------------------
-constexpr int TKS = 2048;          // positions per slice
-constexpr int TKT = 256;           // threads per slice workgroup
-constexpr int TKPT = TKS / TKT;    // consecutive positions per thread
-constexpr int TK_BINS0 = 2048;
-constexpr int TK_MAX_SLICES = 128; // 262144 candidates
-constexpr int TK_CAND_LDS = 8192;  // candidates of the k-th key's bin staged in LDS
-
-__device__ __forceinline__ uint32_t score_key(float s) {
-  uint32_t u = __float_as_uint(s);
-  return (u & 0x80000000u) ? 0u : u;  // -0 and negatives sort as 0
-}
-
 // Exclusive scan of one int per thread over an NT-thread block; the total goes to *total.
 // sW holds 2 * NT / 64 + 1 ints.
 template <int NT>
@@ -642,62 +665,26 @@ __device__ __forceinline__ void slice_keys(const float* s, int n, int sl, uint32
   }
 }
 
-__global__ void __launch_bounds__(TKT) k_tk_hist(const float* __restrict__ scores, int n,
-                                                   uint32_t* __restrict__ hist) {
-  __shared__ uint32_t h[TK_BINS0];
-  const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x, tid = threadIdx.x;
-  for (int b = tid; b < TK_BINS0; b += TKT) h[b] = 0;
-  __syncthreads();
-  const float* s = scores + (size_t)head * n;
-  float v[TKPT];
-#pragma unroll
-  for (int u = 0; u < TKPT; ++u) {  // coalesced: consecutive threads, consecutive positions
-    const int j = sl * TKS + u * TKT + tid;
-    v[u] = j < n ? s[j] : 0.f;
-  }
-#pragma unroll
-  for (int u = 0; u < TKPT; ++u)
-    if (sl * TKS + u * TKT + tid < n) atomicAdd(&h[score_key(v[u]) >> 20], 1u);
-  __syncthreads();
-  uint32_t* o = hist + ((size_t)head * ntk + sl) * TK_BINS0;
-  for (int b = tid; b < TK_BINS0; b += TKT) o[b] = h[b];
-}
-
-__global__ void __launch_bounds__(1024) k_tk_bin(const uint32_t* __restrict__ hist, int ntk, int k,
-                                                 int* __restrict__ state) {
-  __shared__ uint32_t hst[TK_BINS0];
-  __shared__ uint32_t sh_bin, sh_above;
-  __shared__ int sW[2 * 16 + 1];
-  const int head = blockIdx.x;
-  for (int b = threadIdx.x; b < TK_BINS0; b += 1024) {
-    uint32_t c = 0;
-    for (int s0 = 0; s0 < ntk; s0 += 8) {  // eight slices' loads in flight
-      uint32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        v[u] = s0 + u < ntk ? hist[((size_t)head * ntk + s0 + u) * TK_BINS0 + b] : 0u;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) c += v[u];
-    }
-    hst[b] = c;
-  }
-  __syncthreads();
-  find_bin<1024>(hst, TK_BINS0, k, sW, &sh_bin, &sh_above);
-  if (threadIdx.x == 0) {
-    state[2 * head] = (int)sh_bin;
-    state[2 * head + 1] = (int)sh_above;
-  }
-}
-
-__global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ scores, int n,
-                                                   const int* __restrict__ state,
+__global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ scores, int n, int k,
+                                                   const uint32_t* __restrict__ hh,
+                                                   int* __restrict__ state,
                                                    int* __restrict__ cnt, uint32_t* __restrict__ cand) {
   __shared__ int sW[2 * (TKT / 64) + 1];
+  __shared__ uint32_t hst[TK_HBINS];
+  __shared__ uint32_t sh_bin, sh_above;
   const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x;
-  const uint32_t B = (uint32_t)state[2 * head];
   uint32_t key[TKPT];
   bool valid[TKPT];
   slice_keys(scores + (size_t)head * n, n, sl, key, valid);
+  // the head's histogram (every slice workgroup finds the same bin of the k-th key)
+  for (int b = threadIdx.x; b < TK_HBINS; b += TKT) hst[b] = hh[(size_t)head * TK_HBINS + b];
+  __syncthreads();
+  find_bin<TKT>(hst, TK_HBINS, k, sW, &sh_bin, &sh_above);
+  const uint32_t B = sh_bin;
+  if (sl == 0 && threadIdx.x == 0) {
+    state[2 * head] = (int)sh_bin;
+    state[2 * head + 1] = (int)sh_above;
+  }
   int n_gt = 0, n_c = 0;
 #pragma unroll
   for (int u = 0; u < TKPT; ++u) {
@@ -989,7 +976,9 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
   __shared__ __align__(16) T sV[TILE][LDK];
   __shared__ float sRho[4][TILE];
   __shared__ float sSv[D], sSk[D];
+  __shared__ uint32_t sHist[TK_HBINS];  // keys of the final selection's scores
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = 0u;
   const int head = blockIdx.y, sl = blockIdx.x;
   const int c_lo = a.n_s, c_hi = a.N - a.w;
   const float n0 = (float)(a.n_c - a.k_keep);
@@ -1110,11 +1099,14 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
       if (j < c_hi) {
         const float x = ((sRho[0][tid] + sRho[1][tid]) + sRho[2][tid]) + sRho[3][tid];
         const size_t o = (size_t)head * a.n_c + (j - c_lo);
-        a.score[o] = a.abar[o] * sqrtf(x);
+        const float sc = a.abar[o] * sqrtf(x);
+        a.score[o] = sc;
+        atomicAdd(&sHist[score_key(sc) >> 20], 1u);
       }
     }
     __syncthreads();
   }
+  hist_flush<256>(sHist, a.tk_hh + ((size_t)a.H + head) * TK_HBINS);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1162,16 +1154,13 @@ __global__ void __launch_bounds__(256) k_zero_moments(CompressArgs a) {
     if (e_ != hipSuccess) return e_;        \
   } while (0)
 
-static hipError_t launch_topk(const CompressArgs& a, const float* scores, int32_t* out,
-                              hipStream_t st) {
+// `which` selects the histogram the score producer filled (0: first selection, 1: final).
+static hipError_t launch_topk(const CompressArgs& a, const float* scores, int which,
+                              int32_t* out, hipStream_t st) {
   if (a.k_keep <= 0) return hipSuccess;
   const dim3 grid(a.ntk, a.H);
-  hipLaunchKernelGGL(k_tk_hist, grid, dim3(TKT), 0, st, scores, a.n_c, a.tk_hist);
-  MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_tk_bin, dim3(a.H), dim3(1024), 0, st, (const uint32_t*)a.tk_hist, a.ntk,
-                     a.k_keep, a.tk_state);
-  MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_tk_cand, grid, dim3(TKT), 0, st, scores, a.n_c, (const int*)a.tk_state,
+  hipLaunchKernelGGL(k_tk_cand, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep,
+                     (const uint32_t*)(a.tk_hh + (size_t)which * a.H * TK_HBINS), a.tk_state,
                      a.tk_cnt, a.tk_cand);
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep,
@@ -1203,7 +1192,7 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
   MKV_CHECK_LAUNCH();
   const float* first_scores = a.mi_rounds < 0 ? a.abar : a.score0;
   int32_t* first_out = a.mi_rounds >= 1 ? a.kept0 : a.kept;
-  hipError_t te = launch_topk(a, first_scores, first_out, st);
+  hipError_t te = launch_topk(a, first_scores, 0, first_out, st);
   if (te != hipSuccess) return te;
   const dim3 red_grid(((D * D + 2 * D) / 4 + 31) / 32, H);
   if (a.mi_rounds >= 1) {
@@ -1218,7 +1207,7 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
     MKV_CHECK_LAUNCH();
     hipLaunchKernelGGL((k_residual<T, D>), dim3(a.nsl3, H), blk, 0, st, a);
     MKV_CHECK_LAUNCH();
-    te = launch_topk(a, a.score, a.kept, st);
+    te = launch_topk(a, a.score, 1, a.kept, st);
     if (te != hipSuccess) return te;
   }
   hipLaunchKernelGGL((k_gather_out<T, D>), dim3((a.L * (D / 8) + 255) / 256, H), blk, 0, st, a, a.L, 0);

@@ -107,7 +107,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.score = c.take<float>(H * nc * sizeof(float));
   a.kept0 = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
   a.kept = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
-  a.tk_hist = c.take<uint32_t>(H * a.ntk * 2048 * sizeof(uint32_t));
+  a.tk_hh = c.take<uint32_t>(2 * H * 2048 * sizeof(uint32_t));
   a.tk_state = c.take<int32_t>(H * 2 * sizeof(int32_t));
   a.tk_cnt = c.take<int32_t>(H * a.ntk * 2 * sizeof(int32_t));
   a.tk_cand = c.take<uint32_t>(H * a.ntk * 2048 * sizeof(uint32_t));

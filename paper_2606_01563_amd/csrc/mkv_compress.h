@@ -28,7 +28,8 @@ struct CompressArgs {
   float* score;             // [H, n_c]          moment-round score
   int32_t* kept0;           // [H, kmax]         provisional kept positions (ascending)
   int32_t* kept;            // [H, kmax]         final kept positions (ascending)
-  uint32_t* tk_hist;        // [H, ntk, 2048]    top-k: histograms of key bits 30..20
+  uint32_t* tk_hh;          // [2, H, 2048]      top-k: per-head histograms of key bits 30..20
+                            //                   of the first and the final scores
   int32_t* tk_state;        // [H, 2]            top-k: bin of the k-th key, count above it
   int32_t* tk_cnt;          // [H, ntk, 2]       top-k: per slice, keys above the bin, in it
   uint32_t* tk_cand;        // [H, ntk, 2048]    top-k: per slice, the keys in the bin
