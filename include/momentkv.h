@@ -164,7 +164,8 @@ typedef struct {
   int32_t head_dim;     /* d in {64, 128}                                            */
   int32_t cap;          /* rows per head of the cache                                */
   int32_t max_len;      /* upper bound of lens after the append, 1 <= max_len <= cap */
-  int32_t order;        /* 1 = first order (default), 0 = v_bar only                 */
+  int32_t order;        /* 1 = first order (default), 0 = v_bar only, -1 = no        */
+                        /* correction (out = f_R, w_R = 1: the uncorrected ablation) */
   int32_t dtype;        /* mkv_dtype of q, caches, k_new, v_new, out                 */
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
   float tau;            /* covariance clamp threshold, >= 0                          */

@@ -26,6 +26,8 @@ Pinning status (what fixes each function other than itself; see tests/):
   decode                  pinned: no-eviction == SDPA, zero key spread == full
                           attention, second-order error, Jensen bound, weight bias
   greedy_evict            quality reference only (parity unpinned; no printed example)
+  eviction_diagnostics    built from attention_parts and decode_head (pinned above); the
+                          order = -1 ablation pinned to SDPA over the retained rows
   evict_scores_head       pinned: planted zero-residual token, alpha ordering at equal
                           residual norms, n_e = 0 reduction to alpha ||v||
   decode_evict            pinned: zero key spread (evicts the value nearest the mean and
@@ -48,7 +50,8 @@ __all__ = [
     "centered_moments", "moment_residuals", "residual_scores", "select_candidates",
     "compress", "compress_head",
     "decode", "decode_head", "append_tokens", "attention_parts", "greedy_evict",
-    "evict_scores_head", "decode_evict_head", "decode_evict", "moment_storage_bytes",
+    "evict_scores_head", "decode_evict_head", "decode_evict", "eviction_diagnostics",
+    "moment_storage_bytes",
 ]
 
 
@@ -357,7 +360,8 @@ def decode_head(q, k_ret, v_ret, m: Moments, *, scale: float | None = None,
       f_E_hat    = v_bar + S_tilde q / (n_e sqrt(d))                          (Eq. fhat)
       log w_R    = log Z_R - logsumexp(log Z_R, log Z_E_hat)                 (App. C.2)
       out        = w_R f_R + (1 - w_R) f_E_hat                               (Eq. fused)
-    order = 0 drops the covariance term (zeroth-order variant, f_E_hat = v_bar).
+    order = 0 drops the covariance term (zeroth-order variant, f_E_hat = v_bar);
+    order = -1 drops the correction altogether (out = f_R, the ablation without it).
     """
     q = _f64(q)
     K = _f64(k_ret)
@@ -377,7 +381,7 @@ def decode_head(q, k_ret, v_ret, m: Moments, *, scale: float | None = None,
     else:
         f_R = np.zeros(d, F64)
         log_Z_R = -math.inf
-    if m.n_e == 0:
+    if m.n_e == 0 or order < 0:
         return DecodeResult(f_R, f_R, log_Z_R, 1.0, None, None)
     k_bar, v_bar, S_t = centered_moments(m, tau)
     s_bar = float(scale * (q @ k_bar))
@@ -470,6 +474,37 @@ def attention_parts(q, k, v, retained, scale: float | None = None) -> dict:
                 log_Z_R=float(mx + math.log(Z_R)) if Z_R > 0 else -math.inf,
                 log_Z_E=float(mx + math.log(Z_E)) if Z_E > 0 else -math.inf,
                 cos_theta=cos, gamma=gamma)
+
+
+def eviction_diagnostics(q, k, v, retained, *, scale: float | None = None, tau: float = 1e-6,
+                         order: int = 1) -> dict:
+    """Exact quantities of Sec. 3 and Sec. 4 for one query against one head's full context:
+    the evicted weight w_E, cos(theta) between f_E and f_R (Fig. 2), the relative errors
+    of f_R and of the corrected output against full attention f (Eq. relative_error), and
+    how close the moment estimate is to the evicted output: cos(f_E, f_E_hat) and
+    ||f_E_hat - f_E|| / ||f_E|| (Fig. 3).  E is everything not retained; the summary is its
+    exact moments.  Diagnostics only (tests)."""
+    K = _f64(k)
+    V = _f64(v)
+    qq = _f64(q)
+    d = qq.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    parts = attention_parts(qq, K, V, retained, scale)
+    R = np.asarray(retained, dtype=np.int64)
+    E = np.setdiff1d(np.arange(K.shape[0]), R)
+    m = evicted_moments(K, V, E)
+    r = decode_head(qq, K[R], V[R], m, scale=scale, tau=tau, order=order)
+    f, f_E = parts["f"], parts["f_E"]
+    nf = np.linalg.norm(f)
+    out = dict(w_E=parts["w_E"], cos_theta=parts["cos_theta"],
+               rel_err_retained=float(np.linalg.norm(parts["f_R"] - f) / nf),
+               rel_err_corrected=float(np.linalg.norm(r.out - f) / nf))
+    if r.f_E_hat is not None:
+        nE, nH = np.linalg.norm(f_E), np.linalg.norm(r.f_E_hat)
+        out["cos_fE_fEhat"] = float(f_E @ r.f_E_hat / (nE * nH)) if nE > 0 and nH > 0 else float("nan")
+        out["rel_err_fEhat"] = float(np.linalg.norm(r.f_E_hat - f_E) / nE) if nE > 0 else float("nan")
+    return out
 
 
 def greedy_evict(alpha, k, v, protected, budget: int, scale: float | None = None,

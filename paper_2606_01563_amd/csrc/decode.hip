@@ -460,6 +460,7 @@ __device__ __forceinline__ void finish_query(const DecodeArgs& a, int bh, int g,
                                              const QueryCols<D / 64>& qc, const float (&sqv)[D / 64],
                                              bool use_sq, int ne, bool add_new) {
   constexpr int CPL = D / 64;
+  if (a.order < 0) ne = 0;  // no correction: the output is f_R, as with an empty summary
   float dot_k = 0.f, dot_s = 0.f;
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {

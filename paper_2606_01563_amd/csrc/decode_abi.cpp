@@ -51,7 +51,7 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
   if (p->batch < 1 || p->n_q_heads < 1 || p->n_kv_heads < 1 || p->head_dim < 1 || p->cap < 1)
     return MKV_ERR_SHAPE;
   if (p->n_q_heads % p->n_kv_heads) return MKV_ERR_SHAPE;
-  if (p->order != 0 && p->order != 1) return MKV_ERR_SHAPE;
+  if (p->order < -1 || p->order > 1) return MKV_ERR_SHAPE;
   if (!(p->scale >= 0.f) || !std::isfinite(p->scale) || !(p->tau >= 0.f) || !std::isfinite(p->tau))
     return MKV_ERR_SHAPE;
   if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;

@@ -136,10 +136,44 @@ def test_long_window_group_rows_256():
     P.run_decode_steps(gpu, out, 2)
 
 
-def test_zeroth_order_decode_and_no_append():
+@pytest.mark.parametrize("order", [0, -1])
+def test_zeroth_order_or_no_correction_decode_and_no_append(order):
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, ctx_len=600, budgets=(64,))
     out = P.run_compress(gpu, 64, cap=64)
-    P.run_decode_steps(gpu, out, 3, order=0, append=False)
+    P.run_decode_steps(gpu, out, 3, order=order, append=False)
+
+
+def test_ablations_correction_lowers_error_against_full_attention():
+    """Synthetic analog of the component ablation (Sec. 5.3): for the SnapKV-style selection
+    (mi_rounds = -1) and the moment-informed one (mi_rounds = 1), the corrected decode
+    (order 1) is closer to exact attention over the whole context than the uncorrected one
+    (order -1), averaged over the queries; the errors of all four are reported."""
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=4)
+    L = 128
+    N, d = wl.ctx_len, wl.head_dim
+    G = wl.group
+    errs = {}
+    for mi in (-1, 1):
+        out = P.run_compress(gpu, L, cap=L, mi_rounds=mi)
+        for order in (-1, 1):
+            e = []
+            for t in range(4):
+                q = gpu["q_dec"][t]
+                res, _, _, _ = mk.momentkv_decode_attn(q, out.k_out, out.v_out, out.lens, out.n_e,
+                                                       out.s_k, out.s_v, out.S, order=order,
+                                                       max_len=L)
+                # exact attention over all N prefill rows (fp32; the group's KV head)
+                kf = gpu["k"][0].float()
+                vf = gpu["v"][0].float()
+                qf = q[0].float().view(wl.n_kv_heads, G, d)
+                s = torch.matmul(qf, kf.transpose(1, 2).contiguous()) / math.sqrt(d)
+                full = torch.matmul(torch.softmax(s, -1), vf).reshape(-1, d)
+                e.append(float(((res[0].float() - full).norm(dim=-1) / full.norm(dim=-1)).mean()))
+            errs[(mi, order)] = sum(e) / len(e)
+    announce("mean rel err vs full attention " +
+             ", ".join(f"mi={k[0]} order={k[1]}: {v:.4f}" for k, v in sorted(errs.items())))
+    for mi in (-1, 1):
+        assert errs[(mi, 1)] < errs[(mi, -1)]
 
 
 def test_append_into_full_cache_sets_flag_and_skips():

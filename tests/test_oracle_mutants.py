@@ -68,6 +68,7 @@ MUTANTS = {
                               "m = Moments(m.n_e, m.s_k + kj, m.s_v + vj, m.S + np.outer(vj, kj))"),
     "evict_no_slot_move": ("        kc[evicted] = kc[n - 1]\n", "\n"),
     "evict_at_budget": ("    if n > budget:\n", "    if n >= budget:\n"),
+    "no_correction_ignored": ("    if m.n_e == 0 or order < 0:", "    if m.n_e == 0:"),
 }
 
 PIN_TESTS = [name for name in dir(pins) if name.startswith("test_")]

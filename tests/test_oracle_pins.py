@@ -195,6 +195,38 @@ def test_decode_without_eviction_is_softmax_attention():
     np.testing.assert_allclose(r.log_Z_R, lse(K @ q / math.sqrt(d)), rtol=1e-13)
 
 
+def test_decode_without_correction_is_softmax_attention_over_retained():
+    """order = -1 (the ablation without the correction) returns textbook attention over
+    the retained rows whatever the summary, with w_R = 1."""
+    rng = np.random.default_rng(19)
+    d = 12
+    q, K, V, R, E = _split_case(rng, spread=1.0, q_norm=2.0)
+    m = O.evicted_moments(K, V, E)
+    assert m.n_e > 0
+    r = O.decode_head(q, K[R], V[R], m, order=-1)
+    np.testing.assert_allclose(r.out, sdpa(q[None], K[R], V[R], 1 / math.sqrt(len(q)))[0],
+                               rtol=1e-12)
+    assert r.w_R == 1.0
+
+
+def test_eviction_diagnostics_against_library_attention():
+    """The diagnostics are the paper's quantities: w_E from torch softmax weights, the
+    relative error of f_R against SDPA over every row, and the corrected output closer to
+    full attention than f_R on this planted-covariance case."""
+    rng = np.random.default_rng(20)
+    q, K, V, R, E = _split_case(rng, spread=0.3, q_norm=2.0)
+    d = len(q)
+    dg = O.eviction_diagnostics(q, K, V, R)
+    w = torch.softmax(torch.from_numpy(K @ q / math.sqrt(d)), 0).numpy()
+    np.testing.assert_allclose(dg["w_E"], w[E].sum(), rtol=1e-12)
+    full = sdpa(q[None], K, V, 1 / math.sqrt(d))[0]
+    f_R = sdpa(q[None], K[R], V[R], 1 / math.sqrt(d))[0]
+    np.testing.assert_allclose(dg["rel_err_retained"],
+                               np.linalg.norm(f_R - full) / np.linalg.norm(full), rtol=1e-10)
+    assert dg["rel_err_corrected"] < dg["rel_err_retained"]
+    assert dg["cos_fE_fEhat"] > 0.99
+
+
 def test_decode_zero_key_spread_recovers_full_attention():
     """All evicted keys equal: delta = 0, f_E_hat = v_bar = f_E and Z_E_hat = Z_E, so the
     corrected output is exact full attention over R and E (Sec. 4.2, App. B.2)."""
