@@ -22,8 +22,11 @@ Reported (one JSON line): decode attention+correction GB/s (algorithmic bytes / 
 time, the `value`), decode tokens/s, compress ms/layer per budget, per-budget decode
 times (replay of the whole phase minus replay of the phase without that budget, so the
 other budgets still keep the last-level cache cold), a roofline object for the decode call
-and the fp64 oracle timed on the host as a CPU baseline.  Events are recorded on the
-stream the library launches on.
+and the fp64 oracle timed on the host as a CPU baseline.  Two further phases are measured
+the same way on the same compressed stacks and reported beside the headline, which they do
+not change: the decode with the summary in half precision (`decode_half_summary`) and the
+decode step with moment-informed eviction at every token (`evict_decode`).  Events are
+recorded on the stream the library launches on.
 """
 from __future__ import annotations
 
@@ -139,6 +142,65 @@ def cpu_baseline(wl, data, budget: int, heads: int, steps: int) -> dict:
             "decode_s": t_dec, "compress_s": t_comp}
 
 
+def half_summary_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out, dws,
+                             compress_phase, capture, timed_replay) -> dict:
+    """The decode phase again with the summary in half precision (one bf16 plane of the
+    centred covariance, momentkv_prepare_summary(half=True), summary = 2): the moments'
+    storage precision of the paper's App. C.2.  Same graph replay and per-budget
+    subtraction as the headline decode; bytes count the summary at 2 bytes per entry."""
+    N, Hkv, d = wl.ctx_len, wl.n_kv_heads, wl.head_dim
+    G = wl.group
+    T, LB = q_steps.shape[0], q_steps.shape[1]
+    compress_phase(None)
+    torch.cuda.synchronize()
+    # the summaries do not change while decoding, and every compress rewrites them bit for bit
+    halfs = {L: mk.momentkv_prepare_summary(stacks[L].n_e, stacks[L].s_k, stacks[L].s_v,
+                                            stacks[L].S, dtype=wl.dtype, half=True)
+             for L in budgets}
+
+    def call(t, L):
+        st = stacks[L]
+        mk.momentkv_decode_attn(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k, st.s_v,
+                                halfs[L], k_new=kn_steps[t], v_new=vn_steps[t],
+                                max_len=min(L, N) + T, out=out, workspace=dws[L], summary=2)
+
+    def phase(skip=None):
+        for t in range(T):
+            for L in budgets:
+                if L != skip:
+                    call(t, L)
+
+    print("[bench] decode with the half-precision summary: capture", file=sys.stderr, flush=True)
+    graph = capture(phase=phase)
+    without = {L: capture(skip=L, phase=phase) for L in budgets}
+    ev = []
+    for _ in range(args.steps):
+        compress_phase(None)
+        ev.append(timed_replay(graph))
+    torch.cuda.synchronize()
+    if any(int(dws[L][:4].view(torch.int32)[0]) for L in budgets):
+        return {"error": "append overflow in the half-precision summary phase"}
+    total = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    per_budget = {}
+    all_bytes = 0
+    for L in budgets:
+        tl = []
+        for _ in range(args.steps):
+            compress_phase(None)
+            tl.append(timed_replay(without[L]))
+        torch.cuda.synchronize()
+        budget_ms = total - sum(a.elapsed_time(b) for a, b in tl) / len(tl)
+        by = sum(decode_bytes(LB * Hkv, G, d, min(L, N) + t + 1) - LB * Hkv * 2 * d * d
+                 for t in range(T))
+        all_bytes += by
+        per_budget[str(L)] = {"us_per_call": budget_ms / T * 1e3,
+                              "GBps": by / (budget_ms * 1e-3) / 1e9,
+                              "tokens_per_s": wl.batch * T / (budget_ms * 1e-3)}
+    return {"what": "the decode phase with momentkv_prepare_summary(half=True) (summary = 2)",
+            "ms_per_step": total, "tokens_per_s": wl.batch * T * len(budgets) / (total * 1e-3),
+            "GBps": all_bytes / (total * 1e-3) / 1e9, "per_budget": per_budget}
+
+
 def evict_bytes(n_heads: int, G: int, d: int, L: int, elem: int = 2) -> int:
     """Algorithmic HBM bytes of one decode call with eviction at budget L (per KV head,
     summed): the decode bytes over the L + 1 rows seen by Phase 1 (retained rows read once,
@@ -252,6 +314,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-evict", action="store_true",
                     help="skip the decode-with-eviction measurement")
+    ap.add_argument("--no-half", action="store_true",
+                    help="skip the half-precision summary measurement")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one plain copy of "
                          "known size, then 4 tokens x budgets of eager decode calls; prints "
@@ -460,6 +524,13 @@ def main() -> int:
             "decode_tokens_per_s": B * T / (budget_ms * 1e-3),
         }
     value = phase_bytes * len(dec_ms) / dec_s / 1e9
+    half = None
+    if wl.dtype == torch.bfloat16 and not args.no_half:
+        half = half_summary_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out,
+                                        dws, compress_phase, capture, timed_replay)
+        if half.get("error"):
+            print(f"[bench] {half['error']}", file=sys.stderr)
+            return 6
     evict = None if args.no_evict else evict_measurement(
         args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out, compress_phase, capture,
         timed_replay)
@@ -500,6 +571,8 @@ def main() -> int:
                      "avg_launch_us": avg_launch_s * 1e6},
         "wall_s_timed": wall,
     }
+    if half is not None:
+        res["decode_half_summary"] = half
     if evict is not None:
         res["evict_decode"] = evict
     if not args.no_cpu_baseline:

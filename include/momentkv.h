@@ -175,7 +175,8 @@ typedef struct {
                         /* by a merge launch; 0 = automatic (single launch up to     */
                         /* max_len 384, else about 768 slices in the whole grid).    */
   int32_t summary;      /* form of the S argument: 0 = the raw sum S (fp32); 1 = the */
-                        /* prepared form written by momentkv_prepare_summary         */
+                        /* prepared form written by momentkv_prepare_summary; 2 =    */
+                        /* its half-precision form (bf16 caches only)               */
 } mkv_decode_params;
 
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
@@ -186,6 +187,9 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
  * |S_tilde| < tau set to 0 (the same arithmetic the decode applies to a raw S), stored as
  *   dtype bf16: two bf16 planes [B, Hkv, 2, d, d]: hi = RNE(S_tilde), lo = RNE(S_tilde - hi),
  *               so hi + lo equals S_tilde to within 2^-16 of its magnitude;
+ *   dtype bf16, p->summary = 2: the hi plane alone, [B, Hkv, d, d] bf16 (the moments in
+ *               half precision as in App. C.2, rounded after the fp32 centring, so the
+ *               cancellation of S - s_v s_k^T / n_e happens before the rounding);
  *   dtype fp32: S_tilde itself, fp32 [B, Hkv, d, d].
  * Heads with n_e = 0 get zeros.  Uses batch, n_q_heads, n_kv_heads, head_dim, dtype and
  * tau of p (the other fields are validated as for the decode).  `prepared` holds
@@ -204,8 +208,8 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
  *           (out = 0 when n_e = 0 as well).
  * k_new, v_new [B, Hkv, d] or both NULL
  * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d] fp32: the summary, read only
- * S         p->summary = 0: the raw sum, fp32 [B, Hkv, d, d]; p->summary = 1: the output of
- *           momentkv_prepare_summary for the same summary, tau and dtype
+ * S         p->summary = 0: the raw sum, fp32 [B, Hkv, d, d]; p->summary = 1 or 2: the
+ *           output of momentkv_prepare_summary for the same summary, tau, dtype and form
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R

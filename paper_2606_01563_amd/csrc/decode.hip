@@ -95,16 +95,18 @@ __device__ __forceinline__ void append_row(const DecodeArgs& a, int head, int ro
 // ---------------------------------------------------------------- S_tilde q
 // Rows [r0, r0 + 32) of S_tilde q (unscaled) for the queries held in the query fragments
 // (query g in MFMA column g).  load() issues every read; compute() writes result (g, r) to
-// dst[g * D + r] for g < G.  Three forms of the summary:
+// dst[g * D + r] for g < G.  Four forms of the summary:
 //  * raw S (PREP = false): fp32 MFMA; S_tilde = S - s_v s_k^T / n_e, clamped at tau, is
 //    formed as the rows are loaded;
 //  * prepared, fp32 caches: the stored S_tilde on fp32 MFMA;
 //  * prepared, bf16 caches: the stored hi / lo bf16 planes on bf16 MFMA, two products per
-//    32-wide step against the (exact) bf16 queries.
-template <class T, int D, bool PREP>
+//    32-wide step against the (exact) bf16 queries;
+//  * prepared in half precision (PREP = 2, bf16 caches): the hi plane alone, one product.
+template <class T, int D, int PREP>
 struct SqRows {
   static constexpr int KS = D / 32;
-  static constexpr bool HILO = PREP && sizeof(T) == 2;
+  static constexpr bool HILO = PREP == 1 && sizeof(T) == 2;
+  static constexpr bool HI1 = PREP == 2;  // one bf16 plane (bf16 caches only)
   f32x8 raw[2][KS];
   bf16x8 hi[2][KS], lo[2][KS];
   f32x8 skc[KS];
@@ -123,6 +125,14 @@ struct SqRows {
           hi[u][ks] = load_frag(P + (size_t)row * D + 32 * ks + col);
           lo[u][ks] = load_frag(P + (size_t)(D + row) * D + 32 * ks + col);
         }
+      }
+    } else if constexpr (HI1) {
+      const bf16_t* P = reinterpret_cast<const bf16_t*>(a.S) + (size_t)head * D * D;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int row = r0 + 16 * u + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) hi[u][ks] = load_frag(P + (size_t)row * D + 32 * ks + col);
       }
     } else {
       const float* Sh = a.S + (size_t)head * D * D;
@@ -155,6 +165,13 @@ struct SqRows {
           mma(acc[u], lo[u][ks], qf[ks]);
         }
       }
+    } else if constexpr (HI1) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        acc[u] = zero4();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) mma(acc[u], hi[u][ks], qf[ks]);
+      }
     } else {
       float inv_n = 0.f;
       if constexpr (!PREP) inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
@@ -171,7 +188,7 @@ struct SqRows {
           f32x8 af;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            if constexpr (PREP) {
+            if constexpr (PREP == 1) {
               af[e] = raw[u][ks][e];
             } else {
               const float st = raw[u][ks][e] - sv[u] * (skc[ks][e] * inv_n);
@@ -192,10 +209,11 @@ struct SqRows {
 
 // Decode form of the summary: S_tilde = S - s_v s_k^T / n_e with entries below tau set to
 // zero, computed with the same fp32 arithmetic as the raw-summary decode path, stored as
-// hi = RNE_bf16(S_tilde) and lo = RNE_bf16(S_tilde - hi) planes for bf16 caches, or as fp32.
+// hi = RNE_bf16(S_tilde) and lo = RNE_bf16(S_tilde - hi) planes for bf16 caches (the hi
+// plane alone for the half-precision form, hi_only), or as fp32.
 // Grid (D * D / 8 / 256, n_heads); a thread handles 8 consecutive entries of one row.
 template <class T, int D>
-__global__ void __launch_bounds__(256) k_prepare_summary(DecodeArgs a, void* prepared) {
+__global__ void __launch_bounds__(256) k_prepare_summary(DecodeArgs a, void* prepared, int hi_only) {
   const int head = blockIdx.y;
   const int idx = blockIdx.x * 256 + threadIdx.x;
   if (idx >= D * D / 8) return;
@@ -220,9 +238,10 @@ __global__ void __launch_bounds__(256) k_prepare_summary(DecodeArgs a, void* pre
       h[e / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
       l[e / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
     }
-    bf16_t* P = reinterpret_cast<bf16_t*>(prepared) + (size_t)head * 2 * D * D;
+    bf16_t* P = reinterpret_cast<bf16_t*>(prepared) + (size_t)head * (hi_only ? 1 : 2) * D * D;
     *reinterpret_cast<uint4*>(P + (size_t)row * D + c0) = make_uint4(h[0], h[1], h[2], h[3]);
-    *reinterpret_cast<uint4*>(P + (size_t)(D + row) * D + c0) = make_uint4(l[0], l[1], l[2], l[3]);
+    if (!hi_only)
+      *reinterpret_cast<uint4*>(P + (size_t)(D + row) * D + c0) = make_uint4(l[0], l[1], l[2], l[3]);
   } else {
     float4* P = reinterpret_cast<float4*>(reinterpret_cast<float*>(prepared) + ((size_t)head * D + row) * D + c0);
     P[0] = make_float4(st[0], st[1], st[2], st[3]);
@@ -500,7 +519,7 @@ __device__ __forceinline__ void finish_query(const DecodeArgs& a, int bh, int g,
 }
 
 // ---------------------------------------------------------------- fused launch
-template <class T, int D, int GMAX, bool PREP>
+template <class T, int D, int GMAX, int PREP>
 __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int CPL = D / 64;
@@ -576,7 +595,7 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------- split launch
-template <class T, int D, int GMAX, bool PREP>
+template <class T, int D, int GMAX, int PREP>
 __global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int KS = D / 32;
@@ -703,7 +722,7 @@ __global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
   decode_merge_query<T, D>(a, pair / a.G, pair % a.G, lane);
 }
 
-template <class T, int D, int GMAX, bool PREP>
+template <class T, int D, int GMAX, int PREP>
 static hipError_t launch_decode_p(const DecodeArgs& a, hipStream_t st) {
   if (a.fused) {
     hipLaunchKernelGGL((k_decode_fused<T, D, GMAX, PREP>), dim3(a.n_heads), dim3(256), 0, st, a);
@@ -719,7 +738,11 @@ static hipError_t launch_decode_p(const DecodeArgs& a, hipStream_t st) {
 
 template <class T, int D, int GMAX>
 static hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  return a.summary ? launch_decode_p<T, D, GMAX, true>(a, st) : launch_decode_p<T, D, GMAX, false>(a, st);
+  if (a.summary == 1) return launch_decode_p<T, D, GMAX, 1>(a, st);
+  if constexpr (sizeof(T) == 2) {
+    if (a.summary == 2) return launch_decode_p<T, D, GMAX, 2>(a, st);
+  }
+  return launch_decode_p<T, D, GMAX, 0>(a, st);
 }
 
 template <class T, int D>
@@ -737,7 +760,7 @@ hipError_t launch_decode(const DecodeArgs& a, bool bf16, int d, hipStream_t st) 
 template <class T, int D>
 static hipError_t launch_prepare_t(const DecodeArgs& a, void* prepared, hipStream_t st) {
   hipLaunchKernelGGL((k_prepare_summary<T, D>), dim3((D * D / 8 + 255) / 256, a.n_heads), dim3(256), 0,
-                     st, a, prepared);
+                     st, a, prepared, a.summary == 2 ? 1 : 0);
   return hipGetLastError();
 }
 

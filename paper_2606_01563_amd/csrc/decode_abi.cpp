@@ -57,7 +57,8 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
   if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;
   if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
   if (p->n_split < 0) return MKV_ERR_SHAPE;
-  if (p->summary != 0 && p->summary != 1) return MKV_ERR_SHAPE;
+  if (p->summary < 0 || p->summary > 2) return MKV_ERR_SHAPE;
+  if (p->summary == 2 && p->dtype != MKV_BF16) return MKV_ERR_SHAPE;  // half precision: bf16 only
   if (p->max_len < 1 || p->max_len > p->cap) return MKV_ERR_CAPACITY;
   // grid of single-wave workgroups: B * Hkv * (slices + covariance waves)
   int split_len = 0, nsplit = 0;
@@ -107,7 +108,7 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p) {
 
 size_t momentkv_prepared_summary_size(const mkv_decode_params* p) {
   if (check_decode_params(p) != MKV_OK) return 0;
-  return (size_t)p->batch * p->n_kv_heads * p->head_dim * p->head_dim * 4;
+  return (size_t)p->batch * p->n_kv_heads * p->head_dim * p->head_dim * (p->summary == 2 ? 2 : 4);
 }
 
 mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n_e,
@@ -118,7 +119,7 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
   if (!n_e || !s_k || !s_v || !S || !prepared) return MKV_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(prepared) % 16) return MKV_ERR_SHAPE;
   const size_t heads = (size_t)p->batch * p->n_kv_heads, d = p->head_dim;
-  const size_t out_bytes = heads * d * d * 4;
+  const size_t out_bytes = heads * d * d * (p->summary == 2 ? 2 : 4);
   if (ranges_overlap(prepared, out_bytes, S, heads * d * d * 4) ||
       ranges_overlap(prepared, out_bytes, s_k, heads * d * 4) ||
       ranges_overlap(prepared, out_bytes, s_v, heads * d * 4) ||

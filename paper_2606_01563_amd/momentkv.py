@@ -241,14 +241,15 @@ def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6,
 
 def momentkv_prepare_summary(n_e: torch.Tensor, s_k: torch.Tensor, s_v: torch.Tensor,
                              S: torch.Tensor, *, dtype: torch.dtype, tau: float = 1e-6,
-                             out: torch.Tensor | None = None) -> torch.Tensor:
+                             half: bool = False, out: torch.Tensor | None = None) -> torch.Tensor:
     """Decode form of the summary (see the header): bf16 hi/lo planes [B, Hkv, 2, d, d] for
-    dtype bf16, fp32 [B, Hkv, d, d] for fp32.  Pass it as `S` with summary=1."""
+    dtype bf16, fp32 [B, Hkv, d, d] for fp32; half=True (bf16 only) the one-plane
+    half-precision form [B, Hkv, d, d].  Pass it as `S` with summary=1 (summary=2 if half)."""
     B, Hkv, d, _ = S.shape
     code = MKV_BF16 if dtype == torch.bfloat16 else MKV_F32
-    p = DecodeParams(B, Hkv, Hkv, d, 1, 1, 1, code, 0.0, tau, 0, 0)
+    p = DecodeParams(B, Hkv, Hkv, d, 1, 1, 1, code, 0.0, tau, 0, 2 if half else 0)
     if out is None:
-        shape = (B, Hkv, 2, d, d) if dtype == torch.bfloat16 else (B, Hkv, d, d)
+        shape = (B, Hkv, 2, d, d) if dtype == torch.bfloat16 and not half else (B, Hkv, d, d)
         out = torch.empty(shape, dtype=dtype, device=S.device)
     if out.numel() * out.element_size() < momentkv_prepared_summary_size(p):
         raise ValueError("prepared summary buffer too small")

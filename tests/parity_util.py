@@ -153,7 +153,7 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
     """Run `steps` decode calls on the GPU, each checked against the oracle fed the GPU's
     retained cache and fp32 moments.  `lens0` ([B, Hkv], each at most the compressed
     length) replaces the retained lengths before the first step.  Returns the list of max
-    relative errors.  summary=1 passes the prepared summary (the oracle reads the raw
+    relative errors.  summary=1 (2) passes the prepared (half-precision) summary (the oracle reads the raw
     moments)."""
     dt = inp["k"].dtype
     tol = TOL[dt]
@@ -161,7 +161,7 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
     Hq = inp["q_win"].shape[1]
     G = Hq // Hkv
     S_arg = comp.S if summary == 0 else mk.momentkv_prepare_summary(
-        comp.n_e, comp.s_k, comp.s_v, comp.S, dtype=dt, tau=tau)
+        comp.n_e, comp.s_k, comp.s_v, comp.S, dtype=dt, tau=tau, half=summary == 2)
     lens = comp.lens.clone()
     if lens0 is not None:
         lens0 = torch.as_tensor(lens0, dtype=torch.int32)

@@ -129,7 +129,8 @@ def test_budget_at_least_context_is_valid(L):
     (dict(cap=0), SHAPE),
     (dict(order=2), SHAPE),
     (dict(n_split=-1), SHAPE),
-    (dict(summary=2), SHAPE),
+    (dict(summary=3), SHAPE),
+    (dict(summary=2, dtype=0), SHAPE),      # the half-precision summary needs bf16 caches
     (dict(batch=500000), UNSUP),            # decode grid limit: 4M heads x 5 waves
     (dict(head_dim=80), UNSUP),
     (dict(max_len=0), CAPACITY),
@@ -154,6 +155,7 @@ def test_decode_rejects_null_alias_and_small_workspace(L):
 def test_prepared_summary_size_and_validation(L):
     p = dparams()
     assert mk.momentkv_prepared_summary_size(p) == 36 * 8 * 128 * 128 * 4
+    assert mk.momentkv_prepared_summary_size(dparams(summary=2)) == 36 * 8 * 128 * 128 * 2
     assert mk.momentkv_prepared_summary_size(dparams(head_dim=80)) == 0
     ptrs = [(1 << 20) + i * (1 << 36) for i in range(5)]
     f = mk.lib().momentkv_prepare_summary

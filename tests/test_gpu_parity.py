@@ -257,6 +257,72 @@ def test_prepared_summary_matches_centred_clamped_covariance(dtype, d):
             assert np.any(ref != 0)
 
 
+def test_half_precision_summary_is_rounded_covariance():
+    """The one-plane form is RNE_bf16 of the fp32-centred S_tilde: within half a bf16 ulp
+    (8 significant bits: 2^-8 of |S_tilde|) plus the centring error and the clamp band."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, dtype=torch.bfloat16, head_dim=128,
+                         ctx_len=1500, batch=2, n_q_heads=4, n_kv_heads=2, window=16,
+                         budgets=(97,))
+    out = P.run_compress(gpu, 97, cap=97)
+    half = mk.momentkv_prepare_summary(out.n_e, out.s_k, out.s_v, out.S, dtype=torch.bfloat16,
+                                       half=True)
+    full = mk.momentkv_prepare_summary(out.n_e, out.s_k, out.s_v, out.S, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert half.shape == (2, 2, 128, 128)
+    assert torch.equal(half, full[:, :, 0])           # the hi plane of the two-plane form
+    got = P.h64(half)
+    for b in range(2):
+        for h in range(2):
+            m = P.oracle_moments(out, b, h)
+            _, _, ref = O.centered_moments(m, 1e-6)
+            S, sv, sk = P.h64(out.S[b, h]), P.h64(out.s_v[b, h]), P.h64(out.s_k[b, h])
+            bound = (2.0 ** -8 * np.abs(ref) + 2.0 ** -21 * (np.abs(S) + np.abs(np.outer(sv, sk)) / m.n_e)
+                     + 2e-6)
+            assert np.all(np.abs(got[b, h] - ref) <= bound)
+
+
+@pytest.mark.parametrize("n_split", [1, 0])
+def test_decode_with_half_precision_summary(n_split):
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=3, ctx_len=3000, batch=2)
+    out = P.run_compress(gpu, 400, cap=403)
+    P.run_decode_steps(gpu, out, 3, n_split=n_split, summary=2)
+
+
+def test_half_precision_summary_error_against_fp32_summary():
+    """Synthetic analog of the paper's FP16-vs-FP32 moment comparison (App. C.2): one 32K
+    layer at budget 128, where the summary is the largest share of the decode.  Against the
+    oracle and against exact full attention, the half-precision summary's extra error is
+    small next to the approximation error itself."""
+    wl, cpu, gpu = layer("qwen3_4b_stack_n32768", steps=2)
+    L = 128
+    out = P.run_compress(gpu, L, cap=L)
+    d, G = wl.head_dim, wl.group
+    moments = [[P.oracle_moments(out, 0, h) for h in range(wl.n_kv_heads)]]
+    kf, vf = gpu["k"][0].float(), gpu["v"][0].float()
+    res = {}
+    for summ in (1, 2):
+        S_arg = mk.momentkv_prepare_summary(out.n_e, out.s_k, out.s_v, out.S, dtype=torch.bfloat16,
+                                            half=summ == 2)
+        e_orc, e_full = [], []
+        for t in range(2):
+            q = gpu["q_dec"][t]
+            got, _, _, _ = mk.momentkv_decode_attn(q, out.k_out, out.v_out, out.lens, out.n_e, out.s_k,
+                                                   out.s_v, S_arg, max_len=L, summary=summ)
+            ref, _, _, _ = O.decode(P.h64(q), P.h64(out.k_out), P.h64(out.v_out),
+                                    out.lens.cpu().numpy(), moments)
+            g64 = P.h64(got)
+            e_orc.append(max(P.rel_l2(g64[0, i], ref[0, i]) for i in range(wl.n_q_heads)))
+            qf = q[0].float().view(wl.n_kv_heads, G, d)
+            s = torch.matmul(qf, kf.transpose(1, 2).contiguous()) / math.sqrt(d)
+            full = torch.matmul(torch.softmax(s, -1), vf).reshape(-1, d)
+            e_full.append(float(((got[0].float() - full).norm(dim=-1) / full.norm(dim=-1)).mean()))
+        res[summ] = (max(e_orc), sum(e_full) / len(e_full))
+    announce(f"two-plane summary: max rel err vs oracle {res[1][0]:.2e}, vs full attention "
+             f"{res[1][1]:.4f}; half precision: {res[2][0]:.2e}, {res[2][1]:.4f}")
+    assert res[2][0] <= 2e-2
+    assert abs(res[2][1] - res[1][1]) <= 0.05 * res[1][1]
+
+
 # ---------------------------------------------------------------- full-size sampled heads
 @pytest.mark.parametrize("budget", [128, 2048])
 def test_qwen_stack_layer_full_size_sampled_heads(budget):
