@@ -23,6 +23,8 @@ Pinning status (what fixes each function other than itself; see tests/):
                           SnapKV-mode reduction; the batched selection rule itself
                           (one provisional round + moment rounds) is a reading of
                           Algorithm 1 and is *parity unpinned* beyond its definition.
+  head_budgets            pinned: brute-force sort of (-mass, head, position) on tiny
+                          layers, one head = the uniform budget, identical heads split evenly
   decode                  pinned: no-eviction == SDPA, zero key spread == full
                           attention, second-order error, Jensen bound, weight bias
   greedy_evict            quality reference only (parity unpinned; no printed example)
@@ -48,7 +50,7 @@ __all__ = [
     "Moments", "CompressResult", "DecodeResult",
     "window_attention_mass", "chunk_pool", "select_top", "evicted_moments",
     "centered_moments", "moment_residuals", "residual_scores", "select_candidates",
-    "compress", "compress_head",
+    "compress", "compress_head", "head_budgets",
     "decode", "decode_head", "append_tokens", "attention_parts", "greedy_evict",
     "evict_scores_head", "decode_evict_head", "decode_evict", "eviction_diagnostics",
     "moment_storage_bytes",
@@ -319,21 +321,52 @@ def compress_head(q_win, k, v, budget: int, *, n_sink: int = 1, chunk: int = 4,
                           sigma0, sigma, rounds)
 
 
-def compress(q_win, k, v, budget: int, **kw):
+def head_budgets(abar_heads, k_keep: int) -> np.ndarray:
+    """Head-adaptive split of a layer's candidate budget (Sec. 5.1: the budget is allocated
+    across the heads of a layer by their attention mass, as in Ada-KV).
+
+    abar_heads: [Hkv, n_c] pooled window mass of every head's candidates.  Reading: the
+    Hkv * k_keep candidates with the largest mass over the whole layer are kept, equal
+    masses in (head, position) order; head h keeps as many candidates as it has among
+    them.  Returns k_h per head (they sum to Hkv * k_keep, or to every candidate)."""
+    a = _f64(abar_heads)
+    H, n = a.shape
+    flat = a.reshape(-1)
+    keep = min(H * k_keep, flat.size)
+    order = np.lexsort((np.arange(flat.size), -flat))[:keep]
+    return np.bincount(order // n, minlength=H).astype(np.int64)
+
+
+def compress(q_win, k, v, budget: int, *, adaptive: bool = False, **kw):
     """Batched compress over [B, Hq, w, d] window queries and [B, Hkv, N, d] K/V.
 
     Query head hq uses KV head hq // G with G = Hq / Hkv (GQA).  Returns a nested list
-    [B][Hkv] of CompressResult.
+    [B][Hkv] of CompressResult.  adaptive: the per-head candidate counts come from
+    head_budgets over the layer (each head then selects its k_h moment-informed), so head h
+    keeps n_sink + w + k_h tokens.
     """
     q = np.asarray(q_win)
     B, Hq, w, d = q.shape
-    Hkv = np.asarray(k).shape[1]
+    K, V = np.asarray(k), np.asarray(v)
+    Hkv, N = K.shape[1], K.shape[2]
     if Hq % Hkv:
         raise ValueError("Hq must be a multiple of Hkv")
     G = Hq // Hkv
-    return [[compress_head(q[b, h * G:(h + 1) * G], np.asarray(k)[b, h],
-                           np.asarray(v)[b, h], budget, **kw) for h in range(Hkv)]
-            for b in range(B)]
+    if not adaptive or budget >= N:
+        return [[compress_head(q[b, h * G:(h + 1) * G], K[b, h], V[b, h], budget, **kw)
+                 for h in range(Hkv)] for b in range(B)]
+    n_sink, chunk = kw.get("n_sink", 1), kw.get("chunk", 4)
+    scale = kw.get("scale") or 1.0 / math.sqrt(d)
+    if budget < n_sink + w:
+        raise ValueError("budget must cover the sink and window tokens")
+    out = []
+    for b in range(B):
+        abar = np.stack([chunk_pool(window_attention_mass(q[b, h * G:(h + 1) * G], K[b, h], scale),
+                                    n_sink, chunk) for h in range(Hkv)])
+        kh = head_budgets(abar, budget - n_sink - w)
+        out.append([compress_head(q[b, h * G:(h + 1) * G], K[b, h], V[b, h],
+                                  n_sink + w + int(kh[h]), **kw) for h in range(Hkv)])
+    return out
 
 
 # --------------------------------------------------------------------------------------

@@ -69,6 +69,10 @@ MUTANTS = {
     "evict_no_slot_move": ("        kc[evicted] = kc[n - 1]\n", "\n"),
     "evict_at_budget": ("    if n > budget:\n", "    if n >= budget:\n"),
     "no_correction_ignored": ("    if m.n_e == 0 or order < 0:", "    if m.n_e == 0:"),
+    "head_budget_ties_reversed": ("    order = np.lexsort((np.arange(flat.size), -flat))[:keep]",
+                                  "    order = np.lexsort((-np.arange(flat.size), -flat))[:keep]"),
+    "head_budget_lowest_mass": ("    order = np.lexsort((np.arange(flat.size), -flat))[:keep]",
+                                "    order = np.lexsort((np.arange(flat.size), flat))[:keep]"),
 }
 
 PIN_TESTS = [name for name in dir(pins) if name.startswith("test_")]

@@ -652,3 +652,62 @@ def test_evict_batched_matches_per_head():
             np.testing.assert_array_equal(out[b, h * G:(h + 1) * G], r["out"])
             np.testing.assert_array_equal(kc2[b, h], r["k_cache"])
     assert ev[0, 1] == -1 and ln2[0, 1] == L
+
+
+# ------------------------------------------------------------ head-adaptive budgets
+def test_head_budgets_match_bruteforce_sort_with_ties():
+    """Per-head counts equal a brute-force Python sort of (-mass, head, position) over the
+    layer, with planted equal masses inside and across heads."""
+    rng = np.random.default_rng(50)
+    for trial in range(20):
+        H, n = int(rng.integers(2, 5)), int(rng.integers(5, 14))
+        a = rng.integers(0, 6, size=(H, n)).astype(float) / 7.0   # many ties
+        k = int(rng.integers(0, n + 1))
+        items = sorted((-a[h, j], h, j) for h in range(H) for j in range(n))[:H * k]
+        want = [sum(1 for _, h, _ in items if h == hh) for hh in range(H)]
+        got = O.head_budgets(a, k)
+        assert list(got) == want, trial
+        assert got.sum() == H * k
+
+
+def test_head_budgets_one_head_is_the_uniform_budget():
+    rng = np.random.default_rng(51)
+    a = rng.random((1, 40))
+    for k in (0, 1, 17, 40):
+        assert list(O.head_budgets(a, k)) == [k]
+
+
+def test_adaptive_compress_of_identical_heads_is_uniform():
+    """Heads with identical queries, keys and values (no chunk pooling, continuous masses)
+    split the layer budget evenly, so adaptive compress equals uniform compress."""
+    q, K, V = _tiny_prefill(52, G=2, w=4, d=8, N=90)
+    H = 3
+    qq = np.concatenate([q] * H)[None]                  # [1, H*G, w, d]
+    KK = np.stack([K] * H)[None]
+    VV = np.stack([V] * H)[None]
+    ada = O.compress(qq, KK, VV, 30, adaptive=True, chunk=1)
+    uni = O.compress(qq, KK, VV, 30, chunk=1)
+    for h in range(H):
+        np.testing.assert_array_equal(ada[0][h].idx, uni[0][h].idx)
+        np.testing.assert_allclose(ada[0][h].moments.S, uni[0][h].moments.S)
+
+
+def test_adaptive_compress_counts_and_summaries():
+    """Heads keep n_sink + w + k_h tokens with sum k_h = Hkv * k_keep; each head's summary is
+    the brute-force moment sums over its own evicted candidates."""
+    rng = np.random.default_rng(53)
+    H, G, w, d, N, L = 3, 2, 4, 8, 80, 20
+    q = rng.normal(size=(1, H * G, w, d))
+    K = rng.normal(size=(1, H, N, d))
+    K[0, 1] *= 2.5                                         # a sharper head
+    V = rng.normal(size=(1, H, N, d))
+    res = O.compress(q, K, V, L, adaptive=True)
+    kh = [len(r.retained) for r in res[0]]
+    assert sum(kh) == H * (L - 1 - w) and len(set(kh)) > 1
+    for h in range(H):
+        r = res[0][h]
+        assert len(r.idx) == 1 + w + kh[h]
+        E = np.setdiff1d(np.arange(1, N - w), r.retained)
+        np.testing.assert_array_equal(E, r.evicted)
+        S = sum(np.outer(V[0, h, i], K[0, h, i]) for i in E)
+        np.testing.assert_allclose(r.moments.S, S, rtol=1e-12, atol=1e-12)
