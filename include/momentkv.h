@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define MOMENTKV_ABI_VERSION 3
+#define MOMENTKV_ABI_VERSION 4
 
 typedef enum {
   MKV_OK = 0,
@@ -66,7 +66,8 @@ typedef enum {
 typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
 
 /* Limits of this build: head_dim in {64, 128}; G = Hq/Hkv <= 16; G * window <= 512;
- * at most 262144 eviction candidates (ctx_len - window - n_sink) per head; a decode grid
+ * at most 262144 eviction candidates (ctx_len - window - n_sink) per head (per layer with
+ * head-adaptive budgets); a decode grid
  * of at most 2^24 waves (B * Hkv * (token slices + head_dim / 32)). */
 
 /* ------------------------------------------------------------------------------------
@@ -95,6 +96,12 @@ typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
  *      and their K/V rows copied to k_out/v_out; lens = min(budget, N); the raw sums of
  *      the final evicted set E (n_e = |E|, s_k, s_v, S = sum_E v_i k_i^T, fp32).
  *   budget >= N keeps every token: idx = 0..N-1, n_e = 0 and zero moments.
+ *   adaptive = 1 (head-adaptive budgets, Sec. 5.1 after Ada-KV): per sequence, the
+ *      Hkv * k_keep candidates with the largest abar over all the layer's heads (equal
+ *      values in (head, position) order) are counted per head, k_h; head h then selects
+ *      k_h candidates as in step 4 and keeps n_s + w + k_h tokens (lens).  Requires
+ *      cap >= n_s + w + min(n_c, Hkv * k_keep) and Hkv * n_c <= 262144; idx_out then has
+ *      cap entries per head, of which the first lens are written.
  * ---------------------------------------------------------------------------------- */
 typedef struct {
   int32_t batch;        /* B                                                         */
@@ -111,6 +118,7 @@ typedef struct {
   int32_t dtype;        /* mkv_dtype of q_win, k, v, k_out, v_out                    */
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
   float tau;            /* covariance clamp threshold (paper: 1e-6); >= 0            */
+  int32_t adaptive;     /* 0 = budget per head; 1 = head-adaptive split (step 5)     */
 } mkv_compress_params;
 
 /* Optional per-candidate diagnostics (any field may be NULL).  n_c = N - w - n_s.
@@ -120,6 +128,7 @@ typedef struct {
   float* score0;        /* [B, Hkv, n_c] provisional score abar * ||v||               */
   float* score;         /* [B, Hkv, n_c] moment-round score (mi_rounds = 1)           */
   int32_t* kept0;       /* [B, Hkv, k_keep] provisional kept positions, ascending    */
+                        /* (adaptive: [B, Hkv, min(n_c, Hkv*k_keep)], first k_h set) */
 } mkv_compress_debug;
 
 /* Bytes of device workspace momentkv_compress needs for these parameters (0 on invalid
@@ -130,8 +139,9 @@ size_t momentkv_compress_workspace_size(const mkv_compress_params* p);
  * k, v    [B, Hkv, N, d]     prefill keys (post-RoPE) and values, read only
  * k_out, v_out [B, Hkv, cap, d]  retained rows written to rows 0..min(L,N)-1; must not
  *                            overlap k or v (MKV_ERR_ALIAS)
- * idx_out [B, Hkv, min(L,N)] int32 retained positions, ascending
- * lens_out [B, Hkv]          int32, set to min(L, N)
+ * idx_out [B, Hkv, min(L,N)] int32 retained positions, ascending ([B, Hkv, cap] when
+ *                            adaptive)
+ * lens_out [B, Hkv]          int32, set to min(L, N) (n_s + w + k_h when adaptive)
  * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d] fp32, S [B, Hkv, d, d] fp32: outputs,
  *                            overwritten (zero-initialised summary per generation)
  * dbg                        NULL or optional diagnostics

@@ -51,6 +51,12 @@ __device__ __forceinline__ uint32_t score_key(float s) {
 
 constexpr int TK_HBINS = 2048;     // bins of the per-head histogram (key bits 30..20)
 
+// Candidates kept by a head: the uniform k_keep, or its head-adaptive share (clamped to
+// the buffers, since it sizes reads and writes).
+__device__ __forceinline__ int head_keep(const CompressArgs& a, int head) {
+  return a.kh ? min(max(a.kh[head], 0), a.kmax) : a.k_keep;
+}
+
 // Adds a workgroup's LDS histogram to the head's histogram in global memory (integer
 // atomics: the result is exact whatever the order).
 template <int NT>
@@ -448,9 +454,13 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
 // ------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) k_row_combine(CompressArgs a) {
   const int head = blockIdx.y;
-  if (blockIdx.x == 0)  // the score producers below add into these
+  if (blockIdx.x == 0) {  // the score producers below add into these
     for (int b = threadIdx.x; b < 2 * TK_HBINS; b += 256)
       a.tk_hh[((size_t)(b / TK_HBINS) * a.H + head) * TK_HBINS + b % TK_HBINS] = 0u;
+    if (a.adaptive && head % a.Hkv == 0)
+      for (int b = threadIdx.x; b < TK_HBINS; b += 256)
+        a.tk_hs[(size_t)(head / a.Hkv) * TK_HBINS + b] = 0u;
+  }
   const int r = blockIdx.x * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
   float m = -INFINITY, l = 0.f;
@@ -485,6 +495,7 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
   __shared__ float sAj[TILE];
   __shared__ float sRow[512][2];
   __shared__ uint32_t sHist[TK_HBINS];  // keys of the first selection's scores
+  __shared__ uint32_t sHistA[TK_HBINS]; // keys of abar (head-adaptive layer-wide selection)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
@@ -498,7 +509,7 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
     sRow[r][0] = a.rowstat[((size_t)head * a.R + r) * 2 + 0];
     sRow[r][1] = a.rowstat[((size_t)head * a.R + r) * 2 + 1];
   }
-  for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = 0u;
+  for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = sHistA[b] = 0u;
   typename Frag<T>::type qf[MTW][KS];
 #pragma unroll
   for (int k = 0; k < MTW; ++k) {
@@ -575,11 +586,13 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
         a.abar[o] = ab;
         a.score0[o] = s0;
         atomicAdd(&sHist[score_key(a.mi_rounds < 0 ? ab : s0) >> 20], 1u);
+        if (a.adaptive) atomicAdd(&sHistA[score_key(ab) >> 20], 1u);
       }
     }
     __syncthreads();
   }
   hist_flush<256>(sHist, a.tk_hh + (size_t)head * TK_HBINS);
+  if (a.adaptive) hist_flush<256>(sHistA, a.tk_hs + (size_t)(head / a.Hkv) * TK_HBINS);
 }
 
 // ------------------------------------------------------------------------------------
@@ -666,6 +679,7 @@ __device__ __forceinline__ void slice_keys(const float* s, int n, int sl, uint32
 }
 
 __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ scores, int n, int k,
+                                                   const int* __restrict__ kh,
                                                    const uint32_t* __restrict__ hh,
                                                    int* __restrict__ state,
                                                    int* __restrict__ cnt, uint32_t* __restrict__ cand) {
@@ -673,6 +687,8 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
   __shared__ uint32_t hst[TK_HBINS];
   __shared__ uint32_t sh_bin, sh_above;
   const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x;
+  if (kh) k = min(kh[head], n);  // head-adaptive count (uniform over the workgroup)
+  if (k <= 0) return;
   uint32_t key[TKPT];
   bool valid[TKPT];
   slice_keys(scores + (size_t)head * n, n, sl, key, valid);
@@ -705,6 +721,7 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
 }
 
 __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scores, int n, int k,
+                                                    const int* __restrict__ kh,
                                                     const int* __restrict__ state,
                                                     const int* __restrict__ cnt,
                                                     const uint32_t* __restrict__ cand,
@@ -719,6 +736,8 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
   __shared__ uint32_t c_key[TK_CAND_LDS];
   __shared__ uint8_t c_sl[TK_CAND_LDS];
   const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x, tid = threadIdx.x;
+  if (kh) k = min(kh[head], n);  // head-adaptive count (uniform over the workgroup)
+  if (k <= 0) return;
   // the slice's own keys are needed last but depend on nothing: requested first
   uint32_t key[TKPT];
   bool valid[TKPT];
@@ -846,7 +865,7 @@ __global__ void __launch_bounds__(256) k_gather_rows(CompressArgs a) {
   const int head = blockIdx.y;
   const int c = blockIdx.x * 256 + threadIdx.x;
   const int i = c / DG, dg = c % DG;
-  if (i >= a.k_keep) return;
+  if (i >= head_keep(a, head)) return;
   // kept positions are read as addresses: clamped to the context, so that no selection
   // result can move a read outside the head's rows
   const int pos = min(max(a.kept0[(size_t)head * a.kmax + i], 0), a.N - 1);
@@ -873,6 +892,7 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kb
   __shared__ __align__(16) T sVT[D][LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
+  if (nrows < 0) nrows = head_keep(a, head);  // the head's own kept count
   const T* Kh = reinterpret_cast<const T*>(kbase) + ((size_t)head * head_rows + row_off) * D;
   const T* Vh = reinterpret_cast<const T*>(vbase) + ((size_t)head * head_rows + row_off) * D;
   f32x4 cacc[QM][QN];
@@ -950,7 +970,7 @@ __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, fl
     }
     *reinterpret_cast<float4*>(dst) = acc;
   }
-  if (ne_out && blockIdx.x == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - a.k_keep;
+  if (ne_out && blockIdx.x == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - head_keep(a, head);
 }
 
 // ------------------------------------------------------------------------------------
@@ -981,9 +1001,9 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
   for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = 0u;
   const int head = blockIdx.y, sl = blockIdx.x;
   const int c_lo = a.n_s, c_hi = a.N - a.w;
-  const float n0 = (float)(a.n_c - a.k_keep);
-  const float inv_n = 1.f / n0;
-  const float coef = a.scale / n0;
+  const float n0 = (float)(a.n_c - head_keep(a, head));  // 0: everything kept, empty summary
+  const float inv_n = n0 > 0.f ? 1.f / n0 : 0.f;
+  const float coef = n0 > 0.f ? a.scale / n0 : 0.f;
   const T* Kh = reinterpret_cast<const T*>(a.k) + (size_t)head * a.N * D;
   const T* Vh = reinterpret_cast<const T*>(a.v) + (size_t)head * a.N * D;
 
@@ -1119,18 +1139,20 @@ __global__ void __launch_bounds__(256) k_gather_out(CompressArgs a, int n_out, i
   const int head = blockIdx.y;
   const int c = blockIdx.x * 256 + threadIdx.x;
   const int i = c / DG, dg = c % DG;
+  const int kk = keep_all ? 0 : head_keep(a, head);
+  if (!keep_all && a.kh) n_out = a.n_s + kk + a.w;  // head-adaptive: this head's length
   if (blockIdx.x == 0 && threadIdx.x == 0) a.lens_out[head] = n_out;
   if (i >= n_out) return;
   int pos;
   if (keep_all || i < a.n_s) pos = i;
-  else if (i < a.n_s + a.k_keep) pos = a.kept[(size_t)head * a.kmax + (i - a.n_s)];
-  else pos = a.N - a.w + (i - a.n_s - a.k_keep);
+  else if (i < a.n_s + kk) pos = a.kept[(size_t)head * a.kmax + (i - a.n_s)];
+  else pos = a.N - a.w + (i - a.n_s - kk);
   pos = min(max(pos, 0), a.N - 1);  // a kept position is an address: never outside the rows
   const size_t src = ((size_t)head * a.N + pos) * D + 8 * dg;
   const size_t dst = ((size_t)head * a.cap + i) * D + 8 * dg;
   store_frag(reinterpret_cast<T*>(a.k_out) + dst, load_frag(reinterpret_cast<const T*>(a.k) + src));
   store_frag(reinterpret_cast<T*>(a.v_out) + dst, load_frag(reinterpret_cast<const T*>(a.v) + src));
-  if (dg == 0) a.idx_out[(size_t)head * n_out + i] = pos;
+  if (dg == 0) a.idx_out[(size_t)head * a.idx_stride + i] = pos;
 }
 
 template <int D>
@@ -1160,12 +1182,48 @@ static hipError_t launch_topk(const CompressArgs& a, const float* scores, int wh
   if (a.k_keep <= 0) return hipSuccess;
   const dim3 grid(a.ntk, a.H);
   hipLaunchKernelGGL(k_tk_cand, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep,
-                     (const uint32_t*)(a.tk_hh + (size_t)which * a.H * TK_HBINS), a.tk_state,
-                     a.tk_cnt, a.tk_cand);
+                     (const int*)a.kh, (const uint32_t*)(a.tk_hh + (size_t)which * a.H * TK_HBINS),
+                     a.tk_state, a.tk_cnt, a.tk_cand);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep,
+  hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep, (const int*)a.kh,
                      (const int*)a.tk_state, (const int*)a.tk_cnt, (const uint32_t*)a.tk_cand, out,
                      a.kmax, a.n_s);
+  MKV_CHECK_LAUNCH();
+  return hipSuccess;
+}
+
+// Head-adaptive budgets: one layer-wide selection per sequence over the Hkv heads' abar
+// rows (contiguous in memory, position head * n_c + j), the Hkv * k_keep largest with
+// equal values in (head, position) order; then each head's share of them.
+__global__ void __launch_bounds__(64) k_ada_counts(CompressArgs a) {
+  const int b = blockIdx.x;
+  const int K = a.Hkv * a.k_keep;
+  const int32_t* o = a.kept_all + (size_t)b * K;
+  auto lower = [&](int x) {  // first index with o[i] >= x (o ascending)
+    int lo = 0, hi = K;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (o[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+  };
+  for (int h = threadIdx.x; h < a.Hkv; h += 64)
+    a.kh[(size_t)b * a.Hkv + h] = lower((h + 1) * a.n_c) - lower(h * a.n_c);
+}
+
+static hipError_t launch_head_budgets(const CompressArgs& a, hipStream_t st) {
+  if (!a.adaptive || a.k_keep <= 0) return hipSuccess;
+  const int n = a.Hkv * a.n_c, k = a.Hkv * a.k_keep;
+  const dim3 grid(a.ntk_g, a.B);
+  hipLaunchKernelGGL(k_tk_cand, grid, dim3(TKT), 0, st, (const float*)a.abar, n, k,
+                     (const int*)nullptr, (const uint32_t*)a.tk_hs, a.tk_state_g, a.tk_cnt_g,
+                     a.tk_cand_g);
+  MKV_CHECK_LAUNCH();
+  hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, (const float*)a.abar, n, k,
+                     (const int*)nullptr, (const int*)a.tk_state_g, (const int*)a.tk_cnt_g,
+                     (const uint32_t*)a.tk_cand_g, a.kept_all, k, 0);
+  MKV_CHECK_LAUNCH();
+  hipLaunchKernelGGL(k_ada_counts, dim3(a.B), dim3(64), 0, st, a);
   MKV_CHECK_LAUNCH();
   return hipSuccess;
 }
@@ -1190,17 +1248,19 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL((k_mass<T, D, 2 * MTW>), dim3(a.nsl2, H), blk, 0, st, a);
   MKV_CHECK_LAUNCH();
+  hipError_t te = launch_head_budgets(a, st);
+  if (te != hipSuccess) return te;
   const float* first_scores = a.mi_rounds < 0 ? a.abar : a.score0;
   int32_t* first_out = a.mi_rounds >= 1 ? a.kept0 : a.kept;
-  hipError_t te = launch_topk(a, first_scores, 0, first_out, st);
+  te = launch_topk(a, first_scores, 0, first_out, st);
   if (te != hipSuccess) return te;
   const dim3 red_grid(((D * D + 2 * D) / 4 + 31) / 32, H);
   if (a.mi_rounds >= 1) {
     if (a.k_keep > 0) {
-      hipLaunchKernelGGL((k_gather_rows<T, D>), dim3((a.k_keep * (D / 8) + 255) / 256, H), blk, 0, st, a);
+      hipLaunchKernelGGL((k_gather_rows<T, D>), dim3((a.kmax * (D / 8) + 255) / 256, H), blk, 0, st, a);
       MKV_CHECK_LAUNCH();
       hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const void*)a.gath_k,
-                         (const void*)a.gath_v, a.kmax, 0, a.k_keep);
+                         (const void*)a.gath_v, a.kmax, 0, a.kh ? -1 : a.k_keep);
       MKV_CHECK_LAUNCH();
     }
     hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.s0, a.sv0, a.sk0, (int32_t*)nullptr);
@@ -1210,11 +1270,13 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
     te = launch_topk(a, a.score, 1, a.kept, st);
     if (te != hipSuccess) return te;
   }
-  hipLaunchKernelGGL((k_gather_out<T, D>), dim3((a.L * (D / 8) + 255) / 256, H), blk, 0, st, a, a.L, 0);
+  const int n_out_max = a.kh ? a.n_s + a.w + a.kmax : a.L;  // the longest head's rows
+  hipLaunchKernelGGL((k_gather_out<T, D>), dim3((n_out_max * (D / 8) + 255) / 256, H), blk, 0, st, a,
+                     a.L, 0);
   MKV_CHECK_LAUNCH();
   if (a.k_keep > 0) {
     hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const void*)a.k_out,
-                       (const void*)a.v_out, a.cap, a.n_s, a.k_keep);
+                       (const void*)a.v_out, a.cap, a.n_s, a.kh ? -1 : a.k_keep);
     MKV_CHECK_LAUNCH();
   }
   hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.S, a.s_v, a.s_k, a.n_e);
@@ -1231,7 +1293,8 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
     return hipGetLastError();
   if (dbg_kept0 && a.k_keep > 0) {
     const int32_t* src = a.mi_rounds >= 1 ? a.kept0 : a.kept;
-    if (hipMemcpy2DAsync(dbg_kept0, (size_t)a.k_keep * 4, src, (size_t)a.kmax * 4, (size_t)a.k_keep * 4,
+    const size_t rows = a.kh ? a.kmax : a.k_keep;
+    if (hipMemcpy2DAsync(dbg_kept0, rows * 4, src, (size_t)a.kmax * 4, rows * 4,
                          H, hipMemcpyDeviceToDevice, st) != hipSuccess)
       return hipGetLastError();
   }

@@ -36,7 +36,14 @@ mkv_status check_compress_params(const mkv_compress_params* p) {
   if (p->mi_rounds < -1 || p->mi_rounds > 1) return MKV_ERR_UNSUPPORTED;
   if (p->ctx_len - p->window - p->n_sink > kMaxCandidates) return MKV_ERR_UNSUPPORTED;
   if (p->budget < p->ctx_len && p->budget < p->n_sink + p->window) return MKV_ERR_BUDGET;
-  const int n_out = p->budget < p->ctx_len ? p->budget : p->ctx_len;
+  if (p->adaptive != 0 && p->adaptive != 1) return MKV_ERR_SHAPE;
+  int n_out = p->budget < p->ctx_len ? p->budget : p->ctx_len;
+  if (p->adaptive && p->budget < p->ctx_len) {
+    const int64_t n_c = p->ctx_len - p->window - p->n_sink;
+    const int64_t k_keep = p->budget - p->n_sink - p->window;
+    if ((int64_t)p->n_kv_heads * n_c > kMaxCandidates) return MKV_ERR_UNSUPPORTED;
+    n_out = (int)(p->n_sink + p->window + std::min<int64_t>(n_c, (int64_t)p->n_kv_heads * k_keep));
+  }
   if (p->cap < n_out) return MKV_ERR_CAPACITY;
   const double elems = (double)p->batch * p->n_kv_heads * p->ctx_len * p->head_dim;
   if (elems > 4.0e12) return MKV_ERR_UNSUPPORTED;
@@ -62,7 +69,11 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.R = a.G * a.w;
   a.n_c = a.N - a.w - a.n_s;
   a.k_keep = a.L < a.N ? a.L - a.n_s - a.w : 0;
-  a.kmax = a.k_keep > 1 ? a.k_keep : 1;
+  a.adaptive = (p->adaptive && a.L < a.N) ? 1 : 0;
+  // rows of the kept-candidate buffers: k_keep, or the most any head can take
+  const int kcap = a.adaptive ? std::min(a.n_c, a.Hkv * a.k_keep) : a.k_keep;
+  a.kmax = kcap > 1 ? kcap : 1;
+  a.idx_stride = a.adaptive ? p->cap : std::min(a.L, a.N);
   a.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)a.D);
   a.tau = p->tau;
   a.ntile = ceil_div(a.N, 64);
@@ -77,7 +88,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.nsl2 = ceil_div(a.ntile, a.tps2);
   // downdate covariance over the kept rows
   if (a.k_keep > 0) {
-    const int ntr = ceil_div(a.k_keep, 64);
+    const int ntr = ceil_div(a.kmax, 64);  // the most rows any head keeps
     a.nslr = clampi(ceil_div(256, a.H), 1, ntr);
     a.tpsr = ceil_div(ntr, a.nslr);
     a.nslr = ceil_div(ntr, a.tpsr);
@@ -95,6 +106,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   }
   // top-k slices of 2048 candidates (at most 128 for kMaxCandidates)
   a.ntk = ceil_div(a.n_c > 0 ? a.n_c : 1, 2048);
+  a.ntk_g = a.adaptive ? ceil_div(a.Hkv * a.n_c, 2048) : 1;
   const size_t H = a.H, D = a.D, es = elem_size(p->dtype);
   const size_t nc = a.n_c > 0 ? a.n_c : 1;
   Carver c;
@@ -118,6 +130,15 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.sk0 = c.take<float>(H * D * sizeof(float));
   a.gath_k = c.take<void>(H * a.kmax * D * es);
   a.gath_v = c.take<void>(H * a.kmax * D * es);
+  if (a.adaptive) {
+    const size_t Bs = a.B;
+    a.kh = c.take<int32_t>(H * sizeof(int32_t));
+    a.kept_all = c.take<int32_t>(Bs * a.Hkv * std::max(a.k_keep, 1) * sizeof(int32_t));
+    a.tk_hs = c.take<uint32_t>(Bs * 2048 * sizeof(uint32_t));
+    a.tk_state_g = c.take<int32_t>(Bs * 2 * sizeof(int32_t));
+    a.tk_cnt_g = c.take<int32_t>(Bs * a.ntk_g * 2 * sizeof(int32_t));
+    a.tk_cand_g = c.take<uint32_t>(Bs * a.ntk_g * 2048 * sizeof(uint32_t));
+  }
   *total = c.off;
   return a;
 }

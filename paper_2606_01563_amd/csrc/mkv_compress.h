@@ -53,6 +53,16 @@ struct CompressArgs {
   int nslot;                // nsl1 + nslr
   int nsl3, tps3;           // residual pass: slices over candidate tiles of 64
   int ntk;                  // top-k slices of 2048 candidates
+  // head-adaptive budgets (adaptive = 1): a per-sequence selection over the layer
+  int adaptive;
+  int32_t* kh;              // [H] candidates kept per head, or null (k_keep everywhere)
+  int32_t* kept_all;        // [B, Hkv*k_keep] layer-wide kept candidates (head*n_c + j)
+  uint32_t* tk_hs;          // [B, 2048] key histogram of abar over the layer
+  int32_t* tk_state_g;      // [B, 2], and the candidate buffers of that selection:
+  int32_t* tk_cnt_g;        // [B, ntk_g, 2]
+  uint32_t* tk_cand_g;      // [B, ntk_g, 2048]
+  int ntk_g;                // slices of the layer-wide selection
+  int idx_stride;           // entries per head of idx_out
   float scale, tau;
 };
 

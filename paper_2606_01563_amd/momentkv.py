@@ -38,7 +38,8 @@ class CompressParams(ctypes.Structure):
                 ("window", ctypes.c_int32), ("n_sink", ctypes.c_int32),
                 ("chunk", ctypes.c_int32), ("mi_rounds", ctypes.c_int32),
                 ("cap", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("tau", ctypes.c_float)]
+                ("scale", ctypes.c_float), ("tau", ctypes.c_float),
+                ("adaptive", ctypes.c_int32)]
 
 
 class CompressDebug(ctypes.Structure):
@@ -171,27 +172,41 @@ class CompressOutput:
     kept0: torch.Tensor | None = None
 
 
+def compress_rows(N: int, Hkv: int, budget: int, window: int, n_sink: int = 1,
+                  adaptive: bool = False) -> int:
+    """Most rows any head keeps: min(budget, N), or with head-adaptive budgets
+    n_sink + window + min(n_c, Hkv * k_keep)."""
+    if not adaptive or budget >= N:
+        return min(budget, N)
+    n_c = N - window - n_sink
+    return n_sink + window + min(n_c, Hkv * (budget - n_sink - window))
+
+
 def compress_params(q_win, k, budget, *, n_sink=1, chunk=4, mi_rounds=1, cap=None,
-                    scale=0.0, tau=1e-6) -> CompressParams:
+                    scale=0.0, tau=1e-6, adaptive=False) -> CompressParams:
     B, Hq, w, d = q_win.shape
     _, Hkv, N, _ = k.shape
-    n_out = min(budget, N)
+    n_out = compress_rows(N, Hkv, budget, w, n_sink, adaptive)
     return CompressParams(B, Hq, Hkv, d, N, budget, w, n_sink, chunk, mi_rounds,
-                          n_out if cap is None else cap, _dtype_code(k), scale, tau)
+                          n_out if cap is None else cap, _dtype_code(k), scale, tau,
+                          1 if adaptive else 0)
 
 
 def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, budget: int, *,
                       n_sink: int = 1, chunk: int = 4, mi_rounds: int = 1, cap: int | None = None,
-                      scale: float = 0.0, tau: float = 1e-6, debug: bool = False,
-                      out: CompressOutput | None = None,
+                      scale: float = 0.0, tau: float = 1e-6, adaptive: bool = False,
+                      debug: bool = False, out: CompressOutput | None = None,
                       workspace: torch.Tensor | None = None) -> CompressOutput:
-    """Compress [B, Hkv, N, d] prefill K/V to `budget` rows per KV head (see the header)."""
+    """Compress [B, Hkv, N, d] prefill K/V to `budget` rows per KV head (see the header);
+    adaptive=True splits the layer's candidate budget across heads (idx then has `cap`
+    entries per head, the first `lens` of them valid)."""
     p = compress_params(q_win, k, budget, n_sink=n_sink, chunk=chunk, mi_rounds=mi_rounds,
-                        cap=cap, scale=scale, tau=tau)
+                        cap=cap, scale=scale, tau=tau, adaptive=adaptive)
     B, Hq, w, d = q_win.shape
     _, Hkv, N, _ = k.shape
     dev = k.device
-    n_out = min(budget, N)
+    ada = adaptive and budget < N
+    n_out = p.cap if ada else min(budget, N)
     if out is None:
         f32 = dict(dtype=torch.float32, device=dev)
         i32 = dict(dtype=torch.int32, device=dev)
@@ -209,7 +224,8 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
         out.abar = torch.zeros(B, Hkv, n_c, **f32)
         out.score0 = torch.zeros(B, Hkv, n_c, **f32)
         out.score = torch.zeros(B, Hkv, n_c, **f32)
-        out.kept0 = torch.zeros(B, Hkv, max(k_keep, 0), dtype=torch.int32, device=dev)
+        k_rows = min(n_c, Hkv * k_keep) if ada else k_keep
+        out.kept0 = torch.zeros(B, Hkv, max(k_rows, 0), dtype=torch.int32, device=dev)
         dbg = CompressDebug(_ptr(out.abar), _ptr(out.score0), _ptr(out.score),
                             _ptr(out.kept0) if k_keep > 0 else None)
     nbytes = momentkv_compress_workspace_size(p)

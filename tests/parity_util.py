@@ -78,7 +78,7 @@ def check_compress_head(inp_cpu: dict, out: mk.CompressOutput, b: int, h: int, b
     w = q.shape[2]
     scale = 1.0 / math.sqrt(d)
     n_out = min(budget, N)
-    idx = out.idx[b, h].cpu().numpy().astype(np.int64)
+    idx = out.idx[b, h, :n_out].cpu().numpy().astype(np.int64)
     errs = {}
     # retained rows are copies of the input rows (bit-exact)
     tidx = torch.from_numpy(idx)
@@ -103,7 +103,8 @@ def check_compress_head(inp_cpu: dict, out: mk.CompressOutput, b: int, h: int, b
     abar_g = out.abar[b, h].cpu().double().numpy()
     s0_g = out.score0[b, h].cpu().double().numpy()
     s1_g = out.score[b, h].cpu().double().numpy()
-    kept0 = out.kept0[b, h].cpu().numpy().astype(np.int64) if k_keep > 0 else np.zeros(0, np.int64)
+    kept0 = (out.kept0[b, h, :k_keep].cpu().numpy().astype(np.int64) if k_keep > 0
+             else np.zeros(0, np.int64))
     # 1. selection logic is exact on the GPU's own scores
     if k_keep > 0:
         first = abar_g if mi_rounds < 0 else s0_g
@@ -290,3 +291,40 @@ def run_evict_steps(inp: dict, comp: mk.CompressOutput, steps: int, budget: int,
         worst = max(worst, e)
     assert int(ws[:4].view(torch.int32)[0]) == flag
     return worst, swaps, evictions
+
+
+def check_head_budgets(inp_cpu: dict, out: mk.CompressOutput, b: int, budget: int, *,
+                       n_sink=1, chunk=4) -> tuple[np.ndarray, int]:
+    """Head-adaptive split of sequence b: the GPU's per-head counts (lens - n_sink - w) are
+    exactly the split of the GPU's own pooled masses (layer-wide order by (-mass, head,
+    position)); against the oracle's masses, the layer-wide kept sets may differ only by
+    swaps inside the selection band of the boundary mass.  Returns (k_h, swaps)."""
+    dt = inp_cpu["k"].dtype
+    Hkv = inp_cpu["k"].shape[1]
+    w = inp_cpu["q_win"].shape[2]
+    N, d = inp_cpu["k"].shape[2], inp_cpu["k"].shape[3]
+    G = inp_cpu["q_win"].shape[1] // Hkv
+    k_keep = budget - n_sink - w
+    kh = out.lens[b].cpu().numpy().astype(np.int64) - n_sink - w
+    ab_g = out.abar[b].cpu().double().numpy()                      # [Hkv, n_c]
+    np.testing.assert_array_equal(O.head_budgets(ab_g, k_keep), kh)
+    q = h64(inp_cpu["q_win"][b:b + 1])
+    ab_o = np.stack([O.chunk_pool(O.window_attention_mass(q[0, h * G:(h + 1) * G],
+                                                          h64(inp_cpu["k"][b, h]), 1 / math.sqrt(d)),
+                                  n_sink, chunk) for h in range(Hkv)])
+    assert rel_l2(ab_g, ab_o) <= TOL[dt]
+    n = ab_o.shape[1]
+    def kept_set(ab, counts):
+        sel = set()
+        for h in range(Hkv):
+            order = np.lexsort((np.arange(n), -ab[h]))[:counts[h]]
+            sel.update(int(h * n + j) for j in order)
+        return sel
+    got = kept_set(ab_g, kh)
+    ref = kept_set(ab_o, O.head_budgets(ab_o, k_keep))
+    flat = ab_o.reshape(-1)
+    T = np.sort(flat)[::-1][Hkv * k_keep - 1]
+    band = SEL_BAND[dt]
+    for x in got ^ ref:
+        assert abs(flat[x] - T) <= band * T, (x, flat[x], T)
+    return kh, len(got ^ ref) // 2

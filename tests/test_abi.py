@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert mk.momentkv_abi_version() == 3
+    assert mk.momentkv_abi_version() == 4
     for code in range(10):
         assert mk.momentkv_status_string(code) not in ("", "unknown status")
     assert mk.momentkv_status_string(99) == "unknown status"
@@ -37,7 +37,8 @@ def test_abi_version_and_status_strings(L):
 
 def cparams(**kw):
     base = dict(batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, ctx_len=32768, budget=512,
-                window=32, n_sink=1, chunk=4, mi_rounds=1, cap=512, dtype=1, scale=0.0, tau=1e-6)
+                window=32, n_sink=1, chunk=4, mi_rounds=1, cap=512, dtype=1, scale=0.0, tau=1e-6,
+                adaptive=0)
     base.update(kw)
     return mk.CompressParams(**base)
 
@@ -97,6 +98,9 @@ def test_workspace_sizes(L):
     (dict(budget=20), BUDGET),              # < n_sink + window
     (dict(cap=100), CAPACITY),
     (dict(dtype=7), DTYPE),
+    (dict(adaptive=2), SHAPE),
+    (dict(adaptive=1), CAPACITY),          # a head may take up to 8 x 479 candidates
+    (dict(adaptive=1, ctx_len=40000, cap=8000), UNSUP),   # 8 x n_c candidates > 262144
 ])
 def test_compress_rejects_invalid_parameters(L, kw, code):
     assert compress_status(cparams(**kw)) == code
@@ -117,6 +121,14 @@ def test_compress_rejects_null_alias_and_small_workspace(L):
     # workspace overlapping v
     ptrs = [(1 << 20) + i * (1 << 36) for i in range(11)]
     assert mk.lib().momentkv_compress(ctypes.byref(p), *ptrs, None, ptrs[2], size, None) == ALIAS
+
+
+def test_adaptive_workspace_and_capacity(L):
+    rows = 1 + 32 + 8 * 479
+    p = cparams(adaptive=1, cap=rows)
+    assert mk.momentkv_compress_workspace_size(p) > mk.momentkv_compress_workspace_size(cparams())
+    assert mk.compress_rows(32768, 8, 512, 32, 1, adaptive=True) == rows
+    assert compress_status(cparams(adaptive=1, cap=rows - 1)) == CAPACITY
 
 
 def test_budget_at_least_context_is_valid(L):

@@ -451,3 +451,49 @@ def test_evict_group_sizes_and_long_caches(G, budget):
     worst, swaps, n = P.run_evict_steps(gpu, out, 2, budget)
     announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
     assert n == 4
+
+
+# ---------------------------------------------------------------- head-adaptive budgets
+@pytest.mark.parametrize("mi_rounds", [1, 0, -1])
+def test_adaptive_budgets_llama_layer(mi_rounds):
+    """Two sequences x 8 KV heads at budget 160 with the layer's candidate budget split by
+    pooled mass; head 0 made sharper and head 1 flatter so the counts spread widely.  The
+    split, every head's selection with its own count, the moments and the retained rows
+    follow the full protocol; then decode runs over the per-head lengths."""
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=2, ctx_len=3000, batch=2)
+    for x in (cpu, gpu):
+        x["k"][:, 0] *= 3.0
+        x["k"][:, 1] *= 0.05
+    L = 160
+    cap = mk.compress_rows(3000, 8, L, wl.window, adaptive=True)
+    out = P.run_compress(gpu, L, cap=cap, adaptive=True, mi_rounds=mi_rounds)
+    for b in range(2):
+        kh, swaps = P.check_head_budgets(cpu, out, b, L)
+        announce(f"mi_rounds={mi_rounds} seq {b} per-head counts {list(kh)}, swaps {swaps}")
+        assert kh.sum() == 8 * (L - 1 - wl.window) and len(set(kh)) > 2
+        for h in range(8):
+            P.check_compress_head(cpu, out, b, h, int(1 + wl.window + kh[h]), mi_rounds=mi_rounds)
+    if mi_rounds == 1:
+        P.run_decode_steps(gpu, out, 2)
+
+
+def test_adaptive_budgets_with_one_head_equal_uniform():
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1)
+    L = wl.budgets[0]
+    uni = P.run_compress(gpu, L, cap=L)
+    ada = P.run_compress(gpu, L, cap=L, adaptive=True)
+    for name in ("k_out", "v_out", "idx", "lens", "n_e", "s_k", "s_v", "S"):
+        assert torch.equal(getattr(uni, name), getattr(ada, name)), name
+
+
+def test_adaptive_budgets_qwen_layer_full_size():
+    """One 32K layer at budget 128: the layer-wide selection runs over 8 x 32735
+    candidates (128 slices); counts checked against the GPU's masses and the oracle's."""
+    wl, cpu, gpu = layer("qwen3_4b_stack_n32768", steps=1)
+    L = 128
+    cap = mk.compress_rows(wl.ctx_len, 8, L, wl.window, adaptive=True)
+    out = P.run_compress(gpu, L, cap=cap, adaptive=True)
+    kh, swaps = P.check_head_budgets(cpu, out, 0, L)
+    announce(f"qwen 32K per-head counts {list(kh)}, swaps {swaps}")
+    for h in (0, 5):
+        P.check_compress_head(cpu, out, 0, h, int(1 + wl.window + kh[h]))
