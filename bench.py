@@ -24,8 +24,9 @@ times (replay of the whole phase minus replay of the phase without that budget, 
 other budgets still keep the last-level cache cold), a roofline object for the decode call
 and the fp64 oracle timed on the host as a CPU baseline.  Two further phases are measured
 the same way on the same compressed stacks and reported beside the headline, which they do
-not change: the decode with the summary in half precision (`decode_half_summary`) and the
-decode step with moment-informed eviction at every token (`evict_decode`).  Events are
+not change: the decode with the summary in half precision (`decode_half_summary`), the
+compress with head-adaptive budgets (`compress_adaptive`) and the decode step with
+moment-informed eviction at every token (`evict_decode`).  Events are
 recorded on the stream the library launches on.
 """
 from __future__ import annotations
@@ -201,6 +202,51 @@ def half_summary_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_st
             "GBps": all_bytes / (total * 1e-3) / 1e9, "per_budget": per_budget}
 
 
+def adaptive_measurement(args, wl, data, layers, L, dev) -> dict:
+    """Compress of every layer with head-adaptive budgets at budget L (the layer's
+    candidate budget split over its heads by pooled mass): ms per layer from HIP events
+    around the layers' calls, and the spread of the per-head retained lengths."""
+    N, Hkv, d, w = wl.ctx_len, wl.n_kv_heads, wl.head_dim, wl.window
+    cap = mk.compress_rows(N, Hkv, L, w, adaptive=True)
+    B = wl.batch
+    f32 = dict(dtype=torch.float32, device=dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    outs = [mk.CompressOutput(
+        k_out=torch.empty(B, Hkv, cap, d, dtype=wl.dtype, device=dev),
+        v_out=torch.empty(B, Hkv, cap, d, dtype=wl.dtype, device=dev),
+        idx=torch.empty(B, Hkv, cap, **i32), lens=torch.empty(B, Hkv, **i32),
+        n_e=torch.empty(B, Hkv, **i32), s_k=torch.empty(B, Hkv, d, **f32),
+        s_v=torch.empty(B, Hkv, d, **f32), S=torch.empty(B, Hkv, d, d, **f32))
+        for _ in range(layers)]
+    ws = torch.empty(mk.momentkv_compress_workspace_size(
+        mk.compress_params(data[0]["q_win"], data[0]["k"], L, cap=cap, adaptive=True)),
+        dtype=torch.uint8, device=dev)
+
+    def run():
+        for l in range(layers):
+            x = data[l]
+            mk.momentkv_compress(x["q_win"], x["k"], x["v"], L, cap=cap, adaptive=True,
+                                 out=outs[l], workspace=ws)
+
+    run()
+    torch.cuda.synchronize()
+    ev = []
+    for _ in range(args.steps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev) / layers
+    lens = torch.stack([o.lens for o in outs]).float()
+    return {"what": f"momentkv_compress(adaptive=True) of each layer at budget {L}",
+            "budget": L, "compress_ms_per_layer": ms,
+            "retained_rows_per_head": {"min": int(lens.min()), "mean": float(lens.mean()),
+                                       "max": int(lens.max())}}
+
+
 def evict_bytes(n_heads: int, G: int, d: int, L: int, elem: int = 2) -> int:
     """Algorithmic HBM bytes of one decode call with eviction at budget L (per KV head,
     summed): the decode bytes over the L + 1 rows seen by Phase 1 (retained rows read once,
@@ -316,6 +362,8 @@ def main() -> int:
                     help="skip the decode-with-eviction measurement")
     ap.add_argument("--no-half", action="store_true",
                     help="skip the half-precision summary measurement")
+    ap.add_argument("--no-adaptive", action="store_true",
+                    help="skip the head-adaptive compress measurement")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one plain copy of "
                          "known size, then 4 tokens x budgets of eager decode calls; prints "
@@ -531,6 +579,8 @@ def main() -> int:
         if half.get("error"):
             print(f"[bench] {half['error']}", file=sys.stderr)
             return 6
+    ada = None if args.no_adaptive else adaptive_measurement(args, wl, data, layers,
+                                                              budgets[0], dev)
     evict = None if args.no_evict else evict_measurement(
         args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out, compress_phase, capture,
         timed_replay)
@@ -573,6 +623,8 @@ def main() -> int:
     }
     if half is not None:
         res["decode_half_summary"] = half
+    if ada is not None:
+        res["compress_adaptive"] = ada
     if evict is not None:
         res["evict_decode"] = evict
     if not args.no_cpu_baseline:
