@@ -122,6 +122,16 @@ template <int D, int NW> struct CovSplit {
   }
 };
 
+// Transposed tiles in LDS ([dim][token], rows padded by 16 bytes): for bf16 the 16-byte
+// chunks of a row are XOR-swizzled by bits 3..5 of the row, so that the pair writes of a
+// wave (16 column groups, i.e. rows 8g + c, one chunk) spread over the banks while every
+// MFMA fragment read still fetches one whole chunk.  fp32 tiles are not swizzled.
+template <class T>
+__device__ __forceinline__ int tcol(int row, int col) {
+  if constexpr (sizeof(T) == 2) return col ^ (((row >> 3) & 7) << 3);
+  else return col;
+}
+
 // cacc += V_tile^T K_tile over the TILE tokens held transposed in LDS.
 template <class T, int D, int NW, int LD>
 __device__ __forceinline__ void cov_tile(const T (*sVT)[LD], const T (*sKT)[LD],
@@ -131,30 +141,50 @@ __device__ __forceinline__ void cov_tile(const T (*sVT)[LD], const T (*sKT)[LD],
   const int a0 = CovSplit<D, NW>::a0(wave), b0 = CovSplit<D, NW>::b0(wave);
 #pragma unroll
   for (int kk = 0; kk < TILE / 32; ++kk) {
+    const int col = 32 * kk + 8 * (lane >> 4);
     typename Frag<T>::type af[QM];
 #pragma unroll
-    for (int mi = 0; mi < QM; ++mi)
-      af[mi] = load_frag(&sVT[a0 + 16 * mi + (lane & 15)][32 * kk + 8 * (lane >> 4)]);
+    for (int mi = 0; mi < QM; ++mi) {
+      const int r = a0 + 16 * mi + (lane & 15);
+      af[mi] = load_frag(&sVT[r][tcol<T>(r, col)]);
+    }
 #pragma unroll
     for (int ni = 0; ni < QN; ++ni) {
-      typename Frag<T>::type bf = load_frag(&sKT[b0 + 16 * ni + (lane & 15)][32 * kk + 8 * (lane >> 4)]);
+      const int r = b0 + 16 * ni + (lane & 15);
+      typename Frag<T>::type bf = load_frag(&sKT[r][tcol<T>(r, col)]);
 #pragma unroll
       for (int mi = 0; mi < QM; ++mi) mma(cacc[mi][ni], af[mi], bf);
     }
   }
 }
 
-// Register staging of one 64-token tile of K and V for NT threads.  Thread t holds tokens
-// 2p and 2p+1 (p = t % 32) in the 8-column groups g0 + (NT/32)*i (g0 = t / 32, i < NDG):
-// lanes run along tokens, so the transposed LDS copies are written as packed pairs of
-// consecutive tokens and the 32 lanes of a half-wave hit 32 different banks.  With more
-// half-waves than column groups (NT = 512, D = 64) the surplus threads hold nothing.
+// Register staging of one 64-token tile of K and V for NT threads.  Thread t holds the
+// 8-column group g = t % (D/8) of NP token pairs (2p, 2p+1), p = t / (D/8) + PSTEP * i:
+// the lanes of a wave read whole rows (one load instruction covers 64 / (D/8) / 2 rows,
+// contiguous 16-byte pieces), and the transposed LDS copies are written as packed pairs
+// of consecutive tokens.  With more threads than pieces of a tile (NT = 512, D = 64) the
+// surplus threads hold nothing.
 template <class T, int D, int NT> struct TileRegs {
-  static constexpr int GROUPS = D / 8, HALVES = NT / 32;
-  static constexpr int NDG = GROUPS > HALVES ? GROUPS / HALVES : 1;
-  typename Frag<T>::type k[NDG][2], v[NDG][2];
-  static __device__ __forceinline__ bool active(int tid) { return (tid >> 5) < GROUPS; }
-  static __device__ __forceinline__ int group(int tid, int i) { return (tid >> 5) + HALVES * i; }
+  static constexpr int GROUPS = D / 8;
+  static constexpr int PSTEP = NT / GROUPS;              // pairs covered by one register set
+  static constexpr int NP = PSTEP >= TILE / 2 ? 1 : TILE / 2 / PSTEP;
+  typename Frag<T>::type k[NP][2], v[NP][2];
+  // Marks the point where the tile is used: the registers become opaque values there, so
+  // no select or other use is moved up to the load (which would wait for it at once).
+  __device__ __forceinline__ void arrive() {
+#pragma unroll
+    for (int i = 0; i < NP; ++i)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        asm volatile("" : "+v"(k[i][h]));
+        asm volatile("" : "+v"(v[i][h]));
+      }
+  }
+  static __device__ __forceinline__ bool active(int tid) { return tid < TILE / 2 * GROUPS; }
+  static __device__ __forceinline__ int group(int tid) { return tid % GROUPS; }
+  static __device__ __forceinline__ int pair(int tid, int i) {
+    return min(tid / GROUPS, TILE / 2 - 1) + PSTEP * i;  // surplus threads: a valid pair
+  }
 };
 
 __device__ __forceinline__ void store_pair(bf16_t* p, bf16_t lo, bf16_t hi) {
@@ -164,26 +194,31 @@ __device__ __forceinline__ void store_pair(float* p, float lo, float hi) {
   *reinterpret_cast<float2*>(p) = make_float2(lo, hi);
 }
 
-// Rows row0 + 2p and row0 + 2p + 1 of K and V (head base pointers); a false flag loads zeros.
+// Rows row0 + 2p and row0 + 2p + 1 of K and V (head base pointers), clamped to the
+// n_rows readable rows.  Every lane issues all of its loads and nothing selects on them
+// here: a load under a per-lane branch, or a use right after it, would make the compiler
+// wait for the loads at once (the prefetched tile's included) instead of where the tile
+// is used.  Rows past the end are dropped where the tile is used.
 template <class T, int D, int NT>
 __device__ __forceinline__ void tile_load(TileRegs<T, D, NT>& R, const T* Kh, const T* Vh, int row0,
-                                          bool k0, bool k1, bool v0, bool v1, int tid) {
+                                          int n_rows, int tid) {
   typedef TileRegs<T, D, NT> TR;
-  const int p = tid & 31;
-  const bool act = TR::active(tid);
-  const size_t r0 = (size_t)(row0 + 2 * p) * D, r1 = r0 + D;
+  const int col = 8 * TR::group(tid);
 #pragma unroll
-  for (int i = 0; i < TR::NDG; ++i) {
-    const int col = 8 * TR::group(tid, i);
-    R.k[i][0] = (act && k0) ? load_frag(Kh + r0 + col) : zero_frag<T>();
-    R.k[i][1] = (act && k1) ? load_frag(Kh + r1 + col) : zero_frag<T>();
-    R.v[i][0] = (act && v0) ? load_frag(Vh + r0 + col) : zero_frag<T>();
-    R.v[i][1] = (act && v1) ? load_frag(Vh + r1 + col) : zero_frag<T>();
+  for (int i = 0; i < TR::NP; ++i) {
+    const int p = TR::pair(tid, i);
+    const size_t r0 = (size_t)min(row0 + 2 * p, n_rows - 1) * D;
+    const size_t r1 = (size_t)min(row0 + 2 * p + 1, n_rows - 1) * D;
+    R.k[i][0] = load_frag(Kh + r0 + col);
+    R.k[i][1] = load_frag(Kh + r1 + col);
+    R.v[i][0] = load_frag(Vh + r0 + col);
+    R.v[i][1] = load_frag(Vh + r1 + col);
   }
 }
 
-// Transposed copies K^T, V^T of the tile (K rows of non-candidates zeroed), running sums
-// of k and v over the thread's columns and the thread's share of each row's ||v||^2.
+// Transposed copies K^T, V^T of the tile with the rows of tokens outside the summed set
+// zeroed (flag in(j) of token j), running sums of k and v over the thread's 8 columns,
+// and ||v_j||^2 of the thread's tokens over its columns (ss[i][h], token 2p_i + h).
 // bf16: the two tokens' elements are paired with one byte permute per column, and the
 // sums and squares use the bf16 dot2 instruction (exact products, fp32 accumulation).
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -194,69 +229,74 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
                                          c, false);
 }
 
-template <class T, int D, int NT, int LDT>
+template <class T, int D, int NT, int LDT, class In>
 __device__ __forceinline__ void tile_store_t(const TileRegs<T, D, NT>& R, T (*sKT)[LDT],
-                                             T (*sVT)[LDT], bool c0, bool c1,
-                                             float (&sk)[TileRegs<T, D, NT>::NDG][8],
-                                             float (&sv)[TileRegs<T, D, NT>::NDG][8], float& ss0,
-                                             float& ss1, int tid) {
+                                             T (*sVT)[LDT], int tok0, In in, float (&sk)[8],
+                                             float (&sv)[8], float (&ss)[TileRegs<T, D, NT>::NP][2],
+                                             int tid) {
   typedef TileRegs<T, D, NT> TR;
-  const int p = tid & 31;
-  ss0 = ss1 = 0.f;
-  if (!TR::active(tid)) return;
-  if constexpr (sizeof(T) == 2) {
-    constexpr uint32_t ONES = 0x3F803F80u;  // (1.0, 1.0) in bf16
+  const int row = 8 * TR::group(tid);
+  const bool act = TR::active(tid);
 #pragma unroll
-    for (int i = 0; i < TR::NDG; ++i) {
-      const int row = 8 * TR::group(tid, i);
+  for (int i = 0; i < TR::NP; ++i) {
+    const int p = TR::pair(tid, i);
+    const bool c0 = act && in(tok0 + 2 * p), c1 = act && in(tok0 + 2 * p + 1);
+    ss[i][0] = ss[i][1] = 0.f;
+    if constexpr (sizeof(T) == 2) {
+      constexpr uint32_t ONES = 0x3F803F80u;  // (1.0, 1.0) in bf16
       const u32x4 k0 = __builtin_bit_cast(u32x4, R.k[i][0]), k1 = __builtin_bit_cast(u32x4, R.k[i][1]);
       const u32x4 v0 = __builtin_bit_cast(u32x4, R.v[i][0]), v1 = __builtin_bit_cast(u32x4, R.v[i][1]);
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const uint32_t a0 = c0 ? k0[w] : 0u, a1 = c1 ? k1[w] : 0u;
+        const uint32_t b0 = c0 ? v0[w] : 0u, b1 = c1 ? v1[w] : 0u;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const uint32_t sel = h ? 0x07060302u : 0x05040100u;  // (token 0, token 1) of column 2w+h
           const uint32_t kp = __builtin_amdgcn_perm(a1, a0, sel);
-          const uint32_t vp = __builtin_amdgcn_perm(v1[w], v0[w], sel);
-          *reinterpret_cast<uint32_t*>(&sKT[row + 2 * w + h][2 * p]) = kp;
-          *reinterpret_cast<uint32_t*>(&sVT[row + 2 * w + h][2 * p]) = vp;
-          sk[i][2 * w + h] = dot2_bf16(kp, ONES, sk[i][2 * w + h]);
-          sv[i][2 * w + h] = dot2_bf16(vp, ONES, sv[i][2 * w + h]);
+          const uint32_t vp = __builtin_amdgcn_perm(b1, b0, sel);
+          const int r = row + 2 * w + h;
+          if (act) {
+            *reinterpret_cast<uint32_t*>(&sKT[r][tcol<T>(r, 2 * p)]) = kp;
+            *reinterpret_cast<uint32_t*>(&sVT[r][tcol<T>(r, 2 * p)]) = vp;
+          }
+          sk[2 * w + h] = dot2_bf16(kp, ONES, sk[2 * w + h]);
+          sv[2 * w + h] = dot2_bf16(vp, ONES, sv[2 * w + h]);
         }
-        ss0 = dot2_bf16(v0[w], v0[w], ss0);
-        ss1 = dot2_bf16(v1[w], v1[w], ss1);
+        ss[i][0] = dot2_bf16(b0, b0, ss[i][0]);
+        ss[i][1] = dot2_bf16(b1, b1, ss[i][1]);
       }
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < TR::NDG; ++i) {
-      const int row = 8 * TR::group(tid, i);
+    } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float k0 = c0 ? elem_f(R.k[i][0], e) : 0.f, k1 = c1 ? elem_f(R.k[i][1], e) : 0.f;
-        const float x0 = elem_f(R.v[i][0], e), x1 = elem_f(R.v[i][1], e);
-        store_pair(&sKT[row + e][2 * p], k0, k1);
-        store_pair(&sVT[row + e][2 * p], x0, x1);
-        ss0 += x0 * x0;
-        ss1 += x1 * x1;
-        sv[i][e] += x0 + x1;
-        sk[i][e] += k0 + k1;
+        const float x0 = c0 ? elem_f(R.v[i][0], e) : 0.f, x1 = c1 ? elem_f(R.v[i][1], e) : 0.f;
+        if (act) {
+          store_pair(&sKT[row + e][tcol<T>(row + e, 2 * p)], k0, k1);
+          store_pair(&sVT[row + e][tcol<T>(row + e, 2 * p)], x0, x1);
+        }
+        ss[i][0] += x0 * x0;
+        ss[i][1] += x1 * x1;
+        sv[e] += x0 + x1;
+        sk[e] += k0 + k1;
       }
     }
   }
 }
 
-// Write one slot of covariance and (s_v, s_k) partials; `sign` = -1 for downdates.
+// Write one slot of covariance and (s_v, s_k) partials; `sign` = -1 for downdates.  The
+// column sums of the threads sharing a column group are added within each wave (lanes
+// g, g + 16, ... for D = 128) and then over the waves in order through `red`
+// (NW * 2 * D floats of LDS that are free to reuse).
 template <class T, int D, int NT>
 __device__ __forceinline__ void write_cov_partials(
     const CompressArgs& a, int head, int slot,
     f32x4 (&cacc)[CovSplit<D, NT / 64>::QM][CovSplit<D, NT / 64>::QN],
-    float (&sv)[TileRegs<T, D, NT>::NDG][8], float (&sk)[TileRegs<T, D, NT>::NDG][8], float sign,
-    int tid) {
+    float (&sv)[8], float (&sk)[8], float sign, float* red, int tid) {
   constexpr int NW = NT / 64;
   constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
   typedef TileRegs<T, D, NT> TR;
+  constexpr int G = TR::GROUPS;  // 16 or 8: lanes sharing a group are G apart
   const int lane = tid & 63, wave = tid >> 6;
   const int a0 = CovSplit<D, NW>::a0(wave), b0 = CovSplit<D, NW>::b0(wave);
   float* sp = a.spart + ((size_t)head * a.nslot + slot) * D * D;
@@ -268,22 +308,24 @@ __device__ __forceinline__ void write_cov_partials(
       for (int i = 0; i < 4; ++i)
         sp[(size_t)(a0 + 16 * mi + 4 * (lane >> 4) + i) * D + b0 + 16 * ni + (lane & 15)] =
             sign * cacc[mi][ni][i];
-  // the 32 lanes of a half-wave share the column groups of TileRegs
-  float* svk = a.svkpart + ((size_t)head * a.nslot + slot) * 2 * D;
-  const bool act = TR::active(tid);
 #pragma unroll
-  for (int i = 0; i < TR::NDG; ++i)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float x = row16_sum(sv[i][e]);
-      x += __shfl_xor(x, 16);
-      float y = row16_sum(sk[i][e]);
-      y += __shfl_xor(y, 16);
-      if ((lane & 31) == 0 && act) {
-        svk[8 * TR::group(tid, i) + e] = sign * x;
-        svk[D + 8 * TR::group(tid, i) + e] = sign * y;
-      }
+  for (int e = 0; e < 8; ++e) {
+    const float x = same_group_sum<G>(sv[e]), y = same_group_sum<G>(sk[e]);
+    if (lane < G && TR::active(tid)) {
+      red[(wave * 2 + 0) * D + 8 * lane + e] = x;
+      red[(wave * 2 + 1) * D + 8 * lane + e] = y;
     }
+  }
+  __syncthreads();
+  constexpr int NWA = (TILE / 2 * G + 63) / 64 < NW ? (TILE / 2 * G + 63) / 64 : NW;  // waves holding data
+  float* svk = a.svkpart + ((size_t)head * a.nslot + slot) * 2 * D;
+  for (int c = tid; c < 2 * D; c += NT) {
+    const int part = c / D, col = c % D;
+    float acc = 0.f;
+#pragma unroll
+    for (int w = 0; w < NWA; ++w) acc += red[(w * 2 + part) * D + col];
+    svk[c] = sign * acc;
+  }
 }
 
 // ------------------------------------------------------------------------------------
@@ -301,7 +343,7 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
   __shared__ __align__(16) T sK[TILE][LDK];
   __shared__ __align__(16) T sKT[D][LDT];
   __shared__ __align__(16) T sVT[D][LDT];
-  __shared__ float sVn[NW][TILE];
+  __shared__ float sVnorm[kRowsMaxTiles * TILE];  // ||v_j|| of the slice, written at the end
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
@@ -319,10 +361,11 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
   for (int k = 0; k < MTW; ++k) {
     const int mt = wave + NW * k;
     const int r = 16 * mt + (lane & 15);
+    // rows past R repeat row R-1: their statistics are never stored (no select on the
+    // loaded value, which would wait for it before the tile loads are issued)
+    const T* qrow = window_row<T>(a, head, min(r, a.R - 1));
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[k][ks] = (mt < RT && r < a.R) ? load_frag(window_row<T>(a, head, r) + 32 * ks + 8 * (lane >> 4))
-                                       : zero_frag<T>();
+    for (int ks = 0; ks < KS; ++ks) qf[k][ks] = load_frag(qrow + 32 * ks + 8 * (lane >> 4));
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int rr = 16 * mt + 4 * (lane >> 4) + i;
@@ -336,50 +379,52 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
   for (int mi = 0; mi < QM; ++mi)
 #pragma unroll
     for (int ni = 0; ni < QN; ++ni) cacc[mi][ni] = zero4();
-  float sk[TR::NDG][8], sv[TR::NDG][8];
+  float sk[8], sv[8];
 #pragma unroll
-  for (int i = 0; i < TR::NDG; ++i)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) sk[i][e] = sv[i][e] = 0.f;
-  const int p2 = 2 * (tid & 31);
+  for (int e = 0; e < 8; ++e) sk[e] = sv[e] = 0.f;
   auto is_cand = [&](int j) { return j >= c_lo && j < c_hi; };
 
   const int t_beg = sl * a.tps1, t_end = min(t_beg + a.tps1, a.ntile);
   // Two tiles in flight: tile t is staged in R[t & 1], and the load of tile t + 2 is issued
-  // into the same registers as soon as tile t has been written to LDS.
+  // into the same registers as soon as tile t has been written to LDS.  Every step issues
+  // its loads whether or not the tile exists (rows clamped to the slice's last row) and
+  // the loop always runs both steps, so the count of loads in flight is the same on every
+  // path and the compiler waits for exactly the tile being used.
+  const int slice_rows = min(t_end * TILE, a.N);
   auto issue = [&](TR& R, int t) {
-    const int j = t * TILE + p2;
-    tile_load<T, D, NT>(R, Kh, Vh, t * TILE, j < a.N, j + 1 < a.N, is_cand(j), is_cand(j + 1), tid);
+    tile_load<T, D, NT>(R, Kh, Vh, t * TILE, slice_rows, tid);
   };
   auto step = [&](TR& R, int t) {
     const int tok0 = t * TILE;
     const bool tile_has_cand = tok0 < c_hi && tok0 + TILE > c_lo;
-    {
-      const int j = tok0 + p2;
+    const bool live = t < t_end;  // uniform; a step past the slice only issues loads
+    R.arrive();
+    if (live) {
       if (TR::active(tid)) {
 #pragma unroll
-        for (int i = 0; i < TR::NDG; ++i) {
-          store_frag(&sK[p2][8 * TR::group(tid, i)], R.k[i][0]);
-          store_frag(&sK[p2 + 1][8 * TR::group(tid, i)], R.k[i][1]);
+        for (int i = 0; i < TR::NP; ++i) {
+          const int p = TR::pair(tid, i);  // rows past N: their logits are masked
+          store_frag(&sK[2 * p][8 * TR::group(tid)], R.k[i][0]);
+          store_frag(&sK[2 * p + 1][8 * TR::group(tid)], R.k[i][1]);
         }
       }
-      float ss0, ss1;
-      tile_store_t<T, D, NT, LDT>(R, sKT, sVT, is_cand(j), is_cand(j + 1), sk, sv, ss0, ss1, tid);
-      ss0 += __shfl_xor(ss0, 32);
-      ss1 += __shfl_xor(ss1, 32);
-      if (lane < 32) {
-        sVn[wave][p2] = ss0;
-        sVn[wave][p2 + 1] = ss1;
-      }
-      if (t + 2 < t_end) issue(R, t + 2);
-    }
-    __syncthreads();
-    if (tid < TILE && is_cand(tok0 + tid)) {
-      float ss = 0.f;
+      float ss[TR::NP][2];
+      tile_store_t<T, D, NT, LDT>(R, sKT, sVT, tok0, is_cand, sk, sv, ss, tid);
+      // ||v_j||: the GROUPS lanes holding token j's columns are adjacent.  No global
+      // store inside the tile loop: a store among the loads in flight would make the
+      // compiler wait for all of them; the norms wait in LDS.
 #pragma unroll
-      for (int w = 0; w < NW; ++w) ss += sVn[w][tid];
-      a.vnorm[(size_t)head * a.n_c + (tok0 + tid - c_lo)] = sqrtf(ss);
+      for (int i = 0; i < TR::NP; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float x = row_group_sum<TR::GROUPS>(ss[i][h]);
+          if (TR::active(tid) && TR::group(tid) == 0)
+            sVnorm[(t - t_beg) * TILE + 2 * TR::pair(tid, i) + h] = sqrtf(x);
+        }
     }
+    issue(R, t + 2);
+    if (!live) return;
+    __syncthreads();
 
     // window logits for this wave's row tiles; per-lane online (max, sum), updated once
     // per row and tile.  Only tiles reaching past position N-w need the causal/tail mask.
@@ -420,11 +465,18 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
     __syncthreads();
   };
   TR R0, R1;
-  if (t_beg < t_end) issue(R0, t_beg);
-  if (t_beg + 1 < t_end) issue(R1, t_beg + 1);
+  issue(R0, t_beg);
+  __builtin_amdgcn_sched_barrier(0);  // keep the issue order: tile t_beg's loads first
+  issue(R1, t_beg + 1);
   for (int t = t_beg; t < t_end; t += 2) {
     step(R0, t);
-    if (t + 1 < t_end) step(R1, t + 1);
+    step(R1, t + 1);
+  }
+
+  // ||v_j|| of the slice's candidates (the loop ended on a barrier)
+  for (int x = tid; x < (t_end - t_beg) * TILE; x += NT) {
+    const int j = t_beg * TILE + x;
+    if (is_cand(j)) a.vnorm[(size_t)head * a.n_c + (j - c_lo)] = sVnorm[x];
   }
 
   // merge the per-lane row statistics over the 16 lanes holding a row
@@ -445,7 +497,7 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         rp[1] = l;
       }
     }
-  write_cov_partials<T, D, NT>(a, head, sl, cacc, sv, sk, 1.f, tid);
+  write_cov_partials<T, D, NT>(a, head, sl, cacc, sv, sk, 1.f, reinterpret_cast<float*>(&sVT[0][0]), tid);
 }
 
 // ------------------------------------------------------------------------------------
@@ -492,7 +544,7 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
   constexpr int CPT = TILE * DG / 256;
   __shared__ __align__(16) T sK[TILE][LDK];
   __shared__ float sA[4][TILE];
-  __shared__ float sAj[TILE];
+  __shared__ float sAj[kMassMaxTiles * TILE];  // a_j of the slice's tiles
   __shared__ float sRow[512][2];
   __shared__ uint32_t sHist[TK_HBINS];  // keys of the first selection's scores
   __shared__ uint32_t sHistA[TK_HBINS]; // keys of abar (head-adaptive layer-wide selection)
@@ -505,42 +557,46 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
   const float c2 = a.scale * kLog2e;
   const float inv_rows = 1.f / (float)a.R;
 
+  // tiles of this slice that hold candidates (a contiguous range); the next tile's rows
+  // are loaded into registers while the current one is consumed.  Every load is issued
+  // unconditionally (rows clamped to the last candidate of the slice: rows outside the
+  // candidates are never stored) and no global access sits between a prefetch and its
+  // use, so the compiler waits for exactly the tile being used; a_j stays in LDS and the
+  // pooling, scores and histograms follow the loop.
+  const int t_beg = max(sl * a.tps2, c_lo / TILE);
+  const int t_end = min(min(sl * a.tps2 + a.tps2, a.ntile), (c_hi + TILE - 1) / TILE);
+  const int last_row = max(min(t_end * TILE, c_hi) - 1, 0);
+  const int dg = tid % DG;
+  typename Frag<T>::type pk[CPT];
+  auto load_tile = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int j = min(t * TILE + (tid + 256 * i) / DG, last_row);
+      pk[i] = load_frag(Kh + (size_t)j * D + 8 * dg);
+    }
+  };
+  load_tile(t_beg);  // in flight while the row statistics and queries arrive
+
   for (int r = tid; r < a.R; r += 256) {
     sRow[r][0] = a.rowstat[((size_t)head * a.R + r) * 2 + 0];
     sRow[r][1] = a.rowstat[((size_t)head * a.R + r) * 2 + 1];
   }
   for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = sHistA[b] = 0u;
+  // query rows past R repeat row R-1 (their sums are never used)
   typename Frag<T>::type qf[MTW][KS];
 #pragma unroll
   for (int k = 0; k < MTW; ++k) {
     const int mt = wave + 4 * k;
-    const int r = 16 * mt + (lane & 15);
+    const T* qrow = window_row<T>(a, head, min(16 * mt + (lane & 15), a.R - 1));
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[k][ks] = (mt < RT && r < a.R) ? load_frag(window_row<T>(a, head, r) + 32 * ks + 8 * (lane >> 4))
-                                       : zero_frag<T>();
+    for (int ks = 0; ks < KS; ++ks) qf[k][ks] = load_frag(qrow + 32 * ks + 8 * (lane >> 4));
   }
-  const int dg = tid % DG;
   __syncthreads();
 
-  // tiles of this slice that hold candidates (a contiguous range); the next tile's rows
-  // are loaded into registers while the current one is consumed
-  const int t_beg = max(sl * a.tps2, c_lo / TILE);
-  const int t_end = min(min(sl * a.tps2 + a.tps2, a.ntile), (c_hi + TILE - 1) / TILE);
-  typename Frag<T>::type pk[CPT];
-  auto load_tile = [&](int t) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int j = t * TILE + (tid + 256 * i) / DG;
-      pk[i] = (j >= c_lo && j < c_hi) ? load_frag(Kh + (size_t)j * D + 8 * dg) : zero_frag<T>();
-    }
-  };
-  if (t_beg < t_end) load_tile(t_beg);
   for (int t = t_beg; t < t_end; ++t) {
-    const int tok0 = t * TILE;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) store_frag(&sK[(tid + 256 * i) / DG][8 * dg], pk[i]);
-    if (t + 1 < t_end) load_tile(t + 1);
+    load_tile(t + 1);  // past the slice: its last row again
     __syncthreads();
     float col[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -571,26 +627,29 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
       if (lane < 16) sA[wave][16 * nt + lane] = x;
     }
     __syncthreads();
-    if (tid < TILE) sAj[tid] = (((sA[0][tid] + sA[1][tid]) + sA[2][tid]) + sA[3][tid]) * inv_rows;
-    __syncthreads();
-    if (tid < TILE) {
-      const int j = tok0 + tid;
-      if (j >= c_lo && j < c_hi) {
-        const int cs = (j / a.chunk) * a.chunk;
-        const int lo = max(cs, c_lo), hi = min(cs + a.chunk, c_hi);
-        float s = 0.f;
-        for (int i = lo; i < hi; ++i) s += sAj[i - tok0];
-        const float ab = s / (float)(hi - lo);
-        const size_t o = (size_t)head * a.n_c + (j - c_lo);
-        const float s0 = ab * a.vnorm[o];
-        a.abar[o] = ab;
-        a.score0[o] = s0;
-        atomicAdd(&sHist[score_key(a.mi_rounds < 0 ? ab : s0) >> 20], 1u);
-        if (a.adaptive) atomicAdd(&sHistA[score_key(ab) >> 20], 1u);
-      }
-    }
-    __syncthreads();
+    if (tid < TILE)
+      sAj[(t - t_beg) * TILE + tid] = (((sA[0][tid] + sA[1][tid]) + sA[2][tid]) + sA[3][tid]) * inv_rows;
   }
+  __syncthreads();
+  // chunk pooling (chunks are aligned and divide the tile), provisional scores, histograms
+  const int tok_beg = t_beg * TILE;
+  for (int x = tid; x < (t_end - t_beg) * TILE; x += 256) {
+    const int j = tok_beg + x;
+    if (j >= c_lo && j < c_hi) {
+      const int cs = (j / a.chunk) * a.chunk;
+      const int lo = max(cs, c_lo), hi = min(cs + a.chunk, c_hi);
+      float s = 0.f;
+      for (int i = lo; i < hi; ++i) s += sAj[i - tok_beg];
+      const float ab = s / (float)(hi - lo);
+      const size_t o = (size_t)head * a.n_c + (j - c_lo);
+      const float s0 = ab * a.vnorm[o];
+      a.abar[o] = ab;
+      a.score0[o] = s0;
+      atomicAdd(&sHist[score_key(a.mi_rounds < 0 ? ab : s0) >> 20], 1u);
+      if (a.adaptive) atomicAdd(&sHistA[score_key(ab) >> 20], 1u);
+    }
+  }
+  __syncthreads();
   hist_flush<256>(sHist, a.tk_hh + (size_t)head * TK_HBINS);
   if (a.adaptive) hist_flush<256>(sHistA, a.tk_hs + (size_t)(head / a.Hkv) * TK_HBINS);
 }
@@ -900,32 +959,25 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kb
   for (int mi = 0; mi < QM; ++mi)
 #pragma unroll
     for (int ni = 0; ni < QN; ++ni) cacc[mi][ni] = zero4();
-  float sk[TR::NDG][8], sv[TR::NDG][8];
+  float sk[8], sv[8];
 #pragma unroll
-  for (int i = 0; i < TR::NDG; ++i)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) sk[i][e] = sv[i][e] = 0.f;
-  const int p2 = 2 * (tid & 31);
+  for (int e = 0; e < 8; ++e) sk[e] = sv[e] = 0.f;
+  auto in_rows = [&](int j) { return j < nrows; };
   const int ntiles = (nrows + TILE - 1) / TILE;
   const int t_beg = sl * a.tpsr, t_end = min(t_beg + a.tpsr, ntiles);
   TR R;
-  if (t_beg < t_end) {
-    const int j = t_beg * TILE + p2;
-    tile_load<T, D, NT>(R, Kh, Vh, t_beg * TILE, j < nrows, j + 1 < nrows, j < nrows, j + 1 < nrows, tid);
-  }
+  if (t_beg < t_end) tile_load<T, D, NT>(R, Kh, Vh, t_beg * TILE, nrows, tid);
   for (int t = t_beg; t < t_end; ++t) {
-    const int j = t * TILE + p2;
-    float ss0, ss1;
-    tile_store_t<T, D, NT, LDT>(R, sKT, sVT, true, true, sk, sv, ss0, ss1, tid);
-    if (t + 1 < t_end) {
-      const int jn = j + TILE;
-      tile_load<T, D, NT>(R, Kh, Vh, (t + 1) * TILE, jn < nrows, jn + 1 < nrows, jn < nrows, jn + 1 < nrows, tid);
-    }
+    float ss[TR::NP][2];
+    R.arrive();
+    tile_store_t<T, D, NT, LDT>(R, sKT, sVT, t * TILE, in_rows, sk, sv, ss, tid);
+    if (t + 1 < t_end) tile_load<T, D, NT>(R, Kh, Vh, (t + 1) * TILE, nrows, tid);
     __syncthreads();
     cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
   }
-  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, -1.f, tid);
+  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, -1.f,
+                              reinterpret_cast<float*>(&sVT[0][0]), tid);
 }
 
 // ------------------------------------------------------------------------------------
@@ -984,7 +1036,7 @@ __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, fl
 // the four partials are added in wave order.
 // ------------------------------------------------------------------------------------
 template <class T, int D>
-__global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
+__global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) k_residual(CompressArgs a) {
   constexpr int KS = D / 32, DG = D / 8, PAD = 16 / (int)sizeof(T);
   constexpr int LDK = D + PAD;
   constexpr int CPT = TILE * DG / 256;
@@ -995,6 +1047,7 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
   __shared__ __align__(16) T sK[TILE][LDK];
   __shared__ __align__(16) T sV[TILE][LDK];
   __shared__ float sRho[4][TILE];
+  __shared__ float sRes[kResMaxTiles * TILE];  // squared residual norms of the slice
   __shared__ float sSv[D], sSk[D];
   __shared__ uint32_t sHist[TK_HBINS];  // keys of the final selection's scores
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1007,6 +1060,26 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
   const T* Kh = reinterpret_cast<const T*>(a.k) + (size_t)head * a.N * D;
   const T* Vh = reinterpret_cast<const T*>(a.v) + (size_t)head * a.N * D;
 
+  // Candidate tiles of this slice; the next tile's rows are loaded into registers while
+  // the current one is consumed.  Every load is issued unconditionally (rows clamped to
+  // the slice's last candidate: rows past it are never stored) and no global access sits
+  // between a prefetch and its use, so the compiler waits for exactly the tile being
+  // used; the norms stay in LDS and the scores and histogram follow the loop.
+  const int n_tiles = (a.n_c + TILE - 1) / TILE;
+  const int t_beg = sl * a.tps3, t_end = min(t_beg + a.tps3, n_tiles);
+  const int last_row = max(min(c_lo + t_end * TILE, c_hi) - 1, 0);
+  const int dg = tid % DG;
+  FragT pk[CPT], pv[CPT];
+  auto load_tile = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int j = min(c_lo + t * TILE + (tid + 256 * i) / DG, last_row);
+      pk[i] = load_frag(Kh + (size_t)j * D + 8 * dg);
+      pv[i] = load_frag(Vh + (size_t)j * D + 8 * dg);
+    }
+  };
+  load_tile(t_beg);  // in flight while the summary is formed
+
   for (int t = tid; t < D; t += 256) {
     sSv[t] = a.sv0[(size_t)head * D + t];
     sSk[t] = a.sk0[(size_t)head * D + t];
@@ -1015,6 +1088,13 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
   // A fragments: row 16*(MTPW*wave + m) + lane%16, columns 32*ks + 8*(lane/16) + e
   FragT af[MTPW][KS][NPL];
   const float* S0 = a.s0 + (size_t)head * D * D;
+  f32x8 raw[MTPW][KS];  // every read issued before the first is used (one round trip)
+#pragma unroll
+  for (int m = 0; m < MTPW; ++m)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      raw[m][ks] = load_frag(S0 + (size_t)(16 * (MTPW * wave + m) + (lane & 15)) * D + 32 * ks +
+                             8 * (lane >> 4));
 #pragma unroll
   for (int m = 0; m < MTPW; ++m) {
     const int row = 16 * (MTPW * wave + m) + (lane & 15);
@@ -1022,11 +1102,10 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int col = 32 * ks + 8 * (lane >> 4);
-      const f32x8 raw = load_frag(S0 + (size_t)row * D + col);
       float st[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        st[e] = raw[e] - sv * sSk[col + e] * inv_n;
+        st[e] = raw[m][ks][e] - sv * sSk[col + e] * inv_n;
         if (fabsf(st[e]) < a.tau) st[e] = 0.f;
       }
       if constexpr (BF) {
@@ -1054,29 +1133,14 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) vb[m][i] = sSv[16 * (MTPW * wave + m) + 4 * (lane >> 4) + i] * inv_n;
 
-  const int n_tiles = (a.n_c + TILE - 1) / TILE;
-  const int t_beg = sl * a.tps3, t_end = min(t_beg + a.tps3, n_tiles);
-  const int dg = tid % DG;
-  FragT pk[CPT], pv[CPT];
-  auto load_tile = [&](int t) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int j = c_lo + t * TILE + (tid + 256 * i) / DG;
-      const bool ok = j < c_hi;
-      pk[i] = ok ? load_frag(Kh + (size_t)j * D + 8 * dg) : zero_frag<T>();
-      pv[i] = ok ? load_frag(Vh + (size_t)j * D + 8 * dg) : zero_frag<T>();
-    }
-  };
-  if (t_beg < t_end) load_tile(t_beg);
   for (int t = t_beg; t < t_end; ++t) {
-    const int tok0 = c_lo + t * TILE;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int tt = (tid + 256 * i) / DG;
       store_frag(&sK[tt][8 * dg], pk[i]);
       store_frag(&sV[tt][8 * dg], pv[i]);
     }
-    if (t + 1 < t_end) load_tile(t + 1);
+    load_tile(t + 1);  // past the slice: its last row again
     __syncthreads();
     FragT bfr[4][KS];
 #pragma unroll
@@ -1114,18 +1178,20 @@ __global__ void __launch_bounds__(256) k_residual(CompressArgs a) {
       if (lane < 16) sRho[wave][16 * nt + lane] = x;
     }
     __syncthreads();
-    if (tid < TILE) {
-      const int j = tok0 + tid;
-      if (j < c_hi) {
-        const float x = ((sRho[0][tid] + sRho[1][tid]) + sRho[2][tid]) + sRho[3][tid];
-        const size_t o = (size_t)head * a.n_c + (j - c_lo);
-        const float sc = a.abar[o] * sqrtf(x);
-        a.score[o] = sc;
-        atomicAdd(&sHist[score_key(sc) >> 20], 1u);
-      }
-    }
-    __syncthreads();
+    if (tid < TILE)
+      sRes[(t - t_beg) * TILE + tid] = ((sRho[0][tid] + sRho[1][tid]) + sRho[2][tid]) + sRho[3][tid];
   }
+  __syncthreads();
+  for (int x = tid; x < (t_end - t_beg) * TILE; x += 256) {
+    const int j = c_lo + t_beg * TILE + x;
+    if (j < c_hi) {
+      const size_t o = (size_t)head * a.n_c + (j - c_lo);
+      const float sc = a.abar[o] * sqrtf(sRes[x]);
+      a.score[o] = sc;
+      atomicAdd(&sHist[score_key(sc) >> 20], 1u);
+    }
+  }
+  __syncthreads();
   hist_flush<256>(sHist, a.tk_hh + ((size_t)a.H + head) * TK_HBINS);
 }
 

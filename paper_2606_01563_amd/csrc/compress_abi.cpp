@@ -78,13 +78,13 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.tau = p->tau;
   a.ntile = ceil_div(a.N, 64);
   // window-row / covariance pass: about one workgroup per CU (it runs one per CU),
-  // whole 64-token tiles each
+  // whole 64-token tiles each, at most kRowsMaxTiles
   a.nsl1 = clampi(ceil_div(256, a.H), 1, a.ntile);
-  a.tps1 = ceil_div(a.ntile, a.nsl1);
+  a.tps1 = std::min(ceil_div(a.ntile, a.nsl1), mkv::kRowsMaxTiles);
   a.nsl1 = ceil_div(a.ntile, a.tps1);
   // window-mass pass: about 1024 workgroups of 256 threads
   a.nsl2 = clampi(ceil_div(1024, a.H), 1, a.ntile);
-  a.tps2 = ceil_div(a.ntile, a.nsl2);
+  a.tps2 = std::min(ceil_div(a.ntile, a.nsl2), mkv::kMassMaxTiles);
   a.nsl2 = ceil_div(a.ntile, a.tps2);
   // downdate covariance over the kept rows
   if (a.k_keep > 0) {
@@ -101,7 +101,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   {
     const int nu = ceil_div(a.n_c > 0 ? a.n_c : 1, 64);
     a.nsl3 = clampi(ceil_div(512, a.H), 1, nu);
-    a.tps3 = ceil_div(nu, a.nsl3);
+    a.tps3 = std::min(ceil_div(nu, a.nsl3), mkv::kResMaxTiles);
     a.nsl3 = ceil_div(nu, a.tps3);
   }
   // top-k slices of 2048 candidates (at most 128 for kMaxCandidates)

@@ -147,9 +147,11 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
   __shared__ __align__(16) T s_q[16 * QRS];
 
   const int head = blockIdx.x / e.nslice, slice = blockIdx.x % e.nslice;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the wave index and the length are the same for all lanes; held in scalar registers,
+  // they make the block loop below uniform control flow rather than a per-lane loop
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q4 = lane >> 4, r16 = lane & 15;
-  const int old_len = e.lens[head];
+  const int old_len = __builtin_amdgcn_readfirstlane(e.lens[head]);
   const bool can_append = old_len >= 0 && old_len < e.cap;
   // the workgroup whose rows hold the new one appends it (the last one for rows past them)
   if (can_append && wave == 0 && min(old_len / e.slice_len, e.nslice - 1) == slice)
@@ -163,28 +165,30 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
   const T* vc = reinterpret_cast<const T*>(e.v_cache) + (size_t)head * e.cap * D;
   const T* kn = reinterpret_cast<const T*>(e.k_new) + (size_t)head * D;
   const T* vn = reinterpret_cast<const T*>(e.v_new) + (size_t)head * D;
-  const int ML = e.max_len;
-  float* rec = e.rec + (size_t)head * (G + 1) * ML;
+  const int ML = e.rec_len;  // rows of the record planes (whole 32-row blocks)
+  float* rec = e.rec + (size_t)head * (G + 2) * ML;
   const float c2 = e.scale * kLog2e;
 
-  // rows j0 + 16 hh + lane % 16: K and V fragments at dims 32 ks + 8 (lane / 16)
+  // rows j0 + 16 hh + lane % 16: K and V fragments at dims 32 ks + 8 (lane / 16).  Rows
+  // past t1 read row t1 - 1 again (their records land in the padding of the record rows
+  // or are never written): every lane issues every load, so the compiler can count the
+  // loads in flight and waits for one block while the next is still arriving.
   auto load = [&](FragT (&kf)[2][KS], FragT (&vf)[2][KS], int j0) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const int j = j0 + 16 * hh + r16;
-      const bool ok = j < t1;
+      const int j = min(j0 + 16 * hh + r16, t1 - 1);
       const T* kr = j == old_len ? kn : kc + (size_t)j * D;
       const T* vr = j == old_len ? vn : vc + (size_t)j * D;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        kf[hh][ks] = ok ? load_frag(kr + 32 * ks + 8 * q4) : zero_frag<T>();
-        vf[hh][ks] = ok ? load_frag(vr + 32 * ks + 8 * q4) : zero_frag<T>();
+        kf[hh][ks] = load_frag(kr + 32 * ks + 8 * q4);
+        vf[hh][ks] = load_frag(vr + 32 * ks + 8 * q4);
       }
     }
   };
   FragT ka[2][KS], va[2][KS], kb[2][KS], vb[2][KS];
   int j0 = t0 + kEvTB * wave;
-  if (j0 < t1) load(ka, va, j0);  // in flight while the summary is formed
+  load(ka, va, j0);  // in flight while the summary is formed
 
   // the G queries (rows past G zero) go to LDS as the A fragments of the logits, and
   // v_bar = s_v / n_e next to them; their reads are issued before the summary's
@@ -218,13 +222,13 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
       f32x4 lg = zero4();
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) mma(lg, lds_frag(&s_q[r16 * QRS + 32 * ks + 8 * q4]), kf[hh][ks]);
+      // every lane stores (no per-lane branch around a store): rows past t1 land in the
+      // padding of the record planes, padded query slots in plane G + 1
       const int j = j0 + 16 * hh + r16;
-      if (j < t1) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int g = 4 * q4 + i;
-          if (g < G) rec[(size_t)g * ML + j] = lg[i] * c2;
-        }
+      for (int i = 0; i < 4; ++i) {
+        const int g = 4 * q4 + i;
+        rec[(size_t)(g < G ? g : G + 1) * ML + j] = lg[i] * c2;
       }
     }
     // S_tilde k: tile t = 2c + s holds dims 32c + 8 (lane/16) + 4s + i in lane rows
@@ -267,7 +271,7 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
     for (int hh = 0; hh < 2; ++hh) {
       rr[hh] = cross_row_sum(rr[hh]);
       const int j = j0 + 16 * hh + r16;
-      if (j < t1 && q4 == 0) rec[(size_t)G * ML + j] = 0.5f * log2f(rr[hh]);
+      rec[(size_t)G * ML + j] = 0.5f * log2f(rr[hh]);  // the same value from four lanes
     }
   };
   __syncthreads();  // S_tilde and v_bar are in LDS
@@ -275,10 +279,10 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
   // 32-row blocks j0, j0 + 128, ... of this wave; the next block's rows are requested
   // before the current block is processed (two register sets)
   for (; j0 < t1; j0 += 8 * kEvTB) {
-    if (j0 + 4 * kEvTB < t1) load(kb, vb, j0 + 4 * kEvTB);
+    load(kb, vb, j0 + 4 * kEvTB);
     process(ka, va, j0);
     if (j0 + 4 * kEvTB >= t1) break;
-    if (j0 + 8 * kEvTB < t1) load(ka, va, j0 + 8 * kEvTB);
+    load(ka, va, j0 + 8 * kEvTB);
     process(kb, vb, j0 + 4 * kEvTB);
   }
 }
@@ -317,8 +321,8 @@ __global__ void __launch_bounds__(kSelThreads) k_evict_select(EvictArgs e) {
     return;
   }
   const int n_tok = old_len + 1, last = n_tok - 1;
-  const int G = e.G, ML = e.max_len;
-  const float* rec = e.rec + (size_t)head * (G + 1) * ML;
+  const int G = e.G, ML = e.rec_len;
+  const float* rec = e.rec + (size_t)head * (G + 2) * ML;
   T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
   T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
   float4* Sh = reinterpret_cast<float4*>(e.S + (size_t)head * D * D);

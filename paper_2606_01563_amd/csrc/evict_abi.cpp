@@ -40,7 +40,8 @@ mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws
   Carver c;
   c.base = static_cast<char*>(ws);
   c.off = dec;
-  e.rec = c.take<float>((size_t)e.n_heads * (e.G + 1) * p->max_len * sizeof(float));
+  e.rec_len = ceil_div(p->max_len, 32) * 32;
+  e.rec = c.take<float>((size_t)e.n_heads * (e.G + 2) * e.rec_len * sizeof(float));
   *total = c.off;
   return e;
 }

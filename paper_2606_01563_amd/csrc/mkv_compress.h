@@ -7,6 +7,12 @@
 
 namespace mkv {
 
+// Most 64-token tiles one workgroup of the window-row/covariance, window-mass and
+// residual passes takes: its per-token results wait in LDS until its tile loop ends.
+constexpr int kRowsMaxTiles = 64;
+constexpr int kMassMaxTiles = 8;
+constexpr int kResMaxTiles = 32;
+
 struct CompressArgs {
   const void* q_win;        // [B, Hq, w, D]
   const void* k;            // [B, Hkv, N, D]
@@ -48,10 +54,11 @@ struct CompressArgs {
   int kmax;                 // row capacity of kept/gath buffers (>= k_keep, >= 1)
   int ntile;                // ceil(N / 64)
   int nsl1, tps1;           // window-row/covariance pass: slices, tiles per slice
-  int nsl2, tps2;           // window-mass pass: slices, tiles per slice
+                            // (tps1 <= kRowsMaxTiles)
+  int nsl2, tps2;           // window-mass pass: slices, tiles per slice (<= kMassMaxTiles)
   int nslr, tpsr;           // downdate covariance pass over k_keep rows
   int nslot;                // nsl1 + nslr
-  int nsl3, tps3;           // residual pass: slices over candidate tiles of 64
+  int nsl3, tps3;           // residual pass: slices over candidate tiles of 64 (<= kResMaxTiles)
   int ntk;                  // top-k slices of 2048 candidates
   // head-adaptive budgets (adaptive = 1): a per-sequence selection over the layer
   int adaptive;

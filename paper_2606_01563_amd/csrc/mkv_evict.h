@@ -20,11 +20,13 @@ struct EvictArgs {
   float* s_v;
   float* S;                 // [B, Hkv, D, D]
   int32_t* evicted;         // [B, Hkv] or null: slot evicted by this call, -1 if none
-  float* rec;               // [B*Hkv, G + 1, max_len]  per row: G base-2 logits, log2 ||r||
+  float* rec;               // [B*Hkv, G + 2, rec_len]  per row: G base-2 logits, log2 ||r||,
+                            // then a row that takes the logits of padded query slots
   int32_t* flag;            // sticky flag: 1 no room for the new row, 2 lens past max_len,
                             // 4 no finite score, 8 lens above budget before the append
   int n_heads, G, cap, max_len, budget;
   int nslice, slice_len;    // scoring workgroups per KV head, rows per workgroup (x 32)
+  int rec_len;              // max_len rounded up to 32: whole blocks of records fit
   float scale, tau;
 };
 
