@@ -211,6 +211,34 @@ def test_compress_and_decode_are_bit_deterministic():
     assert torch.equal(outs[0], outs[1])
 
 
+@pytest.mark.parametrize("ctx_len", [12000, 33000])
+@pytest.mark.parametrize("mi_rounds", [-1, 0])
+def test_selection_with_all_scores_equal_keeps_the_lowest_positions(ctx_len, mi_rounds):
+    """Every candidate score equal (identical candidate keys give equal window masses;
+    zero values give zero scores): the kept set is the k lowest candidate positions, the
+    tie rule of the selection.  Both sizes put more keys in the k-th key's bin than the
+    refinement stages in LDS (it then reads them from global memory), over 6 and 17
+    slices of 2048 positions."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, ctx_len=ctx_len, budgets=(200,))
+    n_s, budget = 4, 200  # candidates start and end on chunk boundaries: no short chunk
+    c_hi = ctx_len - wl.window
+    k = cpu["k"].clone()
+    k[0, 0, n_s:c_hi] = k[0, 0, 5]
+    v = cpu["v"].clone()
+    if mi_rounds == 0:
+        v[0, 0, n_s:c_hi] = 0.0  # ||v_j|| = 0: every provisional score is 0
+    gpu["k"], gpu["v"] = k.cuda(), v.cuda()
+    out = P.run_compress(gpu, budget, cap=budget, mi_rounds=mi_rounds, n_sink=n_s)
+    k_keep = budget - n_s - wl.window
+    first = (out.abar if mi_rounds < 0 else out.score0)[0, 0].cpu().numpy()
+    assert np.all(first == first[0])
+    expect = np.arange(n_s, n_s + k_keep)
+    idx = out.idx[0, 0].cpu().numpy()
+    np.testing.assert_array_equal(idx[n_s:n_s + k_keep], expect)
+    np.testing.assert_array_equal(out.kept0[0, 0, :k_keep].cpu().numpy(), expect)
+    assert int(out.n_e[0, 0]) == c_hi - n_s - k_keep
+
+
 def test_zero_key_spread_decode_equals_full_attention_on_gpu():
     """Paper invariant end to end: with every candidate key equal, the corrected decode
     output equals full attention over all N tokens (Sec. 4.2, App. B.2)."""
