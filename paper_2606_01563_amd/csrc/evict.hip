@@ -44,6 +44,16 @@ template <int D> struct SumLds<float, D> {
   float st[D * RS];
 };
 
+// bf16 S_tilde rows: 16-byte chunks XOR-swizzled by bit 4 of the row.  The 16 rows one
+// MFMA read touches (r + {0..3, 8..11, 16..19, 24..27}) would otherwise fall pairwise
+// into the same bank group (rows 16 apart); swizzled, each 16-lane pass of the read
+// covers 16 different groups.
+template <class T>
+__device__ __forceinline__ int scol(int row, int col) {
+  if constexpr (sizeof(T) == 2) return col ^ (((row >> 4) & 1) << 5);
+  else return col;
+}
+
 __device__ __forceinline__ bf16x8 lds_frag(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 }
@@ -101,8 +111,8 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumL
         h[x / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
         l[x / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
       }
-      *reinterpret_cast<uint4*>(&sm.hi[row * RS + c0]) = make_uint4(h[0], h[1], h[2], h[3]);
-      *reinterpret_cast<uint4*>(&sm.lo[row * RS + c0]) = make_uint4(l[0], l[1], l[2], l[3]);
+      *reinterpret_cast<uint4*>(&sm.hi[row * RS + scol<T>(row, c0)]) = make_uint4(h[0], h[1], h[2], h[3]);
+      *reinterpret_cast<uint4*>(&sm.lo[row * RS + scol<T>(row, c0)]) = make_uint4(l[0], l[1], l[2], l[3]);
     } else {
       float4* P = reinterpret_cast<float4*>(&sm.st[row * RS + c0]);
       P[0] = make_float4(st[0], st[1], st[2], st[3]);
@@ -242,8 +252,9 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         if constexpr (sizeof(T) == 2) {
-          const bf16x8 ah = lds_frag(&sm.hi[row * RS + 32 * ks + 8 * q4]);
-          const bf16x8 al = lds_frag(&sm.lo[row * RS + 32 * ks + 8 * q4]);
+          const int col = scol<T>(row, 32 * ks + 8 * q4);
+          const bf16x8 ah = lds_frag(&sm.hi[row * RS + col]);
+          const bf16x8 al = lds_frag(&sm.lo[row * RS + col]);
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
             mma(ta[hh], ah, kf[hh][ks]);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cstdint>
 #include <cstring>
 
@@ -18,8 +19,9 @@ namespace {
 
 // ------------------------------------------------------------------ decode + eviction
 // Workspace: the decode layout (its flag first), then the per-row score records.  Scoring
-// workgroups: about two per CU over the grid, each a multiple of 32 rows and at least 256
-// rows, since each one first forms the head's S_tilde.
+// workgroups: slices of a multiple of 32 rows (at least 128), as many per head as keep
+// the busiest CU's work lowest, counting each workgroup's forming of S_tilde as 96 rows
+// (a CU's scoring throughput is shared by the workgroups it holds).
 mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws,
                             size_t* total, mkv::DecodeArgs* da) {
   size_t dec = 0;
@@ -34,8 +36,18 @@ mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws
   e.scale = da->scale;
   e.tau = da->tau;
   e.flag = da->flag;
-  const int want = clampi(ceil_div(512, e.n_heads), 1, std::max(1, p->max_len / 256));
-  e.slice_len = ceil_div(ceil_div(p->max_len, want), 32) * 32;
+  constexpr int64_t kCUs = 256, kBuildRows = 96;
+  int best = 1;
+  int64_t best_cost = INT64_MAX;
+  for (int ns = 1; ns <= std::max(1, p->max_len / 128); ++ns) {
+    const int64_t rows = (int64_t)ceil_div(ceil_div(p->max_len, ns), 32) * 32;
+    const int64_t cost = ((int64_t)e.n_heads * ns + kCUs - 1) / kCUs * (rows + kBuildRows);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = ns;
+    }
+  }
+  e.slice_len = ceil_div(ceil_div(p->max_len, best), 32) * 32;
   e.nslice = ceil_div(p->max_len, e.slice_len);
   Carver c;
   c.base = static_cast<char*>(ws);
