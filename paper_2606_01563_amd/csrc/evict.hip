@@ -145,7 +145,193 @@ __device__ __forceinline__ bool head_evicts(const EvictArgs& e, int old_len) {
 
 }  // namespace
 
-template <class T, int D>
+// Selection (one KV head, NT threads): log2 Z_g over R from the logits, the group-mean
+// softmax weight in the log domain, the argmin (lowest row on ties), then the rank-one
+// update and the move of the last row.  Everything that does not depend on the choice
+// (the summary S, the last row, the score records of up to UB rows per thread) is
+// requested before any of it is used, so a short cache costs three round trips to
+// memory: the records and S together, then the evicted row.  GM bounds the group size
+// G (4, 8 or 16); rows per thread per batch shrink as it grows.  Also handles a head that
+// does not evict this call (append only, or the flags).
+template <int GM, int NW, int D>
+struct SelLds {
+  float m[NW][GM], l[NW][GM], lz[GM];
+  float best[NW];
+  int bj[NW], pick;
+  float kv[2][D];
+};
+
+template <class T, int D, int GM, int NT>
+__device__ __forceinline__ void select_head(const EvictArgs& e, int head, int old_len,
+                                            SelLds<GM, NT / kWave, D>& sl) {
+  constexpr int NW = NT / kWave;
+  constexpr int UB = GM <= 4 ? 8 : (GM <= 8 ? 4 : 2);
+  constexpr int SPER = D * D / 4 / NT;  // float4 entries of S per thread
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool can_append = old_len >= 0 && old_len < e.cap;
+  if (!head_evicts(e, old_len)) {
+    if (tid == 0) {
+      if (!can_append) {
+        atomicOr(e.flag, 1);
+      } else {
+        if (old_len + 1 > e.max_len) atomicOr(e.flag, 2);
+        e.lens[head] = old_len + 1;
+      }
+      if (e.evicted) e.evicted[head] = -1;
+    }
+    return;
+  }
+  const int n_tok = old_len + 1, last = n_tok - 1;
+  const int G = e.G, ML = e.rec_len;
+  const float* rec = e.rec + (size_t)head * (G + 2) * ML;
+  T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
+  T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
+  float4* Sh = reinterpret_cast<float4*>(e.S + (size_t)head * D * D);
+  if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
+
+  // requests independent of the choice
+  float4 s4[SPER];
+#pragma unroll
+  for (int u = 0; u < SPER; ++u) s4[u] = Sh[tid + NT * u];
+  T kl = T(), vl = T();
+  if (tid < D) {
+    kl = kc[(size_t)last * D + tid];
+    vl = vc[(size_t)last * D + tid];
+  }
+  float x[UB][GM], y[UB];
+  auto load_batch = [&](int base) {
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int j = base + tid + NT * u;
+      const bool ok = j < n_tok;
+#pragma unroll
+      for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
+      y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
+    }
+  };
+  const int step = UB * NT;
+  const int nb = (n_tok + step - 1) / step;
+
+  // log2 Z_g over the n_tok rows
+  float m[GM], l[GM];
+#pragma unroll
+  for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
+  for (int b = 0; b < nb; ++b) {
+    load_batch(b * step);
+#pragma unroll
+    for (int u = 0; u < UB; ++u)
+#pragma unroll
+      for (int g = 0; g < GM; ++g) {
+        const float mn = fmaxf(m[g], x[u][g]);
+        if (mn != -INFINITY) {
+          l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x[u][g] - mn);
+          m[g] = mn;
+        }
+      }
+  }
+#pragma unroll
+  for (int g = 0; g < GM; ++g) {
+    if (g < G) {
+      const float M = wave_max(m[g]);
+      const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
+      if (lane == 0) { sl.m[wave][g] = M; sl.l[wave][g] = ls; }
+    }
+  }
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sl.m[w][tid]);
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      if (sl.m[w][tid] != -INFINITY) L += sl.l[w][tid] * fast_exp2(sl.m[w][tid] - M);
+    sl.lz[tid] = M + log2f(L);
+  }
+  __syncthreads();
+
+  // argmin over rows of log2(mean_g alpha_gj) + log2 ||r_j||, lowest row on ties
+  float lz[GM];
+#pragma unroll
+  for (int g = 0; g < GM; ++g) lz[g] = g < G ? sl.lz[g] : 0.f;
+  const float log2_g = log2f((float)G);
+  float best = INFINITY;
+  int bj = INT_MAX;
+  for (int b = 0; b < nb; ++b) {
+    if (nb > 1) load_batch(b * step);  // one batch: still in registers
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int j = b * step + tid + NT * u;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < GM; ++g) mx = fmaxf(mx, g < G ? x[u][g] - lz[g] : -INFINITY);
+      float sm = 0.f;
+#pragma unroll
+      for (int g = 0; g < GM; ++g)
+        if (g < G) sm += fast_exp2(x[u][g] - lz[g] - mx);
+      const float sc = mx + log2f(sm) - log2_g + y[u];
+      if (j < n_tok && sc < best) { best = sc; bj = j; }  // rows rise along a thread
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ob = __shfl_xor(best, off);
+    const int oj = __shfl_xor(bj, off);
+    if (ob < best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+  }
+  if (lane == 0) { sl.best[wave] = best; sl.bj[wave] = bj; }
+  __syncthreads();
+  if (tid == 0) {
+    float bb = sl.best[0];
+    int j = sl.bj[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w)
+      if (sl.best[w] < bb || (sl.best[w] == bb && sl.bj[w] < j)) { bb = sl.best[w]; j = sl.bj[w]; }
+    sl.pick = j;
+  }
+  __syncthreads();
+  const int js = sl.pick;
+  if (js < 0 || js >= n_tok) {  // no comparable score (non-finite inputs): keep every row
+    if (tid == 0) {
+      atomicOr(e.flag, 4);
+      e.lens[head] = n_tok;
+      if (e.evicted) e.evicted[head] = -1;
+    }
+    return;
+  }
+
+  // rank-one update and the move of the last row into slot js
+  if (tid < D) {
+    const T ks = kc[(size_t)js * D + tid], vs = vc[(size_t)js * D + tid];
+    const float kf = to_f<T>(ks), vf = to_f<T>(vs);
+    sl.kv[0][tid] = kf;
+    sl.kv[1][tid] = vf;
+    if (js != last) {
+      kc[(size_t)js * D + tid] = kl;
+      vc[(size_t)js * D + tid] = vl;
+    }
+    e.s_k[(size_t)head * D + tid] += kf;
+    e.s_v[(size_t)head * D + tid] += vf;
+  }
+  if (tid == 0) {
+    e.n_e[head] += 1;
+    e.lens[head] = last;
+    if (e.evicted) e.evicted[head] = js;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < SPER; ++u) {
+    const int idx = tid + NT * u;
+    const int row = idx / (D / 4), c = 4 * (idx % (D / 4));
+    const float va = sl.kv[1][row];
+    s4[u].x = fmaf(va, sl.kv[0][c], s4[u].x);
+    s4[u].y = fmaf(va, sl.kv[0][c + 1], s4[u].y);
+    s4[u].z = fmaf(va, sl.kv[0][c + 2], s4[u].z);
+    s4[u].w = fmaf(va, sl.kv[0][c + 3], s4[u].w);
+    Sh[idx] = s4[u];
+  }
+}
+
+template <class T, int D, int GM>
 __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_scores(EvictArgs e) {
   typedef typename Frag<T>::type FragT;
   constexpr int KS = D / 32;  // contraction steps; also 8-dim groups per lane and row
@@ -155,6 +341,7 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
   __shared__ __align__(16) float s_vbar[D];
   constexpr int QRS = D + 16 / (int)sizeof(T);  // query rows padded by 16 bytes
   __shared__ __align__(16) T s_q[16 * QRS];
+  __shared__ SelLds<GM, kEvThreads / kWave, D> sel;  // the selection, one workgroup per head
 
   const int head = blockIdx.x / e.nslice, slice = blockIdx.x % e.nslice;
   // the wave index and the length are the same for all lanes; held in scalar registers,
@@ -168,7 +355,10 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
     append_new_row<T, D>(e, head, old_len, lane);
   const int t0 = slice * e.slice_len;
   const int t1 = min(t0 + e.slice_len, old_len + 1);
-  if (!head_evicts(e, old_len) || t0 >= t1) return;  // uniform over the workgroup
+  if (!head_evicts(e, old_len) || t0 >= t1) {  // uniform over the workgroup
+    if (e.nslice == 1) select_head<T, D, GM, kEvThreads>(e, head, old_len, sel);  // lens, flags
+    return;
+  }
 
   const int G = e.G;
   const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
@@ -296,201 +486,38 @@ __global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_sc
     load(ka, va, j0 + 8 * kEvTB);
     process(kb, vb, j0 + 4 * kEvTB);
   }
+  // The head's only workgroup selects right away: its records (and the appended row) are
+  // visible to all of its waves after the barrier; no second launch.
+  if (e.nslice == 1) {
+    __syncthreads();
+    select_head<T, D, GM, kEvThreads>(e, head, old_len, sel);
+  }
 }
 
-// Selection: 512 threads per KV head (two heads fit on a CU, so a grid of a few hundred
-// heads runs in one round).  Everything that does not depend on the choice
-// (the summary S, the last row, the score records of up to kSelBatch rows per thread) is
-// requested before any of it is used, so a short cache costs three round trips to
-// memory: lens, then the records and S together, then the evicted row.
-// GM bounds the group size G (4, 8 or 16); rows per thread per batch shrink as it grows.
+// Selection as its own launch, one 512-thread workgroup per KV head (two fit on a CU, so
+// a grid of a few hundred heads runs in one round): used when the scoring ran over
+// several workgroups per head.
 constexpr int kSelThreads = 512;
 
 template <class T, int D, int GM>
 __global__ void __launch_bounds__(kSelThreads) k_evict_select(EvictArgs e) {
-  constexpr int NW = kSelThreads / kWave;
-  constexpr int UB = GM <= 4 ? 8 : (GM <= 8 ? 4 : 2);
-  constexpr int SPER = D * D / 4 / kSelThreads;  // float4 entries of S per thread
-  __shared__ float s_m[NW][GM], s_l[NW][GM], s_lz[GM];
-  __shared__ float s_best[NW];
-  __shared__ int s_bj[NW], s_pick;
-  __shared__ float s_kv[2][D];
-  const int head = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int old_len = e.lens[head];
-  const bool can_append = old_len >= 0 && old_len < e.cap;
-  if (!head_evicts(e, old_len)) {
-    if (tid == 0) {
-      if (!can_append) {
-        atomicOr(e.flag, 1);
-      } else {
-        if (old_len + 1 > e.max_len) atomicOr(e.flag, 2);
-        e.lens[head] = old_len + 1;
-      }
-      if (e.evicted) e.evicted[head] = -1;
-    }
-    return;
-  }
-  const int n_tok = old_len + 1, last = n_tok - 1;
-  const int G = e.G, ML = e.rec_len;
-  const float* rec = e.rec + (size_t)head * (G + 2) * ML;
-  T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
-  T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
-  float4* Sh = reinterpret_cast<float4*>(e.S + (size_t)head * D * D);
-  if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
+  __shared__ SelLds<GM, kSelThreads / kWave, D> sl;
+  select_head<T, D, GM, kSelThreads>(e, blockIdx.x, e.lens[blockIdx.x], sl);
+}
 
-  // requests independent of the choice
-  float4 s4[SPER];
-#pragma unroll
-  for (int u = 0; u < SPER; ++u) s4[u] = Sh[tid + kSelThreads * u];
-  T kl = T(), vl = T();
-  if (tid < D) {
-    kl = kc[(size_t)last * D + tid];
-    vl = vc[(size_t)last * D + tid];
-  }
-  float x[UB][GM], y[UB];
-  auto load_batch = [&](int base) {
-#pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int j = base + tid + kSelThreads * u;
-      const bool ok = j < n_tok;
-#pragma unroll
-      for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
-      y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
-    }
-  };
-  const int step = UB * kSelThreads;
-  const int nb = (n_tok + step - 1) / step;
-
-  // log2 Z_g over the n_tok rows
-  float m[GM], l[GM];
-#pragma unroll
-  for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
-  for (int b = 0; b < nb; ++b) {
-    load_batch(b * step);
-#pragma unroll
-    for (int u = 0; u < UB; ++u)
-#pragma unroll
-      for (int g = 0; g < GM; ++g) {
-        const float mn = fmaxf(m[g], x[u][g]);
-        if (mn != -INFINITY) {
-          l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x[u][g] - mn);
-          m[g] = mn;
-        }
-      }
-  }
-#pragma unroll
-  for (int g = 0; g < GM; ++g) {
-    if (g < G) {
-      const float M = wave_max(m[g]);
-      const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
-      if (lane == 0) { s_m[wave][g] = M; s_l[wave][g] = ls; }
-    }
-  }
-  __syncthreads();
-  if (tid < G) {
-    float M = -INFINITY, L = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_m[w][tid]);
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-      if (s_m[w][tid] != -INFINITY) L += s_l[w][tid] * fast_exp2(s_m[w][tid] - M);
-    s_lz[tid] = M + log2f(L);
-  }
-  __syncthreads();
-
-  // argmin over rows of log2(mean_g alpha_gj) + log2 ||r_j||, lowest row on ties
-  float lz[GM];
-#pragma unroll
-  for (int g = 0; g < GM; ++g) lz[g] = g < G ? s_lz[g] : 0.f;
-  const float log2_g = log2f((float)G);
-  float best = INFINITY;
-  int bj = INT_MAX;
-  for (int b = 0; b < nb; ++b) {
-    if (nb > 1) load_batch(b * step);  // one batch: still in registers
-#pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int j = b * step + tid + kSelThreads * u;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int g = 0; g < GM; ++g) mx = fmaxf(mx, g < G ? x[u][g] - lz[g] : -INFINITY);
-      float sm = 0.f;
-#pragma unroll
-      for (int g = 0; g < GM; ++g)
-        if (g < G) sm += fast_exp2(x[u][g] - lz[g] - mx);
-      const float sc = mx + log2f(sm) - log2_g + y[u];
-      if (j < n_tok && sc < best) { best = sc; bj = j; }  // rows rise along a thread
-    }
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ob = __shfl_xor(best, off);
-    const int oj = __shfl_xor(bj, off);
-    if (ob < best || (ob == best && oj < bj)) { best = ob; bj = oj; }
-  }
-  if (lane == 0) { s_best[wave] = best; s_bj[wave] = bj; }
-  __syncthreads();
-  if (tid == 0) {
-    float bb = s_best[0];
-    int j = s_bj[0];
-#pragma unroll
-    for (int w = 1; w < NW; ++w)
-      if (s_best[w] < bb || (s_best[w] == bb && s_bj[w] < j)) { bb = s_best[w]; j = s_bj[w]; }
-    s_pick = j;
-  }
-  __syncthreads();
-  const int js = s_pick;
-  if (js < 0 || js >= n_tok) {  // no comparable score (non-finite inputs): keep every row
-    if (tid == 0) {
-      atomicOr(e.flag, 4);
-      e.lens[head] = n_tok;
-      if (e.evicted) e.evicted[head] = -1;
-    }
-    return;
-  }
-
-  // rank-one update and the move of the last row into slot js
-  if (tid < D) {
-    const T ks = kc[(size_t)js * D + tid], vs = vc[(size_t)js * D + tid];
-    const float kf = to_f<T>(ks), vf = to_f<T>(vs);
-    s_kv[0][tid] = kf;
-    s_kv[1][tid] = vf;
-    if (js != last) {
-      kc[(size_t)js * D + tid] = kl;
-      vc[(size_t)js * D + tid] = vl;
-    }
-    e.s_k[(size_t)head * D + tid] += kf;
-    e.s_v[(size_t)head * D + tid] += vf;
-  }
-  if (tid == 0) {
-    e.n_e[head] += 1;
-    e.lens[head] = last;
-    if (e.evicted) e.evicted[head] = js;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int u = 0; u < SPER; ++u) {
-    const int idx = tid + kSelThreads * u;
-    const int row = idx / (D / 4), c = 4 * (idx % (D / 4));
-    const float va = s_kv[1][row];
-    s4[u].x = fmaf(va, s_kv[0][c], s4[u].x);
-    s4[u].y = fmaf(va, s_kv[0][c + 1], s4[u].y);
-    s4[u].z = fmaf(va, s_kv[0][c + 2], s4[u].z);
-    s4[u].w = fmaf(va, s_kv[0][c + 3], s4[u].w);
-    Sh[idx] = s4[u];
-  }
+template <class T, int D, int GM>
+static hipError_t launch_evict_g(const EvictArgs& e, hipStream_t st) {
+  hipLaunchKernelGGL((k_evict_scores<T, D, GM>), dim3(e.n_heads * e.nslice), dim3(kEvThreads), 0, st, e);
+  if (e.nslice > 1)
+    hipLaunchKernelGGL((k_evict_select<T, D, GM>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
+  return hipGetLastError();
 }
 
 template <class T, int D>
 static hipError_t launch_evict_t(const EvictArgs& e, hipStream_t st) {
-  hipLaunchKernelGGL((k_evict_scores<T, D>), dim3(e.n_heads * e.nslice), dim3(kEvThreads), 0, st, e);
-  if (e.G <= 4)
-    hipLaunchKernelGGL((k_evict_select<T, D, 4>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
-  else if (e.G <= 8)
-    hipLaunchKernelGGL((k_evict_select<T, D, 8>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
-  else
-    hipLaunchKernelGGL((k_evict_select<T, D, 16>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
-  return hipGetLastError();
+  if (e.G <= 4) return launch_evict_g<T, D, 4>(e, st);
+  if (e.G <= 8) return launch_evict_g<T, D, 8>(e, st);
+  return launch_evict_g<T, D, 16>(e, st);
 }
 
 hipError_t launch_evict(const EvictArgs& e, bool bf16, int d, hipStream_t st) {
