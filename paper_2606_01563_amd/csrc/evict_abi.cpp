@@ -20,8 +20,9 @@ namespace {
 // ------------------------------------------------------------------ decode + eviction
 // Workspace: the decode layout (its flag first), then the per-row score records.  Scoring
 // workgroups: slices of a multiple of 32 rows (at least 128), as many per head as keep
-// the busiest CU's work lowest, counting each workgroup's forming of S_tilde as 96 rows
-// (a CU's scoring throughput is shared by the workgroups it holds).
+// the busiest CU's work lowest (a CU's scoring throughput is shared by the workgroups it
+// holds), counting each workgroup's forming of S_tilde as 96 rows and, with more than
+// one slice per head, the separate selection launch as 384.
 mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws,
                             size_t* total, mkv::DecodeArgs* da) {
   size_t dec = 0;
@@ -36,12 +37,13 @@ mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws
   e.scale = da->scale;
   e.tau = da->tau;
   e.flag = da->flag;
-  constexpr int64_t kCUs = 256, kBuildRows = 96;
+  constexpr int64_t kCUs = 256, kBuildRows = 96, kSelectRows = 384;
   int best = 1;
   int64_t best_cost = INT64_MAX;
   for (int ns = 1; ns <= std::max(1, p->max_len / 128); ++ns) {
     const int64_t rows = (int64_t)ceil_div(ceil_div(p->max_len, ns), 32) * 32;
-    const int64_t cost = ((int64_t)e.n_heads * ns + kCUs - 1) / kCUs * (rows + kBuildRows);
+    const int64_t cost = ((int64_t)e.n_heads * ns + kCUs - 1) / kCUs * (rows + kBuildRows) +
+                         (ns > 1 ? kSelectRows : 0);
     if (cost < best_cost) {
       best_cost = cost;
       best = ns;
