@@ -27,6 +27,7 @@
 //  11 k_cov_rows      covariance of the final kept rows (from k_out), negated.
 //  12 k_reduce        final raw moments S, s_k, s_v, n_e.
 // Every reduction has a fixed order, so results are bit-reproducible.
+#include "mkv_bf16.h"
 #include "mkv_device.h"
 #include "mkv_compress.h"
 
@@ -1109,12 +1110,13 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) k_residual(Compre
         if (fabsf(st[e]) < a.tau) st[e] = 0.f;
       }
       if constexpr (BF) {
-        u16x8 hi, lo;
+        u32x4 hi, lo;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const bf16_t h = f2bf(st[e]);
-          hi[e] = h;
-          lo[e] = f2bf(st[e] - bf2f(h));
+        for (int e = 0; e < 8; e += 2) {
+          uint32_t h, l;
+          bf16_split_pair(st[e], st[e + 1], h, l);
+          hi[e / 2] = h;
+          lo[e / 2] = l;
         }
         af[m][ks][0] = __builtin_bit_cast(FragT, hi);
         af[m][ks][NPL - 1] = __builtin_bit_cast(FragT, lo);

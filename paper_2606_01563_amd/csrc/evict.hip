@@ -22,6 +22,7 @@
 //   Eq. app_update) and the move of the last row into the freed one.
 #include <climits>
 
+#include "mkv_bf16.h"
 #include "mkv_device.h"
 #include "mkv_evict.h"
 
@@ -66,13 +67,6 @@ __device__ __forceinline__ f32x8 lds_frag(const float* p) {
   return r;
 }
 
-// RNE bf16 of a finite value (no NaN case: the summary of finite inputs is finite)
-__device__ __forceinline__ bf16_t f2bf_finite(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
-
 // S_tilde of one head into LDS; every thread handles D*D/8/256 chunks of 8 entries of a
 // row (all loads issued before any is used).
 template <class T, int D>
@@ -105,12 +99,7 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumL
     if constexpr (sizeof(T) == 2) {
       uint32_t h[4], l[4];
 #pragma unroll
-      for (int x = 0; x < 8; x += 2) {
-        const bf16_t h0 = f2bf_finite(st[x]), h1 = f2bf_finite(st[x + 1]);
-        const bf16_t l0 = f2bf_finite(st[x] - bf2f(h0)), l1 = f2bf_finite(st[x + 1] - bf2f(h1));
-        h[x / 2] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        l[x / 2] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-      }
+      for (int x = 0; x < 8; x += 2) bf16_split_pair(st[x], st[x + 1], h[x / 2], l[x / 2]);
       *reinterpret_cast<uint4*>(&sm.hi[row * RS + scol<T>(row, c0)]) = make_uint4(h[0], h[1], h[2], h[3]);
       *reinterpret_cast<uint4*>(&sm.lo[row * RS + scol<T>(row, c0)]) = make_uint4(l[0], l[1], l[2], l[3]);
     } else {
