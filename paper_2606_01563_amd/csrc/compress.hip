@@ -583,7 +583,8 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
     sRow[r][1] = a.rowstat[((size_t)head * a.R + r) * 2 + 1];
   }
   for (int b = tid; b < TK_HBINS; b += 256) sHist[b] = sHistA[b] = 0u;
-  // query rows past R repeat row R-1 (their sums are never used)
+  // query rows past R repeat row R-1: their terms get weight 0 (and a max of +inf, so
+  // that no large logit can overflow into 0 x inf)
   typename Frag<T>::type qf[MTW][KS];
 #pragma unroll
   for (int k = 0; k < MTW; ++k) {
@@ -593,33 +594,37 @@ __global__ void __launch_bounds__(256) k_mass(CompressArgs a) {
     for (int ks = 0; ks < KS; ++ks) qf[k][ks] = load_frag(qrow + 32 * ks + 8 * (lane >> 4));
   }
   __syncthreads();
+  float rmax[MTW][4], rinv[MTW][4];  // row statistics of the lane's result rows
+#pragma unroll
+  for (int k = 0; k < MTW; ++k)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * (wave + 4 * k) + 4 * (lane >> 4) + i;
+      const bool ok = r < a.R;
+      rmax[k][i] = ok ? sRow[r][0] : INFINITY;
+      rinv[k][i] = ok ? sRow[r][1] : 0.f;
+    }
 
   for (int t = t_beg; t < t_end; ++t) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) store_frag(&sK[(tid + 256 * i) / DG][8 * dg], pk[i]);
     load_tile(t + 1);  // past the slice: its last row again
     __syncthreads();
+    // each 16-token group's K fragments are read from LDS once for all row tiles
     float col[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = 0; k < MTW; ++k) {
-      const int mt = wave + 4 * k;
-      if (mt >= RT) continue;
-      float rmax[4], rinv[4];
+    for (int nt = 0; nt < 4; ++nt) {
+      typename Frag<T>::type kb[KS];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 16 * mt + 4 * (lane >> 4) + i;
-        const bool ok = r < a.R;
-        rmax[i] = ok ? sRow[r][0] : 0.f;
-        rinv[i] = ok ? sRow[r][1] : 0.f;
-      }
+      for (int ks = 0; ks < KS; ++ks) kb[ks] = load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
+      for (int k = 0; k < MTW; ++k) {
+        if (wave + 4 * k >= RT) continue;
         f32x4 acc = zero4();
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          mma(acc, qf[k][ks], load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]));
+        for (int ks = 0; ks < KS; ++ks) mma(acc, qf[k][ks], kb[ks]);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) col[nt] += fast_exp2(acc[i] * c2 - rmax[i]) * rinv[i];
+        for (int i = 0; i < 4; ++i) col[nt] += fast_exp2(acc[i] * c2 - rmax[k][i]) * rinv[k][i];
       }
     }
 #pragma unroll
