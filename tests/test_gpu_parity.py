@@ -101,6 +101,22 @@ def test_ragged_shapes_and_both_head_dims(dtype, d, summary):
     P.run_decode_steps(gpu, out, 2, summary=summary, n_split=2)
 
 
+@pytest.mark.parametrize("q_scale", [1.0, 12.0])
+def test_window_rows_not_a_multiple_of_16(q_scale):
+    """G = 3 and a window of 7 give 21 window rows per KV head: the second 16-row tile is
+    mostly padding.  With the queries scaled up, the window logits reach hundreds, so a
+    padded row that repeated the last real row could overflow exp in the window mass; the
+    masses, selections and moments must still follow the oracle."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, ctx_len=900, n_q_heads=6, n_kv_heads=2,
+                         window=7, budgets=(60,))
+    cpu["q_win"] = cpu["q_win"] * q_scale
+    gpu["q_win"] = cpu["q_win"].cuda()
+    out = P.run_compress(gpu, 60, cap=60)
+    assert torch.isfinite(out.abar).all() and torch.isfinite(out.score0).all()
+    for h in range(2):
+        P.check_compress_head(cpu, out, 0, h, 60)
+
+
 @pytest.mark.parametrize("mi_rounds", [-1, 0, 1])
 @pytest.mark.parametrize("chunk", [1, 4, 8])
 def test_selection_modes_and_chunks(mi_rounds, chunk):
