@@ -442,24 +442,37 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         for (int ks = 0; ks < KS; ++ks)
           mma(acc[nt], qf[k][ks], load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]));
       }
+      if (!need_mask) {
+        // every logit finite: the max is taken on the raw products (c2 > 0, so scaling
+        // after the max is exact), the scale folds into the exponent's FMA, and the
+        // rescale is skipped when no lane's max grew (it would multiply by exactly 1)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float x[4];
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          x[nt] = acc[nt][i] * c2;
-          if (need_mask) {
-            const int jj = tok0 + 16 * nt + (lane & 15);
-            if (!(jj <= lim[k][i] && jj < a.N)) x[nt] = -INFINITY;
-          }
+        for (int i = 0; i < 4; ++i) {
+          const float am = fmaxf(fmaxf(acc[0][i], acc[1][i]), fmaxf(acc[2][i], acc[3][i]));
+          const float mn = fmaxf(rm[k][i], am * c2);
+          float l = rl[k][i];
+          if (__any(mn > rm[k][i])) l *= fast_exp2(rm[k][i] - mn);
+          rl[k][i] = l + ((fast_exp2(fmaf(acc[0][i], c2, -mn)) + fast_exp2(fmaf(acc[1][i], c2, -mn))) +
+                          (fast_exp2(fmaf(acc[2][i], c2, -mn)) + fast_exp2(fmaf(acc[3][i], c2, -mn))));
+          rm[k][i] = mn;
         }
-        // branch-free update: with no finite logit yet, shifting by 0 keeps (-inf, 0)
-        const float mn = fmaxf(rm[k][i], fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
-        const float ms = mn == -INFINITY ? 0.f : mn;
-        rl[k][i] = rl[k][i] * fast_exp2(rm[k][i] - ms) +
-                   ((fast_exp2(x[0] - ms) + fast_exp2(x[1] - ms)) +
-                    (fast_exp2(x[2] - ms) + fast_exp2(x[3] - ms)));
-        rm[k][i] = mn;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float x[4];
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) {
+            const int jj = tok0 + 16 * nt + (lane & 15);
+            x[nt] = (jj <= lim[k][i] && jj < a.N) ? acc[nt][i] * c2 : -INFINITY;
+          }
+          // with no finite logit yet, shifting by 0 keeps (-inf, 0)
+          const float mn = fmaxf(rm[k][i], fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+          const float ms = mn == -INFINITY ? 0.f : mn;
+          rl[k][i] = rl[k][i] * fast_exp2(rm[k][i] - ms) +
+                     ((fast_exp2(x[0] - ms) + fast_exp2(x[1] - ms)) +
+                      (fast_exp2(x[2] - ms) + fast_exp2(x[3] - ms)));
+          rm[k][i] = mn;
+        }
       }
     }
     if (tile_has_cand) cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
