@@ -721,28 +721,49 @@ __device__ int block_excl_scan(int x, int* sW, int* total) {
   return res;
 }
 
-// Over bins in descending order, the bin where the running count reaches `need`
-// (1 <= need <= total); thread t owns nb / NT consecutive bins from the top.  Writes
-// (bin, count above it).
-template <int NT>
-__device__ __forceinline__ void find_bin(const uint32_t* hist, int nb, int need, int* sW,
-                                         uint32_t* sh_bin, uint32_t* sh_above) {
-  const int tid = threadIdx.x;
-  const int per = nb / NT;
-  int c = 0;
-  for (int q = 0; q < per; ++q) c += (int)hist[nb - 1 - per * tid - q];
-  int tot;
-  int before = block_excl_scan<NT>(c, sW, &tot);
-  for (int q = 0; q < per; ++q) {
-    const int bin = nb - 1 - per * tid - q;
-    const int h = (int)hist[bin];
-    if (before < need && before + h >= need) {
-      *sh_bin = (uint32_t)bin;
-      *sh_above = (uint32_t)before;
-    }
-    before += h;
+// Over NB histogram bins in descending order, the bin where the running count reaches
+// `need` (1 <= need <= total), found by one wave: lane l holds NB / 64 consecutive bins from
+// the top in registers (16-byte LDS reads), one wave scan of their sums, then the lane
+// whose range crosses `need` walks its bins.  No block-wide scan or barrier.  Returns
+// (bin, count above it) in every lane of the wave.
+template <int NB>
+__device__ __forceinline__ void wave_find_bin(const uint32_t* hist, int need, uint32_t* bin,
+                                              uint32_t* above) {
+  constexpr int PER = NB / 64;
+  const int lane = threadIdx.x & 63;
+  const int lo = NB - PER * (lane + 1);  // the lane's lowest bin
+  uint32_t h[PER];
+#pragma unroll
+  for (int v = 0; v < PER / 4; ++v) {
+    const uint4 x = reinterpret_cast<const uint4*>(hist + lo)[v];
+    h[4 * v] = x.x; h[4 * v + 1] = x.y; h[4 * v + 2] = x.z; h[4 * v + 3] = x.w;
   }
-  __syncthreads();
+  int c = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) c += (int)h[q];
+  int inc = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o);
+    if (lane >= o) inc += y;
+  }
+  int before = inc - c;
+  uint32_t b = 0u, ab = 0u;
+  bool found = false;
+  const bool mine = before < need && inc >= need;
+#pragma unroll
+  for (int q = PER - 1; q >= 0; --q) {  // from the lane's top bin down
+    if (mine && !found && before + (int)h[q] >= need) {
+      b = (uint32_t)(lo + q);
+      ab = (uint32_t)before;
+      found = true;
+    }
+    before += (int)h[q];
+  }
+  const uint64_t m = __ballot(found);
+  const int src = m ? (int)__builtin_ctzll(m) : 0;
+  *bin = (uint32_t)__shfl((int)b, src);
+  *above = (uint32_t)__shfl((int)ab, src);
 }
 
 // The TKPT consecutive keys of thread tid in slice sl (positions >= n give valid = false).
@@ -762,7 +783,7 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
                                                    int* __restrict__ state,
                                                    int* __restrict__ cnt, uint32_t* __restrict__ cand) {
   __shared__ int sW[2 * (TKT / 64) + 1];
-  __shared__ uint32_t hst[TK_HBINS];
+  __shared__ __align__(16) uint32_t hst[TK_HBINS];
   __shared__ uint32_t sh_bin, sh_above;
   const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x;
   if (kh) k = min(kh[head], n);  // head-adaptive count (uniform over the workgroup)
@@ -773,7 +794,12 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
   // the head's histogram (every slice workgroup finds the same bin of the k-th key)
   for (int b = threadIdx.x; b < TK_HBINS; b += TKT) hst[b] = hh[(size_t)head * TK_HBINS + b];
   __syncthreads();
-  find_bin<TKT>(hst, TK_HBINS, k, sW, &sh_bin, &sh_above);
+  if (threadIdx.x < 64) {
+    uint32_t b, ab;
+    wave_find_bin<TK_HBINS>(hst, k, &b, &ab);
+    if (threadIdx.x == 0) { sh_bin = b; sh_above = ab; }
+  }
+  __syncthreads();
   const uint32_t B = sh_bin;
   if (sl == 0 && threadIdx.x == 0) {
     state[2 * head] = (int)sh_bin;
@@ -785,16 +811,17 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
     n_gt += valid[u] && (key[u] >> 20) > B;
     n_c += valid[u] && (key[u] >> 20) == B;
   }
-  int tot_gt, tot_c;
-  block_excl_scan<TKT>(n_gt, sW, &tot_gt);
-  int pos = block_excl_scan<TKT>(n_c, sW, &tot_c);
+  // one scan of both counts, packed in 16-bit halves (a slice holds 2048 positions)
+  int tot;
+  const int before = block_excl_scan<TKT>(n_gt | (n_c << 16), sW, &tot);
+  int pos = before >> 16;
   uint32_t* c = cand + ((size_t)head * ntk + sl) * TKS;
 #pragma unroll
   for (int u = 0; u < TKPT; ++u)
     if (valid[u] && (key[u] >> 20) == B) c[pos++] = key[u];
   if (threadIdx.x == 0) {
-    cnt[((size_t)head * ntk + sl) * 2] = tot_gt;
-    cnt[((size_t)head * ntk + sl) * 2 + 1] = tot_c;
+    cnt[((size_t)head * ntk + sl) * 2] = tot & 0xFFFF;
+    cnt[((size_t)head * ntk + sl) * 2 + 1] = tot >> 16;
   }
 }
 
@@ -806,7 +833,7 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
                                                     int32_t* __restrict__ out, int out_stride,
                                                     int pos_offset) {
   __shared__ int s_gt[TK_MAX_SLICES], s_cn[TK_MAX_SLICES], s_gtT[TK_MAX_SLICES], s_eqT[TK_MAX_SLICES];
-  __shared__ uint32_t hst[1024];
+  __shared__ __align__(16) uint32_t hst[1024];
   __shared__ uint32_t sh_bin, sh_above;
   __shared__ int sW[2 * (TKT / 64) + 1];
   __shared__ int s_off, s_eqb;
@@ -884,11 +911,16 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
       if ((key & mask) == prefix) atomicAdd(&hst[(key >> shift) & 1023u], 1u);
     });
     __syncthreads();
-    find_bin<TKT>(hst, 1024, remaining, sW, &sh_bin, &sh_above);
+    if (tid < 64) {
+      uint32_t b, ab;
+      wave_find_bin<1024>(hst, remaining, &b, &ab);
+      if (tid == 0) { sh_bin = b; sh_above = ab; }
+    }
+    __syncthreads();
     prefix |= sh_bin << shift;
     mask |= 1023u << shift;
     remaining -= (int)sh_above;
-    __syncthreads();
+    __syncthreads();  // hst is cleared again by the next pass
   }
   const uint32_t T = prefix;
   const int need = remaining;  // keys equal to T to keep (>= 1), the lowest positions
@@ -907,22 +939,26 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
     }
   }
   __syncthreads();
-  // the slice's kept positions, in order
-  int n_eq = 0;
+  // the slice's kept positions, in order: one scan of (keys above T, keys at T) per
+  // thread, packed in 16-bit halves; the keys at T kept before a thread are the first of
+  // the need - (keys at T in earlier slices) still to keep
+  int n_gt = 0, n_eq = 0;
 #pragma unroll
-  for (int u = 0; u < TKPT; ++u) n_eq += valid[u] && key[u] == T;
+  for (int u = 0; u < TKPT; ++u) {
+    n_gt += valid[u] && key[u] > T;
+    n_eq += valid[u] && key[u] == T;
+  }
   int tot;
-  int eq_rank = s_eqb + block_excl_scan<TKT>(n_eq, sW, &tot);
+  const int before = block_excl_scan<TKT>(n_gt | (n_eq << 16), sW, &tot);
+  int eq_rank = s_eqb + (before >> 16);
   bool keep[TKPT];
-  int n_keep = 0;
 #pragma unroll
   for (int u = 0; u < TKPT; ++u) {
     const bool eq = valid[u] && key[u] == T;
     keep[u] = (valid[u] && key[u] > T) || (eq && eq_rank < need);
     eq_rank += eq;
-    n_keep += keep[u];
   }
-  int p = s_off + block_excl_scan<TKT>(n_keep, sW, &tot);
+  int p = s_off + (before & 0xFFFF) + min(max(need - s_eqb, 0), before >> 16);
   int32_t* o = out + (size_t)head * out_stride;
   const int j0 = sl * TKS + TKPT * tid;
 #pragma unroll
