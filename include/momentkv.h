@@ -259,7 +259,13 @@ size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);
 
 /* p         as for momentkv_decode_attn with summary = 0: S is the raw sum, updated in
  *           place.  max_len bounds lens after the append (budget < max_len <= cap leaves
- *           room for the new row)
+ *           room for the new row).  n_split selects the launch shape: 0 = automatic; for
+ *           max_len >= 769 (or n_split > 0) one read of the cache, the attention computed
+ *           in the scoring pass over about one workgroup per CU (n_split per KV head when
+ *           n_split > 0) and the evicted row's term removed from it afterwards, then a
+ *           finishing launch; for shorter caches the scoring and selection with one
+ *           workgroup per KV head, then the decode launches of momentkv_decode_attn with
+ *           their automatic split.  Results agree within the dtype's tolerance either way
  * budget    rows per KV head kept by Phase 1, >= 1 (MKV_ERR_BUDGET otherwise)
  * q, k_cache, v_cache, lens, out, lse_out, w_r_out: as momentkv_decode_attn; row lens (the
  *           new token) and row j* of the caches are written, lens is updated

@@ -1,25 +1,37 @@
-// Moment-informed eviction at a decoding step (Algorithm 1 Phase 1), run ahead of the
-// corrected attention of Phase 2 (which then goes through the decode launches on the
-// updated cache and summary).
+// Decode step with moment-informed eviction: Algorithm 1 Phase 1 (one eviction), then the
+// corrected attention of Phase 2 over the new cache and summary, reading the cache once.
 //
-// k_evict_scores: n_heads x nslice workgroups of 4 waves.  The workgroup first forms the
-//   summary's clamped covariance S_tilde = S - s_v s_k^T / n_e (entries below tau set to
-//   zero; zero when n_e = 0) from the raw moments into LDS: hi / lo bf16 planes for bf16
-//   caches, fp32 otherwise.  Each wave then takes 32-row blocks of the workgroup's rows
-//   of R, the new token included (row lens, read from k_new / v_new), and writes for
-//   every row j
-//     x_gj = scale log2(e) q_g . k_j           (base-2 logits of the G queries)
-//     y_j  = log2 ||r_j||,  r_j = v_j - v_bar - (scale / n_e) S_tilde k_j   (Eq. residual)
-//   S_tilde k_j runs on MFMA with the same K fragments as the logits (B operand) and
-//   S_tilde rows from LDS (A operand).  The rows of each 16-row MFMA tile are taken in
-//   the order that leaves every lane holding the products for exactly the dimensions of
-//   v_j it loaded (dims 32c + 8 (lane / 16) + e), so r_j and its squared norm are formed
-//   in registers and finished with a 4-lane sum.
-// k_evict_select: one workgroup per KV head.  log2 Z_g over R from the logits, the
-//   group-mean softmax weight alpha_j = mean_g 2^(x_gj - log2 Z_g) in the log domain (so
-//   no weight underflows), the argmin of log2 alpha_j + y_j (the lowest row on ties),
-//   then the rank-one update n_e += 1, s_k += k*, s_v += v*, S += v* k*^T (App. A.1
-//   Eq. app_update) and the move of the last row into the freed one.
+// k_evict_attn: about one NW-wave workgroup per CU (the LDS holds S_tilde and a V^T tile
+//   per wave), each taking an equal share of the flattened (head, 32-row block) range.
+//   For each head its share touches, the workgroup forms the summary's clamped covariance
+//   S_tilde = S - s_v s_k^T / n_e (entries below tau set to zero; zero when n_e = 0) from
+//   the raw moments into LDS (hi / lo bf16 planes for bf16 caches, fp32 otherwise) if the
+//   head evicts this call, while each wave's first block is in flight.  Each wave then
+//   takes the blocks w, w + NW, ... of the share, the new token included (row lens, read
+//   from k_new / v_new); lane l holds rows j0 + 2 (l % 16) + {0, 1} at dims
+//   32 c + 8 (l / 16) + e.  Per block:
+//     x_gj = scale log2(e) q_g . k_j on MFMA (base-2 logits of the G queries);
+//     if the head evicts, the records x_gj and y_j = log2 ||r_j||, with
+//       r_j = v_j - v_bar - (scale / n_e) S_tilde k_j (Eq. residual); S_tilde k_j runs on
+//       MFMA (S_tilde rows from LDS as A, the K fragments of the logits as B), its A rows
+//       ordered so that each lane receives the dims of v_j it holds, so r_j and its
+//       squared norm are formed in registers;
+//     the attention over every row (which one leaves is not known yet): online softmax
+//       in the base-2 domain and P.V on MFMA through an LDS transpose of V.  The running
+//       max after the block is recorded, so that a row's term can later be taken out
+//       exactly as it was accumulated.
+//   The waves' states are merged in LDS and written as one partial state of the head.
+// k_evict_finish: one workgroup per head combines the head's partial states in order,
+//   then selects and finishes:
+//   log2 Z_g over R from the logits, the group-mean softmax weight
+//   alpha_j = mean_g 2^(x_gj - log2 Z_g) in the log domain (no weight underflows), the
+//   argmin of log2 alpha_j + y_j (the lowest row on ties), the rank-one update n_e += 1,
+//   s_k += k*, s_v += v*, S += v* k*^T (App. A.1 Eq. app_update) and the move of the last
+//   row into the freed slot.  The evicted row's term leaves the attention state; where it
+//   held nearly all of a query's mass (the rest would then keep few significant digits)
+//   the attention over the new cache is computed again instead.  Last, S_tilde q from the
+//   updated summary and the correction w_R f_R + (1 - w_R) (v_bar + (scale / n_e)
+//   S_tilde q) with the Jensen estimate of the evicted mass (Eqs. fhat, jensen, fused).
 #include <climits>
 
 #include "mkv_bf16.h"
@@ -30,30 +42,48 @@ namespace mkv {
 
 namespace {
 
-constexpr int kEvThreads = 256;
-constexpr int kEvTB = 32;  // rows per block
+constexpr int kEvTB = 32;           // rows per block
+constexpr int kFinWaves = 4;        // waves of a finishing workgroup
+constexpr int kMaxSlices = 64;      // partial states merged by one finishing wave
+constexpr float kRedoRatio = 16.f;  // recompute when a removed term exceeds this many
+                                    // times what remains of a query's sum
 
-// LDS copy of S_tilde with rows padded by 16 bytes.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// Orders the wave's own LDS writes and reads for the compiler.  A wave's LDS operations
+// are carried out in issue order, so lanes of one wave exchanging data through LDS need
+// no hardware wait beyond that.
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// x * y rounded on its own, never fused into a following add: the scaled logits are
+// stored and used again later, and must be the same bits in both places.
+__device__ __forceinline__ float mul_nofuse(float x, float y) {
+#pragma clang fp contract(off)
+  return x * y;
+}
+
+// S_tilde in LDS.
 template <class T, int D> struct SumLds;
 template <int D> struct SumLds<bf16_t, D> {
-  static constexpr int RS = D + 8;
-  bf16_t hi[D * RS];
-  bf16_t lo[D * RS];
+  bf16_t hi[D * D];
+  bf16_t lo[D * D];
+  // Element (row, col).  Rows are unpadded; the 16-byte chunks of a row are XOR-swizzled
+  // so that the 16 rows one MFMA operand read touches (r + {0..3, 8..11, 16..19, 24..27})
+  // sit in 16 different chunks, i.e. in different banks (8 chunks for D = 64).
+  static __device__ __forceinline__ int at(int row, int col) {
+    constexpr int NC = D / 8;
+    const int f = ((row & 3) | (((row >> 3) & 3) << 2)) & (NC - 1);
+    return row * D + (((col >> 3) ^ f) << 3) + (col & 7);
+  }
 };
 template <int D> struct SumLds<float, D> {
   static constexpr int RS = D + 4;
   float st[D * RS];
+  static __device__ __forceinline__ int at(int row, int col) { return row * RS + col; }
 };
-
-// bf16 S_tilde rows: 16-byte chunks XOR-swizzled by bit 4 of the row.  The 16 rows one
-// MFMA read touches (r + {0..3, 8..11, 16..19, 24..27}) would otherwise fall pairwise
-// into the same bank group (rows 16 apart); swizzled, each 16-lane pass of the read
-// covers 16 different groups.
-template <class T>
-__device__ __forceinline__ int scol(int row, int col) {
-  if constexpr (sizeof(T) == 2) return col ^ (((row >> 4) & 1) << 5);
-  else return col;
-}
 
 __device__ __forceinline__ bf16x8 lds_frag(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
@@ -67,12 +97,12 @@ __device__ __forceinline__ f32x8 lds_frag(const float* p) {
   return r;
 }
 
-// S_tilde of one head into LDS; every thread handles D*D/8/256 chunks of 8 entries of a
+// S_tilde of one head into LDS; every thread handles D*D/8/NT chunks of 8 entries of a
 // row (all loads issued before any is used).
-template <class T, int D>
+template <class T, int D, int NT>
 __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumLds<T, D>& sm) {
-  constexpr int PER = D * D / 8 / kEvThreads;
-  constexpr int RS = SumLds<T, D>::RS;
+  constexpr int PER = D * D / 8 / NT;
+  static_assert(PER >= 1 && (D * D / 8) % NT == 0, "whole chunks per thread");
   const int tid = threadIdx.x;
   const int c0 = 8 * (tid % (D / 8));
   const int ne = e.n_e[head];
@@ -83,13 +113,13 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumL
   float sv[PER];
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
-    const int row = (tid + kEvThreads * u) / (D / 8);
+    const int row = (tid + NT * u) / (D / 8);
     raw[u] = load_frag(Sh + (size_t)row * D + c0);
     sv[u] = e.s_v[(size_t)head * D + row];
   }
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
-    const int row = (tid + kEvThreads * u) / (D / 8);
+    const int row = (tid + NT * u) / (D / 8);
     float st[8];
 #pragma unroll
     for (int x = 0; x < 8; ++x) {
@@ -100,18 +130,19 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumL
       uint32_t h[4], l[4];
 #pragma unroll
       for (int x = 0; x < 8; x += 2) bf16_split_pair(st[x], st[x + 1], h[x / 2], l[x / 2]);
-      *reinterpret_cast<uint4*>(&sm.hi[row * RS + scol<T>(row, c0)]) = make_uint4(h[0], h[1], h[2], h[3]);
-      *reinterpret_cast<uint4*>(&sm.lo[row * RS + scol<T>(row, c0)]) = make_uint4(l[0], l[1], l[2], l[3]);
+      const int at = SumLds<T, D>::at(row, c0);
+      *reinterpret_cast<uint4*>(&sm.hi[at]) = make_uint4(h[0], h[1], h[2], h[3]);
+      *reinterpret_cast<uint4*>(&sm.lo[at]) = make_uint4(l[0], l[1], l[2], l[3]);
     } else {
-      float4* P = reinterpret_cast<float4*>(&sm.st[row * RS + c0]);
+      float4* P = reinterpret_cast<float4*>(&sm.st[SumLds<T, D>::at(row, c0)]);
       P[0] = make_float4(st[0], st[1], st[2], st[3]);
       P[1] = make_float4(st[4], st[5], st[6], st[7]);
     }
   }
 }
 
-// The new token: wave 0 of the workgroup given the job copies k_new / v_new to cache row
-// `row`, 16 bytes per lane.
+// The new token: the wave given the job copies k_new / v_new to cache row `row`, 16 bytes
+// per lane.
 template <class T, int D>
 __device__ __forceinline__ void append_new_row(const EvictArgs& e, int head, int row, int lane) {
   constexpr int NV = D * (int)sizeof(T) / 16;
@@ -132,373 +163,959 @@ __device__ __forceinline__ bool head_evicts(const EvictArgs& e, int old_len) {
   return old_len >= 0 && old_len < e.cap && old_len + 1 <= e.max_len && old_len + 1 > e.budget;
 }
 
-}  // namespace
+// The G query rows of a head into LDS (rows past G, up to 16, zero): the A operand of
+// the logits.  load() issues the reads, store() writes them once other work is out.
+template <class T, int D, int NT>
+struct QueryRows {
+  static constexpr int QRS = D + 16 / (int)sizeof(T);  // rows padded by 16 bytes
+  static constexpr int QPR = D * (int)sizeof(T) / 16;  // 16-byte pieces per row
+  static constexpr int QPT = (16 * QPR + NT - 1) / NT;
+  uint4 qv[QPT];
+  __device__ __forceinline__ void load(const EvictArgs& e, int head) {
+    const T* qh = reinterpret_cast<const T*>(e.q) + (size_t)head * e.G * D;
+#pragma unroll
+    for (int u = 0; u < QPT; ++u) {
+      const int p = threadIdx.x + NT * u, row = p / QPR;
+      qv[u] = (p < 16 * QPR && row < e.G)
+                  ? *reinterpret_cast<const uint4*>(qh + (size_t)row * D + (p % QPR) * (16 / (int)sizeof(T)))
+                  : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ __forceinline__ void store(T* s_q) const {
+#pragma unroll
+    for (int u = 0; u < QPT; ++u) {
+      const int p = threadIdx.x + NT * u;
+      if (p < 16 * QPR)
+        *reinterpret_cast<uint4*>(&s_q[(p / QPR) * QRS + (p % QPR) * (16 / (int)sizeof(T))]) = qv[u];
+    }
+  }
+};
 
-// Selection (one KV head, NT threads): log2 Z_g over R from the logits, the group-mean
-// softmax weight in the log domain, the argmin (lowest row on ties), then the rank-one
-// update and the move of the last row.  Everything that does not depend on the choice
-// (the summary S, the last row, the score records of up to UB rows per thread) is
-// requested before any of it is used, so a short cache costs three round trips to
-// memory: the records and S together, then the evicted row.  GM bounds the group size
-// G (4, 8 or 16); rows per thread per batch shrink as it grows.  Also handles a head that
-// does not evict this call (append only, or the flags).
+// ---------------------------------------------------------------- attention of a wave
+// Online-softmax attention state of one wave over its blocks; query g = 4 (l / 16) + i
+// sits in MFMA row g, lane l holding entry i.
+template <class T, int D, int GM>
+struct EvAttn {
+  static constexpr int KS = D / 32;
+  static constexpr int NOT = D / 16;              // 16-column output tiles of P.V
+  static constexpr int PT = 16 / (int)sizeof(T);  // LDS row padding (16 bytes)
+  static constexpr int QRS = D + 16 / (int)sizeof(T);
+  typedef typename Frag<T>::type FragT;
+  typedef T VtTile[D][kEvTB + PT];
+  typedef T PTile[GM][kEvTB + PT];
+  static_assert(sizeof(VtTile) >= GM * D * sizeof(float), "o rows fit in the V^T tile");
+
+  float m_run[4], l_run[4];
+  f32x4 oacc[NOT];
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
+#pragma unroll
+    for (int nt = 0; nt < NOT; ++nt) oacc[nt] = zero4();
+  }
+
+  // Base-2 logits c2 q_g . k of the rows j0 + 2 (l % 16) + hh in x[hh] (queries from LDS).
+  static __device__ __forceinline__ void logits(const T* s_q, const FragT (&kf)[2][KS], float c2,
+                                                int lane, f32x4 (&x)[2]) {
+    const int r16 = lane & 15, q4 = lane >> 4;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) mma(acc, lds_frag(&s_q[r16 * QRS + 32 * ks + 8 * q4]), kf[hh][ks]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[hh][i] = mul_nofuse(acc[i], c2);
+    }
+  }
+
+  // One block at j0: x the base-2 logits (rows at or past t_end masked), vf the V
+  // fragments of the same rows (dims 32 c + 8 (l / 16) + e).
+  __device__ __forceinline__ void block(const f32x4 (&x)[2], const FragT (&vf)[2][KS], int j0,
+                                        int t_end, int G, int lane, VtTile& vt, PTile& sp) {
+    const int r16 = lane & 15, q4 = lane >> 4, p2 = 2 * r16;
+    wave_lds_order();  // the previous block's reads of vt / sp come first
+    // V^T into LDS: one 32-bit word per dim holds the lane's two rows
+#pragma unroll
+    for (int c = 0; c < KS; ++c) {
+      const int col0 = 32 * c + 8 * q4;
+      if constexpr (sizeof(T) == 2) {
+        const u32x4_t w0 = __builtin_bit_cast(u32x4_t, vf[0][c]);
+        const u32x4_t w1 = __builtin_bit_cast(u32x4_t, vf[1][c]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh)
+            *reinterpret_cast<uint32_t*>(&vt[col0 + 2 * w + hh][p2]) =
+                __builtin_amdgcn_perm(w1[w], w0[w], hh ? 0x07060302u : 0x05040100u);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          *reinterpret_cast<float2*>(&vt[col0 + e][p2]) = make_float2(elem_f(vf[0][c], e), elem_f(vf[1][c], e));
+      }
+    }
+    // online softmax over the 32 rows
+    float alpha[4];
+    const int ja = j0 + p2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = 4 * q4 + i;
+      const bool gok = g < G;
+      const float xa = (ja < t_end && gok) ? x[0][i] : -INFINITY;
+      const float xb = (ja + 1 < t_end && gok) ? x[1][i] : -INFINITY;
+      const float bm = row16_max(fmaxf(xa, xb));
+      const float mn = fmaxf(m_run[i], bm);
+      float pa = 0.f, pb = 0.f;
+      if (mn == -INFINITY) {
+        alpha[i] = 1.f;
+      } else {
+        alpha[i] = fast_exp2(m_run[i] - mn);
+        pa = fast_exp2(xa - mn);
+        pb = fast_exp2(xb - mn);
+      }
+      l_run[i] = l_run[i] * alpha[i] + row16_sum(pa + pb);
+      m_run[i] = mn;
+      if (g < GM) {
+        sp[g][p2] = from_f<T>(pa);
+        sp[g][p2 + 1] = from_f<T>(pb);
+      }
+    }
+    wave_lds_order();  // P and V^T are in LDS before they are read back
+    // O = alpha O + P . V (A = P rows g, B = V^T)
+    const FragT pfr = (r16 < G) ? load_frag(&sp[min(r16, GM - 1)][8 * q4]) : zero_frag<T>();
+#pragma unroll
+    for (int nt = 0; nt < NOT; ++nt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
+      mma(oacc[nt], pfr, load_frag(&vt[16 * nt + r16][8 * q4]));
+    }
+  }
+
+  // Running max of query 4 (l / 16) + (l % 4) (the same in the 16 lanes of a row).
+  __device__ __forceinline__ float m_of_lane(int lane) const {
+    const int i = lane & 3;
+    return i == 0 ? m_run[0] : (i == 1 ? m_run[1] : (i == 2 ? m_run[2] : m_run[3]));
+  }
+
+  // o rows g < G to so[g * D + col], (max, sum) to ml[2 g].
+  __device__ __forceinline__ void store_lds(float* so, float* ml, int G, int lane) const {
+    const int r16 = lane & 15, q4 = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = 4 * q4 + i;
+      if (g < G) {
+#pragma unroll
+        for (int nt = 0; nt < NOT; ++nt) so[g * D + 16 * nt + r16] = oacc[nt][i];
+        if (r16 == 0) {
+          ml[2 * g] = m_run[i];
+          ml[2 * g + 1] = l_run[i];
+        }
+      }
+    }
+  }
+};
+
+// Merged attention state of the queries g = wave + NW k a wave handles (lane l holds
+// columns CPL l ...).
+template <int GM, int NW, int D>
+struct QState {
+  static constexpr int KQ = (GM + NW - 1) / NW;
+  static constexpr int CPL = D / 64;
+  float M[KQ], l[KQ], o[KQ][CPL];
+};
+
+// Merge of nw wave states (wave w's o rows as floats at so + w * stride, its (max, sum)
+// at ml[w * 2 GM + 2 g]) in wave order.
+template <int GM, int NW, int D>
+__device__ __forceinline__ void merge_waves(QState<GM, NW, D>& qs, const float* so, int stride,
+                                            const float* ml, int nw, int G, int wave, int lane) {
+  constexpr int CPL = D / 64;
+#pragma unroll
+  for (int k = 0; k < QState<GM, NW, D>::KQ; ++k) {
+    const int g = wave + NW * k;
+    float M = -INFINITY, l = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) qs.o[k][c] = 0.f;
+    if (g < G) {
+      for (int w = 0; w < nw; ++w) M = fmaxf(M, ml[w * 2 * GM + 2 * g]);
+      if (M != -INFINITY) {
+        for (int w = 0; w < nw; ++w) {
+          const float wt = fast_exp2(ml[w * 2 * GM + 2 * g] - M);
+          l += ml[w * 2 * GM + 2 * g + 1] * wt;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) qs.o[k][c] += so[w * stride + g * D + lane * CPL + c] * wt;
+        }
+      }
+    }
+    qs.M[k] = M;
+    qs.l[k] = l;
+  }
+}
+
+// LDS of selection and finishing.
 template <int GM, int NW, int D>
 struct SelLds {
   float m[NW][GM], l[NW][GM], lz[GM];
   float best[NW];
-  int bj[NW], pick;
-  float kv[2][D];
+  int bj[NW], pick, redo;
+  float kv[2][D];      // k*, v* of the evicted row
+  float sk[D], sv[D];  // s_k, s_v after this call
+  float sq[GM * D];    // S_tilde q (unscaled), query-major
 };
 
-template <class T, int D, int GM, int NT>
-__device__ __forceinline__ void select_head(const EvictArgs& e, int head, int old_len,
-                                            SelLds<GM, NT / kWave, D>& sl) {
-  constexpr int NW = NT / kWave;
-  constexpr int UB = GM <= 4 ? 8 : (GM <= 8 ? 4 : 2);
-  constexpr int SPER = D * D / 4 / NT;  // float4 entries of S per thread
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// S after the update, staged in LDS for S_tilde q: element (row, col) in 16-byte chunks
+// XOR-swizzled by the row, so that the threads of one row (reading chunks p, p + TPR, ...)
+// and four neighbouring rows fall into different banks.
+template <int D>
+__device__ __forceinline__ int s_at(int row, int col) {
+  return row * D + ((((col >> 2) ^ ((row & 3) << 2))) << 2) + (col & 3);
+}
+
+// Selection and finishing of one KV head by its NW-wave workgroup (see the top of the
+// file).  qs: the merged attention state over every row attended to (R with the new
+// token); vt / sp / ml: LDS for RW waves to compute the attention again; s_q: the query
+// rows in LDS; s_S: LDS for the updated S (D x D floats; it may share the space of vt,
+// which is no longer used when S is written).  Everything that does not depend on the
+// choice (the summary S, s_k, s_v, the last row, the first batch of score records) is
+// requested before any of it is used, and everything that depends only on the choice
+// (the evicted row, its logits and its block's running maxima) in one round trip.
+template <class T, int D, int GM, int NW, int RW, bool ATTN>
+__device__ void select_finish(const EvictArgs& e, int head, int old_len, QState<GM, NW, D>& qs,
+                              SelLds<GM, NW, D>& sl, typename EvAttn<T, D, GM>::VtTile* vt,
+                              typename EvAttn<T, D, GM>::PTile* sp, float* ml, const T* s_q,
+                              float* s_S) {
+  typedef EvAttn<T, D, GM> EA;
+  typedef typename EA::FragT FragT;
+  constexpr int NT = NW * kWave, KS = D / 32, CPL = D / 64, QRS = EA::QRS;
+  constexpr int KQ = QState<GM, NW, D>::KQ;
+  constexpr int UB = GM <= 4 ? 16 : (GM <= 8 ? 8 : 4);  // records per thread per batch
+  constexpr int SPER = D * D / 4 / NT;                 // float4 entries of S per thread
+  constexpr int SCH = SPER < 16 ? SPER : 16;           // of which in registers at a time
+  constexpr int NCH = SPER / SCH;
+  static_assert(SPER >= 1 && SPER % SCH == 0 && NT % (D / 4) == 0, "S layout");
+  static_assert(RW <= NW, "recomputing waves");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool can_append = old_len >= 0 && old_len < e.cap;
-  if (!head_evicts(e, old_len)) {
-    if (tid == 0) {
-      if (!can_append) {
-        atomicOr(e.flag, 1);
-      } else {
-        if (old_len + 1 > e.max_len) atomicOr(e.flag, 2);
-        e.lens[head] = old_len + 1;
-      }
-      if (e.evicted) e.evicted[head] = -1;
-    }
-    return;
-  }
+  const bool evicts = head_evicts(e, old_len);
+  const int G = e.G, ML = e.rec_len, NB = e.rec_len / kEvTB;
   const int n_tok = old_len + 1, last = n_tok - 1;
-  const int G = e.G, ML = e.rec_len;
   const float* rec = e.rec + (size_t)head * (G + 2) * ML;
   T* kc = reinterpret_cast<T*>(e.k_cache) + (size_t)head * e.cap * D;
   T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
   float4* Sh = reinterpret_cast<float4*>(e.S + (size_t)head * D * D);
-  if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
 
   // requests independent of the choice
-  float4 s4[SPER];
+  float4 s4[SCH];
+  if (ATTN || evicts) {
 #pragma unroll
-  for (int u = 0; u < SPER; ++u) s4[u] = Sh[tid + NT * u];
-  T kl = T(), vl = T();
+    for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * u];
+  }
+  float skv = 0.f, svv = 0.f;
   if (tid < D) {
+    skv = e.s_k[(size_t)head * D + tid];
+    svv = e.s_v[(size_t)head * D + tid];
+  }
+  const int ne = e.n_e[head];
+  T kl = T(), vl = T();
+  if (evicts && tid < D) {
     kl = kc[(size_t)last * D + tid];
     vl = vc[(size_t)last * D + tid];
   }
-  float x[UB][GM], y[UB];
-  auto load_batch = [&](int base) {
-#pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int j = base + tid + NT * u;
-      const bool ok = j < n_tok;
-#pragma unroll
-      for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
-      y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
-    }
-  };
-  const int step = UB * NT;
-  const int nb = (n_tok + step - 1) / step;
+  if (tid == 0) sl.redo = 0;
 
-  // log2 Z_g over the n_tok rows
-  float m[GM], l[GM];
+  int js = -1;
+  if (evicts) {
+    if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
+    float x[UB][GM], y[UB];
+    auto load_batch = [&](int base) {
 #pragma unroll
-  for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
-  for (int b = 0; b < nb; ++b) {
-    load_batch(b * step);
+      for (int u = 0; u < UB; ++u) {
+        const int j = base + tid + NT * u;
+        const bool ok = j < n_tok;
 #pragma unroll
-    for (int u = 0; u < UB; ++u)
-#pragma unroll
-      for (int g = 0; g < GM; ++g) {
-        const float mn = fmaxf(m[g], x[u][g]);
-        if (mn != -INFINITY) {
-          l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x[u][g] - mn);
-          m[g] = mn;
-        }
+        for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
+        y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
       }
-  }
-#pragma unroll
-  for (int g = 0; g < GM; ++g) {
-    if (g < G) {
-      const float M = wave_max(m[g]);
-      const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
-      if (lane == 0) { sl.m[wave][g] = M; sl.l[wave][g] = ls; }
-    }
-  }
-  __syncthreads();
-  if (tid < G) {
-    float M = -INFINITY, L = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sl.m[w][tid]);
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-      if (sl.m[w][tid] != -INFINITY) L += sl.l[w][tid] * fast_exp2(sl.m[w][tid] - M);
-    sl.lz[tid] = M + log2f(L);
-  }
-  __syncthreads();
+    };
+    const int step = UB * NT;
+    const int nb = (n_tok + step - 1) / step;
 
-  // argmin over rows of log2(mean_g alpha_gj) + log2 ||r_j||, lowest row on ties
-  float lz[GM];
+    // log2 Z_g over the n_tok rows
+    float m[GM], l[GM];
 #pragma unroll
-  for (int g = 0; g < GM; ++g) lz[g] = g < G ? sl.lz[g] : 0.f;
-  const float log2_g = log2f((float)G);
-  float best = INFINITY;
-  int bj = INT_MAX;
-  for (int b = 0; b < nb; ++b) {
-    if (nb > 1) load_batch(b * step);  // one batch: still in registers
+    for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
+    for (int b = 0; b < nb; ++b) {
+      load_batch(b * step);
 #pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int j = b * step + tid + NT * u;
-      float mx = -INFINITY;
+      for (int u = 0; u < UB; ++u)
 #pragma unroll
-      for (int g = 0; g < GM; ++g) mx = fmaxf(mx, g < G ? x[u][g] - lz[g] : -INFINITY);
-      float sm = 0.f;
+        for (int g = 0; g < GM; ++g) {
+          const float mn = fmaxf(m[g], x[u][g]);
+          if (mn != -INFINITY) {
+            l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x[u][g] - mn);
+            m[g] = mn;
+          }
+        }
+    }
 #pragma unroll
-      for (int g = 0; g < GM; ++g)
-        if (g < G) sm += fast_exp2(x[u][g] - lz[g] - mx);
-      const float sc = mx + log2f(sm) - log2_g + y[u];
-      if (j < n_tok && sc < best) { best = sc; bj = j; }  // rows rise along a thread
+    for (int g = 0; g < GM; ++g) {
+      if (g < G) {
+        const float M = wave_max(m[g]);
+        const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
+        if (lane == 0) { sl.m[wave][g] = M; sl.l[wave][g] = ls; }
+      }
+    }
+    __syncthreads();
+    if (tid < G) {
+      float M = -INFINITY, L = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) M = fmaxf(M, sl.m[w][tid]);
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+        if (sl.m[w][tid] != -INFINITY) L += sl.l[w][tid] * fast_exp2(sl.m[w][tid] - M);
+      sl.lz[tid] = M + log2f(L);
+    }
+    __syncthreads();
+
+    // argmin over rows of log2(mean_g alpha_gj) + log2 ||r_j||, lowest row on ties
+    float lz[GM];
+#pragma unroll
+    for (int g = 0; g < GM; ++g) lz[g] = g < G ? sl.lz[g] : 0.f;
+    const float log2_g = log2f((float)G);
+    float best = INFINITY;
+    int bj = INT_MAX;
+    for (int b = 0; b < nb; ++b) {
+      if (nb > 1) load_batch(b * step);  // one batch: still in registers
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        const int j = b * step + tid + NT * u;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int g = 0; g < GM; ++g) mx = fmaxf(mx, g < G ? x[u][g] - lz[g] : -INFINITY);
+        float sm = 0.f;
+#pragma unroll
+        for (int g = 0; g < GM; ++g)
+          if (g < G) sm += fast_exp2(x[u][g] - lz[g] - mx);
+        const float sc = mx + log2f(sm) - log2_g + y[u];
+        if (j < n_tok && sc < best) { best = sc; bj = j; }  // rows rise along a thread
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float ob = __shfl_xor(best, off);
+      const int oj = __shfl_xor(bj, off);
+      if (ob < best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+    }
+    if (lane == 0) { sl.best[wave] = best; sl.bj[wave] = bj; }
+    __syncthreads();
+    if (tid == 0) {
+      float bb = sl.best[0];
+      int j = sl.bj[0];
+#pragma unroll
+      for (int w = 1; w < NW; ++w)
+        if (sl.best[w] < bb || (sl.best[w] == bb && sl.bj[w] < j)) { bb = sl.best[w]; j = sl.bj[w]; }
+      sl.pick = j;
+    }
+    __syncthreads();
+    js = __builtin_amdgcn_readfirstlane(sl.pick);
+    if (js < 0 || js >= n_tok) js = -1;  // no comparable score (non-finite inputs)
+  }
+
+  // requests that depend on the choice: the evicted row, and per query handled here its
+  // logit and its block's running max
+  float kf = 0.f, vf = 0.f, xj[KQ], mbj[KQ];
+  if (js >= 0) {
+    if (tid < D) {
+      kf = to_f<T>(kc[(size_t)js * D + tid]);
+      vf = to_f<T>(vc[(size_t)js * D + tid]);
+    }
+    if constexpr (ATTN) {
+      const float* bmr = e.blkm + (size_t)head * (G + 1) * NB;
+#pragma unroll
+      for (int k = 0; k < KQ; ++k) {
+        const int g = min(wave + NW * k, G - 1);
+        xj[k] = rec[(size_t)g * ML + js];
+        mbj[k] = bmr[g * NB + js / kEvTB];
+      }
     }
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ob = __shfl_xor(best, off);
-    const int oj = __shfl_xor(bj, off);
-    if (ob < best || (ob == best && oj < bj)) { best = ob; bj = oj; }
-  }
-  if (lane == 0) { sl.best[wave] = best; sl.bj[wave] = bj; }
-  __syncthreads();
-  if (tid == 0) {
-    float bb = sl.best[0];
-    int j = sl.bj[0];
-#pragma unroll
-    for (int w = 1; w < NW; ++w)
-      if (sl.best[w] < bb || (sl.best[w] == bb && sl.bj[w] < j)) { bb = sl.best[w]; j = sl.bj[w]; }
-    sl.pick = j;
-  }
-  __syncthreads();
-  const int js = sl.pick;
-  if (js < 0 || js >= n_tok) {  // no comparable score (non-finite inputs): keep every row
+
+  // bookkeeping: the rank-one update of the vectors and the move of the last row into
+  // slot js, or the length and flags of a call that evicts nothing
+  if (js >= 0) {
+    if (tid < D) {
+      sl.kv[0][tid] = kf;
+      sl.kv[1][tid] = vf;
+      if (js != last) {
+        kc[(size_t)js * D + tid] = kl;
+        vc[(size_t)js * D + tid] = vl;
+      }
+      skv += kf;
+      svv += vf;
+      e.s_k[(size_t)head * D + tid] = skv;
+      e.s_v[(size_t)head * D + tid] = svv;
+    }
     if (tid == 0) {
+      e.n_e[head] = ne + 1;
+      e.lens[head] = last;
+      if (e.evicted) e.evicted[head] = js;
+    }
+  } else if (tid == 0) {
+    if (evicts) {  // no finite score: keep every row
       atomicOr(e.flag, 4);
       e.lens[head] = n_tok;
-      if (e.evicted) e.evicted[head] = -1;
+    } else if (!can_append) {
+      atomicOr(e.flag, 1);
+    } else {
+      if (old_len + 1 > e.max_len) atomicOr(e.flag, 2);
+      e.lens[head] = old_len + 1;
+    }
+    if (e.evicted) e.evicted[head] = -1;
+  }
+  if (tid < D) {
+    sl.sk[tid] = skv;
+    sl.sv[tid] = svv;
+  }
+  const int ne2 = js >= 0 ? ne + 1 : ne;
+  __syncthreads();
+
+  if constexpr (!ATTN) {
+    // the attention runs afterwards on the new state: only S is left to update
+    if (js >= 0) {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        if (ch > 0) {
+#pragma unroll
+          for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * (ch * SCH + u)];
+        }
+#pragma unroll
+        for (int u = 0; u < SCH; ++u) {
+          const int idx = tid + NT * (ch * SCH + u);
+          const int row = idx / (D / 4), c4 = 4 * (idx % (D / 4));
+          const float va = sl.kv[1][row];
+          s4[u].x = fmaf(va, sl.kv[0][c4], s4[u].x);
+          s4[u].y = fmaf(va, sl.kv[0][c4 + 1], s4[u].y);
+          s4[u].z = fmaf(va, sl.kv[0][c4 + 2], s4[u].z);
+          s4[u].w = fmaf(va, sl.kv[0][c4 + 3], s4[u].w);
+          Sh[idx] = s4[u];
+        }
+      }
     }
     return;
   }
-
-  // rank-one update and the move of the last row into slot js
-  if (tid < D) {
-    const T ks = kc[(size_t)js * D + tid], vs = vc[(size_t)js * D + tid];
-    const float kf = to_f<T>(ks), vf = to_f<T>(vs);
-    sl.kv[0][tid] = kf;
-    sl.kv[1][tid] = vf;
-    if (js != last) {
-      kc[(size_t)js * D + tid] = kl;
-      vc[(size_t)js * D + tid] = vl;
+  // The evicted row's term leaves the attention state as it was accumulated: p taken at
+  // its block's running max mb, scaled to the merged max M (the sum holds p in fp32, the
+  // output p rounded to the element type).
+  if (js >= 0) {
+#pragma unroll
+    for (int k = 0; k < KQ; ++k) {
+      const int g = wave + NW * k;
+      if (g < G) {
+        const float pj = fast_exp2(xj[k] - mbj[k]);
+        if (pj > 0.f) {
+          const float s = fast_exp2(mbj[k] - qs.M[k]);
+          const float pl = pj * s, po = to_f<T>(from_f<T>(pj)) * s;
+          const float l2 = qs.l[k] - pl;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) qs.o[k][c] = fmaf(-po, sl.kv[1][lane * CPL + c], qs.o[k][c]);
+          qs.l[k] = l2;
+          if (!(kRedoRatio * l2 >= pl) && lane == 0) sl.redo = 1;
+        }
+      }
     }
-    e.s_k[(size_t)head * D + tid] += kf;
-    e.s_v[(size_t)head * D + tid] += vf;
-  }
-  if (tid == 0) {
-    e.n_e[head] += 1;
-    e.lens[head] = last;
-    if (e.evicted) e.evicted[head] = js;
   }
   __syncthreads();
+
+  // the attention over the new cache (rows [0, last)) again when a removal left too
+  // little of some query's sum; RW waves
+  if (__builtin_amdgcn_readfirstlane(sl.redo)) {
+    const int n = last;  // >= budget >= 1
+    const float c2 = e.scale * kLog2e;
+    const int r16 = lane & 15, q4 = lane >> 4;
+    if (wave < RW) {
+      EA at;
+      at.init();
+      for (int j0 = kEvTB * wave; j0 < n; j0 += kEvTB * RW) {
+        FragT kf2[2][KS], vf2[2][KS];
 #pragma unroll
-  for (int u = 0; u < SPER; ++u) {
-    const int idx = tid + NT * u;
-    const int row = idx / (D / 4), c = 4 * (idx % (D / 4));
-    const float va = sl.kv[1][row];
-    s4[u].x = fmaf(va, sl.kv[0][c], s4[u].x);
-    s4[u].y = fmaf(va, sl.kv[0][c + 1], s4[u].y);
-    s4[u].z = fmaf(va, sl.kv[0][c + 2], s4[u].z);
-    s4[u].w = fmaf(va, sl.kv[0][c + 3], s4[u].w);
-    Sh[idx] = s4[u];
+        for (int hh = 0; hh < 2; ++hh) {
+          const int j = min(j0 + 2 * r16 + hh, n - 1);
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            kf2[hh][ks] = load_frag(kc + (size_t)j * D + 32 * ks + 8 * q4);
+            vf2[hh][ks] = load_frag(vc + (size_t)j * D + 32 * ks + 8 * q4);
+          }
+        }
+        f32x4 xl[2];
+        EA::logits(s_q, kf2, c2, lane, xl);
+        at.block(xl, vf2, j0, n, G, lane, vt[wave], sp[wave]);
+      }
+      wave_lds_order();
+      at.store_lds(reinterpret_cast<float*>(&vt[wave][0][0]), ml + wave * 2 * GM, G, lane);
+    }
+    __syncthreads();
+    merge_waves<GM, NW, D>(qs, reinterpret_cast<const float*>(&vt[0][0][0]),
+                           (int)(sizeof(typename EA::VtTile) / sizeof(float)), ml, RW, G, wave, lane);
+    __syncthreads();  // vt is read before s_S (which may share its space) is written
+  }
+
+  // S after the update S += v* k*^T: written back, and staged in LDS
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) {
+    if (ch > 0) {
+#pragma unroll
+      for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * (ch * SCH + u)];
+    }
+#pragma unroll
+    for (int u = 0; u < SCH; ++u) {
+      const int idx = tid + NT * (ch * SCH + u);
+      const int row = idx / (D / 4), c4 = 4 * (idx % (D / 4));
+      if (js >= 0) {
+        const float va = sl.kv[1][row];
+        s4[u].x = fmaf(va, sl.kv[0][c4], s4[u].x);
+        s4[u].y = fmaf(va, sl.kv[0][c4 + 1], s4[u].y);
+        s4[u].z = fmaf(va, sl.kv[0][c4 + 2], s4[u].z);
+        s4[u].w = fmaf(va, sl.kv[0][c4 + 3], s4[u].w);
+        Sh[idx] = s4[u];
+      }
+      *reinterpret_cast<float4*>(&s_S[s_at<D>(row, c4)]) = s4[u];
+    }
+  }
+  __syncthreads();
+
+  // S_tilde q = (S - s_v s_k^T / n_e) q with entries below tau set to zero: TPR threads
+  // per row of S, each over the chunks p, p + TPR, ... of 4 columns, then a sum over the
+  // row's threads (neighbouring lanes)
+  const bool use_sq = e.order >= 1 && ne2 > 0;
+  if (use_sq) {
+    constexpr int TPR = NT / D;
+    static_assert(TPR >= 1 && TPR <= 8 && D % (4 * TPR) == 0, "threads per row of S");
+    const float inv_n = 1.f / (float)ne2;
+    const int row = tid / TPR, part = tid % TPR;
+    const float sr = sl.sv[row];
+    float acc[GM];
+#pragma unroll
+    for (int g = 0; g < GM; ++g) acc[g] = 0.f;
+#pragma unroll
+    for (int k = 0; k < D / (4 * TPR); ++k) {
+      const int c4 = 4 * (TPR * k + part);
+      const float4 sv4 = *reinterpret_cast<const float4*>(&s_S[s_at<D>(row, c4)]);
+      const float4 sk4 = *reinterpret_cast<const float4*>(&sl.sk[c4]);
+      float st[4] = {sv4.x - sr * (sk4.x * inv_n), sv4.y - sr * (sk4.y * inv_n),
+                     sv4.z - sr * (sk4.z * inv_n), sv4.w - sr * (sk4.w * inv_n)};
+#pragma unroll
+      for (int x = 0; x < 4; ++x) st[x] = fabsf(st[x]) < e.tau ? 0.f : st[x];
+#pragma unroll
+      for (int g = 0; g < GM; ++g) {
+        if (g < G) {
+          const T* qg = s_q + g * QRS + c4;
+          acc[g] += st[0] * to_f<T>(qg[0]) + st[1] * to_f<T>(qg[1]) + st[2] * to_f<T>(qg[2]) +
+                    st[3] * to_f<T>(qg[3]);
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < GM; ++g) {
+      if (g < G) {
+        float a = acc[g];
+        if constexpr (TPR >= 2) a += dpp_f<0xB1>(a);  // quad_perm [1,0,3,2]
+        if constexpr (TPR >= 4) a += dpp_f<0x4E>(a);  // quad_perm [2,3,0,1]
+        if constexpr (TPR >= 8) a += __shfl_xor(a, 4);
+        if (part == 0) sl.sq[g * D + row] = a;
+      }
+    }
+  }
+  __syncthreads();
+
+  // outputs: f_R mixed with f_E_hat = v_bar + scale / n_e * S_tilde q by the Jensen weight
+  const int ne_c = e.order < 0 ? 0 : ne2;  // no correction: the output is f_R
+  const float inv_c = ne_c > 0 ? 1.f / (float)ne_c : 0.f;
+#pragma unroll
+  for (int k = 0; k < KQ; ++k) {
+    const int g = wave + NW * k;
+    if (g < G) {
+      const int col = lane * CPL;
+      float dot_s = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) dot_s += to_f<T>(s_q[g * QRS + col + c]) * sl.sk[col + c];
+      dot_s = wave_sum(dot_s);
+      const float M = qs.M[k], l = qs.l[k];
+      const float log_zr = (l > 0.f) ? (M + __log2f(l)) * kLn2 : -INFINITY;
+      float w_r = 1.f;
+      if (ne_c > 0) {
+        const float log_ze = logf((float)ne_c) + e.scale * dot_s / (float)ne_c;  // Jensen estimate
+        const float hi = fmaxf(log_zr, log_ze);
+        const float lse = hi + logf(expf(log_zr - hi) + expf(log_ze - hi));
+        w_r = expf(log_zr - lse);
+      }
+      T* out = reinterpret_cast<T*>(e.out) + ((size_t)head * G + g) * D + col;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const float f_r = (l > 0.f) ? qs.o[k][c] / l : 0.f;
+        float res = f_r;
+        if (ne_c > 0) {
+          float fe = sl.sv[col + c] * inv_c;
+          if (e.order >= 1) fe += e.scale * inv_c * sl.sq[g * D + col + c];
+          res = w_r * f_r + (1.f - w_r) * fe;
+        }
+        out[c] = from_f<T>(res);
+      }
+      if (lane == 0) {
+        const size_t pair = (size_t)head * G + g;
+        if (e.lse_out) e.lse_out[pair] = log_zr;
+        if (e.w_r_out) e.w_r_out[pair] = w_r;
+      }
+    }
   }
 }
 
-template <class T, int D, int GM>
-__global__ void __launch_bounds__(kEvThreads, sizeof(T) == 2 ? 2 : 1) k_evict_scores(EvictArgs e) {
-  typedef typename Frag<T>::type FragT;
-  constexpr int KS = D / 32;  // contraction steps; also 8-dim groups per lane and row
-  constexpr int NT = D / 16;  // 16-row tiles of S_tilde k
-  constexpr int RS = SumLds<T, D>::RS;
-  __shared__ __align__(16) SumLds<T, D> sm;
-  __shared__ __align__(16) float s_vbar[D];
-  constexpr int QRS = D + 16 / (int)sizeof(T);  // query rows padded by 16 bytes
-  __shared__ __align__(16) T s_q[16 * QRS];
-  __shared__ SelLds<GM, kEvThreads / kWave, D> sel;  // the selection, one workgroup per head
+// Waves per scoring workgroup: with the attention, as many as the LDS holds next to
+// S_tilde (one workgroup per CU); scoring alone, four (two workgroups per CU).
+template <class T, int GM, bool ATTN>
+constexpr int ev_waves() {
+  return !ATTN ? 4 : (sizeof(T) == 2 ? (GM <= 4 ? 8 : 4) : (GM <= 4 ? 4 : 2));
+}
 
-  const int head = blockIdx.x / e.nslice, slice = blockIdx.x % e.nslice;
-  // the wave index and the length are the same for all lanes; held in scalar registers,
-  // they make the block loop below uniform control flow rather than a per-lane loop
+template <class T, int D, int GM, int NW, bool ATTN> struct EvLds;
+template <class T, int D, int GM, int NW> struct EvLds<T, D, GM, NW, true> {
+  typedef EvAttn<T, D, GM> EA;
+  SumLds<T, D> sm;             // S_tilde of the head being scored
+  typename EA::VtTile vt[NW];  // per wave; after a segment, the wave's o rows
+  typename EA::PTile sp[NW];
+  T q[16 * EA::QRS];
+  float vbar[D];
+  float ml[NW * 2 * GM];
+};
+template <class T, int D, int GM, int NW> struct EvLds<T, D, GM, NW, false> {
+  typedef EvAttn<T, D, GM> EA;
+  SumLds<T, D> sm;
+  T q[16 * EA::QRS];
+  float vbar[D];
+  SelLds<GM, NW, D> sel;
+};
+
+template <class T, int D, int GM>
+struct FinLds {
+  typedef EvAttn<T, D, GM> EA;
+  struct Redo {
+    typename EA::VtTile vt[kFinWaves];
+    typename EA::PTile sp[kFinWaves];
+  };
+  union {
+    Redo r;          // an attention computed again
+    float S[D * D];  // then the updated S
+  } u;
+  T q[16 * EA::QRS];
+  float ml[kFinWaves * 2 * GM];
+  SelLds<GM, kFinWaves, D> sel;
+};
+
+// The scoring workgroup that holds block b of the flattened (head, 32-row block) range:
+// workgroup w takes blocks [w N / nwg, (w + 1) N / nwg), N = n_heads * hblocks.
+__device__ __forceinline__ int wg_of_block(const EvictArgs& e, int64_t b) {
+  const int64_t nblk = (int64_t)e.n_heads * e.hblocks;
+  return (int)(((b + 1) * e.nwg - 1) / nblk);
+}
+
+// Blocks [s0, s1) of one head by the NW-wave workgroup (see the top of the file).  With
+// ATTN the rows are scored and attended to, and the merged state is written as the
+// head's partial `slot`; without, a head that evicts is scored, and the workgroup (which
+// then holds the whole head) selects at the end.
+template <class T, int D, int GM, int NW, bool ATTN>
+__device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, NW, ATTN>& L, int head,
+                                           int s0, int s1, int slot) {
+  typedef EvAttn<T, D, GM> EA;
+  typedef typename EA::FragT FragT;
+  constexpr int KS = D / 32;   // contraction steps; also 8-dim groups per lane and row
+  constexpr int NTI = D / 16;  // 16-row tiles of S_tilde k
+  constexpr int NT = NW * kWave;
+  constexpr int CPL = D / 64;
+  // the wave index, lengths and loop bounds are the same for all lanes; held in scalar
+  // registers, they make the loops below uniform control flow rather than per-lane loops
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q4 = lane >> 4, r16 = lane & 15;
-  const int old_len = __builtin_amdgcn_readfirstlane(e.lens[head]);
-  const bool can_append = old_len >= 0 && old_len < e.cap;
-  // the workgroup whose rows hold the new one appends it (the last one for rows past them)
-  if (can_append && wave == 0 && min(old_len / e.slice_len, e.nslice - 1) == slice)
-    append_new_row<T, D>(e, head, old_len, lane);
-  const int t0 = slice * e.slice_len;
-  const int t1 = min(t0 + e.slice_len, old_len + 1);
-  if (!head_evicts(e, old_len) || t0 >= t1) {  // uniform over the workgroup
-    if (e.nslice == 1) select_head<T, D, GM, kEvThreads>(e, head, old_len, sel);  // lens, flags
-    return;
-  }
-
-  const int G = e.G;
-  const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
-  const T* vc = reinterpret_cast<const T*>(e.v_cache) + (size_t)head * e.cap * D;
-  const T* kn = reinterpret_cast<const T*>(e.k_new) + (size_t)head * D;
-  const T* vn = reinterpret_cast<const T*>(e.v_new) + (size_t)head * D;
-  const int ML = e.rec_len;  // rows of the record planes (whole 32-row blocks)
-  float* rec = e.rec + (size_t)head * (G + 2) * ML;
+  const int G = e.G, hb = e.hblocks;
+  const int ML = e.rec_len, NB = e.rec_len / kEvTB;
   const float c2 = e.scale * kLog2e;
 
-  // rows j0 + 16 hh + lane % 16: K and V fragments at dims 32 ks + 8 (lane / 16).  Rows
-  // past t1 read row t1 - 1 again (their records land in the padding of the record rows
-  // or are never written): every lane issues every load, so the compiler can count the
-  // loads in flight and waits for one block while the next is still arriving.
-  auto load = [&](FragT (&kf)[2][KS], FragT (&vf)[2][KS], int j0) {
+  const int old_len = __builtin_amdgcn_readfirstlane(e.lens[head]);
+  const bool can_append = old_len >= 0 && old_len < e.cap;
+  const bool evicts = head_evicts(e, old_len);
+  // rows attended to: R with the new token (the whole cache when there is no room);
+  // scored alone: R when the head evicts, nothing otherwise
+  const int n_rows = !ATTN ? (evicts ? old_len + 1 : 0)
+                           : (can_append ? old_len + 1 : min(max(old_len, 0), e.cap));
+  const int t0 = kEvTB * s0;  // below max_len <= cap
+  const int t1 = s1 == hb ? n_rows : min(kEvTB * s1, n_rows);
+  // the workgroup whose blocks hold the new row appends it (the head's last block for
+  // rows past them)
+  const int nb_new = min(old_len / kEvTB, hb - 1);
+  if (can_append && wave == 0 && nb_new >= s0 && nb_new < s1) append_new_row<T, D>(e, head, old_len, lane);
+
+  if (ATTN || t0 < t1) {  // uniform
+    const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
+    const T* vc = reinterpret_cast<const T*>(e.v_cache) + (size_t)head * e.cap * D;
+    const T* kn = reinterpret_cast<const T*>(e.k_new) + (size_t)head * D;
+    const T* vn = reinterpret_cast<const T*>(e.v_new) + (size_t)head * D;
+    float* rec = e.rec + (size_t)head * (G + 2) * ML;
+    float* bmr = e.blkm + (size_t)head * (G + 1) * NB;
+
+    // rows j0 + 2 (l % 16) + hh; rows past t1 read the last row again (masked in the
+    // attention; their records land in the padding of the record rows): every lane
+    // issues every load, so the compiler can count the loads in flight and waits for one
+    // block while the next is still arriving
+    const int jmax = max(t1 - 1, t0);  // a cache row even for an empty segment
+    auto load = [&](FragT (&kf)[2][KS], FragT (&vf)[2][KS], int j0) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int j = min(j0 + 16 * hh + r16, t1 - 1);
-      const T* kr = j == old_len ? kn : kc + (size_t)j * D;
-      const T* vr = j == old_len ? vn : vc + (size_t)j * D;
+      for (int hh = 0; hh < 2; ++hh) {
+        const int j = min(j0 + 2 * r16 + hh, jmax);
+        const bool nw = can_append && j == old_len;
+        const T* kr = nw ? kn : kc + (size_t)j * D;
+        const T* vr = nw ? vn : vc + (size_t)j * D;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        kf[hh][ks] = load_frag(kr + 32 * ks + 8 * q4);
-        vf[hh][ks] = load_frag(vr + 32 * ks + 8 * q4);
+        for (int ks = 0; ks < KS; ++ks) {
+          kf[hh][ks] = load_frag(kr + 32 * ks + 8 * q4);
+          vf[hh][ks] = load_frag(vr + 32 * ks + 8 * q4);
+        }
       }
-    }
-  };
-  FragT ka[2][KS], va[2][KS], kb[2][KS], vb[2][KS];
-  int j0 = t0 + kEvTB * wave;
-  load(ka, va, j0);  // in flight while the summary is formed
+    };
+    FragT ka[2][KS], va[2][KS], kb[2][KS], vb[2][KS];
+    int j0 = t0 + kEvTB * wave;
+    load(ka, va, j0);  // in flight while the summary is formed
 
-  // the G queries (rows past G zero) go to LDS as the A fragments of the logits, and
-  // v_bar = s_v / n_e next to them; their reads are issued before the summary's
-  constexpr int QPR = D * (int)sizeof(T) / 16;          // 16-byte pieces per query row
-  constexpr int QPT = (16 * QPR + kEvThreads - 1) / kEvThreads;
-  uint4 qv[QPT];
-  const T* qh = reinterpret_cast<const T*>(e.q) + (size_t)head * G * D;
-#pragma unroll
-  for (int u = 0; u < QPT; ++u) {
-    const int p = threadIdx.x + kEvThreads * u, row = p / QPR;
-    qv[u] = (p < 16 * QPR && row < G)
-                ? *reinterpret_cast<const uint4*>(qh + (size_t)row * D + (p % QPR) * (16 / (int)sizeof(T)))
-                : make_uint4(0, 0, 0, 0);
-  }
-  const int ne = e.n_e[head];
-  const float svv = threadIdx.x < D ? e.s_v[(size_t)head * D + threadIdx.x] : 0.f;
+    QueryRows<T, D, NT> qr;
+    qr.load(e, head);
+    const int ne = e.n_e[head];
+    const float svv = threadIdx.x < D ? e.s_v[(size_t)head * D + threadIdx.x] : 0.f;
+    if (evicts) build_summary<T, D, NT>(e, head, L.sm);
+    qr.store(L.q);
+    const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
+    if (threadIdx.x < D) L.vbar[threadIdx.x] = ne > 0 ? svv / (float)ne : 0.f;
+    __syncthreads();  // S_tilde, v_bar and the queries are in LDS
 
-  build_summary<T, D>(e, head, sm);
-
-#pragma unroll
-  for (int u = 0; u < QPT; ++u) {
-    const int p = threadIdx.x + kEvThreads * u;
-    if (p < 16 * QPR)
-      *reinterpret_cast<uint4*>(&s_q[(p / QPR) * QRS + (p % QPR) * (16 / (int)sizeof(T))]) = qv[u];
-  }
-  const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
-  if (threadIdx.x < D) s_vbar[threadIdx.x] = ne > 0 ? svv / (float)ne : 0.f;
-  auto process = [&](const FragT (&kf)[2][KS], const FragT (&vf)[2][KS], int j0) {
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      f32x4 lg = zero4();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) mma(lg, lds_frag(&s_q[r16 * QRS + 32 * ks + 8 * q4]), kf[hh][ks]);
-      // every lane stores (no per-lane branch around a store): rows past t1 land in the
-      // padding of the record planes, padded query slots in plane G + 1
-      const int j = j0 + 16 * hh + r16;
+    EA at;
+    at.init();
+    auto process = [&](const FragT (&kf)[2][KS], const FragT (&vf)[2][KS], int j0) {
+      f32x4 x[2];
+      EA::logits(L.q, kf, c2, lane, x);
+      // scoring records; every lane stores (no branch around a store): a head that does
+      // not evict writes into the first columns of the spare plane G + 1
+      const int col = evicts ? j0 + 2 * r16 : 2 * r16;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int g = 4 * q4 + i;
-        rec[(size_t)(g < G ? g : G + 1) * ML + j] = lg[i] * c2;
+        *reinterpret_cast<float2*>(&rec[(size_t)((evicts && g < G) ? g : G + 1) * ML + col]) =
+            make_float2(x[0][i], x[1][i]);
       }
-    }
-    // S_tilde k: tile t = 2c + s holds dims 32c + 8 (lane/16) + 4s + i in lane rows
-    // 4 (lane/16) + i, i.e. element 4s + i of the lane's V fragment c.
-    float rr[2] = {0.f, 0.f};
+      float rr[2] = {1.f, 1.f};
+      if (evicts) {
+        // S_tilde k: tile t = 2c + s holds dims 32c + 8 (lane/16) + 4s + i in lane rows
+        // 4 (lane/16) + i, i.e. element 4s + i of the lane's V fragment c.
+        rr[0] = rr[1] = 0.f;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int c = t >> 1, s = t & 1;
-      const int row = 32 * c + 8 * (r16 >> 2) + 4 * s + (r16 & 3);
-      f32x4 ta[2] = {zero4(), zero4()};
+        for (int t = 0; t < NTI; ++t) {
+          const int c = t >> 1, s = t & 1;
+          const int row = 32 * c + 8 * (r16 >> 2) + 4 * s + (r16 & 3);
+          f32x4 ta[2] = {zero4(), zero4()};
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        if constexpr (sizeof(T) == 2) {
-          const int col = scol<T>(row, 32 * ks + 8 * q4);
-          const bf16x8 ah = lds_frag(&sm.hi[row * RS + col]);
-          const bf16x8 al = lds_frag(&sm.lo[row * RS + col]);
+          for (int ks = 0; ks < KS; ++ks) {
+            if constexpr (sizeof(T) == 2) {
+              const int a = SumLds<T, D>::at(row, 32 * ks + 8 * q4);
+              const bf16x8 ah = lds_frag(&L.sm.hi[a]);
+              const bf16x8 al = lds_frag(&L.sm.lo[a]);
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            mma(ta[hh], ah, kf[hh][ks]);
-            mma(ta[hh], al, kf[hh][ks]);
+              for (int hh = 0; hh < 2; ++hh) {
+                mma(ta[hh], ah, kf[hh][ks]);
+                mma(ta[hh], al, kf[hh][ks]);
+              }
+            } else {
+              const f32x8 af = lds_frag(&L.sm.st[SumLds<T, D>::at(row, 32 * ks + 8 * q4)]);
+#pragma unroll
+              for (int hh = 0; hh < 2; ++hh) mma(ta[hh], af, kf[hh][ks]);
+            }
           }
-        } else {
-          const f32x8 af = lds_frag(&sm.st[row * RS + 32 * ks + 8 * q4]);
+          const float4 vb4 = *reinterpret_cast<const float4*>(&L.vbar[32 * c + 8 * q4 + 4 * s]);
+          const float vbv[4] = {vb4.x, vb4.y, vb4.z, vb4.w};
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh) mma(ta[hh], af, kf[hh][ks]);
+          for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float r = elem_f(vf[hh][c], 4 * s + i) - vbv[i] - cf * ta[hh][i];
+              rr[hh] += r * r;
+            }
+          // one tile's LDS reads in flight at a time: hoisting all of them would not fit
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        rr[0] = cross_row_sum(rr[0]);
+        rr[1] = cross_row_sum(rr[1]);
+      }
+      *reinterpret_cast<float2*>(&rec[(size_t)(evicts ? G : G + 1) * ML + col]) =
+          make_float2(0.5f * log2f(rr[0]), 0.5f * log2f(rr[1]));  // the same from four lanes
+      if constexpr (ATTN) {
+        at.block(x, vf, j0, t1, G, lane, L.vt[wave], L.sp[wave]);
+        // the running max of query 4 (l / 16) + (l % 4) after this block
+        const int gm = 4 * q4 + (lane & 3);
+        bmr[((evicts && gm < G) ? gm : G) * NB + (evicts ? j0 / kEvTB : 0)] = at.m_of_lane(lane);
+      }
+    };
+
+    // 32-row blocks j0, j0 + 32 NW, ... of this wave; the next block's rows are requested
+    // before the current block is processed (two register sets)
+    for (; j0 < t1; j0 += 2 * NW * kEvTB) {
+      load(kb, vb, j0 + NW * kEvTB);
+      process(ka, va, j0);
+      if (j0 + NW * kEvTB >= t1) break;
+      load(ka, va, j0 + 2 * NW * kEvTB);
+      process(kb, vb, j0 + NW * kEvTB);
+    }
+
+    if constexpr (ATTN) {
+      // the waves' states, merged per query, as the head's partial `slot`
+      wave_lds_order();
+      at.store_lds(reinterpret_cast<float*>(&L.vt[wave][0][0]), L.ml + wave * 2 * GM, G, lane);
+      __syncthreads();
+      QState<GM, NW, D> qs;
+      merge_waves<GM, NW, D>(qs, reinterpret_cast<const float*>(&L.vt[0][0][0]),
+                             (int)(sizeof(typename EA::VtTile) / sizeof(float)), L.ml, NW, G, wave, lane);
+#pragma unroll
+      for (int k = 0; k < QState<GM, NW, D>::KQ; ++k) {
+        const int g = wave + NW * k;
+        if (g < G) {
+          const size_t pb = ((size_t)head * e.maxslots + slot) * G + g;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) e.part_o[pb * D + lane * CPL + c] = qs.o[k][c];
+          if (lane == 0) {
+            e.part_ml[pb * 2] = qs.M[k];
+            e.part_ml[pb * 2 + 1] = qs.l[k];
+          }
         }
       }
-      const float4 vb = *reinterpret_cast<const float4*>(&s_vbar[32 * c + 8 * q4 + 4 * s]);
-      const float vbv[4] = {vb.x, vb.y, vb.z, vb.w};
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float r = elem_f(vf[hh][c], 4 * s + i) - vbv[i] - cf * ta[hh][i];
-          rr[hh] += r * r;
-        }
-      // one tile's LDS reads in flight at a time: hoisting all of them would not fit
-      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      rr[hh] = cross_row_sum(rr[hh]);
-      const int j = j0 + 16 * hh + r16;
-      rec[(size_t)G * ML + j] = 0.5f * log2f(rr[hh]);  // the same value from four lanes
-    }
-  };
-  __syncthreads();  // S_tilde and v_bar are in LDS
-
-  // 32-row blocks j0, j0 + 128, ... of this wave; the next block's rows are requested
-  // before the current block is processed (two register sets)
-  for (; j0 < t1; j0 += 8 * kEvTB) {
-    load(kb, vb, j0 + 4 * kEvTB);
-    process(ka, va, j0);
-    if (j0 + 4 * kEvTB >= t1) break;
-    load(ka, va, j0 + 8 * kEvTB);
-    process(kb, vb, j0 + 4 * kEvTB);
   }
-  // The head's only workgroup selects right away: its records (and the appended row) are
-  // visible to all of its waves after the barrier; no second launch.
-  if (e.nslice == 1) {
+  if constexpr (!ATTN) {
+    // The workgroup holds the whole head: its records and the appended row are visible
+    // to all of its waves after a barrier; the selection needs no second launch.
     __syncthreads();
-    select_head<T, D, GM, kEvThreads>(e, head, old_len, sel);
+    QState<GM, NW, D> none;
+    select_finish<T, D, GM, NW, NW, false>(e, head, old_len, none, L.sel, nullptr, nullptr, nullptr,
+                                           L.q, nullptr);
   }
 }
 
-// Selection as its own launch, one 512-thread workgroup per KV head (two fit on a CU, so
-// a grid of a few hundred heads runs in one round): used when the scoring ran over
-// several workgroups per head.
-constexpr int kSelThreads = 512;
+}  // namespace
 
-template <class T, int D, int GM>
-__global__ void __launch_bounds__(kSelThreads) k_evict_select(EvictArgs e) {
-  __shared__ SelLds<GM, kSelThreads / kWave, D> sl;
-  select_head<T, D, GM, kSelThreads>(e, blockIdx.x, e.lens[blockIdx.x], sl);
+// Scoring pass.  With the attention (ATTN): nwg workgroups (about one per CU) take equal,
+// contiguous shares of the flattened (head, 32-row block) range, so heads of any length
+// spread evenly over the CUs; a share crosses into at most a few heads, each a segment
+// (queries and S_tilde formed per segment), whose merged state is written as the head's
+// partial number w - (first workgroup of the head).  The head's last block also takes
+// rows past hblocks * 32 (a cache longer than max_len after a full call).  Scoring alone:
+// one workgroup per head, which also selects.
+template <class T, int D, int GM, int NW, bool ATTN>
+__global__ void __launch_bounds__(NW * kWave, ATTN ? 1 : 2) k_evict_attn(EvictArgs e) {
+  typedef EvLds<T, D, GM, NW, ATTN> LT;
+  static_assert(sizeof(LT) <= 160 * 1024, "LDS of the scoring workgroup");
+  __shared__ __align__(16) LT L;
+  if constexpr (ATTN) {
+    const int hb = e.hblocks;
+    const int64_t nblk = (int64_t)e.n_heads * hb;
+    const int64_t b0 = (int64_t)blockIdx.x * nblk / e.nwg, b1 = (int64_t)(blockIdx.x + 1) * nblk / e.nwg;
+    for (int head = (int)(b0 / hb); b1 > b0 && (int64_t)head * hb < b1; ++head) {
+      const int s0 = (int)max(b0 - (int64_t)head * hb, (int64_t)0);
+      const int s1 = (int)min(b1 - (int64_t)head * hb, (int64_t)hb);
+      __syncthreads();  // the previous segment's reads of the LDS are done
+      ev_segment<T, D, GM, NW, true>(e, L, head, s0, s1, blockIdx.x - wg_of_block(e, (int64_t)head * hb));
+    }
+  } else {
+    ev_segment<T, D, GM, NW, false>(e, L, blockIdx.x, 0, e.hblocks, 0);
+  }
 }
+
+// Finishing launch, one 4-wave workgroup per KV head (two fit on a CU for bf16): the head's
+// partial states combined in order, then selection, update and correction.
+template <class T, int D, int GM>
+__global__ void __launch_bounds__(kFinWaves * kWave, 2) k_evict_finish(EvictArgs e) {
+  typedef FinLds<T, D, GM> LT;
+  constexpr int NT = kFinWaves * kWave, CPL = D / 64, SUB = 16;
+  static_assert(sizeof(LT) <= 160 * 1024, "LDS of the finishing workgroup");
+  static_assert(sizeof(T) == 4 || sizeof(LT) <= 80 * 1024, "two bf16 finishing workgroups per CU");
+  __shared__ __align__(16) LT L;
+  const int head = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int old_len = __builtin_amdgcn_readfirstlane(e.lens[head]);
+  const int G = e.G;
+  const int hb = e.hblocks;
+  const int ns = wg_of_block(e, (int64_t)(head + 1) * hb - 1) - wg_of_block(e, (int64_t)head * hb) + 1;
+
+  QueryRows<T, D, NT> qr;
+  qr.load(e, head);
+  // the partial states per query, combined in order; every load is issued before the
+  // first is used (partial indices clamped to the count)
+  QState<GM, kFinWaves, D> qs;
+#pragma unroll
+  for (int k = 0; k < QState<GM, kFinWaves, D>::KQ; ++k) {
+    const int g = min(wave + kFinWaves * k, G - 1);  // waves past G: loads never used
+    const size_t base = (size_t)head * e.maxslots;
+    auto o_at = [&](int s, int c) {
+      return e.part_o + ((base + min(s, ns - 1)) * G + g) * D + lane * CPL + c;
+    };
+    const float2 ml = *reinterpret_cast<const float2*>(e.part_ml + ((base + min(lane, ns - 1)) * G + g) * 2);
+    float ov[SUB][CPL];
+#pragma unroll
+    for (int u = 0; u < SUB; ++u)
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) ov[u][c] = *o_at(u, c);
+    const bool live = lane < ns;
+    const float M = wave_max(live ? ml.x : -INFINITY);
+    const float w = (live && M != -INFINITY) ? fast_exp2(ml.x - M) : 0.f;
+    qs.M[k] = M;
+    qs.l[k] = wave_sum(live ? ml.y * w : 0.f);
+    float o[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+    for (int s0 = 0; s0 < ns; s0 += SUB) {
+      if (s0 > 0) {
+#pragma unroll
+        for (int u = 0; u < SUB; ++u)
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) ov[u][c] = *o_at(s0 + u, c);
+      }
+#pragma unroll
+      for (int u = 0; u < SUB; ++u) {
+        if (s0 + u < ns) {
+          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) o[c] = fmaf(wu, ov[u][c], o[c]);
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) qs.o[k][c] = o[c];
+  }
+  qr.store(L.q);
+  __syncthreads();
+  select_finish<T, D, GM, kFinWaves, kFinWaves, true>(e, head, old_len, qs, L.sel, L.u.r.vt,
+                                                      L.u.r.sp, L.ml, L.q, L.u.S);
+}
+
+int evict_waves(bool bf16, int G) {
+  if (bf16) return G <= 4 ? ev_waves<bf16_t, 4, true>() : ev_waves<bf16_t, 16, true>();
+  return G <= 4 ? ev_waves<float, 4, true>() : ev_waves<float, 16, true>();
+}
+
+int evict_max_slices() { return kMaxSlices; }
 
 template <class T, int D, int GM>
 static hipError_t launch_evict_g(const EvictArgs& e, hipStream_t st) {
-  hipLaunchKernelGGL((k_evict_scores<T, D, GM>), dim3(e.n_heads * e.nslice), dim3(kEvThreads), 0, st, e);
-  if (e.nslice > 1)
-    hipLaunchKernelGGL((k_evict_select<T, D, GM>), dim3(e.n_heads), dim3(kSelThreads), 0, st, e);
+  if (e.fused) {
+    constexpr int NW = ev_waves<T, GM, true>();
+    hipLaunchKernelGGL((k_evict_attn<T, D, GM, NW, true>), dim3(e.nwg), dim3(NW * kWave), 0, st, e);
+    hipLaunchKernelGGL((k_evict_finish<T, D, GM>), dim3(e.n_heads), dim3(kFinWaves * kWave), 0, st, e);
+  } else {
+    constexpr int NW = ev_waves<T, GM, false>();
+    hipLaunchKernelGGL((k_evict_attn<T, D, GM, NW, false>), dim3(e.n_heads), dim3(NW * kWave), 0, st, e);
+  }
   return hipGetLastError();
 }
 
@@ -510,6 +1127,7 @@ static hipError_t launch_evict_t(const EvictArgs& e, hipStream_t st) {
 }
 
 hipError_t launch_evict(const EvictArgs& e, bool bf16, int d, hipStream_t st) {
+  if (e.fused && (e.nwg < 1 || e.maxslots < 1 || e.maxslots > kMaxSlices)) return hipErrorInvalidValue;
   if (bf16) return d == 64 ? launch_evict_t<bf16_t, 64>(e, st) : launch_evict_t<bf16_t, 128>(e, st);
   return d == 64 ? launch_evict_t<float, 64>(e, st) : launch_evict_t<float, 128>(e, st);
 }

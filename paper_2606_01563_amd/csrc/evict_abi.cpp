@@ -1,10 +1,10 @@
-// C ABI of the decode step with eviction: argument checks, workspace layout (the decode
-// layout followed by the per-row score records) and the launch sequence.  Nothing here
-// allocates, frees or synchronises.
+// C ABI of the decode step with eviction: argument checks, workspace layout and the
+// launches.  Nothing here allocates, frees or synchronises.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 
@@ -18,44 +18,62 @@ using namespace mkv::abi;
 namespace {
 
 // ------------------------------------------------------------------ decode + eviction
-// Workspace: the decode layout (its flag first), then the per-row score records.  Scoring
-// workgroups: slices of a multiple of 32 rows (at least 128), as many per head as keep
-// the busiest CU's work lowest (a CU's scoring throughput is shared by the workgroups it
-// holds), counting each workgroup's forming of S_tilde as 96 rows and, with more than
-// one slice per head, the separate selection launch as 384.
-mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws,
-                            size_t* total, mkv::DecodeArgs* da) {
-  size_t dec = 0;
-  *da = decode_layout(p, ws, &dec);
+// Two launch shapes.  Fused (one read of the cache; from kFusedMinLen rows, or whenever
+// n_split > 0): the scoring launch has one workgroup per CU of the target (kCUs; n_split
+// per head when n_split > 0), each taking an equal contiguous share of the flattened
+// (head, 32-row block) range, so that a head has at most maxslots partial states (at most
+// evict_max_slices(); fewer workgroups otherwise); a finishing launch follows.  Short
+// caches: scoring and selection with one workgroup per head (two per CU), then the decode
+// launches on the new state; a fused workgroup holds one head's summary and V tiles
+// alone on its CU, which there costs more than the second read of a short cache.
+// Workspace: the flag first, then the score records and the per-block running maxima;
+// fused: the heads' partial states; otherwise the decode workspace (which starts with the
+// same flag).
+constexpr int kCUs = 256;
+constexpr int kFusedMinLen = 769;
+
+mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws, size_t* total,
+                            mkv::DecodeArgs* da) {
   mkv::EvictArgs e;
   std::memset(&e, 0, sizeof e);
-  e.n_heads = da->n_heads;
-  e.G = da->G;
+  e.n_heads = p->batch * p->n_kv_heads;
+  e.G = p->n_q_heads / p->n_kv_heads;
   e.cap = p->cap;
   e.max_len = p->max_len;
   e.budget = budget;
-  e.scale = da->scale;
-  e.tau = da->tau;
-  e.flag = da->flag;
-  constexpr int64_t kCUs = 256, kBuildRows = 96, kSelectRows = 384;
-  int best = 1;
-  int64_t best_cost = INT64_MAX;
-  for (int ns = 1; ns <= std::max(1, p->max_len / 128); ++ns) {
-    const int64_t rows = (int64_t)ceil_div(ceil_div(p->max_len, ns), 32) * 32;
-    const int64_t cost = ((int64_t)e.n_heads * ns + kCUs - 1) / kCUs * (rows + kBuildRows) +
-                         (ns > 1 ? kSelectRows : 0);
-    if (cost < best_cost) {
-      best_cost = cost;
-      best = ns;
-    }
-  }
-  e.slice_len = ceil_div(ceil_div(p->max_len, best), 32) * 32;
-  e.nslice = ceil_div(p->max_len, e.slice_len);
+  e.order = p->order;
+  e.scale = p->scale > 0.f ? p->scale : 1.0f / std::sqrt((float)p->head_dim);
+  e.tau = p->tau;
+  e.hblocks = ceil_div(p->max_len, 32);
+  e.rec_len = 32 * e.hblocks;
+  e.fused = (p->n_split > 0 || p->max_len >= kFusedMinLen) ? 1 : 0;
+  const size_t H = e.n_heads, G = e.G, D = p->head_dim;
   Carver c;
   c.base = static_cast<char*>(ws);
-  c.off = dec;
-  e.rec_len = ceil_div(p->max_len, 32) * 32;
-  e.rec = c.take<float>((size_t)e.n_heads * (e.G + 2) * e.rec_len * sizeof(float));
+  if (e.fused) {
+    const int64_t T = (int64_t)e.n_heads * e.hblocks;
+    int64_t nwg = p->n_split > 0 ? (int64_t)p->n_split * e.n_heads : kCUs;
+    nwg = std::max<int64_t>(1, std::min(nwg, T));
+    auto slots = [&](int64_t n) {
+      const int64_t per = std::max<int64_t>(1, T / n);  // the fewest blocks a workgroup takes
+      return std::min<int64_t>(n, (e.hblocks + per - 1) / per + 1);
+    };
+    while (nwg > 1 && slots(nwg) > mkv::evict_max_slices()) --nwg;
+    e.nwg = (int)nwg;
+    e.maxslots = (int)slots(nwg);
+    e.flag = c.take<int32_t>(sizeof(int32_t));  // zero-filled once by the caller
+  } else {
+    size_t dec = 0;
+    *da = decode_layout(p, ws, &dec);
+    c.off = dec;
+    e.flag = da->flag;
+  }
+  e.rec = c.take<float>(H * (G + 2) * e.rec_len * sizeof(float));
+  e.blkm = c.take<float>(H * (G + 1) * e.hblocks * sizeof(float));
+  if (e.fused) {
+    e.part_o = c.take<float>(H * e.maxslots * G * D * sizeof(float));
+    e.part_ml = c.take<float>(H * e.maxslots * G * 2 * sizeof(float));
+  }
   *total = c.off;
   return e;
 }
@@ -119,9 +137,14 @@ mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, con
   e.s_v = s_v;
   e.S = S;
   e.evicted = evicted_out;
+  e.out = out;
+  e.lse_out = lse_out;
+  e.w_r_out = w_r_out;
   const hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t err = mkv::launch_evict(e, p->dtype == MKV_BF16, p->head_dim, hs);
   if (err != hipSuccess) return MKV_ERR_HIP;
+  if (e.fused) return MKV_OK;
+  // the corrected attention over the new state
   da.q = q;
   da.k_cache = k_cache;
   da.v_cache = v_cache;

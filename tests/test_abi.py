@@ -191,8 +191,9 @@ def evict_status(p, budget, ptr=1 << 20, ws=1 << 40, ws_bytes=None, drop=None):
 def test_decode_evict_sizes_and_validation(L):
     p = dparams()
     size = mk.momentkv_decode_evict_workspace_size(p)
-    # the decode workspace plus (G + 1) fp32 records per row of every head
-    assert size >= mk.momentkv_decode_workspace_size(p) + 36 * 8 * 5 * 640 * 4
+    # per head: (G + 2) fp32 record planes of max_len rows and (G + 1) running maxima per
+    # 32-row block, after the 256-byte flag
+    assert size >= 256 + 36 * 8 * (6 * 640 + 5 * 20) * 4
     assert mk.momentkv_decode_evict_workspace_size(dparams(summary=1)) == 0
     assert evict_status(p, 0) == BUDGET
     assert evict_status(dparams(summary=1), 512) == SHAPE

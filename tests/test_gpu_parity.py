@@ -6,6 +6,7 @@ while spanning many 64-token tiles and a ragged tail; the full-size cases check 
 heads.  See tests/parity_util.py for the protocol and tolerances.
 """
 import math
+import types
 
 import numpy as np
 import pytest
@@ -495,6 +496,45 @@ def test_evict_group_sizes_and_long_caches(G, budget):
     worst, swaps, n = P.run_evict_steps(gpu, out, 2, budget)
     announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
     assert n == 4
+
+
+@pytest.mark.parametrize("n_split", [1, 3])
+@pytest.mark.parametrize("gap,exact", [(5.0, False), (7.5, False), (12.0, True), (40.0, True)])
+def test_evict_row_that_holds_most_of_the_attention(gap, exact, n_split):
+    """The evicted row is one the summary predicts, and its key sits `gap` logits above the
+    rest for every query (G = 4, fp32 caches, one workgroup per head or three slices).
+    Predicted: v_j = v_bar + scale / n_e S_tilde k_j up to fp32 rounding; or exactly, with
+    a summary of zero values (S_tilde = v_bar = 0) and v_j = 0.  At gap 5 the row holds
+    about half of each query's mass and at 7.5 about 92%: its term leaves the accumulated
+    attention in place.  At 12 (99.9%) and 40 (all but ~1e-17) too little would remain,
+    and the attention over the new cache is computed again."""
+    d, G, n, n_ev, js = 128, 4, 100, 50, 37
+    rng = np.random.default_rng(11)
+    K = rng.standard_normal((n + 1, d))
+    V = rng.standard_normal((n + 1, d))
+    ke, ve = rng.standard_normal((n_ev, d)), rng.standard_normal((n_ev, d))
+    if exact:
+        ve[:] = 0.0
+    s_k, s_v, S = ke.sum(0), ve.sum(0), ve.T @ ke
+    q0 = rng.standard_normal(d)
+    Q = q0 + 0.1 * rng.standard_normal((G, d))
+    scale = 1.0 / math.sqrt(d)
+    K[js] = (gap * math.sqrt(d) * q0 / (q0 @ q0)).astype(np.float32)
+    st = S - np.outer(s_v, s_k) / n_ev
+    V[js] = (s_v / n_ev + scale / n_ev * st @ K[js]).astype(np.float32)
+    f32 = lambda a: torch.tensor(np.asarray(a, np.float32)).cuda()
+    comp = types.SimpleNamespace(k_out=f32(K)[None, None], v_out=f32(V)[None, None],
+                                 lens=torch.tensor([[n]], dtype=torch.int32).cuda(),
+                                 n_e=torch.tensor([[n_ev]], dtype=torch.int32).cuda(),
+                                 s_k=f32(s_k)[None, None], s_v=f32(s_v)[None, None],
+                                 S=f32(S)[None, None])
+    inp = {"k": comp.k_out, "q_win": torch.zeros(1, G, 1, d).cuda(),
+           "q_dec": f32(Q)[None, None], "k_new": f32(rng.standard_normal(d))[None, None, None],
+           "v_new": f32(rng.standard_normal(d))[None, None, None]}
+    announce(f"evict dominant row gap={gap} exact={exact} n_split={n_split}")
+    worst, swaps, nev = P.run_evict_steps(inp, comp, 1, n, n_split=n_split)
+    announce(f"worst rel err {worst:.2e}")
+    assert nev == 1 and swaps == 0
 
 
 # ---------------------------------------------------------------- head-adaptive budgets
