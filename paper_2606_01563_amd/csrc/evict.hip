@@ -256,6 +256,7 @@ struct EvAttn {
     }
     // online softmax over the 32 rows
     float alpha[4];
+    bool grew = false;
     const int ja = j0 + p2;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -273,22 +274,37 @@ struct EvAttn {
         pa = fast_exp2(xa - mn);
         pb = fast_exp2(xb - mn);
       }
+      grew |= mn != m_run[i];
       l_run[i] = l_run[i] * alpha[i] + row16_sum(pa + pb);
       m_run[i] = mn;
       if (g < GM) {
-        sp[g][p2] = from_f<T>(pa);
-        sp[g][p2 + 1] = from_f<T>(pb);
+        if constexpr (sizeof(T) == 2) {
+          *reinterpret_cast<uint32_t*>(&sp[g][p2]) = bf16_pair(pa, pb);
+        } else {
+          sp[g][p2] = pa;
+          sp[g][p2 + 1] = pb;
+        }
       }
     }
     wave_lds_order();  // P and V^T are in LDS before they are read back
-    // O = alpha O + P . V (A = P rows g, B = V^T)
+    // O = alpha O + P . V (A = P rows g, B = V^T); alpha is exactly 1 where no running
+    // max grew, so the rescale is skipped when none did in the whole wave
+    const bool rescale = __any(grew);
     const FragT pfr = (r16 < G) ? load_frag(&sp[min(r16, GM - 1)][8 * q4]) : zero_frag<T>();
 #pragma unroll
     for (int nt = 0; nt < NOT; ++nt) {
+      if (rescale) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
+        for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
+      }
       mma(oacc[nt], pfr, load_frag(&vt[16 * nt + r16][8 * q4]));
     }
+  }
+
+  // A weight as the P tile holds it (rounded to the element type).
+  static __device__ __forceinline__ float p_held(float p) {
+    if constexpr (sizeof(T) == 2) return __uint_as_float(bf16_pair(p, 0.f) << 16);
+    else return p;
   }
 
   // Running max of query 4 (l / 16) + (l % 4) (the same in the 16 lanes of a row).
@@ -379,11 +395,13 @@ __device__ __forceinline__ int s_at(int row, int col) {
 // choice (the summary S, s_k, s_v, the last row, the first batch of score records) is
 // requested before any of it is used, and everything that depends only on the choice
 // (the evicted row, its logits and its block's running maxima) in one round trip.
-template <class T, int D, int GM, int NW, int RW, bool ATTN>
-__device__ void select_finish(const EvictArgs& e, int head, int old_len, QState<GM, NW, D>& qs,
+// pre(qs) runs once those first requests are out (the finishing launch combines the
+// partial states there).
+template <class T, int D, int GM, int NW, int RW, bool ATTN, class Pre>
+__device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int old_len, QState<GM, NW, D>& qs,
                               SelLds<GM, NW, D>& sl, typename EvAttn<T, D, GM>::VtTile* vt,
                               typename EvAttn<T, D, GM>::PTile* sp, float* ml, const T* s_q,
-                              float* s_S) {
+                              float* s_S, Pre&& pre) {
   typedef EvAttn<T, D, GM> EA;
   typedef typename EA::FragT FragT;
   constexpr int NT = NW * kWave, KS = D / 32, CPL = D / 64, QRS = EA::QRS;
@@ -422,22 +440,24 @@ __device__ void select_finish(const EvictArgs& e, int head, int old_len, QState<
     kl = kc[(size_t)last * D + tid];
     vl = vc[(size_t)last * D + tid];
   }
+  float x[UB][GM], y[UB];
+  auto load_batch = [&](int base) {
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int j = base + tid + NT * u;
+      const bool ok = j < n_tok;
+#pragma unroll
+      for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
+      y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
+    }
+  };
+  if (evicts) load_batch(0);
+  pre(qs);  // the caller's own requests and work, while these are in flight
   if (tid == 0) sl.redo = 0;
 
   int js = -1;
   if (evicts) {
     if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
-    float x[UB][GM], y[UB];
-    auto load_batch = [&](int base) {
-#pragma unroll
-      for (int u = 0; u < UB; ++u) {
-        const int j = base + tid + NT * u;
-        const bool ok = j < n_tok;
-#pragma unroll
-        for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
-        y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
-      }
-    };
     const int step = UB * NT;
     const int nb = (n_tok + step - 1) / step;
 
@@ -446,7 +466,7 @@ __device__ void select_finish(const EvictArgs& e, int head, int old_len, QState<
 #pragma unroll
     for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
     for (int b = 0; b < nb; ++b) {
-      load_batch(b * step);
+      if (b > 0) load_batch(b * step);
 #pragma unroll
       for (int u = 0; u < UB; ++u)
 #pragma unroll
@@ -615,7 +635,7 @@ __device__ void select_finish(const EvictArgs& e, int head, int old_len, QState<
         const float pj = fast_exp2(xj[k] - mbj[k]);
         if (pj > 0.f) {
           const float s = fast_exp2(mbj[k] - qs.M[k]);
-          const float pl = pj * s, po = to_f<T>(from_f<T>(pj)) * s;
+          const float pl = pj * s, po = EA::p_held(pj) * s;
           const float l2 = qs.l[k] - pl;
 #pragma unroll
           for (int c = 0; c < CPL; ++c) qs.o[k][c] = fmaf(-po, sl.kv[1][lane * CPL + c], qs.o[k][c]);
@@ -999,7 +1019,7 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
     __syncthreads();
     QState<GM, NW, D> none;
     select_finish<T, D, GM, NW, NW, false>(e, head, old_len, none, L.sel, nullptr, nullptr, nullptr,
-                                           L.q, nullptr);
+                                           L.q, nullptr, [](QState<GM, NW, D>&) {});
   }
 }
 
@@ -1037,7 +1057,7 @@ __global__ void __launch_bounds__(NW * kWave, ATTN ? 1 : 2) k_evict_attn(EvictAr
 template <class T, int D, int GM>
 __global__ void __launch_bounds__(kFinWaves * kWave, 2) k_evict_finish(EvictArgs e) {
   typedef FinLds<T, D, GM> LT;
-  constexpr int NT = kFinWaves * kWave, CPL = D / 64, SUB = 16;
+  constexpr int NT = kFinWaves * kWave, CPL = D / 64, SUB = 8;
   static_assert(sizeof(LT) <= 160 * 1024, "LDS of the finishing workgroup");
   static_assert(sizeof(T) == 4 || sizeof(LT) <= 80 * 1024, "two bf16 finishing workgroups per CU");
   __shared__ __align__(16) LT L;
@@ -1050,53 +1070,55 @@ __global__ void __launch_bounds__(kFinWaves * kWave, 2) k_evict_finish(EvictArgs
 
   QueryRows<T, D, NT> qr;
   qr.load(e, head);
-  // the partial states per query, combined in order; every load is issued before the
-  // first is used (partial indices clamped to the count)
-  QState<GM, kFinWaves, D> qs;
+  // the partial states per query, combined in order once the selection's first requests
+  // are out; every load is issued before the first is used (partial indices clamped to
+  // the count)
+  auto combine = [&](QState<GM, kFinWaves, D>& qs) {
 #pragma unroll
-  for (int k = 0; k < QState<GM, kFinWaves, D>::KQ; ++k) {
-    const int g = min(wave + kFinWaves * k, G - 1);  // waves past G: loads never used
-    const size_t base = (size_t)head * e.maxslots;
-    auto o_at = [&](int s, int c) {
-      return e.part_o + ((base + min(s, ns - 1)) * G + g) * D + lane * CPL + c;
-    };
-    const float2 ml = *reinterpret_cast<const float2*>(e.part_ml + ((base + min(lane, ns - 1)) * G + g) * 2);
-    float ov[SUB][CPL];
+    for (int k = 0; k < QState<GM, kFinWaves, D>::KQ; ++k) {
+      const int g = min(wave + kFinWaves * k, G - 1);  // waves past G: loads never used
+      const size_t base = (size_t)head * e.maxslots;
+      auto o_at = [&](int s, int c) {
+        return e.part_o + ((base + min(s, ns - 1)) * G + g) * D + lane * CPL + c;
+      };
+      const float2 ml = *reinterpret_cast<const float2*>(e.part_ml + ((base + min(lane, ns - 1)) * G + g) * 2);
+      float ov[SUB][CPL];
 #pragma unroll
-    for (int u = 0; u < SUB; ++u)
+      for (int u = 0; u < SUB; ++u)
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) ov[u][c] = *o_at(u, c);
-    const bool live = lane < ns;
-    const float M = wave_max(live ? ml.x : -INFINITY);
-    const float w = (live && M != -INFINITY) ? fast_exp2(ml.x - M) : 0.f;
-    qs.M[k] = M;
-    qs.l[k] = wave_sum(live ? ml.y * w : 0.f);
-    float o[CPL];
+        for (int c = 0; c < CPL; ++c) ov[u][c] = *o_at(u, c);
+      const bool live = lane < ns;
+      const float M = wave_max(live ? ml.x : -INFINITY);
+      const float w = (live && M != -INFINITY) ? fast_exp2(ml.x - M) : 0.f;
+      qs.M[k] = M;
+      qs.l[k] = wave_sum(live ? ml.y * w : 0.f);
+      float o[CPL];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) o[c] = 0.f;
-    for (int s0 = 0; s0 < ns; s0 += SUB) {
-      if (s0 > 0) {
+      for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+      for (int s0 = 0; s0 < ns; s0 += SUB) {
+        if (s0 > 0) {
 #pragma unroll
-        for (int u = 0; u < SUB; ++u)
+          for (int u = 0; u < SUB; ++u)
 #pragma unroll
-          for (int c = 0; c < CPL; ++c) ov[u][c] = *o_at(s0 + u, c);
-      }
+            for (int c = 0; c < CPL; ++c) ov[u][c] = *o_at(s0 + u, c);
+        }
 #pragma unroll
-      for (int u = 0; u < SUB; ++u) {
-        if (s0 + u < ns) {
-          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
+        for (int u = 0; u < SUB; ++u) {
+          if (s0 + u < ns) {
+            const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
 #pragma unroll
-          for (int c = 0; c < CPL; ++c) o[c] = fmaf(wu, ov[u][c], o[c]);
+            for (int c = 0; c < CPL; ++c) o[c] = fmaf(wu, ov[u][c], o[c]);
+          }
         }
       }
-    }
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) qs.o[k][c] = o[c];
-  }
-  qr.store(L.q);
-  __syncthreads();
+      for (int c = 0; c < CPL; ++c) qs.o[k][c] = o[c];
+    }
+    qr.store(L.q);  // read after the selection's barriers
+  };
+  QState<GM, kFinWaves, D> qs;
   select_finish<T, D, GM, kFinWaves, kFinWaves, true>(e, head, old_len, qs, L.sel, L.u.r.vt,
-                                                      L.u.r.sp, L.ml, L.q, L.u.S);
+                                                      L.u.r.sp, L.ml, L.q, L.u.S, combine);
 }
 
 int evict_waves(bool bf16, int G) {
