@@ -804,14 +804,14 @@ template <class T, int D, int GM, int NW> struct EvLds<T, D, GM, NW, true> {
   typename EA::VtTile vt[NW];  // per wave; after a segment, the wave's o rows
   typename EA::PTile sp[NW];
   T q[16 * EA::QRS];
-  float vbar[D];
+  float vinit[D];             // s_v / scale: the start of the S_tilde k accumulators
   float ml[NW * 2 * GM];
 };
 template <class T, int D, int GM, int NW> struct EvLds<T, D, GM, NW, false> {
   typedef EvAttn<T, D, GM> EA;
   SumLds<T, D> sm;
   T q[16 * EA::QRS];
-  float vbar[D];
+  float vinit[D];             // s_v / scale: the start of the S_tilde k accumulators
   SelLds<GM, NW, D> sel;
 };
 
@@ -910,8 +910,10 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
     const float svv = threadIdx.x < D ? e.s_v[(size_t)head * D + threadIdx.x] : 0.f;
     if (evicts) build_summary<T, D, NT>(e, head, L.sm);
     qr.store(L.q);
+    // r_j = v_j - cf (v_bar / cf + S_tilde k_j): the accumulators of S_tilde k_j start at
+    // v_bar / cf = s_v / scale, so the mean comes out of the MFMAs
     const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
-    if (threadIdx.x < D) L.vbar[threadIdx.x] = ne > 0 ? svv / (float)ne : 0.f;
+    if (threadIdx.x < D) L.vinit[threadIdx.x] = ne > 0 ? svv / e.scale : 0.f;
     __syncthreads();  // S_tilde, v_bar and the queries are in LDS
 
     EA at;
@@ -937,7 +939,15 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
         for (int t = 0; t < NTI; ++t) {
           const int c = t >> 1, s = t & 1;
           const int row = 32 * c + 8 * (r16 >> 2) + 4 * s + (r16 & 3);
-          f32x4 ta[2] = {zero4(), zero4()};
+          const float4 vb4 = *reinterpret_cast<const float4*>(&L.vinit[32 * c + 8 * q4 + 4 * s]);
+          f32x4 ta[2];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            ta[hh][0] = vb4.x;
+            ta[hh][1] = vb4.y;
+            ta[hh][2] = vb4.z;
+            ta[hh][3] = vb4.w;
+          }
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) {
             if constexpr (sizeof(T) == 2) {
@@ -955,14 +965,12 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
               for (int hh = 0; hh < 2; ++hh) mma(ta[hh], af, kf[hh][ks]);
             }
           }
-          const float4 vb4 = *reinterpret_cast<const float4*>(&L.vbar[32 * c + 8 * q4 + 4 * s]);
-          const float vbv[4] = {vb4.x, vb4.y, vb4.z, vb4.w};
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float r = elem_f(vf[hh][c], 4 * s + i) - vbv[i] - cf * ta[hh][i];
-              rr[hh] += r * r;
+              const float r = fmaf(-cf, ta[hh][i], elem_f(vf[hh][c], 4 * s + i));
+              rr[hh] = fmaf(r, r, rr[hh]);
             }
           // one tile's LDS reads in flight at a time: hoisting all of them would not fit
           __builtin_amdgcn_sched_barrier(0);
