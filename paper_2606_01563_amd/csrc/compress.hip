@@ -1182,12 +1182,15 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) k_residual(Compre
       }
     }
   }
-  // v_bar0 for this lane's result rows: 16*(MTPW*wave + m) + 4*(lane/16) + i
+  // r = v - coef (v_bar0 / coef + S_tilde0 k): the accumulators start at v_bar0 / coef =
+  // s_v0 / scale for this lane's result rows 16*(MTPW*wave + m) + 4*(lane/16) + i, so the
+  // mean comes out of the MFMAs
   float vb[MTPW][4];
 #pragma unroll
   for (int m = 0; m < MTPW; ++m)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) vb[m][i] = sSv[16 * (MTPW * wave + m) + 4 * (lane >> 4) + i] * inv_n;
+    for (int i = 0; i < 4; ++i)
+      vb[m][i] = n0 > 0.f ? sSv[16 * (MTPW * wave + m) + 4 * (lane >> 4) + i] / a.scale : 0.f;
 
   for (int t = t_beg; t < t_end; ++t) {
 #pragma unroll
@@ -1209,7 +1212,9 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) k_residual(Compre
     for (int m = 0; m < MTPW; ++m) {
       f32x4 acc[4];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[nt] = zero4();
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[nt][i] = vb[m][i];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
@@ -1223,8 +1228,8 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) k_residual(Compre
         load4(&sV[16 * nt + (lane & 15)][a0], v);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float r = v[i] - vb[m][i] - coef * acc[nt][i];
-          rho[nt] += r * r;
+          const float r = fmaf(-coef, acc[nt][i], v[i]);
+          rho[nt] = fmaf(r, r, rho[nt]);
         }
       }
     }
