@@ -429,34 +429,39 @@ def test_evict_llama_layer_bf16_launch_shapes(n_split):
     assert n == 10 * 16 and swaps <= n // 50
 
 
+@pytest.mark.parametrize("n_split", [0, 2])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("d", [64, 128])
-def test_evict_budgets_and_lengths_around_the_bound(dtype, d):
-    """Rows over several 128-row scoring slices with a ragged tail, G = 4; per-head
-    lengths below the budget (no eviction: the step is the decode with the append), at it
-    (steady state) and one row over it (flag bit 3, length kept)."""
+def test_evict_budgets_and_lengths_around_the_bound(dtype, d, n_split):
+    """Rows over several 32-row blocks with a ragged tail, G = 4; per-head lengths below
+    the budget (no eviction: the step is the decode with the append), at it (steady state)
+    and one row over it (flag bit 3, length kept).  n_split 0: scoring and selection, then
+    the decode launches; 2: one read of the cache over two scoring workgroups per head."""
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=d, ctx_len=1200,
                          batch=2, n_q_heads=8, n_kv_heads=2, window=16, budgets=(290,))
     out = P.run_compress(gpu, 290, cap=293)
-    announce(f"evict dtype={dtype} d={d}")
-    P.run_evict_steps(gpu, out, 3, 290)                                   # steady state
-    P.run_evict_steps(gpu, out, 3, 292, start=([[290, 289], [260, 1]], out.n_e.cpu()))
-    P.run_evict_steps(gpu, out, 2, 289, flag=8)                           # above budget
+    announce(f"evict dtype={dtype} d={d} n_split={n_split}")
+    P.run_evict_steps(gpu, out, 3, 290, n_split=n_split)                  # steady state
+    P.run_evict_steps(gpu, out, 3, 292, start=([[290, 289], [260, 1]], out.n_e.cpu()),
+                      n_split=n_split)
+    P.run_evict_steps(gpu, out, 2, 289, flag=8, n_split=n_split)         # above budget
 
 
-def test_evict_with_empty_summary_scores_alpha_times_value_norm():
+@pytest.mark.parametrize("n_split", [0, 1])
+def test_evict_with_empty_summary_scores_alpha_times_value_norm(n_split):
     """Budget above the context keeps every token, so n_e = 0: the first evictions use
-    v_bar = S_tilde = 0 and later ones the summary they build."""
+    v_bar = S_tilde = 0 and later ones the summary they build (both launch shapes)."""
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=6, dtype=torch.bfloat16, head_dim=128,
                          ctx_len=700, batch=1, n_q_heads=4, n_kv_heads=2, window=16,
                          budgets=(900,))
     out = P.run_compress(gpu, 900, cap=701)
     assert int(out.n_e.max()) == 0 and int(out.lens.min()) == 700
-    worst, swaps, n = P.run_evict_steps(gpu, out, 6, 700)
+    worst, swaps, n = P.run_evict_steps(gpu, out, 6, 700, n_split=n_split)
     assert n == 12
 
 
-def test_evict_full_cache_sets_flag_and_keeps_state():
+@pytest.mark.parametrize("n_split", [0, 1])
+def test_evict_full_cache_sets_flag_and_keeps_state(n_split):
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, dtype=torch.bfloat16, head_dim=64,
                          ctx_len=600, batch=1, n_q_heads=4, n_kv_heads=1, window=16,
                          budgets=(100,))
@@ -465,11 +470,19 @@ def test_evict_full_cache_sets_flag_and_keeps_state():
     n_e, s_k, s_v, S = out.n_e.clone(), out.s_k.clone(), out.s_v.clone(), out.S.clone()
     ev = torch.empty_like(lens)
     res, _, _, _, ws = mk.momentkv_decode_evict(gpu["q_dec"][0], kc, vc, lens, n_e, s_k, s_v, S,
-                                                gpu["k_new"][0], gpu["v_new"][0], 99)
+                                                gpu["k_new"][0], gpu["v_new"][0], 99,
+                                                n_split=n_split)
     torch.cuda.synchronize()
     assert int(ws[:4].view(torch.int32)[0]) & 1
     assert torch.equal(lens, out.lens) and torch.equal(n_e, out.n_e) and torch.equal(S, out.S)
     assert torch.equal(kc, out.k_out)
+    # the output is the corrected attention over the full cache, without the new token
+    moments = [[O.Moments(int(out.n_e[0, 0]), P.h64(out.s_k[0, 0]), P.h64(out.s_v[0, 0]),
+                          P.h64(out.S[0, 0]))]]
+    ref = O.decode(P.h64(gpu["q_dec"][0]), P.h64(out.k_out), P.h64(out.v_out),
+                   out.lens.cpu().numpy(), moments)[0]
+    got = P.h64(res)
+    assert max(P.rel_l2(got[0, g], ref[0, g]) for g in range(4)) <= P.TOL[torch.bfloat16]
 
 
 def test_evict_qwen_stack_layer_full_size_budget_2048():
