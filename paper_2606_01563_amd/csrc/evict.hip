@@ -392,9 +392,10 @@ __device__ __forceinline__ int s_at(int row, int col) {
 // token); vt / sp / ml: LDS for RW waves to compute the attention again; s_q: the query
 // rows in LDS; s_S: LDS for the updated S (D x D floats; it may share the space of vt,
 // which is no longer used when S is written).  Everything that does not depend on the
-// choice (the summary S, s_k, s_v, the last row, the first batch of score records) is
-// requested before any of it is used, and everything that depends only on the choice
-// (the evicted row, its logits and its block's running maxima) in one round trip.
+// choice (s_k, s_v, the last row, the first batch of score records) is requested before
+// any of it is used, and the summary S with everything that depends only on the choice
+// (the evicted row, its logits and its block's running maxima) in one round trip; S is
+// held in registers only from there on.
 // pre(qs) runs once those first requests are out (the finishing launch combines the
 // partial states there).
 template <class T, int D, int GM, int NW, int RW, bool ATTN, class Pre>
@@ -423,12 +424,9 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
   T* vc = reinterpret_cast<T*>(e.v_cache) + (size_t)head * e.cap * D;
   float4* Sh = reinterpret_cast<float4*>(e.S + (size_t)head * D * D);
 
-  // requests independent of the choice
+  // requests independent of the choice (S follows with those that depend on it: held
+  // in registers only from there on)
   float4 s4[SCH];
-  if (ATTN || evicts) {
-#pragma unroll
-    for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * u];
-  }
   float skv = 0.f, svv = 0.f;
   if (tid < D) {
     skv = e.s_k[(size_t)head * D + tid];
@@ -441,14 +439,21 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
     vl = vc[(size_t)last * D + tid];
   }
   float x[UB][GM], y[UB];
+  // records of rows base + tid + NT u (every load issued, from a valid row; rows past
+  // n_tok and padded query slots then read as -inf, their norm as +inf)
   auto load_batch = [&](int base) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int j = base + tid + NT * u;
       const bool ok = j < n_tok;
+      const int jc = min(j, max(n_tok - 1, 0));
 #pragma unroll
-      for (int g = 0; g < GM; ++g) x[u][g] = (ok && g < G) ? rec[(size_t)g * ML + j] : -INFINITY;
-      y[u] = ok ? rec[(size_t)G * ML + j] : INFINITY;
+      for (int g = 0; g < GM; ++g) {
+        const float v = rec[(size_t)min(g, G - 1) * ML + jc];
+        x[u][g] = (ok && g < G) ? v : -INFINITY;
+      }
+      const float v = rec[(size_t)G * ML + jc];
+      y[u] = ok ? v : INFINITY;
     }
   };
   if (evicts) load_batch(0);
@@ -461,22 +466,25 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
     const int step = UB * NT;
     const int nb = (n_tok + step - 1) / step;
 
-    // log2 Z_g over the n_tok rows
+    // log2 Z_g over the n_tok rows: per batch the thread's max, then its sum (records past
+    // n_tok and padded query slots hold -inf and add nothing; no per-record branch)
     float m[GM], l[GM];
 #pragma unroll
     for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
     for (int b = 0; b < nb; ++b) {
       if (b > 0) load_batch(b * step);
 #pragma unroll
-      for (int u = 0; u < UB; ++u)
+      for (int g = 0; g < GM; ++g) {
+        float mn = m[g];
 #pragma unroll
-        for (int g = 0; g < GM; ++g) {
-          const float mn = fmaxf(m[g], x[u][g]);
-          if (mn != -INFINITY) {
-            l[g] = l[g] * fast_exp2(m[g] - mn) + fast_exp2(x[u][g] - mn);
-            m[g] = mn;
-          }
-        }
+        for (int u = 0; u < UB; ++u) mn = fmaxf(mn, x[u][g]);
+        const float base = mn == -INFINITY ? 0.f : mn;
+        float sum = 0.f;
+#pragma unroll
+        for (int u = 0; u < UB; ++u) sum += fast_exp2(x[u][g] - base);
+        l[g] = l[g] * fast_exp2(m[g] - base) + sum;
+        m[g] = mn;
+      }
     }
 #pragma unroll
     for (int g = 0; g < GM; ++g) {
@@ -512,13 +520,14 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
         const int j = b * step + tid + NT * u;
         float mx = -INFINITY;
 #pragma unroll
-        for (int g = 0; g < GM; ++g) mx = fmaxf(mx, g < G ? x[u][g] - lz[g] : -INFINITY);
+        for (int g = 0; g < GM; ++g) mx = fmaxf(mx, x[u][g] - lz[g]);  // -inf past G
         float sm = 0.f;
 #pragma unroll
-        for (int g = 0; g < GM; ++g)
-          if (g < G) sm += fast_exp2(x[u][g] - lz[g] - mx);
+        for (int g = 0; g < GM; ++g) sm += fast_exp2(x[u][g] - lz[g] - mx);
         const float sc = mx + log2f(sm) - log2_g + y[u];
-        if (j < n_tok && sc < best) { best = sc; bj = j; }  // rows rise along a thread
+        const bool better = j < n_tok && sc < best;  // rows rise along a thread
+        best = better ? sc : best;
+        bj = better ? j : bj;
       }
     }
 #pragma unroll
@@ -542,8 +551,12 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
     if (js < 0 || js >= n_tok) js = -1;  // no comparable score (non-finite inputs)
   }
 
-  // requests that depend on the choice: the evicted row, and per query handled here its
-  // logit and its block's running max
+  // requests that depend on the choice: S (to be updated, or for S_tilde q), the evicted
+  // row, and per query handled here its logit and its block's running max
+  if (ATTN || js >= 0) {
+#pragma unroll
+    for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * u];
+  }
   float kf = 0.f, vf = 0.f, xj[KQ], mbj[KQ];
   if (js >= 0) {
     if (tid < D) {
