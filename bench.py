@@ -336,12 +336,13 @@ def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, ou
     achieved = all_bytes / (total * 1e-3) / 1e9
     return {"what": "per token and budget one momentkv_decode_evict call over the 36 "
                     "caches: append, Phase 1 eviction, Phase 2 corrected attention; cache "
-                    "kept at the budget.  Budgets up to 768: k_evict_attn scoring and "
-                    "selection, then the decode launches; above: k_evict_attn scoring and "
-                    "attention in one read of the cache, then k_evict_finish",
+                    "kept at the budget.  Budgets up to 768: one k_evict_attn launch that "
+                    "scores, selects, updates and attends to the new cache; above: "
+                    "k_evict_attn scoring and attention in one read of the cache, then "
+                    "k_evict_finish",
             "ms_per_step": total, "tokens_per_s": wl.batch * T * len(budgets) / (total * 1e-3),
             "per_budget": per_budget,
-            "roofline": {"kernel": "momentkv_decode_evict call (2-3 launches)", "bound": "hbm",
+            "roofline": {"kernel": "momentkv_decode_evict call (1-2 launches)", "bound": "hbm",
                          "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                          "bytes_per_call": all_bytes / (T * len(budgets)),

@@ -263,9 +263,9 @@ size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);
  *           max_len >= 769 (or n_split > 0) one read of the cache, the attention computed
  *           in the scoring pass over about one workgroup per CU (n_split per KV head when
  *           n_split > 0) and the evicted row's term removed from it afterwards, then a
- *           finishing launch; for shorter caches the scoring and selection with one
- *           workgroup per KV head, then the decode launches of momentkv_decode_attn with
- *           their automatic split.  Results agree within the dtype's tolerance either way
+ *           finishing launch; for shorter caches one launch with one workgroup per KV
+ *           head that scores, selects, updates and then attends to the new cache.
+ *           Results agree within the dtype's tolerance either way
  * budget    rows per KV head kept by Phase 1, >= 1 (MKV_ERR_BUDGET otherwise)
  * q, k_cache, v_cache, lens, out, lse_out, w_r_out: as momentkv_decode_attn; row lens (the
  *           new token) and row j* of the caches are written, lens is updated

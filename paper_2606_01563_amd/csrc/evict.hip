@@ -32,6 +32,10 @@
 //   the attention over the new cache is computed again instead.  Last, S_tilde q from the
 //   updated summary and the correction w_R f_R + (1 - w_R) (v_bar + (scale / n_e)
 //   S_tilde q) with the Jensen estimate of the evicted mass (Eqs. fhat, jensen, fused).
+// Short caches: k_evict_attn without the attention, one workgroup per head (two per CU),
+//   scores the head's rows as above, then selects and finishes as k_evict_finish does,
+//   with the attention over the new cache computed after the update (rows it has just
+//   read, mostly from L2; V^T tiles in the LDS that held S_tilde).
 #include <climits>
 
 #include "mkv_bf16.h"
@@ -553,7 +557,7 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
 
   // requests that depend on the choice: S (to be updated, or for S_tilde q), the evicted
   // row, and per query handled here its logit and its block's running max
-  if (ATTN || js >= 0) {
+  if (ATTN || js >= 0 || e.order >= 1) {
 #pragma unroll
     for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * u];
   }
@@ -613,34 +617,10 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
   const int ne2 = js >= 0 ? ne + 1 : ne;
   __syncthreads();
 
-  if constexpr (!ATTN) {
-    // the attention runs afterwards on the new state: only S is left to update
-    if (js >= 0) {
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        if (ch > 0) {
-#pragma unroll
-          for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * (ch * SCH + u)];
-        }
-#pragma unroll
-        for (int u = 0; u < SCH; ++u) {
-          const int idx = tid + NT * (ch * SCH + u);
-          const int row = idx / (D / 4), c4 = 4 * (idx % (D / 4));
-          const float va = sl.kv[1][row];
-          s4[u].x = fmaf(va, sl.kv[0][c4], s4[u].x);
-          s4[u].y = fmaf(va, sl.kv[0][c4 + 1], s4[u].y);
-          s4[u].z = fmaf(va, sl.kv[0][c4 + 2], s4[u].z);
-          s4[u].w = fmaf(va, sl.kv[0][c4 + 3], s4[u].w);
-          Sh[idx] = s4[u];
-        }
-      }
-    }
-    return;
-  }
   // The evicted row's term leaves the attention state as it was accumulated: p taken at
   // its block's running max mb, scaled to the merged max M (the sum holds p in fp32, the
   // output p rounded to the element type).
-  if (js >= 0) {
+  if (ATTN && js >= 0) {
 #pragma unroll
     for (int k = 0; k < KQ; ++k) {
       const int g = wave + NW * k;
@@ -660,10 +640,11 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
   }
   __syncthreads();
 
-  // the attention over the new cache (rows [0, last)) again when a removal left too
-  // little of some query's sum; RW waves
-  if (__builtin_amdgcn_readfirstlane(sl.redo)) {
-    const int n = last;  // >= budget >= 1
+  // the attention over the new cache (its rows [0, n)) with RW waves: again, when a
+  // removal left too little of some query's sum; without ATTN (no state yet) always
+  if (!ATTN || __builtin_amdgcn_readfirstlane(sl.redo)) {
+    const int n = js >= 0 ? last
+                          : (evicts ? n_tok : (can_append ? old_len + 1 : min(max(old_len, 0), e.cap)));
     const float c2 = e.scale * kLog2e;
     const int r16 = lane & 15, q4 = lane >> 4;
     if (wave < RW) {
@@ -854,7 +835,7 @@ __device__ __forceinline__ int wg_of_block(const EvictArgs& e, int64_t b) {
 // Blocks [s0, s1) of one head by the NW-wave workgroup (see the top of the file).  With
 // ATTN the rows are scored and attended to, and the merged state is written as the
 // head's partial `slot`; without, a head that evicts is scored, and the workgroup (which
-// then holds the whole head) selects at the end.
+// then holds the whole head) selects, updates and attends to the new cache at the end.
 template <class T, int D, int GM, int NW, bool ATTN>
 __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, NW, ATTN>& L, int head,
                                            int s0, int s1, int slot) {
@@ -1036,11 +1017,29 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
   }
   if constexpr (!ATTN) {
     // The workgroup holds the whole head: its records and the appended row are visible
-    // to all of its waves after a barrier; the selection needs no second launch.
+    // to all of its waves after a barrier, and it selects, updates, then attends to the
+    // new cache itself (rows it has just read, mostly from L2), with its V^T tiles where
+    // S_tilde was; no second launch.
+    typedef typename EA::VtTile VtT;
+    typedef typename EA::PTile PtT;
+    constexpr int RW0 = (int)((sizeof(SumLds<T, D>) - NW * 2 * GM * sizeof(float)) / (sizeof(VtT) + sizeof(PtT)));
+    constexpr int RW = RW0 < NW ? RW0 : NW;  // waves that attend (as many as the space holds)
+    static_assert(RW >= 1, "V^T tiles fit in place of S_tilde");
+    static_assert(sizeof(SumLds<T, D>) >= D * D * sizeof(float), "S fits in place of S_tilde");
+    char* base = reinterpret_cast<char*>(&L.sm);
+    VtT* vt = reinterpret_cast<VtT*>(base);
+    PtT* sp = reinterpret_cast<PtT*>(base + RW * sizeof(VtT));
+    float* ml = reinterpret_cast<float*>(base + RW * (sizeof(VtT) + sizeof(PtT)));
+    if (t0 >= t1) {  // a head that does not evict: its queries, for the attention
+      QueryRows<T, D, NT> qr;
+      qr.load(e, head);
+      qr.store(L.q);
+    }
     __syncthreads();
-    QState<GM, NW, D> none;
-    select_finish<T, D, GM, NW, NW, false>(e, head, old_len, none, L.sel, nullptr, nullptr, nullptr,
-                                           L.q, nullptr, [](QState<GM, NW, D>&) {});
+    QState<GM, NW, D> qs;
+    select_finish<T, D, GM, NW, RW, false>(e, head, old_len, qs, L.sel, vt, sp, ml, L.q,
+                                           reinterpret_cast<float*>(&L.sm),
+                                           [](QState<GM, NW, D>&) {});
   }
 }
 
@@ -1052,7 +1051,7 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
 // (queries and S_tilde formed per segment), whose merged state is written as the head's
 // partial number w - (first workgroup of the head).  The head's last block also takes
 // rows past hblocks * 32 (a cache longer than max_len after a full call).  Scoring alone:
-// one workgroup per head, which also selects.
+// one workgroup per head, which also selects, updates and then attends to the new cache.
 template <class T, int D, int GM, int NW, bool ATTN>
 __global__ void __launch_bounds__(NW * kWave, ATTN ? 1 : 2) k_evict_attn(EvictArgs e) {
   typedef EvLds<T, D, GM, NW, ATTN> LT;

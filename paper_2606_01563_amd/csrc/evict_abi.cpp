@@ -11,7 +11,6 @@
 #include "../../include/momentkv.h"
 #include "mkv_abi.h"
 #include "mkv_evict.h"
-#include "mkv_decode.h"
 
 using namespace mkv::abi;
 
@@ -23,17 +22,16 @@ namespace {
 // per head when n_split > 0), each taking an equal contiguous share of the flattened
 // (head, 32-row block) range, so that a head has at most maxslots partial states (at most
 // evict_max_slices(); fewer workgroups otherwise); a finishing launch follows.  Short
-// caches: scoring and selection with one workgroup per head (two per CU), then the decode
-// launches on the new state; a fused workgroup holds one head's summary and V tiles
-// alone on its CU, which there costs more than the second read of a short cache.
+// caches: one launch with one workgroup per head (two per CU) that scores, selects,
+// updates and then attends to the new cache itself (a second read of a short cache,
+// mostly from L2); a fused workgroup holds one head's summary and V tiles alone on its
+// CU, which there costs more than that second read.
 // Workspace: the flag first, then the score records and the per-block running maxima;
-// fused: the heads' partial states; otherwise the decode workspace (which starts with the
-// same flag).
+// fused: then the heads' partial states.
 constexpr int kCUs = 256;
 constexpr int kFusedMinLen = 769;
 
-mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws, size_t* total,
-                            mkv::DecodeArgs* da) {
+mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws, size_t* total) {
   mkv::EvictArgs e;
   std::memset(&e, 0, sizeof e);
   e.n_heads = p->batch * p->n_kv_heads;
@@ -61,13 +59,8 @@ mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws
     while (nwg > 1 && slots(nwg) > mkv::evict_max_slices()) --nwg;
     e.nwg = (int)nwg;
     e.maxslots = (int)slots(nwg);
-    e.flag = c.take<int32_t>(sizeof(int32_t));  // zero-filled once by the caller
-  } else {
-    size_t dec = 0;
-    *da = decode_layout(p, ws, &dec);
-    c.off = dec;
-    e.flag = da->flag;
   }
+  e.flag = c.take<int32_t>(sizeof(int32_t));  // zero-filled once by the caller
   e.rec = c.take<float>(H * (G + 2) * e.rec_len * sizeof(float));
   e.blkm = c.take<float>(H * (G + 1) * e.hblocks * sizeof(float));
   if (e.fused) {
@@ -93,8 +86,7 @@ extern "C" {
 size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p) {
   if (check_evict_params(p, 1) != MKV_OK) return 0;
   size_t total = 0;
-  mkv::DecodeArgs da;
-  evict_layout(p, 1, nullptr, &total, &da);
+  evict_layout(p, 1, nullptr, &total);
   return total;
 }
 
@@ -109,8 +101,7 @@ mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, con
   if (!q || !k_cache || !v_cache || !lens || !k_new || !v_new || !n_e || !s_k || !s_v || !S || !out)
     return MKV_ERR_NULL;
   size_t need = 0;
-  mkv::DecodeArgs da;
-  evict_layout(p, budget, nullptr, &need, &da);
+  evict_layout(p, budget, nullptr, &need);
   if (!workspace || workspace_bytes < need) return MKV_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return MKV_ERR_WORKSPACE;
   const size_t es = elem_size(p->dtype);
@@ -125,7 +116,7 @@ mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, con
       if (ranges_overlap(outs[i], outn[i], outs[j], outn[j])) return MKV_ERR_ALIAS;
   if (ranges_overlap(out, out_bytes, q, out_bytes)) return MKV_ERR_ALIAS;
   size_t total = 0;
-  mkv::EvictArgs e = evict_layout(p, budget, workspace, &total, &da);
+  mkv::EvictArgs e = evict_layout(p, budget, workspace, &total);
   e.q = q;
   e.k_cache = k_cache;
   e.v_cache = v_cache;
@@ -141,25 +132,7 @@ mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, con
   e.lse_out = lse_out;
   e.w_r_out = w_r_out;
   const hipStream_t hs = static_cast<hipStream_t>(stream);
-  hipError_t err = mkv::launch_evict(e, p->dtype == MKV_BF16, p->head_dim, hs);
-  if (err != hipSuccess) return MKV_ERR_HIP;
-  if (e.fused) return MKV_OK;
-  // the corrected attention over the new state
-  da.q = q;
-  da.k_cache = k_cache;
-  da.v_cache = v_cache;
-  da.lens = lens;
-  da.k_new = nullptr;  // appended by the eviction step
-  da.v_new = nullptr;
-  da.n_e = n_e;
-  da.s_k = s_k;
-  da.s_v = s_v;
-  da.S = S;
-  da.out = out;
-  da.lse_out = lse_out;
-  da.w_r_out = w_r_out;
-  err = mkv::launch_decode(da, p->dtype == MKV_BF16, p->head_dim, hs);
-  return err == hipSuccess ? MKV_OK : MKV_ERR_HIP;
+  return mkv::launch_evict(e, p->dtype == MKV_BF16, p->head_dim, hs) == hipSuccess ? MKV_OK : MKV_ERR_HIP;
 }
 
 }  // extern "C"

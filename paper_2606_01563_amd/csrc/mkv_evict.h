@@ -9,8 +9,8 @@ namespace mkv {
 // Decode step with eviction (Algorithm 1: Phase 1, then Phase 2 on the new state).  Fused
 // (one read of the cache): a scoring and attention launch over nwg workgroups that share
 // the heads' 32-row blocks evenly, then a finishing launch with one workgroup per head.
-// Otherwise: scoring and selection with one workgroup per head, after which the caller
-// runs the decode launches on the new state.
+// Otherwise one launch with one workgroup per head: scoring, selection, the update, then
+// the attention over the new cache.
 struct EvictArgs {
   const void* q;            // [B, Hq, D]
   void* k_cache;            // [B, Hkv, cap, D]

@@ -435,8 +435,8 @@ def test_evict_llama_layer_bf16_launch_shapes(n_split):
 def test_evict_budgets_and_lengths_around_the_bound(dtype, d, n_split):
     """Rows over several 32-row blocks with a ragged tail, G = 4; per-head lengths below
     the budget (no eviction: the step is the decode with the append), at it (steady state)
-    and one row over it (flag bit 3, length kept).  n_split 0: scoring and selection, then
-    the decode launches; 2: one read of the cache over two scoring workgroups per head."""
+    and one row over it (flag bit 3, length kept).  n_split 0: one launch that scores,
+    selects, updates and attends to the new cache; 2: one read of the cache over two scoring workgroups per head."""
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=d, ctx_len=1200,
                          batch=2, n_q_heads=8, n_kv_heads=2, window=16, budgets=(290,))
     out = P.run_compress(gpu, 290, cap=293)
