@@ -97,10 +97,12 @@ def build_stack(wl, layers, device):
     return data, time.time() - t0
 
 
-def cpu_baseline(wl, data, budget: int, heads: int, steps: int) -> dict:
-    """The fp64 oracle on the host: compress `heads` KV heads of layer 0 at `budget`, then
-    `steps` decode steps of those heads' query groups.  Scaled to GB/s of decode like
-    `value`; compress time extrapolated per layer."""
+def cpu_baseline(wl, layers_data, budgets, steps: int) -> dict:
+    """The fp64 oracle on the host over a bounded sample of the same workload: every KV head
+    of the given layers, at every budget, compressed, then `steps` decode steps with appends
+    of each (layer, budget) cache, the sequence the GPU decode phase runs.  `value` is the
+    decode phase's algorithmic bytes over its host time (GB/s like the GPU's `value`);
+    compress is reported in ms per layer, measured on whole layers."""
     import numpy as np
     import oracle as O
     try:
@@ -109,37 +111,42 @@ def cpu_baseline(wl, data, budget: int, heads: int, steps: int) -> dict:
     except Exception:  # noqa: BLE001
         blas_threads = 1
     f64 = lambda t: t.float().cpu().double().numpy()  # noqa: E731
-    d, G = wl.head_dim, wl.group
-    q = f64(data["q_win"])[0]
-    K = f64(data["k"])[0]
-    V = f64(data["v"])[0]
-    t0 = time.perf_counter()
-    comp = [O.compress_head(q[h * G:(h + 1) * G], K[h], V[h], budget) for h in range(heads)]
-    t_comp = time.perf_counter() - t0
-    qd = f64(data["q_dec"][:steps])[:, 0]
-    kn = f64(data["k_new"][:steps])[:, 0]
-    vn = f64(data["v_new"][:steps])[:, 0]
-    kc = np.stack([c.k_out for c in comp])[None]
-    vc = np.stack([c.v_out for c in comp])[None]
-    cap = budget + steps
-    kcap = np.zeros((1, heads, cap, d))
-    vcap = np.zeros((1, heads, cap, d))
-    kcap[:, :, :budget] = kc
-    vcap[:, :, :budget] = vc
-    ln = np.full((1, heads), budget)
-    moms = [[c.moments for c in comp]]
+    d, G, Hkv, N = wl.head_dim, wl.group, wl.n_kv_heads, wl.ctx_len
+    t_comp = t_dec = 0.0
     nbytes = 0
-    t0 = time.perf_counter()
-    for t in range(steps):
-        _, _, _, (kcap, vcap, ln) = O.decode(qd[t][None, :heads * G], kcap, vcap, ln, moms,
-                                             k_new=kn[t][None, :heads], v_new=vn[t][None, :heads])
-        nbytes += decode_bytes(heads, G, d, budget + t + 1)
-    t_dec = time.perf_counter() - t0
+    for data in layers_data:
+        q = f64(data["q_win"])[0]
+        K = f64(data["k"])[0]
+        V = f64(data["v"])[0]
+        qd = f64(data["q_dec"][:steps])[:, 0]
+        kn = f64(data["k_new"][:steps])[:, 0]
+        vn = f64(data["v_new"][:steps])[:, 0]
+        for L in budgets:
+            t0 = time.perf_counter()
+            comp = [O.compress_head(q[h * G:(h + 1) * G], K[h], V[h], L) for h in range(Hkv)]
+            t_comp += time.perf_counter() - t0
+            n0 = min(L, N)
+            cap = n0 + steps
+            kcap = np.zeros((1, Hkv, cap, d))
+            vcap = np.zeros((1, Hkv, cap, d))
+            kcap[0, :, :n0] = np.stack([c.k_out for c in comp])
+            vcap[0, :, :n0] = np.stack([c.v_out for c in comp])
+            ln = np.full((1, Hkv), n0)
+            moms = [[c.moments for c in comp]]
+            t0 = time.perf_counter()
+            for t in range(steps):
+                _, _, _, (kcap, vcap, ln) = O.decode(qd[t][None], kcap, vcap, ln, moms,
+                                                     k_new=kn[t][None], v_new=vn[t][None])
+            t_dec += time.perf_counter() - t0
+            nbytes += sum(decode_bytes(Hkv, G, d, n0 + t + 1) for t in range(steps))
+    n_lay = len(layers_data)
     return {"value": nbytes / t_dec / 1e9, "unit": "GB/s", "cores": int(blas_threads),
             "host_cpus": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": f"layer 0, {heads} of {wl.n_kv_heads} KV heads, budget {budget}: "
-                      f"compress, then {steps} decode steps (fp64 NumPy)",
-            "compress_ms_per_layer_extrapolated": t_comp / heads * wl.n_kv_heads * 1e3,
+            "sample": f"layers 0-{n_lay - 1} of {wl.layers} (sequence 0 of {wl.batch}), all {Hkv} "
+                      f"KV heads, budgets "
+                      f"{list(budgets)}: compress each (layer, budget), then {steps} decode "
+                      f"steps with appends (fp64 NumPy)",
+            "compress_ms_per_layer": t_comp / (n_lay * len(budgets)) * 1e3,
             "decode_s": t_dec, "compress_s": t_comp}
 
 
@@ -358,8 +365,8 @@ def main() -> int:
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--budgets", default=None, help="comma list overriding the workload's")
     ap.add_argument("--decode-steps", type=int, default=None)
-    ap.add_argument("--cpu-heads", type=int, default=2)
-    ap.add_argument("--cpu-steps", type=int, default=8)
+    ap.add_argument("--cpu-layers", type=int, default=2,
+                    help="layers in the oracle's host sample (all heads, budgets and steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-evict", action="store_true",
                     help="skip the decode-with-eviction measurement")
@@ -632,8 +639,7 @@ def main() -> int:
         res["evict_decode"] = evict
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(wl, data[0], 512 if 512 in budgets else budgets[0],
-                                           args.cpu_heads, args.cpu_steps)
+        res["cpu_baseline"] = cpu_baseline(wl, data[:max(1, args.cpu_layers)], budgets, T)
     print(json.dumps(res))
     return 0
 
