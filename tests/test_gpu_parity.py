@@ -84,6 +84,23 @@ def test_decode_varied_lengths_and_slice_boundaries(dtype, n_split, append):
                        summary=int(append))
 
 
+@pytest.mark.parametrize("cap", [128, 300])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_single_launch_block_rounds(d, dtype, cap):
+    """The single launch (one 4-wave workgroup per KV head) at per-head lengths on both
+    sides of the 4- and 8-block boundaries (one, two or three 32-row blocks per wave), an
+    empty head, appends, prepared summary."""
+    L = cap - 3
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=d, ctx_len=1000,
+                         batch=3, n_q_heads=4, n_kv_heads=2, window=16, budgets=(L,))
+    out = P.run_compress(gpu, L, cap=cap)
+    lens0 = ([[0, 31], [95, 96], [124, 125]] if cap == 128
+             else [[0, 127], [128, 160], [255, 297]])
+    announce(f"single launch d={d} {dtype} cap={cap} lengths {lens0}")
+    P.run_decode_steps(gpu, out, 3, n_split=1, lens0=lens0, summary=1)
+
+
 # ---------------------------------------------------------------- edge cases
 @pytest.mark.parametrize("summary", [0, 1])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
