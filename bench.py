@@ -97,6 +97,13 @@ def build_stack(wl, layers, device):
     return data, time.time() - t0
 
 
+def percentiles(xs) -> dict:
+    """p10 / p50 / p90 (linear interpolation) and the sample count of a list of times."""
+    import numpy as np
+    q = np.percentile(np.asarray(xs, dtype=np.float64), [10, 50, 90])
+    return {"p10": float(q[0]), "p50": float(q[1]), "p90": float(q[2]), "n": len(xs)}
+
+
 def cpu_baseline(wl, layers_data, budgets, steps: int) -> dict:
     """The fp64 oracle on the host over a bounded sample of the same workload: every KV head
     of the given layers, at every budget, compressed, then `steps` decode steps with appends
@@ -442,10 +449,18 @@ def main() -> int:
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
+            marks = []
             for l in range(layers):
+                if timing is not None and l > 0:   # per-call spread: an event between calls
+                    marks.append(torch.cuda.Event(enable_timing=True))
+                    marks[-1].record()
                 x = data[l]
                 mk.momentkv_compress(x["q_win"], x["k"], x["v"], L, cap=min(L, N) + T,
                                      out=views[L][l], workspace=cws)
+            if timing is not None:
+                marks.append(torch.cuda.Event(enable_timing=True))
+                marks[-1].record()
+                timing["calls"][L].append([e0] + marks)
             st = stacks[L]   # the decode form of the 36 summaries, once per compression
             mk.momentkv_prepare_summary(st.n_e, st.s_k, st.s_v, st.S, dtype=wl.dtype,
                                         out=prepared[L])
@@ -466,7 +481,7 @@ def main() -> int:
                     decode_call(t, L)
 
     def new_timing():
-        return {"compress": {L: [] for L in budgets}}
+        return {"compress": {L: [] for L in budgets}, "calls": {L: [] for L in budgets}}
 
     def capture(skip=None, phase=None):
         g = torch.cuda.CUDAGraph()
@@ -582,6 +597,10 @@ def main() -> int:
             "decode_tokens_per_s": B * T / (budget_ms * 1e-3),
         }
     value = phase_bytes * len(dec_ms) / dec_s / 1e9
+    spread = {"decode_step_ms": percentiles(dec_ms),
+              "compress_call_ms": {str(L): percentiles(
+                  [a.elapsed_time(b) for ev in timing["calls"][L] for a, b in zip(ev, ev[1:])])
+                  for L in budgets}}
     half = None
     if wl.dtype == torch.bfloat16 and not args.no_half:
         half = half_summary_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out,
@@ -630,6 +649,7 @@ def main() -> int:
                      "bytes_per_launch": avg_bytes,
                      "avg_launch_us": avg_launch_s * 1e6},
         "wall_s_timed": wall,
+        "spread": spread,
     }
     if half is not None:
         res["decode_half_summary"] = half
