@@ -36,6 +36,9 @@ Pinning status (what fixes each function other than itself; see tests/):
                           still equals full attention over every token seen), moments
                           equal brute-force sums over everything evicted, token
                           conservation, Phase 2 on the post-eviction state
+  batched wrappers        the query-head -> KV-head grouping of compress, decode and
+  (GQA mapping)           decode_evict pinned to torch SDPA with enable_gqa (which KV head
+                          each query head reads is read off SDPA's own output)
 """
 from __future__ import annotations
 

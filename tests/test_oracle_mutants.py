@@ -71,6 +71,13 @@ MUTANTS = {
     "no_correction_ignored": ("    if m.n_e == 0 or order < 0:", "    if m.n_e == 0:"),
     "head_budget_ties_reversed": ("    order = np.lexsort((np.arange(flat.size), -flat))[:keep]",
                                   "    order = np.lexsort((-np.arange(flat.size), -flat))[:keep]"),
+    "decode_head_modulo": ("            h = hq // G\n", "            h = hq % Hkv\n"),
+    "compress_strided_group": (
+        "return [[compress_head(q[b, h * G:(h + 1) * G], K[b, h], V[b, h], budget, **kw)",
+        "return [[compress_head(q[b, h::Hkv], K[b, h], V[b, h], budget, **kw)"),
+    "decode_evict_strided_group": (
+        "r = decode_evict_head(Q[b, h * G:(h + 1) * G], kc[b, h], vc[b, h], int(ln[b, h]),",
+        "r = decode_evict_head(Q[b, h::Hkv], kc[b, h], vc[b, h], int(ln[b, h]),"),
     "head_budget_lowest_mass": ("    order = np.lexsort((np.arange(flat.size), -flat))[:keep]",
                                 "    order = np.lexsort((np.arange(flat.size), flat))[:keep]"),
 }

@@ -711,3 +711,115 @@ def test_adaptive_compress_counts_and_summaries():
         np.testing.assert_array_equal(E, r.evicted)
         S = sum(np.outer(V[0, h, i], K[0, h, i]) for i in E)
         np.testing.assert_allclose(r.moments.S, S, rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------ grouped-query head mapping
+def sdpa_gqa(q, K, V, scale, mask=None):
+    """torch SDPA with grouped queries (enable_gqa): q [B,Hq,m,d], K [B,Hkv,n,d],
+    V [B,Hkv,n,e] -> [B,Hq,m,e], fp64."""
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x, np.float64))
+    m = None if mask is None else torch.from_numpy(mask)
+    return F.scaled_dot_product_attention(t(q), t(K), t(V), attn_mask=m, scale=scale,
+                                          enable_gqa=True).numpy()
+
+
+def torch_kv_head_of(Hq, Hkv):
+    """The KV head torch's grouped-query SDPA gives each query head: every value row
+    carries a one-hot of its head's index, so each query head's output names its head.
+    This is the GQA layout (Sec. 5.1: 32 query heads over 8 KV heads) taken from a
+    library, not from the oracle."""
+    q = np.ones((1, Hq, 1, 4))
+    K = np.zeros((1, Hkv, 1, 4))
+    V = np.eye(Hkv)[None, :, None, :]
+    return sdpa_gqa(q, K, V, 1.0)[0, :, 0, :].argmax(axis=-1)
+
+
+def test_batched_decode_reads_the_kv_head_of_each_query_group():
+    """oracle.decode over [B, Hq] queries and [B, Hkv] caches: without correction it is
+    torch's grouped-query SDPA over each head's retained rows; with the correction each
+    query head's output is decode_head against the KV head (lens, rows and summary)
+    that torch assigns it."""
+    rng = np.random.default_rng(60)
+    B, Hq, Hkv, d, cap, n = 2, 8, 2, 8, 12, 10
+    q = rng.normal(size=(B, Hq, d)) * 1.5
+    kc = rng.normal(size=(B, Hkv, cap, d))
+    vc = rng.normal(size=(B, Hkv, cap, d))
+    kc[:, 1] += 2.0                                        # heads that differ in law
+    mom = [[O.evicted_moments(rng.normal(size=(5, d)), rng.normal(size=(5, d)) + 3.0 * h,
+                              np.arange(5)) for h in range(Hkv)] for _ in range(B)]
+    scale = 1 / math.sqrt(d)
+    want = sdpa_gqa(q[:, :, None], kc[:, :, :n], vc[:, :, :n], scale)[:, :, 0]
+    lens = np.full((B, Hkv), n)
+    out, lz, wr, _ = O.decode(q, kc, vc, lens, mom, order=-1)
+    np.testing.assert_allclose(out, want, rtol=1e-12, atol=1e-14)
+    zero = [[O.Moments.zeros(d) for _ in range(Hkv)] for _ in range(B)]
+    out0, _, _, _ = O.decode(q, kc, vc, lens, zero)
+    np.testing.assert_allclose(out0, want, rtol=1e-12, atol=1e-14)
+    grp = torch_kv_head_of(Hq, Hkv)
+    lens = np.array([[7, 11], [12, 3]])
+    out1, lz1, wr1, _ = O.decode(q, kc, vc, lens, mom)
+    for b in range(B):
+        for hq in range(Hq):
+            h = grp[hq]
+            r = O.decode_head(q[b, hq], kc[b, h, :lens[b, h]], vc[b, h, :lens[b, h]], mom[b][h])
+            np.testing.assert_allclose(out1[b, hq], r.out, rtol=1e-13)
+            np.testing.assert_allclose(lz1[b, hq], r.log_Z_R, rtol=1e-13)
+            np.testing.assert_allclose(wr1[b, hq], r.w_R, rtol=1e-13)
+
+
+def test_batched_compress_window_mass_groups_queries_by_kv_head():
+    """Each KV head's window mass is the mean of the softmax probabilities of the query
+    heads torch's grouped-query SDPA sends to it: one-hot values over positions, plus a
+    one-hot of the KV head's index that names the group."""
+    rng = np.random.default_rng(61)
+    B, Hq, Hkv, w, d, N = 2, 6, 3, 4, 8, 40
+    q = rng.normal(size=(B, Hq, w, d)) * 1.5
+    K = rng.normal(size=(B, Hkv, N, d)) * (1.0 + np.arange(Hkv))[None, :, None, None]
+    V = rng.normal(size=(B, Hkv, N, d))
+    scale = 1 / math.sqrt(d)
+    onehot = np.zeros((B, Hkv, N, N + Hkv))
+    onehot[:, :, :, :N] = np.eye(N)
+    for h in range(Hkv):
+        onehot[:, h, :, N + h] = 1.0
+    band = torch.ones(w, N, dtype=torch.bool).tril(diagonal=N - w).numpy()
+    P = sdpa_gqa(q, K, onehot, scale, band)                 # [B, Hq, w, N + Hkv]
+    res = O.compress(q, K, V, 1 + w + 6)
+    for b in range(B):
+        head = P[b, :, 0, N:].argmax(axis=-1)              # the KV head of each query head
+        for h in range(Hkv):
+            rows = P[b, head == h, :, : N - w].reshape(-1, N - w)
+            assert rows.shape[0] == w * Hq // Hkv
+            np.testing.assert_allclose(res[b][h].a, rows.mean(axis=0), rtol=1e-12, atol=1e-15)
+
+
+def test_batched_decode_evict_scores_each_kv_head_with_its_query_group():
+    """With an empty summary and unit-norm values the evicted row of each KV head is the
+    one with the lowest mean softmax weight over the query heads torch's grouped-query
+    SDPA sends to that head; without correction the output is that SDPA over the cache
+    left after the eviction."""
+    rng = np.random.default_rng(62)
+    B, Hq, Hkv, d, L = 1, 6, 2, 8, 9
+    grp = torch_kv_head_of(Hq, Hkv)
+    scale = 1 / math.sqrt(d)
+    for trial in range(8):
+        q = rng.normal(size=(B, Hq, d)) * 2.5
+        kc = np.zeros((B, Hkv, L + 2, d))
+        vc = np.zeros((B, Hkv, L + 2, d))
+        kc[:, :, :L] = rng.normal(size=(B, Hkv, L, d))
+        V = rng.normal(size=(B, Hkv, L + 1, d))
+        V /= np.linalg.norm(V, axis=-1, keepdims=True)
+        vc[:, :, :L] = V[:, :, :L]
+        kn = rng.normal(size=(B, Hkv, d))
+        lens = np.full((B, Hkv), L)
+        zero = [[O.Moments.zeros(d) for _ in range(Hkv)] for _ in range(B)]
+        out, _, _, (kc2, vc2, ln2, _), ev, _ = O.decode_evict(q, kc, vc, lens, zero, kn,
+                                                              V[:, :, L], L, order=-1)
+        for b in range(B):
+            for h in range(Hkv):
+                Kh = np.vstack([kc[b, h, :L], kn[b, h][None]])
+                logits = torch.from_numpy(q[b, grp == h] @ Kh.T * scale)   # [G, n]
+                alpha = torch.softmax(logits, dim=1).mean(dim=0).numpy()
+                assert ev[b, h] == int(np.argmin(alpha)), (trial, h)
+        want = sdpa_gqa(q[:, :, None], kc2[:, :, :L], vc2[:, :, :L], scale)[:, :, 0]
+        assert (ln2 == L).all()
+        np.testing.assert_allclose(out, want, rtol=1e-12, atol=1e-14)
