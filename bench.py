@@ -232,7 +232,7 @@ def adaptive_measurement(args, wl, data, layers, L, dev) -> dict:
         n_e=torch.empty(B, Hkv, **i32), s_k=torch.empty(B, Hkv, d, **f32),
         s_v=torch.empty(B, Hkv, d, **f32), S=torch.empty(B, Hkv, d, d, **f32))
         for _ in range(layers)]
-    ws = torch.empty(mk.momentkv_compress_workspace_size(
+    ws = torch.empty(mk.momentkv_compress_workspace_bytes(
         mk.compress_params(data[0]["q_win"], data[0]["k"], L, cap=cap, adaptive=True)),
         dtype=torch.uint8, device=dev)
 
@@ -287,7 +287,7 @@ def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, ou
     for L in budgets:
         Lr = min(L, N)
         p = mk.decode_params(q_steps[0], stacks[L].k_out, max_len=Lr + 1)
-        ews[L] = torch.zeros(mk.momentkv_decode_evict_workspace_size(p), dtype=torch.uint8,
+        ews[L] = torch.zeros(mk.momentkv_decode_evict_workspace_bytes(p), dtype=torch.uint8,
                              device=dev)
 
     def evict_call(t, L):
@@ -426,14 +426,14 @@ def main() -> int:
             idx=torch.empty(LB, Hkv, min(L, N), **i32), lens=torch.empty(LB, Hkv, **i32),
             n_e=torch.empty(LB, Hkv, **i32), s_k=torch.empty(LB, Hkv, d, **f32),
             s_v=torch.empty(LB, Hkv, d, **f32), S=torch.empty(LB, Hkv, d, d, **f32))
-    cws_bytes = max(mk.momentkv_compress_workspace_size(
+    cws_bytes = max(mk.momentkv_compress_workspace_bytes(
         mk.compress_params(data[0]["q_win"], data[0]["k"], L, cap=min(L, N) + T)) for L in budgets)
     cws = torch.empty(cws_bytes, dtype=torch.uint8, device=dev)
     dws = {}
     out = torch.empty(LB, Hq, d, dtype=wl.dtype, device=dev)
     for L in budgets:
         p = mk.decode_params(q_steps[0], stacks[L].k_out, max_len=min(L, N) + T)
-        dws[L] = torch.zeros(mk.momentkv_decode_workspace_size(p), dtype=torch.uint8, device=dev)
+        dws[L] = torch.zeros(mk.momentkv_decode_workspace_bytes(p), dtype=torch.uint8, device=dev)
 
     def layer_view(st, l):
         sl = slice(l * B, (l + 1) * B)

@@ -28,9 +28,9 @@
  *   - K/V/Q tensors and outputs use the element type `dtype` (fp32, or bf16 stored as
  *     uint16 bit patterns, round-to-nearest-even).  Moments are always fp32 (n_e int32).
  *   - The caller owns every buffer, including the workspace sized by the matching
- *     *_workspace_size query.  The library never allocates, frees or synchronises; all
- *     work is enqueued on `stream` (a hipStream_t; NULL = the default stream) and is
- *     stream-ordered.  There is no global mutable state: calls on different streams
+ *     *_workspace_bytes query (the *_workspace_size names are the same functions).
+ *     The library never allocates, frees or synchronises; all work is enqueued on
+ *     `stream` (a hipStream_t; NULL = the default stream) and is stream-ordered.  There is no global mutable state: calls on different streams
  *     with different buffers may run concurrently.
  *   - Every argument is validated on the host before the first launch.  On any error
  *     nothing is launched and the status says why.  A launch failure reported by HIP
@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define MOMENTKV_ABI_VERSION 4
+#define MOMENTKV_ABI_VERSION 5
 
 typedef enum {
   MKV_OK = 0,
@@ -132,7 +132,9 @@ typedef struct {
 } mkv_compress_debug;
 
 /* Bytes of device workspace momentkv_compress needs for these parameters (0 on invalid
- * parameters).  Pure host computation. */
+ * parameters).  Pure host computation.  momentkv_compress_workspace_size is the same
+ * function under its earlier name. */
+size_t momentkv_compress_workspace_bytes(const mkv_compress_params* p);
 size_t momentkv_compress_workspace_size(const mkv_compress_params* p);
 
 /* q_win   [B, Hq, w, d]      window queries (post-RoPE), read only
@@ -145,7 +147,7 @@ size_t momentkv_compress_workspace_size(const mkv_compress_params* p);
  * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d] fp32, S [B, Hkv, d, d] fp32: outputs,
  *                            overwritten (zero-initialised summary per generation)
  * dbg                        NULL or optional diagnostics
- * workspace                  >= momentkv_compress_workspace_size(p) bytes, 256-aligned */
+ * workspace                  >= momentkv_compress_workspace_bytes(p) bytes, 256-aligned */
 mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, const void* k,
                              const void* v, void* k_out, void* v_out, int32_t* idx_out,
                              int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, float* S,
@@ -189,6 +191,9 @@ typedef struct {
                         /* its half-precision form (bf16 caches only)               */
 } mkv_decode_params;
 
+/* Bytes of device workspace momentkv_decode_attn needs for these parameters (0 on invalid
+ * parameters; pure host computation); momentkv_decode_workspace_size is the same function. */
+size_t momentkv_decode_workspace_bytes(const mkv_decode_params* p);
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
 
 /* Decode form of a summary (Eq. fhat's covariance term; clamp of App. C.2).
@@ -223,7 +228,7 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R
- * workspace >= momentkv_decode_workspace_size(p) bytes, 256-aligned.  Its first int32
+ * workspace >= momentkv_decode_workspace_bytes(p) bytes, 256-aligned.  Its first int32
  *           is a sticky overflow flag (set to 1 when an append found a full cache; zero it
  *           before first use to read it).  Calls that share a workspace must be
  *           stream-ordered. */
@@ -255,7 +260,8 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
  * The decision is taken on fp32 scores in the log domain (log alpha_j + log ||r_j||, so
  * no weight underflows); near-equal scores may order differently from exact arithmetic.
  * ---------------------------------------------------------------------------------- */
-size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);
+size_t momentkv_decode_evict_workspace_bytes(const mkv_decode_params* p);
+size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);  /* same function */
 
 /* p         as for momentkv_decode_attn with summary = 0: S is the raw sum, updated in
  *           place.  max_len bounds lens after the append (budget < max_len <= cap leaves
@@ -273,7 +279,7 @@ size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);
  * n_e, s_k, s_v, S: the raw summary (fp32; n_e int32), read and updated in place
  * evicted_out  NULL or [B, Hkv] int32: the row j* evicted by this call (it now holds what
  *           was the last row, unless j* was the last row itself), -1 if none
- * workspace >= momentkv_decode_evict_workspace_size(p) bytes, 256-aligned.  Its first
+ * workspace >= momentkv_decode_evict_workspace_bytes(p) bytes, 256-aligned.  Its first
  *           int32 is a sticky flag: bit 0 = a full cache (lens >= cap) skipped the append
  *           and the eviction; bit 1 = lens + 1 exceeded max_len (appended, no eviction);
  *           bit 2 = no finite score (nothing evicted); bit 3 = lens was above budget

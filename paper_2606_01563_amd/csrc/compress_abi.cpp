@@ -154,6 +154,10 @@ size_t momentkv_compress_workspace_size(const mkv_compress_params* p) {
   return total;
 }
 
+size_t momentkv_compress_workspace_bytes(const mkv_compress_params* p) {
+  return momentkv_compress_workspace_size(p);
+}
+
 mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, const void* k,
                              const void* v, void* k_out, void* v_out, int32_t* idx_out,
                              int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, float* S,

@@ -106,6 +106,10 @@ size_t momentkv_decode_workspace_size(const mkv_decode_params* p) {
   return total;
 }
 
+size_t momentkv_decode_workspace_bytes(const mkv_decode_params* p) {
+  return momentkv_decode_workspace_size(p);
+}
+
 size_t momentkv_prepared_summary_size(const mkv_decode_params* p) {
   if (check_decode_params(p) != MKV_OK) return 0;
   return (size_t)p->batch * p->n_kv_heads * p->head_dim * p->head_dim * (p->summary == 2 ? 2 : 4);

@@ -90,6 +90,10 @@ size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p) {
   return total;
 }
 
+size_t momentkv_decode_evict_workspace_bytes(const mkv_decode_params* p) {
+  return momentkv_decode_evict_workspace_size(p);
+}
+
 mkv_status momentkv_decode_evict(const mkv_decode_params* p, int32_t budget, const void* q,
                                  void* k_cache, void* v_cache, int32_t* lens,
                                  const void* k_new, const void* v_new, int32_t* n_e,

@@ -67,13 +67,17 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
         L = ctypes.CDLL(LIB_PATH)
-        L.momentkv_compress_workspace_size.argtypes = [ctypes.POINTER(CompressParams)]
-        L.momentkv_compress_workspace_size.restype = ctypes.c_size_t
+        for name in ("momentkv_compress_workspace_bytes", "momentkv_compress_workspace_size"):
+            getattr(L, name).argtypes = [ctypes.POINTER(CompressParams)]
+            getattr(L, name).restype = ctypes.c_size_t
+        for name in ("momentkv_decode_workspace_bytes", "momentkv_decode_workspace_size",
+                     "momentkv_decode_evict_workspace_bytes",
+                     "momentkv_decode_evict_workspace_size"):
+            getattr(L, name).argtypes = [ctypes.POINTER(DecodeParams)]
+            getattr(L, name).restype = ctypes.c_size_t
         L.momentkv_compress.argtypes = [ctypes.POINTER(CompressParams)] + [_VP] * 11 + \
             [ctypes.POINTER(CompressDebug), _VP, ctypes.c_size_t, _VP]
         L.momentkv_compress.restype = ctypes.c_int
-        L.momentkv_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeParams)]
-        L.momentkv_decode_workspace_size.restype = ctypes.c_size_t
         L.momentkv_decode_attn.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 13 + \
             [_VP, ctypes.c_size_t, _VP]
         L.momentkv_decode_attn.restype = ctypes.c_int
@@ -82,8 +86,6 @@ def lib() -> ctypes.CDLL:
         L.momentkv_prepared_summary_size.restype = ctypes.c_size_t
         L.momentkv_prepare_summary.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 6
         L.momentkv_prepare_summary.restype = ctypes.c_int
-        L.momentkv_decode_evict_workspace_size.argtypes = [ctypes.POINTER(DecodeParams)]
-        L.momentkv_decode_evict_workspace_size.restype = ctypes.c_size_t
         L.momentkv_decode_evict.argtypes = [ctypes.POINTER(DecodeParams), ctypes.c_int32] + \
             [_VP] * 14 + [_VP, ctypes.c_size_t, _VP]
         L.momentkv_decode_evict.restype = ctypes.c_int
@@ -109,16 +111,22 @@ def momentkv_abi_version() -> int:
     return int(lib().momentkv_abi_version())
 
 
-def momentkv_compress_workspace_size(p: CompressParams) -> int:
-    return int(lib().momentkv_compress_workspace_size(ctypes.byref(p)))
+def momentkv_compress_workspace_bytes(p: CompressParams) -> int:
+    return int(lib().momentkv_compress_workspace_bytes(ctypes.byref(p)))
 
 
-def momentkv_decode_workspace_size(p: DecodeParams) -> int:
-    return int(lib().momentkv_decode_workspace_size(ctypes.byref(p)))
+def momentkv_decode_workspace_bytes(p: DecodeParams) -> int:
+    return int(lib().momentkv_decode_workspace_bytes(ctypes.byref(p)))
 
 
-def momentkv_decode_evict_workspace_size(p: DecodeParams) -> int:
-    return int(lib().momentkv_decode_evict_workspace_size(ctypes.byref(p)))
+def momentkv_decode_evict_workspace_bytes(p: DecodeParams) -> int:
+    return int(lib().momentkv_decode_evict_workspace_bytes(ctypes.byref(p)))
+
+
+# the same functions under their earlier names
+momentkv_compress_workspace_size = momentkv_compress_workspace_bytes
+momentkv_decode_workspace_size = momentkv_decode_workspace_bytes
+momentkv_decode_evict_workspace_size = momentkv_decode_evict_workspace_bytes
 
 
 def momentkv_prepared_summary_size(p: DecodeParams) -> int:
@@ -142,6 +150,43 @@ def _ptr(t: torch.Tensor | None) -> int | None:
     if not t.is_contiguous():
         raise ValueError("tensor must be contiguous")
     return t.data_ptr()
+
+
+def _expect(t, name: str, shape: tuple, dtype: torch.dtype, optional: bool = False):
+    """Raise ValueError unless `t` is a tensor of exactly this shape and dtype (None is
+    allowed when optional).  Runs before any pointer reaches the library: a tensor with
+    the wrong element size or too few elements would be read out of bounds on the GPU."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _same_device(named: dict):
+    """Every given tensor on the GPU, contiguous, and on one device."""
+    devs = set()
+    for name, t in named.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        devs.add(t.device)
+    if len(devs) > 1:
+        raise ValueError(f"tensors are on several devices: {sorted(map(str, devs))}")
+
+
+def _check_workspace(ws, name: str = "workspace"):
+    if ws is not None and (not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8
+                           or ws.dim() != 1):
+        raise ValueError(f"{name} must be a 1-D torch.uint8 tensor")
 
 
 def _stream() -> int:
@@ -200,6 +245,10 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
     """Compress [B, Hkv, N, d] prefill K/V to `budget` rows per KV head (see the header);
     adaptive=True splits the layer's candidate budget across heads (idx then has `cap`
     entries per head, the first `lens` of them valid)."""
+    if not isinstance(q_win, torch.Tensor) or q_win.dim() != 4:
+        raise ValueError("q_win must be a [B, Hq, w, d] tensor")
+    if not isinstance(k, torch.Tensor) or k.dim() != 4:
+        raise ValueError("k must be a [B, Hkv, N, d] tensor")
     p = compress_params(q_win, k, budget, n_sink=n_sink, chunk=chunk, mi_rounds=mi_rounds,
                         cap=cap, scale=scale, tau=tau, adaptive=adaptive)
     B, Hq, w, d = q_win.shape
@@ -207,6 +256,21 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
     dev = k.device
     ada = adaptive and budget < N
     n_out = p.cap if ada else min(budget, N)
+    _expect(q_win, "q_win", (B, Hq, w, d), k.dtype)
+    _expect(v, "v", tuple(k.shape), k.dtype)
+    _check_workspace(workspace)
+    if out is not None:
+        f32, i32 = torch.float32, torch.int32
+        for name, shape, dt in (("k_out", (B, Hkv, p.cap, d), k.dtype),
+                                ("v_out", (B, Hkv, p.cap, d), k.dtype),
+                                ("idx", (B, Hkv, n_out), i32), ("lens", (B, Hkv), i32),
+                                ("n_e", (B, Hkv), i32), ("s_k", (B, Hkv, d), f32),
+                                ("s_v", (B, Hkv, d), f32), ("S", (B, Hkv, d, d), f32)):
+            _expect(getattr(out, name), f"out.{name}", shape, dt)
+    _same_device({"q_win": q_win, "k": k, "v": v, "workspace": workspace,
+                  **({} if out is None else {f"out.{n}": getattr(out, n) for n in
+                                             ("k_out", "v_out", "idx", "lens", "n_e", "s_k",
+                                              "s_v", "S")})})
     if out is None:
         f32 = dict(dtype=torch.float32, device=dev)
         i32 = dict(dtype=torch.int32, device=dev)
@@ -228,7 +292,7 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
         out.kept0 = torch.zeros(B, Hkv, max(k_rows, 0), dtype=torch.int32, device=dev)
         dbg = CompressDebug(_ptr(out.abar), _ptr(out.score0), _ptr(out.score),
                             _ptr(out.kept0) if k_keep > 0 else None)
-    nbytes = momentkv_compress_workspace_size(p)
+    nbytes = momentkv_compress_workspace_bytes(p)
     if nbytes == 0:
         code = lib().momentkv_compress(ctypes.byref(p), *([None] * 11), None, None, 0, None)
         raise MomentKVError(code, "momentkv_compress")
@@ -261,12 +325,22 @@ def momentkv_prepare_summary(n_e: torch.Tensor, s_k: torch.Tensor, s_v: torch.Te
     """Decode form of the summary (see the header): bf16 hi/lo planes [B, Hkv, 2, d, d] for
     dtype bf16, fp32 [B, Hkv, d, d] for fp32; half=True (bf16 only) the one-plane
     half-precision form [B, Hkv, d, d].  Pass it as `S` with summary=1 (summary=2 if half)."""
+    if not isinstance(S, torch.Tensor) or S.dim() != 4:
+        raise ValueError("S must be a [B, Hkv, d, d] tensor")
+    if dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError(f"unsupported dtype {dtype}")
     B, Hkv, d, _ = S.shape
+    _expect(S, "S", (B, Hkv, d, d), torch.float32)
+    _expect(n_e, "n_e", (B, Hkv), torch.int32)
+    _expect(s_k, "s_k", (B, Hkv, d), torch.float32)
+    _expect(s_v, "s_v", (B, Hkv, d), torch.float32)
     code = MKV_BF16 if dtype == torch.bfloat16 else MKV_F32
     p = DecodeParams(B, Hkv, Hkv, d, 1, 1, 1, code, 0.0, tau, 0, 2 if half else 0)
+    shape = (B, Hkv, 2, d, d) if dtype == torch.bfloat16 and not half else (B, Hkv, d, d)
     if out is None:
-        shape = (B, Hkv, 2, d, d) if dtype == torch.bfloat16 and not half else (B, Hkv, d, d)
         out = torch.empty(shape, dtype=dtype, device=S.device)
+    _expect(out, "out", shape, dtype)
+    _same_device({"n_e": n_e, "s_k": s_k, "s_v": s_v, "S": S, "out": out})
     if out.numel() * out.element_size() < momentkv_prepared_summary_size(p):
         raise ValueError("prepared summary buffer too small")
     code = lib().momentkv_prepare_summary(ctypes.byref(p), _ptr(n_e), _ptr(s_k), _ptr(s_v),
@@ -274,6 +348,49 @@ def momentkv_prepare_summary(n_e: torch.Tensor, s_k: torch.Tensor, s_v: torch.Te
     if code != 0:
         raise MomentKVError(code, "momentkv_prepare_summary")
     return out
+
+
+def _check_decode_args(q, k_cache, v_cache, lens, n_e, s_k, s_v, S, k_new, v_new, out, lse,
+                       w_r, workspace, summary: int, evicted=None, need_new: bool = False):
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError("q must be a [B, Hq, d] tensor")
+    if not isinstance(k_cache, torch.Tensor) or k_cache.dim() != 4:
+        raise ValueError("k_cache must be a [B, Hkv, cap, d] tensor")
+    if q.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError(f"q must be float32 or bfloat16, got {q.dtype}")
+    B, Hq, d = q.shape
+    _, Hkv, cap, _ = k_cache.shape
+    f32, i32 = torch.float32, torch.int32
+    _expect(k_cache, "k_cache", (B, Hkv, cap, d), q.dtype)
+    _expect(v_cache, "v_cache", (B, Hkv, cap, d), q.dtype)
+    _expect(lens, "lens", (B, Hkv), i32)
+    _expect(n_e, "n_e", (B, Hkv), i32)
+    _expect(s_k, "s_k", (B, Hkv, d), f32)
+    _expect(s_v, "s_v", (B, Hkv, d), f32)
+    if summary == 0:
+        _expect(S, "S", (B, Hkv, d, d), f32)
+    elif summary == 1:
+        if q.dtype == torch.bfloat16:
+            _expect(S, "S (prepared)", (B, Hkv, 2, d, d), torch.bfloat16)
+        else:
+            _expect(S, "S (prepared)", (B, Hkv, d, d), f32)
+    elif summary == 2:
+        _expect(S, "S (half-precision prepared)", (B, Hkv, d, d), torch.bfloat16)
+    else:
+        raise ValueError(f"summary must be 0, 1 or 2, got {summary}")
+    if (k_new is None) != (v_new is None) or (need_new and k_new is None):
+        raise ValueError("k_new and v_new must be given together" +
+                         (" (required here)" if need_new else ""))
+    _expect(k_new, "k_new", (B, Hkv, d), q.dtype, optional=True)
+    _expect(v_new, "v_new", (B, Hkv, d), q.dtype, optional=True)
+    _expect(out, "out", (B, Hq, d), q.dtype, optional=True)
+    _expect(lse, "lse", (B, Hq), f32, optional=True)
+    _expect(w_r, "w_r", (B, Hq), f32, optional=True)
+    _expect(evicted, "evicted", (B, Hkv), i32, optional=True)
+    _check_workspace(workspace)
+    _same_device(dict(q=q, k_cache=k_cache, v_cache=v_cache, lens=lens, n_e=n_e, s_k=s_k,
+                      s_v=s_v, S=S, k_new=k_new, v_new=v_new, out=out, lse=lse, w_r=w_r,
+                      evicted=evicted, workspace=workspace))
 
 
 def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
@@ -293,13 +410,15 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     int32 of the workspace is the sticky append-overflow flag; a workspace allocated here
     gets it zeroed, a caller-owned one should be zeroed once before first use.
     """
+    _check_decode_args(q, k_cache, v_cache, lens, n_e, s_k, s_v, S, k_new, v_new, out, lse, w_r,
+                       workspace, summary)
     cap = k_cache.shape[2]
     p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
                       scale=scale, tau=tau, n_split=n_split, summary=summary)
     dev = q.device
     if out is None:
         out = torch.empty_like(q)
-    nbytes = momentkv_decode_workspace_size(p)
+    nbytes = momentkv_decode_workspace_bytes(p)
     if nbytes == 0:
         code = lib().momentkv_decode_attn(ctypes.byref(p), *([None] * 13), None, 0, None)
         raise MomentKVError(code, "momentkv_decode_attn")
@@ -328,13 +447,15 @@ def momentkv_decode_evict(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch
     """Decode step with moment-informed eviction (see the header).  The caches, lens and
     the raw summary (n_e, s_k, s_v, S) are updated in place.
     Returns (out, lse, w_r, evicted, workspace)."""
+    _check_decode_args(q, k_cache, v_cache, lens, n_e, s_k, s_v, S, k_new, v_new, out, lse, w_r,
+                       workspace, 0, evicted=evicted, need_new=True)
     cap = k_cache.shape[2]
     p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
                       scale=scale, tau=tau, n_split=n_split, summary=0)
     dev = q.device
     if out is None:
         out = torch.empty_like(q)
-    nbytes = momentkv_decode_evict_workspace_size(p)
+    nbytes = momentkv_decode_evict_workspace_bytes(p)
     if nbytes == 0:
         code = lib().momentkv_decode_evict(ctypes.byref(p), int(budget), *([None] * 14), None,
                                            0, None)

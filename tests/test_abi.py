@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert mk.momentkv_abi_version() == 4
+    assert mk.momentkv_abi_version() == 5
     for code in range(10):
         assert mk.momentkv_status_string(code) not in ("", "unknown status")
     assert mk.momentkv_status_string(99) == "unknown status"
@@ -53,7 +53,7 @@ def dparams(**kw):
 def compress_status(p, ptr=1 << 20, ws_bytes=None, ws=1 << 40):
     """Call momentkv_compress with fake, non-overlapping device addresses; validation must
     reject the call before any of them is touched."""
-    size = mk.momentkv_compress_workspace_size(p)
+    size = mk.momentkv_compress_workspace_bytes(p)
     if ws_bytes is None:
         ws_bytes = size
     step = 1 << 36
@@ -62,7 +62,7 @@ def compress_status(p, ptr=1 << 20, ws_bytes=None, ws=1 << 40):
 
 
 def decode_status(p, ptr=1 << 20, ws=1 << 40, ws_bytes=None, k_new=True):
-    size = mk.momentkv_decode_workspace_size(p)
+    size = mk.momentkv_decode_workspace_bytes(p)
     if ws_bytes is None:
         ws_bytes = size
     step = 1 << 36
@@ -72,14 +72,27 @@ def decode_status(p, ptr=1 << 20, ws=1 << 40, ws_bytes=None, k_new=True):
     return mk.lib().momentkv_decode_attn(ctypes.byref(p), *ptrs, ws, ws_bytes, None)
 
 
+def test_workspace_bytes_and_earlier_size_names_agree(L):
+    """The *_workspace_bytes queries and the earlier *_workspace_size names are one
+    function each."""
+    for p in (cparams(), cparams(budget=2048, ctx_len=131072, window=64), cparams(head_dim=96)):
+        assert L.momentkv_compress_workspace_bytes(ctypes.byref(p)) == \
+            L.momentkv_compress_workspace_size(ctypes.byref(p))
+    for p in (dparams(), dparams(max_len=2048, cap=2048), dparams(max_len=641)):
+        assert L.momentkv_decode_workspace_bytes(ctypes.byref(p)) == \
+            L.momentkv_decode_workspace_size(ctypes.byref(p))
+        assert L.momentkv_decode_evict_workspace_bytes(ctypes.byref(p)) == \
+            L.momentkv_decode_evict_workspace_size(ctypes.byref(p))
+
+
 def test_workspace_sizes(L):
-    assert mk.momentkv_compress_workspace_size(cparams()) > 0
-    assert mk.momentkv_decode_workspace_size(dparams()) > 0
-    assert mk.momentkv_compress_workspace_size(cparams(head_dim=96)) == 0
-    assert mk.momentkv_decode_workspace_size(dparams(max_len=641)) == 0
+    assert mk.momentkv_compress_workspace_bytes(cparams()) > 0
+    assert mk.momentkv_decode_workspace_bytes(dparams()) > 0
+    assert mk.momentkv_compress_workspace_bytes(cparams(head_dim=96)) == 0
+    assert mk.momentkv_decode_workspace_bytes(dparams(max_len=641)) == 0
     # size grows with context and with budget
-    assert mk.momentkv_compress_workspace_size(cparams(ctx_len=131072, window=64, budget=1024, cap=1024)) > \
-        mk.momentkv_compress_workspace_size(cparams())
+    assert mk.momentkv_compress_workspace_bytes(cparams(ctx_len=131072, window=64, budget=1024, cap=1024)) > \
+        mk.momentkv_compress_workspace_bytes(cparams())
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -116,7 +129,7 @@ def test_compress_rejects_null_alias_and_small_workspace(L):
     # k_out aliasing k
     ptrs = [(1 << 20) + i * (1 << 36) for i in range(11)]
     ptrs[3] = ptrs[1]
-    size = mk.momentkv_compress_workspace_size(p)
+    size = mk.momentkv_compress_workspace_bytes(p)
     assert mk.lib().momentkv_compress(ctypes.byref(p), *ptrs, None, 1 << 40, size, None) == ALIAS
     # workspace overlapping v
     ptrs = [(1 << 20) + i * (1 << 36) for i in range(11)]
@@ -126,14 +139,14 @@ def test_compress_rejects_null_alias_and_small_workspace(L):
 def test_adaptive_workspace_and_capacity(L):
     rows = 1 + 32 + 8 * 479
     p = cparams(adaptive=1, cap=rows)
-    assert mk.momentkv_compress_workspace_size(p) > mk.momentkv_compress_workspace_size(cparams())
+    assert mk.momentkv_compress_workspace_bytes(p) > mk.momentkv_compress_workspace_bytes(cparams())
     assert mk.compress_rows(32768, 8, 512, 32, 1, adaptive=True) == rows
     assert compress_status(cparams(adaptive=1, cap=rows - 1)) == CAPACITY
 
 
 def test_budget_at_least_context_is_valid(L):
     p = cparams(ctx_len=300, budget=5000, cap=300)
-    assert mk.momentkv_compress_workspace_size(p) > 0
+    assert mk.momentkv_compress_workspace_bytes(p) > 0
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -160,7 +173,7 @@ def test_decode_rejects_null_alias_and_small_workspace(L):
     assert decode_status(p, ws_bytes=8) == WORKSPACE
     ptrs = [(1 << 20) + i * (1 << 36) for i in range(13)]
     ptrs[10] = ptrs[1]                                   # out aliases the key cache
-    size = mk.momentkv_decode_workspace_size(p)
+    size = mk.momentkv_decode_workspace_bytes(p)
     assert mk.lib().momentkv_decode_attn(ctypes.byref(p), *ptrs, 1 << 40, size, None) == ALIAS
 
 
@@ -179,7 +192,7 @@ def test_prepared_summary_size_and_validation(L):
 
 
 def evict_status(p, budget, ptr=1 << 20, ws=1 << 40, ws_bytes=None, drop=None):
-    size = mk.momentkv_decode_evict_workspace_size(p)
+    size = mk.momentkv_decode_evict_workspace_bytes(p)
     if ws_bytes is None:
         ws_bytes = size
     ptrs = [ptr + i * (1 << 36) if ptr else None for i in range(14)]
@@ -190,11 +203,11 @@ def evict_status(p, budget, ptr=1 << 20, ws=1 << 40, ws_bytes=None, drop=None):
 
 def test_decode_evict_sizes_and_validation(L):
     p = dparams()
-    size = mk.momentkv_decode_evict_workspace_size(p)
+    size = mk.momentkv_decode_evict_workspace_bytes(p)
     # per head: (G + 2) fp32 record planes of max_len rows and (G + 1) running maxima per
     # 32-row block, after the 256-byte flag
     assert size >= 256 + 36 * 8 * (6 * 640 + 5 * 20) * 4
-    assert mk.momentkv_decode_evict_workspace_size(dparams(summary=1)) == 0
+    assert mk.momentkv_decode_evict_workspace_bytes(dparams(summary=1)) == 0
     assert evict_status(p, 0) == BUDGET
     assert evict_status(dparams(summary=1), 512) == SHAPE
     assert evict_status(dparams(head_dim=80), 512) == UNSUP
@@ -210,3 +223,69 @@ def test_decode_evict_sizes_and_validation(L):
     ptrs = [(1 << 20) + i * (1 << 36) for i in range(14)]
     ptrs[9] = ptrs[1]                         # S overlaps the key cache
     assert mk.lib().momentkv_decode_evict(ctypes.byref(p), 512, *ptrs, 1 << 40, size, None) == ALIAS
+
+
+# ------------------------------------------------ binding-side tensor validation (CPU)
+def _decode_tensors(B=2, Hq=8, Hkv=2, d=64, cap=16, dt=None):
+    import torch
+    dt = dt or torch.bfloat16
+    f32, i32 = torch.float32, torch.int32
+    return dict(q=torch.zeros(B, Hq, d, dtype=dt), k_cache=torch.zeros(B, Hkv, cap, d, dtype=dt),
+                v_cache=torch.zeros(B, Hkv, cap, d, dtype=dt), lens=torch.zeros(B, Hkv, dtype=i32),
+                n_e=torch.zeros(B, Hkv, dtype=i32), s_k=torch.zeros(B, Hkv, d, dtype=f32),
+                s_v=torch.zeros(B, Hkv, d, dtype=f32), S=torch.zeros(B, Hkv, d, d, dtype=f32))
+
+
+@pytest.mark.parametrize("name,bad", [
+    ("lens", lambda t: t.long()),
+    ("n_e", lambda t: t[:, :1]),
+    ("s_k", lambda t: t.bfloat16()),
+    ("S", lambda t: t[..., :32]),
+    ("v_cache", lambda t: t.float()),
+])
+def test_decode_binding_rejects_wrong_tensors_before_the_library(name, bad):
+    """A wrong dtype or shape is a ValueError naming the tensor, raised before any pointer
+    reaches the library (an int64 lens or a short summary would be read out of bounds)."""
+    t = _decode_tensors()
+    t[name] = bad(t[name])
+    with pytest.raises(ValueError, match=name):
+        mk.momentkv_decode_attn(**t)
+    with pytest.raises(ValueError, match=name):
+        mk.momentkv_decode_evict(**t, k_new=t["q"][:, :2].clone(), v_new=t["q"][:, :2].clone(),
+                                 budget=4)
+
+
+def test_decode_binding_checks_summary_form_new_rows_and_device():
+    import torch
+    t = _decode_tensors()
+    with pytest.raises(ValueError, match="prepared"):      # summary=1 wants the bf16 planes
+        mk.momentkv_decode_attn(**t, summary=1)
+    with pytest.raises(ValueError, match="together"):
+        mk.momentkv_decode_attn(**t, k_new=torch.zeros(2, 2, 64, dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="required"):
+        mk.momentkv_decode_evict(**t, k_new=None, v_new=None, budget=4)
+    with pytest.raises(ValueError, match="k_new"):
+        mk.momentkv_decode_attn(**t, k_new=torch.zeros(2, 2, 64), v_new=torch.zeros(2, 2, 64))
+    with pytest.raises(ValueError, match="lse"):
+        mk.momentkv_decode_attn(**t, lse=torch.zeros(2, 8, dtype=torch.float64))
+    with pytest.raises(ValueError, match="on the GPU"):    # right shapes, host memory
+        mk.momentkv_decode_attn(**t)
+
+
+def test_compress_and_prepare_binding_reject_wrong_tensors():
+    import torch
+    q = torch.zeros(1, 8, 4, 64, dtype=torch.bfloat16)
+    k = torch.zeros(1, 2, 100, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="v"):
+        mk.momentkv_compress(q, k, k.float(), 20)
+    with pytest.raises(ValueError, match="q_win"):
+        mk.momentkv_compress(q[:, :, :, :32], k, k, 20)
+    with pytest.raises(ValueError, match="on the GPU"):
+        mk.momentkv_compress(q, k, k, 20)
+    t = _decode_tensors()
+    with pytest.raises(ValueError, match="n_e"):
+        mk.momentkv_prepare_summary(t["n_e"].long(), t["s_k"], t["s_v"], t["S"],
+                                    dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="out"):
+        mk.momentkv_prepare_summary(t["n_e"], t["s_k"], t["s_v"], t["S"], dtype=torch.bfloat16,
+                                    out=torch.zeros(2, 2, 64, 64, dtype=torch.bfloat16))
