@@ -13,18 +13,25 @@
 //                     provisional score abar_j ||v_j||, added to the key histogram of
 //                     the first selection.                                 [reads K]
 //   4 k_tk_*          per head: radix select of the k_keep best scores, lower position
-//                     first on ties; writes the kept positions in ascending order.
-//   5 k_gather_rows   rows of the provisional kept set into a compact buffer.
-//   6 k_cov_rows      their covariance and sums, stored negated as extra partial slots.
-//   7 k_reduce        fixed-order sum of all slots = raw moments of the provisional
-//                     evicted set.
+//                     first on ties; writes the kept positions in ascending order, and
+//                     the evicted ones too when they are fewer.
+//   6 k_cov_rows      covariance and sums of the provisional kept rows (read through
+//                     their positions), stored negated as extra partial slots; when the
+//                     evicted rows are fewer than the kept ones, of the evicted rows
+//                     instead, stored as they are.
+//   7 k_reduce        fixed-order sum of the slots = raw moments of the provisional
+//                     evicted set: all slots (the candidates' minus the kept rows'), or
+//                     only the evicted rows' slots.  Summing the evicted rows directly
+//                     when they are the fewer keeps the cancellation of S_C - S_kept from
+//                     growing with the ratio of candidates to evicted rows.
 //   8 k_residual      per (slice, head): centring and clamp of the provisional summary
 //                     into LDS (fp32, or a bf16 hi/lo pair), S_tilde k_j on MFMA,
 //                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm,
 //                     added to the final selection's key histogram.       [reads K, V]
 //   9 k_tk_*          final kept set.
 //  10 k_gather_out    retained rows (sinks, kept, window) -> k_out/v_out, idx, lens.
-//  11 k_cov_rows      covariance of the final kept rows (from k_out), negated.
+//  11 k_cov_rows      covariance of the final kept rows, negated (or of the final
+//                     evicted rows when fewer).
 //  12 k_reduce        final raw moments S, s_k, s_v, n_e.
 // Every reduction has a fixed order, so results are bit-reproducible.
 #include "mkv_bf16.h"
@@ -56,6 +63,13 @@ constexpr int TK_HBINS = 2048;     // bins of the per-head histogram (key bits 3
 // the buffers, since it sizes reads and writes).
 __device__ __forceinline__ int head_keep(const CompressArgs& a, int head) {
   return a.kh ? min(max(a.kh[head], 0), a.kmax) : a.k_keep;
+}
+
+// A head whose evicted candidates are fewer than its kept ones gets its moments summed
+// over the evicted rows; the others as the candidates' sums minus the kept rows'.
+__device__ __forceinline__ bool direct_sums(const CompressArgs& a, int head) {
+  const int k = head_keep(a, head);
+  return a.n_c - k < k;
 }
 
 // Adds a workgroup's LDS histogram to the head's histogram in global memory (integer
@@ -831,7 +845,7 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
                                                     const int* __restrict__ cnt,
                                                     const uint32_t* __restrict__ cand,
                                                     int32_t* __restrict__ out, int out_stride,
-                                                    int pos_offset) {
+                                                    int pos_offset, int32_t* __restrict__ ev_out) {
   __shared__ int s_gt[TK_MAX_SLICES], s_cn[TK_MAX_SLICES], s_gtT[TK_MAX_SLICES], s_eqT[TK_MAX_SLICES];
   __shared__ __align__(16) uint32_t hst[1024];
   __shared__ uint32_t sh_bin, sh_above;
@@ -958,45 +972,53 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
     keep[u] = (valid[u] && key[u] > T) || (eq && eq_rank < need);
     eq_rank += eq;
   }
+  // p = kept positions before the thread's current one, so a position that is not kept
+  // is the (j - p)-th evicted one
   int p = s_off + (before & 0xFFFF) + min(max(need - s_eqb, 0), before >> 16);
   int32_t* o = out + (size_t)head * out_stride;
+  const bool want_ev = ev_out != nullptr && n - k < k;  // uniform over the workgroup
+  int32_t* eo = ev_out ? ev_out + (size_t)head * out_stride : nullptr;
   const int j0 = sl * TKS + TKPT * tid;
 #pragma unroll
   for (int u = 0; u < TKPT; ++u) {
     if (keep[u]) {
       if (p < k) o[p] = j0 + u + pos_offset;
       ++p;
+    } else if (want_ev && valid[u]) {
+      const int e = j0 + u - p;
+      if (e >= 0 && e < n - k) eo[e] = j0 + u + pos_offset;
     }
   }
 }
 
 // ------------------------------------------------------------------------------------
-// Stage 5: rows of the provisional kept set -> compact buffer [H, kmax, D].
+// Stage 6/11: covariance and sums of one head's kept rows (stored negated) or, when they
+// are fewer, of its evicted rows (stored as they are), read through their positions, into
+// the slots after the candidate slices.
 // ------------------------------------------------------------------------------------
-template <class T, int D>
-__global__ void __launch_bounds__(256) k_gather_rows(CompressArgs a) {
-  constexpr int DG = D / 8;
-  const int head = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  const int i = c / DG, dg = c % DG;
-  if (i >= head_keep(a, head)) return;
-  // kept positions are read as addresses: clamped to the context, so that no selection
-  // result can move a read outside the head's rows
-  const int pos = min(max(a.kept0[(size_t)head * a.kmax + i], 0), a.N - 1);
-  const size_t src = ((size_t)head * a.N + pos) * D + 8 * dg;
-  const size_t dst = ((size_t)head * a.kmax + i) * D + 8 * dg;
-  store_frag(reinterpret_cast<T*>(a.gath_k) + dst, load_frag(reinterpret_cast<const T*>(a.k) + src));
-  store_frag(reinterpret_cast<T*>(a.gath_v) + dst, load_frag(reinterpret_cast<const T*>(a.v) + src));
+// Rows list[row0 + 2p] and list[row0 + 2p + 1] of K and V (head base pointers), list
+// entries clamped to the n_rows given and the positions to the head's N rows; issued as
+// tile_load issues its rows.
+template <class T, int D, int NT>
+__device__ __forceinline__ void tile_load_list(TileRegs<T, D, NT>& R, const T* Kh, const T* Vh,
+                                               const int32_t* list, int row0, int n_rows, int N,
+                                               int tid) {
+  typedef TileRegs<T, D, NT> TR;
+  const int col = 8 * TR::group(tid);
+#pragma unroll
+  for (int i = 0; i < TR::NP; ++i) {
+    const int p = TR::pair(tid, i);
+    const int j0 = min(max(list[min(row0 + 2 * p, n_rows - 1)], 0), N - 1);
+    const int j1 = min(max(list[min(row0 + 2 * p + 1, n_rows - 1)], 0), N - 1);
+    R.k[i][0] = load_frag(Kh + (size_t)j0 * D + col);
+    R.k[i][1] = load_frag(Kh + (size_t)j1 * D + col);
+    R.v[i][0] = load_frag(Vh + (size_t)j0 * D + col);
+    R.v[i][1] = load_frag(Vh + (size_t)j1 * D + col);
+  }
 }
 
-// ------------------------------------------------------------------------------------
-// Stage 6/11: covariance and sums of `nrows` consecutive rows, stored negated into the
-// slots after the candidate slices.
-// ------------------------------------------------------------------------------------
 template <class T, int D>
-__global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kbase,
-                                                   const void* vbase, int head_rows,
-                                                   int row_off, int nrows) {
+__global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const int32_t* kept_list) {
   constexpr int NT = 256, NW = 4;
   constexpr int PAD = 16 / (int)sizeof(T);
   constexpr int LDT = TILE + PAD;
@@ -1006,9 +1028,12 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kb
   __shared__ __align__(16) T sVT[D][LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, sl = blockIdx.x;
-  if (nrows < 0) nrows = head_keep(a, head);  // the head's own kept count
-  const T* Kh = reinterpret_cast<const T*>(kbase) + ((size_t)head * head_rows + row_off) * D;
-  const T* Vh = reinterpret_cast<const T*>(vbase) + ((size_t)head * head_rows + row_off) * D;
+  const int kh = head_keep(a, head);
+  const bool direct = direct_sums(a, head);
+  const int nrows = direct ? a.n_c - kh : kh;
+  const int32_t* list = (direct ? a.evl : kept_list) + (size_t)head * a.kmax;
+  const T* Kh = reinterpret_cast<const T*>(a.k) + (size_t)head * a.N * D;
+  const T* Vh = reinterpret_cast<const T*>(a.v) + (size_t)head * a.N * D;
   f32x4 cacc[QM][QN];
 #pragma unroll
   for (int mi = 0; mi < QM; ++mi)
@@ -1021,25 +1046,26 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const void* kb
   const int ntiles = (nrows + TILE - 1) / TILE;
   const int t_beg = sl * a.tpsr, t_end = min(t_beg + a.tpsr, ntiles);
   TR R;
-  if (t_beg < t_end) tile_load<T, D, NT>(R, Kh, Vh, t_beg * TILE, nrows, tid);
+  if (t_beg < t_end) tile_load_list<T, D, NT>(R, Kh, Vh, list, t_beg * TILE, nrows, a.N, tid);
   for (int t = t_beg; t < t_end; ++t) {
     float ss[TR::NP][2];
     R.arrive();
     tile_store_t<T, D, NT, LDT>(R, sKT, sVT, t * TILE, in_rows, sk, sv, ss, tid);
-    if (t + 1 < t_end) tile_load<T, D, NT>(R, Kh, Vh, (t + 1) * TILE, nrows, tid);
+    if (t + 1 < t_end) tile_load_list<T, D, NT>(R, Kh, Vh, list, (t + 1) * TILE, nrows, a.N, tid);
     __syncthreads();
     cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
   }
-  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, -1.f,
+  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, direct ? 1.f : -1.f,
                               reinterpret_cast<float*>(&sVT[0][0]), tid);
 }
 
 // ------------------------------------------------------------------------------------
 // Stage 7/12: fixed-order sum of the partial slots -> raw S, s_v, s_k of the evicted set
-// (stage 7: the provisional set, into the workspace; stage 12: the output moments).
+// (stage 7: the provisional set, into the workspace; stage 12: the output moments): every
+// slot, or only the evicted rows' slots of a head that sums them directly.
 // Eight lanes per float4 of a head's D*D + 2D values, lane `sub` summing slots
-// sub, sub+8, ..., then a fixed xor tree across the eight lanes.
+// s0 + sub, s0 + sub + 8, ..., then a fixed xor tree across the eight lanes.
 // ------------------------------------------------------------------------------------
 template <int D>
 __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, float* sv_out,
@@ -1049,13 +1075,14 @@ __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, fl
   const int f4 = blockIdx.x * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int s0 = direct_sums(a, head) ? a.nsl1 : 0;
   if (f4 < NF4) {
     const bool in_S = f4 < NSF4;
     const float* base = in_S ? a.spart + (size_t)head * a.nslot * D * D + 4 * f4
                              : a.svkpart + (size_t)head * a.nslot * 2 * D + 4 * (f4 - NSF4);
     const size_t stride = in_S ? (size_t)D * D : (size_t)2 * D;
 #pragma unroll 4
-    for (int sl = sub; sl < a.nslot; sl += 8) {
+    for (int sl = s0 + sub; sl < a.nslot; sl += 8) {
       const float4 p = *reinterpret_cast<const float4*>(base + sl * stride);
       acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
     }
@@ -1314,7 +1341,7 @@ static hipError_t launch_topk(const CompressArgs& a, const float* scores, int wh
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep, (const int*)a.kh,
                      (const int*)a.tk_state, (const int*)a.tk_cnt, (const uint32_t*)a.tk_cand, out,
-                     a.kmax, a.n_s);
+                     a.kmax, a.n_s, a.evl);
   MKV_CHECK_LAUNCH();
   return hipSuccess;
 }
@@ -1348,7 +1375,7 @@ static hipError_t launch_head_budgets(const CompressArgs& a, hipStream_t st) {
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, (const float*)a.abar, n, k,
                      (const int*)nullptr, (const int*)a.tk_state_g, (const int*)a.tk_cnt_g,
-                     (const uint32_t*)a.tk_cand_g, a.kept_all, k, 0);
+                     (const uint32_t*)a.tk_cand_g, a.kept_all, k, 0, (int32_t*)nullptr);
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL(k_ada_counts, dim3(a.B), dim3(64), 0, st, a);
   MKV_CHECK_LAUNCH();
@@ -1384,10 +1411,7 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
   const dim3 red_grid(((D * D + 2 * D) / 4 + 31) / 32, H);
   if (a.mi_rounds >= 1) {
     if (a.k_keep > 0) {
-      hipLaunchKernelGGL((k_gather_rows<T, D>), dim3((a.kmax * (D / 8) + 255) / 256, H), blk, 0, st, a);
-      MKV_CHECK_LAUNCH();
-      hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const void*)a.gath_k,
-                         (const void*)a.gath_v, a.kmax, 0, a.kh ? -1 : a.k_keep);
+      hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const int32_t*)a.kept0);
       MKV_CHECK_LAUNCH();
     }
     hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.s0, a.sv0, a.sk0, (int32_t*)nullptr);
@@ -1402,8 +1426,7 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
                      a.L, 0);
   MKV_CHECK_LAUNCH();
   if (a.k_keep > 0) {
-    hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const void*)a.k_out,
-                       (const void*)a.v_out, a.cap, a.n_s, a.kh ? -1 : a.k_keep);
+    hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const int32_t*)a.kept);
     MKV_CHECK_LAUNCH();
   }
   hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.S, a.s_v, a.s_k, a.n_e);

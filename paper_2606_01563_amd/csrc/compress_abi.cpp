@@ -86,7 +86,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.nsl2 = clampi(ceil_div(1024, a.H), 1, a.ntile);
   a.tps2 = std::min(ceil_div(a.ntile, a.nsl2), mkv::kMassMaxTiles);
   a.nsl2 = ceil_div(a.ntile, a.tps2);
-  // downdate covariance over the kept rows
+  // covariance over the kept rows (subtracted) or the evicted rows, whichever are fewer
   if (a.k_keep > 0) {
     const int ntr = ceil_div(a.kmax, 64);  // the most rows any head keeps
     a.nslr = clampi(ceil_div(256, a.H), 1, ntr);
@@ -107,7 +107,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   // top-k slices of 2048 candidates (at most 128 for kMaxCandidates)
   a.ntk = ceil_div(a.n_c > 0 ? a.n_c : 1, 2048);
   a.ntk_g = a.adaptive ? ceil_div(a.Hkv * a.n_c, 2048) : 1;
-  const size_t H = a.H, D = a.D, es = elem_size(p->dtype);
+  const size_t H = a.H, D = a.D;
   const size_t nc = a.n_c > 0 ? a.n_c : 1;
   Carver c;
   c.base = static_cast<char*>(ws);
@@ -128,8 +128,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.s0 = c.take<float>(H * D * D * sizeof(float));
   a.sv0 = c.take<float>(H * D * sizeof(float));
   a.sk0 = c.take<float>(H * D * sizeof(float));
-  a.gath_k = c.take<void>(H * a.kmax * D * es);
-  a.gath_v = c.take<void>(H * a.kmax * D * es);
+  a.evl = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
   if (a.adaptive) {
     const size_t Bs = a.B;
     a.kh = c.take<int32_t>(H * sizeof(int32_t));

@@ -176,7 +176,10 @@ def decode_bounds(q, K, lz_ref, w_ref, m: "O.Moments", *, amplify: float = 1.0,
       log Z_E   log n_e + scale q.s_k / n_e: gamma(d+1) of the absolute terms, 3u of the
                 terms themselves, plus `sk_err` (relative) for a key sum that was itself
                 accumulated on the GPU in fp32;
-      w_R       w_R (1 - w_R) (|d log Z_R| + |d log Z_E|), 1.05 for second order, + 4u."""
+      w_R       w_R = exp(log Z_R - lse) with lse = logsumexp(log Z_R, log Z_E): the errors
+                of the two logs move it by w_R (1 - w_R) (|d log Z_R| + |d log Z_E|) (1.05 for
+                second order); lse's own roundings (the max, the log, the add) move it by
+                w_R 4u (|log Z_R| + |log Z_E| + 2); the exp 4u."""
     d = q.shape[0]
     scale = 1.0 / math.sqrt(d)
     if K.shape[0] > 0:
@@ -193,7 +196,9 @@ def decode_bounds(q, K, lz_ref, w_ref, m: "O.Moments", *, amplify: float = 1.0,
         3 * U32 * (abs(math.log(m.n_e)) + abs(sbar))
     if not math.isfinite(lz_ref):
         return dlz, 4 * U32
-    dw = 1.05 * w_ref * (1.0 - w_ref) * (dlz + dlze) + 4 * U32
+    lze = math.log(m.n_e) + sbar
+    dw = 1.05 * w_ref * (1.0 - w_ref) * (dlz + dlze) + \
+        w_ref * 4 * U32 * (abs(lz_ref) + abs(lze) + 2.0) + 4 * U32
     return dlz, dw
 
 

@@ -170,6 +170,24 @@ def test_long_window_group_rows_256():
     P.run_decode_steps(gpu, out, 2)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("budget", [8100, 33 + 4080, 33 + 4079])
+def test_budget_close_to_context_sums_the_evicted_rows(dtype, budget):
+    """A budget close to the context evicts few candidates (92 of 8159 at 8100): the
+    moments are then summed over the evicted rows themselves, which are fewer than the kept
+    ones, so they stay within 1e-5 however small n_e is (the candidates' sums minus the
+    kept rows' would lose about n_c / n_e times more).  Both sides of the switch: 4079
+    evicted against 4080 kept (direct) and 4080 against 4079 (subtracted)."""
+    wl, cpu, gpu = layer("llama31_8b_layer_n8192", steps=2, n_q_heads=8, n_kv_heads=2,
+                         dtype=dtype)
+    announce(f"budget {budget} of {wl.ctx_len} {dtype}")
+    out = P.run_compress(gpu, budget, cap=budget + 2)
+    for h in range(2):
+        errs = P.check_compress_head(cpu, out, 0, h, budget)
+        announce(f"head {h}: n_e {int(out.n_e[0, h])} S rel err {errs['S']:.2e}")
+    P.run_decode_steps(gpu, out, 2)
+
+
 @pytest.mark.parametrize("order", [0, -1])
 def test_zeroth_order_or_no_correction_decode_and_no_append(order):
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, ctx_len=600, budgets=(64,))
