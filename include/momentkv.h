@@ -240,6 +240,35 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
                                 void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * Decode without a workspace argument.  For callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * Computes exactly what momentkv_decode_attn computes (the same kernels, so the same bits)
+ * with the same arguments, except:
+ *   - the workspace is a library-owned device array of MOMENTKV_NOALLOC_SCRATCH_BYTES on
+ *     each GPU the library runs on, held until the process ends; calls for which
+ *     momentkv_decode_workspace_bytes(p) exceeds it return MKV_ERR_WORKSPACE (at 16 MiB:
+ *     e.g. 2048 KV heads at G = 4, d = 128 and max_len <= 384);
+ *   - flag: NULL, or a device int32 set to 1 when an append finds a full cache (sticky,
+ *     the caller zeroes it); with NULL that event is not reported.
+ * No hipMalloc, hipFree or allocating library routine is called.  The array's device
+ * address is looked up once per device, on the first call with that device current;
+ * `stream` must belong to the current device (MKV_ERR_UNSUPPORTED otherwise).  Every call
+ * on one GPU uses that GPU's array, which keeps the last call's contents (nothing in it
+ * needs to start at zero): calls that overlap in time on one GPU (on different streams,
+ * or from host threads without ordering between them) race on it and must not be issued;
+ * calls on one stream are ordered.
+ * ---------------------------------------------------------------------------------- */
+#define MOMENTKV_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+mkv_status momentkv_decode_attn_noalloc(const mkv_decode_params* p, const void* q,
+                                        void* k_cache, void* v_cache, int32_t* lens,
+                                        const void* k_new, const void* v_new,
+                                        const int32_t* n_e, const float* s_k, const float* s_v,
+                                        const void* S, void* out, float* lse_out,
+                                        float* w_r_out, int32_t* flag, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * Decode step with moment-informed eviction (Algorithm 1, Phase 1 then Phase 2)
  *
  * Per (b, h) and its G queries q_g (query heads hG .. hG + G - 1):

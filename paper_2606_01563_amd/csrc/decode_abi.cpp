@@ -94,6 +94,51 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   return a;
 }
 
+mkv_status check_decode_buffers(const mkv_decode_params* p, const void* q, const void* k_cache,
+                                const void* v_cache, const int32_t* lens, const void* k_new,
+                                const void* v_new, const int32_t* n_e, const float* s_k,
+                                const float* s_v, const void* S, const void* out) {
+  if (!q || !k_cache || !v_cache || !lens || !n_e || !s_k || !s_v || !S || !out) return MKV_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return MKV_ERR_NULL;
+  const size_t es = elem_size(p->dtype);
+  const size_t cache_bytes = (size_t)p->batch * p->n_kv_heads * p->cap * p->head_dim * es;
+  const size_t out_bytes = (size_t)p->batch * p->n_q_heads * p->head_dim * es;
+  if (ranges_overlap(out, out_bytes, k_cache, cache_bytes) ||
+      ranges_overlap(out, out_bytes, v_cache, cache_bytes) ||
+      ranges_overlap(out, out_bytes, q, out_bytes) ||
+      ranges_overlap(k_cache, cache_bytes, v_cache, cache_bytes))
+    return MKV_ERR_ALIAS;
+  return MKV_OK;
+}
+
+bool decode_overlaps(const mkv_decode_params* p, const void* buf, size_t bytes,
+                     const void* k_cache, const void* v_cache, const void* out) {
+  const size_t es = elem_size(p->dtype);
+  const size_t cache_bytes = (size_t)p->batch * p->n_kv_heads * p->cap * p->head_dim * es;
+  const size_t out_bytes = (size_t)p->batch * p->n_q_heads * p->head_dim * es;
+  return ranges_overlap(buf, bytes, k_cache, cache_bytes) ||
+         ranges_overlap(buf, bytes, v_cache, cache_bytes) || ranges_overlap(buf, bytes, out, out_bytes);
+}
+
+void set_decode_buffers(DecodeArgs& a, const void* q, void* k_cache, void* v_cache, int32_t* lens,
+                        const void* k_new, const void* v_new, const int32_t* n_e, const float* s_k,
+                        const float* s_v, const void* S, void* out, float* lse_out,
+                        float* w_r_out) {
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.lens = lens;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.n_e = n_e;
+  a.s_k = s_k;
+  a.s_v = s_v;
+  a.S = static_cast<const float*>(S);
+  a.out = out;
+  a.lse_out = lse_out;
+  a.w_r_out = w_r_out;
+}
+
 }  // namespace abi
 }  // namespace mkv
 
@@ -148,38 +193,17 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
                                 void* stream) {
   mkv_status st = check_decode_params(p);
   if (st != MKV_OK) return st;
-  if (!q || !k_cache || !v_cache || !lens || !n_e || !s_k || !s_v || !S || !out) return MKV_ERR_NULL;
-  if ((k_new == nullptr) != (v_new == nullptr)) return MKV_ERR_NULL;
+  st = check_decode_buffers(p, q, k_cache, v_cache, lens, k_new, v_new, n_e, s_k, s_v, S, out);
+  if (st != MKV_OK) return st;
   size_t need = 0;
   decode_layout(p, nullptr, &need);
   if (!workspace || workspace_bytes < need) return MKV_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return MKV_ERR_WORKSPACE;
-  const size_t es = elem_size(p->dtype);
-  const size_t cache_bytes = (size_t)p->batch * p->n_kv_heads * p->cap * p->head_dim * es;
-  const size_t out_bytes = (size_t)p->batch * p->n_q_heads * p->head_dim * es;
-  if (ranges_overlap(out, out_bytes, k_cache, cache_bytes) ||
-      ranges_overlap(out, out_bytes, v_cache, cache_bytes) ||
-      ranges_overlap(out, out_bytes, q, out_bytes) ||
-      ranges_overlap(k_cache, cache_bytes, v_cache, cache_bytes) ||
-      ranges_overlap(workspace, need, k_cache, cache_bytes) ||
-      ranges_overlap(workspace, need, v_cache, cache_bytes) ||
-      ranges_overlap(workspace, need, out, out_bytes))
-    return MKV_ERR_ALIAS;
+  if (decode_overlaps(p, workspace, need, k_cache, v_cache, out)) return MKV_ERR_ALIAS;
   size_t total = 0;
   mkv::DecodeArgs a = decode_layout(p, workspace, &total);
-  a.q = q;
-  a.k_cache = k_cache;
-  a.v_cache = v_cache;
-  a.lens = lens;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.n_e = n_e;
-  a.s_k = s_k;
-  a.s_v = s_v;
-  a.S = static_cast<const float*>(S);
-  a.out = out;
-  a.lse_out = lse_out;
-  a.w_r_out = w_r_out;
+  set_decode_buffers(a, q, k_cache, v_cache, lens, k_new, v_new, n_e, s_k, s_v, S, out, lse_out,
+                     w_r_out);
   hipError_t e = mkv::launch_decode(a, p->dtype == MKV_BF16, p->head_dim,
                                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MKV_OK : MKV_ERR_HIP;

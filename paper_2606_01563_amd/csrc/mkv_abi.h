@@ -38,6 +38,19 @@ inline size_t elem_size(int32_t dtype) { return dtype == MKV_BF16 ? 2 : 4; }
 // Decode parameters and workspace layout (defined with the decode entry points).
 mkv_status check_decode_params(const mkv_decode_params* p);
 DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* total);
+// Required pointers present and the caches, query and output disjoint.
+mkv_status check_decode_buffers(const mkv_decode_params* p, const void* q, const void* k_cache,
+                                const void* v_cache, const int32_t* lens, const void* k_new,
+                                const void* v_new, const int32_t* n_e, const float* s_k,
+                                const float* s_v, const void* S, const void* out);
+// Whether [buf, buf + bytes) overlaps the caches or the output.
+bool decode_overlaps(const mkv_decode_params* p, const void* buf, size_t bytes,
+                     const void* k_cache, const void* v_cache, const void* out);
+// The caller's buffers into the argument block.
+void set_decode_buffers(DecodeArgs& a, const void* q, void* k_cache, void* v_cache, int32_t* lens,
+                        const void* k_new, const void* v_new, const int32_t* n_e, const float* s_k,
+                        const float* s_v, const void* S, void* out, float* lse_out,
+                        float* w_r_out);
 
 }  // namespace abi
 }  // namespace mkv

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libmomentkv.so")
 HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "momentkv.h")
 
 MKV_F32, MKV_BF16 = 0, 1
+NOALLOC_SCRATCH_BYTES = 16 << 20   # MOMENTKV_NOALLOC_SCRATCH_BYTES
 STATUS = {0: "MKV_OK", 1: "MKV_ERR_NULL", 2: "MKV_ERR_SHAPE", 3: "MKV_ERR_BUDGET",
           4: "MKV_ERR_DTYPE", 5: "MKV_ERR_WORKSPACE", 6: "MKV_ERR_CAPACITY",
           7: "MKV_ERR_ALIAS", 8: "MKV_ERR_HIP", 9: "MKV_ERR_UNSUPPORTED"}
@@ -81,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.momentkv_decode_attn.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 13 + \
             [_VP, ctypes.c_size_t, _VP]
         L.momentkv_decode_attn.restype = ctypes.c_int
+        L.momentkv_decode_attn_noalloc.argtypes = [ctypes.POINTER(DecodeParams)] + [_VP] * 15
+        L.momentkv_decode_attn_noalloc.restype = ctypes.c_int
         L.momentkv_status_string.argtypes = [ctypes.c_int32]
         L.momentkv_prepared_summary_size.argtypes = [ctypes.POINTER(DecodeParams)]
         L.momentkv_prepared_summary_size.restype = ctypes.c_size_t
@@ -433,6 +436,35 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     if code != 0:
         raise MomentKVError(code, "momentkv_decode_attn")
     return out, lse, w_r, ws
+
+
+def momentkv_decode_attn_noalloc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                                 lens: torch.Tensor, n_e: torch.Tensor, s_k: torch.Tensor,
+                                 s_v: torch.Tensor, S: torch.Tensor, *,
+                                 k_new: torch.Tensor | None = None,
+                                 v_new: torch.Tensor | None = None, max_len: int | None = None,
+                                 order: int = 1, scale: float = 0.0, tau: float = 1e-6,
+                                 n_split: int = 0, summary: int = 0, out: torch.Tensor,
+                                 lse: torch.Tensor | None = None, w_r: torch.Tensor | None = None,
+                                 flag: torch.Tensor | None = None):
+    """The corrected decode with no workspace argument (see the header): the library keeps
+    the partial results in its own per-GPU device array.  Every buffer, `out` included, is
+    the caller's, so nothing is allocated here either.  `flag`: None or a one-element int32
+    tensor that the call sets to 1 when an append finds a full cache.  Returns out."""
+    _check_decode_args(q, k_cache, v_cache, lens, n_e, s_k, s_v, S, k_new, v_new, out, lse, w_r,
+                       None, summary)
+    _expect(flag, "flag", (1,), torch.int32, optional=True)
+    _same_device(dict(q=q, flag=flag))
+    cap = k_cache.shape[2]
+    p = decode_params(q, k_cache, max_len=cap if max_len is None else max_len, order=order,
+                      scale=scale, tau=tau, n_split=n_split, summary=summary)
+    code = lib().momentkv_decode_attn_noalloc(
+        ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lens), _ptr(k_new),
+        _ptr(v_new), _ptr(n_e), _ptr(s_k), _ptr(s_v), _ptr(S), _ptr(out), _ptr(lse), _ptr(w_r),
+        _ptr(flag), _stream())
+    if code != 0:
+        raise MomentKVError(code, "momentkv_decode_attn_noalloc")
+    return out
 
 
 def momentkv_decode_evict(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,

@@ -289,3 +289,21 @@ def test_compress_and_prepare_binding_reject_wrong_tensors():
     with pytest.raises(ValueError, match="out"):
         mk.momentkv_prepare_summary(t["n_e"], t["s_k"], t["s_v"], t["S"], dtype=torch.bfloat16,
                                     out=torch.zeros(2, 2, 64, 64, dtype=torch.bfloat16))
+
+
+def test_noalloc_decode_rejects_requests_beyond_its_scratch_before_any_device_call(L):
+    """The decode that allocates nothing refuses work whose workspace would exceed its
+    16 MiB device array, and missing pointers, before touching the GPU."""
+    big = dparams(batch=4096, cap=4096, max_len=4096)
+    assert mk.momentkv_decode_workspace_bytes(big) > mk.NOALLOC_SCRATCH_BYTES
+    small = dparams()
+    assert mk.momentkv_decode_workspace_bytes(small) <= mk.NOALLOC_SCRATCH_BYTES
+    step = 1 << 36
+    ptrs = [(1 << 20) + i * step for i in range(13)]
+    assert L.momentkv_decode_attn_noalloc(ctypes.byref(big), *ptrs, None, None) == WORKSPACE
+    nulls = list(ptrs)
+    nulls[0] = None
+    assert L.momentkv_decode_attn_noalloc(ctypes.byref(small), *nulls, None, None) == NULL
+    assert L.momentkv_decode_attn_noalloc(ctypes.byref(dparams(head_dim=96)), *ptrs, None,
+                                          None) == UNSUP
+    assert L.momentkv_decode_attn_noalloc(None, *ptrs, None, None) == NULL
