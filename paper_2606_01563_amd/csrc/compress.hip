@@ -13,12 +13,12 @@
 //                     provisional score abar_j ||v_j||, added to the key histogram of
 //                     the first selection.                                 [reads K]
 //   4 k_tk_*          per head: radix select of the k_keep best scores, lower position
-//                     first on ties; writes the kept positions in ascending order, and
-//                     the evicted ones too when they are fewer.
-//   6 k_cov_rows      covariance and sums of the provisional kept rows (read through
-//                     their positions), stored negated as extra partial slots; when the
-//                     evicted rows are fewer than the kept ones, of the evicted rows
-//                     instead, stored as they are.
+//                     first on ties; writes the kept positions in ascending order; each
+//                     slice's workgroup
+//                     then adds the covariance and sums of its kept rows (read through
+//                     their positions), stored negated as a partial slot, or, when the
+//                     head's evicted rows are fewer than its kept ones, of its evicted
+//                     rows, stored as they are.
 //   7 k_reduce        fixed-order sum of the slots = raw moments of the provisional
 //                     evicted set: all slots (the candidates' minus the kept rows'), or
 //                     only the evicted rows' slots.  Summing the evicted rows directly
@@ -28,11 +28,10 @@
 //                     into LDS (fp32, or a bf16 hi/lo pair), S_tilde k_j on MFMA,
 //                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm,
 //                     added to the final selection's key histogram.       [reads K, V]
-//   9 k_tk_*          final kept set.
-//  10 k_gather_out    retained rows (sinks, kept, window) -> k_out/v_out, idx, lens.
-//  11 k_cov_rows      covariance of the final kept rows, negated (or of the final
-//                     evicted rows when fewer).
-//  12 k_reduce        final raw moments S, s_k, s_v, n_e.
+//   9 k_tk_*          final kept set and its covariance slots.
+//  10 k_finish        one launch: retained rows (sinks, kept, window) -> k_out/v_out,
+//                     idx, lens; and the final raw moments S, s_k, s_v, n_e (the slots of
+//                     the final selection's covariance, as in stage 7).
 // Every reduction has a fixed order, so results are bit-reproducible.
 #include "mkv_bf16.h"
 #include "mkv_device.h"
@@ -839,13 +838,21 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
   }
 }
 
+// COV: the same workgroup then adds the covariance and sums of its slice's kept rows
+// (negated) or, for a head whose evicted candidates are fewer, of its slice's evicted rows
+// into partial slot nsl1 + slice (the work of a separate pass over the selected rows).
+template <class T, int D>
+__device__ void slice_cov(const CompressArgs& a, int head, int sl, const int32_t* list,
+                          int nrows, float sign);
+
+template <class E, int D, bool COV>
 __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scores, int n, int k,
                                                     const int* __restrict__ kh,
                                                     const int* __restrict__ state,
                                                     const int* __restrict__ cnt,
                                                     const uint32_t* __restrict__ cand,
                                                     int32_t* __restrict__ out, int out_stride,
-                                                    int pos_offset, int32_t* __restrict__ ev_out) {
+                                                    int pos_offset, CompressArgs a) {
   __shared__ int s_gt[TK_MAX_SLICES], s_cn[TK_MAX_SLICES], s_gtT[TK_MAX_SLICES], s_eqT[TK_MAX_SLICES];
   __shared__ __align__(16) uint32_t hst[1024];
   __shared__ uint32_t sh_bin, sh_above;
@@ -854,9 +861,14 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
   __shared__ int s_start[TK_MAX_SLICES + 1];
   __shared__ uint32_t c_key[TK_CAND_LDS];
   __shared__ uint8_t c_sl[TK_CAND_LDS];
+  __shared__ int32_t s_rows[COV ? TKS : 1];  // the slice's rows for the covariance, in order
+  __shared__ int s_nrows;
   const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x, tid = threadIdx.x;
   if (kh) k = min(kh[head], n);  // head-adaptive count (uniform over the workgroup)
-  if (k <= 0) return;
+  if (k <= 0) {
+    if constexpr (COV) slice_cov<E, D>(a, head, sl, s_rows, 0, -1.f);  // a zero slot
+    return;
+  }
   // the slice's own keys are needed last but depend on nothing: requested first
   uint32_t key[TKPT];
   bool valid[TKPT];
@@ -944,11 +956,18 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
     else if (key == T) atomicAdd(&s_eqT[s2], 1);
   });
   __syncthreads();
+  const bool direct = n - k < k;  // the head's evicted candidates are the fewer
   if (tid == 0) {  // fixed order over the slices
     int eb = 0, ob = 0;
     for (int s2 = 0; s2 < ntk; ++s2) {
-      if (s2 == sl) { s_off = ob; s_eqb = eb; }
-      ob += s_gt[s2] + s_gtT[s2] + min(max(need - eb, 0), s_eqT[s2]);
+      const int kept_s2 = s_gt[s2] + s_gtT[s2] + min(max(need - eb, 0), s_eqT[s2]);
+      if (s2 == sl) {
+        s_off = ob;
+        s_eqb = eb;
+        const int valid_s2 = min(TKS, n - s2 * TKS);
+        s_nrows = direct ? valid_s2 - kept_s2 : kept_s2;
+      }
+      ob += kept_s2;
       eb += s_eqT[s2];
     }
   }
@@ -976,18 +995,24 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
   // is the (j - p)-th evicted one
   int p = s_off + (before & 0xFFFF) + min(max(need - s_eqb, 0), before >> 16);
   int32_t* o = out + (size_t)head * out_stride;
-  const bool want_ev = ev_out != nullptr && n - k < k;  // uniform over the workgroup
-  int32_t* eo = ev_out ? ev_out + (size_t)head * out_stride : nullptr;
   const int j0 = sl * TKS + TKPT * tid;
+  const int e_off = sl * TKS - s_off;  // evicted positions before the slice
 #pragma unroll
   for (int u = 0; u < TKPT; ++u) {
     if (keep[u]) {
-      if (p < k) o[p] = j0 + u + pos_offset;
+      if (p < k) {
+        o[p] = j0 + u + pos_offset;
+        if (COV && !direct) s_rows[min(max(p - s_off, 0), TKS - 1)] = j0 + u + pos_offset;
+      }
       ++p;
-    } else if (want_ev && valid[u]) {
+    } else if (COV && valid[u] && direct) {  // not kept: the (j - p)-th evicted position
       const int e = j0 + u - p;
-      if (e >= 0 && e < n - k) eo[e] = j0 + u + pos_offset;
+      if (e >= 0 && e < n - k) s_rows[min(max(e - e_off, 0), TKS - 1)] = j0 + u + pos_offset;
     }
+  }
+  if constexpr (COV) {
+    __syncthreads();
+    slice_cov<E, D>(a, head, sl, s_rows, min(s_nrows, TKS), direct ? 1.f : -1.f);
   }
 }
 
@@ -1017,8 +1042,11 @@ __device__ __forceinline__ void tile_load_list(TileRegs<T, D, NT>& R, const T* K
   }
 }
 
+// Covariance and sums of `nrows` rows of head `head` (positions list[0..nrows), LDS or
+// global), written with `sign` into partial slot nsl1 + sl; 256 threads.
 template <class T, int D>
-__global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const int32_t* kept_list) {
+__device__ void slice_cov(const CompressArgs& a, int head, int sl, const int32_t* list,
+                          int nrows, float sign) {
   constexpr int NT = 256, NW = 4;
   constexpr int PAD = 16 / (int)sizeof(T);
   constexpr int LDT = TILE + PAD;
@@ -1027,11 +1055,6 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const int32_t*
   __shared__ __align__(16) T sKT[D][LDT];
   __shared__ __align__(16) T sVT[D][LDT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int head = blockIdx.y, sl = blockIdx.x;
-  const int kh = head_keep(a, head);
-  const bool direct = direct_sums(a, head);
-  const int nrows = direct ? a.n_c - kh : kh;
-  const int32_t* list = (direct ? a.evl : kept_list) + (size_t)head * a.kmax;
   const T* Kh = reinterpret_cast<const T*>(a.k) + (size_t)head * a.N * D;
   const T* Vh = reinterpret_cast<const T*>(a.v) + (size_t)head * a.N * D;
   f32x4 cacc[QM][QN];
@@ -1044,19 +1067,18 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const int32_t*
   for (int e = 0; e < 8; ++e) sk[e] = sv[e] = 0.f;
   auto in_rows = [&](int j) { return j < nrows; };
   const int ntiles = (nrows + TILE - 1) / TILE;
-  const int t_beg = sl * a.tpsr, t_end = min(t_beg + a.tpsr, ntiles);
   TR R;
-  if (t_beg < t_end) tile_load_list<T, D, NT>(R, Kh, Vh, list, t_beg * TILE, nrows, a.N, tid);
-  for (int t = t_beg; t < t_end; ++t) {
+  if (ntiles > 0) tile_load_list<T, D, NT>(R, Kh, Vh, list, 0, nrows, a.N, tid);
+  for (int t = 0; t < ntiles; ++t) {
     float ss[TR::NP][2];
     R.arrive();
     tile_store_t<T, D, NT, LDT>(R, sKT, sVT, t * TILE, in_rows, sk, sv, ss, tid);
-    if (t + 1 < t_end) tile_load_list<T, D, NT>(R, Kh, Vh, list, (t + 1) * TILE, nrows, a.N, tid);
+    if (t + 1 < ntiles) tile_load_list<T, D, NT>(R, Kh, Vh, list, (t + 1) * TILE, nrows, a.N, tid);
     __syncthreads();
     cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
   }
-  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, direct ? 1.f : -1.f,
+  write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, sign,
                               reinterpret_cast<float*>(&sVT[0][0]), tid);
 }
 
@@ -1068,11 +1090,10 @@ __global__ void __launch_bounds__(256) k_cov_rows(CompressArgs a, const int32_t*
 // s0 + sub, s0 + sub + 8, ..., then a fixed xor tree across the eight lanes.
 // ------------------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, float* sv_out,
-                                                 float* sk_out, int32_t* ne_out) {
+__device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, int bx, float* S_out,
+                                             float* sv_out, float* sk_out, int32_t* ne_out) {
   constexpr int NSF4 = D * D / 4, NF4 = (D * D + 2 * D) / 4;
-  const int head = blockIdx.y;
-  const int f4 = blockIdx.x * 32 + (threadIdx.x >> 3);
+  const int f4 = bx * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   const int s0 = direct_sums(a, head) ? a.nsl1 : 0;
@@ -1104,7 +1125,15 @@ __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, fl
     }
     *reinterpret_cast<float4*>(dst) = acc;
   }
-  if (ne_out && blockIdx.x == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - head_keep(a, head);
+  if (ne_out && bx == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - head_keep(a, head);
+}
+
+template <int D> constexpr int reduce_blocks() { return ((D * D + 2 * D) / 4 + 31) / 32; }
+
+template <int D>
+__global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, float* sv_out,
+                                                 float* sk_out, int32_t* ne_out) {
+  reduce_slots<D>(a, blockIdx.y, blockIdx.x, S_out, sv_out, sk_out, ne_out);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1288,14 +1317,14 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) k_residual(Compre
 // With budget >= N every row is retained.
 // ------------------------------------------------------------------------------------
 template <class T, int D>
-__global__ void __launch_bounds__(256) k_gather_out(CompressArgs a, int n_out, int keep_all) {
+__device__ __forceinline__ void gather_out(const CompressArgs& a, int head, int bx, int n_out,
+                                           int keep_all) {
   constexpr int DG = D / 8;
-  const int head = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int c = bx * 256 + threadIdx.x;
   const int i = c / DG, dg = c % DG;
   const int kk = keep_all ? 0 : head_keep(a, head);
   if (!keep_all && a.kh) n_out = a.n_s + kk + a.w;  // head-adaptive: this head's length
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.lens_out[head] = n_out;
+  if (bx == 0 && threadIdx.x == 0) a.lens_out[head] = n_out;
   if (i >= n_out) return;
   int pos;
   if (keep_all || i < a.n_s) pos = i;
@@ -1307,6 +1336,21 @@ __global__ void __launch_bounds__(256) k_gather_out(CompressArgs a, int n_out, i
   store_frag(reinterpret_cast<T*>(a.k_out) + dst, load_frag(reinterpret_cast<const T*>(a.k) + src));
   store_frag(reinterpret_cast<T*>(a.v_out) + dst, load_frag(reinterpret_cast<const T*>(a.v) + src));
   if (dg == 0) a.idx_out[(size_t)head * a.idx_stride + i] = pos;
+}
+
+template <class T, int D>
+__global__ void __launch_bounds__(256) k_gather_out(CompressArgs a, int n_out, int keep_all) {
+  gather_out<T, D>(a, blockIdx.y, blockIdx.x, n_out, keep_all);
+}
+
+// The last launch: the first reduce_blocks<D>() workgroups of each head sum the final
+// selection's slots into the output moments, the others copy the retained rows.
+template <class T, int D>
+__global__ void __launch_bounds__(256) k_finish(CompressArgs a, int n_out) {
+  const int head = blockIdx.y;
+  constexpr int RB = reduce_blocks<D>();
+  if ((int)blockIdx.x < RB) reduce_slots<D>(a, head, blockIdx.x, a.S, a.s_v, a.s_k, a.n_e);
+  else gather_out<T, D>(a, head, blockIdx.x - RB, n_out, 0);
 }
 
 template <int D>
@@ -1331,6 +1375,8 @@ __global__ void __launch_bounds__(256) k_zero_moments(CompressArgs a) {
   } while (0)
 
 // `which` selects the histogram the score producer filled (0: first selection, 1: final).
+// The selection's covariance slots are written by the same launch (k_tk_write<.., true>).
+template <class T, int D>
 static hipError_t launch_topk(const CompressArgs& a, const float* scores, int which,
                               int32_t* out, hipStream_t st) {
   if (a.k_keep <= 0) return hipSuccess;
@@ -1339,9 +1385,9 @@ static hipError_t launch_topk(const CompressArgs& a, const float* scores, int wh
                      (const int*)a.kh, (const uint32_t*)(a.tk_hh + (size_t)which * a.H * TK_HBINS),
                      a.tk_state, a.tk_cnt, a.tk_cand);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep, (const int*)a.kh,
-                     (const int*)a.tk_state, (const int*)a.tk_cnt, (const uint32_t*)a.tk_cand, out,
-                     a.kmax, a.n_s, a.evl);
+  hipLaunchKernelGGL((k_tk_write<T, D, true>), grid, dim3(TKT), 0, st, scores, a.n_c, a.k_keep,
+                     (const int*)a.kh, (const int*)a.tk_state, (const int*)a.tk_cnt,
+                     (const uint32_t*)a.tk_cand, out, a.kmax, a.n_s, a);
   MKV_CHECK_LAUNCH();
   return hipSuccess;
 }
@@ -1373,9 +1419,9 @@ static hipError_t launch_head_budgets(const CompressArgs& a, hipStream_t st) {
                      (const int*)nullptr, (const uint32_t*)a.tk_hs, a.tk_state_g, a.tk_cnt_g,
                      a.tk_cand_g);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_tk_write, grid, dim3(TKT), 0, st, (const float*)a.abar, n, k,
+  hipLaunchKernelGGL((k_tk_write<float, 64, false>), grid, dim3(TKT), 0, st, (const float*)a.abar, n, k,
                      (const int*)nullptr, (const int*)a.tk_state_g, (const int*)a.tk_cnt_g,
-                     (const uint32_t*)a.tk_cand_g, a.kept_all, k, 0, (int32_t*)nullptr);
+                     (const uint32_t*)a.tk_cand_g, a.kept_all, k, 0, a);
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL(k_ada_counts, dim3(a.B), dim3(64), 0, st, a);
   MKV_CHECK_LAUNCH();
@@ -1406,30 +1452,20 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
   if (te != hipSuccess) return te;
   const float* first_scores = a.mi_rounds < 0 ? a.abar : a.score0;
   int32_t* first_out = a.mi_rounds >= 1 ? a.kept0 : a.kept;
-  te = launch_topk(a, first_scores, 0, first_out, st);
+  te = launch_topk<T, D>(a, first_scores, 0, first_out, st);
   if (te != hipSuccess) return te;
-  const dim3 red_grid(((D * D + 2 * D) / 4 + 31) / 32, H);
   if (a.mi_rounds >= 1) {
-    if (a.k_keep > 0) {
-      hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const int32_t*)a.kept0);
-      MKV_CHECK_LAUNCH();
-    }
-    hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.s0, a.sv0, a.sk0, (int32_t*)nullptr);
+    hipLaunchKernelGGL((k_reduce<D>), dim3(reduce_blocks<D>(), H), blk, 0, st, a, a.s0, a.sv0,
+                       a.sk0, (int32_t*)nullptr);
     MKV_CHECK_LAUNCH();
     hipLaunchKernelGGL((k_residual<T, D>), dim3(a.nsl3, H), blk, 0, st, a);
     MKV_CHECK_LAUNCH();
-    te = launch_topk(a, a.score, 1, a.kept, st);
+    te = launch_topk<T, D>(a, a.score, 1, a.kept, st);
     if (te != hipSuccess) return te;
   }
   const int n_out_max = a.kh ? a.n_s + a.w + a.kmax : a.L;  // the longest head's rows
-  hipLaunchKernelGGL((k_gather_out<T, D>), dim3((n_out_max * (D / 8) + 255) / 256, H), blk, 0, st, a,
-                     a.L, 0);
-  MKV_CHECK_LAUNCH();
-  if (a.k_keep > 0) {
-    hipLaunchKernelGGL((k_cov_rows<T, D>), dim3(a.nslr, H), blk, 0, st, a, (const int32_t*)a.kept);
-    MKV_CHECK_LAUNCH();
-  }
-  hipLaunchKernelGGL((k_reduce<D>), red_grid, blk, 0, st, a, a.S, a.s_v, a.s_k, a.n_e);
+  hipLaunchKernelGGL((k_finish<T, D>), dim3(reduce_blocks<D>() + (n_out_max * (D / 8) + 255) / 256, H),
+                     blk, 0, st, a, a.L);
   MKV_CHECK_LAUNCH();
   // diagnostics
   const size_t nc_bytes = (size_t)H * a.n_c * sizeof(float);

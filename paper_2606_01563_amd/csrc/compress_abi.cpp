@@ -86,17 +86,10 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.nsl2 = clampi(ceil_div(1024, a.H), 1, a.ntile);
   a.tps2 = std::min(ceil_div(a.ntile, a.nsl2), mkv::kMassMaxTiles);
   a.nsl2 = ceil_div(a.ntile, a.tps2);
-  // covariance over the kept rows (subtracted) or the evicted rows, whichever are fewer
-  if (a.k_keep > 0) {
-    const int ntr = ceil_div(a.kmax, 64);  // the most rows any head keeps
-    a.nslr = clampi(ceil_div(256, a.H), 1, ntr);
-    a.tpsr = ceil_div(ntr, a.nslr);
-    a.nslr = ceil_div(ntr, a.tpsr);
-  } else {
-    a.nslr = 0;
-    a.tpsr = 1;
-  }
-  a.nslot = a.nsl1 + a.nslr;
+  // top-k slices of 2048 candidates (at most 128 for kMaxCandidates); each slice's
+  // workgroup also writes one covariance slot of its kept (or evicted) rows
+  a.ntk = ceil_div(a.n_c > 0 ? a.n_c : 1, 2048);
+  a.nslot = a.nsl1 + (a.k_keep > 0 ? a.ntk : 0);
   // residual pass: 64-candidate tiles, about 512 workgroups
   {
     const int nu = ceil_div(a.n_c > 0 ? a.n_c : 1, 64);
@@ -104,8 +97,6 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
     a.tps3 = std::min(ceil_div(nu, a.nsl3), mkv::kResMaxTiles);
     a.nsl3 = ceil_div(nu, a.tps3);
   }
-  // top-k slices of 2048 candidates (at most 128 for kMaxCandidates)
-  a.ntk = ceil_div(a.n_c > 0 ? a.n_c : 1, 2048);
   a.ntk_g = a.adaptive ? ceil_div(a.Hkv * a.n_c, 2048) : 1;
   const size_t H = a.H, D = a.D;
   const size_t nc = a.n_c > 0 ? a.n_c : 1;
@@ -128,7 +119,6 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.s0 = c.take<float>(H * D * D * sizeof(float));
   a.sv0 = c.take<float>(H * D * sizeof(float));
   a.sk0 = c.take<float>(H * D * sizeof(float));
-  a.evl = c.take<int32_t>(H * a.kmax * sizeof(int32_t));
   if (a.adaptive) {
     const size_t Bs = a.B;
     a.kh = c.take<int32_t>(H * sizeof(int32_t));

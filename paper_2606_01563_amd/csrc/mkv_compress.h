@@ -44,9 +44,6 @@ struct CompressArgs {
   float* s0;                // [H, D, D]         raw S of the provisional evicted set
   float* sv0;               // [H, D]            its s_v
   float* sk0;               // [H, D]            its s_k
-  int32_t* evl;             // [H, kmax]         evicted positions (ascending) of a head whose
-                            //                   evicted set is smaller than its kept set: its
-                            //                   moments are summed over these rows directly
   int B, Hq, Hkv, G, N, L, w, n_s, chunk, mi_rounds, cap, D;
   int H;                    // B * Hkv
   int R;                    // G * w window rows per KV head
@@ -57,9 +54,10 @@ struct CompressArgs {
   int nsl1, tps1;           // window-row/covariance pass: slices, tiles per slice
                             // (tps1 <= kRowsMaxTiles)
   int nsl2, tps2;           // window-mass pass: slices, tiles per slice (<= kMassMaxTiles)
-  int nslr, tpsr;           // covariance pass over a head's kept rows (subtracted) or,
-                            // when fewer, its evicted rows (summed directly)
-  int nslot;                // nsl1 + nslr
+  int nslot;                // nsl1 + ntk: the candidate slices' slots, then one slot per
+                            // top-k slice for the covariance of its kept rows (subtracted)
+                            // or, when a head's evicted rows are the fewer, its evicted rows'
+
   int nsl3, tps3;           // residual pass: slices over candidate tiles of 64 (<= kResMaxTiles)
   int ntk;                  // top-k slices of 2048 candidates
   // head-adaptive budgets (adaptive = 1): a per-sequence selection over the layer
