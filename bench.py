@@ -15,14 +15,18 @@ GPU and stay resident in HBM.  One timed step is one pass of the whole hot path:
                     different caches and the 256 MB last-level cache cannot hold them).
 
 The decode phase of a step (all 128 x 5 launches) is captured once as a HIP graph and
-replayed, as a serving loop would run it: the host does not pace the GPU.  The graph's
-replay is checked bit for bit against the same phase run eagerly.
+replayed, as a serving loop would run it: the host does not pace the GPU; so is each
+budget's compress phase (the 36 calls and the summaries' decode form).  Every replay is
+checked bit for bit against the same phase run eagerly.
 
 Reported (one JSON line): decode attention+correction GB/s (algorithmic bytes / replay
 time, the `value`), decode tokens/s, compress ms/layer per budget, per-budget decode
 times (replay of the whole phase minus replay of the phase without that budget, so the
 other budgets still keep the last-level cache cold), a roofline object for the decode call
-and the fp64 oracle timed on the host as a CPU baseline.  Two further phases are measured
+and the fp64 oracle timed on the host as a CPU baseline; `compress_roofline` sets the
+compress call and its context-streaming kernels against HBM and the bf16 MFMA peak (kernel
+times, traffic and MFMA activity from the committed rocprofv3 summary of the workload), and
+`compress_stacked` times one compress call over the whole stack per budget.  Further phases are measured
 the same way on the same compressed stacks and reported beside the headline, which they do
 not change: the decode with the summary in half precision (`decode_half_summary`), the
 compress with head-adaptive budgets (`compress_adaptive`) and the decode step with
@@ -47,6 +51,7 @@ from paper_2606_01563_amd import synth  # noqa: E402
 from paper_2606_01563_amd import momentkv as mk  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of the MI355X
 
 
 def decode_bytes(n_heads: int, G: int, d: int, lens_after: int, elem: int = 2) -> int:
@@ -63,6 +68,105 @@ def compress_bytes(n_kv_heads: int, N: int, d: int, L: int, elem: int = 2) -> in
     """Algorithmic bytes of one layer's compress: K and V read once, retained rows written,
     the summary written."""
     return n_kv_heads * (2 * N * d * elem + 2 * L * d * elem + 4 * d * d + 8 * d + 4 + 4 * L)
+
+
+def compress_kernel_work(n_heads: int, G: int, w: int, N: int, d: int, n_sink: int = 1,
+                         elem: int = 2) -> dict:
+    """Algorithmic HBM bytes and flops per launch of the compress passes that stream the
+    context, for one call over `n_heads` KV heads (C = N - w - n_sink candidates):
+      k_rows_cov   K and V read once; window logits 2 G w N d (MFMA) and the candidate
+                   covariance V_C^T K_C, 2 |C| d^2 (MFMA);
+      k_mass       K read once; the window logits again, 2 G w N d (MFMA);
+      k_residual   K and V of the candidates read once; S_tilde0 k_j for every candidate on
+                   two bf16 planes, 2 x 2 |C| d^2 (MFMA)."""
+    C = N - w - n_sink
+    logits = 2 * G * w * N * d * n_heads
+    cov = 2 * C * d * d * n_heads
+    return {"k_rows_cov": {"bytes": 2 * N * d * elem * n_heads, "flops": logits + cov,
+                           "covariance_flops": cov},
+            "k_mass": {"bytes": N * d * elem * n_heads, "flops": logits},
+            "k_residual": {"bytes": 2 * C * d * elem * n_heads, "flops": 2 * cov}}
+
+
+def _profile_json(path: str, sha_key: str):
+    """The machine-readable block of a committed rocprofv3 summary, or None when the file is
+    missing or the sources it lists have changed since the counters were taken."""
+    import hashlib
+    import re
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(\{.*?\})\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    data = json.loads(m.group(1))
+    h = hashlib.sha256()
+    for src in data["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    return data if h.hexdigest() == data[sha_key] else None
+
+
+def compress_roofline(wl, budgets, ms_per_layer: dict) -> dict:
+    """Compress against its roofs.  The whole call: algorithmic bytes per layer (K and V read
+    once, retained rows and summary written) over the measured ms per layer (HBM roof).  The
+    passes that stream the context, from the committed rocprofv3 summary of this workload
+    (profiles/compress_<workload>.md, only while the compress sources are unchanged): kernel
+    time per launch, algorithmic bytes over it against HBM, MFMA flops over it against the
+    bf16 peak, MFMA-busy share of the kernel's time (SQ_VALU_MFMA_BUSY_CYCLES), measured HBM
+    traffic per call (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy) over the
+    algorithmic bytes; and the covariance's own MFMA utilisation: its flops over the
+    kernel's time, against the bf16 peak."""
+    H, N, d = wl.batch * wl.n_kv_heads, wl.ctx_len, wl.head_dim
+    per_budget = {}
+    for L in budgets:
+        by = compress_bytes(H, N, d, min(L, N))
+        ms = ms_per_layer[str(L)]
+        per_budget[str(L)] = {"bytes": by, "ms": ms, "GBps": by / (ms * 1e-3) / 1e9,
+                              "frac": by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    avg_by = sum(v["bytes"] for v in per_budget.values()) / len(per_budget)
+    avg_ms = sum(v["ms"] for v in per_budget.values()) / len(per_budget)
+    res = {"kernel": "momentkv_compress call (one layer)", "bound": "hbm",
+           "achieved": avg_by / (avg_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": avg_by / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "bytes_per_layer": avg_by,
+           "ms_per_layer": avg_ms, "per_budget": per_budget, "traffic": None, "kernels": None,
+           "covariance_mfma": None}
+    prof = _profile_json(os.path.join(ROOT, "profiles", f"compress_{wl.name}.md"),
+                         "compress_sources_sha256")
+    if prof is None:
+        return res
+    work = compress_kernel_work(H, wl.group, wl.window, N, d, wl.n_sink)
+    kernels = {}
+    for name, k in prof["kernels"].items():
+        short = name.split("<")[0].split("::")[-1]
+        ent = {"avg_us": k["avg_us"], "mfma_busy_pct": k.get("mfma_busy_pct")}
+        if short in work:
+            wk = work[short]
+            t = k["avg_us"] * 1e-6
+            ent.update({"bytes": wk["bytes"], "GBps": wk["bytes"] / t / 1e9,
+                        "frac_hbm": wk["bytes"] / t / 1e9 / HBM_PEAK_GBS,
+                        "mfma_TFLOPs": wk["flops"] / t / 1e12,
+                        "frac_mfma_bf16": wk["flops"] / t / 1e12 / MFMA_BF16_PEAK_TFLOPS})
+        kernels[name] = ent
+    res["kernels"] = kernels
+    ratio = prof.get("traffic_over_algorithmic")
+    res["traffic"] = None if ratio is None else ratio * avg_by
+    rc = [(n, k) for n, k in prof["kernels"].items() if "k_rows_cov" in n]
+    if rc:
+        name, k = rc[0]
+        t = k["avg_us"] * 1e-6
+        cov = work["k_rows_cov"]["covariance_flops"]
+        share = cov / work["k_rows_cov"]["flops"]
+        res["covariance_mfma"] = {
+            "what": "V_C^T K_C on v_mfma_f32_16x16x32_bf16 inside k_rows_cov (which also runs "
+                    "the window logits on the same instruction)",
+            "flops_per_layer": cov, "kernel": name, "kernel_us": k["avg_us"],
+            "achieved_TFLOPs": cov / t / 1e12,
+            "util_of_bf16_peak": cov / t / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+            "kernel_mfma_busy_pct": k.get("mfma_busy_pct"),
+            "covariance_share_of_kernel_mfma": share,
+            "covariance_mfma_busy_pct": None if k.get("mfma_busy_pct") is None
+            else k["mfma_busy_pct"] * share}
+    return res
 
 
 def measured_traffic(workload: str, alg_per_call: dict) -> float | None:
@@ -363,6 +467,44 @@ def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, ou
                          "avg_call_us": total / (T * len(budgets)) * 1e3}}
 
 
+def stacked_measurement(args, wl, data, layers, budgets, dev) -> dict:
+    """momentkv_compress once per budget over the whole stack (batch = layers x sequences,
+    every layer's KV heads in one call): the same per-head work as the per-layer calls, with
+    the fixed cost of each launch shared by the stack's heads.  ms per layer = HIP-event time
+    of the call over the layers; the inputs are the per-layer tensors concatenated (outside
+    the timing)."""
+    N, Hkv, d, w = wl.ctx_len, wl.n_kv_heads, wl.head_dim, wl.window
+    q = torch.cat([x["q_win"] for x in data]).contiguous()
+    k = torch.cat([x["k"] for x in data]).contiguous()
+    v = torch.cat([x["v"] for x in data]).contiguous()
+    res = {}
+    for L in budgets:
+        cap = min(L, N)
+        p = mk.compress_params(q, k, L, cap=cap)
+        ws = torch.empty(mk.momentkv_compress_workspace_bytes(p), dtype=torch.uint8, device=dev)
+        out = mk.momentkv_compress(q, k, v, L, cap=cap, workspace=ws)  # warm-up, allocates out
+        torch.cuda.synchronize()
+        ev = []
+        for _ in range(args.steps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            mk.momentkv_compress(q, k, v, L, cap=cap, out=out, workspace=ws)
+            e1.record()
+            ev.append((e0, e1))
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+        by = compress_bytes(Hkv * wl.batch, N, d, cap)
+        res[str(L)] = {"ms_per_layer": ms / layers, "GBps": by / (ms / layers * 1e-3) / 1e9,
+                       "ms_per_call": ms}
+        del out, ws
+    del q, k, v
+    return {"what": f"one momentkv_compress call per budget over all {layers} layers "
+                    f"(batch {layers * wl.batch}); the per-layer calls are the headline",
+            "per_budget": res,
+            "ms_per_layer": sum(x["ms_per_layer"] for x in res.values()) / len(res)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -381,6 +523,11 @@ def main() -> int:
                     help="skip the half-precision summary measurement")
     ap.add_argument("--no-adaptive", action="store_true",
                     help="skip the head-adaptive compress measurement")
+    ap.add_argument("--no-stacked", action="store_true",
+                    help="skip the one-call-per-stack compress measurement")
+    ap.add_argument("--compress-probe", action="store_true",
+                    help="for rocprofv3 runs: one plain copy of known size, then one compress "
+                         "of every layer per budget (eager); prints the plan as JSON and exits")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one plain copy of "
                          "known size, then 4 tokens x budgets of eager decode calls; prints "
@@ -468,6 +615,40 @@ def main() -> int:
             if timing is not None:
                 timing["compress"][L].append((e0, e1))
 
+    def compress_budget(L):
+        """One budget's compress of every layer and the summaries' decode form (no events)."""
+        for l in range(layers):
+            x = data[l]
+            mk.momentkv_compress(x["q_win"], x["k"], x["v"], L, cap=min(L, N) + T,
+                                 out=views[L][l], workspace=cws)
+        st = stacks[L]
+        mk.momentkv_prepare_summary(st.n_e, st.s_k, st.s_v, st.S, dtype=wl.dtype,
+                                    out=prepared[L])
+
+    def capture_fn(fn):
+        """fn captured as a HIP graph (run once eagerly first on the capture stream)."""
+        g = torch.cuda.CUDAGraph()
+        cs = torch.cuda.Stream()
+        cs.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cs):
+            fn()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=cs):
+                fn()
+        torch.cuda.current_stream().wait_stream(cs)
+        torch.cuda.synchronize()
+        return g
+
+    def compress_replay(cgraphs, timing):
+        """The compress phase as graph replays, one per budget, timed by HIP events."""
+        for L in budgets:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            cgraphs[L].replay()
+            e1.record()
+            timing["compress"][L].append((e0, e1))
+
     def decode_call(t, L):
         st = stacks[L]
         mk.momentkv_decode_attn(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e, st.s_k,
@@ -504,6 +685,20 @@ def main() -> int:
         d1.record()
         return d0, d1
 
+    if args.compress_probe:
+        copy_bytes = 256 << 20
+        src = torch.empty(copy_bytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)                 # calibration: copy_bytes read, copy_bytes written
+        torch.cuda.synchronize()
+        compress_phase(None)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": copy_bytes, "budgets": list(budgets), "layers": layers,
+                          "bytes_per_call": {str(L): compress_bytes(Hkv * B, N, d, min(L, N))
+                                             for L in budgets},
+                          "work": compress_kernel_work(Hkv * B, G, w, N, d, wl.n_sink)}))
+        return 0
+
     if args.traffic_probe:
         compress_phase(None)
         torch.cuda.synchronize()
@@ -532,6 +727,21 @@ def main() -> int:
     # the phase without each budget in turn: a budget's decode time is the difference
     graph = capture()
     graph_without = {L: capture(skip=L) for L in budgets}
+    # the compress phase as graphs too (per budget: the layers' calls and the summaries'
+    # decode form), checked bit for bit against the eager phase
+    cgraphs = {L: capture_fn(lambda L=L: compress_budget(L)) for L in budgets}
+    compress_phase(None)
+    torch.cuda.synchronize()
+    eager = [(stacks[L].idx.clone(), stacks[L].S.clone(), prepared[L].clone()) for L in budgets]
+    for L in budgets:
+        stacks[L].S.zero_()
+        cgraphs[L].replay()
+    torch.cuda.synchronize()
+    if not all(torch.equal(i, stacks[L].idx) and torch.equal(S, stacks[L].S) and
+               torch.equal(pr, prepared[L]) for (i, S, pr), L in zip(eager, budgets)):
+        print("[bench] compress graph replay differs from the eager compress", file=sys.stderr)
+        return 7
+    del eager
 
     timing = new_timing()
     dec_events = []
@@ -541,7 +751,7 @@ def main() -> int:
     wall0 = time.perf_counter()
     s0.record()
     for i in range(args.steps):
-        compress_phase(timing)
+        compress_replay(cgraphs, timing)
         dec_events.append(timed_replay(graph))
         print(f"[bench] step {i + 1}/{args.steps} enqueued", file=sys.stderr, flush=True)
     s1.record()
@@ -577,6 +787,11 @@ def main() -> int:
             ev.append(timed_replay(graph_without[L]))
         torch.cuda.synchronize()
         without_ms[L] = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    # per-call spread of the compress: eager calls with an event between consecutive calls
+    spread_timing = new_timing()
+    for _ in range(args.steps):
+        compress_phase(spread_timing)
+    torch.cuda.synchronize()
 
     per_budget = {}
     alg_per_call = {}
@@ -599,7 +814,7 @@ def main() -> int:
     value = phase_bytes * len(dec_ms) / dec_s / 1e9
     spread = {"decode_step_ms": percentiles(dec_ms),
               "compress_call_ms": {str(L): percentiles(
-                  [a.elapsed_time(b) for ev in timing["calls"][L] for a, b in zip(ev, ev[1:])])
+                  [a.elapsed_time(b) for ev in spread_timing["calls"][L] for a, b in zip(ev, ev[1:])])
                   for L in budgets}}
     half = None
     if wl.dtype == torch.bfloat16 and not args.no_half:
@@ -610,6 +825,8 @@ def main() -> int:
             return 6
     ada = None if args.no_adaptive else adaptive_measurement(args, wl, data, layers,
                                                               budgets[0], dev)
+    stacked = None if args.no_stacked else stacked_measurement(args, wl, data, layers, budgets,
+                                                               dev)
     evict = None if args.no_evict else evict_measurement(
         args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, out, compress_phase, capture,
         timed_replay)
@@ -648,9 +865,13 @@ def main() -> int:
                      "traffic": measured_traffic(wl.name, alg_per_call),
                      "bytes_per_launch": avg_bytes,
                      "avg_launch_us": avg_launch_s * 1e6},
+        "compress_roofline": compress_roofline(
+            wl, budgets, {k: v["compress_ms_per_layer"] for k, v in per_budget.items()}),
         "wall_s_timed": wall,
         "spread": spread,
     }
+    if stacked is not None:
+        res["compress_stacked"] = stacked
     if half is not None:
         res["decode_half_summary"] = half
     if ada is not None:

@@ -66,7 +66,7 @@ typedef enum {
 typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
 
 /* Limits of this build: head_dim in {64, 128}; G = Hq/Hkv <= 16; G * window <= 512;
- * at most 262144 eviction candidates (ctx_len - window - n_sink) per head (per layer with
+ * at most 1048576 eviction candidates (ctx_len - window - n_sink) per head (per layer with
  * head-adaptive budgets); a decode grid
  * of at most 2^24 waves (B * Hkv * (token slices + head_dim / 32)). */
 
@@ -100,7 +100,7 @@ typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
  *      Hkv * k_keep candidates with the largest abar over all the layer's heads (equal
  *      values in (head, position) order) are counted per head, k_h; head h then selects
  *      k_h candidates as in step 4 and keeps n_s + w + k_h tokens (lens).  Requires
- *      cap >= n_s + w + min(n_c, Hkv * k_keep) and Hkv * n_c <= 262144; idx_out then has
+ *      cap >= n_s + w + min(n_c, Hkv * k_keep) and Hkv * n_c <= 1048576; idx_out then has
  *      cap entries per head, of which the first lens are written.
  * ---------------------------------------------------------------------------------- */
 typedef struct {

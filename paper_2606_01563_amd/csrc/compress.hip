@@ -48,7 +48,7 @@ constexpr int TKS = 2048;          // positions per slice
 constexpr int TKT = 256;           // threads per slice workgroup
 constexpr int TKPT = TKS / TKT;    // consecutive positions per thread
 constexpr int TK_BINS0 = 2048;
-constexpr int TK_MAX_SLICES = 128; // 262144 candidates
+constexpr int TK_MAX_SLICES = 512; // 1048576 candidates
 constexpr int TK_CAND_LDS = 8192;  // candidates of the k-th key's bin staged in LDS
 
 __device__ __forceinline__ uint32_t score_key(float s) {
@@ -860,7 +860,7 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
   __shared__ int s_off, s_eqb;
   __shared__ int s_start[TK_MAX_SLICES + 1];
   __shared__ uint32_t c_key[TK_CAND_LDS];
-  __shared__ uint8_t c_sl[TK_CAND_LDS];
+  __shared__ uint16_t c_sl[TK_CAND_LDS];
   __shared__ int32_t s_rows[COV ? TKS : 1];  // the slice's rows for the covariance, in order
   __shared__ int s_nrows;
   const int head = blockIdx.y, sl = blockIdx.x, ntk = gridDim.x, tid = threadIdx.x;
@@ -911,7 +911,7 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int f = f0 + u * TKT + tid;
-        if (f < m) { c_key[f] = v[u]; c_sl[f] = (uint8_t)vs[u]; }
+        if (f < m) { c_key[f] = v[u]; c_sl[f] = (uint16_t)vs[u]; }
       }
     }
   }

@@ -15,7 +15,7 @@ using namespace mkv::abi;
 
 namespace {
 
-constexpr int kMaxCandidates = 1 << 18;  // top-k: at most 128 slices of 2048 candidates
+constexpr int kMaxCandidates = 1 << 20;  // top-k: at most 512 slices of 2048 candidates
 
 // ----------------------------------------------------------------------- compress
 mkv_status check_compress_params(const mkv_compress_params* p) {
@@ -86,7 +86,7 @@ mkv::CompressArgs compress_layout(const mkv_compress_params* p, void* ws, size_t
   a.nsl2 = clampi(ceil_div(1024, a.H), 1, a.ntile);
   a.tps2 = std::min(ceil_div(a.ntile, a.nsl2), mkv::kMassMaxTiles);
   a.nsl2 = ceil_div(a.ntile, a.tps2);
-  // top-k slices of 2048 candidates (at most 128 for kMaxCandidates); each slice's
+  // top-k slices of 2048 candidates (at most 512 for kMaxCandidates); each slice's
   // workgroup also writes one covariance slot of its kept (or evicted) rows
   a.ntk = ceil_div(a.n_c > 0 ? a.n_c : 1, 2048);
   a.nslot = a.nsl1 + (a.k_keep > 0 ? a.ntk : 0);

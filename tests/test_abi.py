@@ -113,7 +113,7 @@ def test_workspace_sizes(L):
     (dict(dtype=7), DTYPE),
     (dict(adaptive=2), SHAPE),
     (dict(adaptive=1), CAPACITY),          # a head may take up to 8 x 479 candidates
-    (dict(adaptive=1, ctx_len=40000, cap=8000), UNSUP),   # 8 x n_c candidates > 262144
+    (dict(adaptive=1, ctx_len=140000, cap=9000), UNSUP),  # 8 x n_c candidates > 1048576
 ])
 def test_compress_rejects_invalid_parameters(L, kw, code):
     assert compress_status(cparams(**kw)) == code
