@@ -404,18 +404,24 @@ def test_half_precision_summary_error_against_fp32_summary():
 
 
 # ---------------------------------------------------------------- full-size sampled heads
-@pytest.mark.parametrize("budget", [128, 2048])
+@pytest.mark.parametrize("budget", [128, 256, 512, 1024, 2048])
 def test_qwen_stack_layer_full_size_sampled_heads(budget):
-    """One 32K-context layer of the Qwen3-4B-shaped stack, both ends of the budget range,
-    checked on two sampled KV heads."""
-    wl, cpu, gpu = layer("qwen3_4b_stack_n32768", layer_idx=3, steps=2)
+    """One 32K-context layer of the Qwen3-4B-shaped stack at every budget of the stack
+    workload, checked on two sampled KV heads; then decode in the benchmark's launch shape
+    (capacity budget + 128, so the single launch up to budget 256 and the split launch from
+    512): 8 steps at 256 and 512 with the prepared summary, 2 steps otherwise."""
+    steps = 8 if budget in (256, 512) else 2
+    wl, cpu, gpu = layer("qwen3_4b_stack_n32768", layer_idx=3, steps=steps)
     announce(f"{wl.name} L={budget}")
-    out = P.run_compress(gpu, budget, cap=budget + 2)
+    out = P.run_compress(gpu, budget, cap=budget + 128)
     for h in (0, 5):
         errs = P.check_compress_head(cpu, out, 0, h, budget)
         announce(f"head {h} {errs}")
-    P.run_decode_steps(gpu, out, 1)
-    P.run_decode_steps(gpu, out, 1, summary=1)
+    if steps == 8:
+        P.run_decode_steps(gpu, out, 8, summary=1)
+    else:
+        P.run_decode_steps(gpu, out, 1)
+        P.run_decode_steps(gpu, out, 1, summary=1)
 
 
 def test_llama_stack_batch8_needles_full_size_sampled_heads():
@@ -431,12 +437,32 @@ def test_llama_stack_batch8_needles_full_size_sampled_heads():
     P.run_decode_steps(gpu, out, 2, summary=1)
 
 
-def test_ruler_128k_full_size_sampled_head():
-    wl, cpu, gpu = layer("ruler_n131072", layer_idx=0, steps=1)
+def test_ruler_128k_full_size_sampled_heads():
+    """The 128K-context stress layer (window 64, planted needles) at budget 1024: two
+    sampled KV heads through the full compress protocol, then two decode steps over all
+    heads."""
+    wl, cpu, gpu = layer("ruler_n131072", layer_idx=0, steps=2)
     announce(f"{wl.name}")
-    out = P.run_compress(gpu, 1024, cap=1025)
-    errs = P.check_compress_head(cpu, out, 0, 2, 1024)
-    announce(f"head 2 {errs}")
+    out = P.run_compress(gpu, 1024, cap=1026)
+    for h in (2, 6):
+        errs = P.check_compress_head(cpu, out, 0, h, 1024)
+        announce(f"head {h} {errs}")
+    P.run_decode_steps(gpu, out, 2)
+
+
+def test_adaptive_budgets_ruler_128k_sampled_head():
+    """Head-adaptive budgets on the 128K layer: the layer-wide selection runs over
+    8 x 131007 candidates (512 slices); the per-head counts are checked against the GPU's
+    masses and the oracle's, one sampled head follows the full compress protocol with its
+    own count, and the decode runs over the per-head lengths."""
+    wl, cpu, gpu = layer("ruler_n131072", layer_idx=1, steps=1)
+    L = 1024
+    cap = mk.compress_rows(wl.ctx_len, 8, L, wl.window, adaptive=True)
+    out = P.run_compress(gpu, L, cap=cap, adaptive=True)
+    kh, swaps = P.check_head_budgets(cpu, out, 0, L)
+    announce(f"128K per-head counts {list(kh)}, swaps {swaps}")
+    h = int(np.argmax(kh))
+    P.check_compress_head(cpu, out, 0, h, int(1 + wl.window + kh[h]))
     P.run_decode_steps(gpu, out, 1)
 
 
