@@ -1,0 +1,84 @@
+"""Where the synthetic workloads sit against the paper's analysis regime (CPU; test
+infrastructure: uses the fp64 oracle).  Writes profiles/regime_synthetic.md.
+
+    python tests/regime_report.py
+
+For KV head 0 of each workload's first layer (sequence 0): the oracle compresses the head
+at each budget (moment-informed selection, one moment round), then for the first two decode
+steps' queries of the head's group it evaluates the quantities of Sec. 3 (Eqs.
+sub-outputs, decomposition, eviction_error, relative_error) exactly over the whole prefix:
+the evicted attention mass w_E, cos(theta) between the evicted and retained sub-outputs,
+the relative error of the retained-only output f_R and of the corrected output against
+full attention, and cos(f_E, f_E_hat) of the first-order moment estimate.  The paper's
+measured regime (Sec. 3, Fig. analysis) on LLaMA-3-8B at L = 128: w_E below 0.08 on average
+(below 0.05 in most layers), cos(theta) near 0, and a retained-only relative error above
+20% on average.  The inputs are seeded synthetic tensors (no model, no dataset); this report
+says how far their attention statistics are from that regime.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import oracle as O  # noqa: E402
+from paper_2606_01563_amd import synth  # noqa: E402
+
+CASES = [("tiny_fp32_n2048", (128,)), ("llama31_8b_layer_n8192", (128, 512)),
+         ("qwen3_4b_stack_n32768", (128, 2048)), ("llama31_8b_stack_b8_n32768", (256,)),
+         ("ruler_n131072", (1024,))]
+
+
+def head_report(wl, L, data, h=0, steps=2) -> dict:
+    f64 = lambda t: t.float().double().numpy()  # noqa: E731
+    G = wl.group
+    q = f64(data["q_win"][0, h * G:(h + 1) * G])
+    K = f64(data["k"][0, h])
+    V = f64(data["v"][0, h])
+    comp = O.compress_head(q, K, V, L, n_sink=wl.n_sink, chunk=wl.chunk)
+    rows = []
+    for t in range(steps):
+        for g in range(G):
+            qd = f64(data["q_dec"][t, 0, h * G + g])
+            rows.append(O.eviction_diagnostics(qd, K, V, comp.idx))
+    keys = ("w_E", "cos_theta", "rel_err_retained", "rel_err_corrected", "cos_fE_fEhat")
+    return {k: float(np.mean([r[k] for r in rows])) for k in keys} | {"queries": len(rows)}
+
+
+def main():
+    out = []
+    for name, budgets in CASES:
+        wl = synth.WORKLOADS[name]
+        t0 = time.time()
+        data = synth.make_layer(wl, 0, device="cpu", decode_steps=2)
+        for L in budgets:
+            r = head_report(wl, L, data)
+            out.append({"workload": name, "budget": L, **r})
+            print(json.dumps(out[-1]), f"({time.time() - t0:.0f}s)", flush=True)
+    lines = ["# Synthetic workloads against the paper's analysis regime", "",
+             "Command: `python tests/regime_report.py` (CPU; fp64 oracle).  KV head 0 of layer 0, "
+             "sequence 0; each row averages the G query heads of the group over the first two "
+             "decode steps.  Quantities of Sec. 3 computed exactly over the whole prefix for the "
+             "set the oracle retains (moment-informed selection).", "",
+             "Paper (Sec. 3, Fig. analysis; LLaMA-3-8B, L = 128): w_E below 0.08 on average, "
+             "cos(theta) near 0, retained-only relative error above 0.20 on average.", "",
+             "| workload | budget | w_E | cos theta | rel. error of f_R | rel. error corrected | cos(f_E, f_E_hat) |",
+             "|---|---|---|---|---|---|---|"]
+    for r in out:
+        lines.append(f"| {r['workload']} | {r['budget']} | {r['w_E']:.3f} | {r['cos_theta']:.3f} | "
+                     f"{r['rel_err_retained']:.3f} | {r['rel_err_corrected']:.3f} | "
+                     f"{r['cos_fE_fEhat']:.3f} |")
+    lines += ["", "```json", json.dumps(out), "```", ""]
+    with open(os.path.join(ROOT, "profiles", "regime_synthetic.md"), "w") as f:
+        f.write("\n".join(lines))
+
+
+if __name__ == "__main__":
+    main()
