@@ -452,6 +452,14 @@ def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, ou
                               "GBps": by / (budget_ms * 1e-3) / 1e9,
                               "tokens_per_s": wl.batch * T / (budget_ms * 1e-3)}
     achieved = all_bytes / (total * 1e-3) / 1e9
+    # measured HBM traffic per call: the committed FETCH_SIZE / WRITE_SIZE summary's ratio
+    # per budget applied to this run's algorithmic bytes (None once the sources differ)
+    prof = _profile_json(os.path.join(ROOT, "profiles", f"traffic_evict_{wl.name}.md"),
+                         "evict_sources_sha256")
+    traffic = None
+    if prof is not None and all(str(L) in prof["traffic_over_algorithmic"] for L in budgets):
+        traffic = sum(prof["traffic_over_algorithmic"][str(L)] * evict_bytes(LB * Hkv, G, d, min(L, N))
+                      for L in budgets) / len(budgets)
     return {"what": "per token and budget one momentkv_decode_evict call over the 36 "
                     "caches: append, Phase 1 eviction, Phase 2 corrected attention; cache "
                     "kept at the budget.  Budgets up to 768: one k_evict_attn launch that "
@@ -462,7 +470,7 @@ def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, ou
             "per_budget": per_budget,
             "roofline": {"kernel": "momentkv_decode_evict call (1-2 launches)", "bound": "hbm",
                          "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                         "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                          "bytes_per_call": all_bytes / (T * len(budgets)),
                          "avg_call_us": total / (T * len(budgets)) * 1e3}}
 
@@ -528,6 +536,10 @@ def main() -> int:
     ap.add_argument("--compress-probe", action="store_true",
                     help="for rocprofv3 runs: one plain copy of known size, then one compress "
                          "of every layer per budget (eager); prints the plan as JSON and exits")
+    ap.add_argument("--evict-probe", action="store_true",
+                    help="for rocprofv3 runs: one plain copy of known size, then 4 tokens x "
+                         "budgets of eager decode calls with eviction; prints the plan as JSON "
+                         "and exits")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one plain copy of "
                          "known size, then 4 tokens x budgets of eager decode calls; prints "
@@ -697,6 +709,32 @@ def main() -> int:
                           "bytes_per_call": {str(L): compress_bytes(Hkv * B, N, d, min(L, N))
                                              for L in budgets},
                           "work": compress_kernel_work(Hkv * B, G, w, N, d, wl.n_sink)}))
+        return 0
+
+    if args.evict_probe:
+        compress_phase(None)
+        torch.cuda.synchronize()
+        copy_bytes = 256 << 20
+        src = torch.empty(copy_bytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)                 # calibration: copy_bytes read, copy_bytes written
+        ews = {}
+        for L in budgets:
+            p = mk.decode_params(q_steps[0], stacks[L].k_out, max_len=min(L, N) + 1)
+            ews[L] = torch.zeros(mk.momentkv_decode_evict_workspace_bytes(p), dtype=torch.uint8,
+                                 device=dev)
+        calls = []
+        for t in range(4):
+            for L in budgets:
+                st = stacks[L]
+                Lr = min(L, N)
+                mk.momentkv_decode_evict(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e,
+                                         st.s_k, st.s_v, st.S, kn_steps[t], vn_steps[t], Lr,
+                                         max_len=Lr + 1, out=out, workspace=ews[L])
+                calls.append({"token": t, "budget": L, "fused": Lr + 1 >= 769,
+                              "bytes": evict_bytes(LB * Hkv, G, d, Lr)})
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": copy_bytes, "calls": calls}))
         return 0
 
     if args.traffic_probe:
