@@ -30,38 +30,51 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
 
-def _compile(src: str) -> tuple[str, int, str]:
-    obj = os.path.join(OBJ, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *COMMON, "-c", src, "-o", obj]
+# Host-side AddressSanitizer and UndefinedBehaviorSanitizer for the sanitized copy of the
+# library (each -fsanitize= applies to the host pass only; device code is built as usual).
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all",
+            "-shared-libasan"]
+OBJ_SAN = os.path.join(CSRC, "_build_san")
+LIB_SAN = os.path.join(OBJ_SAN, "libmomentkv_san.so")
+
+
+def _compile(src: str, sanitize: bool = False) -> tuple[str, int, str]:
+    obj = os.path.join(OBJ_SAN if sanitize else OBJ, os.path.basename(src) + ".o")
+    cmd = [HIPCC, *COMMON, *(SANITIZE if sanitize else []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                     if "packed-fp32-ops" not in l)
     return obj, r.returncode, out
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compile and link the library; sanitize=True builds the host-sanitized copy
+    (csrc/_build_san/libmomentkv_san.so, for the CPU-only checks of the C ABI's validation
+    code) and leaves the product library alone."""
     if not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
-    os.makedirs(OBJ, exist_ok=True)
+    os.makedirs(OBJ_SAN if sanitize else OBJ, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
     jobs = min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
     with ThreadPoolExecutor(jobs) as ex:
-        results = list(ex.map(_compile, srcs))
+        results = list(ex.map(lambda x: _compile(x, sanitize), srcs))
     failed = [(o, out) for o, rc, out in results if rc != 0]
     for o, rc, out in results:
         if out.strip() and (verbose or rc != 0):
             print(out, file=sys.stderr)
     if failed:
         raise RuntimeError("hipcc failed for: " + ", ".join(os.path.basename(o) for o, _ in failed))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *[o for o, _, _ in results],
-           "-o", tmp]
+    lib = LIB_SAN if sanitize else LIB
+    tmp = lib + ".tmp"
+    cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *(SANITIZE if sanitize else []),
+           *[o for o, _, _ in results], "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         print(r.stdout + r.stderr, file=sys.stderr)
         raise RuntimeError("link failed")
-    shutil.move(tmp, LIB)
-    return LIB
+    shutil.move(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

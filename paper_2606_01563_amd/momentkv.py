@@ -16,7 +16,9 @@ from dataclasses import dataclass
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmomentkv.so")
+# MKV_LIB selects another build of the same library (the host-sanitized copy used by the
+# CPU-only checks of the C ABI); the default is the in-tree product library.
+LIB_PATH = os.environ.get("MKV_LIB") or os.path.join(_HERE, "libmomentkv.so")
 HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "momentkv.h")
 
 MKV_F32, MKV_BF16 = 0, 1
