@@ -14,11 +14,12 @@
 //         a decode call is latency bound.
 //
 // split   k_decode_slice + k_decode_merge: a 1-D grid of n_heads x (nsq + nsplit)
-//         single-wave workgroups, then one wave per (b, query head).
+//         single-wave workgroups, then one 4-wave workgroup per KV head.
 //         * n_heads x nsq waves of 32 rows of S_tilde q, written to the workspace;
 //         * n_heads x nsplit token slices (split_len rows below lens) of one KV head,
 //           each written as an unnormalised (o, max, sum) partial;
-//         * merge: the slices in a fixed order, then the new token, then the correction.
+//         * merge: per query, the slices in a fixed order, then the new token, then the
+//           correction.
 //         Used for long caches: reading is bound by how much each CU keeps in flight, so
 //         the finishing time is set by the busiest CU, and thousands of short slices let
 //         the dispatcher balance a few hundred heads over 256 CUs.  Merging in the same
@@ -654,72 +655,90 @@ __global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
 }
 
 // Merge of one query head's slices, the new token and the moment correction (one wave;
-// lane holds columns CPL * lane ...).  Every load is issued before the first reduction:
-// slice indices are clamped to the slice count and slices past the retained length are
-// loaded with the rest but never combined (their workspace rows hold stale data).
+// lane holds columns CPL * lane ...).  load() issues every read of the query's inputs and
+// of its first SUB slices' partials: slice indices are clamped to the slice count and
+// slices past the retained length are loaded with the rest but never combined (their
+// workspace rows hold stale data); finish() combines them in slice order.
 template <class T, int D>
-__device__ __forceinline__ void decode_merge_query(const DecodeArgs& a, int bh, int g, int lane) {
-  constexpr int CPL = D / 64;       // columns per lane
-  constexpr int SUB = 16;           // slices whose o rows are in flight together
-  const int G = a.G;
-  const int col = lane * CPL;
-  const size_t sbase = (size_t)bh * a.nsplit;
-  const int last = a.nsplit - 1;
-  auto o_row = [&](int s) { return a.part_o + ((sbase + min(s, last)) * G + g) * D + col; };
-
-  float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((sbase + min(lane, last)) * G + g) * 2);
+struct MergeQuery {
+  static constexpr int CPL = D / 64;  // columns per lane
+  static constexpr int SUB = 16;      // slices whose o rows are in flight together
+  float2 ml;
   float ov[SUB][CPL];
-#pragma unroll
-  for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(u), ov[u]);
-  const int old_len = a.lens[bh];
-  const int ne = a.n_e[bh];
   float sqv[CPL];
-  load_cols<CPL>(a.sq + ((size_t)bh * G + g) * D + col, sqv);  // meaningful when nsq > 0
-  const QueryCols<CPL> qc = load_query_cols<T, D>(a, bh, g, lane);
+  QueryCols<CPL> qc;
 
-  const HeadLen hl = head_len(a, old_len);
-  const int n_live = live_slices(a, hl.cache_len);
-  float M = -INFINITY, l = 0.f, o[CPL];
+  __device__ __forceinline__ const float* o_row(const DecodeArgs& a, int bh, int g, int s, int lane) const {
+    return a.part_o + (((size_t)bh * a.nsplit + min(s, a.nsplit - 1)) * a.G + g) * D + lane * CPL;
+  }
+  __device__ __forceinline__ float2 ml_of(const DecodeArgs& a, int bh, int g, int s) const {
+    return *reinterpret_cast<const float2*>(
+        a.part_ml + (((size_t)bh * a.nsplit + min(s, a.nsplit - 1)) * a.G + g) * 2);
+  }
+
+  __device__ __forceinline__ void load(const DecodeArgs& a, int bh, int g, int lane) {
+    ml = ml_of(a, bh, g, lane);
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) o[c] = 0.f;
-  for (int c0 = 0; c0 < n_live; c0 += kWave) {
-    if (c0 > 0) ml = *reinterpret_cast<const float2*>(a.part_ml + ((sbase + min(c0 + lane, last)) * G + g) * 2);
-    const bool live = c0 + lane < n_live;
-    const float mn = fmaxf(M, wave_max(live ? ml.x : -INFINITY));
-    if (mn == -INFINITY) continue;  // nothing attended to so far
-    const float r = fast_exp2(M - mn);
-    const float w = live ? fast_exp2(ml.x - mn) : 0.f;
-    l = l * r + wave_sum(live ? ml.y * w : 0.f);
+    for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(a, bh, g, u, lane), ov[u]);
+    load_cols<CPL>(a.sq + ((size_t)bh * a.G + g) * D + lane * CPL, sqv);  // used when nsq > 0
+    qc = load_query_cols<T, D>(a, bh, g, lane);
+  }
+
+  __device__ __forceinline__ void finish(const DecodeArgs& a, int bh, int g, int lane,
+                                         const HeadLen& hl, int ne) {
+    const int n_live = live_slices(a, hl.cache_len);
+    float M = -INFINITY, l = 0.f, o[CPL];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) o[c] *= r;
-    M = mn;
-    const int cn = min(kWave, n_live - c0);
-    for (int s0 = 0; s0 < cn; s0 += SUB) {
-      if (c0 + s0 > 0) {
+    for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+    for (int c0 = 0; c0 < n_live; c0 += kWave) {
+      if (c0 > 0) ml = ml_of(a, bh, g, c0 + lane);
+      const bool live = c0 + lane < n_live;
+      const float mn = fmaxf(M, wave_max(live ? ml.x : -INFINITY));
+      if (mn == -INFINITY) continue;  // nothing attended to so far
+      const float r = fast_exp2(M - mn);
+      const float w = live ? fast_exp2(ml.x - mn) : 0.f;
+      l = l * r + wave_sum(live ? ml.y * w : 0.f);
 #pragma unroll
-        for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(c0 + s0 + u), ov[u]);
-      }
+      for (int c = 0; c < CPL; ++c) o[c] *= r;
+      M = mn;
+      const int cn = min(kWave, n_live - c0);
+      for (int s0 = 0; s0 < cn; s0 += SUB) {
+        if (c0 + s0 > 0) {
 #pragma unroll
-      for (int u = 0; u < SUB; ++u) {
-        if (s0 + u < cn) {
-          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
+          for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(a, bh, g, c0 + s0 + u, lane), ov[u]);
+        }
 #pragma unroll
-          for (int c = 0; c < CPL; ++c) o[c] += wu * ov[u][c];
+        for (int u = 0; u < SUB; ++u) {
+          if (s0 + u < cn) {
+            const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) o[c] += wu * ov[u][c];
+          }
         }
       }
     }
+    finish_query<T, D>(a, bh, g, lane, M, l, o, qc, sqv, a.nsq > 0, ne, hl.can_append);
   }
-  finish_query<T, D>(a, bh, g, lane, M, l, o, qc, sqv, a.nsq > 0, ne, hl.can_append);
-  // the g == 0 wave of a KV head bumps lens (every slice read it in the previous launch)
-  if (lane == 0 && g == 0 && hl.can_append) a.lens[bh] = old_len + 1;
-}
+};
 
+// One 4-wave workgroup per KV head; wave w merges queries w, w + 4, ...  lens is read by
+// every wave before the barrier and bumped after it, so no query of the head can see the
+// bumped length.
 template <class T, int D>
 __global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
-  const int pair = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (pair >= a.n_pairs) return;
-  decode_merge_query<T, D>(a, pair / a.G, pair % a.G, lane);
+  const int wave = threadIdx.x >> 6;
+  const int head = blockIdx.x;
+  MergeQuery<T, D> mq;
+  if (wave < a.G) mq.load(a, head, wave, lane);
+  const HeadLen hl = head_len(a, a.lens[head]);
+  const int ne = a.n_e[head];
+  for (int g = wave; g < a.G; g += 4) {
+    if (g != wave) mq.load(a, head, g, lane);
+    mq.finish(a, head, g, lane, hl, ne);
+  }
+  __syncthreads();  // every wave has read lens
+  if (threadIdx.x == 0 && hl.can_append) a.lens[head] = hl.old_len + 1;
 }
 
 template <class T, int D, int GMAX, int PREP>
@@ -732,7 +751,7 @@ static hipError_t launch_decode_p(const DecodeArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((k_decode_slice<T, D, GMAX, PREP>), dim3(grid), dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_decode_merge<T, D>), dim3((a.n_pairs + 3) / 4), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((k_decode_merge<T, D>), dim3(a.n_heads), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -67,6 +67,20 @@ def test_decode_slice_counts(n_split):
     P.run_decode_steps(gpu, out, 3, n_split=n_split)
 
 
+@pytest.mark.parametrize("n_split", [1, 3])
+@pytest.mark.parametrize("G", [8, 16])
+def test_decode_large_query_groups(G, n_split):
+    """G = 8 and 16 query heads per KV head, more queries than the four waves of a
+    workgroup: the single launch and three slices, with appends over several steps (each
+    query of a head must see the length from before the step's append)."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=torch.bfloat16, head_dim=128,
+                         ctx_len=1000, batch=2, n_q_heads=2 * G, n_kv_heads=2, window=16,
+                         budgets=(97,))
+    out = P.run_compress(gpu, 97, cap=100)
+    announce(f"G={G} n_split={n_split}")
+    P.run_decode_steps(gpu, out, 3, n_split=n_split, summary=1)
+
+
 @pytest.mark.parametrize("append", [True, False])
 @pytest.mark.parametrize("n_split", [0, 3, 4])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
@@ -141,6 +155,27 @@ def test_selection_modes_and_chunks(mi_rounds, chunk):
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, ctx_len=700, budgets=(80,))
     out = P.run_compress(gpu, 80, chunk=chunk, mi_rounds=mi_rounds)
     P.check_compress_head(cpu, out, 0, 0, 80, chunk=chunk, mi_rounds=mi_rounds)
+
+
+@pytest.mark.parametrize("mi_rounds,budget", [(2, 97), (3, 97), (8, 97), (2, 950)])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_several_moment_rounds(dtype, mi_rounds, budget):
+    """mi_rounds > 1: each round scores with the moments of the round before's evicted set
+    (k_reduce, k_residual and the selection repeated); the final scores, kept set and
+    moments against the oracle's rounds.  Budget 950 of 1000 evicts fewer candidates than
+    it keeps, so every round sums the evicted rows directly."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=1, dtype=dtype, head_dim=128, ctx_len=1000,
+                         batch=1, n_q_heads=4, n_kv_heads=2, window=16, budgets=(budget,))
+    announce(f"mi_rounds={mi_rounds} budget={budget} {dtype}")
+    out = P.run_compress(gpu, budget, cap=budget, mi_rounds=mi_rounds)
+    for h in range(2):
+        errs = P.check_compress_head(cpu, out, 0, h, budget, mi_rounds=mi_rounds)
+        announce(f"head {h} {errs}")
+    if mi_rounds == 2 and budget == 97:
+        # on this input the first moment round changes the kept set of both heads, so the
+        # second round scores with other moments than the first did
+        one = P.run_compress(gpu, budget, cap=budget, mi_rounds=1)
+        assert not torch.equal(one.score, out.score)
 
 
 def test_budget_equal_to_protected_tokens_evicts_every_candidate():
