@@ -91,7 +91,8 @@ typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
  *        S_tilde k_j (Eq. residual), score_j = abar_j * ||r_j||; keep the k_keep best.
  *        "Best" = larger score; equal scores keep the lower position.
  *      mi_rounds = -1 keeps the k_keep largest abar (attention only); 0 stops after the
- *      provisional round.  This build supports mi_rounds in {-1, 0, 1}.
+ *      provisional round; mi_rounds = r >= 1 runs r moment rounds, each with the
+ *      moments of the round before.  This build supports mi_rounds in [-1, 8].
  *   5. Outputs: the retained positions idx (ascending: sinks, kept candidates, window)
  *      and their K/V rows copied to k_out/v_out; lens = min(budget, N); the raw sums of
  *      the final evicted set E (n_e = |E|, s_k, s_v, S = sum_E v_i k_i^T, fp32).
@@ -113,7 +114,7 @@ typedef struct {
   int32_t window;       /* w, 1 <= w < N                                             */
   int32_t n_sink;       /* n_s >= 0 attention-sink tokens kept at the start          */
   int32_t chunk;        /* c >= 1 pooling chunk                                      */
-  int32_t mi_rounds;    /* -1, 0 or 1 (see step 4)                                   */
+  int32_t mi_rounds;    /* -1 .. 8 (see step 4)                                      */
   int32_t cap;          /* rows per head of k_out/v_out, >= min(budget, N)           */
   int32_t dtype;        /* mkv_dtype of q_win, k, v, k_out, v_out                    */
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
@@ -126,7 +127,7 @@ typedef struct {
 typedef struct {
   float* abar;          /* [B, Hkv, n_c] pooled window mass                           */
   float* score0;        /* [B, Hkv, n_c] provisional score abar * ||v||               */
-  float* score;         /* [B, Hkv, n_c] moment-round score (mi_rounds = 1)           */
+  float* score;         /* [B, Hkv, n_c] last moment round's score (mi_rounds >= 1)   */
   int32_t* kept0;       /* [B, Hkv, k_keep] provisional kept positions, ascending    */
                         /* (adaptive: [B, Hkv, min(n_c, Hkv*k_keep)], first k_h set) */
 } mkv_compress_debug;

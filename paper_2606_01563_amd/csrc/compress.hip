@@ -28,7 +28,10 @@
 //                     into LDS (fp32, or a bf16 hi/lo pair), S_tilde k_j on MFMA,
 //                     ||v_j - v_bar - c S_tilde k_j||, score_j = abar_j * that norm,
 //                     added to the final selection's key histogram.       [reads K, V]
-//   9 k_tk_*          final kept set and its covariance slots.
+//   9 k_tk_*          kept set of the moment round and its covariance slots.
+//                     mi_rounds > 1 repeats stages 7-9, each round scoring with the
+//                     moments of the round before (k_reduce also clears the histogram
+//                     the next k_residual fills).
 //  10 k_finish        one launch: retained rows (sinks, kept, window) -> k_out/v_out,
 //                     idx, lens; and the final raw moments S, s_k, s_v, n_e (the slots of
 //                     the final selection's covariance, as in stage 7).
@@ -1130,10 +1133,15 @@ __device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, in
 
 template <int D> constexpr int reduce_blocks() { return ((D * D + 2 * D) / 4 + 31) / 32; }
 
+// Also clears the head's histogram of the moment round that follows (the round before
+// filled it, and its selection has read it).
 template <int D>
 __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, float* sv_out,
                                                  float* sk_out, int32_t* ne_out) {
   reduce_slots<D>(a, blockIdx.y, blockIdx.x, S_out, sv_out, sk_out, ne_out);
+  if (blockIdx.x == 0)
+    for (int b = threadIdx.x; b < TK_HBINS; b += 256)
+      a.tk_hh[((size_t)a.H + blockIdx.y) * TK_HBINS + b] = 0u;
 }
 
 // ------------------------------------------------------------------------------------
@@ -1454,7 +1462,9 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
   int32_t* first_out = a.mi_rounds >= 1 ? a.kept0 : a.kept;
   te = launch_topk<T, D>(a, first_scores, 0, first_out, st);
   if (te != hipSuccess) return te;
-  if (a.mi_rounds >= 1) {
+  // moment rounds: the previous selection's slots give its evicted set's moments, which
+  // score the candidates again; every round's selection rewrites the slots
+  for (int r = 1; r <= a.mi_rounds; ++r) {
     hipLaunchKernelGGL((k_reduce<D>), dim3(reduce_blocks<D>(), H), blk, 0, st, a, a.s0, a.sv0,
                        a.sk0, (int32_t*)nullptr);
     MKV_CHECK_LAUNCH();

@@ -16,6 +16,7 @@ using namespace mkv::abi;
 namespace {
 
 constexpr int kMaxCandidates = 1 << 20;  // top-k: at most 512 slices of 2048 candidates
+constexpr int kMaxRounds = 8;          // moment rounds after the provisional one
 
 // ----------------------------------------------------------------------- compress
 mkv_status check_compress_params(const mkv_compress_params* p) {
@@ -33,7 +34,7 @@ mkv_status check_compress_params(const mkv_compress_params* p) {
   if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
   if ((p->n_q_heads / p->n_kv_heads) * p->window > 512) return MKV_ERR_UNSUPPORTED;
   if (64 % p->chunk) return MKV_ERR_UNSUPPORTED;
-  if (p->mi_rounds < -1 || p->mi_rounds > 1) return MKV_ERR_UNSUPPORTED;
+  if (p->mi_rounds < -1 || p->mi_rounds > kMaxRounds) return MKV_ERR_UNSUPPORTED;
   if (p->ctx_len - p->window - p->n_sink > kMaxCandidates) return MKV_ERR_UNSUPPORTED;
   if (p->budget < p->ctx_len && p->budget < p->n_sink + p->window) return MKV_ERR_BUDGET;
   if (p->adaptive != 0 && p->adaptive != 1) return MKV_ERR_SHAPE;

@@ -136,7 +136,10 @@ def compress_score_bounds(qg, K, V, ref, kept0, *, n_sink: int, chunk: int, mi_r
     if mi_rounds < 1:
         return out
     Kc, Vc = K[cand], V[cand]
-    R0 = np.asarray(kept0, dtype=np.int64)
+    # the summary of the last round is the round before's evicted set: the GPU's provisional
+    # one for mi_rounds = 1, else the oracle's (the GPU's unless an intermediate cut fell on
+    # a near-tie, which the final comparison would then report)
+    R0 = np.asarray(kept0 if mi_rounds < 2 else ref.rounds[-2], dtype=np.int64)
     n0 = len(cand) - len(R0)
     m0 = O.evicted_moments(K, V, np.setdiff1d(cand, R0))
     if n0 == 0:

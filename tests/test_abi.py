@@ -105,7 +105,7 @@ def test_workspace_sizes(L):
     (dict(scale=float("nan")), SHAPE),
     (dict(head_dim=96), UNSUP),
     (dict(chunk=3), UNSUP),                 # chunk must divide 64
-    (dict(mi_rounds=2), UNSUP),
+    (dict(mi_rounds=9), UNSUP),             # at most 8 moment rounds
     (dict(n_q_heads=8 * 17), UNSUP),        # G > 16
     (dict(window=200), UNSUP),              # G * w > 512
     (dict(budget=20), BUDGET),              # < n_sink + window
