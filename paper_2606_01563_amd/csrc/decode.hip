@@ -282,20 +282,24 @@ struct BlockAttn {
   float m_run[4], l_run[4];
   f32x4 oacc[NT];
 
+  // Rows at or past t_end are loaded from row t_end - 1 (row 0 when t_end = 0), so no
+  // load sits under a per-lane condition: their logits are masked in run() and their
+  // weights are zero, so the copies contribute nothing.
   __device__ __forceinline__ void load(int j0, int lane) {
+    const int last = max(t_end, 1) - 1;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const int j = j0 + 16 * hh + (lane & 15);
+      const int j = min(j0 + 16 * hh + (lane & 15), last);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        kf[hh][ks] = (j < t_end) ? load_frag(kc + (size_t)j * D + 32 * ks + 8 * (lane >> 4)) : zero_frag<T>();
+        kf[hh][ks] = load_frag(kc + (size_t)j * D + 32 * ks + 8 * (lane >> 4));
     }
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const int j = j0 + 2 * (lane & 15) + hh;
+      const int j = min(j0 + 2 * (lane & 15) + hh, last);
 #pragma unroll
       for (int c = 0; c < NVC; ++c)
-        vf[hh][c] = (j < t_end) ? load_frag(vc + (size_t)j * D + 8 * ((lane >> 4) + 4 * c)) : zero_frag<T>();
+        vf[hh][c] = load_frag(vc + (size_t)j * D + 8 * ((lane >> 4) + 4 * c));
     }
   }
 
@@ -355,6 +359,7 @@ struct BlockAttn {
       if (j0 + stride < t_end) load(j0 + stride, lane);
       // ---- online softmax over the 32 tokens (rows g = gbase + i)
       float alpha[4];
+      bool grew = false;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int ja = j0 + (lane & 15), jb = ja + 16;
@@ -371,6 +376,7 @@ struct BlockAttn {
           pa = fast_exp2(xa - mn);
           pb = fast_exp2(xb - mn);
         }
+        grew |= mn != m_run[i];
         l_run[i] = l_run[i] * alpha[i] + row16_sum(pa + pb);
         m_run[i] = mn;
         if (gbase + i < GMAX) {
@@ -379,12 +385,16 @@ struct BlockAttn {
         }
       }
       wave_lds_order();  // P and V^T are in LDS before they are read back
-      // ---- O = alpha * O + P . V on MFMA (A = P rows g, B = V^T)
+      // ---- O = alpha * O + P . V on MFMA (A = P rows g, B = V^T); alpha is exactly 1
+      // where no running max grew, so the rescale is skipped when none did in the wave
+      const bool rescale = __any(grew);
       const FragT pfr = ((lane & 15) < G) ? load_frag(&sp[lane & 15][8 * (lane >> 4)]) : zero_frag<T>();
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
+        if (rescale) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
+          for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
+        }
         mma(oacc[nt], pfr, load_frag(&vt[16 * nt + (lane & 15)][8 * (lane >> 4)]));
       }
     }
