@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define MOMENTKV_ABI_VERSION 5
+#define MOMENTKV_ABI_VERSION 6
 
 typedef enum {
   MKV_OK = 0,
@@ -183,10 +183,12 @@ typedef struct {
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
   float tau;            /* covariance clamp threshold, >= 0                          */
   int32_t n_split;      /* work split over each KV head's cache: 1 = one workgroup   */
-                        /* per KV head, single launch; k > 1 = k token slices of one */
-                        /* wave each (rows rounded up to a multiple of 32) followed  */
-                        /* by a merge launch; 0 = automatic (single launch up to     */
-                        /* max_len 384, else about 768 slices in the whole grid).    */
+                        /* per KV head; k > 1 = k token slices of one wave each      */
+                        /* (rows rounded up to a multiple of 32), merged in the same */
+                        /* launch by the last wave of the head to finish; 0 =        */
+                        /* automatic (one workgroup per KV head up to max_len 384,   */
+                        /* else about 768 slices in the whole grid).  One launch     */
+                        /* either way.                                               */
   int32_t summary;      /* form of the S argument: 0 = the raw sum S (fp32); 1 = the */
                         /* prepared form written by momentkv_prepare_summary; 2 =    */
                         /* its half-precision form (bf16 caches only)               */
@@ -196,6 +198,14 @@ typedef struct {
  * parameters; pure host computation); momentkv_decode_workspace_size is the same function. */
 size_t momentkv_decode_workspace_bytes(const mkv_decode_params* p);
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p);
+
+/* Leading bytes of that workspace that must be zero before a call (0 on invalid
+ * parameters): the sticky flag, then one arrival counter per KV head that the split shape
+ * uses to find the last slice of a head to finish.  Every call leaves the counters at zero,
+ * so a workspace zeroed once serves any number of calls; a workspace reused for a call
+ * with a larger value here needs the bytes beyond the previous value zeroed first (they
+ * may hold partial results of earlier calls). */
+size_t momentkv_decode_workspace_zero_bytes(const mkv_decode_params* p);
 
 /* Decode form of a summary (Eq. fhat's covariance term; clamp of App. C.2).
  *
@@ -229,10 +239,10 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R
- * workspace >= momentkv_decode_workspace_bytes(p) bytes, 256-aligned.  Its first int32
- *           is a sticky overflow flag (set to 1 when an append found a full cache; zero it
- *           before first use to read it).  Calls that share a workspace must be
- *           stream-ordered. */
+ * workspace >= momentkv_decode_workspace_bytes(p) bytes, 256-aligned, whose first
+ *           momentkv_decode_workspace_zero_bytes(p) bytes are zero (see there).  Its first
+ *           int32 is a sticky overflow flag (set to 1 when an append found a full cache).
+ *           Calls that share a workspace must be stream-ordered. */
 mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void* k_cache,
                                 void* v_cache, int32_t* lens, const void* k_new,
                                 const void* v_new, const int32_t* n_e, const float* s_k,
@@ -255,9 +265,10 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
  * No hipMalloc, hipFree or allocating library routine is called.  The array's device
  * address is looked up once per device, on the first call with that device current;
  * `stream` must belong to the current device (MKV_ERR_UNSUPPORTED otherwise).  Every call
- * on one GPU uses that GPU's array, which keeps the last call's contents (nothing in it
- * needs to start at zero): calls that overlap in time on one GPU (on different streams,
- * or from host threads without ordering between them) race on it and must not be issued;
+ * on one GPU uses that GPU's array, which keeps the last call's contents: its arrival
+ * counters (a fixed region at its start, zero when the library is loaded) are back at zero
+ * when a call completes.  Calls that overlap in time on one GPU (on different streams, or
+ * from host threads without ordering between them) race on it and must not be issued;
  * calls on one stream are ordered.
  * ---------------------------------------------------------------------------------- */
 #define MOMENTKV_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)

@@ -13,19 +13,18 @@
 //         products run while the cache rows are in flight.  Used for short caches, where
 //         a decode call is latency bound.
 //
-// split   k_decode_slice + k_decode_merge: a 1-D grid of n_heads x (nsq + nsplit)
-//         single-wave workgroups, then one 4-wave workgroup per KV head.
-//         * n_heads x nsq waves of 32 rows of S_tilde q, written to the workspace;
+// split   k_decode_slice: one launch, a 1-D grid of n_heads x (nsq + nsplit) single-wave
+//         workgroups:
+//         * n_heads x nsq waves of 32 rows of S_tilde q;
 //         * n_heads x nsplit token slices (split_len rows below lens) of one KV head,
-//           each written as an unnormalised (o, max, sum) partial;
-//         * merge: per query, the slices in a fixed order, then the new token, then the
-//           correction.
+//           each an unnormalised (o, max, sum) partial;
+//         each wave hands its result over through agent-scope stores and counts itself in
+//         on the head's counter, and the wave that completes the count merges the head:
+//         per query, the slices in a fixed order, then the new token, then the
+//         correction (so the result does not depend on which wave merges).
 //         Used for long caches: reading is bound by how much each CU keeps in flight, so
 //         the finishing time is set by the busiest CU, and thousands of short slices let
-//         the dispatcher balance a few hundred heads over 256 CUs.  Merging in the same
-//         launch (the last slice to finish merges) would need a device-scope
-//         release/acquire per workgroup, which on this multi-XCD part is a write-back and
-//         an invalidate of the whole L2 each time: dearer than the second launch.
+//         the dispatcher balance a few hundred heads over 256 CUs.
 //
 // Common to both: Q.K^T and P.V run on MFMA over 32-token blocks (the G queries padded to
 // 16 rows) with the online softmax in the base-2 domain.  The new token (k_new, v_new) is
@@ -62,6 +61,38 @@ __device__ __forceinline__ int live_slices(const DecodeArgs& a, int cache_len) {
 __device__ __forceinline__ void wave_lds_order() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
+}
+
+// ---------------------------------------------------------------- in-launch hand-off
+// Partial results that one workgroup hands to another within the split launch go through
+// agent-scope relaxed atomic stores and loads, which are not served from the per-XCD
+// caches (those are not kept coherent with each other).  A writer waits until its own
+// stores have completed before it counts itself in on the head's arrival counter, and the
+// last arrival reads the partials only after the count, so no device-scope fence is
+// needed (on this part such a fence writes back and invalidates a whole L2).
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent2(float* p, float x, float y) {
+  const uint64_t u = (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_agent2(const float* p) {
+  const uint64_t u = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)u), __uint_as_float((uint32_t)(u >> 32)));
+}
+// s_waitcnt with vmcnt = 0 and the other counters at their maximum: every vector memory
+// operation of the wave issued so far (stores included) has completed.
+constexpr int kWaitVmem = 0x0F70;
+__device__ __forceinline__ void stores_complete() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(kWaitVmem);
+}
+__device__ __forceinline__ void loads_after_count() {
+  __builtin_amdgcn_s_waitcnt(kWaitVmem);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
 // Query fragments of one KV head's group (A operand of Q.K^T, B operand of S_tilde q):
@@ -152,6 +183,8 @@ struct SqRows {
     }
   }
 
+  // AGENT: dst is read by another workgroup of the launch (agent-scope stores)
+  template <bool AGENT = false>
   __device__ __forceinline__ void compute(const DecodeArgs& a, const typename Frag<T>::type (&qf)[KS],
                                           int r0, int lane, float* dst) {
     const int g = lane & 15;
@@ -203,8 +236,17 @@ struct SqRows {
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (g < a.G) dst[(size_t)g * D + r0 + 16 * u + 4 * (lane >> 4) + i] = acc[u][i];
+      for (int i = 0; i < 4; i += 2) {
+        float* p = dst + (size_t)g * D + r0 + 16 * u + 4 * (lane >> 4) + i;
+        if (g < a.G) {
+          if constexpr (AGENT) {
+            st_agent2(p, acc[u][i], acc[u][i + 1]);
+          } else {
+            p[0] = acc[u][i];
+            p[1] = acc[u][i + 1];
+          }
+        }
+      }
   }
 };
 
@@ -606,6 +648,185 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------- split launch
+// CPL consecutive elements of a row as floats (16 or 32 bytes, one or two loads), and the
+// converse store.
+template <int CPL>
+__device__ __forceinline__ void load_span(const float* p, float (&v)[CPL]) {
+#pragma unroll
+  for (int c = 0; c < CPL; c += 4) {
+    const float4 t = *reinterpret_cast<const float4*>(p + c);
+    v[c] = t.x; v[c + 1] = t.y; v[c + 2] = t.z; v[c + 3] = t.w;
+  }
+}
+template <int CPL>
+__device__ __forceinline__ void load_span(const bf16_t* p, float (&v)[CPL]) {
+  static_assert(CPL == 4 || CPL == 8, "4 or 8 columns");
+  uint32_t w[CPL / 2];
+  if constexpr (CPL == 8) {
+    const uint4 t = *reinterpret_cast<const uint4*>(p);
+    w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
+  } else {
+    const uint2 t = *reinterpret_cast<const uint2*>(p);
+    w[0] = t.x; w[1] = t.y;
+  }
+#pragma unroll
+  for (int c = 0; c < CPL / 2; ++c) {
+    v[2 * c] = __uint_as_float(w[c] << 16);
+    v[2 * c + 1] = __uint_as_float(w[c] & 0xffff0000u);
+  }
+}
+template <int CPL>
+__device__ __forceinline__ void store_span(float* p, const float (&v)[CPL]) {
+#pragma unroll
+  for (int c = 0; c < CPL; c += 4)
+    *reinterpret_cast<float4*>(p + c) = make_float4(v[c], v[c + 1], v[c + 2], v[c + 3]);
+}
+template <int CPL>
+__device__ __forceinline__ void store_span(bf16_t* p, const float (&v)[CPL]) {
+  uint32_t w[CPL / 2];
+#pragma unroll
+  for (int c = 0; c < CPL / 2; ++c) w[c] = (uint32_t)f2bf(v[2 * c]) | ((uint32_t)f2bf(v[2 * c + 1]) << 16);
+  if constexpr (CPL == 8) *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+  else *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+}
+
+// Merge of one KV head by the last wave of the split launch to count itself in: four
+// query heads at a time, query g0 + lane / 16 in each 16-lane row, the lane holding columns
+// CPL * (lane % 16) ... + CPL.  The slices' (max, sum) pairs are combined in slice order,
+// sixteen at a time (lane % 16 = slice), their o rows SUBR at a time; then the new token is
+// folded in and the moment correction applied, as in the single-launch path.  The slices'
+// partials and the S_tilde q rows are read with agent-scope loads.
+template <class T, int D>
+__device__ __forceinline__ void merge_head(const DecodeArgs& a, int head, int lane) {
+  constexpr int CPL = D / 16;  // columns per lane
+  constexpr int SUBR = 4;      // slices whose o rows are in flight together
+  const int r = lane & 15, c0 = CPL * r, G = a.G;
+  const HeadLen hl = head_len(a, a.lens[head]);
+  const int ne = a.order < 0 ? 0 : a.n_e[head];  // order -1: the output is f_R
+  const int n_live = live_slices(a, hl.cache_len);
+  const int last = max(n_live, 1) - 1;
+  const bool use_sq = a.nsq > 0;
+  for (int g0 = 0; g0 < G; g0 += 4) {
+    const bool gok = g0 + (lane >> 4) < G;
+    const int g = min(g0 + (lane >> 4), G - 1);  // rows past G repeat the last query, unstored
+    const size_t pair = (size_t)head * G + g;
+    auto ml_of = [&](int s) {
+      return ld_agent2(a.part_ml + (((size_t)head * a.nsplit + min(s, last)) * G + g) * 2);
+    };
+    auto o_row = [&](int s, float (&v)[CPL]) {
+      const float* p = a.part_o + (((size_t)head * a.nsplit + min(s, last)) * G + g) * D + c0;
+#pragma unroll
+      for (int c = 0; c < CPL; c += 2) {
+        const float2 t = ld_agent2(p + c);
+        v[c] = t.x;
+        v[c + 1] = t.y;
+      }
+    };
+    // every read of the query's inputs before the first reduction
+    float2 ml = ml_of(r);
+    float ov[SUBR][CPL];
+#pragma unroll
+    for (int u = 0; u < SUBR; ++u) o_row(u, ov[u]);
+    float sqv[CPL], q[CPL], kn[CPL], vn[CPL], sk[CPL], sv[CPL];
+    if (use_sq) {
+      const float* p = a.sq + pair * D + c0;
+#pragma unroll
+      for (int c = 0; c < CPL; c += 2) {
+        const float2 t = ld_agent2(p + c);
+        sqv[c] = t.x;
+        sqv[c + 1] = t.y;
+      }
+    }
+    const T* qp = reinterpret_cast<const T*>(a.q) + pair * D + c0;
+    const bool has_new = a.k_new != nullptr;
+    load_span<CPL>(qp, q);
+    load_span<CPL>(has_new ? reinterpret_cast<const T*>(a.k_new) + (size_t)head * D + c0 : qp, kn);
+    load_span<CPL>(has_new ? reinterpret_cast<const T*>(a.v_new) + (size_t)head * D + c0 : qp, vn);
+    load_span<CPL>(a.s_k + (size_t)head * D + c0, sk);
+    load_span<CPL>(a.s_v + (size_t)head * D + c0, sv);
+
+    float M = -INFINITY, l = 0.f, o[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+    for (int s0 = 0; s0 < n_live; s0 += 16) {
+      if (s0 > 0) ml = ml_of(s0 + r);
+      const bool live = s0 + r < n_live;
+      const float mn = fmaxf(M, row16_max(live ? ml.x : -INFINITY));
+      if (mn == -INFINITY) continue;  // nothing attended to so far (uniform over the row)
+      const float rs = fast_exp2(M - mn);
+      const float w = live ? fast_exp2(ml.x - mn) : 0.f;
+      l = l * rs + row16_sum(live ? ml.y * w : 0.f);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) o[c] *= rs;
+      M = mn;
+      const int cn = min(16, n_live - s0);
+      for (int u0 = 0; u0 < cn; u0 += SUBR) {
+        if (s0 + u0 > 0) {
+#pragma unroll
+          for (int u = 0; u < SUBR; ++u) o_row(s0 + u0 + u, ov[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < SUBR; ++u) {
+          const float wu = __shfl(w, (lane & 48) + min(u0 + u, 15));
+          if (u0 + u < cn) {
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) o[c] += wu * ov[u][c];
+          }
+        }
+      }
+    }
+    // the new token after the cache rows, then the correction (finish_query's arithmetic
+    // with the dot products summed over the row's 16 lanes)
+    float dot_k = 0.f, dot_s = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      dot_k += q[c] * kn[c];
+      dot_s += q[c] * sk[c];
+    }
+    dot_k = row16_sum(dot_k);
+    dot_s = row16_sum(dot_s);
+    if (hl.can_append) {
+      const float x = dot_k * a.scale * kLog2e;
+      const float mn = fmaxf(M, x);
+      const float rr = fast_exp2(M - mn), w = fast_exp2(x - mn);
+      l = l * rr + w;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) o[c] = o[c] * rr + w * vn[c];
+      M = mn;
+    }
+    const Mix mx = mix_weights(M, l, ne, dot_s, a.scale);
+    const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+    float res[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const float f_r = (l > 0.f) ? o[c] / l : 0.f;
+      res[c] = f_r;
+      if (ne > 0) {
+        float fe = sv[c] * inv_n;
+        if (use_sq) fe += a.scale * inv_n * sqv[c];
+        res[c] = mx.w_r * f_r + (1.f - mx.w_r) * fe;
+      }
+    }
+    if (gok) {
+      store_span<CPL>(reinterpret_cast<T*>(a.out) + pair * D + c0, res);
+      if (r == 0) {
+        if (a.lse_out) a.lse_out[pair] = mx.log_zr;
+        if (a.w_r_out) a.w_r_out[pair] = mx.w_r;
+      }
+    }
+  }
+  if (lane == 0) {
+    // every other wave of the head has counted itself in, and so has read lens
+    __hip_atomic_store(a.cnt + head, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (hl.can_append) a.lens[head] = hl.old_len + 1;
+  }
+}
+
+// One launch, a 1-D grid of single-wave workgroups: n_heads x nsq waves of 32 rows of
+// S_tilde q, then n_heads x nsplit token slices.  Each wave writes its result (S_tilde q
+// rows, or the slice's unnormalised (o, max, sum)), then counts itself in on its head's
+// counter; the wave that completes the count merges the head (merge_head) and sets the
+// counter back to zero for the next call.
 template <class T, int D, int GMAX, int PREP>
 __global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
@@ -633,122 +854,43 @@ __global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
     const int r0 = 32 * (idx % nsq);
     SqRows<T, D, PREP> sq;
     sq.load(a, head, r0, lane);
-    sq.compute(a, qf, r0, lane, a.sq + (size_t)head * G * D);
-    return;
-  }
-  const int split = idx % a.nsplit;
-  const HeadLen hl = head_len(a, a.lens[head]);
-  const int t0 = split * a.split_len;
-  BA ba;
-  ba.kc = reinterpret_cast<const T*>(a.k_cache) + (size_t)head * a.cap * D;
-  ba.vc = reinterpret_cast<const T*>(a.v_cache) + (size_t)head * a.cap * D;
-  ba.t_end = max(t0, min(t0 + a.split_len, hl.cache_len));
-  ba.init();
-  ba.load(t0, lane);  // nothing for an empty slice
-  if (a.k_new != nullptr && !hl.can_append && split == 0 && lane == 0) atomicOr(a.flag, 1);
-  // the slice whose range holds row old_len (the last slice for rows past the split)
-  if (hl.can_append && min(hl.old_len / a.split_len, a.nsplit - 1) == split)
-    append_row<T, D>(a, head, hl.old_len, lane);
-  if (t0 >= ba.t_end) return;  // empty slice: the merge skips it
-  typename BA::VtTile& vt = *reinterpret_cast<typename BA::VtTile*>(s_vt);
-  ba.run(qf, t0, BA::TB, a.scale * kLog2e, G, lane, vt, s_p);
-
-  // partials through LDS so that they leave in 16-byte stores
-  wave_lds_order();
-  float* so = reinterpret_cast<float*>(s_vt);
-  ba.store_lds(so, s_ml, G, lane);
-  wave_lds_order();
-  const size_t pbase = ((size_t)head * a.nsplit + split) * G;
-  float4* po = reinterpret_cast<float4*>(a.part_o + pbase * D);
-  for (int c = lane; c < G * D / 4; c += kWave) po[c] = reinterpret_cast<const float4*>(so)[c];
-  if (lane < 2 * G) a.part_ml[pbase * 2 + lane] = s_ml[lane];
-}
-
-// Merge of one query head's slices, the new token and the moment correction (one wave;
-// lane holds columns CPL * lane ...).  load() issues every read of the query's inputs and
-// of its first SUB slices' partials: slice indices are clamped to the slice count and
-// slices past the retained length are loaded with the rest but never combined (their
-// workspace rows hold stale data); finish() combines them in slice order.
-template <class T, int D>
-struct MergeQuery {
-  static constexpr int CPL = D / 64;  // columns per lane
-  static constexpr int SUB = 16;      // slices whose o rows are in flight together
-  float2 ml;
-  float ov[SUB][CPL];
-  float sqv[CPL];
-  QueryCols<CPL> qc;
-
-  __device__ __forceinline__ const float* o_row(const DecodeArgs& a, int bh, int g, int s, int lane) const {
-    return a.part_o + (((size_t)bh * a.nsplit + min(s, a.nsplit - 1)) * a.G + g) * D + lane * CPL;
-  }
-  __device__ __forceinline__ float2 ml_of(const DecodeArgs& a, int bh, int g, int s) const {
-    return *reinterpret_cast<const float2*>(
-        a.part_ml + (((size_t)bh * a.nsplit + min(s, a.nsplit - 1)) * a.G + g) * 2);
-  }
-
-  __device__ __forceinline__ void load(const DecodeArgs& a, int bh, int g, int lane) {
-    ml = ml_of(a, bh, g, lane);
-#pragma unroll
-    for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(a, bh, g, u, lane), ov[u]);
-    load_cols<CPL>(a.sq + ((size_t)bh * a.G + g) * D + lane * CPL, sqv);  // used when nsq > 0
-    qc = load_query_cols<T, D>(a, bh, g, lane);
-  }
-
-  __device__ __forceinline__ void finish(const DecodeArgs& a, int bh, int g, int lane,
-                                         const HeadLen& hl, int ne) {
-    const int n_live = live_slices(a, hl.cache_len);
-    float M = -INFINITY, l = 0.f, o[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) o[c] = 0.f;
-    for (int c0 = 0; c0 < n_live; c0 += kWave) {
-      if (c0 > 0) ml = ml_of(a, bh, g, c0 + lane);
-      const bool live = c0 + lane < n_live;
-      const float mn = fmaxf(M, wave_max(live ? ml.x : -INFINITY));
-      if (mn == -INFINITY) continue;  // nothing attended to so far
-      const float r = fast_exp2(M - mn);
-      const float w = live ? fast_exp2(ml.x - mn) : 0.f;
-      l = l * r + wave_sum(live ? ml.y * w : 0.f);
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) o[c] *= r;
-      M = mn;
-      const int cn = min(kWave, n_live - c0);
-      for (int s0 = 0; s0 < cn; s0 += SUB) {
-        if (c0 + s0 > 0) {
-#pragma unroll
-          for (int u = 0; u < SUB; ++u) load_cols<CPL>(o_row(a, bh, g, c0 + s0 + u, lane), ov[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < SUB; ++u) {
-          if (s0 + u < cn) {
-            const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u));
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) o[c] += wu * ov[u][c];
-          }
-        }
-      }
+    sq.template compute<true>(a, qf, r0, lane, a.sq + (size_t)head * G * D);
+  } else {
+    const int split = idx % a.nsplit;
+    const HeadLen hl = head_len(a, a.lens[head]);
+    const int t0 = split * a.split_len;
+    BA ba;
+    ba.kc = reinterpret_cast<const T*>(a.k_cache) + (size_t)head * a.cap * D;
+    ba.vc = reinterpret_cast<const T*>(a.v_cache) + (size_t)head * a.cap * D;
+    ba.t_end = max(t0, min(t0 + a.split_len, hl.cache_len));
+    ba.init();
+    ba.load(t0, lane);  // rows clamped into the cache for an empty slice; never used
+    if (a.k_new != nullptr && !hl.can_append && split == 0 && lane == 0) atomicOr(a.flag, 1);
+    // the slice whose range holds row old_len (the last slice for rows past the split)
+    if (hl.can_append && min(hl.old_len / a.split_len, a.nsplit - 1) == split)
+      append_row<T, D>(a, head, hl.old_len, lane);
+    if (t0 < ba.t_end) {  // an empty slice writes nothing: the merge skips it
+      typename BA::VtTile& vt = *reinterpret_cast<typename BA::VtTile*>(s_vt);
+      ba.run(qf, t0, BA::TB, a.scale * kLog2e, G, lane, vt, s_p);
+      // partials through LDS so that each lane stores whole 8-byte pairs
+      wave_lds_order();
+      float* so = reinterpret_cast<float*>(s_vt);
+      ba.store_lds(so, s_ml, G, lane);
+      wave_lds_order();
+      const size_t pbase = ((size_t)head * a.nsplit + split) * G;
+      float* po = a.part_o + pbase * D;
+      for (int c = lane; c < G * D / 2; c += kWave) st_agent2(po + 2 * c, so[2 * c], so[2 * c + 1]);
+      if (lane < G) st_agent2(a.part_ml + (pbase + lane) * 2, s_ml[2 * lane], s_ml[2 * lane + 1]);
     }
-    finish_query<T, D>(a, bh, g, lane, M, l, o, qc, sqv, a.nsq > 0, ne, hl.can_append);
   }
-};
-
-// One 4-wave workgroup per KV head; wave w merges queries w, w + 4, ...  lens is read by
-// every wave before the barrier and bumped after it, so no query of the head can see the
-// bumped length.
-template <class T, int D>
-__global__ void __launch_bounds__(256) k_decode_merge(DecodeArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int head = blockIdx.x;
-  MergeQuery<T, D> mq;
-  if (wave < a.G) mq.load(a, head, wave, lane);
-  const HeadLen hl = head_len(a, a.lens[head]);
-  const int ne = a.n_e[head];
-  for (int g = wave; g < a.G; g += 4) {
-    if (g != wave) mq.load(a, head, g, lane);
-    mq.finish(a, head, g, lane, hl, ne);
-  }
-  __syncthreads();  // every wave has read lens
-  if (threadIdx.x == 0 && hl.can_append) a.lens[head] = hl.old_len + 1;
+  // count in; the wave completing the head's count merges it
+  stores_complete();
+  int prior = 0;
+  if (lane == 0) prior = atomicAdd(a.cnt + head, 1);
+  prior = __builtin_amdgcn_readfirstlane(prior);
+  if (prior != a.nsq + a.nsplit - 1) return;
+  loads_after_count();
+  merge_head<T, D>(a, head, lane);
 }
 
 template <class T, int D, int GMAX, int PREP>
@@ -759,9 +901,6 @@ static hipError_t launch_decode_p(const DecodeArgs& a, hipStream_t st) {
   }
   const unsigned grid = (unsigned)a.n_heads * (unsigned)(a.nsq + a.nsplit);
   hipLaunchKernelGGL((k_decode_slice<T, D, GMAX, PREP>), dim3(grid), dim3(64), 0, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_decode_merge<T, D>), dim3(a.n_heads), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -68,7 +68,8 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
   return MKV_OK;
 }
 
-mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* total) {
+mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* total,
+                              size_t cnt_slots) {
   mkv::DecodeArgs a;
   std::memset(&a, 0, sizeof a);
   a.n_heads = p->batch * p->n_kv_heads;
@@ -86,7 +87,10 @@ mkv::DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* tota
   const size_t H = a.n_heads, D = p->head_dim, G = a.G;
   Carver c;
   c.base = static_cast<char*>(ws);
-  a.flag = c.take<int32_t>(sizeof(int32_t));  // zero-filled once by the caller
+  // The leading bytes (the flag, then one arrival counter per head) are zero-filled by
+  // the caller before first use; every call leaves the counters at zero.
+  a.flag = c.take<int32_t>(sizeof(int32_t));
+  a.cnt = c.take<int32_t>(std::max<size_t>(cnt_slots, H) * sizeof(int32_t));
   a.part_o = c.take<float>(H * a.nsplit * G * D * sizeof(float));
   a.part_ml = c.take<float>(H * a.nsplit * G * 2 * sizeof(float));
   a.sq = c.take<float>(H * G * D * sizeof(float));
@@ -147,12 +151,18 @@ extern "C" {
 size_t momentkv_decode_workspace_size(const mkv_decode_params* p) {
   if (check_decode_params(p) != MKV_OK) return 0;
   size_t total = 0;
-  decode_layout(p, nullptr, &total);
+  decode_layout(p, nullptr, &total, 0);
   return total;
 }
 
 size_t momentkv_decode_workspace_bytes(const mkv_decode_params* p) {
   return momentkv_decode_workspace_size(p);
+}
+
+size_t momentkv_decode_workspace_zero_bytes(const mkv_decode_params* p) {
+  if (check_decode_params(p) != MKV_OK) return 0;
+  const size_t heads = (size_t)p->batch * p->n_kv_heads;
+  return align_up(sizeof(int32_t)) + align_up(heads * sizeof(int32_t));
 }
 
 size_t momentkv_prepared_summary_size(const mkv_decode_params* p) {
@@ -175,7 +185,7 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
       ranges_overlap(prepared, out_bytes, n_e, heads * 4))
     return MKV_ERR_ALIAS;
   size_t total = 0;
-  mkv::DecodeArgs a = decode_layout(p, nullptr, &total);
+  mkv::DecodeArgs a = decode_layout(p, nullptr, &total, 0);
   a.n_e = n_e;
   a.s_k = s_k;
   a.s_v = s_v;
@@ -196,12 +206,12 @@ mkv_status momentkv_decode_attn(const mkv_decode_params* p, const void* q, void*
   st = check_decode_buffers(p, q, k_cache, v_cache, lens, k_new, v_new, n_e, s_k, s_v, S, out);
   if (st != MKV_OK) return st;
   size_t need = 0;
-  decode_layout(p, nullptr, &need);
+  decode_layout(p, nullptr, &need, 0);
   if (!workspace || workspace_bytes < need) return MKV_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return MKV_ERR_WORKSPACE;
   if (decode_overlaps(p, workspace, need, k_cache, v_cache, out)) return MKV_ERR_ALIAS;
   size_t total = 0;
-  mkv::DecodeArgs a = decode_layout(p, workspace, &total);
+  mkv::DecodeArgs a = decode_layout(p, workspace, &total, 0);
   set_decode_buffers(a, q, k_cache, v_cache, lens, k_new, v_new, n_e, s_k, s_v, S, out, lse_out,
                      w_r_out);
   hipError_t e = mkv::launch_decode(a, p->dtype == MKV_BF16, p->head_dim,

@@ -15,9 +15,15 @@ using namespace mkv::abi;
 namespace {
 
 constexpr size_t kScratchBytes = MOMENTKV_NOALLOC_SCRATCH_BYTES;
+// Arrival counters of the split launch: a fixed region at the start of the array, so that
+// calls of every shape find them where the previous call left them (at zero).  A call
+// needs at least 512 bytes of partials per KV head, so no call that fits the array has
+// more heads than this.
+constexpr size_t kCounterSlots = kScratchBytes / 512;
 
 // The decode workspace of momentkv_decode_attn_noalloc.  In host code this name is only a
 // stand-in for the symbol: its device address comes from hipGetSymbolAddress, per device.
+// Zero when the code object is loaded; every call leaves its counter region at zero.
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 constexpr int kMaxDevices = 64;
@@ -54,8 +60,9 @@ mkv_status momentkv_decode_attn_noalloc(const mkv_decode_params* p, const void* 
   mkv_status st = check_decode_params(p);
   if (st != MKV_OK) return st;
   size_t need = 0;
-  decode_layout(p, nullptr, &need);
-  if (need > kScratchBytes) return MKV_ERR_WORKSPACE;
+  decode_layout(p, nullptr, &need, kCounterSlots);
+  if (need > kScratchBytes || (size_t)p->batch * p->n_kv_heads > kCounterSlots)
+    return MKV_ERR_WORKSPACE;
   st = check_decode_buffers(p, q, k_cache, v_cache, lens, k_new, v_new, n_e, s_k, s_v, S, out);
   if (st != MKV_OK) return st;
   if (flag && decode_overlaps(p, flag, sizeof(int32_t), k_cache, v_cache, out)) return MKV_ERR_ALIAS;
@@ -69,7 +76,7 @@ mkv_status momentkv_decode_attn_noalloc(const mkv_decode_params* p, const void* 
   void* ws = nullptr;
   if (scratch_address(dev, &ws) != hipSuccess) return MKV_ERR_HIP;
   size_t total = 0;
-  mkv::DecodeArgs a = decode_layout(p, ws, &total);
+  mkv::DecodeArgs a = decode_layout(p, ws, &total, kCounterSlots);
   if (flag) a.flag = flag;  // otherwise the flag slot of the scratch, which nobody reads
   set_decode_buffers(a, q, k_cache, v_cache, lens, k_new, v_new, n_e, s_k, s_v, S, out, lse_out,
                      w_r_out);

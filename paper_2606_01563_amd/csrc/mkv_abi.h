@@ -37,7 +37,9 @@ inline size_t elem_size(int32_t dtype) { return dtype == MKV_BF16 ? 2 : 4; }
 
 // Decode parameters and workspace layout (defined with the decode entry points).
 mkv_status check_decode_params(const mkv_decode_params* p);
-DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* total);
+// The arrival counters take max(cnt_slots, heads) slots after the flag (a fixed region when
+// one buffer serves calls of every shape).
+DecodeArgs decode_layout(const mkv_decode_params* p, void* ws, size_t* total, size_t cnt_slots);
 // Required pointers present and the caches, query and output disjoint.
 mkv_status check_decode_buffers(const mkv_decode_params* p, const void* q, const void* k_cache,
                                 const void* v_cache, const int32_t* lens, const void* k_new,

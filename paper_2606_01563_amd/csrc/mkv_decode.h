@@ -25,6 +25,7 @@ struct DecodeArgs {
   float* part_ml;           // [B*Hkv, nsplit, G, 2]  (max in log2 units, sum)
   float* sq;                // [B*Hkv, G, D]  S_tilde q (unscaled)
   int32_t* flag;            // sticky append-overflow flag
+  int32_t* cnt;             // [n_heads] arrival counters of the split launch, zero between calls
   int n_heads;              // B * Hkv
   int n_pairs;              // B * Hq
   int Hkv, G, cap;

@@ -74,6 +74,7 @@ def lib() -> ctypes.CDLL:
             getattr(L, name).argtypes = [ctypes.POINTER(CompressParams)]
             getattr(L, name).restype = ctypes.c_size_t
         for name in ("momentkv_decode_workspace_bytes", "momentkv_decode_workspace_size",
+                     "momentkv_decode_workspace_zero_bytes",
                      "momentkv_decode_evict_workspace_bytes",
                      "momentkv_decode_evict_workspace_size"):
             getattr(L, name).argtypes = [ctypes.POINTER(DecodeParams)]
@@ -311,9 +312,18 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
     return out
 
 
-def decode_workspace_zero_bytes(p: DecodeParams) -> int:
-    """Leading workspace bytes (the append-overflow flag) to zero before first use."""
-    return 256
+def momentkv_decode_workspace_zero_bytes(p: DecodeParams) -> int:
+    """Leading decode-workspace bytes that must be zero before a call (the append-overflow
+    flag and the per-head arrival counters, which every call leaves at zero)."""
+    return int(lib().momentkv_decode_workspace_zero_bytes(ctypes.byref(p)))
+
+
+def _zero_prefix(ws: torch.Tensor, nbytes: int) -> None:
+    """Zeroes the leading nbytes of a decode workspace unless this tensor object is known
+    to have them at zero already (zeroed here before; calls leave them at zero)."""
+    if getattr(ws, "_mkv_zeroed", 0) < nbytes:
+        ws[:nbytes].zero_()
+        ws._mkv_zeroed = nbytes
 
 
 def decode_params(q, k_cache, *, max_len, order=1, scale=0.0, tau=1e-6,
@@ -412,8 +422,10 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     `S` is the raw sum (summary=0) or the output of momentkv_prepare_summary (summary=1).
 
     `max_len` bounds lens after the append (defaults to the cache capacity).  The first
-    int32 of the workspace is the sticky append-overflow flag; a workspace allocated here
-    gets it zeroed, a caller-owned one should be zeroed once before first use.
+    int32 of the workspace is the sticky append-overflow flag.  The leading
+    momentkv_decode_workspace_zero_bytes(p) bytes (the flag and the per-head arrival
+    counters) are zeroed here the first time a workspace tensor is used with this prefix
+    length (the flag included); calls leave the counters at zero.
     """
     _check_decode_args(q, k_cache, v_cache, lens, n_e, s_k, s_v, S, k_new, v_new, out, lse, w_r,
                        workspace, summary)
@@ -427,10 +439,8 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     if nbytes == 0:
         code = lib().momentkv_decode_attn(ctypes.byref(p), *([None] * 13), None, 0, None)
         raise MomentKVError(code, "momentkv_decode_attn")
-    fresh = workspace is None or workspace.numel() < nbytes
     ws = _workspace(nbytes, dev, workspace)
-    if fresh:
-        ws[:decode_workspace_zero_bytes(p)].zero_()
+    _zero_prefix(ws, momentkv_decode_workspace_zero_bytes(p))
     code = lib().momentkv_decode_attn(
         ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lens), _ptr(k_new),
         _ptr(v_new), _ptr(n_e), _ptr(s_k), _ptr(s_v), _ptr(S), _ptr(out), _ptr(lse), _ptr(w_r),
@@ -497,7 +507,7 @@ def momentkv_decode_evict(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch
     fresh = workspace is None or workspace.numel() < nbytes
     ws = _workspace(nbytes, dev, workspace)
     if fresh:
-        ws[:decode_workspace_zero_bytes(p)].zero_()
+        ws[:256].zero_()  # the sticky flag
     code = lib().momentkv_decode_evict(
         ctypes.byref(p), int(budget), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lens),
         _ptr(k_new), _ptr(v_new), _ptr(n_e), _ptr(s_k), _ptr(s_v), _ptr(S), _ptr(out),

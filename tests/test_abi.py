@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert mk.momentkv_abi_version() == 5
+    assert mk.momentkv_abi_version() == 6
     for code in range(10):
         assert mk.momentkv_status_string(code) not in ("", "unknown status")
     assert mk.momentkv_status_string(99) == "unknown status"
@@ -93,6 +93,18 @@ def test_workspace_sizes(L):
     # size grows with context and with budget
     assert mk.momentkv_compress_workspace_bytes(cparams(ctx_len=131072, window=64, budget=1024, cap=1024)) > \
         mk.momentkv_compress_workspace_bytes(cparams())
+
+
+def test_decode_zero_prefix_covers_the_flag_and_one_counter_per_head(L):
+    """The leading bytes to zero: the flag's 256-byte slot, then one int32 arrival counter
+    per KV head (rounded up to 256 bytes), inside the workspace; 0 on invalid parameters."""
+    for batch in (1, 36, 65):
+        p = dparams(batch=batch)
+        heads = batch * p.n_kv_heads
+        zb = mk.momentkv_decode_workspace_zero_bytes(p)
+        assert zb == 256 + (4 * heads + 255) // 256 * 256
+        assert zb < mk.momentkv_decode_workspace_bytes(p)
+    assert mk.momentkv_decode_workspace_zero_bytes(dparams(max_len=641)) == 0
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -81,6 +81,50 @@ def test_decode_large_query_groups(G, n_split):
     P.run_decode_steps(gpu, out, 3, n_split=n_split, summary=1)
 
 
+def test_split_decode_repeats_bit_exact_and_leaves_counters_at_zero():
+    """The split shape merges each head in the launch (the last slice to finish): 24
+    repeated calls on the same inputs give the same bits whichever wave merged, the
+    per-head arrival counters are back at zero after every call, the result agrees with
+    the single-workgroup shape, and a workspace first used by a call with fewer heads
+    serves a call with more (its extra counter bytes are zeroed by the binding)."""
+    g = torch.Generator(device="cuda").manual_seed(7)
+    B, Hkv, G, d, cap = 36, 8, 4, 128, 700
+    kc = torch.randn(B, Hkv, cap, d, device="cuda", generator=g).to(torch.bfloat16)
+    vc = torch.randn(B, Hkv, cap, d, device="cuda", generator=g).to(torch.bfloat16)
+    q = torch.randn(B, Hkv * G, d, device="cuda", generator=g).to(torch.bfloat16)
+    lens = torch.randint(0, cap + 1, (B, Hkv), device="cuda", generator=g, dtype=torch.int32)
+    n_e = torch.randint(0, 5000, (B, Hkv), device="cuda", generator=g, dtype=torch.int32)
+    s_k = torch.randn(B, Hkv, d, device="cuda", generator=g) * 30
+    s_v = torch.randn(B, Hkv, d, device="cuda", generator=g) * 30
+    S = torch.randn(B, Hkv, d, d, device="cuda", generator=g) * 50
+    args = (q, kc, vc, lens, n_e, s_k, s_v, S)
+    small = tuple(t[:2] for t in args)
+    for n_split in (3, 0):
+        ws = mk.momentkv_decode_attn(*small, max_len=cap, n_split=n_split)[3]
+        ref = None
+        for rep in range(24):
+            o, lse, w, ws = mk.momentkv_decode_attn(*args, max_len=cap, n_split=n_split,
+                                                    lse=torch.empty(B, Hkv * G, device="cuda"),
+                                                    w_r=torch.empty(B, Hkv * G, device="cuda"),
+                                                    workspace=ws)
+            if ref is None:
+                ref = (o.clone(), lse.clone(), w.clone())
+            else:
+                assert torch.equal(o, ref[0]) and torch.equal(lse, ref[1]) and torch.equal(w, ref[2]), rep
+            cnt = ws[256:256 + 4 * B * Hkv].view(torch.int32)
+            assert int(cnt.abs().sum()) == 0, rep
+        one, lse1, w1, _ = mk.momentkv_decode_attn(*args, max_len=cap, n_split=1,
+                                                   lse=torch.empty(B, Hkv * G, device="cuda"),
+                                                   w_r=torch.empty(B, Hkv * G, device="cuda"))
+        rel = (one.float() - ref[0].float()).norm(dim=-1) / one.float().norm(dim=-1).clamp_min(1e-30)
+        announce(f"n_split={n_split}: split vs single workgroup, max rel {float(rel.max()):.2e}")
+        assert float(rel.max()) < 2e-2
+        finite = torch.isfinite(lse1)
+        assert torch.equal(finite, torch.isfinite(ref[1]))
+        assert float((lse1[finite] - ref[1][finite]).abs().max()) < 1e-4
+        assert float((w1 - ref[2]).abs().max()) < 1e-4
+
+
 @pytest.mark.parametrize("append", [True, False])
 @pytest.mark.parametrize("n_split", [0, 3, 4])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
