@@ -827,8 +827,11 @@ __device__ __forceinline__ void merge_head(const DecodeArgs& a, int head, int la
 // rows, or the slice's unnormalised (o, max, sum)), then counts itself in on its head's
 // counter; the wave that completes the count merges the head (merge_head) and sets the
 // counter back to zero for the next call.
+// bf16: three waves per SIMD fit without spills (the accumulators move from AGPRs to
+// VGPRs); the fp32 form keeps the compiler's choice.
 template <class T, int D, int GMAX, int PREP>
-__global__ void __launch_bounds__(64) k_decode_slice(DecodeArgs a) {
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 ? 3 : 1)))
+k_decode_slice(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int KS = D / 32;
   constexpr int VT_BYTES = (int)sizeof(typename BA::VtTile);
