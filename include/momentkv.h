@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define MOMENTKV_ABI_VERSION 6
+#define MOMENTKV_ABI_VERSION 7
 
 typedef enum {
   MKV_OK = 0,
@@ -95,7 +95,8 @@ typedef enum { MKV_F32 = 0, MKV_BF16 = 1 } mkv_dtype;
  *      moments of the round before.  This build supports mi_rounds in [-1, 8].
  *   5. Outputs: the retained positions idx (ascending: sinks, kept candidates, window)
  *      and their K/V rows copied to k_out/v_out; lens = min(budget, N); the raw sums of
- *      the final evicted set E (n_e = |E|, s_k, s_v, S = sum_E v_i k_i^T, fp32).
+ *      the final evicted set E (n_e = |E|, s_k, s_v, S = sum_E v_i k_i^T), accumulated
+ *      in fp32; S is stored in fp32 or, with moment_dtype = MKV_BF16, in bf16.
  *   budget >= N keeps every token: idx = 0..N-1, n_e = 0 and zero moments.
  *   adaptive = 1 (head-adaptive budgets, Sec. 5.1 after Ada-KV): per sequence, the
  *      Hkv * k_keep candidates with the largest abar over all the layer's heads (equal
@@ -120,6 +121,9 @@ typedef struct {
   float scale;          /* logit scale; 0 selects 1/sqrt(d)                          */
   float tau;            /* covariance clamp threshold (paper: 1e-6); >= 0            */
   int32_t adaptive;     /* 0 = budget per head; 1 = head-adaptive split (step 5)     */
+  int32_t moment_dtype; /* mkv_dtype of the output S: MKV_F32, or MKV_BF16 = the fp32 */
+                        /* sum rounded once to bf16 (RNE), the 16-bit moment storage */
+                        /* of App. C.2 (s_k, s_v stay fp32: 2d of the d^2 + 2d)      */
 } mkv_compress_params;
 
 /* Optional per-candidate diagnostics (any field may be NULL).  n_c = N - w - n_s.
@@ -151,7 +155,7 @@ size_t momentkv_compress_workspace_size(const mkv_compress_params* p);
  * workspace                  >= momentkv_compress_workspace_bytes(p) bytes, 256-aligned */
 mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, const void* k,
                              const void* v, void* k_out, void* v_out, int32_t* idx_out,
-                             int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, float* S,
+                             int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, void* S,
                              const mkv_compress_debug* dbg, void* workspace,
                              size_t workspace_bytes, void* stream);
 
@@ -191,7 +195,9 @@ typedef struct {
                         /* either way.                                               */
   int32_t summary;      /* form of the S argument: 0 = the raw sum S (fp32); 1 = the */
                         /* prepared form written by momentkv_prepare_summary; 2 =    */
-                        /* its half-precision form (bf16 caches only)               */
+                        /* its half-precision form (bf16 caches only); 3 = the raw   */
+                        /* sum stored in bf16 (compress with moment_dtype MKV_BF16), */
+                        /* centred and clamped in fp32 as for 0                      */
 } mkv_decode_params;
 
 /* Bytes of device workspace momentkv_decode_attn needs for these parameters (0 on invalid
@@ -220,7 +226,8 @@ size_t momentkv_decode_workspace_zero_bytes(const mkv_decode_params* p);
  * Heads with n_e = 0 get zeros.  Uses batch, n_q_heads, n_kv_heads, head_dim, dtype and
  * tau of p (the other fields are validated as for the decode).  `prepared` holds
  * momentkv_prepared_summary_size(p) bytes (16-byte aligned) and must not overlap the
- * inputs.  Decode calls with p->summary = 1 read it in place of S. */
+ * inputs.  Decode calls with p->summary = 1 (2) read it in place of S.  S is the fp32 raw
+ * sum; p->summary = 3 (a bf16 raw sum) has no prepared form (MKV_ERR_SHAPE, size 0). */
 size_t momentkv_prepared_summary_size(const mkv_decode_params* p);
 mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n_e,
                                     const float* s_k, const float* s_v, const float* S,
@@ -235,7 +242,8 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
  * k_new, v_new [B, Hkv, d] or both NULL
  * n_e [B, Hkv] int32, s_k, s_v [B, Hkv, d] fp32: the summary, read only
  * S         p->summary = 0: the raw sum, fp32 [B, Hkv, d, d]; p->summary = 1 or 2: the
- *           output of momentkv_prepare_summary for the same summary, tau, dtype and form
+ *           output of momentkv_prepare_summary for the same summary, tau, dtype and form;
+ *           p->summary = 3: the raw sum in bf16 [B, Hkv, d, d]
  * out       [B, Hq, d]
  * lse_out   NULL or [B, Hq] fp32: log Z_R (retained partition function, logits scaled)
  * w_r_out   NULL or [B, Hq] fp32: the mixing weight w_R

@@ -1092,9 +1092,11 @@ __device__ void slice_cov(const CompressArgs& a, int head, int sl, const int32_t
 // Eight lanes per float4 of a head's D*D + 2D values, lane `sub` summing slots
 // s0 + sub, s0 + sub + 8, ..., then a fixed xor tree across the eight lanes.
 // ------------------------------------------------------------------------------------
+// S_bf16: S_out holds bf16 (each fp32 sum rounded once, to nearest even).
 template <int D>
-__device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, int bx, float* S_out,
-                                             float* sv_out, float* sk_out, int32_t* ne_out) {
+__device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, int bx, void* S_out,
+                                             bool S_bf16, float* sv_out, float* sk_out,
+                                             int32_t* ne_out) {
   constexpr int NSF4 = D * D / 4, NF4 = (D * D + 2 * D) / 4;
   const int f4 = bx * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
@@ -1119,14 +1121,19 @@ __device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, in
     acc.w += __shfl_xor(acc.w, x);
   }
   if (f4 < NF4 && sub == 0) {
-    float* dst;
-    if (f4 < NSF4) {
-      dst = S_out + (size_t)head * D * D + 4 * f4;
+    if (f4 < NSF4 && S_bf16) {
+      bf16_t* dst = static_cast<bf16_t*>(S_out) + (size_t)head * D * D + 4 * f4;
+      *reinterpret_cast<uint2*>(dst) = make_uint2(bf16_pair(acc.x, acc.y), bf16_pair(acc.z, acc.w));
     } else {
-      const int e = 4 * (f4 - NSF4);  // [0, D): s_v, [D, 2D): s_k
-      dst = e < D ? sv_out + (size_t)head * D + e : sk_out + (size_t)head * D + (e - D);
+      float* dst;
+      if (f4 < NSF4) {
+        dst = static_cast<float*>(S_out) + (size_t)head * D * D + 4 * f4;
+      } else {
+        const int e = 4 * (f4 - NSF4);  // [0, D): s_v, [D, 2D): s_k
+        dst = e < D ? sv_out + (size_t)head * D + e : sk_out + (size_t)head * D + (e - D);
+      }
+      *reinterpret_cast<float4*>(dst) = acc;
     }
-    *reinterpret_cast<float4*>(dst) = acc;
   }
   if (ne_out && bx == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - head_keep(a, head);
 }
@@ -1138,7 +1145,7 @@ template <int D> constexpr int reduce_blocks() { return ((D * D + 2 * D) / 4 + 3
 template <int D>
 __global__ void __launch_bounds__(256) k_reduce(CompressArgs a, float* S_out, float* sv_out,
                                                  float* sk_out, int32_t* ne_out) {
-  reduce_slots<D>(a, blockIdx.y, blockIdx.x, S_out, sv_out, sk_out, ne_out);
+  reduce_slots<D>(a, blockIdx.y, blockIdx.x, S_out, false, sv_out, sk_out, ne_out);
   if (blockIdx.x == 0)
     for (int b = threadIdx.x; b < TK_HBINS; b += 256)
       a.tk_hh[((size_t)a.H + blockIdx.y) * TK_HBINS + b] = 0u;
@@ -1357,15 +1364,17 @@ template <class T, int D>
 __global__ void __launch_bounds__(256) k_finish(CompressArgs a, int n_out) {
   const int head = blockIdx.y;
   constexpr int RB = reduce_blocks<D>();
-  if ((int)blockIdx.x < RB) reduce_slots<D>(a, head, blockIdx.x, a.S, a.s_v, a.s_k, a.n_e);
+  if ((int)blockIdx.x < RB) reduce_slots<D>(a, head, blockIdx.x, a.S, a.S_bf16, a.s_v, a.s_k, a.n_e);
   else gather_out<T, D>(a, head, blockIdx.x - RB, n_out, 0);
 }
 
 template <int D>
 __global__ void __launch_bounds__(256) k_zero_moments(CompressArgs a) {
   const int head = blockIdx.y;
-  for (int e = blockIdx.x * 256 + threadIdx.x; e < D * D; e += gridDim.x * 256)
-    a.S[(size_t)head * D * D + e] = 0.f;
+  for (int e = blockIdx.x * 256 + threadIdx.x; e < D * D; e += gridDim.x * 256) {
+    if (a.S_bf16) static_cast<bf16_t*>(a.S)[(size_t)head * D * D + e] = 0;
+    else static_cast<float*>(a.S)[(size_t)head * D * D + e] = 0.f;
+  }
   if (blockIdx.x == 0) {
     for (int t = threadIdx.x; t < D; t += 256) {
       a.s_k[(size_t)head * D + t] = 0.f;

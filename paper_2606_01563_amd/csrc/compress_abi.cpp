@@ -38,6 +38,7 @@ mkv_status check_compress_params(const mkv_compress_params* p) {
   if (p->ctx_len - p->window - p->n_sink > kMaxCandidates) return MKV_ERR_UNSUPPORTED;
   if (p->budget < p->ctx_len && p->budget < p->n_sink + p->window) return MKV_ERR_BUDGET;
   if (p->adaptive != 0 && p->adaptive != 1) return MKV_ERR_SHAPE;
+  if (p->moment_dtype != MKV_F32 && p->moment_dtype != MKV_BF16) return MKV_ERR_DTYPE;
   int n_out = p->budget < p->ctx_len ? p->budget : p->ctx_len;
   if (p->adaptive && p->budget < p->ctx_len) {
     const int64_t n_c = p->ctx_len - p->window - p->n_sink;
@@ -150,7 +151,7 @@ size_t momentkv_compress_workspace_bytes(const mkv_compress_params* p) {
 
 mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, const void* k,
                              const void* v, void* k_out, void* v_out, int32_t* idx_out,
-                             int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, float* S,
+                             int32_t* lens_out, int32_t* n_e, float* s_k, float* s_v, void* S,
                              const mkv_compress_debug* dbg, void* workspace,
                              size_t workspace_bytes, void* stream) {
   mkv_status st = check_compress_params(p);
@@ -183,6 +184,7 @@ mkv_status momentkv_compress(const mkv_compress_params* p, const void* q_win, co
   a.s_k = s_k;
   a.s_v = s_v;
   a.S = S;
+  a.S_bf16 = p->moment_dtype == MKV_BF16 ? 1 : 0;
   hipError_t e = mkv::launch_compress(a, p->dtype == MKV_BF16, static_cast<hipStream_t>(stream),
                                       dbg ? dbg->abar : nullptr, dbg ? dbg->score0 : nullptr,
                                       dbg ? dbg->score : nullptr, dbg ? dbg->kept0 : nullptr);

@@ -133,12 +133,14 @@ __device__ __forceinline__ void append_row(const DecodeArgs& a, int head, int ro
 //  * prepared, fp32 caches: the stored S_tilde on fp32 MFMA;
 //  * prepared, bf16 caches: the stored hi / lo bf16 planes on bf16 MFMA, two products per
 //    32-wide step against the (exact) bf16 queries;
-//  * prepared in half precision (PREP = 2, bf16 caches): the hi plane alone, one product.
+//  * prepared in half precision (PREP = 2, bf16 caches): the hi plane alone, one product;
+//  * raw S stored in bf16 (PREP = 3): as the raw fp32 form, from bf16 loads.
 template <class T, int D, int PREP>
 struct SqRows {
   static constexpr int KS = D / 32;
   static constexpr bool HILO = PREP == 1 && sizeof(T) == 2;
   static constexpr bool HI1 = PREP == 2;  // one bf16 plane (bf16 caches only)
+  static constexpr bool RAW = PREP == 0 || PREP == 3;  // centred and clamped here
   f32x8 raw[2][KS];
   bf16x8 hi[2][KS], lo[2][KS];
   f32x8 skc[KS];
@@ -167,15 +169,23 @@ struct SqRows {
         for (int ks = 0; ks < KS; ++ks) hi[u][ks] = load_frag(P + (size_t)row * D + 32 * ks + col);
       }
     } else {
-      const float* Sh = a.S + (size_t)head * D * D;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int row = r0 + 16 * u + (lane & 15);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) raw[u][ks] = load_frag(Sh + (size_t)row * D + 32 * ks + col);
-        if constexpr (!PREP) sv[u] = a.s_v[(size_t)head * D + row];
+        for (int ks = 0; ks < KS; ++ks) {
+          const size_t off = ((size_t)head * D + row) * D + 32 * ks + col;
+          if constexpr (PREP == 3) {
+            const bf16x8 b = load_frag(reinterpret_cast<const bf16_t*>(a.S) + off);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) raw[u][ks][e] = elem_f(b, e);
+          } else {
+            raw[u][ks] = load_frag(a.S + off);
+          }
+        }
+        if constexpr (RAW) sv[u] = a.s_v[(size_t)head * D + row];
       }
-      if constexpr (!PREP) {
+      if constexpr (RAW) {
         ne = a.n_e[head];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) skc[ks] = load_frag(a.s_k + (size_t)head * D + 32 * ks + col);
@@ -208,7 +218,7 @@ struct SqRows {
       }
     } else {
       float inv_n = 0.f;
-      if constexpr (!PREP) inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
+      if constexpr (RAW) inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
       f32x8 qb[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
@@ -910,6 +920,7 @@ static hipError_t launch_decode_p(const DecodeArgs& a, hipStream_t st) {
 template <class T, int D, int GMAX>
 static hipError_t launch_decode_t(const DecodeArgs& a, hipStream_t st) {
   if (a.summary == 1) return launch_decode_p<T, D, GMAX, 1>(a, st);
+  if (a.summary == 3) return launch_decode_p<T, D, GMAX, 3>(a, st);
   if constexpr (sizeof(T) == 2) {
     if (a.summary == 2) return launch_decode_p<T, D, GMAX, 2>(a, st);
   }

@@ -57,7 +57,7 @@ mkv_status check_decode_params(const mkv_decode_params* p) {
   if (p->head_dim != 64 && p->head_dim != 128) return MKV_ERR_UNSUPPORTED;
   if (p->n_q_heads / p->n_kv_heads > 16) return MKV_ERR_UNSUPPORTED;
   if (p->n_split < 0) return MKV_ERR_SHAPE;
-  if (p->summary < 0 || p->summary > 2) return MKV_ERR_SHAPE;
+  if (p->summary < 0 || p->summary > 3) return MKV_ERR_SHAPE;
   if (p->summary == 2 && p->dtype != MKV_BF16) return MKV_ERR_SHAPE;  // half precision: bf16 only
   if (p->max_len < 1 || p->max_len > p->cap) return MKV_ERR_CAPACITY;
   // grid of single-wave workgroups: B * Hkv * (slices + covariance waves)
@@ -166,7 +166,7 @@ size_t momentkv_decode_workspace_zero_bytes(const mkv_decode_params* p) {
 }
 
 size_t momentkv_prepared_summary_size(const mkv_decode_params* p) {
-  if (check_decode_params(p) != MKV_OK) return 0;
+  if (check_decode_params(p) != MKV_OK || p->summary == 3) return 0;
   return (size_t)p->batch * p->n_kv_heads * p->head_dim * p->head_dim * (p->summary == 2 ? 2 : 4);
 }
 
@@ -175,6 +175,7 @@ mkv_status momentkv_prepare_summary(const mkv_decode_params* p, const int32_t* n
                                     void* prepared, void* stream) {
   mkv_status st = check_decode_params(p);
   if (st != MKV_OK) return st;
+  if (p->summary == 3) return MKV_ERR_SHAPE;  // the raw bf16 form has no prepared form
   if (!n_e || !s_k || !s_v || !S || !prepared) return MKV_ERR_NULL;
   if (reinterpret_cast<uintptr_t>(prepared) % 16) return MKV_ERR_SHAPE;
   const size_t heads = (size_t)p->batch * p->n_kv_heads, d = p->head_dim;

@@ -24,7 +24,8 @@ struct CompressArgs {
   int32_t* n_e;             // [B, Hkv]
   float* s_k;               // [B, Hkv, D]
   float* s_v;
-  float* S;                 // [B, Hkv, D, D]
+  void* S;                  // [B, Hkv, D, D] fp32, or bf16 when S_bf16
+  int S_bf16;               // the output S in bf16 (RNE of the fp32 sum)
   // workspace
   float* rowpart;           // [H, nsl1, R, 2]   per-slice (max log2, sum) of each window row
   float* rowstat;           // [H, R, 2]         (max log2, 1/Z)

@@ -17,7 +17,8 @@ struct DecodeArgs {
   const int32_t* n_e;       // [B, Hkv]
   const float* s_k;         // [B, Hkv, D]
   const float* s_v;
-  const float* S;           // [B, Hkv, D, D] raw sum, or the prepared form (summary = 1)
+  const float* S;           // [B, Hkv, D, D] raw fp32 sum (summary 0), the prepared form
+                            // (1, 2), or the raw sum stored in bf16 (3)
   void* out;                // [B, Hq, D]
   float* lse_out;           // [B, Hq] or null
   float* w_r_out;           // [B, Hq] or null
@@ -32,7 +33,7 @@ struct DecodeArgs {
   int fused;                // 1: one workgroup per KV head, single launch
   int nsplit, split_len;    // split launch: token slices per KV head, rows per slice (x 32)
   int nsq;                  // S_tilde q waves per KV head (D / 32 rows each; 0 at order 0)
-  int summary;              // 0: S is the raw sum; 1: S is the prepared form
+  int summary;              // 0: raw fp32 S; 1, 2: prepared forms; 3: raw bf16 S
   int order;
   float scale, tau;
 };

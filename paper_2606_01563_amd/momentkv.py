@@ -42,7 +42,7 @@ class CompressParams(ctypes.Structure):
                 ("chunk", ctypes.c_int32), ("mi_rounds", ctypes.c_int32),
                 ("cap", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("tau", ctypes.c_float),
-                ("adaptive", ctypes.c_int32)]
+                ("adaptive", ctypes.c_int32), ("moment_dtype", ctypes.c_int32)]
 
 
 class CompressDebug(ctypes.Structure):
@@ -216,7 +216,7 @@ class CompressOutput:
     n_e: torch.Tensor         # [B, Hkv] int32
     s_k: torch.Tensor         # [B, Hkv, d] fp32
     s_v: torch.Tensor
-    S: torch.Tensor           # [B, Hkv, d, d] fp32
+    S: torch.Tensor           # [B, Hkv, d, d] fp32, or bf16 (moment_dtype=torch.bfloat16)
     abar: torch.Tensor | None = None
     score0: torch.Tensor | None = None
     score: torch.Tensor | None = None
@@ -234,29 +234,36 @@ def compress_rows(N: int, Hkv: int, budget: int, window: int, n_sink: int = 1,
 
 
 def compress_params(q_win, k, budget, *, n_sink=1, chunk=4, mi_rounds=1, cap=None,
-                    scale=0.0, tau=1e-6, adaptive=False) -> CompressParams:
+                    scale=0.0, tau=1e-6, adaptive=False,
+                    moment_dtype=torch.float32) -> CompressParams:
     B, Hq, w, d = q_win.shape
     _, Hkv, N, _ = k.shape
     n_out = compress_rows(N, Hkv, budget, w, n_sink, adaptive)
+    if moment_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError(f"moment_dtype must be float32 or bfloat16, got {moment_dtype}")
     return CompressParams(B, Hq, Hkv, d, N, budget, w, n_sink, chunk, mi_rounds,
                           n_out if cap is None else cap, _dtype_code(k), scale, tau,
-                          1 if adaptive else 0)
+                          1 if adaptive else 0,
+                          MKV_BF16 if moment_dtype == torch.bfloat16 else MKV_F32)
 
 
 def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, budget: int, *,
                       n_sink: int = 1, chunk: int = 4, mi_rounds: int = 1, cap: int | None = None,
                       scale: float = 0.0, tau: float = 1e-6, adaptive: bool = False,
+                      moment_dtype: torch.dtype = torch.float32,
                       debug: bool = False, out: CompressOutput | None = None,
                       workspace: torch.Tensor | None = None) -> CompressOutput:
     """Compress [B, Hkv, N, d] prefill K/V to `budget` rows per KV head (see the header);
     adaptive=True splits the layer's candidate budget across heads (idx then has `cap`
-    entries per head, the first `lens` of them valid)."""
+    entries per head, the first `lens` of them valid); moment_dtype=torch.bfloat16 stores
+    the output S in bf16 (pass it to the decode with summary=3)."""
     if not isinstance(q_win, torch.Tensor) or q_win.dim() != 4:
         raise ValueError("q_win must be a [B, Hq, w, d] tensor")
     if not isinstance(k, torch.Tensor) or k.dim() != 4:
         raise ValueError("k must be a [B, Hkv, N, d] tensor")
     p = compress_params(q_win, k, budget, n_sink=n_sink, chunk=chunk, mi_rounds=mi_rounds,
-                        cap=cap, scale=scale, tau=tau, adaptive=adaptive)
+                        cap=cap, scale=scale, tau=tau, adaptive=adaptive,
+                        moment_dtype=moment_dtype)
     B, Hq, w, d = q_win.shape
     _, Hkv, N, _ = k.shape
     dev = k.device
@@ -271,7 +278,7 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
                                 ("v_out", (B, Hkv, p.cap, d), k.dtype),
                                 ("idx", (B, Hkv, n_out), i32), ("lens", (B, Hkv), i32),
                                 ("n_e", (B, Hkv), i32), ("s_k", (B, Hkv, d), f32),
-                                ("s_v", (B, Hkv, d), f32), ("S", (B, Hkv, d, d), f32)):
+                                ("s_v", (B, Hkv, d), f32), ("S", (B, Hkv, d, d), moment_dtype)):
             _expect(getattr(out, name), f"out.{name}", shape, dt)
     _same_device({"q_win": q_win, "k": k, "v": v, "workspace": workspace,
                   **({} if out is None else {f"out.{n}": getattr(out, n) for n in
@@ -285,7 +292,8 @@ def momentkv_compress(q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor, bud
             v_out=torch.empty(B, Hkv, p.cap, d, dtype=k.dtype, device=dev),
             idx=torch.empty(B, Hkv, n_out, **i32), lens=torch.empty(B, Hkv, **i32),
             n_e=torch.empty(B, Hkv, **i32), s_k=torch.empty(B, Hkv, d, **f32),
-            s_v=torch.empty(B, Hkv, d, **f32), S=torch.empty(B, Hkv, d, d, **f32))
+            s_v=torch.empty(B, Hkv, d, **f32),
+            S=torch.empty(B, Hkv, d, d, dtype=moment_dtype, device=dev))
     dbg = None
     if debug and budget < N:
         n_c = N - w - n_sink
@@ -391,8 +399,10 @@ def _check_decode_args(q, k_cache, v_cache, lens, n_e, s_k, s_v, S, k_new, v_new
             _expect(S, "S (prepared)", (B, Hkv, d, d), f32)
     elif summary == 2:
         _expect(S, "S (half-precision prepared)", (B, Hkv, d, d), torch.bfloat16)
+    elif summary == 3:
+        _expect(S, "S (raw, bf16)", (B, Hkv, d, d), torch.bfloat16)
     else:
-        raise ValueError(f"summary must be 0, 1 or 2, got {summary}")
+        raise ValueError(f"summary must be 0, 1, 2 or 3, got {summary}")
     if (k_new is None) != (v_new is None) or (need_new and k_new is None):
         raise ValueError("k_new and v_new must be given together" +
                          (" (required here)" if need_new else ""))
@@ -419,7 +429,8 @@ def momentkv_decode_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
                          workspace: torch.Tensor | None = None):
     """Corrected decode attention (see the header).  Returns (out, lse, w_r, workspace).
 
-    `S` is the raw sum (summary=0) or the output of momentkv_prepare_summary (summary=1).
+    `S` is the raw sum (summary=0), the output of momentkv_prepare_summary (summary=1, or 2
+    for its half-precision form), or the raw sum stored in bf16 (summary=3).
 
     `max_len` bounds lens after the append (defaults to the cache capacity).  The first
     int32 of the workspace is the sticky append-overflow flag.  The leading

@@ -358,13 +358,15 @@ def run_decode_steps(inp: dict, comp: mk.CompressOutput, steps: int, *, order=1,
     retained cache and fp32 moments.  `lens0` ([B, Hkv], each at most the compressed
     length) replaces the retained lengths before the first step.  Returns the list of max
     relative errors.  summary=1 (2) passes the prepared (half-precision) summary (the oracle reads the raw
-    moments)."""
+    moments); summary=3 passes a raw S stored in bf16 (compress with moment_dtype bf16), which
+    the oracle reads as it is."""
     dt = inp["k"].dtype
     tol = TOL[dt]
     B, Hkv, cap, d = comp.k_out.shape
     Hq = inp["q_win"].shape[1]
     G = Hq // Hkv
-    S_arg = comp.S if summary == 0 else mk.momentkv_prepare_summary(
+    # summary 3: comp.S is the raw sum stored in bf16, and the oracle reads the same values
+    S_arg = comp.S if summary in (0, 3) else mk.momentkv_prepare_summary(
         comp.n_e, comp.s_k, comp.s_v, comp.S, dtype=dt, tau=tau, half=summary == 2)
     lens = comp.lens.clone()
     if lens0 is not None:

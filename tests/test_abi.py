@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert mk.momentkv_abi_version() == 6
+    assert mk.momentkv_abi_version() == 7
     for code in range(10):
         assert mk.momentkv_status_string(code) not in ("", "unknown status")
     assert mk.momentkv_status_string(99) == "unknown status"
@@ -38,7 +38,7 @@ def test_abi_version_and_status_strings(L):
 def cparams(**kw):
     base = dict(batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, ctx_len=32768, budget=512,
                 window=32, n_sink=1, chunk=4, mi_rounds=1, cap=512, dtype=1, scale=0.0, tau=1e-6,
-                adaptive=0)
+                adaptive=0, moment_dtype=0)
     base.update(kw)
     return mk.CompressParams(**base)
 
@@ -126,6 +126,8 @@ def test_decode_zero_prefix_covers_the_flag_and_one_counter_per_head(L):
     (dict(adaptive=2), SHAPE),
     (dict(adaptive=1), CAPACITY),          # a head may take up to 8 x 479 candidates
     (dict(adaptive=1, ctx_len=140000, cap=9000), UNSUP),  # 8 x n_c candidates > 1048576
+    (dict(moment_dtype=2), DTYPE),           # output S: fp32 or bf16
+    (dict(moment_dtype=-1), DTYPE),
 ])
 def test_compress_rejects_invalid_parameters(L, kw, code):
     assert compress_status(cparams(**kw)) == code
@@ -166,7 +168,7 @@ def test_budget_at_least_context_is_valid(L):
     (dict(cap=0), SHAPE),
     (dict(order=2), SHAPE),
     (dict(n_split=-1), SHAPE),
-    (dict(summary=3), SHAPE),
+    (dict(summary=4), SHAPE),
     (dict(summary=2, dtype=0), SHAPE),      # the half-precision summary needs bf16 caches
     (dict(batch=500000), UNSUP),            # decode grid limit: 4M heads x 5 waves
     (dict(head_dim=80), UNSUP),
@@ -201,6 +203,11 @@ def test_prepared_summary_size_and_validation(L):
     assert f(ctypes.byref(p), *ptrs[:4], ptrs[4] + 8, None) == SHAPE      # misaligned
     assert f(ctypes.byref(p), *ptrs[:4], ptrs[3] + 64, None) == ALIAS     # overlaps S
     assert f(ctypes.byref(dparams(dtype=5)), *ptrs, None) == DTYPE
+    # the raw sum stored in bf16 (summary = 3) is read by the decode as it is: nothing to
+    # prepare
+    assert mk.momentkv_prepared_summary_size(dparams(summary=3)) == 0
+    assert f(ctypes.byref(dparams(summary=3)), *ptrs, None) == SHAPE
+    assert mk.momentkv_decode_workspace_bytes(dparams(summary=3)) > 0  # a valid decode form
 
 
 def evict_status(p, budget, ptr=1 << 20, ws=1 << 40, ws_bytes=None, drop=None):
@@ -272,6 +279,10 @@ def test_decode_binding_checks_summary_form_new_rows_and_device():
     t = _decode_tensors()
     with pytest.raises(ValueError, match="prepared"):      # summary=1 wants the bf16 planes
         mk.momentkv_decode_attn(**t, summary=1)
+    with pytest.raises(ValueError, match="raw, bf16"):     # summary=3 wants a bf16 raw S
+        mk.momentkv_decode_attn(**t, summary=3)
+    with pytest.raises(ValueError, match="summary must be"):
+        mk.momentkv_decode_attn(**t, summary=4)
     with pytest.raises(ValueError, match="together"):
         mk.momentkv_decode_attn(**t, k_new=torch.zeros(2, 2, 64, dtype=torch.bfloat16))
     with pytest.raises(ValueError, match="required"):
@@ -294,6 +305,8 @@ def test_compress_and_prepare_binding_reject_wrong_tensors():
         mk.momentkv_compress(q[:, :, :, :32], k, k, 20)
     with pytest.raises(ValueError, match="on the GPU"):
         mk.momentkv_compress(q, k, k, 20)
+    with pytest.raises(ValueError, match="moment_dtype"):
+        mk.momentkv_compress(q, k, k, 20, moment_dtype=torch.float16)
     t = _decode_tensors()
     with pytest.raises(ValueError, match="n_e"):
         mk.momentkv_prepare_summary(t["n_e"].long(), t["s_k"], t["s_v"], t["S"],

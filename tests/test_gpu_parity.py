@@ -81,6 +81,44 @@ def test_decode_large_query_groups(G, n_split):
     P.run_decode_steps(gpu, out, 3, n_split=n_split, summary=1)
 
 
+@pytest.mark.parametrize("n_split", [1, 3])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_bf16_moment_storage(dtype, n_split):
+    """Moments stored in 16 bits (App. C.2): compress with moment_dtype bf16 writes the
+    fp32 sum rounded once to bf16 (bit for bit torch's round-to-nearest-even cast of the
+    fp32 output of the same call, every other output unchanged; against the oracle's
+    brute-force sum over the evicted set, within the bf16 unit roundoff 2^-8 of each entry
+    plus the probabilistic fp32 summation bound 8 sqrt(n) 2^-24 sum |v_a k_b|),
+    and the decode reading that raw bf16 S (summary 3, centred in fp32) matches the oracle
+    fed the same bf16 values, through appends."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=dtype, head_dim=128, ctx_len=1500,
+                         batch=2, n_q_heads=8, n_kv_heads=2, window=16, budgets=(97,))
+    ref = P.run_compress(gpu, 97, cap=100)
+    out = P.run_compress(gpu, 97, cap=100, moment_dtype=torch.bfloat16)
+    assert out.S.dtype == torch.bfloat16
+    assert torch.equal(out.S, ref.S.to(torch.bfloat16))
+    for f in ("idx", "lens", "n_e", "s_k", "s_v"):
+        assert torch.equal(getattr(out, f), getattr(ref, f)), f
+    # rows past lens are unwritten (the outputs were allocated uninitialised)
+    assert torch.equal(out.k_out[:, :, :97], ref.k_out[:, :, :97])
+    assert torch.equal(out.v_out[:, :, :97], ref.v_out[:, :, :97])
+    for b in range(2):
+        for h in range(2):
+            n_out = int(out.lens[b, h])
+            idx = out.idx[b, h, :n_out].cpu().numpy()
+            K, V = P.h64(cpu["k"][b, h]), P.h64(cpu["v"][b, h])
+            ev = np.setdiff1d(np.arange(K.shape[0]), idx)
+            exact = O.evicted_moments(K, V, ev).S
+            got = P.h64(out.S[b, h])
+            sum_abs = np.abs(V[ev]).T @ np.abs(K[ev])
+            delta = 8.0 * math.sqrt(len(ev)) * 2.0 ** -24 * sum_abs
+            bound = 2.0 ** -8 * np.abs(exact) + (1 + 2.0 ** -8) * delta
+            assert bool(np.all(np.abs(got - exact) <= bound)), (b, h, float(np.max(np.abs(got - exact) / bound)))
+    announce(f"{dtype} n_split={n_split}: bf16 S within its rounding bound")
+    worst = P.run_decode_steps(gpu, out, 3, n_split=n_split, summary=3)
+    announce(f"decode from bf16 raw moments, worst rel err {max(worst):.2e}")
+
+
 def test_split_decode_repeats_bit_exact_and_leaves_counters_at_zero():
     """The split shape merges each head in the launch (the last slice to finish): 24
     repeated calls on the same inputs give the same bits whichever wave merged, the

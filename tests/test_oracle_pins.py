@@ -268,7 +268,7 @@ def _err_ratios(errs):
 
 def test_decode_first_order_error_is_second_order_in_key_spread():
     """||f_E - f_E_hat|| = O(eps^2) when the evicted key deviations shrink by eps
-    (App. B.1 Eq. app_error_bound): halving eps divides the error by ~4.  The
+    (App. A.2 Eq. app_error_bound): halving eps divides the error by ~4.  The
     zeroth-order variant (v_bar only) is only O(eps): ratio ~2."""
     d = 16
     errs1, errs0, errs_full = [], [], []
@@ -348,7 +348,7 @@ def test_exact_decomposition_of_full_attention():
 def test_residual_is_second_order_close_to_true_evicted_output_at_own_key():
     """r_j = v_j - f_E_hat(q = k_j): the residual's prediction term is the first-order
     estimate of the evicted attention output evaluated at token j's own key, so
-    r_j - (v_j - f_E(k_j)) is O(eps^2) in the evicted key spread (Sec. 4.2, App. B.1)."""
+    r_j - (v_j - f_E(k_j)) is O(eps^2) in the evicted key spread (Sec. 4.2, App. A.2)."""
     d = 8
     errs = []
     for eps in [0.2, 0.1, 0.05, 0.025]:
