@@ -897,25 +897,25 @@ __global__ void __launch_bounds__(TKT) k_tk_write(const float* __restrict__ scor
   const int m = s_start[ntk];
   const bool in_lds = m <= TK_CAND_LDS;
   if (in_lds) {
-    for (int f0 = 0; f0 < m; f0 += TKT * 8) {
-      uint32_t v[8];
-      int vs[8];
+    // the slice of every flat index first (each slice's range filled in LDS), then all
+    // loads of the thread, from clamped addresses, then the keys' stores
+    for (int s2 = 0; s2 < ntk; ++s2)
+      for (int f = s_start[s2] + tid; f < s_start[s2 + 1]; f += TKT) c_sl[f] = (uint16_t)s2;
+    __syncthreads();
+    constexpr int GU = TK_CAND_LDS / TKT;
+    uint32_t v[GU];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int f = f0 + u * TKT + tid;
-        int lo = 0, hi = ntk;  // s_start[lo] <= f < s_start[hi]
-        while (hi - lo > 1) {
-          const int mid = (lo + hi) >> 1;
-          if (s_start[mid] <= f) lo = mid; else hi = mid;
-        }
-        vs[u] = lo;
-        v[u] = f < m ? cand[((size_t)head * ntk + lo) * TKS + (f - s_start[lo])] : 0u;
+    for (int u = 0; u < GU; ++u) {
+      if (u * TKT < m) {  // uniform
+        const int f = min(u * TKT + tid, m - 1);
+        const int s2 = c_sl[f];
+        v[u] = cand[((size_t)head * ntk + s2) * TKS + (f - s_start[s2])];
       }
+    }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int f = f0 + u * TKT + tid;
-        if (f < m) { c_key[f] = v[u]; c_sl[f] = (uint16_t)vs[u]; }
-      }
+    for (int u = 0; u < GU; ++u) {
+      const int f = u * TKT + tid;
+      if (f < m) c_key[f] = v[u];
     }
   }
   __syncthreads();
