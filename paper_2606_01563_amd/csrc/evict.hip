@@ -443,21 +443,34 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
     vl = vc[(size_t)last * D + tid];
   }
   float x[UB][GM], y[UB];
-  // records of rows base + tid + NT u (every load issued, from a valid row; rows past
-  // n_tok and padded query slots then read as -inf, their norm as +inf)
+  // records of rows base + 4 (tid + NT v) + w (record u = 4 v + w): one 16-byte read per
+  // plane and four rows, every read issued and inside the record planes (rec_len is a
+  // multiple of 32); rows past n_tok and padded query slots then read as -inf, their
+  // norm as +inf.  The masks come after a scheduling barrier, so that all of the reads
+  // are out before the first is waited for.
   auto load_batch = [&](int base) {
+    float4 r4[UB / 4][GM + 1];
 #pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int j = base + tid + NT * u;
-      const bool ok = j < n_tok;
-      const int jc = min(j, max(n_tok - 1, 0));
+    for (int v = 0; v < UB / 4; ++v) {
+      const int jc = min(base + 4 * (tid + NT * v), ML - 4);  // past the planes: rows past n_tok
 #pragma unroll
-      for (int g = 0; g < GM; ++g) {
-        const float v = rec[(size_t)min(g, G - 1) * ML + jc];
-        x[u][g] = (ok && g < G) ? v : -INFINITY;
+      for (int g = 0; g <= GM; ++g)
+        r4[v][g] = *reinterpret_cast<const float4*>(rec + (size_t)(g < GM ? min(g, G - 1) : G) * ML + jc);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int v = 0; v < UB / 4; ++v) {
+      const int j0 = base + 4 * (tid + NT * v);
+#pragma unroll
+      for (int g = 0; g <= GM; ++g) {
+        const float rv[4] = {r4[v][g].x, r4[v][g].y, r4[v][g].z, r4[v][g].w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const bool ok = j0 + w < n_tok;
+          if (g < GM) x[4 * v + w][g] = (ok && g < G) ? rv[w] : -INFINITY;
+          else y[4 * v + w] = ok ? rv[w] : INFINITY;
+        }
       }
-      const float v = rec[(size_t)G * ML + jc];
-      y[u] = ok ? v : INFINITY;
     }
   };
   if (evicts) load_batch(0);
@@ -465,50 +478,69 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
   if (tid == 0) sl.redo = 0;
 
   int js = -1;
+  bool s_req = false;  // S requested
   if (evicts) {
     if (tid == 0 && old_len > e.budget) atomicOr(e.flag, 8);  // one eviction cannot reach budget
     const int step = UB * NT;
     const int nb = (n_tok + step - 1) / step;
 
-    // log2 Z_g over the n_tok rows: per batch the thread's max, then its sum (records past
-    // n_tok and padded query slots hold -inf and add nothing; no per-record branch)
-    float m[GM], l[GM];
+    if constexpr (ATTN) {
+      // log2 Z_g from the merged attention state: it holds the same n_tok base-2 logits
 #pragma unroll
-    for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
-    for (int b = 0; b < nb; ++b) {
-      if (b > 0) load_batch(b * step);
+      for (int k = 0; k < KQ; ++k) {
+        const int g = wave + NW * k;
+        if (g < G && lane == 0) sl.lz[g] = qs.M[k] + log2f(qs.l[k]);
+      }
+      __syncthreads();
+    } else {
+      // log2 Z_g over the n_tok rows: per batch the thread's max, then its sum (records past
+      // n_tok and padded query slots hold -inf and add nothing; no per-record branch)
+      float m[GM], l[GM];
+#pragma unroll
+      for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
+      for (int b = 0; b < nb; ++b) {
+        if (b > 0) load_batch(b * step);
+#pragma unroll
+        for (int g = 0; g < GM; ++g) {
+          float mn = m[g];
+#pragma unroll
+          for (int u = 0; u < UB; ++u) mn = fmaxf(mn, x[u][g]);
+          const float base = mn == -INFINITY ? 0.f : mn;
+          float sum = 0.f;
+#pragma unroll
+          for (int u = 0; u < UB; ++u) sum += fast_exp2(x[u][g] - base);
+          l[g] = l[g] * fast_exp2(m[g] - base) + sum;
+          m[g] = mn;
+        }
+      }
 #pragma unroll
       for (int g = 0; g < GM; ++g) {
-        float mn = m[g];
-#pragma unroll
-        for (int u = 0; u < UB; ++u) mn = fmaxf(mn, x[u][g]);
-        const float base = mn == -INFINITY ? 0.f : mn;
-        float sum = 0.f;
-#pragma unroll
-        for (int u = 0; u < UB; ++u) sum += fast_exp2(x[u][g] - base);
-        l[g] = l[g] * fast_exp2(m[g] - base) + sum;
-        m[g] = mn;
+        if (g < G) {
+          const float M = wave_max(m[g]);
+          const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
+          if (lane == 0) { sl.m[wave][g] = M; sl.l[wave][g] = ls; }
+        }
       }
-    }
+      __syncthreads();
+      if (tid < G) {
+        float M = -INFINITY, L = 0.f;
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g < G) {
-        const float M = wave_max(m[g]);
-        const float ls = wave_sum(M == -INFINITY ? 0.f : l[g] * fast_exp2(m[g] - M));
-        if (lane == 0) { sl.m[wave][g] = M; sl.l[wave][g] = ls; }
+        for (int w = 0; w < NW; ++w) M = fmaxf(M, sl.m[w][tid]);
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+          if (sl.m[w][tid] != -INFINITY) L += sl.l[w][tid] * fast_exp2(sl.m[w][tid] - M);
+        sl.lz[tid] = M + log2f(L);
       }
+      __syncthreads();
     }
-    __syncthreads();
-    if (tid < G) {
-      float M = -INFINITY, L = 0.f;
+
+    // S does not depend on the choice: with all of it in one register chunk, it is
+    // requested here and arrives while the scores are compared
+    if (NCH == 1) {
 #pragma unroll
-      for (int w = 0; w < NW; ++w) M = fmaxf(M, sl.m[w][tid]);
-#pragma unroll
-      for (int w = 0; w < NW; ++w)
-        if (sl.m[w][tid] != -INFINITY) L += sl.l[w][tid] * fast_exp2(sl.m[w][tid] - M);
-      sl.lz[tid] = M + log2f(L);
+      for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * u];
+      s_req = true;
     }
-    __syncthreads();
 
     // argmin over rows of log2(mean_g alpha_gj) + log2 ||r_j||, lowest row on ties
     float lz[GM];
@@ -521,7 +553,7 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
       if (nb > 1) load_batch(b * step);  // one batch: still in registers
 #pragma unroll
       for (int u = 0; u < UB; ++u) {
-        const int j = b * step + tid + NT * u;
+        const int j = b * step + 4 * (tid + NT * (u / 4)) + (u % 4);
         float mx = -INFINITY;
 #pragma unroll
         for (int g = 0; g < GM; ++g) mx = fmaxf(mx, x[u][g] - lz[g]);  // -inf past G
@@ -557,7 +589,7 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
 
   // requests that depend on the choice: S (to be updated, or for S_tilde q), the evicted
   // row, and per query handled here its logit and its block's running max
-  if (ATTN || js >= 0 || e.order >= 1) {
+  if (!s_req && (ATTN || js >= 0 || e.order >= 1)) {
 #pragma unroll
     for (int u = 0; u < SCH; ++u) s4[u] = Sh[tid + NT * u];
   }
@@ -698,45 +730,77 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
   }
   __syncthreads();
 
-  // S_tilde q = (S - s_v s_k^T / n_e) q with entries below tau set to zero: TPR threads
-  // per row of S, each over the chunks p, p + TPR, ... of 4 columns, then a sum over the
-  // row's threads (neighbouring lanes)
+  // S_tilde q = (S - s_v s_k^T / n_e) q with entries below tau set to zero.  Thread
+  // (r, p) takes rows r, r + NT / TPR, ... and the column chunks 4 (p + TPR c); its chunks'
+  // s_k / n_e and query entries stay in registers over its rows (queries GB at a time),
+  // and the TPR neighbouring lanes of a row add their sums.
   const bool use_sq = e.order >= 1 && ne2 > 0;
   if (use_sq) {
-    constexpr int TPR = NT / D;
-    static_assert(TPR >= 1 && TPR <= 8 && D % (4 * TPR) == 0, "threads per row of S");
+    constexpr int TPR = 8, RPP = NT / TPR, RPT = D / RPP, CPT = D / (4 * TPR);
+    constexpr int GB = GM < 4 ? GM : 4;
+    static_assert(NT % TPR == 0 && D % RPP == 0 && CPT >= 1 && GM % GB == 0, "S_tilde q layout");
     const float inv_n = 1.f / (float)ne2;
-    const int row = tid / TPR, part = tid % TPR;
-    const float sr = sl.sv[row];
-    float acc[GM];
+    const int r0 = tid / TPR, part = tid % TPR;
+    float skn[CPT][4];
 #pragma unroll
-    for (int g = 0; g < GM; ++g) acc[g] = 0.f;
-#pragma unroll
-    for (int k = 0; k < D / (4 * TPR); ++k) {
-      const int c4 = 4 * (TPR * k + part);
-      const float4 sv4 = *reinterpret_cast<const float4*>(&s_S[s_at<D>(row, c4)]);
-      const float4 sk4 = *reinterpret_cast<const float4*>(&sl.sk[c4]);
-      float st[4] = {sv4.x - sr * (sk4.x * inv_n), sv4.y - sr * (sk4.y * inv_n),
-                     sv4.z - sr * (sk4.z * inv_n), sv4.w - sr * (sk4.w * inv_n)};
-#pragma unroll
-      for (int x = 0; x < 4; ++x) st[x] = fabsf(st[x]) < e.tau ? 0.f : st[x];
-#pragma unroll
-      for (int g = 0; g < GM; ++g) {
-        if (g < G) {
-          const T* qg = s_q + g * QRS + c4;
-          acc[g] += st[0] * to_f<T>(qg[0]) + st[1] * to_f<T>(qg[1]) + st[2] * to_f<T>(qg[2]) +
-                    st[3] * to_f<T>(qg[3]);
-        }
-      }
+    for (int c = 0; c < CPT; ++c) {
+      const float4 sk4 = *reinterpret_cast<const float4*>(&sl.sk[4 * (part + TPR * c)]);
+      skn[c][0] = sk4.x * inv_n;
+      skn[c][1] = sk4.y * inv_n;
+      skn[c][2] = sk4.z * inv_n;
+      skn[c][3] = sk4.w * inv_n;
     }
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g < G) {
-        float a = acc[g];
-        if constexpr (TPR >= 2) a += dpp_f<0xB1>(a);  // quad_perm [1,0,3,2]
-        if constexpr (TPR >= 4) a += dpp_f<0x4E>(a);  // quad_perm [2,3,0,1]
-        if constexpr (TPR >= 8) a += __shfl_xor(a, 4);
-        if (part == 0) sl.sq[g * D + row] = a;
+    for (int g0 = 0; g0 < GM; g0 += GB) {
+      if (g0 < G) {
+        float qv[GB][CPT][4];
+#pragma unroll
+        for (int gi = 0; gi < GB; ++gi)
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) {
+            const T* qg = s_q + min(g0 + gi, G - 1) * QRS + 4 * (part + TPR * c);
+            float f[4];
+            if constexpr (sizeof(T) == 2) {  // four bf16 in one 8-byte read
+              const uint2 w = *reinterpret_cast<const uint2*>(qg);
+              f[0] = __uint_as_float(w.x << 16);
+              f[1] = __uint_as_float(w.x & 0xffff0000u);
+              f[2] = __uint_as_float(w.y << 16);
+              f[3] = __uint_as_float(w.y & 0xffff0000u);
+            } else {
+              const float4 w = *reinterpret_cast<const float4*>(qg);
+              f[0] = w.x; f[1] = w.y; f[2] = w.z; f[3] = w.w;
+            }
+#pragma unroll
+            for (int x = 0; x < 4; ++x) qv[gi][c][x] = g0 + gi < G ? f[x] : 0.f;
+          }
+#pragma unroll
+        for (int k = 0; k < RPT; ++k) {
+          const int row = r0 + RPP * k;
+          const float sr = sl.sv[row];
+          float acc[GB];
+#pragma unroll
+          for (int gi = 0; gi < GB; ++gi) acc[gi] = 0.f;
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) {
+            const float4 s4v = *reinterpret_cast<const float4*>(&s_S[s_at<D>(row, 4 * (part + TPR * c))]);
+            float st[4] = {s4v.x - sr * skn[c][0], s4v.y - sr * skn[c][1], s4v.z - sr * skn[c][2],
+                           s4v.w - sr * skn[c][3]};
+#pragma unroll
+            for (int x = 0; x < 4; ++x) st[x] = fabsf(st[x]) < e.tau ? 0.f : st[x];
+#pragma unroll
+            for (int gi = 0; gi < GB; ++gi)
+#pragma unroll
+              for (int x = 0; x < 4; ++x) acc[gi] = fmaf(st[x], qv[gi][c][x], acc[gi]);
+          }
+#pragma unroll
+          for (int gi = 0; gi < GB; ++gi) {
+            float a = acc[gi];
+            a += dpp_f<0xB1>(a);   // quad_perm [1,0,3,2]
+            a += dpp_f<0x4E>(a);   // quad_perm [2,3,0,1]
+            a += dpp_f<0x141>(a);  // row_half_mirror: the other quad of the eight lanes
+            if (part == 0 && g0 + gi < G) sl.sq[(g0 + gi) * D + row] = a;
+          }
+        }
       }
     }
   }
