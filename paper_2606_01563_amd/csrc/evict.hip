@@ -62,6 +62,15 @@ __device__ __forceinline__ void wave_lds_order() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// The thread's index as a value the compiler cannot move: per-thread offsets derived from
+// it are formed where a segment needs them instead of being hoisted out of the loop over
+// segments (where, kept live across the block loop, they would be spilled).
+__device__ __forceinline__ int tid_here() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 // x * y rounded on its own, never fused into a following add: the scaled logits are
 // stored and used again later, and must be the same bits in both places.
 __device__ __forceinline__ float mul_nofuse(float x, float y) {
@@ -101,16 +110,16 @@ __device__ __forceinline__ f32x8 lds_frag(const float* p) {
   return r;
 }
 
-// S_tilde of one head into LDS; every thread handles D*D/8/NT chunks of 8 entries of a
-// row (all loads issued before any is used).
+// S_tilde of one head into LDS (ne = n_e of the head, as loaded by the caller); every
+// thread handles D*D/8/NT chunks of 8 entries of a row.  All of the loads are issued
+// before anything that depends on ne (a scheduling barrier), so that they are not held
+// back behind the caller's loads in flight.
 template <class T, int D, int NT>
-__device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumLds<T, D>& sm) {
+__device__ __forceinline__ void build_summary(const EvictArgs& e, int head, int ne, SumLds<T, D>& sm) {
   constexpr int PER = D * D / 8 / NT;
   static_assert(PER >= 1 && (D * D / 8) % NT == 0, "whole chunks per thread");
-  const int tid = threadIdx.x;
+  const int tid = tid_here();
   const int c0 = 8 * (tid % (D / 8));
-  const int ne = e.n_e[head];
-  const float inv_n = ne > 0 ? 1.f / (float)ne : 0.f;
   const float* Sh = e.S + (size_t)head * D * D;
   const f32x8 skc = load_frag(e.s_k + (size_t)head * D + c0);
   f32x8 raw[PER];
@@ -121,6 +130,8 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, SumL
     raw[u] = load_frag(Sh + (size_t)row * D + c0);
     sv[u] = e.s_v[(size_t)head * D + row];
   }
+  __builtin_amdgcn_sched_barrier(0);
+  const float inv_n = 1.f / (float)max(ne, 1);  // unused when ne <= 0 (S_tilde = 0)
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     const int row = (tid + NT * u) / (D / 8);
@@ -177,18 +188,20 @@ struct QueryRows {
   uint4 qv[QPT];
   __device__ __forceinline__ void load(const EvictArgs& e, int head) {
     const T* qh = reinterpret_cast<const T*>(e.q) + (size_t)head * e.G * D;
+    const int tid = tid_here();
 #pragma unroll
     for (int u = 0; u < QPT; ++u) {
-      const int p = threadIdx.x + NT * u, row = p / QPR;
+      const int p = tid + NT * u, row = p / QPR;
       qv[u] = (p < 16 * QPR && row < e.G)
                   ? *reinterpret_cast<const uint4*>(qh + (size_t)row * D + (p % QPR) * (16 / (int)sizeof(T)))
                   : make_uint4(0, 0, 0, 0);
     }
   }
   __device__ __forceinline__ void store(T* s_q) const {
+    const int tid = tid_here();
 #pragma unroll
     for (int u = 0; u < QPT; ++u) {
-      const int p = threadIdx.x + NT * u;
+      const int p = tid + NT * u;
       if (p < 16 * QPR)
         *reinterpret_cast<uint4*>(&s_q[(p / QPR) * QRS + (p % QPR) * (16 / (int)sizeof(T))]) = qv[u];
     }
@@ -911,7 +924,8 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
   constexpr int CPL = D / 64;
   // the wave index, lengths and loop bounds are the same for all lanes; held in scalar
   // registers, they make the loops below uniform control flow rather than per-lane loops
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tid = tid_here();
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q4 = lane >> 4, r16 = lane & 15;
   const int G = e.G, hb = e.hblocks;
   const int ML = e.rec_len, NB = e.rec_len / kEvTB;
@@ -927,9 +941,10 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
   const int t0 = kEvTB * s0;  // below max_len <= cap
   const int t1 = s1 == hb ? n_rows : min(kEvTB * s1, n_rows);
   // the workgroup whose blocks hold the new row appends it (the head's last block for
-  // rows past them)
+  // rows past them); nothing in this launch reads that cache row (the new token is read
+  // from k_new / v_new), so the copy waits until the segment's rows are read
   const int nb_new = min(old_len / kEvTB, hb - 1);
-  if (can_append && wave == 0 && nb_new >= s0 && nb_new < s1) append_new_row<T, D>(e, head, old_len, lane);
+  const bool appends = can_append && wave == 0 && nb_new >= s0 && nb_new < s1;
 
   if (ATTN || t0 < t1) {  // uniform
     const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
@@ -965,13 +980,13 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
     QueryRows<T, D, NT> qr;
     qr.load(e, head);
     const int ne = e.n_e[head];
-    const float svv = threadIdx.x < D ? e.s_v[(size_t)head * D + threadIdx.x] : 0.f;
-    if (evicts) build_summary<T, D, NT>(e, head, L.sm);
+    const float svv = tid < D ? e.s_v[(size_t)head * D + tid] : 0.f;
+    if (evicts) build_summary<T, D, NT>(e, head, ne, L.sm);
     qr.store(L.q);
     // r_j = v_j - cf (v_bar / cf + S_tilde k_j): the accumulators of S_tilde k_j start at
     // v_bar / cf = s_v / scale, so the mean comes out of the MFMAs
     const float cf = ne > 0 ? e.scale / (float)ne : 0.f;
-    if (threadIdx.x < D) L.vinit[threadIdx.x] = ne > 0 ? svv / e.scale : 0.f;
+    if (tid < D) L.vinit[tid] = ne > 0 ? svv / e.scale : 0.f;
     __syncthreads();  // S_tilde, v_bar and the queries are in LDS
 
     EA at;
@@ -1079,6 +1094,7 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
       }
     }
   }
+  if (appends) append_new_row<T, D>(e, head, old_len, lane);
   if constexpr (!ATTN) {
     // The workgroup holds the whole head: its records and the appended row are visible
     // to all of its waves after a barrier, and it selects, updates, then attends to the
