@@ -783,13 +783,20 @@ __device__ __forceinline__ void wave_find_bin(const uint32_t* hist, int need, ui
 }
 
 // The TKPT consecutive keys of thread tid in slice sl (positions >= n give valid = false).
+// Every read is issued, from a position clamped into the row (the score arrays hold at
+// least one entry per row), before the first is used: a read under a per-lane condition
+// would be waited for before the next one is issued.
 __device__ __forceinline__ void slice_keys(const float* s, int n, int sl, uint32_t (&key)[TKPT],
                                            bool (&valid)[TKPT]) {
   const int j0 = sl * TKS + TKPT * threadIdx.x;
+  float v[TKPT];
+#pragma unroll
+  for (int u = 0; u < TKPT; ++u) v[u] = s[max(min(j0 + u, n - 1), 0)];
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < TKPT; ++u) {
     valid[u] = j0 + u < n;
-    key[u] = valid[u] ? score_key(s[j0 + u]) : 0u;
+    key[u] = valid[u] ? score_key(v[u]) : 0u;
   }
 }
 
@@ -807,8 +814,18 @@ __global__ void __launch_bounds__(TKT) k_tk_cand(const float* __restrict__ score
   uint32_t key[TKPT];
   bool valid[TKPT];
   slice_keys(scores + (size_t)head * n, n, sl, key, valid);
-  // the head's histogram (every slice workgroup finds the same bin of the k-th key)
-  for (int b = threadIdx.x; b < TK_HBINS; b += TKT) hst[b] = hh[(size_t)head * TK_HBINS + b];
+  // the head's histogram (every slice workgroup finds the same bin of the k-th key): each
+  // thread's bins in 16-byte reads, all issued before the first LDS store
+  {
+    static_assert(TK_HBINS % (4 * TKT) == 0, "whole 16-byte pieces per thread");
+    constexpr int HPT = TK_HBINS / 4 / TKT;
+    const uint4* src = reinterpret_cast<const uint4*>(hh + (size_t)head * TK_HBINS);
+    uint4 hv[HPT];
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) hv[u] = src[threadIdx.x + TKT * u];
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) reinterpret_cast<uint4*>(hst)[threadIdx.x + TKT * u] = hv[u];
+  }
   __syncthreads();
   if (threadIdx.x < 64) {
     uint32_t b, ab;

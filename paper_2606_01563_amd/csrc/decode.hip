@@ -623,11 +623,13 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   ba.t_end = hl.cache_len;
   if (BA::TB * (wave + 1) > ba.t_end) ba.clear_v_past_end(BA::TB * wave, lane);
   if (wave == 0 && lane == 0 && a.k_new != nullptr && !hl.can_append) atomicOr(a.flag, 1);
-  if (wave == 3 && hl.can_append) append_row<T, D>(a, head, hl.old_len, lane);
   if (sq_rows) sq.compute(a, qf, 32 * wave, lane, s_sq);
   ba.run(qf, BA::TB * wave, 4 * BA::TB, a.scale * kLog2e, G, lane, vt, s_p[wave]);
   wave_lds_order();  // the last block's reads of the V^T tile come before it is reused
   ba.store_lds(reinterpret_cast<float*>(s_vt[wave]), s_ml[wave], G, lane);
+  // the copy of the new token into the cache: nothing here reads that row (the token is
+  // attended to from k_new / v_new), so it waits until the wave's own rows are used
+  if (wave == 3 && hl.can_append) append_row<T, D>(a, head, hl.old_len, lane);
   __syncthreads();
 
   // one wave per query: merge the four waves' states, then the new token and correction
@@ -861,12 +863,14 @@ k_decode_slice(DecodeArgs a) {
   const int head = is_sq ? idx / nsq : idx / a.nsplit;   // b * Hkv + h
   const int G = a.G;
   const T* qh = reinterpret_cast<const T*>(a.q) + (size_t)head * G * D;
+  // the query fragments are requested after the wave's other reads: zeroing the rows past
+  // G right after the reads would otherwise hold those back until the queries arrive
   typename BA::FragT qf[KS];
-  load_query_frags<T, D>(qh, G, lane, qf);
   if (is_sq) {
     const int r0 = 32 * (idx % nsq);
     SqRows<T, D, PREP> sq;
     sq.load(a, head, r0, lane);
+    load_query_frags<T, D>(qh, G, lane, qf);
     sq.template compute<true>(a, qf, r0, lane, a.sq + (size_t)head * G * D);
   } else {
     const int split = idx % a.nsplit;
@@ -878,6 +882,7 @@ k_decode_slice(DecodeArgs a) {
     ba.t_end = max(t0, min(t0 + a.split_len, hl.cache_len));
     ba.init();
     ba.load(t0, lane);  // rows clamped into the cache for an empty slice; never used
+    load_query_frags<T, D>(qh, G, lane, qf);
     if (a.k_new != nullptr && !hl.can_append && split == 0 && lane == 0) atomicOr(a.flag, 1);
     // the slice whose range holds row old_len (the last slice for rows past the split)
     if (hl.can_append && min(hl.old_len / a.split_len, a.nsplit - 1) == split)
