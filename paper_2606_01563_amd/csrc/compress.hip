@@ -82,14 +82,6 @@ __device__ __forceinline__ void hist_flush(const uint32_t* lh, uint32_t* gh) {
     if (lh[b]) atomicAdd(&gh[b], lh[b]);
 }
 
-__device__ __forceinline__ void store_frag(bf16_t* p, const bf16x8& f) {
-  *reinterpret_cast<uint4*>(p) = __builtin_bit_cast(uint4, f);
-}
-__device__ __forceinline__ void store_frag(float* p, const f32x8& f) {
-  reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
-  reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
-}
-
 __device__ __forceinline__ void load4(const bf16_t* p, float (&o)[4]) {
   uint2 u = *reinterpret_cast<const uint2*>(p);
   o[0] = bf2f((bf16_t)(u.x & 0xffffu));
@@ -169,6 +161,28 @@ __device__ __forceinline__ void cov_tile(const T (*sVT)[LD], const T (*sKT)[LD],
     for (int ni = 0; ni < QN; ++ni) {
       const int r = b0 + 16 * ni + (lane & 15);
       typename Frag<T>::type bf = load_frag(&sKT[r][tcol<T>(r, col)]);
+#pragma unroll
+      for (int mi = 0; mi < QM; ++mi) mma(cacc[mi][ni], af[mi], bf);
+    }
+  }
+}
+
+// The same from the tiles as they are (bf16, [token][dim], row stride ld): both operands
+// read transposed out of LDS, so nothing is written transposed.
+template <int D, int NW>
+__device__ __forceinline__ void cov_tile_tr(const bf16_t* sV, const bf16_t* sK, int ld,
+                                            f32x4 (&cacc)[CovSplit<D, NW>::QM][CovSplit<D, NW>::QN],
+                                            int wave, int lane) {
+  constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
+  const int a0 = CovSplit<D, NW>::a0(wave), b0 = CovSplit<D, NW>::b0(wave);
+#pragma unroll
+  for (int kk = 0; kk < TILE / 32; ++kk) {
+    bf16x8 af[QM];
+#pragma unroll
+    for (int mi = 0; mi < QM; ++mi) af[mi] = lds_frag_tr(sV, ld, 32 * kk, a0 + 16 * mi, lane);
+#pragma unroll
+    for (int ni = 0; ni < QN; ++ni) {
+      const bf16x8 bf = lds_frag_tr(sK, ld, 32 * kk, b0 + 16 * ni, lane);
 #pragma unroll
       for (int mi = 0; mi < QM; ++mi) mma(cacc[mi][ni], af[mi], bf);
     }
@@ -301,6 +315,46 @@ __device__ __forceinline__ void tile_store_t(const TileRegs<T, D, NT>& R, T (*sK
   }
 }
 
+// bf16 tiles kept as they are: V rows into sV ([token][dim], row stride LDV) with the rows
+// of tokens outside the summed set zeroed (K rows are stored by the caller as they are;
+// zero V rows take those tokens out of V^T K), and the same sums and squares as above.
+template <int D, int NT, int LDV, class In>
+__device__ __forceinline__ void tile_sums_nat(const TileRegs<bf16_t, D, NT>& R, bf16_t (*sV)[LDV],
+                                              int tok0, In in, float (&sk)[8], float (&sv)[8],
+                                              float (&ss)[TileRegs<bf16_t, D, NT>::NP][2], int tid) {
+  typedef TileRegs<bf16_t, D, NT> TR;
+  constexpr uint32_t ONES = 0x3F803F80u;  // (1.0, 1.0) in bf16
+  const bool act = TR::active(tid);
+#pragma unroll
+  for (int i = 0; i < TR::NP; ++i) {
+    const int p = TR::pair(tid, i);
+    const bool c0 = act && in(tok0 + 2 * p), c1 = act && in(tok0 + 2 * p + 1);
+    ss[i][0] = ss[i][1] = 0.f;
+    const u32x4 k0 = __builtin_bit_cast(u32x4, R.k[i][0]), k1 = __builtin_bit_cast(u32x4, R.k[i][1]);
+    const u32x4 v0 = __builtin_bit_cast(u32x4, R.v[i][0]), v1 = __builtin_bit_cast(u32x4, R.v[i][1]);
+    u32x4 m0, m1;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t a0 = c0 ? k0[w] : 0u, a1 = c1 ? k1[w] : 0u;
+      const uint32_t b0 = c0 ? v0[w] : 0u, b1 = c1 ? v1[w] : 0u;
+      m0[w] = b0;
+      m1[w] = b1;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t sel = h ? 0x07060302u : 0x05040100u;  // (token 0, token 1) of column 2w+h
+        sk[2 * w + h] = dot2_bf16(__builtin_amdgcn_perm(a1, a0, sel), ONES, sk[2 * w + h]);
+        sv[2 * w + h] = dot2_bf16(__builtin_amdgcn_perm(b1, b0, sel), ONES, sv[2 * w + h]);
+      }
+      ss[i][0] = dot2_bf16(b0, b0, ss[i][0]);
+      ss[i][1] = dot2_bf16(b1, b1, ss[i][1]);
+    }
+    if (act) {
+      *reinterpret_cast<u32x4*>(&sV[2 * p][8 * TR::group(tid)]) = m0;
+      *reinterpret_cast<u32x4*>(&sV[2 * p + 1][8 * TR::group(tid)]) = m1;
+    }
+  }
+}
+
 // Write one slot of covariance and (s_v, s_k) partials; `sign` = -1 for downdates.  The
 // column sums of the threads sharing a column group are added within each wave (lanes
 // g, g + 16, ... for D = 128) and then over the waves in order through `red`
@@ -353,13 +407,15 @@ constexpr int RC_THREADS = 512;  // k_rows_cov workgroup: 8 waves
 template <class T, int D, int MTW>
 __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
   constexpr int NT = RC_THREADS, NW = NT / 64;
+  constexpr bool BF = sizeof(T) == 2;  // bf16: K and V tiles as they are (transposed reads)
   constexpr int KS = D / 32, PAD = 16 / (int)sizeof(T);
-  constexpr int LDK = D + PAD, LDT = TILE + PAD;
+  constexpr int LDK = BF ? D + 16 : D + PAD, LDT = TILE + PAD;  // bf16 rows padded by 32 bytes
   constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
   typedef TileRegs<T, D, NT> TR;
   __shared__ __align__(16) T sK[TILE][LDK];
-  __shared__ __align__(16) T sKT[D][LDT];
-  __shared__ __align__(16) T sVT[D][LDT];
+  __shared__ __align__(16) T sV[BF ? TILE : 1][LDK];     // bf16: V rows, candidates only
+  __shared__ __align__(16) T sKT[BF ? 1 : D][LDT];       // fp32: K^T, V^T
+  __shared__ __align__(16) T sVT[BF ? 1 : D][LDT];
   __shared__ float sVnorm[kRowsMaxTiles * TILE];  // ||v_j|| of the slice, written at the end
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -426,7 +482,10 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         }
       }
       float ss[TR::NP][2];
-      tile_store_t<T, D, NT, LDT>(R, sKT, sVT, tok0, is_cand, sk, sv, ss, tid);
+      if constexpr (BF)
+        tile_sums_nat<D, NT, LDK>(R, sV, tok0, is_cand, sk, sv, ss, tid);
+      else
+        tile_store_t<T, D, NT, LDT>(R, sKT, sVT, tok0, is_cand, sk, sv, ss, tid);
       // ||v_j||: the GROUPS lanes holding token j's columns are adjacent.  No global
       // store inside the tile loop: a store among the loads in flight would make the
       // compiler wait for all of them; the norms wait in LDS.
@@ -491,7 +550,12 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         }
       }
     }
-    if (tile_has_cand) cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
+    if (tile_has_cand) {
+      if constexpr (BF)
+        cov_tile_tr<D, NW>(&sV[0][0], &sK[0][0], LDK, cacc, wave, lane);
+      else
+        cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
+    }
     __syncthreads();
   };
   TR R0, R1;
@@ -527,7 +591,9 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         rp[1] = l;
       }
     }
-  write_cov_partials<T, D, NT>(a, head, sl, cacc, sv, sk, 1.f, reinterpret_cast<float*>(&sVT[0][0]), tid);
+  static_assert(sizeof(sV) + sizeof(sVT) >= NW * 2 * D * sizeof(float), "LDS for the column sums");
+  write_cov_partials<T, D, NT>(a, head, sl, cacc, sv, sk, 1.f,
+                               BF ? reinterpret_cast<float*>(&sV[0][0]) : reinterpret_cast<float*>(&sVT[0][0]), tid);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1068,12 +1134,13 @@ template <class T, int D>
 __device__ void slice_cov(const CompressArgs& a, int head, int sl, const int32_t* list,
                           int nrows, float sign) {
   constexpr int NT = 256, NW = 4;
+  constexpr bool BF = sizeof(T) == 2;  // bf16: K and V tiles as they are (transposed reads)
   constexpr int PAD = 16 / (int)sizeof(T);
-  constexpr int LDT = TILE + PAD;
+  constexpr int LDT = TILE + PAD, LDN = D + 16;
   constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
   typedef TileRegs<T, D, NT> TR;
-  __shared__ __align__(16) T sKT[D][LDT];
-  __shared__ __align__(16) T sVT[D][LDT];
+  __shared__ __align__(16) T sKT[BF ? TILE : D][BF ? LDN : LDT];  // bf16: K rows; fp32: K^T
+  __shared__ __align__(16) T sVT[BF ? TILE : D][BF ? LDN : LDT];  // bf16: V rows; fp32: V^T
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const T* Kh = reinterpret_cast<const T*>(a.k) + (size_t)head * a.N * D;
   const T* Vh = reinterpret_cast<const T*>(a.v) + (size_t)head * a.N * D;
@@ -1092,10 +1159,25 @@ __device__ void slice_cov(const CompressArgs& a, int head, int sl, const int32_t
   for (int t = 0; t < ntiles; ++t) {
     float ss[TR::NP][2];
     R.arrive();
-    tile_store_t<T, D, NT, LDT>(R, sKT, sVT, t * TILE, in_rows, sk, sv, ss, tid);
+    if constexpr (BF) {
+      if (TR::active(tid)) {
+#pragma unroll
+        for (int i = 0; i < TR::NP; ++i) {
+          const int p = TR::pair(tid, i);
+          store_frag(&sKT[2 * p][8 * TR::group(tid)], R.k[i][0]);
+          store_frag(&sKT[2 * p + 1][8 * TR::group(tid)], R.k[i][1]);
+        }
+      }
+      tile_sums_nat<D, NT, LDN>(R, sVT, t * TILE, in_rows, sk, sv, ss, tid);
+    } else {
+      tile_store_t<T, D, NT, LDT>(R, sKT, sVT, t * TILE, in_rows, sk, sv, ss, tid);
+    }
     if (t + 1 < ntiles) tile_load_list<T, D, NT>(R, Kh, Vh, list, (t + 1) * TILE, nrows, a.N, tid);
     __syncthreads();
-    cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
+    if constexpr (BF)
+      cov_tile_tr<D, NW>(&sVT[0][0], &sKT[0][0], LDN, cacc, wave, lane);
+    else
+      cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     __syncthreads();
   }
   write_cov_partials<T, D, NT>(a, head, a.nsl1 + sl, cacc, sv, sk, sign,

@@ -323,8 +323,12 @@ struct BlockAttn {
   static constexpr int NVC = D / 32;       // V chunks (16 or 32 bytes) per lane and token
   static constexpr int NT = D / 16;        // 16-column output tiles of P.V
   static constexpr int PT = 16 / (int)sizeof(T);  // LDS row padding (16 bytes)
+  static constexpr bool TR = sizeof(T) == 2;       // bf16: V kept in its own layout
+  static constexpr int LDV = D + 16;               // bf16 V rows padded by 32 bytes
   typedef typename Frag<T>::type FragT;
-  typedef T VtTile[D][TB + PT];
+  // bf16: the block's V rows as they are, read back transposed as MFMA operands; fp32:
+  // V^T, written transposed
+  typedef typename Pick<TR, T[TB][LDV], T[D][TB + PT]>::type VtTile;
   typedef T PTile[16][TB + PT];
 
   const T* kc;
@@ -386,21 +390,15 @@ struct BlockAttn {
         for (int ks = 0; ks < KS; ++ks) mma(acc[hh], qf[ks], kf[hh][ks]);
       }
       wave_lds_order();  // the previous block's reads of vt / sp come first
-      // ---- V^T into LDS (columns 2p, 2p+1 of row dim)
+      // ---- V into LDS: bf16 rows as they are (tokens 2p, 2p+1); fp32 transposed
       {
         const int p2 = 2 * (lane & 15);
 #pragma unroll
         for (int c = 0; c < NVC; ++c) {
           const int col0 = 8 * ((lane >> 4) + 4 * c);
-          if constexpr (sizeof(T) == 2) {
-            const u32x4_t w0 = __builtin_bit_cast(u32x4_t, vf[0][c]);
-            const u32x4_t w1 = __builtin_bit_cast(u32x4_t, vf[1][c]);
+          if constexpr (TR) {
 #pragma unroll
-            for (int w = 0; w < 4; ++w)
-#pragma unroll
-              for (int hh = 0; hh < 2; ++hh)
-                *reinterpret_cast<uint32_t*>(&vt[col0 + 2 * w + hh][p2]) =
-                    __builtin_amdgcn_perm(w1[w], w0[w], hh ? 0x07060302u : 0x05040100u);
+            for (int hh = 0; hh < 2; ++hh) store_frag(&vt[p2 + hh][col0], vf[hh][c]);
           } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e)
@@ -447,7 +445,10 @@ struct BlockAttn {
 #pragma unroll
           for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
         }
-        mma(oacc[nt], pfr, load_frag(&vt[16 * nt + (lane & 15)][8 * (lane >> 4)]));
+        if constexpr (TR)
+          mma(oacc[nt], pfr, lds_frag_tr(&vt[0][0], LDV, 0, 16 * nt, lane));
+        else
+          mma(oacc[nt], pfr, load_frag(&vt[16 * nt + (lane & 15)][8 * (lane >> 4)]));
       }
     }
   }

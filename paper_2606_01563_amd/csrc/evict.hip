@@ -217,8 +217,12 @@ struct EvAttn {
   static constexpr int NOT = D / 16;              // 16-column output tiles of P.V
   static constexpr int PT = 16 / (int)sizeof(T);  // LDS row padding (16 bytes)
   static constexpr int QRS = D + 16 / (int)sizeof(T);
+  static constexpr bool TR = sizeof(T) == 2;       // bf16: V kept in its own layout
+  static constexpr int LDV = D + 16;               // bf16 V rows padded by 32 bytes
   typedef typename Frag<T>::type FragT;
-  typedef T VtTile[D][kEvTB + PT];
+  // bf16: the block's V rows as they are, read back transposed as MFMA operands; fp32:
+  // V^T, written transposed
+  typedef typename Pick<TR, T[kEvTB][LDV], T[D][kEvTB + PT]>::type VtTile;
   typedef T PTile[GM][kEvTB + PT];
   static_assert(sizeof(VtTile) >= GM * D * sizeof(float), "o rows fit in the V^T tile");
 
@@ -252,19 +256,14 @@ struct EvAttn {
                                         int t_end, int G, int lane, VtTile& vt, PTile& sp) {
     const int r16 = lane & 15, q4 = lane >> 4, p2 = 2 * r16;
     wave_lds_order();  // the previous block's reads of vt / sp come first
-    // V^T into LDS: one 32-bit word per dim holds the lane's two rows
+    // V into LDS: bf16 rows as they are (the lane's rows p2, p2 + 1); fp32 transposed, one
+    // 64-bit word per dim holding the lane's two rows
 #pragma unroll
     for (int c = 0; c < KS; ++c) {
       const int col0 = 32 * c + 8 * q4;
-      if constexpr (sizeof(T) == 2) {
-        const u32x4_t w0 = __builtin_bit_cast(u32x4_t, vf[0][c]);
-        const u32x4_t w1 = __builtin_bit_cast(u32x4_t, vf[1][c]);
+      if constexpr (TR) {
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh)
-            *reinterpret_cast<uint32_t*>(&vt[col0 + 2 * w + hh][p2]) =
-                __builtin_amdgcn_perm(w1[w], w0[w], hh ? 0x07060302u : 0x05040100u);
+        for (int hh = 0; hh < 2; ++hh) store_frag(&vt[p2 + hh][col0], vf[hh][c]);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -314,7 +313,10 @@ struct EvAttn {
 #pragma unroll
         for (int i = 0; i < 4; ++i) oacc[nt][i] *= alpha[i];
       }
-      mma(oacc[nt], pfr, load_frag(&vt[16 * nt + r16][8 * q4]));
+      if constexpr (TR)
+        mma(oacc[nt], pfr, lds_frag_tr(&vt[0][0], LDV, 0, 16 * nt, lane));
+      else
+        mma(oacc[nt], pfr, load_frag(&vt[16 * nt + r16][8 * q4]));
     }
   }
 

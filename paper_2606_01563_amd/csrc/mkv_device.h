@@ -58,6 +58,19 @@ __device__ __forceinline__ f32x8 load_frag(const float* p) {
   return r;
 }
 
+// The converse of load_frag.
+__device__ __forceinline__ void store_frag(bf16_t* p, const bf16x8& f) {
+  *reinterpret_cast<uint4*>(p) = __builtin_bit_cast(uint4, f);
+}
+__device__ __forceinline__ void store_frag(float* p, const f32x8& f) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+// Compile-time choice between two types.
+template <bool C, class A, class B> struct Pick { typedef A type; };
+template <class A, class B> struct Pick<false, A, B> { typedef B type; };
+
 template <class T> __device__ __forceinline__ typename Frag<T>::type zero_frag();
 template <> __device__ __forceinline__ bf16x8 zero_frag<bf16_t>() {
   return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
@@ -91,6 +104,22 @@ __device__ __forceinline__ void mma(f32x4& c, const bf16x8& a, const bf16x8& b) 
 __device__ __forceinline__ void mma(f32x4& c, const f32x8& a, const f32x8& b) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
+}
+
+// An MFMA operand fragment read transposed from a row-major bf16 tile in LDS whose rows
+// run along the contraction: lane l receives tile[r0 + 8 (l / 16) + e][c0 + l % 16],
+// e = 0..7 (the B layout above with the tile's columns as n; the A layout with them as
+// m).  ds_read_b64_tr_b16 hands each group of 16 lanes a 4 x 16 block whose row m is read
+// by lanes 4m .. 4m + 3 (eight bytes each) and gives lane j the block's column j; two
+// such reads cover the eight rows.  ld (elements) and c0 keep every read 8-byte aligned.
+__device__ __forceinline__ bf16x8 lds_frag_tr(const bf16_t* tile, int ld, int r0, int c0, int lane) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const int i = lane & 15;
+  const bf16_t* p = tile + (r0 + 8 * (lane >> 4) + (i >> 2)) * ld + c0 + 4 * (i & 3);
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * ld));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 __device__ __forceinline__ f32x4 zero4() {
