@@ -4,8 +4,9 @@
 // Stages, all on the caller's stream (H = B*Hkv heads, C = [n_s, N-w) candidates):
 //   1 k_rows_cov      per (slice of 64-token tiles, head): window logits Q.K^T on MFMA,
 //                     per-row online (max, sum) over the visible keys; for candidate
-//                     tokens also the covariance V^T K on MFMA (tiles transposed through
-//                     LDS), the sums s_k, s_v and ||v_j||.                 [reads K, V]
+//                     tokens also the covariance V^T K on MFMA (bf16: both operands
+//                     read transposed out of the row-major LDS tiles; fp32: tiles
+//                     written transposed), the sums s_k, s_v and ||v_j||.  [reads K, V]
 //   2 k_row_combine   per head: merge the row partials in slice order -> (max, 1/Z);
 //                     zeroes the head's two top-k key histograms.
 //   3 k_mass          per (slice, head): logits again, softmax mass summed over the
@@ -141,7 +142,7 @@ __device__ __forceinline__ int tcol(int row, int col) {
   else return col;
 }
 
-// cacc += V_tile^T K_tile over the TILE tokens held transposed in LDS.
+// cacc += V_tile^T K_tile over the TILE tokens held transposed in LDS (fp32 tiles).
 template <class T, int D, int NW, int LD>
 __device__ __forceinline__ void cov_tile(const T (*sVT)[LD], const T (*sKT)[LD],
                                          f32x4 (&cacc)[CovSplit<D, NW>::QM][CovSplit<D, NW>::QN],
@@ -192,8 +193,8 @@ __device__ __forceinline__ void cov_tile_tr(const bf16_t* sV, const bf16_t* sK, 
 // Register staging of one 64-token tile of K and V for NT threads.  Thread t holds the
 // 8-column group g = t % (D/8) of NP token pairs (2p, 2p+1), p = t / (D/8) + PSTEP * i:
 // the lanes of a wave read whole rows (one load instruction covers 64 / (D/8) / 2 rows,
-// contiguous 16-byte pieces), and the transposed LDS copies are written as packed pairs
-// of consecutive tokens.  With more threads than pieces of a tile (NT = 512, D = 64) the
+// contiguous 16-byte pieces); the rows go to LDS as they are (bf16) or transposed, as
+// packed pairs of consecutive tokens (fp32).  With more threads than pieces of a tile (NT = 512, D = 64) the
 // surplus threads hold nothing.
 template <class T, int D, int NT> struct TileRegs {
   static constexpr int GROUPS = D / 8;
@@ -247,7 +248,8 @@ __device__ __forceinline__ void tile_load(TileRegs<T, D, NT>& R, const T* Kh, co
   }
 }
 
-// Transposed copies K^T, V^T of the tile with the rows of tokens outside the summed set
+// Transposed copies K^T, V^T of the tile (the fp32 path; a bf16 variant with the copies
+// written as they are follows) with the rows of tokens outside the summed set
 // zeroed (flag in(j) of token j), running sums of k and v over the thread's 8 columns,
 // and ||v_j||^2 of the thread's tokens over its columns (ss[i][h], token 2p_i + h).
 // bf16: the two tokens' elements are paired with one byte permute per column, and the

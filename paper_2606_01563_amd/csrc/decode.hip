@@ -308,8 +308,9 @@ __global__ void __launch_bounds__(256) k_prepare_summary(DecodeArgs a, void* pre
 //  * K rows are MFMA B fragments of Q.K^T (lane: row (lane%16) + 16h, 8 dims at
 //    8*(lane/16) + 32*ks);
 //  * V rows are loaded as token pairs (lane: rows 2p, 2p+1 with p = lane%16, 8-column
-//    groups lane/16 + 4c) and written transposed to the wave's LDS tile, each dword
-//    holding the two tokens of one column;
+//    groups lane/16 + 4c) and written to the wave's LDS tile as they are (bf16; read back
+//    as B fragments of P.V with the transposing LDS read) or transposed (fp32, each
+//    64-bit word holding the two tokens of one column);
 //  * P goes to LDS as the A operand of P.V (bf16 for bf16 caches, fp32 otherwise) and P.V
 //    runs on MFMA: out[g][dim] in the same lane layout as the logits, so the online
 //    softmax rescale needs no shuffles.
@@ -434,8 +435,8 @@ struct BlockAttn {
           sp[gbase + i][16 + (lane & 15)] = from_f<T>(pb);
         }
       }
-      wave_lds_order();  // P and V^T are in LDS before they are read back
-      // ---- O = alpha * O + P . V on MFMA (A = P rows g, B = V^T); alpha is exactly 1
+      wave_lds_order();  // P and V are in LDS before they are read back
+      // ---- O = alpha * O + P . V on MFMA (A = P rows g, B = V); alpha is exactly 1
       // where no running max grew, so the rescale is skipped when none did in the wave
       const bool rescale = __any(grew);
       const FragT pfr = ((lane & 15) < G) ? load_frag(&sp[lane & 15][8 * (lane >> 4)]) : zero_frag<T>();
@@ -588,9 +589,9 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int CPL = D / 64;
   constexpr int KS = D / 32;
-  // per-wave V^T tile; after the wave's blocks it holds the wave's o rows as floats
+  // per-wave V tile; after the wave's blocks it holds the wave's o rows as floats
   constexpr int VT_BYTES = (int)sizeof(typename BA::VtTile);
-  static_assert(VT_BYTES >= GMAX * D * 4, "o rows fit in the V^T tile");
+  static_assert(VT_BYTES >= GMAX * D * 4, "o rows fit in the V tile");
   __shared__ __align__(16) unsigned char s_vt[4][VT_BYTES];
   __shared__ __align__(16) T s_p[4][16][BA::TB + BA::PT];
   __shared__ float s_ml[4][GMAX * 2];
@@ -626,7 +627,7 @@ __global__ void __launch_bounds__(256) k_decode_fused(DecodeArgs a) {
   if (wave == 0 && lane == 0 && a.k_new != nullptr && !hl.can_append) atomicOr(a.flag, 1);
   if (sq_rows) sq.compute(a, qf, 32 * wave, lane, s_sq);
   ba.run(qf, BA::TB * wave, 4 * BA::TB, a.scale * kLog2e, G, lane, vt, s_p[wave]);
-  wave_lds_order();  // the last block's reads of the V^T tile come before it is reused
+  wave_lds_order();  // the last block's reads of the V tile come before it is reused
   ba.store_lds(reinterpret_cast<float*>(s_vt[wave]), s_ml[wave], G, lane);
   // the copy of the new token into the cache: nothing here reads that row (the token is
   // attended to from k_new / v_new), so it waits until the wave's own rows are used
@@ -848,7 +849,7 @@ k_decode_slice(DecodeArgs a) {
   typedef BlockAttn<T, D, GMAX> BA;
   constexpr int KS = D / 32;
   constexpr int VT_BYTES = (int)sizeof(typename BA::VtTile);
-  static_assert(VT_BYTES >= GMAX * D * 4, "o rows fit in the V^T tile");
+  static_assert(VT_BYTES >= GMAX * D * 4, "o rows fit in the V tile");
   __shared__ __align__(16) unsigned char s_vt[VT_BYTES];
   __shared__ __align__(16) T s_p[16][BA::TB + BA::PT];
   __shared__ float s_ml[GMAX * 2];

@@ -1,7 +1,7 @@
 // Decode step with moment-informed eviction: Algorithm 1 Phase 1 (one eviction), then the
 // corrected attention of Phase 2 over the new cache and summary, reading the cache once.
 //
-// k_evict_attn: about one NW-wave workgroup per CU (the LDS holds S_tilde and a V^T tile
+// k_evict_attn: about one NW-wave workgroup per CU (the LDS holds S_tilde and a V tile
 //   per wave), each taking an equal share of the flattened (head, 32-row block) range.
 //   For each head its share touches, the workgroup forms the summary's clamped covariance
 //   S_tilde = S - s_v s_k^T / n_e (entries below tau set to zero; zero when n_e = 0) from
@@ -17,7 +17,8 @@
 //       ordered so that each lane receives the dims of v_j it holds, so r_j and its
 //       squared norm are formed in registers;
 //     the attention over every row (which one leaves is not known yet): online softmax
-//       in the base-2 domain and P.V on MFMA through an LDS transpose of V.  The running
+//       in the base-2 domain and P.V on MFMA, V read back out of LDS with the transposing
+//       LDS read (bf16) or written transposed (fp32).  The running
 //       max after the block is recorded, so that a row's term can later be taken out
 //       exactly as it was accumulated.
 //   The waves' states are merged in LDS and written as one partial state of the head.
@@ -35,7 +36,7 @@
 // Short caches: k_evict_attn without the attention, one workgroup per head (two per CU),
 //   scores the head's rows as above, then selects and finishes as k_evict_finish does,
 //   with the attention over the new cache computed after the update (rows it has just
-//   read, mostly from L2; V^T tiles in the LDS that held S_tilde).
+//   read, mostly from L2; V tiles in the LDS that held S_tilde).
 #include <climits>
 
 #include "mkv_bf16.h"
@@ -224,7 +225,7 @@ struct EvAttn {
   // V^T, written transposed
   typedef typename Pick<TR, T[kEvTB][LDV], T[D][kEvTB + PT]>::type VtTile;
   typedef T PTile[GM][kEvTB + PT];
-  static_assert(sizeof(VtTile) >= GM * D * sizeof(float), "o rows fit in the V^T tile");
+  static_assert(sizeof(VtTile) >= GM * D * sizeof(float), "o rows fit in the V tile");
 
   float m_run[4], l_run[4];
   f32x4 oacc[NOT];
@@ -302,8 +303,8 @@ struct EvAttn {
         }
       }
     }
-    wave_lds_order();  // P and V^T are in LDS before they are read back
-    // O = alpha O + P . V (A = P rows g, B = V^T); alpha is exactly 1 where no running
+    wave_lds_order();  // P and V are in LDS before they are read back
+    // O = alpha O + P . V (A = P rows g, B = V); alpha is exactly 1 where no running
     // max grew, so the rescale is skipped when none did in the whole wave
     const bool rescale = __any(grew);
     const FragT pfr = (r16 < G) ? load_frag(&sp[min(r16, GM - 1)][8 * q4]) : zero_frag<T>();
@@ -1100,13 +1101,13 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
   if constexpr (!ATTN) {
     // The workgroup holds the whole head: its records and the appended row are visible
     // to all of its waves after a barrier, and it selects, updates, then attends to the
-    // new cache itself (rows it has just read, mostly from L2), with its V^T tiles where
+    // new cache itself (rows it has just read, mostly from L2), with its V tiles where
     // S_tilde was; no second launch.
     typedef typename EA::VtTile VtT;
     typedef typename EA::PTile PtT;
     constexpr int RW0 = (int)((sizeof(SumLds<T, D>) - NW * 2 * GM * sizeof(float)) / (sizeof(VtT) + sizeof(PtT)));
     constexpr int RW = RW0 < NW ? RW0 : NW;  // waves that attend (as many as the space holds)
-    static_assert(RW >= 1, "V^T tiles fit in place of S_tilde");
+    static_assert(RW >= 1, "V tiles fit in place of S_tilde");
     static_assert(sizeof(SumLds<T, D>) >= D * D * sizeof(float), "S fits in place of S_tilde");
     char* base = reinterpret_cast<char*>(&L.sm);
     VtT* vt = reinterpret_cast<VtT*>(base);
