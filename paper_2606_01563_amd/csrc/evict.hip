@@ -111,12 +111,13 @@ __device__ __forceinline__ f32x8 lds_frag(const float* p) {
   return r;
 }
 
-// S_tilde of one head into LDS (ne = n_e of the head, as loaded by the caller); every
-// thread handles D*D/8/NT chunks of 8 entries of a row.  All of the loads are issued
-// before anything that depends on ne (a scheduling barrier), so that they are not held
-// back behind the caller's loads in flight.
+// S_tilde of one head into LDS; every thread handles D*D/8/NT chunks of 8 entries of a
+// row.  n_e is read after the rows of S and everything that depends on it follows a
+// scheduling barrier, so that no read here waits behind the caller's reads in flight
+// (the compiler moves a uniform value read from memory to a scalar register at once).
+// Returns n_e.
 template <class T, int D, int NT>
-__device__ __forceinline__ void build_summary(const EvictArgs& e, int head, int ne, SumLds<T, D>& sm) {
+__device__ __forceinline__ int build_summary(const EvictArgs& e, int head, SumLds<T, D>& sm) {
   constexpr int PER = D * D / 8 / NT;
   static_assert(PER >= 1 && (D * D / 8) % NT == 0, "whole chunks per thread");
   const int tid = tid_here();
@@ -131,6 +132,7 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, int 
     raw[u] = load_frag(Sh + (size_t)row * D + c0);
     sv[u] = e.s_v[(size_t)head * D + row];
   }
+  const int ne = e.n_e[head];
   __builtin_amdgcn_sched_barrier(0);
   const float inv_n = 1.f / (float)max(ne, 1);  // unused when ne <= 0 (S_tilde = 0)
 #pragma unroll
@@ -155,22 +157,31 @@ __device__ __forceinline__ void build_summary(const EvictArgs& e, int head, int 
       P[1] = make_float4(st[4], st[5], st[6], st[7]);
     }
   }
+  return ne;
 }
 
 // The new token: the wave given the job copies k_new / v_new to cache row `row`, 16 bytes
-// per lane.
+// per lane; the read and the write may also be issued apart (append_read, append_write).
 template <class T, int D>
-__device__ __forceinline__ void append_new_row(const EvictArgs& e, int head, int row, int lane) {
+__device__ __forceinline__ uint4 append_read(const EvictArgs& e, int head, int lane) {
+  constexpr int NV = D * (int)sizeof(T) / 16;
+  const bool is_v = lane >= NV;
+  const uint4* src = reinterpret_cast<const uint4*>(
+      reinterpret_cast<const T*>(is_v ? e.v_new : e.k_new) + (size_t)head * D) + lane % NV;
+  return *src;  // every lane reads inside the row; lanes past 2 NV write nothing
+}
+template <class T, int D>
+__device__ __forceinline__ void append_write(const EvictArgs& e, int head, int row, int lane,
+                                             const uint4& piece) {
   constexpr int NV = D * (int)sizeof(T) / 16;
   if (lane < 2 * NV) {
-    const bool is_v = lane >= NV;
-    const int piece = lane % NV;
-    const uint4* src = reinterpret_cast<const uint4*>(
-        reinterpret_cast<const T*>(is_v ? e.v_new : e.k_new) + (size_t)head * D) + piece;
-    T* cache = reinterpret_cast<T*>(is_v ? e.v_cache : e.k_cache);
-    uint4* dst = reinterpret_cast<uint4*>(cache + ((size_t)head * e.cap + row) * D) + piece;
-    *dst = *src;
+    T* cache = reinterpret_cast<T*>(lane >= NV ? e.v_cache : e.k_cache);
+    reinterpret_cast<uint4*>(cache + ((size_t)head * e.cap + row) * D)[lane % NV] = piece;
   }
+}
+template <class T, int D>
+__device__ __forceinline__ void append_new_row(const EvictArgs& e, int head, int row, int lane) {
+  append_write<T, D>(e, head, row, lane, append_read<T, D>(e, head, lane));
 }
 
 // Whether this call evicts from the head: the new row fits in the cache and in the
@@ -464,6 +475,11 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
   // multiple of 32); rows past n_tok and padded query slots then read as -inf, their
   // norm as +inf.  The masks come after a scheduling barrier, so that all of the reads
   // are out before the first is waited for.
+  // Groups of four rows v of the batch at `base` that hold any row below n_tok (the same
+  // for every thread): the others are not scored.
+  auto groups_in = [&](int base) {
+    return min(UB / 4, (n_tok - base + 4 * NT - 1) / (4 * NT));
+  };
   auto load_batch = [&](int base) {
     float4 r4[UB / 4][GM + 1];
 #pragma unroll
@@ -516,15 +532,18 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
       for (int g = 0; g < GM; ++g) { m[g] = -INFINITY; l[g] = 0.f; }
       for (int b = 0; b < nb; ++b) {
         if (b > 0) load_batch(b * step);
+        const int nv = groups_in(b * step);
 #pragma unroll
         for (int g = 0; g < GM; ++g) {
           float mn = m[g];
 #pragma unroll
-          for (int u = 0; u < UB; ++u) mn = fmaxf(mn, x[u][g]);
+          for (int u = 0; u < UB; ++u)
+            if (u / 4 < nv) mn = fmaxf(mn, x[u][g]);
           const float base = mn == -INFINITY ? 0.f : mn;
           float sum = 0.f;
 #pragma unroll
-          for (int u = 0; u < UB; ++u) sum += fast_exp2(x[u][g] - base);
+          for (int u = 0; u < UB; ++u)
+            if (u / 4 < nv) sum += fast_exp2(x[u][g] - base);
           l[g] = l[g] * fast_exp2(m[g] - base) + sum;
           m[g] = mn;
         }
@@ -567,8 +586,10 @@ __device__ __forceinline__ void select_finish(const EvictArgs& e, int head, int 
     int bj = INT_MAX;
     for (int b = 0; b < nb; ++b) {
       if (nb > 1) load_batch(b * step);  // one batch: still in registers
+      const int nv = groups_in(b * step);
 #pragma unroll
       for (int u = 0; u < UB; ++u) {
+        if (u / 4 >= nv) continue;
         const int j = b * step + 4 * (tid + NT * (u / 4)) + (u % 4);
         float mx = -INFINITY;
 #pragma unroll
@@ -944,10 +965,14 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
   const int t0 = kEvTB * s0;  // below max_len <= cap
   const int t1 = s1 == hb ? n_rows : min(kEvTB * s1, n_rows);
   // the workgroup whose blocks hold the new row appends it (the head's last block for
-  // rows past them); nothing in this launch reads that cache row (the new token is read
-  // from k_new / v_new), so the copy waits until the segment's rows are read
+  // rows past them); nothing reads that cache row before the segment's rows are read (the
+  // new token is read from k_new / v_new), so the copy is written after them: with the
+  // attention, read then as well (no registers held over the loop); scoring alone, read
+  // here (the workgroup then waits for nothing but its own rows)
   const int nb_new = min(old_len / kEvTB, hb - 1);
   const bool appends = can_append && wave == 0 && nb_new >= s0 && nb_new < s1;
+  uint4 new_piece = make_uint4(0, 0, 0, 0);
+  if (!ATTN && appends) new_piece = append_read<T, D>(e, head, lane);
 
   if (ATTN || t0 < t1) {  // uniform
     const T* kc = reinterpret_cast<const T*>(e.k_cache) + (size_t)head * e.cap * D;
@@ -982,9 +1007,8 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
 
     QueryRows<T, D, NT> qr;
     qr.load(e, head);
-    const int ne = e.n_e[head];
     const float svv = tid < D ? e.s_v[(size_t)head * D + tid] : 0.f;
-    if (evicts) build_summary<T, D, NT>(e, head, ne, L.sm);
+    const int ne = evicts ? build_summary<T, D, NT>(e, head, L.sm) : e.n_e[head];
     qr.store(L.q);
     // r_j = v_j - cf (v_bar / cf + S_tilde k_j): the accumulators of S_tilde k_j start at
     // v_bar / cf = s_v / scale, so the mean comes out of the MFMAs
@@ -1097,7 +1121,10 @@ __device__ __forceinline__ void ev_segment(const EvictArgs& e, EvLds<T, D, GM, N
       }
     }
   }
-  if (appends) append_new_row<T, D>(e, head, old_len, lane);
+  if (appends) {
+    if constexpr (ATTN) append_new_row<T, D>(e, head, old_len, lane);
+    else append_write<T, D>(e, head, old_len, lane, new_piece);
+  }
   if constexpr (!ATTN) {
     // The workgroup holds the whole head: its records and the appended row are visible
     // to all of its waves after a barrier, and it selects, updates, then attends to the
