@@ -894,9 +894,10 @@ def main() -> int:
         "decode_ms_per_step": sum(dec_ms) / len(dec_ms),
         "compress_ms_per_layer": {k: v["compress_ms_per_layer"] for k, v in per_budget.items()},
         "per_budget": per_budget,
-        "roofline": {"kernel": "momentkv_decode_attn call over the 36-layer stack: "
-                               "k_decode_fused (max_len <= 384) or k_decode_slice + "
-                               "k_decode_merge; time per call from the graph replays",
+        "roofline": {"kernel": "momentkv_decode_attn call over the stack: one launch, "
+                               "k_decode_fused (max_len <= 384) or k_decode_slice (the last "
+                               "wave of each head merges it); time per call from the graph "
+                               "replays",
                      "bound": "hbm", "achieved": avg_bytes / avg_launch_s / 1e9,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": avg_bytes / avg_launch_s / 1e9 / HBM_PEAK_GBS,
