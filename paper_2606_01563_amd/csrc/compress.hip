@@ -51,7 +51,6 @@ constexpr int TILE = 64;  // tokens per tile
 constexpr int TKS = 2048;          // positions per slice
 constexpr int TKT = 256;           // threads per slice workgroup
 constexpr int TKPT = TKS / TKT;    // consecutive positions per thread
-constexpr int TK_BINS0 = 2048;
 constexpr int TK_MAX_SLICES = 512; // 1048576 candidates
 constexpr int TK_CAND_LDS = 8192;  // candidates of the k-th key's bin staged in LDS
 
@@ -1549,7 +1548,6 @@ static hipError_t launch_head_budgets(const CompressArgs& a, hipStream_t st) {
 template <class T, int D, int MTW>
 static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg_abar,
                                float* dbg_score0, float* dbg_score, int32_t* dbg_kept0) {
-  constexpr bool BF = sizeof(T) == 2;
   const dim3 blk(256);
   const int H = a.H;
   if (a.L >= a.N) {
