@@ -413,8 +413,11 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
   constexpr int LDK = BF ? D + 16 : D + PAD, LDT = TILE + PAD;  // bf16 rows padded by 32 bytes
   constexpr int QM = CovSplit<D, NW>::QM, QN = CovSplit<D, NW>::QN;
   typedef TileRegs<T, D, NT> TR;
-  __shared__ __align__(16) T sK[TILE][LDK];
-  __shared__ __align__(16) T sV[BF ? TILE : 1][LDK];     // bf16: V rows, candidates only
+  // bf16: two buffers, so that tile t + 1 is stored while slower waves still read tile t
+  // (one barrier per tile); fp32, and bf16 with four row tiles per wave (registers): one
+  constexpr int NB = BF && MTW < 4 ? 2 : 1;
+  __shared__ __align__(16) T sK[NB][TILE][LDK];
+  __shared__ __align__(16) T sV[NB][BF ? TILE : 1][LDK];  // bf16: V rows, candidates only
   __shared__ __align__(16) T sKT[BF ? 1 : D][LDT];       // fp32: K^T, V^T
   __shared__ __align__(16) T sVT[BF ? 1 : D][LDT];
   __shared__ float sVnorm[kRowsMaxTiles * TILE];  // ||v_j|| of the slice, written at the end
@@ -472,19 +475,21 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
     const int tok0 = t * TILE;
     const bool tile_has_cand = tok0 < c_hi && tok0 + TILE > c_lo;
     const bool live = t < t_end;  // uniform; a step past the slice only issues loads
+    T (*cK)[LDK] = sK[t & (NB - 1)];
+    T (*cV)[LDK] = sV[t & (NB - 1)];
     R.arrive();
     if (live) {
       if (TR::active(tid)) {
 #pragma unroll
         for (int i = 0; i < TR::NP; ++i) {
           const int p = TR::pair(tid, i);  // rows past N: their logits are masked
-          store_frag(&sK[2 * p][8 * TR::group(tid)], R.k[i][0]);
-          store_frag(&sK[2 * p + 1][8 * TR::group(tid)], R.k[i][1]);
+          store_frag(&cK[2 * p][8 * TR::group(tid)], R.k[i][0]);
+          store_frag(&cK[2 * p + 1][8 * TR::group(tid)], R.k[i][1]);
         }
       }
       float ss[TR::NP][2];
       if constexpr (BF)
-        tile_sums_nat<D, NT, LDK>(R, sV, tok0, is_cand, sk, sv, ss, tid);
+        tile_sums_nat<D, NT, LDK>(R, cV, tok0, is_cand, sk, sv, ss, tid);
       else
         tile_store_t<T, D, NT, LDT>(R, sKT, sVT, tok0, is_cand, sk, sv, ss, tid);
       // ||v_j||: the GROUPS lanes holding token j's columns are adjacent.  No global
@@ -516,7 +521,7 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
         acc[nt] = zero4();
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          mma(acc[nt], qf[k][ks], load_frag(&sK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]));
+          mma(acc[nt], qf[k][ks], load_frag(&cK[16 * nt + (lane & 15)][32 * ks + 8 * (lane >> 4)]));
       }
       if (!need_mask) {
         // every logit finite: the max is taken on the raw products (c2 > 0, so scaling
@@ -553,11 +558,11 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
     }
     if (tile_has_cand) {
       if constexpr (BF)
-        cov_tile_tr<D, NW>(&sV[0][0], &sK[0][0], LDK, cacc, wave, lane);
+        cov_tile_tr<D, NW>(&cV[0][0], &cK[0][0], LDK, cacc, wave, lane);
       else
         cov_tile<T, D, NW, LDT>(sVT, sKT, cacc, wave, lane);
     }
-    __syncthreads();
+    if constexpr (NB == 1) __syncthreads();  // the single buffer is written again next step
   };
   TR R0, R1;
   issue(R0, t_beg);
@@ -568,7 +573,8 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
     step(R1, t + 1);
   }
 
-  // ||v_j|| of the slice's candidates (the loop ended on a barrier)
+  if constexpr (NB == 2) __syncthreads();  // the last tile read before sV is reused below
+  // ||v_j|| of the slice's candidates
   for (int x = tid; x < (t_end - t_beg) * TILE; x += NT) {
     const int j = t_beg * TILE + x;
     if (is_cand(j)) a.vnorm[(size_t)head * a.n_c + (j - c_lo)] = sVnorm[x];
@@ -594,15 +600,49 @@ __global__ void __launch_bounds__(RC_THREADS) k_rows_cov(CompressArgs a) {
     }
   static_assert(sizeof(sV) + sizeof(sVT) >= NW * 2 * D * sizeof(float), "LDS for the column sums");
   write_cov_partials<T, D, NT>(a, head, sl, cacc, sv, sk, 1.f,
-                               BF ? reinterpret_cast<float*>(&sV[0][0]) : reinterpret_cast<float*>(&sVT[0][0]), tid);
+                               BF ? reinterpret_cast<float*>(&sV[0][0][0]) : reinterpret_cast<float*>(&sVT[0][0]), tid);
 }
 
 // ------------------------------------------------------------------------------------
 // Stage 2: merge row partials -> (max, 1/Z) per window row.  Eight lanes per row, each
-// merging every eighth slice, then a fixed xor tree across the eight.
+// merging every eighth slice, then a fixed xor tree across the eight.  The same launch
+// adds up the nsl1 candidate covariance slots of the head into slot 0 (same lane scheme:
+// eight lanes per float4, each summing every eighth slot), so that the later sums of the
+// moments read one slot for the candidates.  Each float4 is read and then written by the
+// same eight lanes, so no other workgroup reads what slot 0 receives.
 // ------------------------------------------------------------------------------------
+template <int D> constexpr int reduce_blocks() { return ((D * D + 2 * D) / 4 + 31) / 32; }
+
+template <int D>
+__device__ __forceinline__ void sum_cand_slots(const CompressArgs& a, int head, int bx) {
+  constexpr int NSF4 = D * D / 4, NF4 = (D * D + 2 * D) / 4;
+  const int f4 = bx * 32 + (threadIdx.x >> 3);
+  const int sub = threadIdx.x & 7;
+  if (f4 >= NF4) return;  // whole groups of eight lanes leave together
+  const bool in_S = f4 < NSF4;
+  float* base = in_S ? a.spart + (size_t)head * a.nslot * D * D + 4 * f4
+                     : a.svkpart + (size_t)head * a.nslot * 2 * D + 4 * (f4 - NSF4);
+  const size_t stride = in_S ? (size_t)D * D : (size_t)2 * D;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int sl = sub; sl < a.nsl1; sl += 8) {
+    const float4 p = *reinterpret_cast<const float4*>(base + sl * stride);
+    acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
+  }
+#pragma unroll
+  for (int x = 1; x < 8; x <<= 1) {
+    acc.x += __shfl_xor(acc.x, x, 8);
+    acc.y += __shfl_xor(acc.y, x, 8);
+    acc.z += __shfl_xor(acc.z, x, 8);
+    acc.w += __shfl_xor(acc.w, x, 8);
+  }
+  if (sub == 0) *reinterpret_cast<float4*>(base) = acc;
+}
+
+template <int D>
 __global__ void __launch_bounds__(256) k_row_combine(CompressArgs a) {
   const int head = blockIdx.y;
+  sum_cand_slots<D>(a, head, blockIdx.x);
   if (blockIdx.x == 0) {  // the score producers below add into these
     for (int b = threadIdx.x; b < 2 * TK_HBINS; b += 256)
       a.tk_hh[((size_t)(b / TK_HBINS) * a.H + head) * TK_HBINS + b % TK_HBINS] = 0u;
@@ -610,6 +650,7 @@ __global__ void __launch_bounds__(256) k_row_combine(CompressArgs a) {
       for (int b = threadIdx.x; b < TK_HBINS; b += 256)
         a.tk_hs[(size_t)(head / a.Hkv) * TK_HBINS + b] = 0u;
   }
+  if ((int)blockIdx.x * 32 >= a.R) return;  // uniform over the workgroup
   const int r = blockIdx.x * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
   float m = -INFINITY, l = 0.f;
@@ -1187,10 +1228,11 @@ __device__ void slice_cov(const CompressArgs& a, int head, int sl, const int32_t
 
 // ------------------------------------------------------------------------------------
 // Stage 7/12: fixed-order sum of the partial slots -> raw S, s_v, s_k of the evicted set
-// (stage 7: the provisional set, into the workspace; stage 12: the output moments): every
-// slot, or only the evicted rows' slots of a head that sums them directly.
-// Eight lanes per float4 of a head's D*D + 2D values, lane `sub` summing slots
-// s0 + sub, s0 + sub + 8, ..., then a fixed xor tree across the eight lanes.
+// (stage 7: the provisional set, into the workspace; stage 12: the output moments): the
+// candidates' sums (slot 0, where the row-statistics launch has added up the candidate
+// slots) and the selection's slots, or only the evicted rows' slots of a head that sums
+// them directly.  Eight lanes per float4 of a head's D*D + 2D values, lane `sub` summing
+// the listed slots sub, sub + 8, ..., then a fixed xor tree across the eight lanes.
 // ------------------------------------------------------------------------------------
 // S_bf16: S_out holds bf16 (each fp32 sum rounded once, to nearest even).
 template <int D>
@@ -1201,14 +1243,18 @@ __device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, in
   const int f4 = bx * 32 + (threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  const int s0 = direct_sums(a, head) ? a.nsl1 : 0;
+  // listed slots: u = 0 is slot 0 (the candidates' sums) unless the head sums directly,
+  // then the selection's slots nsl1 ... nslot - 1
+  const int lead = direct_sums(a, head) ? 0 : 1;
+  const int n_use = a.nslot - a.nsl1 + lead;
   if (f4 < NF4) {
     const bool in_S = f4 < NSF4;
     const float* base = in_S ? a.spart + (size_t)head * a.nslot * D * D + 4 * f4
                              : a.svkpart + (size_t)head * a.nslot * 2 * D + 4 * (f4 - NSF4);
     const size_t stride = in_S ? (size_t)D * D : (size_t)2 * D;
 #pragma unroll 4
-    for (int sl = s0 + sub; sl < a.nslot; sl += 8) {
+    for (int u = sub; u < n_use; u += 8) {
+      const int sl = u < lead ? 0 : a.nsl1 + u - lead;
       const float4 p = *reinterpret_cast<const float4*>(base + sl * stride);
       acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
     }
@@ -1237,8 +1283,6 @@ __device__ __forceinline__ void reduce_slots(const CompressArgs& a, int head, in
   }
   if (ne_out && bx == 0 && threadIdx.x == 0) ne_out[head] = a.n_c - head_keep(a, head);
 }
-
-template <int D> constexpr int reduce_blocks() { return ((D * D + 2 * D) / 4 + 31) / 32; }
 
 // Also clears the head's histogram of the moment round that follows (the round before
 // filled it, and its selection has read it).
@@ -1560,7 +1604,7 @@ static hipError_t run_compress(const CompressArgs& a, hipStream_t st, float* dbg
   }
   hipLaunchKernelGGL((k_rows_cov<T, D, MTW>), dim3(a.nsl1, H), dim3(RC_THREADS), 0, st, a);
   MKV_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_row_combine, dim3((a.R + 31) / 32, H), blk, 0, st, a);
+  hipLaunchKernelGGL((k_row_combine<D>), dim3(std::max((a.R + 31) / 32, reduce_blocks<D>()), H), blk, 0, st, a);
   MKV_CHECK_LAUNCH();
   hipLaunchKernelGGL((k_mass<T, D, 2 * MTW>), dim3(a.nsl2, H), blk, 0, st, a);
   MKV_CHECK_LAUNCH();

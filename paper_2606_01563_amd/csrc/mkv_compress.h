@@ -40,7 +40,8 @@ struct CompressArgs {
   int32_t* tk_state;        // [H, 2]            top-k: bin of the k-th key, count above it
   int32_t* tk_cnt;          // [H, ntk, 2]       top-k: per slice, keys above the bin, in it
   uint32_t* tk_cand;        // [H, ntk, 2048]    top-k: per slice, the keys in the bin
-  float* spart;             // [H, nslot, D, D]  covariance partials
+  float* spart;             // [H, nslot, D, D]  covariance partials (after the row-statistics
+                            // launch, slot 0 holds the sum of slots 0 .. nsl1 - 1)
   float* svkpart;           // [H, nslot, 2, D]  (s_v, s_k) partials
   float* s0;                // [H, D, D]         raw S of the provisional evicted set
   float* sv0;               // [H, D]            its s_v
