@@ -54,6 +54,10 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of the MI355X
 
 
+# max_len from which momentkv_decode_evict (n_split = 0) takes the one-read shape: a scoring
+# launch with the attention, then a finishing launch (shorter caches: one launch)
+EVICT_ONE_READ_MIN_LEN = 320
+
 def decode_bytes(n_heads: int, G: int, d: int, lens_after: int, elem: int = 2) -> int:
     """Algorithmic HBM bytes of one decode launch (per KV head, summed over heads):
     retained K and V rows read, the d x d summary and its two vectors and count read,
@@ -462,7 +466,7 @@ def evict_measurement(args, wl, budgets, stacks, q_steps, kn_steps, vn_steps, ou
                       for L in budgets) / len(budgets)
     return {"what": "per token and budget one momentkv_decode_evict call over the 36 "
                     "caches: append, Phase 1 eviction, Phase 2 corrected attention; cache "
-                    "kept at the budget.  Budgets up to 768: one k_evict_attn launch that "
+                    "kept at the budget.  Caches under 320 rows: one k_evict_attn launch that "
                     "scores, selects, updates and attends to the new cache; above: "
                     "k_evict_attn scoring and attention in one read of the cache, then "
                     "k_evict_finish",
@@ -731,7 +735,7 @@ def main() -> int:
                 mk.momentkv_decode_evict(q_steps[t], st.k_out, st.v_out, st.lens, st.n_e,
                                          st.s_k, st.s_v, st.S, kn_steps[t], vn_steps[t], Lr,
                                          max_len=Lr + 1, out=out, workspace=ews[L])
-                calls.append({"token": t, "budget": L, "fused": Lr + 1 >= 769,
+                calls.append({"token": t, "budget": L, "fused": Lr + 1 >= EVICT_ONE_READ_MIN_LEN,
                               "bytes": evict_bytes(LB * Hkv, G, d, Lr)})
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": copy_bytes, "calls": calls}))

@@ -315,7 +315,7 @@ size_t momentkv_decode_evict_workspace_size(const mkv_decode_params* p);  /* sam
 /* p         as for momentkv_decode_attn with summary = 0: S is the raw sum, updated in
  *           place.  max_len bounds lens after the append (budget < max_len <= cap leaves
  *           room for the new row).  n_split selects the launch shape: 0 = automatic; for
- *           max_len >= 769 (or n_split > 0) one read of the cache, the attention computed
+ *           max_len >= 320 (or n_split > 0) one read of the cache, the attention computed
  *           in the scoring pass over about one workgroup per CU (n_split per KV head when
  *           n_split > 0) and the evicted row's term removed from it afterwards, then a
  *           finishing launch; for shorter caches one launch with one workgroup per KV

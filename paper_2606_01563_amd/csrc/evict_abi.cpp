@@ -29,7 +29,7 @@ namespace {
 // Workspace: the flag first, then the score records and the per-block running maxima;
 // fused: then the heads' partial states.
 constexpr int kCUs = 256;
-constexpr int kFusedMinLen = 769;
+constexpr int kFusedMinLen = 320;  // measured on a 288-head stack: 384 rows and more fused
 
 mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws, size_t* total) {
   mkv::EvictArgs e;

@@ -625,16 +625,17 @@ def test_evict_budgets_and_lengths_around_the_bound(dtype, d, n_split):
     P.run_evict_steps(gpu, out, 2, 289, flag=8, n_split=n_split)         # above budget
 
 
-@pytest.mark.parametrize("n_split", [0, 1])
-def test_evict_with_empty_summary_scores_alpha_times_value_norm(n_split):
+@pytest.mark.parametrize("n_split,ctx", [(0, 300), (0, 700), (1, 700)])
+def test_evict_with_empty_summary_scores_alpha_times_value_norm(n_split, ctx):
     """Budget above the context keeps every token, so n_e = 0: the first evictions use
-    v_bar = S_tilde = 0 and later ones the summary they build (both launch shapes)."""
+    v_bar = S_tilde = 0 and later ones the summary they build (the short-cache launch at
+    300 rows, the one-read shape at 700 rows over all CUs and one workgroup per head)."""
     wl, cpu, gpu = layer("tiny_fp32_n2048", steps=6, dtype=torch.bfloat16, head_dim=128,
-                         ctx_len=700, batch=1, n_q_heads=4, n_kv_heads=2, window=16,
+                         ctx_len=ctx, batch=1, n_q_heads=4, n_kv_heads=2, window=16,
                          budgets=(900,))
-    out = P.run_compress(gpu, 900, cap=701)
-    assert int(out.n_e.max()) == 0 and int(out.lens.min()) == 700
-    worst, swaps, n = P.run_evict_steps(gpu, out, 6, 700, n_split=n_split)
+    out = P.run_compress(gpu, 900, cap=ctx + 1)
+    assert int(out.n_e.max()) == 0 and int(out.lens.min()) == ctx
+    worst, swaps, n = P.run_evict_steps(gpu, out, 6, ctx, n_split=n_split)
     assert n == 12
 
 
