@@ -5,10 +5,12 @@
 //   1 k_rows_cov      per (slice of 64-token tiles, head): window logits Q.K^T on MFMA,
 //                     per-row online (max, sum) over the visible keys; for candidate
 //                     tokens also the covariance V^T K on MFMA (bf16: both operands
-//                     read transposed out of the row-major LDS tiles; fp32: tiles
-//                     written transposed), the sums s_k, s_v and ||v_j||.  [reads K, V]
+//                     read transposed out of the row-major LDS tiles, two tile buffers;
+//                     fp32: tiles written transposed), the sums s_k, s_v and ||v_j||,
+//                     one partial slot per slice.                         [reads K, V]
 //   2 k_row_combine   per head: merge the row partials in slice order -> (max, 1/Z);
-//                     zeroes the head's two top-k key histograms.
+//                     add up the slices' slots into slot 0 (the candidates' sums);
+//                     zero the head's two top-k key histograms.
 //   3 k_mass          per (slice, head): logits again, softmax mass summed over the
 //                     window rows -> a_j, aligned chunk pooling -> abar_j,
 //                     provisional score abar_j ||v_j||, added to the key histogram of
@@ -21,8 +23,8 @@
 //                     head's evicted rows are fewer than its kept ones, of its evicted
 //                     rows, stored as they are.
 //   7 k_reduce        fixed-order sum of the slots = raw moments of the provisional
-//                     evicted set: all slots (the candidates' minus the kept rows'), or
-//                     only the evicted rows' slots.  Summing the evicted rows directly
+//                     evicted set: slot 0 and the kept rows' slots (the candidates' sums
+//                     minus the kept rows'), or only the evicted rows' slots.  Summing the evicted rows directly
 //                     when they are the fewer keeps the cancellation of S_C - S_kept from
 //                     growing with the ratio of candidates to evicted rows.
 //   8 k_residual      per (slice, head): centring and clamp of the provisional summary
