@@ -625,6 +625,21 @@ def test_evict_budgets_and_lengths_around_the_bound(dtype, d, n_split):
     P.run_evict_steps(gpu, out, 2, 289, flag=8, n_split=n_split)         # above budget
 
 
+@pytest.mark.parametrize("budget", [318, 319])
+def test_evict_at_the_launch_shape_bound(budget):
+    """Caches of 319 and 320 rows (max_len = budget + 1), the two sides of the automatic
+    choice between the short-cache launch and the one-read shape (G = 4, bf16, d = 128):
+    both follow the oracle's trajectory."""
+    wl, cpu, gpu = layer("tiny_fp32_n2048", steps=3, dtype=torch.bfloat16, head_dim=128,
+                         ctx_len=1200, batch=1, n_q_heads=8, n_kv_heads=2, window=16,
+                         budgets=(budget,))
+    out = P.run_compress(gpu, budget, cap=budget + 1)
+    announce(f"evict at the shape bound: budget {budget}, max_len {budget + 1}")
+    worst, swaps, n = P.run_evict_steps(gpu, out, 3, budget)
+    announce(f"worst rel err {worst:.2e}, swaps {swaps} of {n}")
+    assert n == 3 * 2
+
+
 @pytest.mark.parametrize("n_split,ctx", [(0, 300), (0, 700), (1, 700)])
 def test_evict_with_empty_summary_scores_alpha_times_value_norm(n_split, ctx):
     """Budget above the context keeps every token, so n_e = 0: the first evictions use
