@@ -29,7 +29,9 @@ namespace {
 // Workspace: the flag first, then the score records and the per-block running maxima;
 // fused: then the heads' partial states.
 constexpr int kCUs = 256;
-constexpr int kFusedMinLen = 320;  // measured on a 288-head stack: 384 rows and more fused
+// max_len from which the one-read shape runs (on a 288-head stack it was the faster one
+// from 384 rows up and the slower one at 256)
+constexpr int kFusedMinLen = 320;
 
 mkv::EvictArgs evict_layout(const mkv_decode_params* p, int32_t budget, void* ws, size_t* total) {
   mkv::EvictArgs e;
